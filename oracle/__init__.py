@@ -1,0 +1,269 @@
+"""WhiteMatter CPU oracle (test infrastructure only).
+
+A thin ctypes binding over ``wm_oracle.c``: a plain fp64 statement of the
+WhiteMatter cross-layer KV pool (Section 3.1, Steps 1-3, router
+initialization) and of decode-time channel attention with the learned dummy
+slot (Section 3.2). Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the GPU library never does, and the
+two share no code.
+
+Arrays are numpy float64, C-contiguous, in the layouts below (N = B*T_new):
+
+    H       [B, T_new, L, D]        per-layer states entering each layer
+    alpha   [2, N, k, L]            mixing weights, key branch then value
+    mixed   [2, k, N, D]            mixed channels (before the mid RMSNorm)
+    Kc, Vc  [k, B, Hkv, S_cap, d]   channel-major cache; token i of sequence b
+                                    is stored at slot ctx_len[b] + i
+    Q       [L, B, Hq, T_new, d]    consumer queries after q-norm and RoPE
+    O       [L, B, T_new, Hq*d]     attention output per consumer layer
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "wm_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+MIX_LINEAR, MIX_SOFTMAX = 0, 1
+MASK_PAPER, MASK_INCLUSIVE = 0, 1
+
+PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
+               "Kd", "Vd", "g_in", "Wq", "g_qnorm")
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (fp64, IEEE semantics, OpenMP over rows)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in
+                ("B", "T_new", "L", "k", "D", "Hq", "Hkv", "d", "p", "S_cap",
+                 "mix_mode", "mask_mode")] + [("eps", ctypes.c_double),
+                                              ("rope_theta", ctypes.c_double)]
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_NAMES]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = ctypes.CDLL(_LIB)
+    return _lib
+
+
+@dataclass
+class Dims:
+    B: int
+    T_new: int
+    L: int
+    k: int
+    D: int
+    Hq: int
+    Hkv: int
+    d: int
+    p: int = 1
+    S_cap: int = 0
+    mix_mode: int = MIX_LINEAR
+    mask_mode: int = MASK_PAPER
+    eps: float = 1e-6
+    rope_theta: float = 1e6
+
+    @property
+    def N(self) -> int:
+        return self.B * self.T_new
+
+    @property
+    def Lp(self) -> int:
+        return (self.L + self.p - 1) // self.p
+
+    def c(self) -> _Dims:
+        return _Dims(self.B, self.T_new, self.L, self.k, self.D, self.Hq, self.Hkv, self.d,
+                     self.p, self.S_cap, self.mix_mode, self.mask_mode, self.eps,
+                     self.rope_theta)
+
+
+def _f64(a) -> np.ndarray:
+    if hasattr(a, "detach"):  # a torch tensor: exact widening to float64 on the CPU
+        a = a.detach().to("cpu").double().numpy()
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _ilist(lst):
+    if lst is None:
+        return None, 0, None
+    arr = np.ascontiguousarray(np.asarray(lst, dtype=np.int32))
+    return arr, len(arr), arr.ctypes.data_as(ctypes.c_void_p)
+
+
+class Params:
+    """Holds float64 copies of the parameters, keeping them alive for the C calls."""
+
+    def __init__(self, params: dict):
+        self.arrays = {n: _f64(params[n]) for n in PARAM_NAMES}
+        self.c = _Params(*[_ptr(self.arrays[n]) for n in PARAM_NAMES])
+
+
+def _as_params(params) -> Params:
+    return params if isinstance(params, Params) else Params(params)
+
+
+def _ctx(dims: Dims, ctx_len):
+    if ctx_len is None:
+        ctx_len = np.zeros(dims.B, dtype=np.int32)
+    arr = np.ascontiguousarray(np.asarray(ctx_len, dtype=np.int32))
+    assert arr.shape == (dims.B,)
+    return arr
+
+
+# ------------------------------------------------------------- primitives
+
+def rmsnorm(x, g, eps: float = 1e-6) -> np.ndarray:
+    x, g = _f64(x), _f64(g)
+    y = np.empty_like(x)
+    lib().wmo_rmsnorm(_ptr(x), _ptr(g), ctypes.c_int(x.size), ctypes.c_double(eps), _ptr(y))
+    return y
+
+
+def rope(x, pos: float, theta: float = 1e6) -> np.ndarray:
+    y = _f64(x).copy()
+    lib().wmo_rope(_ptr(y), ctypes.c_int(y.size), ctypes.c_double(pos), ctypes.c_double(theta))
+    return y
+
+
+def router_layers(L: int, p: int) -> list:
+    n = lib().wmo_router_inputs(ctypes.c_int(L), ctypes.c_int(p))
+    sel = np.zeros(n, dtype=np.int32)
+    lib().wmo_router_layers(ctypes.c_int(L), ctypes.c_int(p), _ptr(sel))
+    return sel.tolist()
+
+
+def init_bias(L: int, k: int) -> np.ndarray:
+    b = np.zeros(k * L, dtype=np.float64)
+    rc = lib().wmo_init_bias(ctypes.c_int(L), ctypes.c_int(k), _ptr(b))
+    if rc != 0:
+        raise ValueError("k must lie in [1, L]")
+    return b
+
+
+def channel_groups(L: int, k: int, chan_map):
+    m = np.ascontiguousarray(np.asarray(chan_map, dtype=np.int32))
+    off = np.zeros(k + 1, dtype=np.int32)
+    mem = np.zeros(L, dtype=np.int32)
+    rc = lib().wmo_channel_groups(ctypes.c_int(L), ctypes.c_int(k), _ptr(m), _ptr(off), _ptr(mem))
+    if rc != 0:
+        raise ValueError("channel map entry outside [0, k)")
+    return off, mem
+
+
+def attend_row(q, K, V, kd=None, vd=None) -> np.ndarray:
+    q, K, V = _f64(q), _f64(K), _f64(V)
+    d = q.size
+    o = np.zeros(d, dtype=np.float64)
+    kd_p = vd_p = None
+    if kd is not None:
+        kd, vd = _f64(kd), _f64(vd)
+        kd_p, vd_p = _ptr(kd), _ptr(vd)
+    lib().wmo_attend_row(ctypes.c_int(d), _ptr(q), _ptr(K), ctypes.c_long(d), _ptr(V),
+                         ctypes.c_long(d), ctypes.c_long(K.shape[0]), kd_p, vd_p, _ptr(o))
+    return o
+
+
+# ------------------------------------------------------------ whole tensors
+
+def router_mix(dims: Dims, params, H, toks=None):
+    P = _as_params(params)
+    H = _f64(H)
+    alpha = np.zeros((2, dims.N, dims.k, dims.L))
+    mixed = np.zeros((2, dims.k, dims.N, dims.D))
+    arr, n, p = _ilist(toks)
+    lib().wmo_router_mix(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(H), p, ctypes.c_int(n),
+                         _ptr(alpha), _ptr(mixed))
+    return alpha, mixed
+
+
+def empty_cache(dims: Dims, fill: float = np.nan):
+    shape = (dims.k, dims.B, dims.Hkv, dims.S_cap, dims.d)
+    return np.full(shape, fill), np.full(shape, fill)
+
+
+def kv_project(dims: Dims, params, mixed, ctx_len, Kc, Vc, toks=None):
+    """Writes the listed tokens' cache rows into Kc, Vc (float64, in place)."""
+    P = _as_params(params)
+    mixed = _f64(mixed)
+    ctx = _ctx(dims, ctx_len)
+    arr, n, p = _ilist(toks)
+    assert Kc.dtype == np.float64 and Kc.flags.c_contiguous and Vc.flags.c_contiguous
+    lib().wmo_kv_project(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(mixed), _ptr(ctx), p,
+                         ctypes.c_int(n), _ptr(Kc), _ptr(Vc))
+
+
+def pool(dims: Dims, params, H, ctx_len, Kc, Vc, toks=None):
+    P = _as_params(params)
+    H = _f64(H)
+    ctx = _ctx(dims, ctx_len)
+    arr, n, p = _ilist(toks)
+    assert Kc.dtype == np.float64 and Kc.flags.c_contiguous and Vc.flags.c_contiguous
+    lib().wmo_pool(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(H), _ptr(ctx), p,
+                   ctypes.c_int(n), _ptr(Kc), _ptr(Vc))
+
+
+def q_project(dims: Dims, params, H, ctx_len=None, toks=None) -> np.ndarray:
+    P = _as_params(params)
+    H = _f64(H)
+    ctx = _ctx(dims, ctx_len)
+    Q = np.zeros((dims.L, dims.B, dims.Hq, dims.T_new, dims.d))
+    arr, n, p = _ilist(toks)
+    lib().wmo_q_project(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(H), _ptr(ctx), p,
+                        ctypes.c_int(n), _ptr(Q))
+    return Q
+
+
+def channel_attend(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, rows=None) -> np.ndarray:
+    P = _as_params(params)
+    Q, Kc, Vc = _f64(Q), _f64(Kc), _f64(Vc)
+    ctx = _ctx(dims, ctx_len)
+    m = np.ascontiguousarray(np.asarray(chan_map, dtype=np.int32))
+    O = np.zeros((dims.L, dims.B, dims.T_new, dims.Hq * dims.d))
+    arr, n, p = _ilist(rows)
+    lib().wmo_channel_attend(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(Q), _ptr(m),
+                             _ptr(ctx), _ptr(Kc), _ptr(Vc), p, ctypes.c_int(n), _ptr(O))
+    return O
+
+
+def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc) -> np.ndarray:
+    """Fused step; Kc/Vc (float64, in place) gain the new tokens' slots."""
+    P = _as_params(params)
+    H = _f64(H)
+    ctx = _ctx(dims, ctx_len)
+    m = np.ascontiguousarray(np.asarray(chan_map, dtype=np.int32))
+    O = np.zeros((dims.L, dims.B, dims.T_new, dims.Hq * dims.d))
+    lib().wmo_layer_step(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(H), _ptr(m), _ptr(ctx),
+                         _ptr(Kc), _ptr(Vc), _ptr(O))
+    return O
+
+
+def num_threads() -> int:
+    return int(lib().wmo_num_threads())
