@@ -1,0 +1,211 @@
+/*
+ * whitematter.h -- C ABI of libwhitematter.so, the MI355X (gfx950) hot path of
+ * WhiteMatter ("WhiteMatter: All-to-All Cross-Layer Connections via KV
+ * Mixing"): the cross-layer KV pool of Section 3.1 and the per-layer channel
+ * attention of Section 3.1 Step 3 / Section 3.2.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ *  - Tensors are caller-owned, contiguous, row-major, in the layouts given
+ *    below. "Device" pointers must point to GPU memory of the current HIP
+ *    device and be 16-byte aligned; "host" pointers are ordinary memory.
+ *  - Element type: every tensor named "in dtype" is fp32 (WM_F32) or bf16
+ *    (WM_BF16) as dims->dtype says; mixing weights and workspaces are fp32.
+ *  - The library never allocates device memory. Scratch comes from the
+ *    caller: ws points to at least wm_workspace_size(dims, op) bytes of device
+ *    memory, 256-byte aligned, and ws_bytes states its size.
+ *  - Every call validates on the host first and launches nothing on error.
+ *    Work is enqueued asynchronously on `stream` (NULL = the null stream);
+ *    nothing synchronises. Calls keep no state between them, so concurrent
+ *    calls are safe as long as their output and workspace buffers differ.
+ *  - Return value: WM_OK or one of the WM_ERR_* codes; wm_last_error() gives
+ *    a message for the calling thread's last failure.
+ *  - N = B * T_new new tokens; token n = b * T_new + i of sequence b sits at
+ *    position ctx_len[b] + i and is cached at that slot.
+ *  - ctx_len (device, int32 [B], NULL = all zero) must lie in [0, ctx_max];
+ *    ctx_max + T_new <= S_cap is checked on the host. A ctx_len entry outside
+ *    that range leaves that sequence's outputs unspecified but never causes an
+ *    access outside the given buffers.
+ */
+#ifndef WHITEMATTER_H
+#define WHITEMATTER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *wm_stream_t; /* a hipStream_t */
+
+enum wm_status {
+  WM_OK = 0,
+  WM_ERR_ARG = 1,         /* null, misaligned or negative argument */
+  WM_ERR_SHAPE = 2,       /* inconsistent or unsupported dimensions */
+  WM_ERR_DTYPE = 3,       /* unknown dtype / mode value */
+  WM_ERR_MAP = 4,         /* consumer->channel map entry outside [0, k) */
+  WM_ERR_CAPACITY = 5,    /* ctx_max + T_new > S_cap */
+  WM_ERR_WORKSPACE = 6,   /* ws NULL, misaligned or smaller than required */
+  WM_ERR_LAUNCH = 7       /* the HIP runtime rejected a launch */
+};
+
+enum wm_dtype { WM_F32 = 0, WM_BF16 = 1 };
+
+/* Mixing weights: the paper's signed linear router (Section 3.1 Step 1), or
+ * additionally normalised by a softmax over the L source layers of each
+ * channel row (weights positive, summing to 1). */
+enum wm_mix_mode { WM_MIX_LINEAR = 0, WM_MIX_SOFTMAX = 1 };
+
+/* Attention mask: the paper's (Section 3.2) -- a learned dummy slot plus the
+ * cached slots strictly before the query's own position, so a token never
+ * reads its own channels -- or standard causal (slots <= own position, no
+ * dummy). */
+enum wm_mask_mode { WM_MASK_PAPER = 0, WM_MASK_INCLUSIVE = 1 };
+
+enum wm_op {
+  WM_OP_ROUTER_MIX = 0,
+  WM_OP_KV_PROJECT = 1,
+  WM_OP_Q_PROJECT = 2,
+  WM_OP_CHANNEL_ATTEND = 3,
+  WM_OP_LAYER_STEP = 4
+};
+
+/* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
+ * D a multiple of 32, Hq a multiple of Hkv, d in {32, 64}, 1 <= p <= L,
+ * L * D * sizeof(dtype) <= 64 KiB. */
+typedef struct wm_dims {
+  int32_t B;         /* sequences */
+  int32_t T_new;     /* new tokens per sequence in this call */
+  int32_t L;         /* decoder layers = source layers = consumer layers */
+  int32_t k;         /* KV channels */
+  int32_t D;         /* hidden width */
+  int32_t Hq;        /* query heads */
+  int32_t Hkv;       /* KV heads; query head h reads KV head h / (Hq / Hkv) */
+  int32_t d;         /* head dimension */
+  int32_t p;         /* router reads every p-th source layer counting down from L-1 */
+  int32_t S_cap;     /* cache slots per (channel, sequence, KV head) */
+  int32_t ctx_max;   /* upper bound on ctx_len[b] */
+  int32_t dtype;     /* enum wm_dtype */
+  int32_t mix_mode;  /* enum wm_mix_mode */
+  int32_t mask_mode; /* enum wm_mask_mode */
+  float eps;         /* RMSNorm epsilon (e.g. 1e-6) */
+  float rope_theta;  /* RoPE base (e.g. 1e6) */
+} wm_dims;
+
+/* Parameters, device pointers, in dtype, row-major. L' = ceil(L / p). */
+typedef struct wm_params {
+  const void *g_pre;   /* [2][L][D]        pre-mix RMSNorm gains, key then value branch */
+  const void *W_alpha; /* [2][k*L][L'*D]   router weights; input = normed states of layers
+                                           {L-1-p*m}, stacked in ascending layer order */
+  const void *b_alpha; /* [2][k*L]         router bias; alpha[j][l] = out[j*L + l] */
+  const void *g_mid;   /* [2][k][D]        mid RMSNorm gains per channel */
+  const void *Wk;      /* [k][Hkv*d][D]    key projection per channel */
+  const void *Wv;      /* [k][Hkv*d][D]    value projection per channel */
+  const void *g_knorm; /* [k][d]           key-norm gain per channel (shared by KV heads) */
+  const void *Kd;      /* [k][Hkv][d]      learned dummy key (used as stored, no RoPE) */
+  const void *Vd;      /* [k][Hkv][d]      learned dummy value */
+  const void *g_in;    /* [L][D]           consumer input RMSNorm gains */
+  const void *Wq;      /* [L][Hq*d][D]     consumer query projections */
+  const void *g_qnorm; /* [L][d]           consumer q-norm gains (shared by query heads) */
+} wm_params;
+
+/* Section 3.1 Step 1 (mix L states into k channels), both branches.
+ *   H         device [B][T_new][L][D] in dtype: state entering each layer
+ *   alpha_out device [2][N][k][L] fp32 or NULL: mixing weights per token
+ *             (linear router output, or its softmax over l in WM_MIX_SOFTMAX)
+ *   mixed_out device [2][k][N][D] in dtype: h~_j = sum_l alpha[j][l] RMSNorm(h_l)
+ * Uses g_pre, W_alpha, b_alpha. */
+int wm_router_mix(const wm_dims *dims, const wm_params *params, const void *H,
+                  float *alpha_out, void *mixed_out, void *ws, size_t ws_bytes,
+                  wm_stream_t stream);
+
+/* Section 3.1 Step 2 (KV projections and cache storage).
+ *   mixed   device [2][k][N][D] in dtype: mixed channels (key branch, value branch)
+ *   ctx_len device int32 [B] or NULL
+ *   Kc, Vc  device [k][B][Hkv][S_cap][d] in dtype: channel-major cache. Slot
+ *           ctx_len[b] + i receives RoPE(knorm(W^K_j RMSNorm(h~^K_j))) and
+ *           W^V_j RMSNorm(h~^V_j); no other slot is written.
+ * Uses g_mid, Wk, Wv, g_knorm. */
+int wm_kv_project(const wm_dims *dims, const wm_params *params, const void *mixed,
+                  const int32_t *ctx_len, void *Kc, void *Vc, void *ws, size_t ws_bytes,
+                  wm_stream_t stream);
+
+/* The consumer's query (the unchanged Qwen3 block, Section 4.1):
+ * Q_l = RoPE(qnorm(W^Q_l RMSNorm_in(h_l))) at the token's position.
+ *   H       device [B][T_new][L][D] in dtype
+ *   ctx_len device int32 [B] or NULL
+ *   Q       device [L][B][Hq][T_new][d] in dtype
+ * Uses g_in, Wq, g_qnorm. */
+int wm_q_project(const wm_dims *dims, const wm_params *params, const void *H,
+                 const int32_t *ctx_len, void *Q, void *ws, size_t ws_bytes,
+                 wm_stream_t stream);
+
+/* Section 3.1 Step 3 and Section 3.2: consumer l attends channel chan_map[l].
+ *   Q        device [L][B][Hq][T_new][d] in dtype (after q-norm and RoPE)
+ *   chan_map host int32 [L], entries in [0, k) (the paper's choice is l mod k)
+ *   ctx_len  device int32 [B] or NULL
+ *   Kc, Vc   device [k][B][Hkv][S_cap][d] in dtype (read only)
+ *   O        device [L][B][T_new][Hq*d] in dtype: softmax(q K^T / sqrt(d)) V over
+ *            the visible slots of the mask mode (dummy Kd/Vd of the channel
+ *            included in WM_MASK_PAPER)
+ * Uses Kd, Vd. T_new <= 4 takes the split-S decode kernels. */
+int wm_channel_attend(const wm_dims *dims, const wm_params *params, const void *Q,
+                      const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
+                      const void *Vc, void *O, void *ws, size_t ws_bytes,
+                      wm_stream_t stream);
+
+/* The fused step: pool the T_new new tokens of every sequence into cache slots
+ * [ctx_len[b], ctx_len[b] + T_new) (Steps 1-2), project the consumer queries,
+ * then every consumer attends its channel (Step 3). With ctx_len = 0 and
+ * T_new = T this is one full-sequence (Jacobi) pass, Section 3.3; with
+ * T_new = 1 it is a decode step, Section 3.2.
+ *   H        device [B][T_new][L][D] in dtype
+ *   chan_map host int32 [L]
+ *   ctx_len  device int32 [B] or NULL
+ *   Kc, Vc   device [k][B][Hkv][S_cap][d] in dtype (slots < ctx_len[b] read, new
+ *            slots written)
+ *   O        device [L][B][T_new][Hq*d] in dtype */
+int wm_layer_step(const wm_dims *dims, const wm_params *params, const void *H,
+                  const int32_t *chan_map, const int32_t *ctx_len, void *Kc, void *Vc,
+                  void *O, void *ws, size_t ws_bytes, wm_stream_t stream);
+
+/* wm_layer_step that also records caller-created HIP events (hipEvent_t,
+ * passed as void*) on `stream` at its phase boundaries, for per-phase timing of
+ * the fused step: events[0] before the row norms, [1] before the router, [2]
+ * before the mix, [3] before the K/V projection, [4] before the Q projection,
+ * [5] before the channel attention, [6] after it. The array holds
+ * WM_PROFILE_EVENTS non-NULL handles, owned by the caller. Results and errors
+ * are those of wm_layer_step. */
+#define WM_PROFILE_EVENTS 7
+int wm_layer_step_profiled(const wm_dims *dims, const wm_params *params, const void *H,
+                           const int32_t *chan_map, const int32_t *ctx_len, void *Kc, void *Vc,
+                           void *O, void *ws, size_t ws_bytes, wm_stream_t stream,
+                           void *const *events);
+
+/* Bytes of device workspace the op needs for these dims (0 if dims invalid). */
+size_t wm_workspace_size(const wm_dims *dims, int op);
+
+/* Host-only validation of dims for op (and of chan_map when non-NULL). */
+int wm_validate(const wm_dims *dims, int op, const int32_t *chan_map);
+
+/* Host helpers (no GPU work). */
+/* Inverse of chan_map (Section 3.1 Step 3): channel c is read by layers
+ * members[offsets[c] .. offsets[c+1]) in ascending order. offsets has k+1
+ * entries, members L. */
+int wm_channel_groups(int32_t L, int32_t k, const int32_t *chan_map, int32_t *offsets,
+                      int32_t *members);
+/* The paper's fixed selection: map[l] = l mod k. */
+int wm_default_map(int32_t L, int32_t k, int32_t *chan_map);
+/* The paper's router bias initialisation (Section 3.1, Router initialization):
+ * k = 1 top layer; 1 < k < L layer l -> channel l mod k; k = L channel j <-
+ * layer min(j+1, L-1). b has k*L floats, alpha[j][l] = b[j*L + l]. */
+int wm_init_bias(int32_t L, int32_t k, float *b);
+
+const char *wm_last_error(void);
+const char *wm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WHITEMATTER_H */

@@ -230,6 +230,19 @@ def pool(dims: Dims, params, H, ctx_len, Kc, Vc, toks=None):
                    ctypes.c_int(n), _ptr(Kc), _ptr(Vc))
 
 
+def pool_rows(dims: Dims, params, H, ctx_len=None, toks=None):
+    """Each token's cache rows (K, V), shape [N, k, Hkv, d], at position ctx_len[b] + i."""
+    P = _as_params(params)
+    H = _f64(H)
+    ctx = _ctx(dims, ctx_len)
+    Kr = np.zeros((dims.N, dims.k, dims.Hkv, dims.d))
+    Vr = np.zeros_like(Kr)
+    arr, n, p = _ilist(toks)
+    lib().wmo_pool_rows(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(H), _ptr(ctx), p,
+                        ctypes.c_int(n), _ptr(Kr), _ptr(Vr))
+    return Kr, Vr
+
+
 def q_project(dims: Dims, params, H, ctx_len=None, toks=None) -> np.ndarray:
     P = _as_params(params)
     H = _f64(H)

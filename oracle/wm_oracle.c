@@ -423,6 +423,27 @@ void wmo_pool(const wmo_dims *dm, const wmo_params *P, const double *H, const in
     }
 }
 
+/* Steps 1 and 2 for the listed tokens, returning each token's cache rows
+ * Krows/Vrows[n][k][Hkv][d] (as stored at its slot) instead of a cache. */
+void wmo_pool_rows(const wmo_dims *dm, const wmo_params *P, const double *H, const int *ctx_len,
+                   const int *toks, int ntok, double *Krows, double *Vrows)
+{
+    int N = dm->B * dm->T_new, L = dm->L, k = dm->k, D = dm->D, KV = dm->k * dm->Hkv * dm->d;
+    int cnt = list_len(toks, ntok, N);
+#pragma omp parallel for schedule(dynamic)
+    for (int t = 0; t < cnt; ++t) {
+        int n = toks ? toks[t] : t;
+        int b = n / dm->T_new, i = n % dm->T_new;
+        long pos = (long)(ctx_len ? ctx_len[b] : 0) + i;
+        double *al = (double *)malloc(sizeof(double) * 2 * k * L);
+        double *mx = (double *)malloc(sizeof(double) * 2 * k * D);
+        wmo_pool_mix_token(dm, P, H + (size_t)n * L * D, al, mx);
+        wmo_project_token(dm, P, mx, (double)pos, Krows + (size_t)n * KV, Vrows + (size_t)n * KV);
+        free(mx);
+        free(al);
+    }
+}
+
 void wmo_q_project(const wmo_dims *dm, const wmo_params *P, const double *H, const int *ctx_len,
                    const int *toks, int ntok, double *Q)
 {

@@ -1,0 +1,225 @@
+"""Python binding of libwhitematter.so -- the MI355X (gfx950) WhiteMatter hot path.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of the library (see include/whitematter.h for the C ABI). PyTorch
+supplies device memory and streams. There is no fallback: if the library is
+missing, importing the compute entry points raises.
+
+The library shares the HIP runtime that torch has loaded, so torch is
+imported before the library is opened.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwhitematter.so")
+
+OK, ERR_ARG, ERR_SHAPE, ERR_DTYPE, ERR_MAP, ERR_CAPACITY, ERR_WORKSPACE, ERR_LAUNCH = range(8)
+F32, BF16 = 0, 1
+MIX_LINEAR, MIX_SOFTMAX = 0, 1
+MASK_PAPER, MASK_INCLUSIVE = 0, 1
+OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP = range(5)
+
+PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
+               "Kd", "Vd", "g_in", "Wq", "g_qnorm")
+
+
+class WMError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("whitematter error %d: %s" % (code, msg))
+        self.code = code
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("B", "T_new", "L", "k", "D", "Hq", "Hkv", "d", "p", "S_cap", "ctx_max",
+                 "dtype", "mix_mode", "mask_mode")] + [("eps", ctypes.c_float),
+                                                       ("rope_theta", ctypes.c_float)]
+
+    @property
+    def N(self) -> int:
+        return self.B * self.T_new
+
+
+class Params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_NAMES]
+
+
+_lib = None
+_vp, _i32p, _sz = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """Open libwhitematter.so (built by paper_2608_18486_amd.build); raise if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libwhitematter.so is not built (%s); run "
+                          "`python -m paper_2608_18486_amd.build`" % LIB_PATH)
+    L = ctypes.CDLL(LIB_PATH)
+    D, P = ctypes.POINTER(Dims), ctypes.POINTER(Params)
+    sig = {
+        "wm_router_mix": [D, P, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_kv_project": [D, P, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_q_project": [D, P, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_channel_attend": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_layer_step": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_validate": [D, ctypes.c_int, _i32p],
+        "wm_channel_groups": [ctypes.c_int32, ctypes.c_int32, _i32p, _i32p, _i32p],
+        "wm_default_map": [ctypes.c_int32, ctypes.c_int32, _i32p],
+        "wm_init_bias": [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_float)],
+    }
+    for name, argtypes in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = argtypes
+        fn.restype = ctypes.c_int
+    L.wm_workspace_size.argtypes = [D, ctypes.c_int]
+    L.wm_workspace_size.restype = ctypes.c_size_t
+    L.wm_last_error.restype = ctypes.c_char_p
+    L.wm_version.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def last_error() -> str:
+    return lib().wm_last_error().decode()
+
+
+def version() -> str:
+    return lib().wm_version().decode()
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise WMError(rc, last_error())
+
+
+def make_dims(B, T_new, L, k, D, Hq, Hkv, d, p=1, S_cap=0, ctx_max=0, dtype=BF16,
+              mix_mode=MIX_LINEAR, mask_mode=MASK_PAPER, eps=1e-6, rope_theta=1e6) -> Dims:
+    return Dims(B, T_new, L, k, D, Hq, Hkv, d, p, S_cap, ctx_max, dtype, mix_mode, mask_mode,
+                eps, rope_theta)
+
+
+def dtype_code(t: torch.dtype) -> int:
+    if t == torch.bfloat16:
+        return BF16
+    if t == torch.float32:
+        return F32
+    raise ValueError("unsupported dtype %s" % t)
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _map(chan_map):
+    arr = (ctypes.c_int32 * len(chan_map))(*[int(c) for c in chan_map])
+    return arr
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+class ParamSet:
+    """Device parameters (a dict of tensors keyed by PARAM_NAMES) as a wm_params."""
+
+    def __init__(self, params: dict):
+        self.tensors = {n: params[n].contiguous() for n in PARAM_NAMES}
+        self.c = Params(*[self.tensors[n].data_ptr() for n in PARAM_NAMES])
+
+
+def _params(params) -> ParamSet:
+    return params if isinstance(params, ParamSet) else ParamSet(params)
+
+
+def workspace_size(dims: Dims, op: int) -> int:
+    return int(lib().wm_workspace_size(ctypes.byref(dims), op))
+
+
+def workspace(dims: Dims, op: int, device="cuda") -> torch.Tensor:
+    """Allocate the op's workspace with torch (the caching allocator aligns to >= 512 B)."""
+    n = workspace_size(dims, op)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def _ws(dims, op, ws, device):
+    if device is None:
+        device = "cuda"
+    if ws is None:
+        ws = workspace(dims, op, device)
+    return ws, ws.data_ptr(), ws.numel()
+
+
+def validate(dims: Dims, op: int, chan_map=None) -> int:
+    m = _map(chan_map) if chan_map is not None else None
+    return int(lib().wm_validate(ctypes.byref(dims), op, m))
+
+
+def channel_groups(L: int, k: int, chan_map):
+    off = (ctypes.c_int32 * (k + 1))()
+    mem = (ctypes.c_int32 * L)()
+    _check(lib().wm_channel_groups(L, k, _map(chan_map), off, mem))
+    return list(off), list(mem)
+
+
+def default_map(L: int, k: int):
+    m = (ctypes.c_int32 * L)()
+    _check(lib().wm_default_map(L, k, m))
+    return list(m)
+
+
+def init_bias(L: int, k: int):
+    b = (ctypes.c_float * (k * L))()
+    _check(lib().wm_init_bias(L, k, b))
+    return list(b)
+
+
+# ------------------------------------------------------------ compute calls
+
+def router_mix(dims: Dims, params, H, mixed_out, alpha_out=None, ws=None, stream=None):
+    P = _params(params)
+    ws, wp, wn = _ws(dims, OP_ROUTER_MIX, ws, getattr(H, "device", None))
+    _check(lib().wm_router_mix(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H), _ptr(alpha_out),
+                               _ptr(mixed_out), wp, wn, _stream(stream)))
+
+
+def kv_project(dims: Dims, params, mixed, ctx_len, Kc, Vc, ws=None, stream=None):
+    P = _params(params)
+    ws, wp, wn = _ws(dims, OP_KV_PROJECT, ws, getattr(mixed, "device", None))
+    _check(lib().wm_kv_project(ctypes.byref(dims), ctypes.byref(P.c), _ptr(mixed), _ptr(ctx_len),
+                               _ptr(Kc), _ptr(Vc), wp, wn, _stream(stream)))
+
+
+def q_project(dims: Dims, params, H, ctx_len, Q, ws=None, stream=None):
+    P = _params(params)
+    ws, wp, wn = _ws(dims, OP_Q_PROJECT, ws, getattr(H, "device", None))
+    _check(lib().wm_q_project(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H), _ptr(ctx_len),
+                              _ptr(Q), wp, wn, _stream(stream)))
+
+
+def channel_attend(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, ws=None, stream=None):
+    P = _params(params)
+    ws, wp, wn = _ws(dims, OP_CHANNEL_ATTEND, ws, getattr(Q, "device", None))
+    _check(lib().wm_channel_attend(ctypes.byref(dims), ctypes.byref(P.c), _ptr(Q),
+                                   _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O),
+                                   wp, wn, _stream(stream)))
+
+
+def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws=None, stream=None):
+    P = _params(params)
+    ws, wp, wn = _ws(dims, OP_LAYER_STEP, ws, getattr(H, "device", None))
+    _check(lib().wm_layer_step(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H), _map(chan_map),
+                               _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O), wp, wn,
+                               _stream(stream)))

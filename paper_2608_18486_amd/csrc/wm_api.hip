@@ -1,0 +1,462 @@
+// Host layer of libwhitematter.so: the C ABI declared in include/whitematter.h.
+// Validates every argument on the host before anything is enqueued, lays out
+// the caller's workspace, builds the channel -> consumers table and launches
+// the kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/whitematter.h"
+#include "wm_internal.hpp"
+
+using wm::bf16;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+size_t elem_size(const wm_dims& d) { return d.dtype == WM_BF16 ? 2 : 4; }
+bool decode_path(const wm_dims& d) { return d.T_new <= 4; }
+
+struct Layout {
+  size_t rinv = 0, alpha = 0, mixed = 0, rinv_mid = 0, tab = 0, q = 0, part = 0, total = 0;
+};
+
+wm::Shape make_shape(const wm_dims& d) {
+  wm::Shape s;
+  s.B = d.B;
+  s.T_new = d.T_new;
+  s.L = d.L;
+  s.k = d.k;
+  s.D = d.D;
+  s.Hq = d.Hq;
+  s.Hkv = d.Hkv;
+  s.d = d.d;
+  s.p = d.p;
+  s.Lp = (d.L + d.p - 1) / d.p;
+  s.S_cap = d.S_cap;
+  s.mix_softmax = d.mix_mode == WM_MIX_SOFTMAX;
+  s.mask_paper = d.mask_mode == WM_MASK_PAPER;
+  s.eps = d.eps;
+  s.rope_theta = d.rope_theta;
+  s.ctx_max = d.ctx_max;
+  return s;
+}
+
+// Workspace regions for an op (offsets in bytes, each 256-byte aligned).
+Layout layout(const wm_dims& d, int op) {
+  Layout Ly;
+  const size_t N = (size_t)d.B * d.T_new, es = elem_size(d);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += al256(bytes);
+    return at;
+  };
+  const bool all = op == WM_OP_LAYER_STEP;
+  if (op == WM_OP_ROUTER_MIX || op == WM_OP_Q_PROJECT || all) Ly.rinv = take(N * d.L * 4);
+  if (op == WM_OP_ROUTER_MIX || all) Ly.alpha = take(2 * N * d.k * d.L * 4);
+  if (all) Ly.mixed = take(2 * (size_t)d.k * N * d.D * es);
+  if (op == WM_OP_ROUTER_MIX || op == WM_OP_KV_PROJECT || all)
+    Ly.rinv_mid = take(2 * (size_t)d.k * N * 4);
+  if (op == WM_OP_KV_PROJECT || op == WM_OP_Q_PROJECT || all) Ly.tab = take(N * d.d * 4);
+  if (all) Ly.q = take((size_t)d.L * N * d.Hq * d.d * es);
+  if ((op == WM_OP_CHANNEL_ATTEND || all) && decode_path(d))
+    Ly.part = take(wm::decode_partials_bytes(make_shape(d)));
+  Ly.total = N == 0 ? 0 : off;
+  return Ly;
+}
+
+bool uses_cache(int op) {
+  return op == WM_OP_KV_PROJECT || op == WM_OP_CHANNEL_ATTEND || op == WM_OP_LAYER_STEP;
+}
+
+int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
+  if (!dp) return fail(WM_ERR_ARG, "dims is NULL");
+  const wm_dims& d = *dp;
+  if (op < WM_OP_ROUTER_MIX || op > WM_OP_LAYER_STEP) return fail(WM_ERR_ARG, "unknown op %d", op);
+  if (d.dtype != WM_F32 && d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "unknown dtype %d", d.dtype);
+  if (d.mix_mode != WM_MIX_LINEAR && d.mix_mode != WM_MIX_SOFTMAX)
+    return fail(WM_ERR_DTYPE, "unknown mix_mode %d", d.mix_mode);
+  if (d.mask_mode != WM_MASK_PAPER && d.mask_mode != WM_MASK_INCLUSIVE)
+    return fail(WM_ERR_DTYPE, "unknown mask_mode %d", d.mask_mode);
+  if (d.B < 0 || d.T_new < 0) return fail(WM_ERR_ARG, "B and T_new must be >= 0");
+  if (d.L < 1 || d.L > wm::kMaxLayers) return fail(WM_ERR_SHAPE, "L must be in [1, %d]", wm::kMaxLayers);
+  if (d.k < 1 || d.k > d.L) return fail(WM_ERR_SHAPE, "k must be in [1, L]");
+  if (d.D < 32 || d.D % 32 != 0) return fail(WM_ERR_SHAPE, "D must be a positive multiple of 32");
+  if (d.Hq < 1 || d.Hkv < 1 || d.Hq % d.Hkv != 0)
+    return fail(WM_ERR_SHAPE, "Hq must be a positive multiple of Hkv");
+  if (d.d != 32 && d.d != 64) return fail(WM_ERR_SHAPE, "head dim d must be 32 or 64");
+  if (d.p < 1 || d.p > d.L) return fail(WM_ERR_SHAPE, "p must be in [1, L]");
+  if (!(d.eps > 0.f) || !std::isfinite(d.eps)) return fail(WM_ERR_ARG, "eps must be positive");
+  if (!(d.rope_theta > 0.f) || !std::isfinite(d.rope_theta))
+    return fail(WM_ERR_ARG, "rope_theta must be positive");
+  if (d.ctx_max < 0) return fail(WM_ERR_ARG, "ctx_max must be >= 0");
+  if (uses_cache(op)) {
+    if (d.S_cap < 1) return fail(WM_ERR_SHAPE, "S_cap must be >= 1");
+    if ((long long)d.ctx_max + d.T_new > d.S_cap)
+      return fail(WM_ERR_CAPACITY, "ctx_max + T_new = %lld exceeds S_cap = %d",
+                  (long long)d.ctx_max + d.T_new, d.S_cap);
+  }
+  const long long N = (long long)d.B * d.T_new;
+  if (N > (1LL << 30)) return fail(WM_ERR_SHAPE, "B * T_new too large");
+  if ((N + 127) / 128 > 65535) return fail(WM_ERR_SHAPE, "B * T_new exceeds the grid limit");
+  if ((long long)d.Hq * d.B * d.L > 65535 || (long long)d.Hkv * d.B * d.k > 65535)
+    return fail(WM_ERR_SHAPE, "heads x sequences x layers exceeds the grid limit");
+  if (op == WM_OP_ROUTER_MIX || op == WM_OP_LAYER_STEP) {
+    size_t lds = (size_t)d.L * d.D * elem_size(d) + 4 * (2 * (size_t)d.k * d.L + 4 * d.k);
+    if (lds > 65536) return fail(WM_ERR_SHAPE, "L * D too large for the mix kernel (%zu B of LDS)", lds);
+  }
+  if (chan_map) {
+    for (int l = 0; l < d.L; ++l)
+      if (chan_map[l] < 0 || chan_map[l] >= d.k)
+        return fail(WM_ERR_MAP, "chan_map[%d] = %d is outside [0, %d)", l, chan_map[l], d.k);
+  }
+  return WM_OK;
+}
+
+int need_ptr(const void* p, const char* name) {
+  if (!p) return fail(WM_ERR_ARG, "%s is NULL", name);
+  if ((uintptr_t)p % 16 != 0) return fail(WM_ERR_ARG, "%s is not 16-byte aligned", name);
+  return WM_OK;
+}
+
+int check_ws(const wm_dims& d, int op, void* ws, size_t ws_bytes) {
+  size_t need = layout(d, op).total;
+  if (need == 0) return WM_OK;
+  if (!ws) return fail(WM_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if ((uintptr_t)ws % 256 != 0) return fail(WM_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (ws_bytes < need) return fail(WM_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+  return WM_OK;
+}
+
+int launched() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(WM_ERR_LAUNCH, "launch failed: %s", hipGetErrorString(e));
+  return WM_OK;
+}
+
+#define WM_TRY(x)              \
+  do {                         \
+    int _rc = (x);             \
+    if (_rc != WM_OK) return _rc; \
+  } while (0)
+
+wm::LayerTable router_layers(const wm_dims& d) {
+  wm::LayerTable t{};
+  int Lp = (d.L + d.p - 1) / d.p;
+  for (int m = 0; m < Lp; ++m) t.v[Lp - 1 - m] = d.L - 1 - d.p * m;
+  return t;
+}
+
+wm::LayerTable map_table(const wm_dims& d, const int32_t* chan_map) {
+  wm::LayerTable t{};
+  for (int l = 0; l < d.L; ++l) t.v[l] = chan_map[l];
+  return t;
+}
+
+wm::ChannelGroups groups(const wm_dims& d, const int32_t* chan_map) {
+  wm::ChannelGroups g{};
+  wm_channel_groups(d.L, d.k, chan_map, g.offsets, g.members);
+  return g;
+}
+
+char* at(void* ws, size_t off) { return (char*)ws + off; }
+
+// ----------------------------------------------------------------- ops
+template <typename T>
+void run_router_mix(const wm_dims& d, const wm_params& P, const T* H, float* alpha_out, T* mixed,
+                    void* ws, hipStream_t s) {
+  wm::Shape sh = make_shape(d);
+  Layout Ly = layout(d, WM_OP_ROUTER_MIX);
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* alpha = alpha_out ? alpha_out : (float*)at(ws, Ly.alpha);
+  wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
+  wm::launch_router<T>(sh, router_layers(d), H, rinv, (const T*)P.g_pre, (const T*)P.W_alpha,
+                       (const T*)P.b_alpha, alpha, s);
+  wm::launch_mix<T>(sh, H, rinv, (const T*)P.g_pre, alpha, mixed, (float*)at(ws, Ly.rinv_mid), s);
+}
+
+template <typename T>
+void run_kv_project(const wm_dims& d, const wm_params& P, const T* mixed, const int32_t* ctx_len,
+                    T* Kc, T* Vc, void* ws, hipStream_t s) {
+  wm::Shape sh = make_shape(d);
+  Layout Ly = layout(d, WM_OP_KV_PROJECT);
+  float* rinv_mid = (float*)at(ws, Ly.rinv_mid);
+  float* tab = (float*)at(ws, Ly.tab);
+  wm::launch_row_rms<T>(mixed, 2L * sh.k * sh.N(), sh.D, sh.eps, rinv_mid, s);
+  wm::launch_rope_table(sh, ctx_len, tab, s);
+  wm::launch_kv_project<T>(sh, mixed, rinv_mid, (const T*)P.g_mid, (const T*)P.Wk,
+                           (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc, s);
+}
+
+template <typename T>
+void run_q_project(const wm_dims& d, const wm_params& P, const T* H, const int32_t* ctx_len, T* Q,
+                   void* ws, hipStream_t s) {
+  wm::Shape sh = make_shape(d);
+  Layout Ly = layout(d, WM_OP_Q_PROJECT);
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* tab = (float*)at(ws, Ly.tab);
+  wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
+  wm::launch_rope_table(sh, ctx_len, tab, s);
+  wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
+                          tab, Q, s);
+}
+
+template <typename T>
+void run_attend(const wm_dims& d, const wm_params& P, const T* Q, const int32_t* chan_map,
+                const int32_t* ctx_len, const T* Kc, const T* Vc, T* O, float* part,
+                hipStream_t s) {
+  wm::Shape sh = make_shape(d);
+  wm::LayerTable mt = map_table(d, chan_map);
+  if (decode_path(d))
+    wm::launch_attend_decode<T>(sh, mt, groups(d, chan_map), Q, Kc, Vc, (const T*)P.Kd,
+                                (const T*)P.Vd, ctx_len, part, O, s);
+  else
+    wm::launch_attend_prefill<T>(sh, mt, Q, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len, O, s);
+}
+
+template <typename T>
+void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int32_t* chan_map,
+                    const int32_t* ctx_len, T* Kc, T* Vc, T* O, void* ws, hipStream_t s,
+                    void* const* events) {
+  auto mark = [&](int i) {
+    if (events) (void)hipEventRecord((hipEvent_t)events[i], s);
+  };
+  wm::Shape sh = make_shape(d);
+  Layout Ly = layout(d, WM_OP_LAYER_STEP);
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* alpha = (float*)at(ws, Ly.alpha);
+  T* mixed = (T*)at(ws, Ly.mixed);
+  float* rinv_mid = (float*)at(ws, Ly.rinv_mid);
+  float* tab = (float*)at(ws, Ly.tab);
+  T* Q = (T*)at(ws, Ly.q);
+  mark(0);
+  wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
+  wm::launch_rope_table(sh, ctx_len, tab, s);
+  mark(1);
+  wm::launch_router<T>(sh, router_layers(d), H, rinv, (const T*)P.g_pre, (const T*)P.W_alpha,
+                       (const T*)P.b_alpha, alpha, s);
+  mark(2);
+  wm::launch_mix<T>(sh, H, rinv, (const T*)P.g_pre, alpha, mixed, rinv_mid, s);
+  mark(3);
+  wm::launch_kv_project<T>(sh, mixed, rinv_mid, (const T*)P.g_mid, (const T*)P.Wk,
+                           (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc, s);
+  mark(4);
+  wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
+                          tab, Q, s);
+  mark(5);
+  run_attend<T>(d, P, Q, chan_map, ctx_len, Kc, Vc, O, (float*)at(ws, Ly.part), s);
+  mark(6);
+}
+
+int check_params(const wm_params* P, std::initializer_list<int> which) {
+  if (!P) return fail(WM_ERR_ARG, "params is NULL");
+  static const char* names[] = {"g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv",
+                                "g_knorm", "Kd", "Vd", "g_in", "Wq", "g_qnorm"};
+  const void* ptrs[] = {P->g_pre, P->W_alpha, P->b_alpha, P->g_mid, P->Wk, P->Wv,
+                        P->g_knorm, P->Kd, P->Vd, P->g_in, P->Wq, P->g_qnorm};
+  for (int i : which) {
+    if (!ptrs[i]) return fail(WM_ERR_ARG, "params->%s is NULL", names[i]);
+    if ((uintptr_t)ptrs[i] % 16 != 0)
+      return fail(WM_ERR_ARG, "params->%s is not 16-byte aligned", names[i]);
+  }
+  return WM_OK;
+}
+
+enum { P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD, P_GIN, P_WQ, P_GQN };
+
+}  // namespace
+
+extern "C" {
+
+const char* wm_last_error(void) { return g_err; }
+const char* wm_version(void) { return "whitematter-gfx950 0.1.0"; }
+
+int wm_validate(const wm_dims* dims, int op, const int32_t* chan_map) {
+  return validate_dims(dims, op, chan_map);
+}
+
+size_t wm_workspace_size(const wm_dims* dims, int op) {
+  if (validate_dims(dims, op, nullptr) != WM_OK) return 0;
+  return layout(*dims, op).total;
+}
+
+int wm_channel_groups(int32_t L, int32_t k, const int32_t* chan_map, int32_t* offsets,
+                      int32_t* members) {
+  if (!chan_map || !offsets || !members) return fail(WM_ERR_ARG, "NULL argument");
+  if (L < 1 || k < 1) return fail(WM_ERR_SHAPE, "L and k must be >= 1");
+  for (int l = 0; l < L; ++l)
+    if (chan_map[l] < 0 || chan_map[l] >= k)
+      return fail(WM_ERR_MAP, "chan_map[%d] = %d is outside [0, %d)", l, chan_map[l], k);
+  int pos = 0;
+  for (int c = 0; c < k; ++c) {
+    offsets[c] = pos;
+    for (int l = 0; l < L; ++l)
+      if (chan_map[l] == c) members[pos++] = l;
+  }
+  offsets[k] = pos;
+  return WM_OK;
+}
+
+int wm_default_map(int32_t L, int32_t k, int32_t* chan_map) {
+  if (!chan_map) return fail(WM_ERR_ARG, "NULL argument");
+  if (L < 1 || k < 1 || k > L) return fail(WM_ERR_SHAPE, "need 1 <= k <= L");
+  for (int l = 0; l < L; ++l) chan_map[l] = l % k;
+  return WM_OK;
+}
+
+int wm_init_bias(int32_t L, int32_t k, float* b) {
+  if (!b) return fail(WM_ERR_ARG, "NULL argument");
+  if (L < 1 || k < 1 || k > L) return fail(WM_ERR_SHAPE, "need 1 <= k <= L");
+  std::memset(b, 0, sizeof(float) * (size_t)k * L);
+  if (k == 1) {
+    b[L - 1] = 1.f;  // the single channel starts on the top layer
+  } else if (k < L) {
+    for (int l = 0; l < L; ++l) b[(l % k) * L + l] = 1.f;  // cyclic
+  } else {
+    for (int j = 0; j < k; ++j) b[j * L + (j + 1 < L - 1 ? j + 1 : L - 1)] = 1.f;  // shifted identity
+  }
+  return WM_OK;
+}
+
+int wm_router_mix(const wm_dims* dims, const wm_params* params, const void* H, float* alpha_out,
+                  void* mixed_out, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  WM_TRY(validate_dims(dims, WM_OP_ROUTER_MIX, nullptr));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA}));
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(need_ptr(mixed_out, "mixed_out"));
+  if (alpha_out && (uintptr_t)alpha_out % 16) return fail(WM_ERR_ARG, "alpha_out is not 16-byte aligned");
+  WM_TRY(check_ws(d, WM_OP_ROUTER_MIX, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  if (d.dtype == WM_BF16)
+    run_router_mix<bf16>(d, *params, (const bf16*)H, alpha_out, (bf16*)mixed_out, ws, s);
+  else
+    run_router_mix<float>(d, *params, (const float*)H, alpha_out, (float*)mixed_out, ws, s);
+  return launched();
+}
+
+int wm_kv_project(const wm_dims* dims, const wm_params* params, const void* mixed,
+                  const int32_t* ctx_len, void* Kc, void* Vc, void* ws, size_t ws_bytes,
+                  wm_stream_t stream) {
+  WM_TRY(validate_dims(dims, WM_OP_KV_PROJECT, nullptr));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_params(params, {P_GMID, P_WK, P_WV, P_GKN}));
+  WM_TRY(need_ptr(mixed, "mixed"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(check_ws(d, WM_OP_KV_PROJECT, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  if (d.dtype == WM_BF16)
+    run_kv_project<bf16>(d, *params, (const bf16*)mixed, ctx_len, (bf16*)Kc, (bf16*)Vc, ws, s);
+  else
+    run_kv_project<float>(d, *params, (const float*)mixed, ctx_len, (float*)Kc, (float*)Vc, ws, s);
+  return launched();
+}
+
+int wm_q_project(const wm_dims* dims, const wm_params* params, const void* H,
+                 const int32_t* ctx_len, void* Q, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  WM_TRY(validate_dims(dims, WM_OP_Q_PROJECT, nullptr));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_params(params, {P_GIN, P_WQ, P_GQN}));
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(need_ptr(Q, "Q"));
+  WM_TRY(check_ws(d, WM_OP_Q_PROJECT, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  if (d.dtype == WM_BF16)
+    run_q_project<bf16>(d, *params, (const bf16*)H, ctx_len, (bf16*)Q, ws, s);
+  else
+    run_q_project<float>(d, *params, (const float*)H, ctx_len, (float*)Q, ws, s);
+  return launched();
+}
+
+int wm_channel_attend(const wm_dims* dims, const wm_params* params, const void* Q,
+                      const int32_t* chan_map, const int32_t* ctx_len, const void* Kc,
+                      const void* Vc, void* O, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_CHANNEL_ATTEND, chan_map));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_KD, P_VD}));
+  else if (!params) return fail(WM_ERR_ARG, "params is NULL");
+  WM_TRY(need_ptr(Q, "Q"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(need_ptr(O, "O"));
+  WM_TRY(check_ws(d, WM_OP_CHANNEL_ATTEND, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  float* part = (float*)at(ws, layout(d, WM_OP_CHANNEL_ATTEND).part);
+  if (d.dtype == WM_BF16)
+    run_attend<bf16>(d, *params, (const bf16*)Q, chan_map, ctx_len, (const bf16*)Kc,
+                     (const bf16*)Vc, (bf16*)O, part, s);
+  else
+    run_attend<float>(d, *params, (const float*)Q, chan_map, ctx_len, (const float*)Kc,
+                      (const float*)Vc, (float*)O, part, s);
+  return launched();
+}
+
+static int layer_step_impl(const wm_dims* dims, const wm_params* params, const void* H,
+                           const int32_t* chan_map, const int32_t* ctx_len, void* Kc, void* Vc,
+                           void* O, void* ws, size_t ws_bytes, wm_stream_t stream,
+                           void* const* events) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_LAYER_STEP, chan_map));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD,
+                               P_GIN, P_WQ, P_GQN}));
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(need_ptr(O, "O"));
+  WM_TRY(check_ws(d, WM_OP_LAYER_STEP, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  if (d.dtype == WM_BF16)
+    run_layer_step<bf16>(d, *params, (const bf16*)H, chan_map, ctx_len, (bf16*)Kc, (bf16*)Vc,
+                         (bf16*)O, ws, s, events);
+  else
+    run_layer_step<float>(d, *params, (const float*)H, chan_map, ctx_len, (float*)Kc, (float*)Vc,
+                          (float*)O, ws, s, events);
+  return launched();
+}
+
+int wm_layer_step(const wm_dims* dims, const wm_params* params, const void* H,
+                  const int32_t* chan_map, const int32_t* ctx_len, void* Kc, void* Vc, void* O,
+                  void* ws, size_t ws_bytes, wm_stream_t stream) {
+  return layer_step_impl(dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws, ws_bytes, stream,
+                         nullptr);
+}
+
+int wm_layer_step_profiled(const wm_dims* dims, const wm_params* params, const void* H,
+                           const int32_t* chan_map, const int32_t* ctx_len, void* Kc, void* Vc,
+                           void* O, void* ws, size_t ws_bytes, wm_stream_t stream,
+                           void* const* events) {
+  if (!events) return fail(WM_ERR_ARG, "events is NULL");
+  for (int i = 0; i < WM_PROFILE_EVENTS; ++i)
+    if (!events[i]) return fail(WM_ERR_ARG, "events[%d] is NULL", i);
+  return layer_step_impl(dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws, ws_bytes, stream,
+                         events);
+}
+
+}  // extern "C"

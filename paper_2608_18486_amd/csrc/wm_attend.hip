@@ -1,0 +1,515 @@
+// Per-layer channel attention (paper Section 3.1 Step 3, Section 3.2).
+//
+// Consumer layer l reads channel c = map[l] of the channel-major cache
+// Kc/Vc[k][B][Hkv][S_cap][d]. A query at position t sees, in the paper's mask,
+// the learned dummy slot of its channel and the cached slots s < t (a token
+// never reads its own channels); in the inclusive mask it sees slots s <= t and
+// no dummy. The dummy enters the online softmax as its initial state
+// (m = q.Kd, l = 1, acc = Vd), which is exactly a prepended KV slot.
+//
+// Full-sequence form (attend_prefill): flash attention on the matrix cores.
+// Each wave owns 64 queries and computes S^T = K Q^T so that a lane holds one
+// query's scores in registers (row max and sum need one cross-half exchange),
+// then O^T = V^T P^T with P^T taken straight from those registers (the MFMA
+// k-slot order is chosen to match; see wm_device.hpp). K blocks are staged
+// row-major and V blocks transposed in LDS.
+//
+// Decode form (attend_decode + combine): split-S over the cache, one
+// workgroup per (split, channel, sequence, KV head) serving every query row
+// that reads that channel and head (all its consumer layers, grouped query
+// heads and new tokens), so each channel slice is streamed from HBM once.
+#include "wm_device.hpp"
+#include "wm_internal.hpp"
+
+namespace wm {
+
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_frag_4_4(const T* p0, const T* p1);
+template <>
+__device__ __forceinline__ bf16x8 ld_frag_4_4<bf16>(const bf16* p0, const bf16* p1) {
+  bf16x4 a = *(const bf16x4*)p0, b = *(const bf16x4*)p1;
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+template <>
+__device__ __forceinline__ f32x8 ld_frag_4_4<float>(const float* p0, const float* p1) {
+  f32x4 a = *(const f32x4*)p0, b = *(const f32x4*)p1;
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <typename T> struct AttnArgs {
+  const T *Q, *Kc, *Vc, *Kd, *Vd;
+  const int32_t* ctx_len;
+  T* O;
+  int B, T_new, L, Hq, Hkv, S_cap, mask_paper, n_qtiles;
+  float scale_log2;  // log2(e) / sqrt(d)
+  LayerTable chan;
+};
+
+template <typename T, int DH> struct PrefillCfg {
+  static constexpr int BQ = 256;   // queries per workgroup (4 waves x 64)
+  static constexpr int BKV = 64;   // keys per block
+  static constexpr int PAD = sizeof(T) == 2 ? 8 : 4;
+  static constexpr int LDK = DH + PAD;   // Ks: [BKV][LDK]
+  static constexpr int LDV = BKV + PAD;  // Vt: [DH][LDV]
+  static constexpr int NKS = DH / 16;    // k16 steps of Q K^T
+  static constexpr int NDT = DH / 32;    // 32-row tiles of O^T
+};
+
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void attend_prefill_kernel(AttnArgs<T> a) {
+  using C = PrefillCfg<T, DH>;
+  __shared__ __align__(16) T Ks[C::BKV * C::LDK];
+  __shared__ __align__(16) T Vt[DH * C::LDV];
+
+  const int qtile = a.n_qtiles - 1 - (int)blockIdx.x;  // longest causal rows first
+  int y = blockIdx.y;
+  const int hq = y % a.Hq;
+  y /= a.Hq;
+  const int b = y % a.B, l = y / a.B;
+  const int c = a.chan.v[l];
+  const int kvh = hq / (a.Hq / a.Hkv);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, r = lane & 31;
+  const int ctx = a.ctx_len ? a.ctx_len[b] : 0;
+  const int incl = a.mask_paper ? 0 : 1;
+  const int q0 = qtile * C::BQ, qw0 = q0 + 64 * w;
+
+  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
+  const T* Kb = a.Kc + cbase;
+  const T* Vb = a.Vc + cbase;
+
+  frag_t<T> qf[2][C::NKS];
+  const T* Qb = a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * DH;
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    int qi = qw0 + 32 * qt + r;
+#pragma unroll
+    for (int ks = 0; ks < C::NKS; ++ks)
+      qf[qt][ks] = qi < a.T_new ? ld_frag<T>(Qb + (long)qi * DH + 16 * ks + 8 * h) : zero_frag<T>();
+  }
+
+  float m[2], lsum[2];
+  f32x16 o[C::NDT][2];
+  if (a.mask_paper) {
+    const T* kd = a.Kd + ((long)c * a.Hkv + kvh) * DH;
+    const T* vd = a.Vd + ((long)c * a.Hkv + kvh) * DH;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float part = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < C::NKS; ++ks)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) part += to_f32(qf[qt][ks][i]) * to_f32(kd[16 * ks + 8 * h + i]);
+      m[qt] = part + __shfl_xor(part, 32, 64);
+      lsum[qt] = h == 0 ? 1.f : 0.f;  // the two half-waves keep partial row sums
+#pragma unroll
+      for (int dt = 0; dt < C::NDT; ++dt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) o[dt][qt][q] = to_f32(vd[32 * dt + 8 * (q >> 2) + 4 * h + (q & 3)]);
+    }
+  } else {
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      m[qt] = kNegBig;
+      lsum[qt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] = zero16();
+    }
+  }
+
+  const int qlast = min(q0 + C::BQ, a.T_new) - 1;
+  const int kend = min(ctx + qlast + incl, a.S_cap);   // slots the workgroup may see
+  const int wq_last = min(qw0 + 63, a.T_new - 1);
+  const int wkend = wq_last >= qw0 ? ctx + wq_last + incl : 0;  // slots this wave may see
+  const int wfree = ctx + qw0 + incl;                  // slots < wfree are visible to all its rows
+
+  for (int k0 = 0; k0 < kend; k0 += C::BKV) {
+    __syncthreads();
+    for (int f = tid; f < C::BKV * DH / 8; f += 256) {
+      int key = f / (DH / 8), dc = (f % (DH / 8)) * 8;
+      int s = k0 + key;
+      frag_t<T> kv, vv;
+      if (s < kend) {
+        kv = ld_frag<T>(Kb + (long)s * DH + dc);
+        vv = ld_frag<T>(Vb + (long)s * DH + dc);
+      } else {
+        kv = zero_frag<T>();
+        vv = zero_frag<T>();
+      }
+      st_frag<T>(Ks + key * C::LDK + dc, kv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) Vt[(dc + i) * C::LDV + key] = vv[i];
+    }
+    __syncthreads();
+    if (k0 >= wkend) continue;
+
+    f32x16 st[2][2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      st[kt][0] = zero16();
+      st[kt][1] = zero16();
+#pragma unroll
+      for (int ks = 0; ks < C::NKS; ++ks) {
+        frag_t<T> kf = ld_frag<T>(Ks + (32 * kt + r) * C::LDK + 16 * ks + 8 * h);
+        st[kt][0] = mma32(st[kt][0], kf, qf[0][ks]);
+        st[kt][1] = mma32(st[kt][1], kf, qf[1][ks]);
+      }
+    }
+
+    const bool need_mask = k0 + C::BKV > wfree;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      const int t = ctx + qw0 + 32 * qt + r;
+      float mx = m[qt];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          float v = st[kt][qt][q];
+          if (need_mask) {
+            int s = k0 + 32 * kt + 8 * (q >> 2) + 4 * h + (q & 3);
+            if (s >= t + incl) v = kNegBig;
+          }
+          st[kt][qt][q] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float alpha = fast_exp2((m[qt] - mx) * a.scale_log2);
+      m[qt] = mx;
+      float ps = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          float v = st[kt][qt][q];
+          float p = v > 0.5f * kNegBig ? fast_exp2((v - mx) * a.scale_log2) : 0.f;
+          st[kt][qt][q] = p;
+          ps += p;
+        }
+      lsum[qt] = lsum[qt] * alpha + ps;
+#pragma unroll
+      for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] *= alpha;
+    }
+
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        frag_t<T> pf[2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) pf[qt][i] = from_f32<T>(st[kt][qt][8 * hf + i]);
+        const int kc = 32 * kt + 16 * hf + 4 * h;
+#pragma unroll
+        for (int dt = 0; dt < C::NDT; ++dt) {
+          const T* vrow = Vt + (32 * dt + r) * C::LDV;
+          frag_t<T> vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
+          o[dt][0] = mma32(o[dt][0], vf, pf[0]);
+          o[dt][1] = mma32(o[dt][1], vf, pf[1]);
+        }
+      }
+  }
+
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const int qi = qw0 + 32 * qt + r;
+    const float lt = lsum[qt] + __shfl_xor(lsum[qt], 32, 64);
+    if (qi >= a.T_new) continue;
+    const float inv = 1.0f / lt;
+    T* dst = a.O + ((((long)l * a.B + b) * a.T_new + qi) * a.Hq + hq) * DH;
+#pragma unroll
+    for (int dt = 0; dt < C::NDT; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = o[dt][qt][4 * g + i] * inv;
+        store4(dst + 32 * dt + 8 * g + 4 * h, v);
+      }
+  }
+}
+
+template <typename T>
+void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q, const T* Kc,
+                           const T* Vc, const T* Kd, const T* Vd, const int32_t* ctx_len, T* O,
+                           hipStream_t s) {
+  if (sh.N() <= 0) return;
+  AttnArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
+                sh.mask_paper, (sh.T_new + 255) / 256,
+                kLog2e / sqrtf((float)sh.d), chan_map};
+  dim3 grid(a.n_qtiles, sh.Hq * sh.B * sh.L);
+  if (sh.d == 64)
+    hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((attend_prefill_kernel<T, 32>), grid, dim3(256), 0, s, a);
+}
+
+// ------------------------------------------------------------------ decode
+constexpr int kSplitLen = 512;  // cache slots per split workgroup
+
+int decode_splits(const Shape& sh) {
+  long kend = (long)sh.ctx_max + sh.T_new;  // upper bound on visible slots
+  int n = (int)((kend + kSplitLen - 1) / kSplitLen);
+  return n < 1 ? 1 : n;
+}
+
+size_t decode_partials_bytes(const Shape& sh) {
+  size_t rows = (size_t)sh.L * sh.B * sh.Hq * sh.T_new;
+  return rows * decode_splits(sh) * (sh.d + 2) * sizeof(float);
+}
+
+template <typename T> struct DecodeArgs {
+  const T *Q, *Kc, *Vc, *Kd, *Vd;
+  const int32_t* ctx_len;
+  float* part;  // [L][B][Hq][T_new][nsplit][d + 2]: unnormalised o, m, l
+  T* O;
+  int B, T_new, L, Hq, Hkv, S_cap, mask_paper, nsplit;
+  float scale_log2;
+  LayerTable chan;
+  ChannelGroups cg;
+};
+
+// Merge online-softmax state (m2, l2, o2) into (m, l, o).
+__device__ __forceinline__ void merge_state(float& m, float& l, float* o, float m2, float l2,
+                                            const float* o2, int n, float c) {
+  float M = fmaxf(m, m2);
+  float a1 = fast_exp2((m - M) * c), a2 = fast_exp2((m2 - M) * c);
+  l = l * a1 + l2 * a2;
+  for (int i = 0; i < n; ++i) o[i] = o[i] * a1 + o2[i] * a2;
+  m = M;
+}
+
+template <typename T, int DH, int NG>
+__global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
+  constexpr int LPS = DH / 8;    // lanes per cache slot (8 elements each)
+  constexpr int SPW = 64 / LPS;  // slots per wave per sweep
+  constexpr int U = 4;           // slots in flight per lane
+  __shared__ float red[4][NG][DH + 2];
+
+  const int split = blockIdx.x;
+  int y = blockIdx.y;
+  const int kvh = y % a.Hkv;
+  y /= a.Hkv;
+  const int b = y % a.B, c = y / a.B;
+  const int off = a.cg.offsets[c], nmem = a.cg.offsets[c + 1] - off;
+  if (nmem == 0) return;
+  const int grp = a.Hq / a.Hkv;
+  const int G = nmem * grp * a.T_new;
+  const int ctx = a.ctx_len ? a.ctx_len[b] : 0;
+  const int incl = a.mask_paper ? 0 : 1;
+  const int kend = min(ctx + a.T_new - 1 + incl, a.S_cap);
+  const int s0 = split * kSplitLen, s1 = min(s0 + kSplitLen, kend);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int sg = lane / LPS, c8 = lane % LPS;
+  const float cl2 = a.scale_log2;
+
+  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
+  const T* Kb = a.Kc + cbase;
+  const T* Vb = a.Vc + cbase;
+
+  for (int g0 = 0; g0 < G; g0 += NG) {
+    const int ng = min(NG, G - g0);
+    float q[NG][8], m[NG], ls[NG], o[NG][8];
+    int vis[NG];
+    long rowid[NG];
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {
+      m[gi] = kNegBig;
+      ls[gi] = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[gi][i] = 0.f;
+      if (gi < ng) {
+        int g = g0 + gi;
+        int i = g % a.T_new, gq = (g / a.T_new) % grp, mi = g / (a.T_new * grp);
+        int l = a.cg.members[off + mi], hq = kvh * grp + gq;
+        rowid[gi] = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + i;
+        load8(a.Q + rowid[gi] * DH + 8 * c8, q[gi]);
+        vis[gi] = ctx + i + incl;
+      } else {
+        rowid[gi] = 0;
+        vis[gi] = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) q[gi][i] = 0.f;
+      }
+    }
+
+    for (int sb = s0 + w * SPW * U; sb < s1; sb += 4 * SPW * U) {
+      float kv[U][8], vv[U][8];
+      int sl[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        int s = sb + u * SPW + sg;
+        sl[u] = s;
+        if (s < s1) {
+          load8(Kb + (long)s * DH + 8 * c8, kv[u]);
+          load8(Vb + (long)s * DH + 8 * c8, vv[u]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) kv[u][i] = vv[u][i] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int gi = 0; gi < NG; ++gi) {
+          float p = 0.f;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) p += q[gi][i] * kv[u][i];
+#pragma unroll
+          for (int x = 1; x < LPS; x <<= 1) p += __shfl_xor(p, x, 64);
+          const bool ok = sl[u] < s1 && sl[u] < vis[gi];
+          if (ok) {
+            float M = fmaxf(m[gi], p);
+            float al = fast_exp2((m[gi] - M) * cl2), pe = fast_exp2((p - M) * cl2);
+            ls[gi] = ls[gi] * al + pe;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) o[gi][i] = o[gi][i] * al + pe * vv[u][i];
+            m[gi] = M;
+          }
+        }
+    }
+    // merge the slot groups of the wave (lanes that share c8)
+#pragma unroll
+    for (int msk = LPS; msk < 64; msk <<= 1)
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+        float m2 = __shfl_xor(m[gi], msk, 64), l2 = __shfl_xor(ls[gi], msk, 64), o2[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o2[i] = __shfl_xor(o[gi][i], msk, 64);
+        merge_state(m[gi], ls[gi], o[gi], m2, l2, o2, 8, cl2);
+      }
+    if (sg == 0) {
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) red[w][gi][8 * c8 + i] = o[gi][i];
+        if (c8 == 0) {
+          red[w][gi][DH] = m[gi];
+          red[w][gi][DH + 1] = ls[gi];
+        }
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < ng * DH; e += 256) {
+      int gi = e / DH, dd = e % DH;
+      float M = kNegBig;
+      for (int ww = 0; ww < 4; ++ww) M = fmaxf(M, red[ww][gi][DH]);
+      float Lsum = 0.f, Osum = 0.f;
+      for (int ww = 0; ww < 4; ++ww) {
+        float sc = fast_exp2((red[ww][gi][DH] - M) * cl2);
+        Lsum += red[ww][gi][DH + 1] * sc;
+        Osum += red[ww][gi][dd] * sc;
+      }
+      // recompute the row id for gi (registers are per-lane; rows are uniform)
+      int g = g0 + gi;
+      int i = g % a.T_new, gq = (g / a.T_new) % grp, mi = g / (a.T_new * grp);
+      int l = a.cg.members[off + mi], hq = kvh * grp + gq;
+      long rid = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + i;
+      float* dst = a.part + (rid * a.nsplit + split) * (DH + 2);
+      dst[dd] = Osum;
+      if (dd == 0) {
+        dst[DH] = M;
+        dst[DH + 1] = Lsum;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// One wave per query row: fold the dummy slot and all split partials.
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void attend_combine_kernel(DecodeArgs<T> a) {
+  constexpr int EPL = DH / 64 > 0 ? DH / 64 : 1;  // elements per lane
+  const long rows = (long)a.L * a.B * a.Hq * a.T_new;
+  const long rid = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (rid >= rows) return;
+  long t = rid;
+  const int i = (int)(t % a.T_new);
+  t /= a.T_new;
+  const int hq = (int)(t % a.Hq);
+  t /= a.Hq;
+  const int b = (int)(t % a.B), l = (int)(t / a.B);
+  const int c = a.chan.v[l], kvh = hq / (a.Hq / a.Hkv);
+  const float cl2 = a.scale_log2;
+
+  float M, Lsum, o[EPL];
+  const bool active = lane * EPL < DH;
+  if (a.mask_paper) {
+    const T* q = a.Q + rid * DH;
+    const T* kd = a.Kd + ((long)c * a.Hkv + kvh) * DH;
+    const T* vd = a.Vd + ((long)c * a.Hkv + kvh) * DH;
+    float part = 0.f;
+    for (int e = 0; e < EPL; ++e)
+      if (active) part += to_f32(q[lane * EPL + e]) * to_f32(kd[lane * EPL + e]);
+    M = wave_sum(part);
+    Lsum = 1.f;
+    for (int e = 0; e < EPL; ++e) o[e] = active ? to_f32(vd[lane * EPL + e]) : 0.f;
+  } else {
+    M = kNegBig;
+    Lsum = 0.f;
+    for (int e = 0; e < EPL; ++e) o[e] = 0.f;
+  }
+  const float* src = a.part + rid * a.nsplit * (DH + 2);
+  for (int sidx = 0; sidx < a.nsplit; ++sidx) {
+    const float* ps = src + (long)sidx * (DH + 2);
+    float o2[EPL];
+    for (int e = 0; e < EPL; ++e) o2[e] = active ? ps[lane * EPL + e] : 0.f;
+    merge_state(M, Lsum, o, ps[DH], ps[DH + 1], o2, EPL, cl2);
+  }
+  if (active) {
+    T* dst = a.O + ((((long)l * a.B + b) * a.T_new + i) * a.Hq + hq) * DH;
+    for (int e = 0; e < EPL; ++e) dst[lane * EPL + e] = from_f32<T>(o[e] / Lsum);
+  }
+}
+
+template <typename T, int DH>
+static void decode_dispatch(const DecodeArgs<T>& a, int G, dim3 grid, hipStream_t s) {
+  if (G <= 1)
+    hipLaunchKernelGGL((attend_decode_kernel<T, DH, 1>), grid, dim3(256), 0, s, a);
+  else if (G <= 2)
+    hipLaunchKernelGGL((attend_decode_kernel<T, DH, 2>), grid, dim3(256), 0, s, a);
+  else if (G <= 4)
+    hipLaunchKernelGGL((attend_decode_kernel<T, DH, 4>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((attend_decode_kernel<T, DH, 8>), grid, dim3(256), 0, s, a);
+  long rows = (long)a.L * a.B * a.Hq * a.T_new;
+  hipLaunchKernelGGL((attend_combine_kernel<T, DH>), dim3((unsigned)((rows + 3) / 4)), dim3(256),
+                     0, s, a);
+}
+
+template <typename T>
+void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const ChannelGroups& cg,
+                          const T* Q, const T* Kc, const T* Vc, const T* Kd, const T* Vd,
+                          const int32_t* ctx_len, float* partials, T* O, hipStream_t s) {
+  if (sh.N() <= 0) return;
+  DecodeArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, partials, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv,
+                  sh.S_cap, sh.mask_paper, decode_splits(sh), kLog2e / sqrtf((float)sh.d),
+                  chan_map, cg};
+  int maxmem = 0;
+  for (int c = 0; c < sh.k; ++c) {
+    int n = cg.offsets[c + 1] - cg.offsets[c];
+    if (n > maxmem) maxmem = n;
+  }
+  int G = maxmem * (sh.Hq / sh.Hkv) * sh.T_new;
+  dim3 grid(a.nsplit, sh.Hkv * sh.B * sh.k);
+  if (sh.d == 64)
+    decode_dispatch<T, 64>(a, G, grid, s);
+  else
+    decode_dispatch<T, 32>(a, G, grid, s);
+}
+
+#define WM_INST(T)                                                                              \
+  template void launch_attend_prefill<T>(const Shape&, const LayerTable&, const T*, const T*,   \
+                                         const T*, const T*, const T*, const int32_t*, T*,      \
+                                         hipStream_t);                                          \
+  template void launch_attend_decode<T>(const Shape&, const LayerTable&, const ChannelGroups&,  \
+                                        const T*, const T*, const T*, const T*, const T*,       \
+                                        const int32_t*, float*, T*, hipStream_t);
+WM_INST(float)
+WM_INST(bf16)
+#undef WM_INST
+
+}  // namespace wm

@@ -1,0 +1,114 @@
+// Device-side building blocks shared by the WhiteMatter kernels (gfx950 only).
+//
+// Matrix-core convention used everywhere: a 32x32 MFMA tile is fed, per
+// "k16 step", with 8 operand elements per lane. Lane l (h = l / 32, r = l % 32)
+// supplies A[row r][k slots 8h .. 8h+7] and B[k slots 8h .. 8h+7][col r]. The
+// hardware sums over all 16 slots, so any assignment of logical k indices to
+// slots is valid as long as A and B use the same one; the kernels rely on this
+// to feed P^T straight from the softmax registers.
+//   bf16 : one v_mfma_f32_32x32x16_bf16 per k16 step
+//   fp32 : eight v_mfma_f32_32x32x2f32 (slot pair {i, 8+i} per instruction)
+// Result layout (all 32x32 MFMAs): lane l holds column l % 32 and, in register
+// q = 0..15, row 8*(q/4) + 4*(l/32) + (q%4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wm {
+
+typedef __bf16 bf16;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(8))) float f32x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegBig = -1.0e30f;
+
+template <typename T> struct Frag;                 // 8 operand elements of one lane
+template <> struct Frag<bf16> { typedef bf16x8 type; };
+template <> struct Frag<float> { typedef f32x8 type; };
+template <typename T> using frag_t = typename Frag<T>::type;
+
+__device__ __forceinline__ f32x16 mma32(f32x16 acc, const bf16x8& a, const bf16x8& b) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mma32(f32x16 acc, const f32x8& a, const f32x8& b) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[i], acc, 0, 0, 0);
+  return acc;
+}
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+// 8 consecutive elements <-> 8 floats (16 B for bf16, 32 B for fp32).
+__device__ __forceinline__ void load8(const bf16* p, float* out) {
+  bf16x8 v = *(const bf16x8*)p;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) out[i] = (float)v[i];
+}
+__device__ __forceinline__ void load8(const float* p, float* out) {
+  f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { out[i] = a[i]; out[4 + i] = b[i]; }
+}
+__device__ __forceinline__ void store8(bf16* p, const float* in) {
+  bf16x8 v;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (bf16)in[i];
+  *(bf16x8*)p = v;
+}
+__device__ __forceinline__ void store8(float* p, const float* in) {
+  f32x4 a, b;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { a[i] = in[i]; b[i] = in[4 + i]; }
+  *(f32x4*)p = a;
+  *(f32x4*)(p + 4) = b;
+}
+__device__ __forceinline__ void store4(bf16* p, const float* in) {
+  bf16x4 v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (bf16)in[i];
+  *(bf16x4*)p = v;
+}
+__device__ __forceinline__ void store4(float* p, const float* in) {
+  f32x4 v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = in[i];
+  *(f32x4*)p = v;
+}
+
+// Raw 8-element copies (no conversion), used to move operand tiles.
+template <typename T> __device__ __forceinline__ frag_t<T> ld_frag(const T* p) {
+  return *(const frag_t<T>*)p;
+}
+template <typename T> __device__ __forceinline__ void st_frag(T* p, const frag_t<T>& v) {
+  *(frag_t<T>*)p = v;
+}
+template <typename T> __device__ __forceinline__ frag_t<T> zero_frag() {
+  frag_t<T> v;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = from_f32<T>(0.f);
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+}  // namespace wm

@@ -1,0 +1,78 @@
+// Internal launch interface between the C-ABI host layer and the kernels.
+// All launches are asynchronous on the given stream; shapes are validated by
+// the caller (wm_api.cpp) before any launch.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace wm {
+
+typedef __bf16 bf16;
+constexpr int kMaxLayers = 64;  // L limit (kernel-argument tables are sized by it)
+constexpr int kMaxHeadDim = 128;
+
+struct Shape {
+  int B, T_new, L, k, D, Hq, Hkv, d, p, Lp, S_cap;
+  int mix_softmax;   // 1: softmax over source layers per channel row
+  int mask_paper;    // 1: dummy slot + strictly earlier slots; 0: slots <= own position
+  float eps, rope_theta;
+  int ctx_max;       // host-side bound on ctx_len[b] (sizes the attention grid)
+  __host__ __device__ int N() const { return B * T_new; }
+};
+
+struct LayerTable {  // small per-call integer tables, passed by value
+  int v[kMaxLayers];
+};
+
+// -- pool side (Steps 1 and 2) ------------------------------------------------
+// rinv[r] = 1 / sqrt(mean(X[r][:]^2) + eps) for rows of length D.
+template <typename T>
+void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStream_t s);
+
+// tab[n][m] = (cos, sin)(pos(n) * theta^(-2m/d)), pos(n) = ctx_len[b] + i, computed in fp64.
+void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipStream_t s);
+
+// logits[br][n][o] = sum over stacked layers of W_alpha[br][o] . normed state + b_alpha[br][o]
+template <typename T>
+void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
+                   const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits,
+                   hipStream_t s);
+
+// alpha (in: logits [2][N][k*L], out: mixing weights) -> mixed[2][k][N][D], rinv_mid[2][k][N]
+template <typename T>
+void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
+                T* mixed, float* rinv_mid, hipStream_t s);
+
+// mixed -> K (mid norm, W^K_j, key norm, RoPE) and V (mid norm, W^V_j) at slot ctx_len[b]+i
+template <typename T>
+void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, const T* g_mid,
+                       const T* Wk, const T* Wv, const T* g_knorm, const float* rope_tab,
+                       const int32_t* ctx_len, T* Kc, T* Vc, hipStream_t s);
+
+// H -> Q[L][B][Hq][T_new][d] (input norm, W^Q_l, q norm, RoPE)
+template <typename T>
+void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g_in,
+                      const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q,
+                      hipStream_t s);
+
+// -- consumer side (Step 3) ---------------------------------------------------
+struct ChannelGroups {       // CSR inverse of the consumer -> channel map
+  int offsets[kMaxLayers + 1];
+  int members[kMaxLayers];
+};
+
+template <typename T>
+void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q,
+                           const T* Kc, const T* Vc, const T* Kd, const T* Vd,
+                           const int32_t* ctx_len, T* O, hipStream_t s);
+
+// Split-S decode for small T_new; partials live in the workspace.
+size_t decode_partials_bytes(const Shape& sh);
+int decode_splits(const Shape& sh);
+template <typename T>
+void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const ChannelGroups& cg,
+                          const T* Q, const T* Kc, const T* Vc, const T* Kd, const T* Vd,
+                          const int32_t* ctx_len, float* partials, T* O, hipStream_t s);
+
+}  // namespace wm

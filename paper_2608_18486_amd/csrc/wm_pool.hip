@@ -1,0 +1,390 @@
+// Cross-layer KV pool kernels (paper Section 3.1, Steps 1 and 2).
+//
+//   row_rms      1 / RMS of every (token, layer) state (the pre-mix and the
+//                consumer input norms share it; only the gains differ)
+//   rope_table   (cos, sin) of pos * theta^(-2m/d) per new token, in fp64
+//   router       alpha logits = W_alpha xi + b_alpha on the matrix cores; xi is
+//                the stack of normed states of layers {L-1-p*m}
+//   mix          (optional softmax over source layers) and the per-token mix
+//                h~_j = sum_l alpha[j][l] h^_l, plus 1 / RMS of each channel
+//   kv_project   per-channel W^K_j / W^V_j on the matrix cores, with the mid
+//                RMSNorm folded into the operand and key norm + RoPE + the
+//                channel-major cache store in the epilogue
+//   q_project    the consumer's query: input norm, W^Q_l, q norm, RoPE
+#include "wm_gemm.hpp"
+#include "wm_internal.hpp"
+
+namespace wm {
+
+// ----------------------------------------------------------------- row rms
+template <typename T>
+__global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int D, float eps,
+                                                      float* rinv) {
+  long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const T* x = X + row * D;
+  float ss = 0.f;
+  for (int e = lane * 8; e < D; e += 512) {
+    float v[8];
+    load8(x + e, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += v[i] * v[i];
+  }
+  ss = wave_sum(ss);
+  if (lane == 0) rinv[row] = 1.0f / sqrtf(ss / (float)D + eps);
+}
+
+template <typename T>
+void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStream_t s) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(row_rms_kernel<T>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, X,
+                     rows, D, eps, rinv);
+}
+
+// -------------------------------------------------------------- rope table
+__global__ __launch_bounds__(256) void rope_table_kernel(const int32_t* ctx_len, int B,
+                                                         int T_new, int d, double theta,
+                                                         float* tab) {
+  int half = d / 2;
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)B * T_new * half) return;
+  int m = (int)(idx % half);
+  long n = idx / half;
+  int b = (int)(n / T_new), i = (int)(n % T_new);
+  double pos = (double)((ctx_len ? ctx_len[b] : 0) + i);
+  double freq = pow(theta, -2.0 * (double)m / (double)d);
+  double sn, cs;
+  sincos(pos * freq, &sn, &cs);
+  tab[2 * idx] = (float)cs;
+  tab[2 * idx + 1] = (float)sn;
+}
+
+void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipStream_t s) {
+  long total = (long)sh.N() * (sh.d / 2);
+  if (total <= 0) return;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                     ctx_len, sh.B, sh.T_new, sh.d, (double)sh.rope_theta, tab);
+}
+
+// -------------------------------------------------------- GEMM functors
+// Weight rows: W + g * group_stride + o * K (nullptr past Nout).
+template <typename T> struct WeightRows {
+  const T* W;
+  long group_stride;
+  int Nout, K;
+  __device__ const T* operator()(int g, int o) const {
+    return o < Nout ? W + (long)g * group_stride + (long)o * K : nullptr;
+  }
+};
+
+// K/V projection weights: group g = branch * k + channel.
+template <typename T> struct KVWeightRows {
+  const T *Wk, *Wv;
+  int k, Nout, K;
+  __device__ const T* operator()(int g, int o) const {
+    if (o >= Nout) return nullptr;
+    int br = g / k, j = g - br * k;
+    return (br ? Wv : Wk) + ((long)j * Nout + o) * K;
+  }
+};
+
+// Router operand: the stacked normed states xi (gain and 1/RMS applied, one rounding).
+template <typename T> struct RouterA {
+  const T* H;
+  const float* rinv;
+  const T* g_pre;
+  LayerTable sel;
+  int L, D;
+  __device__ void operator()(int br, int n, int k, float* out) const {
+    int m = k / D, e = k - m * D, layer = sel.v[m];
+    const T* x = H + ((long)n * L + layer) * D + e;
+    const T* g = g_pre + ((long)br * L + layer) * D + e;
+    float rs = rinv[(long)n * L + layer];
+#pragma unroll
+    for (int hv = 0; hv < 2; ++hv) {
+      float xv[8], gv[8];
+      load8(x + 8 * hv, xv);
+      load8(g + 8 * hv, gv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) out[8 * hv + i] = xv[i] * gv[i] * rs;
+    }
+  }
+};
+
+// Generic normed-row operand: X[g][row][k] * gain[g][k] * rs[g][row].
+template <typename T> struct NormedRowsA {
+  const T* X;
+  long x_gstride, x_rstride;
+  const T* gain;
+  long g_gstride;
+  const float* rs;
+  long rs_gstride, rs_rstride;
+  __device__ void operator()(int g, int row, int k, float* out) const {
+    const T* x = X + (long)g * x_gstride + (long)row * x_rstride + k;
+    const T* gg = gain + (long)g * g_gstride + k;
+    float s = rs[(long)g * rs_gstride + (long)row * rs_rstride];
+#pragma unroll
+    for (int hv = 0; hv < 2; ++hv) {
+      float xv[8], gv[8];
+      load8(x + 8 * hv, xv);
+      load8(gg + 8 * hv, gv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) out[8 * hv + i] = xv[i] * gv[i] * s;
+    }
+  }
+};
+
+template <typename T> struct RouterEpi {
+  float* logits;
+  const T* bias;
+  int M, Nout;
+  __device__ void operator()(int br, int m0, int n0, const float* C, int ldc, int tid) const {
+    int col = tid & 127, o = n0 + col;
+    if (o >= Nout) return;
+    float b = to_f32(bias[(long)br * Nout + o]);
+    for (int row = tid >> 7; row < 128; row += 2) {
+      int n = m0 + row;
+      if (n >= M) break;
+      logits[((long)br * M + n) * Nout + o] = C[row * ldc + col] + b;
+    }
+  }
+};
+
+// One head row: RMS over d, gain, RoPE with the per-token (cos, sin) table, store.
+template <typename T>
+__device__ __forceinline__ void head_norm_rope_store(const float* c, T* dst, const T* gain,
+                                                     const float* tab, int d, float eps) {
+  float ss = 0.f;
+  for (int e = 0; e < d; e += 4) {
+    f32x4 v = *(const f32x4*)(c + e);
+    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+  }
+  float rs = 1.0f / sqrtf(ss / (float)d + eps);
+  int half = d / 2;
+  for (int m = 0; m < half; m += 4) {
+    f32x4 x1 = *(const f32x4*)(c + m), x2 = *(const f32x4*)(c + m + half);
+    float y1[4], y2[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float a = x1[i] * rs * to_f32(gain[m + i]);
+      float b = x2[i] * rs * to_f32(gain[m + half + i]);
+      float cs = tab[2 * (m + i)], sn = tab[2 * (m + i) + 1];
+      y1[i] = a * cs - b * sn;
+      y2[i] = b * cs + a * sn;
+    }
+    store4(dst + m, y1);
+    store4(dst + m + half, y2);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void head_store(const float* c, T* dst, int d) {
+  for (int e = 0; e < d; e += 4) {
+    f32x4 v = *(const f32x4*)(c + e);
+    float y[4] = {v[0], v[1], v[2], v[3]};
+    store4(dst + e, y);
+  }
+}
+
+template <typename T> struct KVEpi {
+  T *Kc, *Vc;
+  const T* g_knorm;
+  const float* tab;
+  const int32_t* ctx_len;
+  int M, Nout, d, T_new, B, Hkv, S_cap, k;
+  float eps;
+  __device__ void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const {
+    int br = g / k, j = g - br * k;
+    int hpt = 128 / d;
+    for (int it = tid; it < 128 * hpt; it += 256) {
+      int row = it & 127, hh = it >> 7;
+      int n = m0 + row, col0 = n0 + hh * d;
+      if (n >= M || col0 >= Nout) continue;
+      int b = n / T_new, i = n - b * T_new;
+      long slot = (long)(ctx_len ? ctx_len[b] : 0) + i;
+      if (slot < 0 || slot >= S_cap) continue;
+      int head = col0 / d;
+      long off = ((((long)j * B + b) * Hkv + head) * S_cap + slot) * d;
+      const float* c = C + row * ldc + hh * d;
+      if (br == 0)
+        head_norm_rope_store(c, Kc + off, g_knorm + (long)j * d, tab + (long)n * d, d, eps);
+      else
+        head_store(c, Vc + off, d);
+    }
+  }
+};
+
+template <typename T> struct QEpi {
+  T* Q;
+  const T* g_qnorm;
+  const float* tab;
+  int M, Nout, d, T_new, B, Hq;
+  float eps;
+  __device__ void operator()(int l, int m0, int n0, const float* C, int ldc, int tid) const {
+    int hpt = 128 / d;
+    for (int it = tid; it < 128 * hpt; it += 256) {
+      int row = it & 127, hh = it >> 7;
+      int n = m0 + row, col0 = n0 + hh * d;
+      if (n >= M || col0 >= Nout) continue;
+      int b = n / T_new, i = n - b * T_new, head = col0 / d;
+      long off = ((((long)l * B + b) * Hq + head) * T_new + i) * d;
+      head_norm_rope_store(C + row * ldc + hh * d, Q + off, g_qnorm + (long)l * d,
+                           tab + (long)n * d, d, eps);
+    }
+  }
+};
+
+// ------------------------------------------------------------------ router
+template <typename T>
+void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
+                   const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits,
+                   hipStream_t s) {
+  int M = sh.N(), Nout = sh.k * sh.L, K = sh.Lp * sh.D;
+  if (M <= 0) return;
+  RouterA<T> a{H, rinv, g_pre, sel, sh.L, sh.D};
+  WeightRows<T> w{W_alpha, (long)Nout * K, Nout, K};
+  RouterEpi<T> e{logits, b_alpha, M, Nout};
+  dim3 grid((Nout + 127) / 128, (M + 127) / 128, 2);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, RouterA<T>, WeightRows<T>, RouterEpi<T>>), grid,
+                     dim3(256), 0, s, M, Nout, K, a, w, e);
+}
+
+// --------------------------------------------------------------------- mix
+// One block per token. LDS holds the token's L states and the 2 x k x L
+// coefficients alpha[j][l] / RMS(h_l); each thread owns 8 consecutive columns.
+template <typename T>
+__global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* H, const float* rinv,
+                                                  const T* g_pre, float* alpha, T* mixed,
+                                                  float* rinv_mid) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int L = sh.L, k = sh.k, D = sh.D, N = sh.N();
+  const long n = blockIdx.x;
+  T* hs = (T*)smem;
+  float* coef = (float*)(smem + (size_t)L * D * sizeof(T));
+  float* part = coef + 2 * k * L;  // [2 waves][2k]
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+
+  const T* hsrc = H + n * L * D;
+  for (int e = tid * 8; e < L * D; e += 128 * 8) st_frag<T>(hs + e, ld_frag<T>(hsrc + e));
+
+  if (tid < 2 * k) {
+    int br = tid / k, j = tid - br * k;
+    float* row = alpha + ((long)br * N + n) * k * L + (long)j * L;
+    if (sh.mix_softmax) {
+      float mx = row[0];
+      for (int l = 1; l < L; ++l) mx = fmaxf(mx, row[l]);
+      float z = 0.f;
+      for (int l = 0; l < L; ++l) z += expf(row[l] - mx);
+      float iz = 1.0f / z;
+      for (int l = 0; l < L; ++l) row[l] = expf(row[l] - mx) * iz;
+    }
+    for (int l = 0; l < L; ++l) coef[(br * k + j) * L + l] = row[l] * rinv[n * L + l];
+  }
+  __syncthreads();
+
+  constexpr int JC = 4;
+  const int ncg = D / 8;
+  for (int br = 0; br < 2; ++br) {
+    for (int j0 = 0; j0 < k; j0 += JC) {
+      float ss[JC] = {0.f, 0.f, 0.f, 0.f};
+      for (int cg = tid; cg < ncg; cg += 128) {
+        float acc[JC][8];
+#pragma unroll
+        for (int jj = 0; jj < JC; ++jj)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[jj][i] = 0.f;
+        for (int l = 0; l < L; ++l) {
+          float xv[8], gv[8];
+          load8(hs + l * D + cg * 8, xv);
+          load8(g_pre + ((long)br * L + l) * D + cg * 8, gv);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) xv[i] *= gv[i];
+#pragma unroll
+          for (int jj = 0; jj < JC; ++jj) {
+            if (j0 + jj < k) {
+              float c = coef[(br * k + j0 + jj) * L + l];
+#pragma unroll
+              for (int i = 0; i < 8; ++i) acc[jj][i] += c * xv[i];
+            }
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < JC; ++jj) {
+          if (j0 + jj < k) {
+            store8(mixed + (((long)br * k + j0 + jj) * N + n) * D + cg * 8, acc[jj]);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ss[jj] += acc[jj][i] * acc[jj][i];
+          }
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < JC; ++jj) {
+        float v = wave_sum(ss[jj]);
+        if (lane == 0 && j0 + jj < k) part[wv * 2 * k + br * k + j0 + jj] = v;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < 2 * k) {
+    float v = part[tid] + part[2 * k + tid];
+    int br = tid / k, j = tid - br * k;
+    rinv_mid[((long)br * k + j) * N + n] = 1.0f / sqrtf(v / (float)D + sh.eps);
+  }
+}
+
+template <typename T>
+void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
+                T* mixed, float* rinv_mid, hipStream_t s) {
+  if (sh.N() <= 0) return;
+  size_t smem = (size_t)sh.L * sh.D * sizeof(T) + sizeof(float) * (2 * sh.k * sh.L + 4 * sh.k);
+  hipLaunchKernelGGL(mix_kernel<T>, dim3(sh.N()), dim3(128), smem, s, sh, H, rinv, g_pre, alpha,
+                     mixed, rinv_mid);
+}
+
+// ------------------------------------------------------------- projections
+template <typename T>
+void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, const T* g_mid,
+                       const T* Wk, const T* Wv, const T* g_knorm, const float* rope_tab,
+                       const int32_t* ctx_len, T* Kc, T* Vc, hipStream_t s) {
+  int M = sh.N(), Nout = sh.Hkv * sh.d, K = sh.D;
+  if (M <= 0) return;
+  NormedRowsA<T> a{mixed, (long)M * K, K, g_mid, K, rinv_mid, M, 1};
+  KVWeightRows<T> w{Wk, Wv, sh.k, Nout, K};
+  KVEpi<T> e{Kc, Vc, g_knorm, rope_tab, ctx_len, M, Nout, sh.d, sh.T_new, sh.B, sh.Hkv,
+             sh.S_cap, sh.k, sh.eps};
+  dim3 grid((Nout + 127) / 128, (M + 127) / 128, 2 * sh.k);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, NormedRowsA<T>, KVWeightRows<T>, KVEpi<T>>), grid,
+                     dim3(256), 0, s, M, Nout, K, a, w, e);
+}
+
+template <typename T>
+void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g_in,
+                      const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q,
+                      hipStream_t s) {
+  int M = sh.N(), Nout = sh.Hq * sh.d, K = sh.D;
+  if (M <= 0) return;
+  NormedRowsA<T> a{H, K, (long)sh.L * K, g_in, K, rinv, 1, sh.L};
+  WeightRows<T> w{Wq, (long)Nout * K, Nout, K};
+  QEpi<T> e{Q, g_qnorm, rope_tab, M, Nout, sh.d, sh.T_new, sh.B, sh.Hq, sh.eps};
+  dim3 grid((Nout + 127) / 128, (M + 127) / 128, sh.L);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, NormedRowsA<T>, WeightRows<T>, QEpi<T>>), grid,
+                     dim3(256), 0, s, M, Nout, K, a, w, e);
+}
+
+#define WM_INST(T)                                                                             \
+  template void launch_row_rms<T>(const T*, long, int, float, float*, hipStream_t);            \
+  template void launch_router<T>(const Shape&, const LayerTable&, const T*, const float*,      \
+                                 const T*, const T*, const T*, float*, hipStream_t);           \
+  template void launch_mix<T>(const Shape&, const T*, const float*, const T*, float*, T*,      \
+                              float*, hipStream_t);                                            \
+  template void launch_kv_project<T>(const Shape&, const T*, const float*, const T*, const T*, \
+                                     const T*, const T*, const float*, const int32_t*, T*, T*, \
+                                     hipStream_t);                                             \
+  template void launch_q_project<T>(const Shape&, const T*, const float*, const T*, const T*,  \
+                                    const T*, const float*, T*, hipStream_t);
+WM_INST(float)
+WM_INST(bf16)
+#undef WM_INST
+
+}  // namespace wm

@@ -1,0 +1,179 @@
+"""Host-side checks of the C ABI (no GPU needed): every declared symbol is exported,
+validation returns the documented error codes before anything is launched, and the
+host helpers agree bit-for-bit with the oracle."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "whitematter.h")
+
+
+@pytest.fixture(scope="module")
+def wm():
+    import paper_2608_18486_amd as wm
+    from paper_2608_18486_amd import build
+    if not os.path.exists(wm.LIB_PATH):
+        build.build()
+    wm.lib()
+    return wm
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char \*)\s*\*?(wm_\w+)\s*\(", text,
+                                 flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol(wm):
+    names = _declared()
+    assert len(names) >= 12, names
+    for n in names:
+        assert hasattr(wm.lib(), n), n
+    assert wm.version().startswith("whitematter-gfx950")
+
+
+def _dims(wm, **kw):
+    base = dict(B=2, T_new=16, L=4, k=2, D=64, Hq=4, Hkv=2, d=32, p=1, S_cap=64, ctx_max=8,
+                dtype=wm.BF16)
+    base.update(kw)
+    return wm.make_dims(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(L=0), "ERR_SHAPE"), (dict(L=65, k=2), "ERR_SHAPE"), (dict(k=5), "ERR_SHAPE"),
+    (dict(k=0), "ERR_SHAPE"), (dict(D=48), "ERR_SHAPE"), (dict(D=0), "ERR_SHAPE"),
+    (dict(Hq=3), "ERR_SHAPE"), (dict(Hkv=0), "ERR_SHAPE"), (dict(d=48), "ERR_SHAPE"),
+    (dict(d=128), "ERR_SHAPE"), (dict(p=0), "ERR_SHAPE"), (dict(p=5), "ERR_SHAPE"),
+    (dict(dtype=7), "ERR_DTYPE"), (dict(mix_mode=2), "ERR_DTYPE"), (dict(mask_mode=-1), "ERR_DTYPE"),
+    (dict(B=-1), "ERR_ARG"), (dict(T_new=-3), "ERR_ARG"), (dict(eps=0.0), "ERR_ARG"),
+    (dict(rope_theta=-1.0), "ERR_ARG"), (dict(ctx_max=-1), "ERR_ARG"),
+    (dict(ctx_max=60, T_new=5), "ERR_CAPACITY"), (dict(S_cap=0), "ERR_SHAPE"),
+    (dict(L=64, k=8, D=1024), "ERR_SHAPE"),
+])
+def test_validation_error_codes(wm, kw, code):
+    d = _dims(wm, **kw)
+    chan_map = [l % 2 for l in range(max(d.L, 1))]
+    assert wm.validate(d, wm.OP_LAYER_STEP, chan_map) == getattr(wm, code)
+    assert wm.workspace_size(_dims(wm, **kw), wm.OP_LAYER_STEP) == 0
+
+
+def test_capacity_only_matters_for_cache_ops(wm):
+    d = _dims(wm, ctx_max=60, T_new=5)
+    assert wm.validate(d, wm.OP_ROUTER_MIX) == wm.OK
+    assert wm.validate(d, wm.OP_Q_PROJECT) == wm.OK
+    assert wm.validate(d, wm.OP_KV_PROJECT) == wm.ERR_CAPACITY
+    assert wm.validate(d, wm.OP_CHANNEL_ATTEND, [0, 1, 0, 1]) == wm.ERR_CAPACITY
+
+
+def test_map_validation(wm):
+    d = _dims(wm)
+    assert wm.validate(d, wm.OP_LAYER_STEP, [0, 1, 0, 1]) == wm.OK
+    assert wm.validate(d, wm.OP_LAYER_STEP, [0, 2, 0, 1]) == wm.ERR_MAP
+    assert wm.validate(d, wm.OP_LAYER_STEP, [0, -1, 0, 1]) == wm.ERR_MAP
+    assert "chan_map[1]" in wm.last_error()
+
+
+class _FakeTensor:
+    """Stands in for a device tensor in calls that must fail validation before any launch."""
+
+    def __init__(self, addr):
+        self.addr = addr
+
+    def is_contiguous(self):
+        return True
+
+    def data_ptr(self):
+        return self.addr
+
+    def numel(self):
+        return 1 << 20
+
+
+def _fake_params(wm, addr=0x100000):
+    return {n: _FakeTensor(addr + 0x1000 * i) for i, n in enumerate(wm.PARAM_NAMES)}
+
+
+class _P:
+    def __init__(self, wm, params):
+        self.c = wm.Params(*[params[n].data_ptr() for n in wm.PARAM_NAMES])
+
+
+def _call(wm, fn, dims, *ptrs, ws=0x400000, ws_bytes=1 << 30, params=None):
+    P = _P(wm, params or _fake_params(wm))
+    L = wm.lib()
+    f = getattr(L, fn)
+    return f(ctypes.byref(dims), ctypes.byref(P.c), *ptrs, ws, ws_bytes, None)
+
+
+def test_entry_points_reject_bad_pointers_before_launch(wm):
+    d = _dims(wm)
+    m = (ctypes.c_int32 * 4)(0, 1, 0, 1)
+    good = 0x200000
+    # NULL and misaligned tensors
+    assert _call(wm, "wm_router_mix", d, None, None, good) == wm.ERR_ARG
+    assert _call(wm, "wm_router_mix", d, good + 8, None, good) == wm.ERR_ARG
+    assert _call(wm, "wm_kv_project", d, good, None, None, good) == wm.ERR_ARG
+    assert _call(wm, "wm_q_project", d, good, None, None) == wm.ERR_ARG
+    assert _call(wm, "wm_channel_attend", d, good, m, None, good, good, None) == wm.ERR_ARG
+    assert _call(wm, "wm_layer_step", d, good, None, None, good, good, good) == wm.ERR_ARG
+    # NULL parameter
+    bad = _fake_params(wm)
+    bad["Wq"] = _FakeTensor(0)
+    assert _call(wm, "wm_q_project", d, good, None, good, params=bad) == wm.ERR_ARG
+    assert "Wq" in wm.last_error()
+    # workspace: NULL, misaligned, too small
+    assert _call(wm, "wm_layer_step", d, good, m, None, good, good, good, ws=0) == wm.ERR_WORKSPACE
+    assert _call(wm, "wm_layer_step", d, good, m, None, good, good, good, ws=0x400010) == \
+        wm.ERR_WORKSPACE
+    need = wm.workspace_size(d, wm.OP_LAYER_STEP)
+    assert _call(wm, "wm_layer_step", d, good, m, None, good, good, good, ws_bytes=need - 1) == \
+        wm.ERR_WORKSPACE
+    # map and capacity errors surface through the entry points too
+    m_bad = (ctypes.c_int32 * 4)(0, 3, 0, 1)
+    assert _call(wm, "wm_layer_step", d, good, m_bad, None, good, good, good) == wm.ERR_MAP
+    d_cap = _dims(wm, ctx_max=60)
+    assert _call(wm, "wm_kv_project", d_cap, good, None, good, good) == wm.ERR_CAPACITY
+
+
+def test_empty_inputs_are_a_no_op(wm):
+    for kw in (dict(B=0), dict(T_new=0)):
+        d = _dims(wm, **kw)
+        assert wm.workspace_size(d, wm.OP_LAYER_STEP) == 0
+        m = (ctypes.c_int32 * 4)(0, 1, 0, 1)
+        # no pointers at all: an empty call returns before touching any of them
+        assert _call(wm, "wm_layer_step", d, None, m, None, None, None, None, ws=0, ws_bytes=0) == wm.OK
+
+
+def test_workspace_sizes_grow_with_the_problem(wm):
+    small = wm.workspace_size(_dims(wm, T_new=16), wm.OP_LAYER_STEP)
+    big = wm.workspace_size(_dims(wm, T_new=32, S_cap=128), wm.OP_LAYER_STEP)
+    assert 0 < small < big
+    for op in range(5):
+        assert wm.workspace_size(_dims(wm), op) >= 0
+
+
+def test_channel_groups_match_oracle(wm, oracle_lib):
+    rng = np.random.default_rng(0)
+    for L in (1, 4, 5, 12, 24, 64):
+        for k in sorted({1, 2, max(1, L // 2), L}):
+            maps = [[l % k for l in range(L)], [l * k // L for l in range(L)],
+                    rng.integers(0, k, size=L).tolist()]
+            for m in maps:
+                off, mem = wm.channel_groups(L, k, m)
+                o_off, o_mem = oracle_lib.channel_groups(L, k, m)
+                assert off == o_off.tolist() and mem == o_mem.tolist()
+    with pytest.raises(wm.WMError):
+        wm.channel_groups(4, 2, [0, 1, 2, 0])
+
+
+def test_init_bias_and_default_map_match_oracle(wm, oracle_lib):
+    for L in (1, 2, 4, 5, 12, 16, 24):
+        for k in range(1, L + 1):
+            assert wm.init_bias(L, k) == oracle_lib.init_bias(L, k).tolist()
+            assert wm.default_map(L, k) == [l % k for l in range(L)]
+    with pytest.raises(wm.WMError):
+        wm.init_bias(4, 5)

@@ -1,0 +1,353 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 CPU oracle.
+
+Tolerances (stated in the workloads' terms): fp32 max |gpu - ref| <= 1e-5;
+bf16 max |gpu - ref| / max |ref| <= 2e-2 per output tensor. Integer work (which
+slots are written, the channel each consumer reads) must match exactly: caches
+start as NaN sentinels and the set of slots the kernels wrote must equal the
+oracle's.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32_ABS = 1e-5
+TOL_BF16_REL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def wm():
+    import paper_2608_18486_amd as wm
+    wm.lib()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return wm
+
+
+def _f64(t):
+    return t.detach().to("cpu").double().numpy()
+
+
+def check_close(gpu, ref, dtype, name):
+    g = _f64(gpu) if torch.is_tensor(gpu) else np.asarray(gpu, dtype=np.float64)
+    r = np.asarray(ref, dtype=np.float64)
+    assert g.shape == r.shape, (name, g.shape, r.shape)
+    assert np.isfinite(g).all(), "%s: non-finite GPU output" % name
+    err = np.abs(g - r).max() if g.size else 0.0
+    if dtype == "f32":
+        assert err <= TOL_F32_ABS, "%s: max abs err %.3e > %.0e" % (name, err, TOL_F32_ABS)
+    else:
+        scale = np.abs(r).max() if r.size else 1.0
+        rel = err / max(scale, 1e-30)
+        assert rel <= TOL_BF16_REL, "%s: normwise rel err %.3e > %.0e" % (name, rel, TOL_BF16_REL)
+    return err
+
+
+def _odims(w, **kw):
+    base = dict(B=w.B, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d, p=w.p,
+                S_cap=w.S_cap)
+    base.update(kw)
+    return oracle.Dims(**base)
+
+
+def _gdims(wm, w, **kw):
+    base = dict(B=w.B, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d, p=w.p,
+                S_cap=w.S_cap, ctx_max=w.ctx, dtype=wm.F32 if w.dtype == "f32" else wm.BF16)
+    base.update(kw)
+    return wm.make_dims(**base)
+
+
+def _dev(P):
+    return {k: v.cuda() for k, v in P.items()}
+
+
+def _bias(w):
+    return oracle.init_bias(w.L, w.k)
+
+
+def _written_mask(w, ctx):
+    """[B, S_cap] bool: the slots the step writes for each sequence."""
+    m = np.zeros((w.B, w.S_cap), dtype=bool)
+    for b in range(w.B):
+        m[b, ctx[b]:ctx[b] + w.T_new] = True
+    return m
+
+
+def _check_cache(Kg, Ko, Kin, w, ctx, dtype, name):
+    """Written slots within tolerance, every other slot bit-identical to the input, and
+    the NaN-sentinel write set equal to the oracle's."""
+    kg = _f64(Kg)
+    nan_g, nan_o = np.isnan(kg), np.isnan(Ko)
+    assert (nan_g == nan_o).all(), "%s: written slot set differs from the oracle's" % name
+    mask = _written_mask(w, ctx)[None, :, None, :, None]
+    mask = np.broadcast_to(mask, kg.shape)
+    check_close(kg[mask], Ko[mask], dtype, name + " (written slots)")
+    kin = _f64(Kin)
+    same = ~mask & ~np.isnan(kin)
+    assert (kg[same] == kin[same]).all(), "%s: a slot outside the write set changed" % name
+
+
+# ---------------------------------------------------------------- small cases
+
+SMALL = {
+    "c1_tiny_f32": synth.WORKLOADS["c1_tiny_f32"],
+    "bf16_ragged_gqa": synth.small("bf16_ragged_gqa"),
+    "bf16_d64_k1": synth.small("bf16_d64_k1", B=1, T_new=97, L=3, k=1, D=128, Hq=2, Hkv=1, d=64),
+    "f32_d64_kL": synth.small("f32_d64_kL", B=2, T_new=70, L=4, k=4, D=64, Hq=2, Hkv=2, d=64,
+                              dtype="f32"),
+    "bf16_long_T300": synth.small("bf16_long_T300", B=1, T_new=300, L=2, k=2, D=64, Hq=2, Hkv=1,
+                                  d=64),
+}
+
+
+def _layer_step_case(wm, w, mix_mode=0, mask_mode=0, gains="unit", ragged=False, p=None):
+    if p is not None:
+        w = synth.Workload(w.name, w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.ctx, w.dtype,
+                           w.chan_map, p, w.seed)
+    print("case", w.name, "mix", mix_mode, "mask", mask_mode, "gains", gains, "ragged", ragged,
+          "p", w.p, flush=True)
+    rng = np.random.default_rng(w.seed)
+    bias = _bias(w) + rng.normal(0, 0.3, size=w.k * w.L)
+    P = synth.make_params(w, bias, gains=gains)
+    H = synth.make_states(w)
+    ctx = synth.make_ctx_len(w, ragged=ragged)
+    K0, V0 = synth.make_cache_cpu(w)
+
+    Ko, Vo = _f64(K0).copy(), _f64(V0).copy()
+    Oo = oracle.layer_step(_odims(w, mix_mode=mix_mode, mask_mode=mask_mode), P, H, w.chan_map,
+                           ctx.numpy(), Ko, Vo)
+
+    dims = _gdims(wm, w, mix_mode=mix_mode, mask_mode=mask_mode)
+    Kg, Vg = K0.cuda(), V0.cuda()
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    wm.layer_step(dims, _dev(P), H.cuda(), w.chan_map, ctx.cuda(), Kg, Vg, O)
+    torch.cuda.synchronize()
+    _check_cache(Kg, Ko, K0, w, ctx.numpy(), w.dtype, w.name + " K")
+    _check_cache(Vg, Vo, V0, w, ctx.numpy(), w.dtype, w.name + " V")
+    check_close(O, Oo, w.dtype, w.name + " O")
+    return O
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_layer_step_small(wm, name):
+    _layer_step_case(wm, SMALL[name])
+
+
+@pytest.mark.parametrize("mix_mode,mask_mode,gains", [(1, 0, "unit"), (0, 1, "random"),
+                                                      (1, 1, "random"), (0, 0, "random")])
+def test_layer_step_modes(wm, mix_mode, mask_mode, gains):
+    _layer_step_case(wm, SMALL["bf16_ragged_gqa"], mix_mode, mask_mode, gains)
+    _layer_step_case(wm, SMALL["c1_tiny_f32"], mix_mode, mask_mode, gains)
+
+
+@pytest.mark.parametrize("p", [2, 3])
+def test_layer_step_router_subsampling(wm, p):
+    _layer_step_case(wm, SMALL["bf16_ragged_gqa"], p=p)
+    _layer_step_case(wm, SMALL["c1_tiny_f32"], p=p)
+
+
+@pytest.mark.parametrize("T_new", [1, 2, 4, 5, 33])
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_layer_step_with_context(wm, T_new, mask_mode):
+    """Decode (T_new <= 4, split-S kernels) and chunked prefill (T_new > 4) over a cached
+    context of ragged length per sequence."""
+    for dtype in ("bf16", "f32"):
+        w = synth.small("ctx_%s_T%d" % (dtype, T_new), B=3, T_new=T_new, L=5, k=2, D=64, Hq=4,
+                        Hkv=2, d=32 if dtype == "f32" else 64, ctx=700, dtype=dtype)
+        _layer_step_case(wm, w, mask_mode=mask_mode, ragged=True)
+
+
+def test_layer_step_is_deterministic(wm):
+    w = SMALL["bf16_ragged_gqa"]
+    a = _layer_step_case(wm, w)
+    b = _layer_step_case(wm, w)
+    assert torch.equal(a, b)
+
+
+def test_empty_call_is_a_no_op(wm):
+    w = synth.small("empty", B=0)
+    dims = _gdims(wm, w)
+    P = _dev(synth.make_params(synth.small(), _bias(synth.small())))
+    wm.layer_step(dims, P, None, w.chan_map, None, None, None, None)
+
+
+# --------------------------------------------------------------- single ops
+
+@pytest.mark.parametrize("name", ["c1_tiny_f32", "bf16_ragged_gqa"])
+@pytest.mark.parametrize("mix_mode", [0, 1])
+def test_router_mix(wm, name, mix_mode):
+    w = SMALL[name]
+    rng = np.random.default_rng(3)
+    P = synth.make_params(w, rng.normal(0, 1, size=(2, w.k * w.L)), gains="random")
+    H = synth.make_states(w)
+    ao, mo = oracle.router_mix(_odims(w, mix_mode=mix_mode), P, H)
+    dims = _gdims(wm, w, mix_mode=mix_mode)
+    alpha = torch.empty((2, w.N, w.k, w.L), dtype=torch.float32, device="cuda")
+    mixed = torch.empty((2, w.k, w.N, w.D), dtype=w.torch_dtype, device="cuda")
+    wm.router_mix(dims, _dev(P), H.cuda(), mixed, alpha)
+    torch.cuda.synchronize()
+    check_close(alpha, ao, w.dtype, name + " alpha")
+    check_close(mixed, mo, w.dtype, name + " mixed")
+    if mix_mode == 1:
+        s = alpha.sum(-1)
+        assert torch.allclose(s, torch.ones_like(s), atol=1e-5) and (alpha > 0).all()
+
+
+def test_router_zero_weights_give_bias_exactly(wm):
+    """W_alpha = 0: the mixing weights are the bias, exactly (fp32 and bf16)."""
+    for name in ("c1_tiny_f32", "bf16_ragged_gqa"):
+        w = SMALL[name]
+        P = synth.make_params(w, _bias(w), zero_router=True)
+        dims = _gdims(wm, w)
+        alpha = torch.empty((2, w.N, w.k, w.L), dtype=torch.float32, device="cuda")
+        mixed = torch.empty((2, w.k, w.N, w.D), dtype=w.torch_dtype, device="cuda")
+        wm.router_mix(dims, _dev(P), synth.make_states(w).cuda(), mixed, alpha)
+        torch.cuda.synchronize()
+        want = P["b_alpha"].float().reshape(2, 1, w.k, w.L).expand(2, w.N, w.k, w.L)
+        assert torch.equal(alpha.cpu(), want)
+
+
+@pytest.mark.parametrize("name", ["c1_tiny_f32", "bf16_ragged_gqa", "f32_d64_kL"])
+def test_kv_project(wm, name):
+    w = SMALL[name]
+    w = synth.Workload(w.name, w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, 50, w.dtype,
+                       w.chan_map, w.p, w.seed)
+    P = synth.make_params(w, _bias(w), gains="random")
+    mixed = synth.make_mixed(w)
+    ctx = synth.make_ctx_len(w, ragged=True)
+    K0, V0 = synth.make_cache_cpu(w)
+    Ko, Vo = _f64(K0).copy(), _f64(V0).copy()
+    oracle.kv_project(_odims(w), P, mixed, ctx.numpy(), Ko, Vo)
+    Kg, Vg = K0.cuda(), V0.cuda()
+    wm.kv_project(_gdims(wm, w), _dev(P), mixed.cuda(), ctx.cuda(), Kg, Vg)
+    torch.cuda.synchronize()
+    _check_cache(Kg, Ko, K0, w, ctx.numpy(), w.dtype, name + " K")
+    _check_cache(Vg, Vo, V0, w, ctx.numpy(), w.dtype, name + " V")
+
+
+@pytest.mark.parametrize("name", ["c1_tiny_f32", "bf16_ragged_gqa", "bf16_d64_k1"])
+def test_q_project(wm, name):
+    w = SMALL[name]
+    P = synth.make_params(w, _bias(w), gains="random")
+    H = synth.make_states(w)
+    ctx = torch.arange(w.B, dtype=torch.int32) * 37
+    Qo = oracle.q_project(_odims(w), P, H, ctx.numpy())
+    Q = torch.empty((w.L, w.B, w.Hq, w.T_new, w.d), dtype=w.torch_dtype, device="cuda")
+    wm.q_project(_gdims(wm, w, S_cap=0, ctx_max=0), _dev(P), H.cuda(), ctx.cuda(), Q)
+    torch.cuda.synchronize()
+    check_close(Q, Qo, w.dtype, name + " Q")
+
+
+@pytest.mark.parametrize("T_new,ctx", [(64, 0), (300, 0), (40, 200), (1, 1000), (3, 513)])
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_channel_attend(wm, T_new, ctx, mask_mode):
+    """Attention alone on seeded queries and a seeded cache, with a channel map where
+    several consumers share a channel (and one channel has none)."""
+    for dtype, d in (("bf16", 64), ("f32", 32)):
+        w = synth.small("attn_%s" % dtype, B=2, T_new=T_new, L=5, k=3, D=64, Hq=4, Hkv=2, d=d,
+                        ctx=ctx + T_new, dtype=dtype, chan_map=[2, 0, 2, 2, 0])
+        P = synth.make_params(w, _bias(w))
+        Q = synth.make_queries(w)
+        Kc, Vc = synth.make_cache_cpu(w)
+        ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+        Oo = oracle.channel_attend(_odims(w, mask_mode=mask_mode), P, Q, w.chan_map,
+                                   ctx_len.numpy(), _f64(Kc), _f64(Vc))
+        O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+        dims = _gdims(wm, w, mask_mode=mask_mode, ctx_max=ctx)
+        wm.channel_attend(dims, _dev(P), Q.cuda(), w.chan_map, ctx_len.cuda(), Kc.cuda(),
+                          Vc.cuda(), O)
+        torch.cuda.synchronize()
+        check_close(O, Oo, dtype, "attend %s T%d ctx%d" % (dtype, T_new, ctx))
+
+
+# ------------------------------------------------------------ full workloads
+
+FULL = ["c2_T2048_L12_k12", "c3_T2048_L12_k6", "c4_T4096_L24_k12"]
+
+
+def _sample_rows(w, b):
+    ls = sorted({0, w.L // 2, w.L - 1})
+    ts = sorted({0, 1, 63, 64, 255, 256, 1023, w.T_new // 2 + 7, w.T_new - 1})
+    return [(l * w.B + b) * w.T_new + t for l in ls for t in ts]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_sequence_step_at_full_size(wm, name):
+    """The full-size pass as the benchmark runs it; sampled sequences are re-computed by the
+    oracle (every cache slot of the sequence, sampled attention rows)."""
+    w = synth.WORKLOADS[name]
+    print("full", name, flush=True)
+    P = synth.make_params(w, _bias(w))
+    H = synth.make_states(w)
+    dims = _gdims(wm, w)
+    Kg = torch.full((w.k, w.B, w.Hkv, w.S_cap, w.d), float("nan"), dtype=w.torch_dtype,
+                    device="cuda")
+    Vg = torch.full_like(Kg, float("nan"))
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    wm.layer_step(dims, _dev(P), H.cuda(), w.chan_map, None, Kg, Vg, O)
+    torch.cuda.synchronize()
+    assert not torch.isnan(Kg[:, :, :, :w.T_new]).any()
+    assert torch.isnan(Kg[:, :, :, w.T_new:]).all()
+    PP = oracle.Params(P)
+    samples = (0, w.B - 1) if w.T_new * w.L <= 2048 * 12 else (w.B - 1,)
+    for b in samples:
+        w1 = synth.Workload(w.name, 1, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, 0, w.dtype,
+                            w.chan_map, w.p, w.seed)
+        dm = _odims(w1)
+        Ko, Vo = oracle.empty_cache(dm)
+        oracle.pool(dm, PP, H[b:b + 1], None, Ko, Vo)
+        check_close(Kg[:, b:b + 1, :, :w.T_new], Ko[:, :, :, :w.T_new], w.dtype, name + " K")
+        check_close(Vg[:, b:b + 1, :, :w.T_new], Vo[:, :, :, :w.T_new], w.dtype, name + " V")
+        rows = _sample_rows(w1, 0)
+        toks = sorted({r % w.T_new for r in rows})
+        Qo = oracle.q_project(dm, PP, H[b:b + 1], None, toks)
+        Oo = oracle.channel_attend(dm, PP, Qo, w.chan_map, None, Ko, Vo, rows)
+        g = O[:, b].float().cpu().numpy()
+        for l in sorted({r // w.T_new for r in rows}):
+            for t in toks:
+                check_close(g[l, t], Oo[l, 0, t], w.dtype, "%s O l=%d t=%d b=%d" % (name, l, t, b))
+
+
+def test_decode_step_at_full_size(wm):
+    """The 32768-context decode step: 64 new tokens appended to 12 channels, 24 consumers
+    attend; every new slot is checked, and sampled sequences' outputs are re-computed by the
+    oracle over the same cached context."""
+    w = synth.WORKLOADS["c5_decode_S32768"]
+    print("full decode", flush=True)
+    P = synth.make_params(w, _bias(w))
+    H = synth.make_states(w)
+    Kg, Vg = synth.make_cache_device(w)
+    ctx = torch.full((w.B,), w.ctx, dtype=torch.int32)
+    samples = (0, w.B - 1)
+    host = {b: (Kg[:, b:b + 1, :, :w.ctx].cpu(), Vg[:, b:b + 1, :, :w.ctx].cpu())
+            for b in samples}
+    O = torch.empty((w.L, w.B, 1, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    wm.layer_step(_gdims(wm, w), _dev(P), H.cuda(), w.chan_map, ctx.cuda(), Kg, Vg, O)
+    torch.cuda.synchronize()
+    PP = oracle.Params(P)
+    Kn, Vn = oracle.pool_rows(_odims(w), PP, H, ctx.numpy())   # [B, k, Hkv, d]
+    check_close(Kg[:, :, :, w.ctx], Kn.transpose(1, 0, 2, 3), w.dtype, "decode K new slot")
+    check_close(Vg[:, :, :, w.ctx], Vn.transpose(1, 0, 2, 3), w.dtype, "decode V new slot")
+    assert torch.isnan(Kg[:, :, :, w.ctx + 1:]).all()
+    del Kg, Vg
+    torch.cuda.empty_cache()
+    for b in samples:
+        w1 = synth.Workload(w.name, 1, 1, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.ctx, w.dtype,
+                            w.chan_map, w.p, w.seed)
+        dm = _odims(w1, S_cap=w.ctx + 1)
+        Kh, Vh = host.pop(b)
+        Ko = np.empty((w.k, 1, w.Hkv, w.ctx + 1, w.d))
+        Ko[:, :, :, :w.ctx] = _f64(Kh)
+        Ko[:, 0, :, w.ctx] = Kn[b]
+        del Kh
+        Vo = np.empty_like(Ko)
+        Vo[:, :, :, :w.ctx] = _f64(Vh)
+        Vo[:, 0, :, w.ctx] = Vn[b]
+        del Vh
+        Qo = oracle.q_project(dm, PP, H[b:b + 1], [w.ctx])
+        Oo = oracle.channel_attend(dm, PP, Qo, w.chan_map, [w.ctx], Ko, Vo)
+        check_close(O[:, b:b + 1], Oo, w.dtype, "decode O b=%d" % b)
+        del Ko, Vo
