@@ -1,0 +1,338 @@
+"""Benchmark of the fused WhiteMatter step on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step = one wm_layer_step call: pool the new tokens into the channel cache
+(row norms, router, mix, per-channel K/V projection with key norm + RoPE),
+project every consumer's queries, and run every consumer's attention over its
+channel. The default workload is the 2048-token full-sequence (Jacobi) pass
+with B = 8, L = 12, k = 12, D = 768, 12 heads of 64 (bf16). Inputs are
+synthetic and already resident in HBM when the timed region starts.
+
+Prints one JSON line: tokens/s of the step, the roofline of the dominant
+kernel (timed with HIP events recorded by the library on its own stream at the
+phase boundaries of every timed step) and the CPU oracle's tokens/s on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+WORKLOAD_LABEL = {
+    "c1_tiny_f32": "full-sequence pass, B1 T64 L4 k2 D64 2x32, fp32",
+    "c2_T2048_L12_k12": "full-sequence pass, B8 T2048 L12 k12 D768 12x64, bf16, map l->l",
+    "c3_T2048_L12_k6": "full-sequence pass, B8 T2048 L12 k6 D768 12x64, bf16, map l->l//2",
+    "c4_T4096_L24_k12": "full-sequence pass, B4 T4096 L24 k12 D1024 16x64, bf16, map l->l%12",
+    "c5_decode_S32768": "decode step, B64 ctx32768 L24 k12 D1024 16x64, bf16, map l->l%12",
+}
+
+
+# ------------------------------------------------------------ cost model
+# Algorithmic work of the step (what the method must compute / move; matrix
+# multiplies count 2 flops per multiply-add).
+
+def router_flops_per_token(L, k, D, p):
+    """Both branches: W_alpha [kL x L'D] times the stacked normed states."""
+    return 2 * 2 * k * L * ((L + p - 1) // p) * D
+
+
+def mix_flops_per_token(L, k, D):
+    """Both branches: a [k x L] by [L x D] product per token."""
+    return 2 * 2 * k * L * D
+
+
+def kv_flops_per_token(k, Hkv, d, D):
+    """W^K_j and W^V_j for every channel j."""
+    return 2 * 2 * k * Hkv * d * D
+
+
+def q_flops_per_token(L, Hq, d, D):
+    return 2 * L * Hq * d * D
+
+
+def attn_flops(L, Hq, d, visible_pairs):
+    """QK^T and PV: 4 d flops per (query head, visible slot) pair, per consumer layer."""
+    return 4 * d * Hq * L * visible_pairs
+
+
+def visible_pairs(w):
+    """Sum over queries of the slots each one reads: dummy + slots < t in the paper's
+    mask (t + 1 in total), the same count as slots <= t without the dummy."""
+    return w.B * sum(w.ctx + i + 1 for i in range(w.T_new))
+
+
+def phase_costs(w):
+    """Per-phase (flops, HBM bytes) of one step."""
+    es = 4 if w.dtype == "f32" else 2
+    N, L, k, D, Hq, Hkv, d, p = w.N, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.p
+    Lp = (L + p - 1) // p
+    H_bytes = N * L * D * es
+    cache_write = 2 * k * N * Hkv * d * es
+    used = len(set(w.chan_map))
+    cache_read = 2 * used * w.B * Hkv * (w.ctx + w.T_new) * d * es
+    return {
+        "norms": (0, H_bytes),
+        "router": (N * router_flops_per_token(L, k, D, p),
+                   N * Lp * D * es + 2 * k * L * Lp * D * es),
+        "mix": (N * mix_flops_per_token(L, k, D), H_bytes + 2 * k * N * D * es),
+        "kv_project": (N * kv_flops_per_token(k, Hkv, d, D),
+                       2 * k * N * D * es + 2 * k * Hkv * d * D * es + cache_write),
+        "q_project": (N * q_flops_per_token(L, Hq, d, D),
+                      H_bytes + L * Hq * d * D * es + L * N * Hq * d * es),
+        "attend": (attn_flops(L, Hq, d, visible_pairs(w)),
+                   L * N * Hq * d * es + cache_read + L * N * Hq * d * es),
+    }
+
+
+def step_cost(w):
+    c = phase_costs(w)
+    min_bytes = (w.N * w.L * w.D + 2 * w.k * w.L * ((w.L + w.p - 1) // w.p) * w.D
+                 + 2 * w.k * w.Hkv * w.d * w.D + w.L * w.Hq * w.d * w.D) * (
+        4 if w.dtype == "f32" else 2)
+    es = 4 if w.dtype == "f32" else 2
+    min_bytes += 2 * w.k * w.N * w.Hkv * w.d * es  # cache write
+    used = len(set(w.chan_map))
+    min_bytes += 2 * used * w.B * w.Hkv * (w.ctx + w.T_new) * w.d * es  # each channel read once
+    min_bytes += w.L * w.N * w.Hq * w.d * es  # O
+    return sum(f for f, _ in c.values()), min_bytes
+
+
+# ------------------------------------------------------------ HIP events
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch has loaded (the library uses the same)."""
+
+    def __init__(self):
+        path = None
+        with open("/proc/self/maps") as f:
+            for line in f:
+                if "libamdhip64" in line:
+                    path = line.split()[-1]
+                    break
+        if path is None:
+            raise RuntimeError("the HIP runtime is not loaded")
+        self.hip = ctypes.CDLL(path)
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self) -> int:
+        ev = ctypes.c_void_p()
+        rc = self.hip.hipEventCreate(ctypes.byref(ev))
+        if rc != 0:
+            raise RuntimeError("hipEventCreate failed: %d" % rc)
+        return ev.value
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b)
+        if rc != 0:
+            raise RuntimeError("hipEventElapsedTime failed: %d" % rc)
+        return ms.value
+
+    def destroy(self, ev):
+        self.hip.hipEventDestroy(ev)
+
+
+# ------------------------------------------------------------ traffic
+
+def _kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_18486_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch from committed rocprofv3 FETCH_SIZE/WRITE_SIZE counters, if they
+    were taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    ent = rec.get(workload, {}).get(kernel)
+    if not ent or ent.get("source_hash") != _kernel_source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+# ------------------------------------------------------------ CPU baseline
+
+def cpu_baseline(w, P, H_cpu, cache_dev):
+    """The oracle, as it stands, on a bounded sample: one sequence of a full-sequence pass,
+    or two sequences of a decode step."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from tests import synth
+
+    oracle.build(force=False)
+    nseq = 1 if w.T_new > 1 else 2
+    w1 = synth.Workload(w.name, nseq, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.ctx, w.dtype,
+                        w.chan_map, w.p, w.seed)
+    dm = oracle.Dims(B=nseq, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d,
+                     p=w.p, S_cap=w.ctx + w.T_new)
+    PP = oracle.Params(P)
+    Kc, Vc = oracle.empty_cache(dm)
+    if w.ctx:
+        Kc[:, :, :, :w.ctx] = cache_dev[0][:, :nseq, :, :w.ctx].double().cpu().numpy()
+        Vc[:, :, :, :w.ctx] = cache_dev[1][:, :nseq, :, :w.ctx].double().cpu().numpy()
+    Hs = H_cpu[:nseq]
+    ctx = np.full(nseq, w.ctx, dtype=np.int32)
+    t0 = time.perf_counter()
+    oracle.layer_step(dm, PP, Hs, w.chan_map, ctx, Kc, Vc)
+    dt = time.perf_counter() - t0
+    toks = nseq * w.T_new
+    return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d of %d sequences (%d tokens), whole step (pool, queries, attention over "
+                      "%d cached + new slots), %.1f s" % (nseq, w.B, toks, w.ctx, dt)}
+
+
+# ------------------------------------------------------------ main
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2_T2048_L12_k12", choices=sorted(WORKLOAD_LABEL))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the WhiteMatter step here runs on a single MI355X "
+              "(--gpus %d is not supported)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_18486_amd as wm
+    from tests import synth
+
+    w = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)  # noqa: E731
+    log("bench: workload %s (%s)" % (w.name, WORKLOAD_LABEL[w.name]))
+
+    bias = np.asarray(wm.init_bias(w.L, w.k))
+    P_cpu = synth.make_params(w, bias)
+    P = wm.ParamSet({k: v.to(dev) for k, v in P_cpu.items()})
+    H_cpu = synth.make_states(w)
+    H = H_cpu.to(dev)
+    if w.ctx:
+        Kc, Vc = synth.make_cache_device(w, device=dev)
+    else:
+        Kc = torch.zeros((w.k, w.B, w.Hkv, w.S_cap, w.d), dtype=w.torch_dtype, device=dev)
+        Vc = torch.zeros_like(Kc)
+    ctx = torch.full((w.B,), w.ctx, dtype=torch.int32, device=dev)
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device=dev)
+    dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p, S_cap=w.S_cap,
+                        ctx_max=w.ctx, dtype=wm.dtype_code(w.torch_dtype))
+    ws = wm.workspace(dims, wm.OP_LAYER_STEP, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    hip = HipEvents()
+    events = [[hip.create() for _ in range(wm.PROFILE_EVENTS)] for _ in range(args.steps)]
+    for _ in range(args.warmup):
+        wm.layer_step(dims, P, H, w.chan_map, ctx, Kc, Vc, O, ws=ws, stream=stream)
+    torch.cuda.synchronize()
+    log("bench: warmup done, timing %d steps" % args.steps)
+
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        wm.layer_step_profiled(dims, P, H, w.chan_map, ctx, Kc, Vc, O, events[s], ws=ws,
+                               stream=stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall = t1 - t0
+
+    phase_ms = {name: [] for name in wm.PHASES}
+    step_ms = []
+    for ev in events:
+        for i, name in enumerate(wm.PHASES):
+            phase_ms[name].append(hip.elapsed_ms(ev[i], ev[i + 1]))
+        step_ms.append(hip.elapsed_ms(ev[0], ev[-1]))
+    for ev in events:
+        for e in ev:
+            hip.destroy(e)
+    mean = {k: float(np.mean(v)) for k, v in phase_ms.items()}
+    costs = phase_costs(w)
+    flops, min_bytes = step_cost(w)
+    for name in wm.PHASES:
+        f, b = costs[name]
+        t = mean[name] * 1e-3
+        log("bench: phase %-10s %8.3f ms  %8.1f TFLOP/s  %8.1f GB/s" % (
+            name, mean[name], f / t / 1e12 if t else 0, b / t / 1e9 if t else 0))
+
+    dom = max(mean, key=mean.get)
+    f, b = costs[dom]
+    t_dom = mean[dom] * 1e-3
+    ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if f / max(b, 1) >= ridge:
+        achieved = f / t_dom / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[w.dtype],
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[w.dtype], 4)}
+    else:
+        achieved = b / t_dom / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["kernel"] = {"attend": "attend_prefill_kernel" if w.T_new > 4 else
+                      "attend_decode_kernel + attend_combine_kernel",
+                      "kv_project": "gemm_nt_kernel (K/V projection)",
+                      "q_project": "gemm_nt_kernel (Q projection)",
+                      "router": "gemm_nt_kernel (router)", "mix": "mix_kernel",
+                      "norms": "row_rms_kernel + rope_table_kernel"}[dom]
+    roof["phase"] = dom
+    roof["duration_ms"] = round(mean[dom], 4)
+    roof["traffic"] = measured_traffic(w.name, dom)
+
+    ms_per_step = wall / args.steps * 1e3
+    tokens = w.N * args.steps
+    line = {
+        "metric": "tokens/s of mix+KV-proj+channel-attention step; % of HBM / MFMA roofline",
+        "value": round(tokens / wall, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_LABEL[w.name], "B": w.B, "T_new": w.T_new,
+                   "ctx": w.ctx, "L": w.L, "k": w.k, "D": w.D, "Hq": w.Hq, "Hkv": w.Hkv,
+                   "d": w.d, "p": w.p, "tokens_per_step": w.N},
+        "roofline": roof,
+        "step_roofline": {"gflop": round(flops / 1e9, 2), "min_hbm_gb": round(min_bytes / 1e9, 3),
+                          "event_ms_per_step_median": round(float(np.median(step_ms)), 4),
+                          "phases_ms": {k: round(v, 4) for k, v in mean.items()}},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: CPU oracle baseline ...")
+        line["cpu_baseline"] = cpu_baseline(w, P_cpu, H_cpu, (Kc, Vc))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

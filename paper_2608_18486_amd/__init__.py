@@ -69,6 +69,7 @@ def lib() -> ctypes.CDLL:
         "wm_q_project": [D, P, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_channel_attend": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_layer_step": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_layer_step_profiled": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp],
         "wm_validate": [D, ctypes.c_int, _i32p],
         "wm_channel_groups": [ctypes.c_int32, ctypes.c_int32, _i32p, _i32p, _i32p],
         "wm_default_map": [ctypes.c_int32, ctypes.c_int32, _i32p],
@@ -223,3 +224,19 @@ def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws=None, str
     _check(lib().wm_layer_step(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H), _map(chan_map),
                                _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O), wp, wn,
                                _stream(stream)))
+
+
+PROFILE_EVENTS = 7
+PHASES = ("norms", "router", "mix", "kv_project", "q_project", "attend")
+
+
+def layer_step_profiled(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, events, ws=None,
+                        stream=None):
+    """layer_step that records PROFILE_EVENTS caller-created hipEvent_t handles (ints) at
+    its phase boundaries on the stream."""
+    P = _params(params)
+    ws, wp, wn = _ws(dims, OP_LAYER_STEP, ws, getattr(H, "device", None))
+    ev = (ctypes.c_void_p * PROFILE_EVENTS)(*events)
+    _check(lib().wm_layer_step_profiled(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H),
+                                        _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
+                                        _ptr(O), wp, wn, _stream(stream), ev))
