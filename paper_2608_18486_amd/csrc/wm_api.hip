@@ -31,7 +31,8 @@ size_t elem_size(const wm_dims& d) { return d.dtype == WM_BF16 ? 2 : 4; }
 bool decode_path(const wm_dims& d) { return d.T_new <= 4; }
 
 struct Layout {
-  size_t rinv = 0, alpha = 0, mixed = 0, rinv_mid = 0, tab = 0, q = 0, part = 0, total = 0;
+  size_t rinv = 0, alpha = 0, mixed = 0, rinv_mid = 0, tab = 0, q = 0, part = 0, wkv = 0, wq = 0,
+         total = 0;
 };
 
 wm::Shape make_shape(const wm_dims& d) {
@@ -75,6 +76,8 @@ Layout layout(const wm_dims& d, int op) {
   if (all) Ly.q = take((size_t)d.L * N * d.Hq * d.d * es);
   if ((op == WM_OP_CHANNEL_ATTEND || all) && decode_path(d))
     Ly.part = take(wm::decode_partials_bytes(make_shape(d)));
+  if (op == WM_OP_KV_PROJECT || all) Ly.wkv = take(wm::kv_fold_elems(make_shape(d)) * es);
+  if (op == WM_OP_Q_PROJECT || all) Ly.wq = take(wm::q_fold_elems(make_shape(d)) * es);
   Ly.total = N == 0 ? 0 : off;
   return Ly;
 }
@@ -199,7 +202,8 @@ void run_kv_project(const wm_dims& d, const wm_params& P, const T* mixed, const 
   wm::launch_row_rms<T>(mixed, 2L * sh.k * sh.N(), sh.D, sh.eps, rinv_mid, s);
   wm::launch_rope_table(sh, ctx_len, tab, s);
   wm::launch_kv_project<T>(sh, mixed, rinv_mid, (const T*)P.g_mid, (const T*)P.Wk,
-                           (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc, s);
+                           (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc,
+                           (T*)at(ws, Ly.wkv), s);
 }
 
 template <typename T>
@@ -212,7 +216,7 @@ void run_q_project(const wm_dims& d, const wm_params& P, const T* H, const int32
   wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
   wm::launch_rope_table(sh, ctx_len, tab, s);
   wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
-                          tab, Q, s);
+                          tab, Q, (T*)at(ws, Ly.wq), s);
 }
 
 template <typename T>
@@ -253,10 +257,11 @@ void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int3
   wm::launch_mix<T>(sh, H, rinv, (const T*)P.g_pre, alpha, mixed, rinv_mid, s);
   mark(3);
   wm::launch_kv_project<T>(sh, mixed, rinv_mid, (const T*)P.g_mid, (const T*)P.Wk,
-                           (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc, s);
+                           (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc,
+                           (T*)at(ws, Ly.wkv), s);
   mark(4);
   wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
-                          tab, Q, s);
+                          tab, Q, (T*)at(ws, Ly.wq), s);
   mark(5);
   run_attend<T>(d, P, Q, chan_map, ctx_len, Kc, Vc, O, (float*)at(ws, Ly.part), s);
   mark(6);

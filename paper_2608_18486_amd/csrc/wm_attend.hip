@@ -55,13 +55,29 @@ template <typename T, int DH> struct PrefillCfg {
   static constexpr int LDV = BKV + PAD;  // Vt: [DH][LDV]
   static constexpr int NKS = DH / 16;    // k16 steps of Q K^T
   static constexpr int NDT = DH / 32;    // 32-row tiles of O^T
+  static constexpr int KFR = BKV * DH / 8 / 256;          // K fragments staged per thread
+  static constexpr int VIT = (BKV / 2) * (DH / 8);        // (key pair, 8-column) items per block
+  static constexpr int VPT = (VIT + 255) / 256;           // items per thread
+  static constexpr float kRescale = 8.0f;                 // log2 headroom before rescaling
 };
 
+// Paired-key transposed store of two V rows' 8 columns: Vt[c][key], Vt[c][key+1].
+__device__ __forceinline__ void st_pair_t(bf16* vt, int ld, const bf16x8& a, const bf16x8& b) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) *(bf16x2*)(vt + i * ld) = bf16x2{a[i], b[i]};
+}
+__device__ __forceinline__ void st_pair_t(float* vt, int ld, const f32x8& a, const f32x8& b) {
+  typedef __attribute__((ext_vector_type(2))) float f32x2;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) *(f32x2*)(vt + i * ld) = f32x2{a[i], b[i]};
+}
+
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void attend_prefill_kernel(AttnArgs<T> a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attend_prefill_kernel(AttnArgs<T> a) {
   using C = PrefillCfg<T, DH>;
-  __shared__ __align__(16) T Ks[C::BKV * C::LDK];
-  __shared__ __align__(16) T Vt[DH * C::LDV];
+  __shared__ __align__(16) T Ks[2][C::BKV * C::LDK];
+  __shared__ __align__(16) T Vt[2][DH * C::LDV];
 
   const int qtile = a.n_qtiles - 1 - (int)blockIdx.x;  // longest causal rows first
   int y = blockIdx.y;
@@ -74,6 +90,8 @@ __global__ __launch_bounds__(256) void attend_prefill_kernel(AttnArgs<T> a) {
   const int ctx = a.ctx_len ? a.ctx_len[b] : 0;
   const int incl = a.mask_paper ? 0 : 1;
   const int q0 = qtile * C::BQ, qw0 = q0 + 64 * w;
+  const float cl2 = a.scale_log2;
+  const float thresh = C::kRescale / cl2;
 
   const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
   const T* Kb = a.Kc + cbase;
@@ -89,6 +107,8 @@ __global__ __launch_bounds__(256) void attend_prefill_kernel(AttnArgs<T> a) {
       qf[qt][ks] = qi < a.T_new ? ld_frag<T>(Qb + (long)qi * DH + 16 * ks + 8 * h) : zero_frag<T>();
   }
 
+  // running state per query row (lanes r and r + 32 hold the same row): reference max,
+  // partial row sum (each half-wave sums its own keys), and O^T
   float m[2], lsum[2];
   f32x16 o[C::NDT][2];
   if (a.mask_paper) {
@@ -102,7 +122,7 @@ __global__ __launch_bounds__(256) void attend_prefill_kernel(AttnArgs<T> a) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) part += to_f32(qf[qt][ks][i]) * to_f32(kd[16 * ks + 8 * h + i]);
       m[qt] = part + __shfl_xor(part, 32, 64);
-      lsum[qt] = h == 0 ? 1.f : 0.f;  // the two half-waves keep partial row sums
+      lsum[qt] = h == 0 ? 1.f : 0.f;
 #pragma unroll
       for (int dt = 0; dt < C::NDT; ++dt)
 #pragma unroll
@@ -123,93 +143,117 @@ __global__ __launch_bounds__(256) void attend_prefill_kernel(AttnArgs<T> a) {
   const int wq_last = min(qw0 + 63, a.T_new - 1);
   const int wkend = wq_last >= qw0 ? ctx + wq_last + incl : 0;  // slots this wave may see
   const int wfree = ctx + qw0 + incl;                  // slots < wfree are visible to all its rows
+  const int nblk = (kend + C::BKV - 1) / C::BKV;
 
-  for (int k0 = 0; k0 < kend; k0 += C::BKV) {
-    __syncthreads();
-    for (int f = tid; f < C::BKV * DH / 8; f += 256) {
-      int key = f / (DH / 8), dc = (f % (DH / 8)) * 8;
-      int s = k0 + key;
-      frag_t<T> kv, vv;
-      if (s < kend) {
-        kv = ld_frag<T>(Kb + (long)s * DH + dc);
-        vv = ld_frag<T>(Vb + (long)s * DH + dc);
-      } else {
-        kv = zero_frag<T>();
-        vv = zero_frag<T>();
-      }
-      st_frag<T>(Ks + key * C::LDK + dc, kv);
+  // staged next block: K fragments (row-major copy) and V key pairs (transposed store)
+  frag_t<T> kreg[C::KFR], vreg[C::VPT][2];
+  auto fetch = [&](int k0) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) Vt[(dc + i) * C::LDV + key] = vv[i];
+    for (int i = 0; i < C::KFR; ++i) {
+      int f = tid + 256 * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8, s = k0 + key;
+      kreg[i] = s < kend ? ld_frag<T>(Kb + (long)s * DH + dc) : zero_frag<T>();
     }
-    __syncthreads();
-    if (k0 >= wkend) continue;
-
-    f32x16 st[2][2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      st[kt][0] = zero16();
-      st[kt][1] = zero16();
-#pragma unroll
-      for (int ks = 0; ks < C::NKS; ++ks) {
-        frag_t<T> kf = ld_frag<T>(Ks + (32 * kt + r) * C::LDK + 16 * ks + 8 * h);
-        st[kt][0] = mma32(st[kt][0], kf, qf[0][ks]);
-        st[kt][1] = mma32(st[kt][1], kf, qf[1][ks]);
+    for (int i = 0; i < C::VPT; ++i) {
+      int it = tid + 256 * i;
+      if (it < C::VIT) {
+        int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2), s = k0 + 2 * kp;
+        vreg[i][0] = s < kend ? ld_frag<T>(Vb + (long)s * DH + 8 * dg) : zero_frag<T>();
+        vreg[i][1] = s + 1 < kend ? ld_frag<T>(Vb + (long)(s + 1) * DH + 8 * dg) : zero_frag<T>();
       }
     }
+  };
+  auto stage = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < C::KFR; ++i) {
+      int f = tid + 256 * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8;
+      st_frag<T>(&Ks[buf][key * C::LDK + dc], kreg[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < C::VPT; ++i) {
+      int it = tid + 256 * i;
+      if (it < C::VIT) {
+        int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2);
+        st_pair_t(&Vt[buf][(8 * dg) * C::LDV + 2 * kp], C::LDV, vreg[i][0], vreg[i][1]);
+      }
+    }
+  };
 
-    const bool need_mask = k0 + C::BKV > wfree;
+  if (nblk > 0) {
+    fetch(0);
+    stage(0);
+  }
+  __syncthreads();
+  for (int j = 0; j < nblk; ++j) {
+    const int k0 = j * C::BKV, buf = j & 1;
+    if (j + 1 < nblk) fetch(k0 + C::BKV);
+    if (k0 < wkend) {
+      const T* ks_ = Ks[buf];
+      const T* vt_ = Vt[buf];
+      const bool need_mask = k0 + C::BKV > wfree;
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-      const int t = ctx + qw0 + 32 * qt + r;
-      float mx = m[qt];
+      for (int kt = 0; kt < 2; ++kt) {  // two 32-key halves, each with its own softmax update
+        if (k0 + 32 * kt >= wkend) break;
+        f32x16 st[2];
+        st[0] = zero16();
+        st[1] = zero16();
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+        for (int ks = 0; ks < C::NKS; ++ks) {
+          frag_t<T> kf = ld_frag<T>(ks_ + (32 * kt + r) * C::LDK + 16 * ks + 8 * h);
+          st[0] = mma32(st[0], kf, qf[0][ks]);
+          st[1] = mma32(st[1], kf, qf[1][ks]);
+        }
+        frag_t<T> pf[2][2];  // [qt][hf]
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          float v = st[kt][qt][q];
+        for (int qt = 0; qt < 2; ++qt) {
           if (need_mask) {
-            int s = k0 + 32 * kt + 8 * (q >> 2) + 4 * h + (q & 3);
-            if (s >= t + incl) v = kNegBig;
+            const int t = ctx + qw0 + 32 * qt + r;
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              int s = k0 + 32 * kt + 8 * (q >> 2) + 4 * h + (q & 3);
+              if (s >= t + incl) st[qt][q] = kNegBig;
+            }
           }
-          st[kt][qt][q] = v;
-          mx = fmaxf(mx, v);
+          float mx = st[qt][0];
+#pragma unroll
+          for (int q = 1; q < 16; ++q) mx = fmaxf(mx, st[qt][q]);
+          mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+          const bool grow = mx > m[qt] + thresh;
+          if (__any(grow)) {
+            const float mn = grow ? mx : m[qt];
+            const float alpha = fast_exp2((m[qt] - mn) * cl2);
+            m[qt] = mn;
+            lsum[qt] *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] *= alpha;
+          }
+          const float mc = m[qt] * cl2;
+          float ps = 0.f;
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            float v = st[qt][q];
+            float p = fast_exp2(v * cl2 - mc);
+            if (need_mask) p = v > 0.5f * kNegBig ? p : 0.f;
+            ps += p;
+            pf[qt][q >> 3][q & 7] = from_f32<T>(p);
+          }
+          lsum[qt] += ps;
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float alpha = fast_exp2((m[qt] - mx) * a.scale_log2);
-      m[qt] = mx;
-      float ps = 0.f;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+        for (int hf = 0; hf < 2; ++hf) {
+          const int kc = 32 * kt + 16 * hf + 4 * h;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          float v = st[kt][qt][q];
-          float p = v > 0.5f * kNegBig ? fast_exp2((v - mx) * a.scale_log2) : 0.f;
-          st[kt][qt][q] = p;
-          ps += p;
-        }
-      lsum[qt] = lsum[qt] * alpha + ps;
-#pragma unroll
-      for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] *= alpha;
-    }
-
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        frag_t<T> pf[2];
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-          for (int i = 0; i < 8; ++i) pf[qt][i] = from_f32<T>(st[kt][qt][8 * hf + i]);
-        const int kc = 32 * kt + 16 * hf + 4 * h;
-#pragma unroll
-        for (int dt = 0; dt < C::NDT; ++dt) {
-          const T* vrow = Vt + (32 * dt + r) * C::LDV;
-          frag_t<T> vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
-          o[dt][0] = mma32(o[dt][0], vf, pf[0]);
-          o[dt][1] = mma32(o[dt][1], vf, pf[1]);
+          for (int dt = 0; dt < C::NDT; ++dt) {
+            const T* vrow = vt_ + (32 * dt + r) * C::LDV;
+            frag_t<T> vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
+            o[dt][0] = mma32(o[dt][0], vf, pf[0][hf]);
+            o[dt][1] = mma32(o[dt][1], vf, pf[1][hf]);
+          }
         }
       }
+    }
+    if (j + 1 < nblk) stage(buf ^ 1);
+    __syncthreads();
   }
 
 #pragma unroll

@@ -3,30 +3,37 @@
 // which is how the router, the per-channel K/V projections and the per-layer
 // Q projections store them. blockIdx.z selects the group g.
 //
-// The A operand is produced on the fly by an ALoad functor (it applies the
-// RMSNorm gain and row scale and rounds once to the operand type), the B
-// operand is copied from the weights, and an Epi functor consumes the fp32
-// C tile from LDS (bias, per-head norm, RoPE, cache store ...).
+// An ALoad functor produces the A operand fragments (a plain copy, or the
+// router's normed states), a BLoad functor points at weight rows, and an Epi
+// functor consumes the fp32 C tile from LDS (bias, row scale, per-head norm,
+// RoPE, cache store ...).
 //
-// Tile: 128 x 128 x 32, 256 threads = 4 waves in a 2 x 2 grid, each wave
-// owning 64 x 64 = 2 x 2 MFMA 32x32 tiles. The next K slice is fetched into
-// registers while the current one is multiplied.
+// K must be a multiple of 32; a last half slice (bf16) is zero-filled.
+// Tile 128 x 128 x BK (BK = 64 for bf16, 32 for fp32), 256 threads = 4 waves
+// in a 2 x 2 grid, each wave owning 64 x 64 = 2 x 2 MFMA 32x32 tiles. LDS is
+// double-buffered: the next K slice is fetched into registers while the
+// current one is multiplied, then stored to the other buffer, with one
+// barrier per K slice.
 #pragma once
 #include "wm_device.hpp"
 
 namespace wm {
 
 template <typename T> struct GemmCfg {
-  static constexpr int BM = 128, BN = 128, BK = 32;
+  static constexpr int BM = 128, BN = 128;
+  static constexpr int BK = sizeof(T) == 2 ? 64 : 32;
   static constexpr int PAD = sizeof(T) == 2 ? 8 : 4;  // keeps 16-B row alignment
   static constexpr int LDA = BK + PAD;                 // LDS row stride (elements)
   static constexpr int LDC = BN + 4;                   // fp32 C tile row stride
-  static constexpr int AB_BYTES = 2 * BM * LDA * (int)sizeof(T);
+  static constexpr int FR = BM * BK / 8 / 256;         // operand fragments per thread per slice
+  static constexpr int TPR = BK / (8 * FR);            // threads per tile row
+  static constexpr int STAGE = 2 * BM * LDA;           // elements per stage (A and B)
+  static constexpr int AB_BYTES = 2 * STAGE * (int)sizeof(T);
   static constexpr int C_BYTES = BM * LDC * 4;
   static constexpr int SMEM = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
 };
 
-// ALoad: void operator()(int g, int row, int k, float* out16) const   (16 elements)
+// ALoad: void operator()(int g, int row, int k, frag_t<T>* out) const  (FR consecutive frags)
 // BLoad: const T* operator()(int g, int o) const  -> row o of W_g (nullptr if o >= Nout)
 // Epi:   void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const
 template <typename T, class ALoad, class BLoad, class Epi>
@@ -34,8 +41,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, AL
                                                       BLoad bload, Epi epi) {
   using C = GemmCfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM];
-  T* As = (T*)smem;
-  T* Bs = As + C::BM * C::LDA;
+  T* stage0 = (T*)smem;
   float* Cs = (float*)smem;
 
   const int g = blockIdx.z;
@@ -43,8 +49,8 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, AL
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = w >> 1, wn = w & 1, h = lane >> 5, r = lane & 31;
 
-  // each thread moves 16 consecutive k-elements of one A row and one B row
-  const int lrow = tid >> 1, lk = (tid & 1) * 16;
+  // each thread moves FR consecutive fragments of one A row and one B row per slice
+  const int lrow = tid / C::TPR, lk = (tid % C::TPR) * 8 * C::FR;
   const bool arow_ok = m0 + lrow < M;
   const T* brow = bload(g, n0 + lrow);
 
@@ -54,43 +60,40 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, AL
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
 
-  float av[16];
-  frag_t<T> bv0, bv1;
+  frag_t<T> av[C::FR], bv[C::FR];
   auto fetch = [&](int k0) {
-    if (arow_ok) {
+    const bool kin = k0 + lk < K;  // the thread's chunk lies wholly inside or outside K
+    if (arow_ok && kin) {
       aload(g, m0 + lrow, k0 + lk, av);
     } else {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) av[i] = 0.f;
+      for (int i = 0; i < C::FR; ++i) av[i] = zero_frag<T>();
     }
-    if (brow) {
-      bv0 = ld_frag<T>(brow + k0 + lk);
-      bv1 = ld_frag<T>(brow + k0 + lk + 8);
-    } else {
-      bv0 = zero_frag<T>();
-      bv1 = zero_frag<T>();
+#pragma unroll
+    for (int i = 0; i < C::FR; ++i)
+      bv[i] = brow && kin ? ld_frag<T>(brow + k0 + lk + 8 * i) : zero_frag<T>();
+  };
+  auto stage = [&](int buf) {
+    T* As = stage0 + buf * C::STAGE;
+    T* Bs = As + C::BM * C::LDA;
+#pragma unroll
+    for (int i = 0; i < C::FR; ++i) {
+      st_frag<T>(As + lrow * C::LDA + lk + 8 * i, av[i]);
+      st_frag<T>(Bs + lrow * C::LDA + lk + 8 * i, bv[i]);
     }
   };
 
+  const int nk = (K + C::BK - 1) / C::BK;
   fetch(0);
-  for (int k0 = 0; k0 < K; k0 += C::BK) {
-    __syncthreads();
-    {
-      frag_t<T> a0, a1;
+  stage(0);
+  __syncthreads();
+  for (int kb = 0; kb < nk; ++kb) {
+    const int buf = kb & 1;
+    if (kb + 1 < nk) fetch((kb + 1) * C::BK);
+    const T* As = stage0 + buf * C::STAGE;
+    const T* Bs = As + C::BM * C::LDA;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        a0[i] = from_f32<T>(av[i]);
-        a1[i] = from_f32<T>(av[8 + i]);
-      }
-      st_frag<T>(As + lrow * C::LDA + lk, a0);
-      st_frag<T>(As + lrow * C::LDA + lk + 8, a1);
-      st_frag<T>(Bs + lrow * C::LDA + lk, bv0);
-      st_frag<T>(Bs + lrow * C::LDA + lk + 8, bv1);
-    }
-    __syncthreads();
-    if (k0 + C::BK < K) fetch(k0 + C::BK);
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < C::BK / 16; ++ks) {
       frag_t<T> a[2], b[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -103,8 +106,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, AL
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = mma32(acc[i][j], a[i], b[j]);
     }
+    if (kb + 1 < nk) stage(buf ^ 1);
+    __syncthreads();
   }
-  __syncthreads();
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll

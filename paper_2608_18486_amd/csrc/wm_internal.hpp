@@ -44,16 +44,19 @@ template <typename T>
 void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
                 T* mixed, float* rinv_mid, hipStream_t s);
 
-// mixed -> K (mid norm, W^K_j, key norm, RoPE) and V (mid norm, W^V_j) at slot ctx_len[b]+i
+// mixed -> K (mid norm, W^K_j, key norm, RoPE) and V (mid norm, W^V_j) at slot ctx_len[b]+i.
+// wfold: workspace for the gain-folded weights, kv_fold_elems(sh) elements.
+size_t kv_fold_elems(const Shape& sh);
 template <typename T>
 void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, const T* g_mid,
                        const T* Wk, const T* Wv, const T* g_knorm, const float* rope_tab,
-                       const int32_t* ctx_len, T* Kc, T* Vc, hipStream_t s);
+                       const int32_t* ctx_len, T* Kc, T* Vc, T* wfold, hipStream_t s);
 
-// H -> Q[L][B][Hq][T_new][d] (input norm, W^Q_l, q norm, RoPE)
+// H -> Q[L][B][Hq][T_new][d] (input norm, W^Q_l, q norm, RoPE); wfold: q_fold_elems(sh).
+size_t q_fold_elems(const Shape& sh);
 template <typename T>
 void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g_in,
-                      const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q,
+                      const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q, T* wfold,
                       hipStream_t s);
 
 // -- consumer side (Step 3) ---------------------------------------------------

@@ -7,10 +7,12 @@
 //                the stack of normed states of layers {L-1-p*m}
 //   mix          (optional softmax over source layers) and the per-token mix
 //                h~_j = sum_l alpha[j][l] h^_l, plus 1 / RMS of each channel
-//   kv_project   per-channel W^K_j / W^V_j on the matrix cores, with the mid
-//                RMSNorm folded into the operand and key norm + RoPE + the
-//                channel-major cache store in the epilogue
-//   q_project    the consumer's query: input norm, W^Q_l, q norm, RoPE
+//   kv_project   per-channel W^K_j / W^V_j on the matrix cores; the mid
+//                RMSNorm gain is folded into a per-call copy of the weights and
+//                its 1/RMS, the key norm, RoPE and the channel-major cache
+//                store happen in the epilogue
+//   q_project    the consumer's query (input norm, W^Q_l, q norm, RoPE), built
+//                the same way
 #include "wm_gemm.hpp"
 #include "wm_internal.hpp"
 
@@ -78,17 +80,6 @@ template <typename T> struct WeightRows {
   }
 };
 
-// K/V projection weights: group g = branch * k + channel.
-template <typename T> struct KVWeightRows {
-  const T *Wk, *Wv;
-  int k, Nout, K;
-  __device__ const T* operator()(int g, int o) const {
-    if (o >= Nout) return nullptr;
-    int br = g / k, j = g - br * k;
-    return (br ? Wv : Wk) + ((long)j * Nout + o) * K;
-  }
-};
-
 // Router operand: the stacked normed states xi (gain and 1/RMS applied, one rounding).
 template <typename T> struct RouterA {
   const T* H;
@@ -96,42 +87,30 @@ template <typename T> struct RouterA {
   const T* g_pre;
   LayerTable sel;
   int L, D;
-  __device__ void operator()(int br, int n, int k, float* out) const {
+  __device__ void operator()(int br, int n, int k, frag_t<T>* out) const {
     int m = k / D, e = k - m * D, layer = sel.v[m];
     const T* x = H + ((long)n * L + layer) * D + e;
     const T* g = g_pre + ((long)br * L + layer) * D + e;
     float rs = rinv[(long)n * L + layer];
 #pragma unroll
-    for (int hv = 0; hv < 2; ++hv) {
+    for (int f = 0; f < GemmCfg<T>::FR; ++f) {
       float xv[8], gv[8];
-      load8(x + 8 * hv, xv);
-      load8(g + 8 * hv, gv);
+      load8(x + 8 * f, xv);
+      load8(g + 8 * f, gv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) out[8 * hv + i] = xv[i] * gv[i] * rs;
+      for (int i = 0; i < 8; ++i) out[f][i] = from_f32<T>(xv[i] * gv[i] * rs);
     }
   }
 };
 
-// Generic normed-row operand: X[g][row][k] * gain[g][k] * rs[g][row].
-template <typename T> struct NormedRowsA {
+// Plain operand rows: X[g * gstride + row * rstride + k] (scales live elsewhere).
+template <typename T> struct CopyRowsA {
   const T* X;
-  long x_gstride, x_rstride;
-  const T* gain;
-  long g_gstride;
-  const float* rs;
-  long rs_gstride, rs_rstride;
-  __device__ void operator()(int g, int row, int k, float* out) const {
-    const T* x = X + (long)g * x_gstride + (long)row * x_rstride + k;
-    const T* gg = gain + (long)g * g_gstride + k;
-    float s = rs[(long)g * rs_gstride + (long)row * rs_rstride];
+  long gstride, rstride;
+  __device__ void operator()(int g, int row, int k, frag_t<T>* out) const {
+    const T* x = X + (long)g * gstride + (long)row * rstride + k;
 #pragma unroll
-    for (int hv = 0; hv < 2; ++hv) {
-      float xv[8], gv[8];
-      load8(x + 8 * hv, xv);
-      load8(gg + 8 * hv, gv);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) out[8 * hv + i] = xv[i] * gv[i] * s;
-    }
+    for (int f = 0; f < GemmCfg<T>::FR; ++f) out[f] = ld_frag<T>(x + 8 * f);
   }
 };
 
@@ -151,16 +130,18 @@ template <typename T> struct RouterEpi {
   }
 };
 
-// One head row: RMS over d, gain, RoPE with the per-token (cos, sin) table, store.
+// One head row of a GEMM result (times the row scale sc): RMS over d, gain, RoPE with the
+// per-token (cos, sin) table, store.
 template <typename T>
-__device__ __forceinline__ void head_norm_rope_store(const float* c, T* dst, const T* gain,
-                                                     const float* tab, int d, float eps) {
+__device__ __forceinline__ void head_norm_rope_store(const float* c, float sc, T* dst,
+                                                     const T* gain, const float* tab, int d,
+                                                     float eps) {
   float ss = 0.f;
   for (int e = 0; e < d; e += 4) {
-    f32x4 v = *(const f32x4*)(c + e);
+    f32x4 v = *(const f32x4*)(c + e) * sc;
     ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
   }
-  float rs = 1.0f / sqrtf(ss / (float)d + eps);
+  float rs = sc / sqrtf(ss / (float)d + eps);
   int half = d / 2;
   for (int m = 0; m < half; m += 4) {
     f32x4 x1 = *(const f32x4*)(c + m), x2 = *(const f32x4*)(c + m + half);
@@ -179,9 +160,9 @@ __device__ __forceinline__ void head_norm_rope_store(const float* c, T* dst, con
 }
 
 template <typename T>
-__device__ __forceinline__ void head_store(const float* c, T* dst, int d) {
+__device__ __forceinline__ void head_store(const float* c, float sc, T* dst, int d) {
   for (int e = 0; e < d; e += 4) {
-    f32x4 v = *(const f32x4*)(c + e);
+    f32x4 v = *(const f32x4*)(c + e) * sc;
     float y[4] = {v[0], v[1], v[2], v[3]};
     store4(dst + e, y);
   }
@@ -189,6 +170,7 @@ __device__ __forceinline__ void head_store(const float* c, T* dst, int d) {
 
 template <typename T> struct KVEpi {
   T *Kc, *Vc;
+  const float* rs;  // [2k][M] 1 / RMS of each mixed channel row (the mid RMSNorm)
   const T* g_knorm;
   const float* tab;
   const int32_t* ctx_len;
@@ -207,19 +189,21 @@ template <typename T> struct KVEpi {
       int head = col0 / d;
       long off = ((((long)j * B + b) * Hkv + head) * S_cap + slot) * d;
       const float* c = C + row * ldc + hh * d;
+      const float sc = rs[(long)g * M + n];
       if (br == 0)
-        head_norm_rope_store(c, Kc + off, g_knorm + (long)j * d, tab + (long)n * d, d, eps);
+        head_norm_rope_store(c, sc, Kc + off, g_knorm + (long)j * d, tab + (long)n * d, d, eps);
       else
-        head_store(c, Vc + off, d);
+        head_store(c, sc, Vc + off, d);
     }
   }
 };
 
 template <typename T> struct QEpi {
   T* Q;
+  const float* rs;  // [M][L] 1 / RMS of each consumer's input state (the input RMSNorm)
   const T* g_qnorm;
   const float* tab;
-  int M, Nout, d, T_new, B, Hq;
+  int M, Nout, d, T_new, B, Hq, L;
   float eps;
   __device__ void operator()(int l, int m0, int n0, const float* C, int ldc, int tid) const {
     int hpt = 128 / d;
@@ -229,8 +213,8 @@ template <typename T> struct QEpi {
       if (n >= M || col0 >= Nout) continue;
       int b = n / T_new, i = n - b * T_new, head = col0 / d;
       long off = ((((long)l * B + b) * Hq + head) * T_new + i) * d;
-      head_norm_rope_store(C + row * ldc + hh * d, Q + off, g_qnorm + (long)l * d,
-                           tab + (long)n * d, d, eps);
+      head_norm_rope_store(C + row * ldc + hh * d, rs[(long)n * L + l], Q + off,
+                           g_qnorm + (long)l * d, tab + (long)n * d, d, eps);
     }
   }
 };
@@ -343,32 +327,68 @@ void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, 
 }
 
 // ------------------------------------------------------------- projections
+// Fold an RMSNorm gain into the weights that consume the normed vector:
+// Wf[grp][o][e] = W[grp][o][e] * gain[grp][e]; the row's 1/RMS is applied in the
+// GEMM epilogue. The K/V projections take two source tensors (groups [0, split)
+// from W0 = W^K, the rest from W1 = W^V).
+template <typename T>
+__global__ __launch_bounds__(256) void fold_gain_kernel(const T* W0, const T* W1, int split,
+                                                        const T* gain, T* Wf, int groups,
+                                                        int Nout, int K) {
+  long idx = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
+  long per = (long)Nout * K;
+  if (idx >= per * groups) return;
+  int grp = (int)(idx / per);
+  long rem = idx - (long)grp * per;
+  int e = (int)(rem % K);
+  const T* src = grp < split ? W0 + (long)grp * per + rem : W1 + (long)(grp - split) * per + rem;
+  float wv[8], gv[8];
+  load8(src, wv);
+  load8(gain + (long)grp * K + e, gv);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) wv[i] *= gv[i];
+  store8(Wf + idx, wv);
+}
+
+template <typename T>
+static void fold_gain(const T* W0, const T* W1, int split, const T* gain, T* Wf, int groups,
+                      int Nout, int K, hipStream_t s) {
+  long total = (long)groups * Nout * K / 8;
+  hipLaunchKernelGGL(fold_gain_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                     W0, W1, split, gain, Wf, groups, Nout, K);
+}
+
+size_t kv_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.Hkv * sh.d * sh.D; }
+size_t q_fold_elems(const Shape& sh) { return (size_t)sh.L * sh.Hq * sh.d * sh.D; }
+
 template <typename T>
 void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, const T* g_mid,
                        const T* Wk, const T* Wv, const T* g_knorm, const float* rope_tab,
-                       const int32_t* ctx_len, T* Kc, T* Vc, hipStream_t s) {
+                       const int32_t* ctx_len, T* Kc, T* Vc, T* wfold, hipStream_t s) {
   int M = sh.N(), Nout = sh.Hkv * sh.d, K = sh.D;
   if (M <= 0) return;
-  NormedRowsA<T> a{mixed, (long)M * K, K, g_mid, K, rinv_mid, M, 1};
-  KVWeightRows<T> w{Wk, Wv, sh.k, Nout, K};
-  KVEpi<T> e{Kc, Vc, g_knorm, rope_tab, ctx_len, M, Nout, sh.d, sh.T_new, sh.B, sh.Hkv,
-             sh.S_cap, sh.k, sh.eps};
+  fold_gain<T>(Wk, Wv, sh.k, g_mid, wfold, 2 * sh.k, Nout, K, s);
+  CopyRowsA<T> a{mixed, (long)M * K, K};
+  WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
+  KVEpi<T> e{Kc, Vc, rinv_mid, g_knorm, rope_tab, ctx_len, M, Nout, sh.d, sh.T_new, sh.B,
+             sh.Hkv, sh.S_cap, sh.k, sh.eps};
   dim3 grid((Nout + 127) / 128, (M + 127) / 128, 2 * sh.k);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, NormedRowsA<T>, KVWeightRows<T>, KVEpi<T>>), grid,
+  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, KVEpi<T>>), grid,
                      dim3(256), 0, s, M, Nout, K, a, w, e);
 }
 
 template <typename T>
 void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g_in,
-                      const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q,
+                      const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q, T* wfold,
                       hipStream_t s) {
   int M = sh.N(), Nout = sh.Hq * sh.d, K = sh.D;
   if (M <= 0) return;
-  NormedRowsA<T> a{H, K, (long)sh.L * K, g_in, K, rinv, 1, sh.L};
-  WeightRows<T> w{Wq, (long)Nout * K, Nout, K};
-  QEpi<T> e{Q, g_qnorm, rope_tab, M, Nout, sh.d, sh.T_new, sh.B, sh.Hq, sh.eps};
+  fold_gain<T>(Wq, Wq, sh.L, g_in, wfold, sh.L, Nout, K, s);
+  CopyRowsA<T> a{H, K, (long)sh.L * K};
+  WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
+  QEpi<T> e{Q, rinv, g_qnorm, rope_tab, M, Nout, sh.d, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
   dim3 grid((Nout + 127) / 128, (M + 127) / 128, sh.L);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, NormedRowsA<T>, WeightRows<T>, QEpi<T>>), grid,
+  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, QEpi<T>>), grid,
                      dim3(256), 0, s, M, Nout, K, a, w, e);
 }
 
@@ -380,9 +400,9 @@ void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g
                               float*, hipStream_t);                                            \
   template void launch_kv_project<T>(const Shape&, const T*, const float*, const T*, const T*, \
                                      const T*, const T*, const float*, const int32_t*, T*, T*, \
-                                     hipStream_t);                                             \
+                                     T*, hipStream_t);                                         \
   template void launch_q_project<T>(const Shape&, const T*, const float*, const T*, const T*,  \
-                                    const T*, const float*, T*, hipStream_t);
+                                    const T*, const float*, T*, T*, hipStream_t);
 WM_INST(float)
 WM_INST(bf16)
 #undef WM_INST
