@@ -72,6 +72,77 @@ __device__ __forceinline__ void st_pair_t(float* vt, int ld, const f32x8& a, con
   for (int i = 0; i < 8; ++i) *(f32x2*)(vt + i * ld) = f32x2{a[i], b[i]};
 }
 
+// One 64-key block for one wave (64 queries = 2 tiles of 32): two 32-key halves, each
+// S^T = K Q^T, online-softmax update (lazy rescale), O^T += V^T P^T. MASK selects the
+// code for blocks that straddle the causal boundary of some of the wave's rows.
+template <typename T, int DH, bool MASK>
+__device__ __forceinline__ void attend_block(const T* __restrict__ ks_, const T* __restrict__ vt_,
+                                             const frag_t<T> (&qf)[2][DH / 16], float (&m)[2],
+                                             float (&lsum)[2], f32x16 (&o)[DH / 32][2], int k0,
+                                             int wkend, int tq0, int incl, int h, int r,
+                                             float cl2, float thresh) {
+  using C = PrefillCfg<T, DH>;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    if (MASK && k0 + 32 * kt >= wkend) break;  // this half is past every row of the wave
+    f32x16 st[2];
+    st[0] = zero16();
+    st[1] = zero16();
+#pragma unroll
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      frag_t<T> kf = ld_frag<T>(ks_ + (32 * kt + r) * C::LDK + 16 * ks + 8 * h);
+      st[0] = mma32(st[0], kf, qf[0][ks]);
+      st[1] = mma32(st[1], kf, qf[1][ks]);
+    }
+    frag_t<T> pf[2][2];  // [qt][hf]
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      if (MASK) {
+        // slot k0 + 32kt + 8(q/4) + 4h + q%4 is visible to the row at position t iff
+        // it is < t + incl
+        const int lim = tq0 + 32 * qt + r + incl - (k0 + 32 * kt + 4 * h);
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          if (8 * (q >> 2) + (q & 3) >= lim) st[qt][q] = kNegBig;
+      }
+      float mx = st[qt][0];
+#pragma unroll
+      for (int q = 1; q < 16; ++q) mx = fmaxf(mx, st[qt][q]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const bool grow = mx > m[qt] + thresh;
+      if (__any(grow)) {
+        const float mn = grow ? mx : m[qt];
+        const float alpha = fast_exp2((m[qt] - mn) * cl2);
+        m[qt] = mn;
+        lsum[qt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] *= alpha;
+      }
+      const float mc = m[qt] * cl2;
+      float ps = 0.f;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        float p = fast_exp2(st[qt][q] * cl2 - mc);
+        if (MASK) p = st[qt][q] > 0.5f * kNegBig ? p : 0.f;
+        ps += p;
+        pf[qt][q >> 3][q & 7] = from_f32<T>(p);
+      }
+      lsum[qt] += ps;
+    }
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int kc = 32 * kt + 16 * hf + 4 * h;
+#pragma unroll
+      for (int dt = 0; dt < C::NDT; ++dt) {
+        const T* vrow = vt_ + (32 * dt + r) * C::LDV;
+        frag_t<T> vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
+        o[dt][0] = mma32(o[dt][0], vf, pf[0][hf]);
+        o[dt][1] = mma32(o[dt][1], vf, pf[1][hf]);
+      }
+    }
+  }
+}
+
 template <typename T, int DH>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attend_prefill_kernel(AttnArgs<T> a) {
@@ -188,69 +259,12 @@ void attend_prefill_kernel(AttnArgs<T> a) {
     const int k0 = j * C::BKV, buf = j & 1;
     if (j + 1 < nblk) fetch(k0 + C::BKV);
     if (k0 < wkend) {
-      const T* ks_ = Ks[buf];
-      const T* vt_ = Vt[buf];
-      const bool need_mask = k0 + C::BKV > wfree;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {  // two 32-key halves, each with its own softmax update
-        if (k0 + 32 * kt >= wkend) break;
-        f32x16 st[2];
-        st[0] = zero16();
-        st[1] = zero16();
-#pragma unroll
-        for (int ks = 0; ks < C::NKS; ++ks) {
-          frag_t<T> kf = ld_frag<T>(ks_ + (32 * kt + r) * C::LDK + 16 * ks + 8 * h);
-          st[0] = mma32(st[0], kf, qf[0][ks]);
-          st[1] = mma32(st[1], kf, qf[1][ks]);
-        }
-        frag_t<T> pf[2][2];  // [qt][hf]
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          if (need_mask) {
-            const int t = ctx + qw0 + 32 * qt + r;
-#pragma unroll
-            for (int q = 0; q < 16; ++q) {
-              int s = k0 + 32 * kt + 8 * (q >> 2) + 4 * h + (q & 3);
-              if (s >= t + incl) st[qt][q] = kNegBig;
-            }
-          }
-          float mx = st[qt][0];
-#pragma unroll
-          for (int q = 1; q < 16; ++q) mx = fmaxf(mx, st[qt][q]);
-          mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-          const bool grow = mx > m[qt] + thresh;
-          if (__any(grow)) {
-            const float mn = grow ? mx : m[qt];
-            const float alpha = fast_exp2((m[qt] - mn) * cl2);
-            m[qt] = mn;
-            lsum[qt] *= alpha;
-#pragma unroll
-            for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] *= alpha;
-          }
-          const float mc = m[qt] * cl2;
-          float ps = 0.f;
-#pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            float v = st[qt][q];
-            float p = fast_exp2(v * cl2 - mc);
-            if (need_mask) p = v > 0.5f * kNegBig ? p : 0.f;
-            ps += p;
-            pf[qt][q >> 3][q & 7] = from_f32<T>(p);
-          }
-          lsum[qt] += ps;
-        }
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const int kc = 32 * kt + 16 * hf + 4 * h;
-#pragma unroll
-          for (int dt = 0; dt < C::NDT; ++dt) {
-            const T* vrow = vt_ + (32 * dt + r) * C::LDV;
-            frag_t<T> vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
-            o[dt][0] = mma32(o[dt][0], vf, pf[0][hf]);
-            o[dt][1] = mma32(o[dt][1], vf, pf[1][hf]);
-          }
-        }
-      }
+      if (k0 + C::BKV > wfree)
+        attend_block<T, DH, true>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
+                                  h, r, cl2, thresh);
+      else
+        attend_block<T, DH, false>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
+                                   h, r, cl2, thresh);
     }
     if (j + 1 < nblk) stage(buf ^ 1);
     __syncthreads();
