@@ -47,18 +47,24 @@ template <typename T> struct AttnArgs {
   LayerTable chan;
 };
 
+constexpr int kPrefillWaves = 8;  // waves per prefill workgroup
+
 template <typename T, int DH> struct PrefillCfg {
-  static constexpr int BQ = 256;   // queries per workgroup (4 waves x 64)
-  static constexpr int BKV = 64;   // keys per block
+  static constexpr int NW = kPrefillWaves;
+  static constexpr int QT = 1;          // 32-query tiles per wave
+  static constexpr int NT = 64 * NW;    // threads
+  static constexpr int BQ = 32 * QT * NW;  // queries per workgroup
+  static constexpr int BKV = 64;        // keys per block
   static constexpr int PAD = sizeof(T) == 2 ? 8 : 4;
   static constexpr int LDK = DH + PAD;   // Ks: [BKV][LDK]
   static constexpr int LDV = BKV + PAD;  // Vt: [DH][LDV]
   static constexpr int NKS = DH / 16;    // k16 steps of Q K^T
   static constexpr int NDT = DH / 32;    // 32-row tiles of O^T
-  static constexpr int KFR = BKV * DH / 8 / 256;          // K fragments staged per thread
-  static constexpr int VIT = (BKV / 2) * (DH / 8);        // (key pair, 8-column) items per block
-  static constexpr int VPT = (VIT + 255) / 256;           // items per thread
-  static constexpr float kRescale = 8.0f;                 // log2 headroom before rescaling
+  static constexpr int KIT = BKV * DH / 8;             // K fragments per block
+  static constexpr int KFR = (KIT + NT - 1) / NT;      // ... per thread
+  static constexpr int VIT = (BKV / 2) * (DH / 8);     // (key pair, 8-column) items per block
+  static constexpr int VPT = (VIT + NT - 1) / NT;      // ... per thread
+  static constexpr float kRescale = 8.0f;              // log2 headroom before rescaling
 };
 
 // Paired-key transposed store of two V rows' 8 columns: Vt[c][key], Vt[c][key+1].
@@ -72,31 +78,31 @@ __device__ __forceinline__ void st_pair_t(float* vt, int ld, const f32x8& a, con
   for (int i = 0; i < 8; ++i) *(f32x2*)(vt + i * ld) = f32x2{a[i], b[i]};
 }
 
-// One 64-key block for one wave (64 queries = 2 tiles of 32): two 32-key halves, each
+// One 64-key block for one wave (QT tiles of 32 queries): two 32-key halves, each
 // S^T = K Q^T, online-softmax update (lazy rescale), O^T += V^T P^T. MASK selects the
 // code for blocks that straddle the causal boundary of some of the wave's rows.
 template <typename T, int DH, bool MASK>
-__device__ __forceinline__ void attend_block(const T* __restrict__ ks_, const T* __restrict__ vt_,
-                                             const frag_t<T> (&qf)[2][DH / 16], float (&m)[2],
-                                             float (&lsum)[2], f32x16 (&o)[DH / 32][2], int k0,
-                                             int wkend, int tq0, int incl, int h, int r,
-                                             float cl2, float thresh) {
+__device__ __forceinline__ void attend_block(
+    const T* __restrict__ ks_, const T* __restrict__ vt_,
+    const frag_t<T> (&qf)[PrefillCfg<T, DH>::QT][DH / 16], float (&m)[PrefillCfg<T, DH>::QT],
+    float (&lsum)[PrefillCfg<T, DH>::QT], f32x16 (&o)[DH / 32][PrefillCfg<T, DH>::QT], int k0,
+    int wkend, int tq0, int incl, int h, int r, float cl2, float thresh) {
   using C = PrefillCfg<T, DH>;
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
     if (MASK && k0 + 32 * kt >= wkend) break;  // this half is past every row of the wave
-    f32x16 st[2];
-    st[0] = zero16();
-    st[1] = zero16();
+    f32x16 st[C::QT];
+#pragma unroll
+    for (int qt = 0; qt < C::QT; ++qt) st[qt] = zero16();
 #pragma unroll
     for (int ks = 0; ks < C::NKS; ++ks) {
       frag_t<T> kf = ld_frag<T>(ks_ + (32 * kt + r) * C::LDK + 16 * ks + 8 * h);
-      st[0] = mma32(st[0], kf, qf[0][ks]);
-      st[1] = mma32(st[1], kf, qf[1][ks]);
-    }
-    frag_t<T> pf[2][2];  // [qt][hf]
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+      for (int qt = 0; qt < C::QT; ++qt) st[qt] = mma32(st[qt], kf, qf[qt][ks]);
+    }
+    frag_t<T> pf[C::QT][2];  // [qt][hf]
+#pragma unroll
+    for (int qt = 0; qt < C::QT; ++qt) {
       if (MASK) {
         // slot k0 + 32kt + 8(q/4) + 4h + q%4 is visible to the row at position t iff
         // it is < t + incl
@@ -136,22 +142,25 @@ __device__ __forceinline__ void attend_block(const T* __restrict__ ks_, const T*
       for (int dt = 0; dt < C::NDT; ++dt) {
         const T* vrow = vt_ + (32 * dt + r) * C::LDV;
         frag_t<T> vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
-        o[dt][0] = mma32(o[dt][0], vf, pf[0][hf]);
-        o[dt][1] = mma32(o[dt][1], vf, pf[1][hf]);
+#pragma unroll
+        for (int qt = 0; qt < C::QT; ++qt) o[dt][qt] = mma32(o[dt][qt], vf, pf[qt][hf]);
       }
     }
   }
 }
 
 template <typename T, int DH>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void attend_prefill_kernel(AttnArgs<T> a) {
+__global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(AttnArgs<T> a) {
   using C = PrefillCfg<T, DH>;
+  constexpr int QT = C::QT;
   __shared__ __align__(16) T Ks[2][C::BKV * C::LDK];
   __shared__ __align__(16) T Vt[2][DH * C::LDV];
 
-  const int qtile = a.n_qtiles - 1 - (int)blockIdx.x;  // longest causal rows first
-  int y = blockIdx.y;
+  // 1-D grid over (consumer, sequence, head, query tile); each XCD takes a contiguous
+  // run of heads, and a head's tiles run longest causal rows first on one L2
+  const int tile = xcd_tile(blockIdx.x, a.n_qtiles * a.Hq * a.B * a.L);
+  const int qtile = a.n_qtiles - 1 - tile % a.n_qtiles;
+  int y = tile / a.n_qtiles;
   const int hq = y % a.Hq;
   y /= a.Hq;
   const int b = y % a.B, l = y / a.B;
@@ -160,7 +169,7 @@ void attend_prefill_kernel(AttnArgs<T> a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, r = lane & 31;
   const int ctx = a.ctx_len ? a.ctx_len[b] : 0;
   const int incl = a.mask_paper ? 0 : 1;
-  const int q0 = qtile * C::BQ, qw0 = q0 + 64 * w;
+  const int q0 = qtile * C::BQ, qw0 = q0 + 32 * QT * w;
   const float cl2 = a.scale_log2;
   const float thresh = C::kRescale / cl2;
 
@@ -168,10 +177,10 @@ void attend_prefill_kernel(AttnArgs<T> a) {
   const T* Kb = a.Kc + cbase;
   const T* Vb = a.Vc + cbase;
 
-  frag_t<T> qf[2][C::NKS];
+  frag_t<T> qf[QT][C::NKS];
   const T* Qb = a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * DH;
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     int qi = qw0 + 32 * qt + r;
 #pragma unroll
     for (int ks = 0; ks < C::NKS; ++ks)
@@ -180,13 +189,13 @@ void attend_prefill_kernel(AttnArgs<T> a) {
 
   // running state per query row (lanes r and r + 32 hold the same row): reference max,
   // partial row sum (each half-wave sums its own keys), and O^T
-  float m[2], lsum[2];
-  f32x16 o[C::NDT][2];
+  float m[QT], lsum[QT];
+  f32x16 o[C::NDT][QT];
   if (a.mask_paper) {
     const T* kd = a.Kd + ((long)c * a.Hkv + kvh) * DH;
     const T* vd = a.Vd + ((long)c * a.Hkv + kvh) * DH;
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       float part = 0.f;
 #pragma unroll
       for (int ks = 0; ks < C::NKS; ++ks)
@@ -201,7 +210,7 @@ void attend_prefill_kernel(AttnArgs<T> a) {
     }
   } else {
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       m[qt] = kNegBig;
       lsum[qt] = 0.f;
 #pragma unroll
@@ -211,7 +220,7 @@ void attend_prefill_kernel(AttnArgs<T> a) {
 
   const int qlast = min(q0 + C::BQ, a.T_new) - 1;
   const int kend = min(ctx + qlast + incl, a.S_cap);   // slots the workgroup may see
-  const int wq_last = min(qw0 + 63, a.T_new - 1);
+  const int wq_last = min(qw0 + 32 * QT - 1, a.T_new - 1);
   const int wkend = wq_last >= qw0 ? ctx + wq_last + incl : 0;  // slots this wave may see
   const int wfree = ctx + qw0 + incl;                  // slots < wfree are visible to all its rows
   const int nblk = (kend + C::BKV - 1) / C::BKV;
@@ -221,12 +230,12 @@ void attend_prefill_kernel(AttnArgs<T> a) {
   auto fetch = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < C::KFR; ++i) {
-      int f = tid + 256 * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8, s = k0 + key;
-      kreg[i] = s < kend ? ld_frag<T>(Kb + (long)s * DH + dc) : zero_frag<T>();
+      int f = tid + C::NT * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8, s = k0 + key;
+      kreg[i] = f < C::KIT && s < kend ? ld_frag<T>(Kb + (long)s * DH + dc) : zero_frag<T>();
     }
 #pragma unroll
     for (int i = 0; i < C::VPT; ++i) {
-      int it = tid + 256 * i;
+      int it = tid + C::NT * i;
       if (it < C::VIT) {
         int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2), s = k0 + 2 * kp;
         vreg[i][0] = s < kend ? ld_frag<T>(Vb + (long)s * DH + 8 * dg) : zero_frag<T>();
@@ -237,12 +246,12 @@ void attend_prefill_kernel(AttnArgs<T> a) {
   auto stage = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < C::KFR; ++i) {
-      int f = tid + 256 * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8;
-      st_frag<T>(&Ks[buf][key * C::LDK + dc], kreg[i]);
+      int f = tid + C::NT * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8;
+      if (f < C::KIT) st_frag<T>(&Ks[buf][key * C::LDK + dc], kreg[i]);
     }
 #pragma unroll
     for (int i = 0; i < C::VPT; ++i) {
-      int it = tid + 256 * i;
+      int it = tid + C::NT * i;
       if (it < C::VIT) {
         int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2);
         st_pair_t(&Vt[buf][(8 * dg) * C::LDV + 2 * kp], C::LDV, vreg[i][0], vreg[i][1]);
@@ -271,7 +280,7 @@ void attend_prefill_kernel(AttnArgs<T> a) {
   }
 
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     const int qi = qw0 + 32 * qt + r;
     const float lt = lsum[qt] + __shfl_xor(lsum[qt], 32, 64);
     if (qi >= a.T_new) continue;
@@ -294,14 +303,16 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
                            const T* Vc, const T* Kd, const T* Vd, const int32_t* ctx_len, T* O,
                            hipStream_t s) {
   if (sh.N() <= 0) return;
+  constexpr int BQ = PrefillCfg<T, 64>::BQ, NT = PrefillCfg<T, 64>::NT;
+  static_assert(BQ == PrefillCfg<T, 32>::BQ && NT == PrefillCfg<T, 32>::NT, "tile shapes");
   AttnArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
-                sh.mask_paper, (sh.T_new + 255) / 256,
+                sh.mask_paper, (sh.T_new + BQ - 1) / BQ,
                 kLog2e / sqrtf((float)sh.d), chan_map};
-  dim3 grid(a.n_qtiles, sh.Hq * sh.B * sh.L);
+  dim3 grid(a.n_qtiles * sh.Hq * sh.B * sh.L);
   if (sh.d == 64)
-    hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(NT), 0, s, a);
   else
-    hipLaunchKernelGGL((attend_prefill_kernel<T, 32>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attend_prefill_kernel<T, 32>), grid, dim3(NT), 0, s, a);
 }
 
 // ------------------------------------------------------------------ decode

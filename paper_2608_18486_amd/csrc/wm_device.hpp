@@ -98,6 +98,19 @@ template <typename T> __device__ __forceinline__ frag_t<T> zero_frag() {
   return v;
 }
 
+// Workgroups are dispatched round-robin over the chip's 8 XCDs (block i goes to
+// XCD i % 8), and each XCD has its own L2. Remap the linear block index so that
+// XCD x walks a contiguous share of the tile sequence: tiles that share
+// operands (the N tiles of one GEMM row block, the query tiles of one attention
+// head) stay on one L2, and every XCD gets an equal slice of a sequence whose
+// costs repeat (heavy and light causal tiles alike).
+constexpr int kNumXcd = 8;
+__device__ __forceinline__ int xcd_tile(int block, int total) {
+  const int x = block % kNumXcd, s = block / kNumXcd;
+  const int per = total / kNumXcd, rem = total % kNumXcd;
+  return x * per + min(x, rem) + s;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -36,16 +36,21 @@ template <typename T> struct GemmCfg {
 // ALoad: void operator()(int g, int row, int k, frag_t<T>* out) const  (FR consecutive frags)
 // BLoad: const T* operator()(int g, int o) const  -> row o of W_g (nullptr if o >= Nout)
 // Epi:   void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const
+// Launched on a 1-D grid of groups x row tiles x column tiles blocks; the tile
+// order is (group, row tile, column tile) and is spread over the XCDs so the
+// column tiles of a row block share one L2.
 template <typename T, class ALoad, class BLoad, class Epi>
-__global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, ALoad aload,
-                                                      BLoad bload, Epi epi) {
+__global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, int groups,
+                                                      ALoad aload, BLoad bload, Epi epi) {
   using C = GemmCfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM];
   T* stage0 = (T*)smem;
   float* Cs = (float*)smem;
 
-  const int g = blockIdx.z;
-  const int m0 = blockIdx.y * C::BM, n0 = blockIdx.x * C::BN;
+  const int nt = (Nout + C::BN - 1) / C::BN, mt = (M + C::BM - 1) / C::BM;
+  const int tile = xcd_tile(blockIdx.x, groups * mt * nt);
+  const int g = tile / (mt * nt);
+  const int m0 = (tile / nt % mt) * C::BM, n0 = (tile % nt) * C::BN;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = w >> 1, wn = w & 1, h = lane >> 5, r = lane & 31;
 

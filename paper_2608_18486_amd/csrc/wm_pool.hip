@@ -69,6 +69,10 @@ void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipS
                      ctx_len, sh.B, sh.T_new, sh.d, (double)sh.rope_theta, tab);
 }
 
+static unsigned gemm_blocks(int M, int Nout, int groups) {
+  return (unsigned)(groups * ((M + 127) / 128) * ((Nout + 127) / 128));
+}
+
 // -------------------------------------------------------- GEMM functors
 // Weight rows: W + g * group_stride + o * K (nullptr past Nout).
 template <typename T> struct WeightRows {
@@ -229,9 +233,8 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
   RouterA<T> a{H, rinv, g_pre, sel, sh.L, sh.D};
   WeightRows<T> w{W_alpha, (long)Nout * K, Nout, K};
   RouterEpi<T> e{logits, b_alpha, M, Nout};
-  dim3 grid((Nout + 127) / 128, (M + 127) / 128, 2);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, RouterA<T>, WeightRows<T>, RouterEpi<T>>), grid,
-                     dim3(256), 0, s, M, Nout, K, a, w, e);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, RouterA<T>, WeightRows<T>, RouterEpi<T>>),
+                     dim3(gemm_blocks(M, Nout, 2)), dim3(256), 0, s, M, Nout, K, 2, a, w, e);
 }
 
 // --------------------------------------------------------------------- mix
@@ -372,9 +375,9 @@ void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, c
   WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
   KVEpi<T> e{Kc, Vc, rinv_mid, g_knorm, rope_tab, ctx_len, M, Nout, sh.d, sh.T_new, sh.B,
              sh.Hkv, sh.S_cap, sh.k, sh.eps};
-  dim3 grid((Nout + 127) / 128, (M + 127) / 128, 2 * sh.k);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, KVEpi<T>>), grid,
-                     dim3(256), 0, s, M, Nout, K, a, w, e);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, KVEpi<T>>),
+                     dim3(gemm_blocks(M, Nout, 2 * sh.k)), dim3(256), 0, s, M, Nout, K, 2 * sh.k,
+                     a, w, e);
 }
 
 template <typename T>
@@ -387,9 +390,8 @@ void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g
   CopyRowsA<T> a{H, K, (long)sh.L * K};
   WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
   QEpi<T> e{Q, rinv, g_qnorm, rope_tab, M, Nout, sh.d, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
-  dim3 grid((Nout + 127) / 128, (M + 127) / 128, sh.L);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, QEpi<T>>), grid,
-                     dim3(256), 0, s, M, Nout, K, a, w, e);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, QEpi<T>>),
+                     dim3(gemm_blocks(M, Nout, sh.L)), dim3(256), 0, s, M, Nout, K, sh.L, a, w, e);
 }
 
 #define WM_INST(T)                                                                             \
