@@ -118,6 +118,18 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if ((N + 127) / 128 > 65535) return fail(WM_ERR_SHAPE, "B * T_new exceeds the grid limit");
   if ((long long)d.Hq * d.B * d.L > 65535 || (long long)d.Hkv * d.B * d.k > 65535)
     return fail(WM_ERR_SHAPE, "heads x sequences x layers exceeds the grid limit");
+  {
+    // tiles are read through 32-bit buffer views: every operand view must span < 2 GiB
+    const double es = (double)elem_size(d), lim = 2147483647.0;
+    const double views[] = {(double)N * d.L * d.D * es,            // H
+                            (double)N * d.D * es,                  // one mixed channel
+                            (double)d.S_cap * d.d * es,            // one cache slice
+                            (double)d.Hq * d.d * d.D * es,         // one Q projection
+                            (double)d.Hkv * d.d * d.D * es,        // one K/V projection
+                            (double)d.k * d.L * ((d.L + d.p - 1) / d.p) * d.D * es};  // router
+    for (double v : views)
+      if (v >= lim) return fail(WM_ERR_SHAPE, "an operand spans more than 2 GiB (%.0f B)", v);
+  }
   if (op == WM_OP_ROUTER_MIX || op == WM_OP_LAYER_STEP) {
     size_t lds = (size_t)d.L * d.D * elem_size(d) + 4 * (2 * (size_t)d.k * d.L + 4 * d.k);
     if (lds > 65536) return fail(WM_ERR_SHAPE, "L * D too large for the mix kernel (%zu B of LDS)", lds);

@@ -47,11 +47,14 @@ template <typename T> struct AttnArgs {
   LayerTable chan;
 };
 
-constexpr int kPrefillWaves = 8;  // waves per prefill workgroup
+#ifndef WM_PREFILL_WAVES
+#define WM_PREFILL_WAVES 8
+#endif
+constexpr int kPrefillWaves = WM_PREFILL_WAVES;  // waves per prefill workgroup
 
 template <typename T, int DH> struct PrefillCfg {
   static constexpr int NW = kPrefillWaves;
-  static constexpr int QT = 1;          // 32-query tiles per wave
+  static constexpr int QT = 256 / (32 * NW);  // 32-query tiles per wave (256 queries per block)
   static constexpr int NT = 64 * NW;    // threads
   static constexpr int BQ = 32 * QT * NW;  // queries per workgroup
   static constexpr int BKV = 64;        // keys per block
@@ -114,7 +117,7 @@ __device__ __forceinline__ void attend_block(
       float mx = st[qt][0];
 #pragma unroll
       for (int q = 1; q < 16; ++q) mx = fmaxf(mx, st[qt][q]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      mx = halves_max(mx);
       const bool grow = mx > m[qt] + thresh;
       if (__any(grow)) {
         const float mn = grow ? mx : m[qt];
@@ -201,7 +204,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
       for (int ks = 0; ks < C::NKS; ++ks)
 #pragma unroll
         for (int i = 0; i < 8; ++i) part += to_f32(qf[qt][ks][i]) * to_f32(kd[16 * ks + 8 * h + i]);
-      m[qt] = part + __shfl_xor(part, 32, 64);
+      m[qt] = halves_sum(part);
       lsum[qt] = h == 0 ? 1.f : 0.f;
 #pragma unroll
       for (int dt = 0; dt < C::NDT; ++dt)
@@ -227,20 +230,26 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
 
   // staged next block: K fragments (row-major copy) and V key pairs (transposed store)
   frag_t<T> kreg[C::KFR], vreg[C::VPT][2];
+  // the (channel, sequence, KV head) slice through buffer views: slots at or past kend
+  // read as zeros without a branch
+  const __amdgpu_buffer_rsrc_t kview = make_view(Kb, (uint32_t)a.S_cap * DH * sizeof(T));
+  const __amdgpu_buffer_rsrc_t vview = make_view(Vb, (uint32_t)a.S_cap * DH * sizeof(T));
+  auto slot_off = [&](int s, int col) {
+    return s < kend ? (uint32_t)(s * DH + col) * (uint32_t)sizeof(T) : kOffOob;
+  };
   auto fetch = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < C::KFR; ++i) {
-      int f = tid + C::NT * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8, s = k0 + key;
-      kreg[i] = f < C::KIT && s < kend ? ld_frag<T>(Kb + (long)s * DH + dc) : zero_frag<T>();
+      int f = tid + C::NT * i, key = f / (DH / 8), dc = (f % (DH / 8)) * 8;
+      kreg[i] = buf_frag<T>(kview, f < C::KIT ? slot_off(k0 + key, dc) : kOffOob);
     }
 #pragma unroll
     for (int i = 0; i < C::VPT; ++i) {
       int it = tid + C::NT * i;
-      if (it < C::VIT) {
-        int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2), s = k0 + 2 * kp;
-        vreg[i][0] = s < kend ? ld_frag<T>(Vb + (long)s * DH + 8 * dg) : zero_frag<T>();
-        vreg[i][1] = s + 1 < kend ? ld_frag<T>(Vb + (long)(s + 1) * DH + 8 * dg) : zero_frag<T>();
-      }
+      int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2), s = k0 + 2 * kp;
+      bool ok = it < C::VIT;
+      vreg[i][0] = buf_frag<T>(vview, ok ? slot_off(s, 8 * dg) : kOffOob);
+      vreg[i][1] = buf_frag<T>(vview, ok ? slot_off(s + 1, 8 * dg) : kOffOob);
     }
   };
   auto stage = [&](int buf) {
@@ -259,14 +268,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
     }
   };
 
-  if (nblk > 0) {
-    fetch(0);
-    stage(0);
-  }
+  // fetch and stage run unconditionally (a block past kend reads zeros and lands in the
+  // idle buffer), so the only branches in the loop are wave-uniform compute skips
+  fetch(0);
+  stage(0);
   __syncthreads();
   for (int j = 0; j < nblk; ++j) {
     const int k0 = j * C::BKV, buf = j & 1;
-    if (j + 1 < nblk) fetch(k0 + C::BKV);
+    fetch(k0 + C::BKV);
     if (k0 < wkend) {
       if (k0 + C::BKV > wfree)
         attend_block<T, DH, true>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
@@ -275,14 +284,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
         attend_block<T, DH, false>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
                                    h, r, cl2, thresh);
     }
-    if (j + 1 < nblk) stage(buf ^ 1);
+    stage(buf ^ 1);
     __syncthreads();
   }
 
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int qi = qw0 + 32 * qt + r;
-    const float lt = lsum[qt] + __shfl_xor(lsum[qt], 32, 64);
+    const float lt = halves_sum(lsum[qt]);
     if (qi >= a.T_new) continue;
     const float inv = 1.0f / lt;
     T* dst = a.O + ((((long)l * a.B + b) * a.T_new + qi) * a.Hq + hq) * DH;

@@ -98,6 +98,33 @@ template <typename T> __device__ __forceinline__ frag_t<T> zero_frag() {
   return v;
 }
 
+// Buffer loads through a resource descriptor: an offset at or past the
+// descriptor's range returns zeros, so guarded tile loads need no branch (and
+// the compiler keeps exact wait counts for loads still in flight). Every view
+// spans less than 2 GiB (checked on the host); kOffOob is past any such range.
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+constexpr uint32_t kOffOob = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_view(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+__device__ __forceinline__ i32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+// One operand fragment (8 elements) at byte offset off.
+template <typename T> __device__ __forceinline__ frag_t<T> buf_frag(__amdgpu_buffer_rsrc_t r,
+                                                                    uint32_t off);
+template <> __device__ __forceinline__ bf16x8 buf_frag<bf16>(__amdgpu_buffer_rsrc_t r,
+                                                             uint32_t off) {
+  return __builtin_bit_cast(bf16x8, buf_ld16(r, off));
+}
+template <> __device__ __forceinline__ f32x8 buf_frag<float>(__amdgpu_buffer_rsrc_t r,
+                                                             uint32_t off) {
+  f32x4 a = __builtin_bit_cast(f32x4, buf_ld16(r, off));
+  f32x4 b = __builtin_bit_cast(f32x4, buf_ld16(r, off + 16));
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // Workgroups are dispatched round-robin over the chip's 8 XCDs (block i goes to
 // XCD i % 8), and each XCD has its own L2. Remap the linear block index so that
 // XCD x walks a contiguous share of the tile sequence: tiles that share
@@ -109,6 +136,17 @@ __device__ __forceinline__ int xcd_tile(int block, int total) {
   const int x = block % kNumXcd, s = block / kNumXcd;
   const int per = total / kNumXcd, rem = total % kNumXcd;
   return x * per + min(x, rem) + s;
+}
+
+// Combine a value with the same lane of the other half-wave (lane i with i ^ 32)
+// through v_permlane32_swap, without a trip through LDS.
+__device__ __forceinline__ float halves_max(float v) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float v) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

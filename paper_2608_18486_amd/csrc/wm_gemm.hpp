@@ -13,11 +13,17 @@
 // in a 2 x 2 grid, each wave owning 64 x 64 = 2 x 2 MFMA 32x32 tiles. LDS is
 // double-buffered: the next K slice is fetched into registers while the
 // current one is multiplied, then stored to the other buffer, with one
-// barrier per K slice.
+// barrier per K slice. A ring of PIPE register stages keeps the global loads of
+// later slices in flight while the current one is multiplied.
 #pragma once
 #include "wm_device.hpp"
 
 namespace wm {
+
+// A group's weight matrix [Nout][K] seen through a buffer resource.
+template <typename T> struct WeightView {
+  __amdgpu_buffer_rsrc_t rsrc;
+};
 
 template <typename T> struct GemmCfg {
   static constexpr int BM = 128, BN = 128;
@@ -31,10 +37,13 @@ template <typename T> struct GemmCfg {
   static constexpr int AB_BYTES = 2 * STAGE * (int)sizeof(T);
   static constexpr int C_BYTES = BM * LDC * 4;
   static constexpr int SMEM = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
+  static constexpr int PIPE = 3;                       // K slices held in registers
 };
 
-// ALoad: void operator()(int g, int row, int k, frag_t<T>* out) const  (FR consecutive frags)
-// BLoad: const T* operator()(int g, int o) const  -> row o of W_g (nullptr if o >= Nout)
+// ALoad: State begin(int g) const;
+//        void load(const State&, int row, int k, bool ok, frag_t<T>* out) const
+//          (FR consecutive frags of row `row` from column k; zeros when !ok)
+// BLoad: WeightView<T> view(int g) const  -> the group's [Nout][K] weights
 // Epi:   void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const
 // Launched on a 1-D grid of groups x row tiles x column tiles blocks; the tile
 // order is (group, row tile, column tile) and is spread over the XCDs so the
@@ -57,7 +66,10 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, in
   // each thread moves FR consecutive fragments of one A row and one B row per slice
   const int lrow = tid / C::TPR, lk = (tid % C::TPR) * 8 * C::FR;
   const bool arow_ok = m0 + lrow < M;
-  const T* brow = bload(g, n0 + lrow);
+  const auto ast = aload.begin(g);
+  const auto wv = bload.view(g);
+  const bool brow_ok = n0 + lrow < Nout;
+  const uint32_t brow_off = (uint32_t)((n0 + lrow) * K) * (uint32_t)sizeof(T);
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -65,36 +77,27 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, in
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
 
-  frag_t<T> av[C::FR], bv[C::FR];
-  auto fetch = [&](int k0) {
+  // K slices in flight: slice kb + P is fetched while slice kb is multiplied, so each
+  // slice's global loads have P - 1 slices of matrix-core work to land.
+  constexpr int P = C::PIPE;
+  frag_t<T> av[P][C::FR], bv[P][C::FR];
+  auto fetch = [&](int k0, frag_t<T>* a_out, frag_t<T>* b_out) {
     const bool kin = k0 + lk < K;  // the thread's chunk lies wholly inside or outside K
-    if (arow_ok && kin) {
-      aload(g, m0 + lrow, k0 + lk, av);
-    } else {
+    aload.load(ast, m0 + lrow, k0 + lk, arow_ok && kin, a_out);
+    const uint32_t off = brow_ok && kin ? brow_off + (uint32_t)(k0 + lk) * sizeof(T) : kOffOob;
 #pragma unroll
-      for (int i = 0; i < C::FR; ++i) av[i] = zero_frag<T>();
-    }
-#pragma unroll
-    for (int i = 0; i < C::FR; ++i)
-      bv[i] = brow && kin ? ld_frag<T>(brow + k0 + lk + 8 * i) : zero_frag<T>();
+    for (int i = 0; i < C::FR; ++i) b_out[i] = buf_frag<T>(wv.rsrc, off + 8 * i * sizeof(T));
   };
-  auto stage = [&](int buf) {
+  auto stage = [&](int buf, const frag_t<T>* a_in, const frag_t<T>* b_in) {
     T* As = stage0 + buf * C::STAGE;
     T* Bs = As + C::BM * C::LDA;
 #pragma unroll
     for (int i = 0; i < C::FR; ++i) {
-      st_frag<T>(As + lrow * C::LDA + lk + 8 * i, av[i]);
-      st_frag<T>(Bs + lrow * C::LDA + lk + 8 * i, bv[i]);
+      st_frag<T>(As + lrow * C::LDA + lk + 8 * i, a_in[i]);
+      st_frag<T>(Bs + lrow * C::LDA + lk + 8 * i, b_in[i]);
     }
   };
-
-  const int nk = (K + C::BK - 1) / C::BK;
-  fetch(0);
-  stage(0);
-  __syncthreads();
-  for (int kb = 0; kb < nk; ++kb) {
-    const int buf = kb & 1;
-    if (kb + 1 < nk) fetch((kb + 1) * C::BK);
+  auto compute = [&](int buf) {
     const T* As = stage0 + buf * C::STAGE;
     const T* Bs = As + C::BM * C::LDA;
 #pragma unroll
@@ -111,8 +114,26 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, in
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = mma32(acc[i][j], a[i], b[j]);
     }
-    if (kb + 1 < nk) stage(buf ^ 1);
-    __syncthreads();
+  };
+
+  // The slice count is padded to a multiple of P; padded slices read zeros through the
+  // out-of-range offset, so the loop body has no branch and every load's wait count
+  // stays exact.
+  const int nk = (K + C::BK - 1) / C::BK;
+  const int nkp = (nk + P - 1) / P * P;
+#pragma unroll
+  for (int u = 0; u < P; ++u) fetch(u * C::BK, av[u], bv[u]);
+  stage(0, av[0], bv[0]);
+  __syncthreads();
+  for (int kb0 = 0; kb0 < nkp; kb0 += P) {
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      const int kb = kb0 + u;  // slot u held slice kb, already staged into buffer kb & 1
+      fetch((kb + P) * C::BK, av[u], bv[u]);
+      compute(kb & 1);
+      stage((kb + 1) & 1, av[(u + 1) % P], bv[(u + 1) % P]);
+      __syncthreads();
+    }
   }
 #pragma unroll
   for (int i = 0; i < 2; ++i)

@@ -74,47 +74,60 @@ static unsigned gemm_blocks(int M, int Nout, int groups) {
 }
 
 // -------------------------------------------------------- GEMM functors
-// Weight rows: W + g * group_stride + o * K (nullptr past Nout).
+// Weight matrices W + g * group_stride, [Nout][K] each.
 template <typename T> struct WeightRows {
   const T* W;
   long group_stride;
   int Nout, K;
-  __device__ const T* operator()(int g, int o) const {
-    return o < Nout ? W + (long)g * group_stride + (long)o * K : nullptr;
+  __device__ WeightView<T> view(int g) const {
+    return {make_view(W + (long)g * group_stride, (uint32_t)((long)Nout * K * sizeof(T)))};
   }
 };
 
 // Router operand: the stacked normed states xi (gain and 1/RMS applied, one rounding).
+// Rows past M read zeros (their 1/RMS index is clamped to a valid row).
 template <typename T> struct RouterA {
   const T* H;
   const float* rinv;
   const T* g_pre;
   LayerTable sel;
-  int L, D;
-  __device__ void operator()(int br, int n, int k, frag_t<T>* out) const {
-    int m = k / D, e = k - m * D, layer = sel.v[m];
-    const T* x = H + ((long)n * L + layer) * D + e;
-    const T* g = g_pre + ((long)br * L + layer) * D + e;
-    float rs = rinv[(long)n * L + layer];
+  int L, D, M;
+  struct State {
+    __amdgpu_buffer_rsrc_t h;
+    const T* g;
+  };
+  __device__ State begin(int br) const {
+    return {make_view(H, (uint32_t)((long)M * L * D * sizeof(T))), g_pre + (long)br * L * D};
+  }
+  __device__ void load(const State& st, int n, int k, bool ok, frag_t<T>* out) const {
+    const int m = k / D, e = k - m * D, layer = sel.v[m];
+    const uint32_t off = ok ? (uint32_t)(((long)n * L + layer) * D + e) * sizeof(T) : kOffOob;
+    const T* g = st.g + (long)layer * D + e;
+    const float rs = rinv[(long)min(n, M - 1) * L + layer];
 #pragma unroll
     for (int f = 0; f < GemmCfg<T>::FR; ++f) {
-      float xv[8], gv[8];
-      load8(x + 8 * f, xv);
+      frag_t<T> x = buf_frag<T>(st.h, off + 8 * f * sizeof(T));
+      float gv[8];
       load8(g + 8 * f, gv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) out[f][i] = from_f32<T>(xv[i] * gv[i] * rs);
+      for (int i = 0; i < 8; ++i) out[f][i] = from_f32<T>(to_f32(x[i]) * gv[i] * rs);
     }
   }
 };
 
-// Plain operand rows: X[g * gstride + row * rstride + k] (scales live elsewhere).
+// Plain operand rows: X[g * gstride + row * rstride + k] for rows < M (scales live elsewhere).
 template <typename T> struct CopyRowsA {
   const T* X;
   long gstride, rstride;
-  __device__ void operator()(int g, int row, int k, frag_t<T>* out) const {
-    const T* x = X + (long)g * gstride + (long)row * rstride + k;
+  int M;
+  __device__ __amdgpu_buffer_rsrc_t begin(int g) const {
+    return make_view(X + (long)g * gstride, (uint32_t)((long)M * rstride * sizeof(T)));
+  }
+  __device__ void load(const __amdgpu_buffer_rsrc_t& r, int row, int k, bool ok,
+                       frag_t<T>* out) const {
+    const uint32_t off = ok ? (uint32_t)((long)row * rstride + k) * sizeof(T) : kOffOob;
 #pragma unroll
-    for (int f = 0; f < GemmCfg<T>::FR; ++f) out[f] = ld_frag<T>(x + 8 * f);
+    for (int f = 0; f < GemmCfg<T>::FR; ++f) out[f] = buf_frag<T>(r, off + 8 * f * sizeof(T));
   }
 };
 
@@ -230,7 +243,7 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
                    hipStream_t s) {
   int M = sh.N(), Nout = sh.k * sh.L, K = sh.Lp * sh.D;
   if (M <= 0) return;
-  RouterA<T> a{H, rinv, g_pre, sel, sh.L, sh.D};
+  RouterA<T> a{H, rinv, g_pre, sel, sh.L, sh.D, M};
   WeightRows<T> w{W_alpha, (long)Nout * K, Nout, K};
   RouterEpi<T> e{logits, b_alpha, M, Nout};
   hipLaunchKernelGGL((gemm_nt_kernel<T, RouterA<T>, WeightRows<T>, RouterEpi<T>>),
@@ -371,7 +384,7 @@ void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, c
   int M = sh.N(), Nout = sh.Hkv * sh.d, K = sh.D;
   if (M <= 0) return;
   fold_gain<T>(Wk, Wv, sh.k, g_mid, wfold, 2 * sh.k, Nout, K, s);
-  CopyRowsA<T> a{mixed, (long)M * K, K};
+  CopyRowsA<T> a{mixed, (long)M * K, K, M};
   WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
   KVEpi<T> e{Kc, Vc, rinv_mid, g_knorm, rope_tab, ctx_len, M, Nout, sh.d, sh.T_new, sh.B,
              sh.Hkv, sh.S_cap, sh.k, sh.eps};
@@ -387,7 +400,7 @@ void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g
   int M = sh.N(), Nout = sh.Hq * sh.d, K = sh.D;
   if (M <= 0) return;
   fold_gain<T>(Wq, Wq, sh.L, g_in, wfold, sh.L, Nout, K, s);
-  CopyRowsA<T> a{H, K, (long)sh.L * K};
+  CopyRowsA<T> a{H, K, (long)sh.L * K, M};
   WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
   QEpi<T> e{Q, rinv, g_qnorm, rope_tab, M, Nout, sh.d, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
   hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, QEpi<T>>),
