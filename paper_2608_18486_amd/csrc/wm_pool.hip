@@ -147,41 +147,65 @@ template <typename T> struct RouterEpi {
   }
 };
 
-// One head row of a GEMM result (times the row scale sc): RMS over d, gain, RoPE with the
-// per-token (cos, sin) table, store.
-template <typename T>
-__device__ __forceinline__ void head_norm_rope_store(const float* c, float sc, T* dst,
-                                                     const T* gain, const float* tab, int d,
-                                                     float eps) {
-  float ss = 0.f;
-  for (int e = 0; e < d; e += 4) {
-    f32x4 v = *(const f32x4*)(c + e) * sc;
-    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
-  }
-  float rs = sc / sqrtf(ss / (float)d + eps);
-  int half = d / 2;
-  for (int m = 0; m < half; m += 4) {
-    f32x4 x1 = *(const f32x4*)(c + m), x2 = *(const f32x4*)(c + m + half);
-    float y1[4], y2[4];
+// Head-wise epilogue shared by the K/V and Q projections. A C tile row holds
+// 128 / d heads; d / 8 consecutive lanes own one (row, head) item, 8 contiguous
+// elements each, so a lane group reads its row from LDS without bank conflicts
+// and writes the whole d-element head row (one 128-B line for d = 64) at once.
+// Per item: scale by the row's 1/RMS, then either store (V) or RMS-normalise
+// over the head, apply the gain and rotate the pairs (m, m + d/2) (K, Q); the
+// partner of element m lives d/16 lanes away.
+template <typename T, int DH> struct HeadItems {
+  static constexpr int LPI = DH / 8;          // lanes per item
+  static constexpr int IPP = 256 / LPI;       // items per pass of 256 threads
+  static constexpr int ITEMS = 128 * (128 / DH);
+};
+
+template <int LPI>
+__device__ __forceinline__ float group_sum(float v) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float a = x1[i] * rs * to_f32(gain[m + i]);
-      float b = x2[i] * rs * to_f32(gain[m + half + i]);
-      float cs = tab[2 * (m + i)], sn = tab[2 * (m + i) + 1];
-      y1[i] = a * cs - b * sn;
-      y2[i] = b * cs + a * sn;
-    }
-    store4(dst + m, y1);
-    store4(dst + m + half, y2);
-  }
+  for (int x = 1; x < LPI; x <<= 1) v += __shfl_xor(v, x, 64);
+  return v;
 }
 
-template <typename T>
-__device__ __forceinline__ void head_store(const float* c, float sc, T* dst, int d) {
-  for (int e = 0; e < d; e += 4) {
-    f32x4 v = *(const f32x4*)(c + e) * sc;
-    float y[4] = {v[0], v[1], v[2], v[3]};
-    store4(dst + e, y);
+// c: this lane's 8 fp32 values; sc: row scale; normalise+rotate when gain != nullptr.
+template <typename T, int DH>
+__device__ __forceinline__ void head_chunk(float* c, float sc, const T* gain, const float* tabrow,
+                                           int lane_c, float eps, T* dst) {
+  constexpr int LPI = DH / 8;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) c[i] *= sc;
+  if (gain) {
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += c[i] * c[i];
+    ss = group_sum<LPI>(ss);
+    const float rs = 1.0f / sqrtf(ss / (float)DH + eps);
+    float gv[8];
+    load8(gain + 8 * lane_c, gv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) c[i] *= rs * gv[i];
+    // pair (m, m + DH/2): lanes c < LPI/2 hold m, lanes c >= LPI/2 hold m + DH/2
+    const bool lo = lane_c < LPI / 2;
+    const int mc = lo ? lane_c : lane_c - LPI / 2;  // which 8 pairs
+    float cs[8], sn[8];
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+      f32x4 t = *(const f32x4*)(tabrow + 2 * (8 * mc + i));
+      cs[i] = t[0];
+      sn[i] = t[1];
+      cs[i + 1] = t[2];
+      sn[i + 1] = t[3];
+    }
+    float y[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float other = __shfl_xor(c[i], LPI / 2, 64);
+      // lo: x1 = c, x2 = other -> x1 cos - x2 sin;  hi: x2 = c, x1 = other -> x2 cos + x1 sin
+      y[i] = lo ? c[i] * cs[i] - other * sn[i] : c[i] * cs[i] + other * sn[i];
+    }
+    store8(dst, y);
+  } else {
+    store8(dst, c);
   }
 }
 
@@ -193,25 +217,31 @@ template <typename T> struct KVEpi {
   const int32_t* ctx_len;
   int M, Nout, d, T_new, B, Hkv, S_cap, k;
   float eps;
-  __device__ void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const {
-    int br = g / k, j = g - br * k;
-    int hpt = 128 / d;
-    for (int it = tid; it < 128 * hpt; it += 256) {
-      int row = it & 127, hh = it >> 7;
-      int n = m0 + row, col0 = n0 + hh * d;
+  template <int DH>
+  __device__ void run(int g, int m0, int n0, const float* C, int ldc, int tid) const {
+    using HI = HeadItems<T, DH>;
+    const int br = g / k, j = g - br * k;
+    const int lane_c = tid % HI::LPI;
+    for (int it = tid / HI::LPI; it < HI::ITEMS; it += HI::IPP) {
+      const int row = it & 127, hh = it >> 7;
+      const int n = m0 + row, col0 = n0 + hh * DH;
       if (n >= M || col0 >= Nout) continue;
-      int b = n / T_new, i = n - b * T_new;
-      long slot = (long)(ctx_len ? ctx_len[b] : 0) + i;
+      const int b = n / T_new, i = n - b * T_new;
+      const long slot = (long)(ctx_len ? ctx_len[b] : 0) + i;
       if (slot < 0 || slot >= S_cap) continue;
-      int head = col0 / d;
-      long off = ((((long)j * B + b) * Hkv + head) * S_cap + slot) * d;
-      const float* c = C + row * ldc + hh * d;
-      const float sc = rs[(long)g * M + n];
-      if (br == 0)
-        head_norm_rope_store(c, sc, Kc + off, g_knorm + (long)j * d, tab + (long)n * d, d, eps);
-      else
-        head_store(c, sc, Vc + off, d);
+      const int head = col0 / DH;
+      const long off = ((((long)j * B + b) * Hkv + head) * S_cap + slot) * DH + 8 * lane_c;
+      float c[8];
+      const float* src = C + row * ldc + hh * DH + 8 * lane_c;
+      *(f32x4*)c = *(const f32x4*)src;
+      *(f32x4*)(c + 4) = *(const f32x4*)(src + 4);
+      head_chunk<T, DH>(c, rs[(long)g * M + n], br == 0 ? g_knorm + (long)j * DH : nullptr,
+                        tab + (long)n * DH, lane_c, eps, (br == 0 ? Kc : Vc) + off);
     }
+  }
+  __device__ void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const {
+    if (d == 64) run<64>(g, m0, n0, C, ldc, tid);
+    else run<32>(g, m0, n0, C, ldc, tid);
   }
 };
 
@@ -222,17 +252,27 @@ template <typename T> struct QEpi {
   const float* tab;
   int M, Nout, d, T_new, B, Hq, L;
   float eps;
-  __device__ void operator()(int l, int m0, int n0, const float* C, int ldc, int tid) const {
-    int hpt = 128 / d;
-    for (int it = tid; it < 128 * hpt; it += 256) {
-      int row = it & 127, hh = it >> 7;
-      int n = m0 + row, col0 = n0 + hh * d;
+  template <int DH>
+  __device__ void run(int l, int m0, int n0, const float* C, int ldc, int tid) const {
+    using HI = HeadItems<T, DH>;
+    const int lane_c = tid % HI::LPI;
+    for (int it = tid / HI::LPI; it < HI::ITEMS; it += HI::IPP) {
+      const int row = it & 127, hh = it >> 7;
+      const int n = m0 + row, col0 = n0 + hh * DH;
       if (n >= M || col0 >= Nout) continue;
-      int b = n / T_new, i = n - b * T_new, head = col0 / d;
-      long off = ((((long)l * B + b) * Hq + head) * T_new + i) * d;
-      head_norm_rope_store(C + row * ldc + hh * d, rs[(long)n * L + l], Q + off,
-                           g_qnorm + (long)l * d, tab + (long)n * d, d, eps);
+      const int b = n / T_new, i = n - b * T_new, head = col0 / DH;
+      const long off = ((((long)l * B + b) * Hq + head) * T_new + i) * DH + 8 * lane_c;
+      float c[8];
+      const float* src = C + row * ldc + hh * DH + 8 * lane_c;
+      *(f32x4*)c = *(const f32x4*)src;
+      *(f32x4*)(c + 4) = *(const f32x4*)(src + 4);
+      head_chunk<T, DH>(c, rs[(long)n * L + l], g_qnorm + (long)l * DH, tab + (long)n * DH,
+                        lane_c, eps, Q + off);
     }
+  }
+  __device__ void operator()(int l, int m0, int n0, const float* C, int ldc, int tid) const {
+    if (d == 64) run<64>(l, m0, n0, C, ldc, tid);
+    else run<32>(l, m0, n0, C, ldc, tid);
   }
 };
 
