@@ -131,7 +131,7 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
       if (v >= lim) return fail(WM_ERR_SHAPE, "an operand spans more than 2 GiB (%.0f B)", v);
   }
   if (op == WM_OP_ROUTER_MIX || op == WM_OP_LAYER_STEP) {
-    size_t lds = (size_t)d.L * d.D * elem_size(d) + 4 * (2 * (size_t)d.k * d.L + 4 * d.k);
+    size_t lds = wm::mix_smem_bytes(d.L, d.k, d.D, elem_size(d));
     if (lds > 65536) return fail(WM_ERR_SHAPE, "L * D too large for the mix kernel (%zu B of LDS)", lds);
   }
   if (chan_map) {

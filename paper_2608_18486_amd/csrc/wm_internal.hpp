@@ -40,6 +40,7 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
                    hipStream_t s);
 
 // alpha (in: logits [2][N][k*L], out: mixing weights) -> mixed[2][k][N][D], rinv_mid[2][k][N]
+size_t mix_smem_bytes(int L, int k, int D, size_t elem_bytes);
 template <typename T>
 void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
                 T* mixed, float* rinv_mid, hipStream_t s);

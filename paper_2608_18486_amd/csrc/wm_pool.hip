@@ -291,23 +291,30 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
 }
 
 // --------------------------------------------------------------------- mix
-// One block per token. LDS holds the token's L states and the 2 x k x L
-// coefficients alpha[j][l] / RMS(h_l); each thread owns 8 consecutive columns.
-template <typename T>
-__global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* H, const float* rinv,
-                                                  const T* g_pre, float* alpha, T* mixed,
-                                                  float* rinv_mid) {
+// One block per token; each thread owns 8 consecutive columns. LDS holds the
+// token's L states and the coefficients alpha[j][l] / RMS(h_l), stored layer-
+// major with the channel count padded to JC (zeros), so a thread reads JC
+// coefficients of one layer with JC/4 broadcast loads. For each branch the
+// thread scales a layer's 8 columns by the gain once and accumulates them into
+// all JC channels, then stores the channels and their sums of squares.
+template <typename T, int JC>
+__global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* __restrict__ H,
+                                                  const float* __restrict__ rinv,
+                                                  const T* __restrict__ g_pre, float* alpha,
+                                                  T* __restrict__ mixed, float* rinv_mid) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int L = sh.L, k = sh.k, D = sh.D, N = sh.N();
+  const int kp = (k + JC - 1) / JC * JC;  // padded channel count
   const long n = blockIdx.x;
   T* hs = (T*)smem;
-  float* coef = (float*)(smem + (size_t)L * D * sizeof(T));
-  float* part = coef + 2 * k * L;  // [2 waves][2k]
+  float* coef = (float*)(smem + ((size_t)L * D * sizeof(T) + 15) / 16 * 16);  // [2][L][kp]
+  float* part = coef + 2 * L * kp;                                             // [2 waves][2k]
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
 
   const T* hsrc = H + n * L * D;
   for (int e = tid * 8; e < L * D; e += 128 * 8) st_frag<T>(hs + e, ld_frag<T>(hsrc + e));
-
+  for (int e = tid; e < 2 * L * kp; e += 128) coef[e] = 0.f;
+  __syncthreads();
   if (tid < 2 * k) {
     int br = tid / k, j = tid - br * k;
     float* row = alpha + ((long)br * N + n) * k * L + (long)j * L;
@@ -319,34 +326,40 @@ __global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* H, const fl
       float iz = 1.0f / z;
       for (int l = 0; l < L; ++l) row[l] = expf(row[l] - mx) * iz;
     }
-    for (int l = 0; l < L; ++l) coef[(br * k + j) * L + l] = row[l] * rinv[n * L + l];
+    for (int l = 0; l < L; ++l) coef[((long)br * L + l) * kp + j] = row[l] * rinv[n * L + l];
   }
   __syncthreads();
 
-  constexpr int JC = 4;
   const int ncg = D / 8;
   for (int br = 0; br < 2; ++br) {
     for (int j0 = 0; j0 < k; j0 += JC) {
-      float ss[JC] = {0.f, 0.f, 0.f, 0.f};
+      float ss[JC];
+#pragma unroll
+      for (int jj = 0; jj < JC; ++jj) ss[jj] = 0.f;
       for (int cg = tid; cg < ncg; cg += 128) {
         float acc[JC][8];
 #pragma unroll
         for (int jj = 0; jj < JC; ++jj)
 #pragma unroll
           for (int i = 0; i < 8; ++i) acc[jj][i] = 0.f;
+        // the next layer's gains are fetched one layer ahead (clamped, so unconditionally)
+        const T* gbase = g_pre + (long)br * L * D + cg * 8;
+        frag_t<T> gnext = ld_frag<T>(gbase);
         for (int l = 0; l < L; ++l) {
-          float xv[8], gv[8];
+          const frag_t<T> gcur = gnext;
+          gnext = ld_frag<T>(gbase + (long)min(l + 1, L - 1) * D);
+          float xv[8];
           load8(hs + l * D + cg * 8, xv);
-          load8(g_pre + ((long)br * L + l) * D + cg * 8, gv);
 #pragma unroll
-          for (int i = 0; i < 8; ++i) xv[i] *= gv[i];
+          for (int i = 0; i < 8; ++i) xv[i] *= to_f32(gcur[i]);
+          const float* cl = coef + ((long)br * L + l) * kp + j0;
 #pragma unroll
-          for (int jj = 0; jj < JC; ++jj) {
-            if (j0 + jj < k) {
-              float c = coef[(br * k + j0 + jj) * L + l];
+          for (int jq = 0; jq < JC; jq += 4) {
+            f32x4 c4 = *(const f32x4*)(cl + jq);
 #pragma unroll
-              for (int i = 0; i < 8; ++i) acc[jj][i] += c * xv[i];
-            }
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+              for (int i = 0; i < 8; ++i) acc[jq + t][i] += c4[t] * xv[i];
           }
         }
 #pragma unroll
@@ -373,13 +386,25 @@ __global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* H, const fl
   }
 }
 
+static int mix_chunk(int k) { return k <= 4 ? 4 : k <= 8 ? 8 : k <= 12 ? 12 : 16; }
+
+size_t mix_smem_bytes(int L, int k, int D, size_t es) {
+  int jc = mix_chunk(k), kp = (k + jc - 1) / jc * jc;
+  return ((size_t)L * D * es + 15) / 16 * 16 + sizeof(float) * (2 * (size_t)L * kp + 4 * k);
+}
+
 template <typename T>
 void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
                 T* mixed, float* rinv_mid, hipStream_t s) {
   if (sh.N() <= 0) return;
-  size_t smem = (size_t)sh.L * sh.D * sizeof(T) + sizeof(float) * (2 * sh.k * sh.L + 4 * sh.k);
-  hipLaunchKernelGGL(mix_kernel<T>, dim3(sh.N()), dim3(128), smem, s, sh, H, rinv, g_pre, alpha,
-                     mixed, rinv_mid);
+  size_t smem = mix_smem_bytes(sh.L, sh.k, sh.D, sizeof(T));
+  dim3 grid(sh.N()), block(128);
+  switch (mix_chunk(sh.k)) {
+    case 4: hipLaunchKernelGGL((mix_kernel<T, 4>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, mixed, rinv_mid); break;
+    case 8: hipLaunchKernelGGL((mix_kernel<T, 8>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, mixed, rinv_mid); break;
+    case 12: hipLaunchKernelGGL((mix_kernel<T, 12>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, mixed, rinv_mid); break;
+    default: hipLaunchKernelGGL((mix_kernel<T, 16>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, mixed, rinv_mid); break;
+  }
 }
 
 // ------------------------------------------------------------- projections
