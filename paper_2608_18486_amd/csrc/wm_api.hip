@@ -32,7 +32,7 @@ bool decode_path(const wm_dims& d) { return d.T_new <= 4; }
 
 struct Layout {
   size_t rinv = 0, alpha = 0, mixed = 0, rinv_mid = 0, tab = 0, q = 0, part = 0, wkv = 0, wq = 0,
-         total = 0;
+         wa = 0, rpart = 0, total = 0;
 };
 
 wm::Shape make_shape(const wm_dims& d) {
@@ -78,6 +78,10 @@ Layout layout(const wm_dims& d, int op) {
     Ly.part = take(wm::decode_partials_bytes(make_shape(d)));
   if (op == WM_OP_KV_PROJECT || all) Ly.wkv = take(wm::kv_fold_elems(make_shape(d)) * es);
   if (op == WM_OP_Q_PROJECT || all) Ly.wq = take(wm::q_fold_elems(make_shape(d)) * es);
+  if (op == WM_OP_ROUTER_MIX || all) {
+    Ly.wa = take(wm::router_fold_elems(make_shape(d)) * es);
+    Ly.rpart = take(wm::router_partials_bytes(make_shape(d)));
+  }
   Ly.total = N == 0 ? 0 : off;
   return Ly;
 }
@@ -126,7 +130,7 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
                             (double)d.S_cap * d.d * es,            // one cache slice
                             (double)d.Hq * d.d * d.D * es,         // one Q projection
                             (double)d.Hkv * d.d * d.D * es,        // one K/V projection
-                            (double)d.k * d.L * ((d.L + d.p - 1) / d.p) * d.D * es};  // router
+                            2.0 * d.k * d.L * ((d.L + d.p - 1) / d.p) * d.D * es};  // router
     for (double v : views)
       if (v >= lim) return fail(WM_ERR_SHAPE, "an operand spans more than 2 GiB (%.0f B)", v);
   }
@@ -200,7 +204,8 @@ void run_router_mix(const wm_dims& d, const wm_params& P, const T* H, float* alp
   float* alpha = alpha_out ? alpha_out : (float*)at(ws, Ly.alpha);
   wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
   wm::launch_router<T>(sh, router_layers(d), H, rinv, (const T*)P.g_pre, (const T*)P.W_alpha,
-                       (const T*)P.b_alpha, alpha, s);
+                       (const T*)P.b_alpha, alpha, (T*)at(ws, Ly.wa), (float*)at(ws, Ly.rpart),
+                       s);
   wm::launch_mix<T>(sh, H, rinv, (const T*)P.g_pre, alpha, mixed, (float*)at(ws, Ly.rinv_mid), s);
 }
 
@@ -264,7 +269,8 @@ void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int3
   wm::launch_rope_table(sh, ctx_len, tab, s);
   mark(1);
   wm::launch_router<T>(sh, router_layers(d), H, rinv, (const T*)P.g_pre, (const T*)P.W_alpha,
-                       (const T*)P.b_alpha, alpha, s);
+                       (const T*)P.b_alpha, alpha, (T*)at(ws, Ly.wa), (float*)at(ws, Ly.rpart),
+                       s);
   mark(2);
   wm::launch_mix<T>(sh, H, rinv, (const T*)P.g_pre, alpha, mixed, rinv_mid, s);
   mark(3);

@@ -1,152 +1,172 @@
-// Grouped "NT" GEMM on the matrix cores: C_g[m][o] = sum_k A_g[m][k] * W_g[o][k].
-// Both operands are K-contiguous (activations row-major, weights [out][in]),
-// which is how the router, the per-channel K/V projections and the per-layer
-// Q projections store them. blockIdx.z selects the group g.
+// Grouped projection GEMM on the matrix cores, computed transposed:
+//   C_g^T[o][n] = sum_k W_g[o][k] * X_g[n][k]
+// W_g is a group's weight matrix [Nout][K] and X_g its activations (one row of
+// K per token), both K-contiguous. Computing C^T puts one token in each lane of
+// an MFMA result: lane (h, r) of a 32x32 block holds token r and output channels
+// 8*(q/4) + 4h + q%4, q = 0..15. A head of d channels therefore lives in one
+// token's lane pair (h = 0, 1): its RMS norm needs a single cross-half swap,
+// the rotate-half RoPE pairs (m, m + d/2) sit in the same lane, and 4
+// consecutive channels leave as one vector store. The epilogue runs on the
+// accumulators in registers; there is no C tile in LDS.
 //
-// An ALoad functor produces the A operand fragments (a plain copy, or the
-// router's normed states), a BLoad functor points at weight rows, and an Epi
-// functor consumes the fp32 C tile from LDS (bias, row scale, per-head norm,
-// RoPE, cache store ...).
-//
-// K must be a multiple of 32; a last half slice (bf16) is zero-filled.
-// Tile 128 x 128 x BK (BK = 64 for bf16, 32 for fp32), 256 threads = 4 waves
-// in a 2 x 2 grid, each wave owning 64 x 64 = 2 x 2 MFMA 32x32 tiles. LDS is
-// double-buffered: the next K slice is fetched into registers while the
-// current one is multiplied, then stored to the other buffer, with one
-// barrier per K slice. A ring of PIPE register stages keeps the global loads of
-// later slices in flight while the current one is multiplied.
+// Macro tile OT x NTOK (channels x tokens) = (32 WO WGO) x (32 WN WGN) with
+// WGO x WGN waves, each owning WO x WN blocks of 32 x 32. Per K slice of BK the
+// W and X tiles are fetched into registers PIPE slices ahead (buffer loads:
+// rows past the matrix and padded slices read zeros, so the loop has no
+// divergent branch and keeps exact wait counts), stored to the other half of a
+// double-buffered LDS stage, and multiplied with one barrier per slice.
 #pragma once
 #include "wm_device.hpp"
 
 namespace wm {
 
-// A group's weight matrix [Nout][K] seen through a buffer resource.
-template <typename T> struct WeightView {
+template <typename T, int BK_, int WGO_, int WGN_, int WO_, int WN_> struct ProjCfg {
+  static constexpr int BK = BK_, WGO = WGO_, WGN = WGN_, WO = WO_, WN = WN_;
+  static constexpr int NT = 64 * WGO * WGN;                 // threads
+  static constexpr int OT = 32 * WO * WGO, NTOK = 32 * WN * WGN;
+  static constexpr int PAD = sizeof(T) == 2 ? 8 : 4;         // keeps 16-B row alignment
+  static constexpr int LDA = BK + PAD;                       // LDS row stride (elements)
+  static constexpr int CPR = BK / 8;                         // fragments per tile row
+  static constexpr int FW = (OT * CPR + NT - 1) / NT;        // W fragments per thread
+  static constexpr int FX = (NTOK * CPR + NT - 1) / NT;      // X fragments per thread
+  static constexpr int STAGE = (OT + NTOK) * LDA;            // elements per LDS stage
+  static constexpr int PIPE = 2;                             // K slices held in registers
+  static_assert(BK % 16 == 0, "K slices hold whole k16 steps");
+};
+
+// A group's row-major matrix seen through a buffer resource: rows of row_bytes;
+// the loader's slice(k0) gives the byte offset of column k0 within a row.
+struct RowsView {
   __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t row_bytes;
 };
 
-template <typename T> struct GemmCfg {
-  static constexpr int BM = 128, BN = 128;
-  static constexpr int BK = sizeof(T) == 2 ? 64 : 32;
-  static constexpr int PAD = sizeof(T) == 2 ? 8 : 4;  // keeps 16-B row alignment
-  static constexpr int LDA = BK + PAD;                 // LDS row stride (elements)
-  static constexpr int LDC = BN + 4;                   // fp32 C tile row stride
-  static constexpr int FR = BM * BK / 8 / 256;         // operand fragments per thread per slice
-  static constexpr int TPR = BK / (8 * FR);            // threads per tile row
-  static constexpr int STAGE = 2 * BM * LDA;           // elements per stage (A and B)
-  static constexpr int AB_BYTES = 2 * STAGE * (int)sizeof(T);
-  static constexpr int C_BYTES = BM * LDC * 4;
-  static constexpr int SMEM = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
-  static constexpr int PIPE = 3;                       // K slices held in registers
-};
+// XLoad / WLoad: RowsView view(int g) const; uint32_t slice(int k0) const
+//   (activations [M][..] and weights [Nout][..]; slice() is uniform over the block)
+// kspan: 0, or the K range of each group for split K: group g then covers
+//   columns [g kspan, min(K, (g+1) kspan)) of one shared matrix pair.
+// Epi:   struct State;
+//        template <class C> void begin(int g, int nw0, int lane, State&) const
+//        template <class C> void segment(int g, int seg, int nw0,
+//                                        f32x16 (&acc)[C::WO][C::WN], int lane, State&) const
+//          (entering K segment seg, i.e. slice seg * seg_len; the router rescales there)
+//        template <class C> void finish(int g, int ow0, int nw0,
+//                                       f32x16 (&acc)[C::WO][C::WN], int lane, State&) const
+//          (ow0 / nw0: the wave's first channel / token)
+// Launched on a 1-D grid of groups x token tiles x channel tiles; the tile order
+// (group, token tile, channel tile) is spread over the XCDs so the channel tiles
+// of a token block share one L2.
+template <class C, typename T, class XLoad, class WLoad, class Epi>
+__global__ __launch_bounds__(C::NT) void proj_gemm_kernel(int M, int Nout, int K, int groups,
+                                                          int seg_len, int kspan, XLoad xl,
+                                                          WLoad wl, Epi epi) {
+  __shared__ __align__(16) T smem[2 * C::STAGE];
 
-// ALoad: State begin(int g) const;
-//        void load(const State&, int row, int k, bool ok, frag_t<T>* out) const
-//          (FR consecutive frags of row `row` from column k; zeros when !ok)
-// BLoad: WeightView<T> view(int g) const  -> the group's [Nout][K] weights
-// Epi:   void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const
-// Launched on a 1-D grid of groups x row tiles x column tiles blocks; the tile
-// order is (group, row tile, column tile) and is spread over the XCDs so the
-// column tiles of a row block share one L2.
-template <typename T, class ALoad, class BLoad, class Epi>
-__global__ __launch_bounds__(256) void gemm_nt_kernel(int M, int Nout, int K, int groups,
-                                                      ALoad aload, BLoad bload, Epi epi) {
-  using C = GemmCfg<T>;
-  __shared__ __align__(16) unsigned char smem[C::SMEM];
-  T* stage0 = (T*)smem;
-  float* Cs = (float*)smem;
-
-  const int nt = (Nout + C::BN - 1) / C::BN, mt = (M + C::BM - 1) / C::BM;
-  const int tile = xcd_tile(blockIdx.x, groups * mt * nt);
-  const int g = tile / (mt * nt);
-  const int m0 = (tile / nt % mt) * C::BM, n0 = (tile % nt) * C::BN;
+  const int ot = (Nout + C::OT - 1) / C::OT, mt = (M + C::NTOK - 1) / C::NTOK;
+  const int tile = xcd_tile(blockIdx.x, groups * mt * ot);
+  const int g = tile / (mt * ot);
+  const int n0 = (tile / ot % mt) * C::NTOK, o0 = (tile % ot) * C::OT;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1, h = lane >> 5, r = lane & 31;
+  const int wo = w % C::WGO, wn = w / C::WGO;
+  const int h = lane >> 5, r = lane & 31;
 
-  // each thread moves FR consecutive fragments of one A row and one B row per slice
-  const int lrow = tid / C::TPR, lk = (tid % C::TPR) * 8 * C::FR;
-  const bool arow_ok = m0 + lrow < M;
-  const auto ast = aload.begin(g);
-  const auto wv = bload.view(g);
-  const bool brow_ok = n0 + lrow < Nout;
-  const uint32_t brow_off = (uint32_t)((n0 + lrow) * K) * (uint32_t)sizeof(T);
-
-  f32x16 acc[2][2];
+  const RowsView xv = xl.view(g), wv = wl.view(g);
+  // fragment f of this thread: tile row idx / CPR, 8-element chunk idx % CPR
+  uint32_t xoff[C::FX], woff[C::FW];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int f = 0; f < C::FX; ++f) {
+    const int idx = tid + f * C::NT, row = idx / C::CPR, ch = idx % C::CPR;
+    const bool ok = idx < C::NTOK * C::CPR && n0 + row < M;
+    xoff[f] = ok ? (uint32_t)(n0 + row) * xv.row_bytes + ch * 8 * (uint32_t)sizeof(T) : kOffOob;
+  }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
+  for (int f = 0; f < C::FW; ++f) {
+    const int idx = tid + f * C::NT, row = idx / C::CPR, ch = idx % C::CPR;
+    const bool ok = idx < C::OT * C::CPR && o0 + row < Nout;
+    woff[f] = ok ? (uint32_t)(o0 + row) * wv.row_bytes + ch * 8 * (uint32_t)sizeof(T) : kOffOob;
+  }
 
-  // K slices in flight: slice kb + P is fetched while slice kb is multiplied, so each
-  // slice's global loads have P - 1 slices of matrix-core work to land.
+  f32x16 acc[C::WO][C::WN];
+#pragma unroll
+  for (int i = 0; i < C::WO; ++i)
+#pragma unroll
+    for (int j = 0; j < C::WN; ++j) acc[i][j] = zero16();
+
   constexpr int P = C::PIPE;
-  frag_t<T> av[P][C::FR], bv[P][C::FR];
-  auto fetch = [&](int k0, frag_t<T>* a_out, frag_t<T>* b_out) {
-    const bool kin = k0 + lk < K;  // the thread's chunk lies wholly inside or outside K
-    aload.load(ast, m0 + lrow, k0 + lk, arow_ok && kin, a_out);
-    const uint32_t off = brow_ok && kin ? brow_off + (uint32_t)(k0 + lk) * sizeof(T) : kOffOob;
+  frag_t<T> xr[P][C::FX], wr[P][C::FW];
+  // Rows past the matrix keep the out-of-range offset whatever the slice adds
+  // (every view spans less than 2 GiB).
+  const int kbeg = kspan > 0 ? g * kspan : 0;
+  const int kend = kspan > 0 ? min(K, kbeg + kspan) : K;
+  auto fetch = [&](int k0, frag_t<T>* x_out, frag_t<T>* w_out) {
+    const bool kin = k0 < kend;
+    const uint32_t xs = kin ? xl.slice(k0) : 0u, ws = kin ? wl.slice(k0) : 0u;
 #pragma unroll
-    for (int i = 0; i < C::FR; ++i) b_out[i] = buf_frag<T>(wv.rsrc, off + 8 * i * sizeof(T));
+    for (int f = 0; f < C::FX; ++f) x_out[f] = buf_frag<T>(xv.rsrc, kin ? xoff[f] + xs : kOffOob);
+#pragma unroll
+    for (int f = 0; f < C::FW; ++f) w_out[f] = buf_frag<T>(wv.rsrc, kin ? woff[f] + ws : kOffOob);
   };
-  auto stage = [&](int buf, const frag_t<T>* a_in, const frag_t<T>* b_in) {
-    T* As = stage0 + buf * C::STAGE;
-    T* Bs = As + C::BM * C::LDA;
+  auto stage = [&](int buf, const frag_t<T>* x_in, const frag_t<T>* w_in) {
+    T* Ws = smem + buf * C::STAGE;
+    T* Xs = Ws + C::OT * C::LDA;
 #pragma unroll
-    for (int i = 0; i < C::FR; ++i) {
-      st_frag<T>(As + lrow * C::LDA + lk + 8 * i, a_in[i]);
-      st_frag<T>(Bs + lrow * C::LDA + lk + 8 * i, b_in[i]);
+    for (int f = 0; f < C::FX; ++f) {
+      const int idx = tid + f * C::NT;
+      if (C::NTOK * C::CPR % C::NT == 0 || idx < C::NTOK * C::CPR)
+        st_frag<T>(Xs + (idx / C::CPR) * C::LDA + (idx % C::CPR) * 8, x_in[f]);
+    }
+#pragma unroll
+    for (int f = 0; f < C::FW; ++f) {
+      const int idx = tid + f * C::NT;
+      if (C::OT * C::CPR % C::NT == 0 || idx < C::OT * C::CPR)
+        st_frag<T>(Ws + (idx / C::CPR) * C::LDA + (idx % C::CPR) * 8, w_in[f]);
     }
   };
   auto compute = [&](int buf) {
-    const T* As = stage0 + buf * C::STAGE;
-    const T* Bs = As + C::BM * C::LDA;
+    const T* Ws = smem + buf * C::STAGE;
+    const T* Xs = Ws + C::OT * C::LDA;
 #pragma unroll
     for (int ks = 0; ks < C::BK / 16; ++ks) {
-      frag_t<T> a[2], b[2];
+      frag_t<T> a[C::WO], b[C::WN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = ld_frag<T>(As + (64 * wm + 32 * i + r) * C::LDA + 16 * ks + 8 * h);
+      for (int i = 0; i < C::WO; ++i)
+        a[i] = ld_frag<T>(Ws + (32 * (wo * C::WO + i) + r) * C::LDA + 16 * ks + 8 * h);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[j] = ld_frag<T>(Bs + (64 * wn + 32 * j + r) * C::LDA + 16 * ks + 8 * h);
+      for (int j = 0; j < C::WN; ++j)
+        b[j] = ld_frag<T>(Xs + (32 * (wn * C::WN + j) + r) * C::LDA + 16 * ks + 8 * h);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < C::WO; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mma32(acc[i][j], a[i], b[j]);
+        for (int j = 0; j < C::WN; ++j) acc[i][j] = mma32(acc[i][j], a[i], b[j]);
     }
   };
 
+  const int ow0 = o0 + 32 * C::WO * wo, nw0 = n0 + 32 * C::WN * wn;
+  typename Epi::State est;
+  epi.template begin<C>(g, nw0, lane, est);
+
   // The slice count is padded to a multiple of P; padded slices read zeros through the
-  // out-of-range offset, so the loop body has no branch and every load's wait count
-  // stays exact.
-  const int nk = (K + C::BK - 1) / C::BK;
-  const int nkp = (nk + P - 1) / P * P;
+  // out-of-range offset, so the loop body has no divergent branch.
+  // Slices are counted from kbeg (a multiple of BK); kb below is the absolute slice.
+  const int kb_beg = kbeg / C::BK, kb_end = (kend + C::BK - 1) / C::BK;
+  const int nkp = (kb_end - kb_beg + P - 1) / P * P;
 #pragma unroll
-  for (int u = 0; u < P; ++u) fetch(u * C::BK, av[u], bv[u]);
-  stage(0, av[0], bv[0]);
+  for (int u = 0; u < P; ++u) fetch((kb_beg + u) * C::BK, xr[u], wr[u]);
+  stage(0, xr[0], wr[0]);
   __syncthreads();
-  for (int kb0 = 0; kb0 < nkp; kb0 += P) {
+  for (int i0 = 0; i0 < nkp; i0 += P) {
 #pragma unroll
     for (int u = 0; u < P; ++u) {
-      const int kb = kb0 + u;  // slot u held slice kb, already staged into buffer kb & 1
-      fetch((kb + P) * C::BK, av[u], bv[u]);
-      compute(kb & 1);
-      stage((kb + 1) & 1, av[(u + 1) % P], bv[(u + 1) % P]);
+      const int i = i0 + u, kb = kb_beg + i;  // slot u held slice kb, staged into buffer i & 1
+      fetch((kb + P) * C::BK, xr[u], wr[u]);
+      compute(i & 1);
+      if ((kb + 1) % seg_len == 0 && kb + 1 < kb_end)
+        epi.template segment<C>(g, (kb + 1) / seg_len, nw0, acc, lane, est);
+      stage((i + 1) & 1, xr[(u + 1) % P], wr[(u + 1) % P]);
       __syncthreads();
     }
   }
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        int row = 64 * wm + 32 * i + 8 * (q >> 2) + 4 * h + (q & 3);
-        int col = 64 * wn + 32 * j + r;
-        Cs[row * C::LDC + col] = acc[i][j][q];
-      }
-  __syncthreads();
-  epi(g, m0, n0, Cs, C::LDC, tid);
+  epi.template finish<C>(g, ow0, nw0, acc, lane, est);
 }
 
 }  // namespace wm

@@ -10,7 +10,7 @@ namespace wm {
 
 typedef __bf16 bf16;
 constexpr int kMaxLayers = 64;  // L limit (kernel-argument tables are sized by it)
-constexpr int kMaxHeadDim = 128;
+constexpr int kMaxHeadDim = 64;  // head dims 32 and 64 are supported
 
 struct Shape {
   int B, T_new, L, k, D, Hq, Hkv, d, p, Lp, S_cap;
@@ -34,10 +34,14 @@ void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStr
 void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipStream_t s);
 
 // logits[br][n][o] = sum over stacked layers of W_alpha[br][o] . normed state + b_alpha[br][o]
+// wfold: router_fold_elems(sh) elements (weights with the pre-mix gain folded in);
+// part: router_partials_bytes(sh) bytes of split-K partial sums (may be 0).
+size_t router_fold_elems(const Shape& sh);
+size_t router_partials_bytes(const Shape& sh);
 template <typename T>
 void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
-                   const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits,
-                   hipStream_t s);
+                   const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits, T* wfold,
+                   float* part, hipStream_t s);
 
 // alpha (in: logits [2][N][k*L], out: mixing weights) -> mixed[2][k][N][D], rinv_mid[2][k][N]
 size_t mix_smem_bytes(int L, int k, int D, size_t elem_bytes);

@@ -69,225 +69,388 @@ void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipS
                      ctx_len, sh.B, sh.T_new, sh.d, (double)sh.rope_theta, tab);
 }
 
-static unsigned gemm_blocks(int M, int Nout, int groups) {
-  return (unsigned)(groups * ((M + 127) / 128) * ((Nout + 127) / 128));
-}
-
-// -------------------------------------------------------- GEMM functors
-// Weight matrices W + g * group_stride, [Nout][K] each.
-template <typename T> struct WeightRows {
-  const T* W;
-  long group_stride;
-  int Nout, K;
-  __device__ WeightView<T> view(int g) const {
-    return {make_view(W + (long)g * group_stride, (uint32_t)((long)Nout * K * sizeof(T)))};
-  }
-};
-
-// Router operand: the stacked normed states xi (gain and 1/RMS applied, one rounding).
-// Rows past M read zeros (their 1/RMS index is clamped to a valid row).
-template <typename T> struct RouterA {
-  const T* H;
-  const float* rinv;
-  const T* g_pre;
-  LayerTable sel;
-  int L, D, M;
-  struct State {
-    __amdgpu_buffer_rsrc_t h;
-    const T* g;
-  };
-  __device__ State begin(int br) const {
-    return {make_view(H, (uint32_t)((long)M * L * D * sizeof(T))), g_pre + (long)br * L * D};
-  }
-  __device__ void load(const State& st, int n, int k, bool ok, frag_t<T>* out) const {
-    const int m = k / D, e = k - m * D, layer = sel.v[m];
-    const uint32_t off = ok ? (uint32_t)(((long)n * L + layer) * D + e) * sizeof(T) : kOffOob;
-    const T* g = st.g + (long)layer * D + e;
-    const float rs = rinv[(long)min(n, M - 1) * L + layer];
-#pragma unroll
-    for (int f = 0; f < GemmCfg<T>::FR; ++f) {
-      frag_t<T> x = buf_frag<T>(st.h, off + 8 * f * sizeof(T));
-      float gv[8];
-      load8(g + 8 * f, gv);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) out[f][i] = from_f32<T>(to_f32(x[i]) * gv[i] * rs);
-    }
-  }
-};
-
-// Plain operand rows: X[g * gstride + row * rstride + k] for rows < M (scales live elsewhere).
-template <typename T> struct CopyRowsA {
+// -------------------------------------------------------- GEMM operands
+// Plain rows: X[g * gstride + row * rstride + k], rows < rows (weights or activations).
+template <typename T> struct PlainRows {
   const T* X;
   long gstride, rstride;
-  int M;
-  __device__ __amdgpu_buffer_rsrc_t begin(int g) const {
-    return make_view(X + (long)g * gstride, (uint32_t)((long)M * rstride * sizeof(T)));
+  int rows;
+  __device__ RowsView view(int g) const {
+    return {make_view(X + (long)g * gstride, (uint32_t)((long)rows * rstride * sizeof(T))),
+            (uint32_t)(rstride * sizeof(T))};
   }
-  __device__ void load(const __amdgpu_buffer_rsrc_t& r, int row, int k, bool ok,
-                       frag_t<T>* out) const {
-    const uint32_t off = ok ? (uint32_t)((long)row * rstride + k) * sizeof(T) : kOffOob;
-#pragma unroll
-    for (int f = 0; f < GemmCfg<T>::FR; ++f) out[f] = buf_frag<T>(r, off + 8 * f * sizeof(T));
-  }
+  __device__ uint32_t slice(int k0) const { return (uint32_t)k0 * (uint32_t)sizeof(T); }
 };
 
-template <typename T> struct RouterEpi {
-  float* logits;
-  const T* bias;
-  int M, Nout;
-  __device__ void operator()(int br, int m0, int n0, const float* C, int ldc, int tid) const {
-    int col = tid & 127, o = n0 + col;
-    if (o >= Nout) return;
-    float b = to_f32(bias[(long)br * Nout + o]);
-    for (int row = tid >> 7; row < 128; row += 2) {
-      int n = m0 + row;
-      if (n >= M) break;
-      logits[((long)br * M + n) * Nout + o] = C[row * ldc + col] + b;
-    }
+// Router operand: token n's row is the stack of the selected layers' raw states,
+// column k = m * D + e reading H[n][sel[m]][e] (the 1/RMS is applied to the
+// accumulators, the gain is folded into the weights).
+template <typename T> struct StackedRows {
+  const T* H;
+  LayerTable sel;
+  int L, D, M;
+  __device__ RowsView view(int) const {
+    return {make_view(H, (uint32_t)((long)M * L * D * sizeof(T))),
+            (uint32_t)((long)L * D * sizeof(T))};
+  }
+  __device__ uint32_t slice(int k0) const {
+    const int m = k0 / D, e = k0 - m * D;
+    return (uint32_t)(sel.v[m] * D + e) * (uint32_t)sizeof(T);
   }
 };
 
-// Head-wise epilogue shared by the K/V and Q projections. A C tile row holds
-// 128 / d heads; d / 8 consecutive lanes own one (row, head) item, 8 contiguous
-// elements each, so a lane group reads its row from LDS without bank conflicts
-// and writes the whole d-element head row (one 128-B line for d = 64) at once.
-// Per item: scale by the row's 1/RMS, then either store (V) or RMS-normalise
-// over the head, apply the gain and rotate the pairs (m, m + d/2) (K, Q); the
-// partner of element m lives d/16 lanes away.
-template <typename T, int DH> struct HeadItems {
-  static constexpr int LPI = DH / 8;          // lanes per item
-  static constexpr int IPP = 256 / LPI;       // items per pass of 256 threads
-  static constexpr int ITEMS = 128 * (128 / DH);
-};
-
-template <int LPI>
-__device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int x = 1; x < LPI; x <<= 1) v += __shfl_xor(v, x, 64);
-  return v;
+// ------------------------------------------------------ head epilogue
+// The K/V and Q projections end in the same per-head work on the transposed
+// accumulators. For token n (lane r of block column jn) and a head of DH
+// channels held by the wave, value v = 0 .. DH/2-1 of the lane sits in block
+// v / 16, register v % 16, i.e. at channel m(v) = 32 (v/16) + 8 ((v%16)/4) +
+// 4h + v%4; the other half of the head is in the partner lane (h ^ 1).
+//   scale by the row's 1/RMS; then either store (V) or RMS-normalise over the
+//   head (one cross-half sum), apply the gain and rotate: value v < DH/4 pairs
+//   with v + DH/4 (channels m and m + DH/2), at angle index m(v).
+template <int DH> __device__ __forceinline__ int head_chan(int v, int h) {
+  return 32 * (v >> 4) + 8 * ((v & 15) >> 2) + 4 * h + (v & 3);
 }
 
-// c: this lane's 8 fp32 values; sc: row scale; normalise+rotate when gain != nullptr.
-template <typename T, int DH>
-__device__ __forceinline__ void head_chunk(float* c, float sc, const T* gain, const float* tabrow,
-                                           int lane_c, float eps, T* dst) {
-  constexpr int LPI = DH / 8;
+template <typename T, int DH, int WO, int WN, class ScaleAt, class DstAt>
+__device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, int nw0, int lane,
+                                              int M, bool rotate, const T* gain,
+                                              const float* tab, float eps, ScaleAt scale_at,
+                                              DstAt dst_at) {
+  constexpr int NV = DH / 2;          // values of one head per lane
+  constexpr int HPW = 32 * WO / DH;   // heads per wave
+  static_assert(HPW * DH == 32 * WO, "a wave holds whole heads");
+  const int h = lane >> 5, r = lane & 31;
+  float gv[NV];
+  if (rotate) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) c[i] *= sc;
-  if (gain) {
-    float ss = 0.f;
+    for (int c = 0; c < NV / 4; ++c) {
+      const T* gp = gain + head_chan<DH>(4 * c, h);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) ss += c[i] * c[i];
-    ss = group_sum<LPI>(ss);
-    const float rs = 1.0f / sqrtf(ss / (float)DH + eps);
-    float gv[8];
-    load8(gain + 8 * lane_c, gv);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) c[i] *= rs * gv[i];
-    // pair (m, m + DH/2): lanes c < LPI/2 hold m, lanes c >= LPI/2 hold m + DH/2
-    const bool lo = lane_c < LPI / 2;
-    const int mc = lo ? lane_c : lane_c - LPI / 2;  // which 8 pairs
-    float cs[8], sn[8];
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) {
-      f32x4 t = *(const f32x4*)(tabrow + 2 * (8 * mc + i));
-      cs[i] = t[0];
-      sn[i] = t[1];
-      cs[i + 1] = t[2];
-      sn[i + 1] = t[3];
+      for (int t = 0; t < 4; ++t) gv[4 * c + t] = to_f32(gp[t]);
     }
-    float y[8];
+  }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float other = __shfl_xor(c[i], LPI / 2, 64);
-      // lo: x1 = c, x2 = other -> x1 cos - x2 sin;  hi: x2 = c, x1 = other -> x2 cos + x1 sin
-      y[i] = lo ? c[i] * cs[i] - other * sn[i] : c[i] * cs[i] + other * sn[i];
+  for (int jn = 0; jn < WN; ++jn) {
+    const int n = nw0 + 32 * jn + r;
+    const bool in = n < M;
+    const int nn = in ? n : M - 1;
+    const float sc = scale_at(nn);
+    f32x4 tb[DH / 16][2];  // (cos, sin) of angle indices 8g + 4h + t, t = 0..3
+    if (rotate) {
+#pragma unroll
+      for (int g = 0; g < DH / 16; ++g) {
+        const float* tp = tab + (long)nn * DH + 2 * (8 * g + 4 * h);
+        tb[g][0] = *(const f32x4*)tp;
+        tb[g][1] = *(const f32x4*)(tp + 4);
+      }
     }
-    store8(dst, y);
-  } else {
-    store8(dst, c);
+#pragma unroll
+    for (int hw = 0; hw < HPW; ++hw) {
+      float c[NV];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) c[v] = acc[hw * (DH / 32) + (v >> 4)][jn][v & 15] * sc;
+      if (rotate) {
+        float ss = 0.f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) ss += c[v] * c[v];
+        ss = halves_sum(ss);
+        const float rs = 1.0f / sqrtf(ss / (float)DH + eps);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) c[v] *= rs * gv[v];
+#pragma unroll
+        for (int v = 0; v < NV / 2; ++v) {
+          const int t = v & 3;
+          const float cs = tb[v >> 2][t >> 1][2 * (t & 1)], sn = tb[v >> 2][t >> 1][2 * (t & 1) + 1];
+          const float x1 = c[v], x2 = c[v + NV / 2];
+          c[v] = x1 * cs - x2 * sn;
+          c[v + NV / 2] = x2 * cs + x1 * sn;
+        }
+      }
+      T* dst = dst_at(nn, (ow0 + hw * DH) / DH);
+      const bool ok = in && dst != nullptr;
+      if constexpr (sizeof(T) == 2) {
+        // chunks 2p, 2p+1 (channels m0 + 4h + 0..3 and m0 + 8 + 4h + 0..3): one swap of
+        // the middle quarters gives lane h the 8 contiguous channels m0 + 8h .. m0 + 8h + 7
+#pragma unroll
+        for (int p = 0; p < NV / 8; ++p) {
+          uint32_t a[2], b[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            bf16x2 x = {(bf16)c[8 * p + 2 * i], (bf16)c[8 * p + 2 * i + 1]};
+            bf16x2 y = {(bf16)c[8 * p + 4 + 2 * i], (bf16)c[8 * p + 4 + 2 * i + 1]};
+            a[i] = __builtin_bit_cast(uint32_t, x);
+            b[i] = __builtin_bit_cast(uint32_t, y);
+            auto sw = __builtin_amdgcn_permlane32_swap(a[i], b[i], false, false);
+            a[i] = sw[0];
+            b[i] = sw[1];
+          }
+          if (ok) {
+            i32x4 o = {(int)a[0], (int)a[1], (int)b[0], (int)b[1]};
+            *(i32x4*)(dst + 32 * (p >> 1) + 16 * (p & 1) + 8 * h) = o;
+          }
+        }
+      } else {
+        if (ok) {
+#pragma unroll
+          for (int q = 0; q < NV / 4; ++q) {
+            f32x4 o = {c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]};
+            *(f32x4*)(dst + head_chan<DH>(4 * q, h)) = o;
+          }
+        }
+      }
+    }
+    // one token block at a time: hoisting the next block's accumulator reads and
+    // loads above this point would hold them all in registers at once
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-template <typename T> struct KVEpi {
+struct NoState {};
+
+template <typename T, int DH> struct KVEpi {
   T *Kc, *Vc;
   const float* rs;  // [2k][M] 1 / RMS of each mixed channel row (the mid RMSNorm)
   const T* g_knorm;
   const float* tab;
   const int32_t* ctx_len;
-  int M, Nout, d, T_new, B, Hkv, S_cap, k;
+  int M, T_new, B, Hkv, S_cap, k;
   float eps;
-  template <int DH>
-  __device__ void run(int g, int m0, int n0, const float* C, int ldc, int tid) const {
-    using HI = HeadItems<T, DH>;
+  using State = NoState;
+  template <class C> __device__ void begin(int, int, int, State&) const {}
+  template <class C>
+  __device__ void segment(int, int, int, f32x16 (&)[C::WO][C::WN], int, State&) const {}
+  template <class C>
+  __device__ void finish(int g, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
+                         State&) const {
     const int br = g / k, j = g - br * k;
-    const int lane_c = tid % HI::LPI;
-    for (int it = tid / HI::LPI; it < HI::ITEMS; it += HI::IPP) {
-      const int row = it & 127, hh = it >> 7;
-      const int n = m0 + row, col0 = n0 + hh * DH;
-      if (n >= M || col0 >= Nout) continue;
-      const int b = n / T_new, i = n - b * T_new;
-      const long slot = (long)(ctx_len ? ctx_len[b] : 0) + i;
-      if (slot < 0 || slot >= S_cap) continue;
-      const int head = col0 / DH;
-      const long off = ((((long)j * B + b) * Hkv + head) * S_cap + slot) * DH + 8 * lane_c;
-      float c[8];
-      const float* src = C + row * ldc + hh * DH + 8 * lane_c;
-      *(f32x4*)c = *(const f32x4*)src;
-      *(f32x4*)(c + 4) = *(const f32x4*)(src + 4);
-      head_chunk<T, DH>(c, rs[(long)g * M + n], br == 0 ? g_knorm + (long)j * DH : nullptr,
-                        tab + (long)n * DH, lane_c, eps, (br == 0 ? Kc : Vc) + off);
-    }
-  }
-  __device__ void operator()(int g, int m0, int n0, const float* C, int ldc, int tid) const {
-    if (d == 64) run<64>(g, m0, n0, C, ldc, tid);
-    else run<32>(g, m0, n0, C, ldc, tid);
+    const bool key = br == 0;
+    T* base = key ? Kc : Vc;
+    head_epilogue<T, DH, C::WO, C::WN>(
+        acc, ow0, nw0, lane, M, key, g_knorm + (long)j * DH, tab, eps,
+        [&](int n) { return rs[(long)g * M + n]; },
+        [&](int n, int head) -> T* {
+          if (head >= Hkv) return nullptr;
+          const int b = n / T_new, i = n - b * T_new;
+          const long slot = (long)(ctx_len ? ctx_len[b] : 0) + i;
+          if (slot < 0 || slot >= S_cap) return nullptr;
+          return base + ((((long)j * B + b) * Hkv + head) * S_cap + slot) * DH;
+        });
   }
 };
 
-template <typename T> struct QEpi {
+template <typename T, int DH> struct QEpi {
   T* Q;
   const float* rs;  // [M][L] 1 / RMS of each consumer's input state (the input RMSNorm)
   const T* g_qnorm;
   const float* tab;
-  int M, Nout, d, T_new, B, Hq, L;
+  int M, T_new, B, Hq, L;
   float eps;
-  template <int DH>
-  __device__ void run(int l, int m0, int n0, const float* C, int ldc, int tid) const {
-    using HI = HeadItems<T, DH>;
-    const int lane_c = tid % HI::LPI;
-    for (int it = tid / HI::LPI; it < HI::ITEMS; it += HI::IPP) {
-      const int row = it & 127, hh = it >> 7;
-      const int n = m0 + row, col0 = n0 + hh * DH;
-      if (n >= M || col0 >= Nout) continue;
-      const int b = n / T_new, i = n - b * T_new, head = col0 / DH;
-      const long off = ((((long)l * B + b) * Hq + head) * T_new + i) * DH + 8 * lane_c;
-      float c[8];
-      const float* src = C + row * ldc + hh * DH + 8 * lane_c;
-      *(f32x4*)c = *(const f32x4*)src;
-      *(f32x4*)(c + 4) = *(const f32x4*)(src + 4);
-      head_chunk<T, DH>(c, rs[(long)n * L + l], g_qnorm + (long)l * DH, tab + (long)n * DH,
-                        lane_c, eps, Q + off);
-    }
-  }
-  __device__ void operator()(int l, int m0, int n0, const float* C, int ldc, int tid) const {
-    if (d == 64) run<64>(l, m0, n0, C, ldc, tid);
-    else run<32>(l, m0, n0, C, ldc, tid);
+  using State = NoState;
+  template <class C> __device__ void begin(int, int, int, State&) const {}
+  template <class C>
+  __device__ void segment(int, int, int, f32x16 (&)[C::WO][C::WN], int, State&) const {}
+  template <class C>
+  __device__ void finish(int l, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
+                         State&) const {
+    head_epilogue<T, DH, C::WO, C::WN>(
+        acc, ow0, nw0, lane, M, true, g_qnorm + (long)l * DH, tab, eps,
+        [&](int n) { return rs[(long)n * L + l]; },
+        [&](int n, int head) -> T* {
+          if (head >= Hq) return nullptr;
+          const int b = n / T_new, i = n - b * T_new;
+          return Q + ((((long)l * B + b) * Hq + head) * T_new + i) * DH;
+        });
   }
 };
 
+// Router epilogue. Column block m of the stacked operand is layer sel[m]'s raw
+// state; its 1/RMS is a per-token factor, so the accumulators are kept in units
+// of the current layer's 1/RMS: at a layer boundary they are multiplied by
+// rinv(previous) / rinv(next), and by rinv(last) at the end. With split K a
+// block covers the layers [s * per, ...) and writes a partial sum for the
+// reduction; without it the bias is added and the logits are stored directly.
+template <typename T> struct RouterEpi {
+  float* out;        // splits == 1: logits [2][M][kL]; else partials [splits][M][2kL]
+  const T* bias;     // [2kL]
+  const float* rinv; // [M][L]
+  LayerTable sel;
+  int M, Nout, kL, L, Lp, seg_per_split, splits;
+  struct State {
+    float cur[4], nxt[4];
+  };
+  __device__ float rinv_at(int n, int m) const {
+    return rinv[(long)n * L + sel.v[min(m, Lp - 1)]];
+  }
+  template <class C> __device__ void begin(int s, int nw0, int lane, State& st) const {
+    static_assert(C::WN <= 4, "router state holds 4 token blocks");
+    const int m0 = s * seg_per_split;
+#pragma unroll
+    for (int jn = 0; jn < C::WN; ++jn) {
+      const int n = min(nw0 + 32 * jn + (lane & 31), M - 1);
+      st.cur[jn] = rinv_at(n, m0);
+      st.nxt[jn] = rinv_at(n, m0 + 1);
+    }
+  }
+  template <class C>
+  __device__ void segment(int, int seg, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
+                          State& st) const {
+#pragma unroll
+    for (int jn = 0; jn < C::WN; ++jn) {
+      const float f = st.cur[jn] / st.nxt[jn];
+#pragma unroll
+      for (int i = 0; i < C::WO; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[i][jn][q] *= f;
+      st.cur[jn] = st.nxt[jn];
+      const int n = min(nw0 + 32 * jn + (lane & 31), M - 1);
+      st.nxt[jn] = rinv_at(n, seg + 1);
+    }
+  }
+  template <class C>
+  __device__ void finish(int s, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
+                         State& st) const {
+    const int h = lane >> 5, r = lane & 31;
+#pragma unroll
+    for (int jn = 0; jn < C::WN; ++jn) {
+      const int n = nw0 + 32 * jn + r;
+      if (n >= M) continue;
+#pragma unroll
+      for (int i = 0; i < C::WO; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int o = ow0 + 32 * i + 8 * (q >> 2) + 4 * h + (q & 3);
+          if (o >= Nout) continue;
+          const float v = acc[i][jn][q] * st.cur[jn];
+          if (splits == 1) {
+            const int br = o >= kL, oo = o - br * kL;
+            out[((long)br * M + n) * kL + oo] = v + to_f32(bias[o]);
+          } else {
+            out[((long)s * M + n) * Nout + o] = v;
+          }
+        }
+    }
+  }
+};
+
+// logits[br][n][o'] = sum_s part[s][n][br kL + o'] + bias[br kL + o']
+template <typename T>
+__global__ __launch_bounds__(256) void router_reduce_kernel(const float* part, const T* bias,
+                                                            float* logits, int M, int kL,
+                                                            int splits) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x, total = (long)M * 2 * kL;
+  if (idx >= total) return;
+  const int n = (int)(idx / (2 * kL)), o = (int)(idx - (long)n * 2 * kL);
+  float v = to_f32(bias[o]);
+  for (int s = 0; s < splits; ++s) v += part[(long)s * total + idx];
+  const int br = o >= kL, oo = o - br * kL;
+  logits[((long)br * M + n) * kL + oo] = v;
+}
+
+// Router weights with the pre-mix gain folded in: Wf[o][m D + e] =
+// W_alpha[o][m D + e] * g_pre[o / kL][sel[m]][e], o over both branches.
+template <typename T>
+__global__ __launch_bounds__(256) void router_fold_kernel(const T* W, const T* g_pre,
+                                                          LayerTable sel, int kL, int L, int Lp,
+                                                          int D, T* Wf) {
+  const long idx = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
+  const long K = (long)Lp * D, total = 2 * kL * K;
+  if (idx >= total) return;
+  const int o = (int)(idx / K);
+  const long kk = idx - o * K;
+  const int m = (int)(kk / D), e = (int)(kk - (long)m * D);
+  float wv[8], gv[8];
+  load8(W + idx, wv);
+  load8(g_pre + ((long)(o / kL) * L + sel.v[m]) * D + e, gv);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) wv[i] *= gv[i];
+  store8(Wf + idx, wv);
+}
+
+template <class C> static unsigned proj_blocks(int M, int Nout, int groups) {
+  return (unsigned)(groups * ((M + C::NTOK - 1) / C::NTOK) * ((Nout + C::OT - 1) / C::OT));
+}
+
+template <class C, typename T, class XL, class WL, class Epi>
+static void launch_proj(int M, int Nout, int K, int groups, int seg_len, int kspan,
+                        const XL& xl, const WL& wl, const Epi& e, hipStream_t s) {
+  hipLaunchKernelGGL((proj_gemm_kernel<C, T, XL, WL, Epi>), dim3(proj_blocks<C>(M, Nout, groups)),
+                     dim3(C::NT), 0, s, M, Nout, K, groups, seg_len, kspan, xl, wl, e);
+}
+constexpr int kNoSegments = 1 << 30;
+
+// Tile shapes. Large token counts: 128 channels x 256 tokens per block, 64 x 128
+// per wave (bf16). Few tokens (decode): 128 x 64. fp32 halves the token tile.
+template <typename T, bool FEW> struct ProjShape;
+template <> struct ProjShape<bf16, false> { using C = ProjCfg<bf16, 32, 2, 2, 2, 4>; };
+template <> struct ProjShape<bf16, true> { using C = ProjCfg<bf16, 32, 2, 2, 2, 1>; };
+template <> struct ProjShape<float, false> { using C = ProjCfg<float, 32, 2, 2, 2, 2>; };
+template <> struct ProjShape<float, true> { using C = ProjCfg<float, 32, 2, 2, 2, 1>; };
+// Router: 96 channels x 128 tokens per block (the channel count 2kL is small and
+// often a multiple of 96), 96 x 32 per wave.
+template <typename T, bool FEW> struct RouterShape;
+template <> struct RouterShape<bf16, false> { using C = ProjCfg<bf16, 32, 1, 4, 3, 1>; };
+template <> struct RouterShape<bf16, true> { using C = ProjCfg<bf16, 32, 1, 2, 3, 1>; };
+template <> struct RouterShape<float, false> { using C = ProjCfg<float, 32, 1, 4, 3, 1>; };
+template <> struct RouterShape<float, true> { using C = ProjCfg<float, 32, 1, 2, 3, 1>; };
+
+constexpr int kFewTokens = 64;
+
 // ------------------------------------------------------------------ router
+size_t router_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.L * sh.Lp * sh.D; }
+
+// Layers per K split: enough blocks to cover the chip, splitting K at layer
+// boundaries when the token and channel tiles alone give few blocks.
+static int router_layers_per_split(const Shape& sh) {
+  const int tok = sh.N() <= kFewTokens ? 64 : 128;
+  const long blocks = (long)((sh.N() + tok - 1) / tok) * ((2 * sh.k * sh.L + 95) / 96);
+  int s = 1;
+  while (s < sh.Lp && blocks * s < 512) s *= 2;
+  return (sh.Lp + s - 1) / s;
+}
+
+static int router_splits(const Shape& sh) {  // every split covers at least one layer
+  const int per = router_layers_per_split(sh);
+  return (sh.Lp + per - 1) / per;
+}
+
+size_t router_partials_bytes(const Shape& sh) {
+  const int s = router_splits(sh);
+  return s > 1 ? (size_t)s * sh.N() * 2 * sh.k * sh.L * sizeof(float) : 0;
+}
+
+template <typename T, bool FEW>
+static void router_gemm(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
+                        const T* wf, const T* b_alpha, float* logits, float* part,
+                        hipStream_t s) {
+  using C = typename RouterShape<T, FEW>::C;
+  const int M = sh.N(), kL = sh.k * sh.L, Nout = 2 * kL, K = sh.Lp * sh.D;
+  const int seg = sh.D / C::BK, splits = router_splits(sh);
+  const int per = router_layers_per_split(sh);
+  StackedRows<T> x{H, sel, sh.L, sh.D, M};
+  PlainRows<T> w{wf, 0, K, Nout};
+  RouterEpi<T> e{splits > 1 ? part : logits, b_alpha, rinv, sel, M, Nout, kL, sh.L, sh.Lp, per,
+                 splits};
+  // the split index plays the group: split s covers layers [s per, (s+1) per)
+  launch_proj<C, T>(M, Nout, K, splits, seg, per * sh.D, x, w, e, s);
+  if (splits > 1) {
+    const long total = (long)M * Nout;
+    hipLaunchKernelGGL(router_reduce_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256),
+                       0, s, part, b_alpha, logits, M, kL, splits);
+  }
+}
+
 template <typename T>
 void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
-                   const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits,
-                   hipStream_t s) {
-  int M = sh.N(), Nout = sh.k * sh.L, K = sh.Lp * sh.D;
+                   const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits, T* wfold,
+                   float* part, hipStream_t s) {
+  const int M = sh.N();
   if (M <= 0) return;
-  RouterA<T> a{H, rinv, g_pre, sel, sh.L, sh.D, M};
-  WeightRows<T> w{W_alpha, (long)Nout * K, Nout, K};
-  RouterEpi<T> e{logits, b_alpha, M, Nout};
-  hipLaunchKernelGGL((gemm_nt_kernel<T, RouterA<T>, WeightRows<T>, RouterEpi<T>>),
-                     dim3(gemm_blocks(M, Nout, 2)), dim3(256), 0, s, M, Nout, K, 2, a, w, e);
+  const long total = (long)router_fold_elems(sh) / 8;
+  hipLaunchKernelGGL(router_fold_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                     s, W_alpha, g_pre, sel, sh.k * sh.L, sh.L, sh.Lp, sh.D, wfold);
+  if (M <= kFewTokens) router_gemm<T, true>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
+  else router_gemm<T, false>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
 }
 
 // --------------------------------------------------------------------- mix
@@ -442,40 +605,69 @@ static void fold_gain(const T* W0, const T* W1, int split, const T* gain, T* Wf,
 size_t kv_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.Hkv * sh.d * sh.D; }
 size_t q_fold_elems(const Shape& sh) { return (size_t)sh.L * sh.Hq * sh.d * sh.D; }
 
+template <typename T, int DH, bool FEW>
+static void kv_gemm(const Shape& sh, const T* mixed, const float* rinv_mid, const T* wfold,
+                    const T* g_knorm, const float* rope_tab, const int32_t* ctx_len, T* Kc, T* Vc,
+                    hipStream_t s) {
+  using C = typename ProjShape<T, FEW>::C;
+  const int M = sh.N(), Nout = sh.Hkv * DH, K = sh.D;
+  PlainRows<T> x{mixed, (long)M * K, K, M};
+  PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
+  KVEpi<T, DH> e{Kc, Vc, rinv_mid, g_knorm, rope_tab, ctx_len, M, sh.T_new, sh.B, sh.Hkv,
+                 sh.S_cap, sh.k, sh.eps};
+  launch_proj<C, T>(M, Nout, K, 2 * sh.k, kNoSegments, 0, x, w, e, s);
+}
+
 template <typename T>
 void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, const T* g_mid,
                        const T* Wk, const T* Wv, const T* g_knorm, const float* rope_tab,
                        const int32_t* ctx_len, T* Kc, T* Vc, T* wfold, hipStream_t s) {
-  int M = sh.N(), Nout = sh.Hkv * sh.d, K = sh.D;
+  const int M = sh.N();
   if (M <= 0) return;
-  fold_gain<T>(Wk, Wv, sh.k, g_mid, wfold, 2 * sh.k, Nout, K, s);
-  CopyRowsA<T> a{mixed, (long)M * K, K, M};
-  WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
-  KVEpi<T> e{Kc, Vc, rinv_mid, g_knorm, rope_tab, ctx_len, M, Nout, sh.d, sh.T_new, sh.B,
-             sh.Hkv, sh.S_cap, sh.k, sh.eps};
-  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, KVEpi<T>>),
-                     dim3(gemm_blocks(M, Nout, 2 * sh.k)), dim3(256), 0, s, M, Nout, K, 2 * sh.k,
-                     a, w, e);
+  fold_gain<T>(Wk, Wv, sh.k, g_mid, wfold, 2 * sh.k, sh.Hkv * sh.d, sh.D, s);
+  const bool few = M <= kFewTokens;
+  if (sh.d == 64) {
+    if (few) kv_gemm<T, 64, true>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
+    else kv_gemm<T, 64, false>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
+  } else {
+    if (few) kv_gemm<T, 32, true>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
+    else kv_gemm<T, 32, false>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
+  }
+}
+
+template <typename T, int DH, bool FEW>
+static void q_gemm(const Shape& sh, const T* H, const float* rinv, const T* wfold,
+                   const T* g_qnorm, const float* rope_tab, T* Q, hipStream_t s) {
+  using C = typename ProjShape<T, FEW>::C;
+  const int M = sh.N(), Nout = sh.Hq * DH, K = sh.D;
+  PlainRows<T> x{H, K, (long)sh.L * K, M};
+  PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
+  QEpi<T, DH> e{Q, rinv, g_qnorm, rope_tab, M, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
+  launch_proj<C, T>(M, Nout, K, sh.L, kNoSegments, 0, x, w, e, s);
 }
 
 template <typename T>
 void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g_in,
                       const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q, T* wfold,
                       hipStream_t s) {
-  int M = sh.N(), Nout = sh.Hq * sh.d, K = sh.D;
+  const int M = sh.N();
   if (M <= 0) return;
-  fold_gain<T>(Wq, Wq, sh.L, g_in, wfold, sh.L, Nout, K, s);
-  CopyRowsA<T> a{H, K, (long)sh.L * K, M};
-  WeightRows<T> w{wfold, (long)Nout * K, Nout, K};
-  QEpi<T> e{Q, rinv, g_qnorm, rope_tab, M, Nout, sh.d, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
-  hipLaunchKernelGGL((gemm_nt_kernel<T, CopyRowsA<T>, WeightRows<T>, QEpi<T>>),
-                     dim3(gemm_blocks(M, Nout, sh.L)), dim3(256), 0, s, M, Nout, K, sh.L, a, w, e);
+  fold_gain<T>(Wq, Wq, sh.L, g_in, wfold, sh.L, sh.Hq * sh.d, sh.D, s);
+  const bool few = M <= kFewTokens;
+  if (sh.d == 64) {
+    if (few) q_gemm<T, 64, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
+    else q_gemm<T, 64, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
+  } else {
+    if (few) q_gemm<T, 32, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
+    else q_gemm<T, 32, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
+  }
 }
 
 #define WM_INST(T)                                                                             \
   template void launch_row_rms<T>(const T*, long, int, float, float*, hipStream_t);            \
   template void launch_router<T>(const Shape&, const LayerTable&, const T*, const float*,      \
-                                 const T*, const T*, const T*, float*, hipStream_t);           \
+                                 const T*, const T*, const T*, float*, T*, float*,             \
+                                 hipStream_t);                                                 \
   template void launch_mix<T>(const Shape&, const T*, const float*, const T*, float*, T*,      \
                               float*, hipStream_t);                                            \
   template void launch_kv_project<T>(const Shape&, const T*, const float*, const T*, const T*, \
