@@ -9,7 +9,7 @@
 #include <cstdio>
 #include <cstring>
 
-#include "../../include/whitematter.h"
+#include "whitematter.h"
 #include "wm_internal.hpp"
 
 using wm::bf16;

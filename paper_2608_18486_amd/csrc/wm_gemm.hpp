@@ -24,13 +24,25 @@ template <typename T, int BK_, int WGO_, int WGN_, int WO_, int WN_> struct Proj
   static constexpr int BK = BK_, WGO = WGO_, WGN = WGN_, WO = WO_, WN = WN_;
   static constexpr int NT = 64 * WGO * WGN;                 // threads
   static constexpr int OT = 32 * WO * WGO, NTOK = 32 * WN * WGN;
-  static constexpr int PAD = sizeof(T) == 2 ? 8 : 4;         // keeps 16-B row alignment
+  // bf16 with BK = 32: 64-B LDS rows whose four 16-B chunks are XOR-swizzled
+  // (chunk c of row r at c ^ ((r / 2) % 4)), so the 8 lanes of a 128-B LDS cycle
+  // hit distinct banks both when a wave stages two rows of 4 chunks and when it
+  // reads one chunk of 8 consecutive rows. Otherwise rows are padded.
+  static constexpr bool SWZ = sizeof(T) == 2 && BK == 32;
+  static constexpr int PAD = SWZ ? 0 : sizeof(T) == 2 ? 8 : 4;  // keeps 16-B row alignment
   static constexpr int LDA = BK + PAD;                       // LDS row stride (elements)
   static constexpr int CPR = BK / 8;                         // fragments per tile row
+  // element offset of 8-element chunk ch of tile row row
+  __device__ static int chunk_at(int row, int ch) {
+    return row * LDA + 8 * (SWZ ? ch ^ ((row >> 1) & 3) : ch);
+  }
   static constexpr int FW = (OT * CPR + NT - 1) / NT;        // W fragments per thread
   static constexpr int FX = (NTOK * CPR + NT - 1) / NT;      // X fragments per thread
   static constexpr int STAGE = (OT + NTOK) * LDA;            // elements per LDS stage
-  static constexpr int PIPE = 2;                             // K slices held in registers
+#ifndef WM_PROJ_PIPE
+#define WM_PROJ_PIPE 2
+#endif
+  static constexpr int PIPE = WM_PROJ_PIPE;                  // K slices held in registers
   static_assert(BK % 16 == 0, "K slices hold whole k16 steps");
 };
 
@@ -113,13 +125,13 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_kernel(int M, int Nout, int K
     for (int f = 0; f < C::FX; ++f) {
       const int idx = tid + f * C::NT;
       if (C::NTOK * C::CPR % C::NT == 0 || idx < C::NTOK * C::CPR)
-        st_frag<T>(Xs + (idx / C::CPR) * C::LDA + (idx % C::CPR) * 8, x_in[f]);
+        st_frag<T>(Xs + C::chunk_at(idx / C::CPR, idx % C::CPR), x_in[f]);
     }
 #pragma unroll
     for (int f = 0; f < C::FW; ++f) {
       const int idx = tid + f * C::NT;
       if (C::OT * C::CPR % C::NT == 0 || idx < C::OT * C::CPR)
-        st_frag<T>(Ws + (idx / C::CPR) * C::LDA + (idx % C::CPR) * 8, w_in[f]);
+        st_frag<T>(Ws + C::chunk_at(idx / C::CPR, idx % C::CPR), w_in[f]);
     }
   };
   auto compute = [&](int buf) {
@@ -130,10 +142,10 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_kernel(int M, int Nout, int K
       frag_t<T> a[C::WO], b[C::WN];
 #pragma unroll
       for (int i = 0; i < C::WO; ++i)
-        a[i] = ld_frag<T>(Ws + (32 * (wo * C::WO + i) + r) * C::LDA + 16 * ks + 8 * h);
+        a[i] = ld_frag<T>(Ws + C::chunk_at(32 * (wo * C::WO + i) + r, 2 * ks + h));
 #pragma unroll
       for (int j = 0; j < C::WN; ++j)
-        b[j] = ld_frag<T>(Xs + (32 * (wn * C::WN + j) + r) * C::LDA + 16 * ks + 8 * h);
+        b[j] = ld_frag<T>(Xs + C::chunk_at(32 * (wn * C::WN + j) + r, 2 * ks + h));
 #pragma unroll
       for (int i = 0; i < C::WO; ++i)
 #pragma unroll

@@ -200,9 +200,6 @@ __device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, in
         }
       }
     }
-    // one token block at a time: hoisting the next block's accumulator reads and
-    // loads above this point would hold them all in registers at once
-    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -382,7 +379,10 @@ constexpr int kNoSegments = 1 << 30;
 // Tile shapes. Large token counts: 128 channels x 256 tokens per block, 64 x 128
 // per wave (bf16). Few tokens (decode): 128 x 64. fp32 halves the token tile.
 template <typename T, bool FEW> struct ProjShape;
-template <> struct ProjShape<bf16, false> { using C = ProjCfg<bf16, 32, 2, 2, 2, 4>; };
+#ifndef WM_PROJ_BF16
+#define WM_PROJ_BF16 32, 2, 2, 2, 4
+#endif
+template <> struct ProjShape<bf16, false> { using C = ProjCfg<bf16, WM_PROJ_BF16>; };
 template <> struct ProjShape<bf16, true> { using C = ProjCfg<bf16, 32, 2, 2, 2, 1>; };
 template <> struct ProjShape<float, false> { using C = ProjCfg<float, 32, 2, 2, 2, 2>; };
 template <> struct ProjShape<float, true> { using C = ProjCfg<float, 32, 2, 2, 2, 1>; };
@@ -460,6 +460,8 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
 // coefficients of one layer with JC/4 broadcast loads. For each branch the
 // thread scales a layer's 8 columns by the gain once and accumulates them into
 // all JC channels, then stores the channels and their sums of squares.
+constexpr int kMixBatch = 12;
+
 template <typename T, int JC>
 __global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* __restrict__ H,
                                                   const float* __restrict__ rinv,
@@ -474,8 +476,22 @@ __global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* __restrict_
   float* part = coef + 2 * L * kp;                                             // [2 waves][2k]
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
 
-  const T* hsrc = H + n * L * D;
-  for (int e = tid * 8; e < L * D; e += 128 * 8) st_frag<T>(hs + e, ld_frag<T>(hsrc + e));
+  // The token's L states go to LDS in batches of kMixBatch loads per thread, all in
+  // flight together (past the row they read zeros through the buffer view).
+  const auto hv = make_view(H + n * L * D, (uint32_t)((long)L * D * sizeof(T)));
+  for (int e0 = tid * 8; e0 < L * D; e0 += 128 * 8 * kMixBatch) {
+    frag_t<T> v[kMixBatch];
+#pragma unroll
+    for (int b = 0; b < kMixBatch; ++b) {
+      const int e = e0 + b * 128 * 8;
+      v[b] = buf_frag<T>(hv, e < L * D ? (uint32_t)e * (uint32_t)sizeof(T) : kOffOob);
+    }
+#pragma unroll
+    for (int b = 0; b < kMixBatch; ++b) {
+      const int e = e0 + b * 128 * 8;
+      if (e < L * D) st_frag<T>(hs + e, v[b]);
+    }
+  }
   for (int e = tid; e < 2 * L * kp; e += 128) coef[e] = 0.f;
   __syncthreads();
   if (tid < 2 * k) {
@@ -549,17 +565,231 @@ __global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* __restrict_
   }
 }
 
-static int mix_chunk(int k) { return k <= 4 ? 4 : k <= 8 ? 8 : k <= 12 ? 12 : 16; }
+// Channels per pass of the VALU mix: 4 keeps the accumulators small enough for
+// several blocks per SIMD (the kernel waits on memory more than it computes).
+static int mix_chunk(int) { return 4; }
 
 size_t mix_smem_bytes(int L, int k, int D, size_t es) {
   int jc = mix_chunk(k), kp = (k + jc - 1) / jc * jc;
   return ((size_t)L * D * es + 15) / 16 * 16 + sizeof(float) * (2 * (size_t)L * kp + 4 * k);
 }
 
+// ---------------------------------------------------------- mix (MFMA)
+// The bf16 mix as a batch of small matrix products on the matrix cores: for
+// token n and branch br, mixed^T[e][j] = sum_l Hh[l][e] C[j][l] with
+// Hh = g_pre[br] * h_n (rounded to bf16 once, staged in LDS) and
+// C[j][l] = alpha[br][n][j][l] / RMS(h_l), split into bf16 hi + lo parts so the
+// coefficients keep about 16 significant bits. One 16x16x32 MFMA covers 16
+// states e, 16 channels j and all L <= 32 layers; lane group g of the operand
+// takes layers g + 4t (t = 0..7), which spreads its LDS gathers over all banks.
+// A block of 256 threads walks kMixTok consecutive tokens; the next token's
+// states and coefficients are fetched while the current token's second branch
+// is multiplied. In softmax mode alpha is normalised beforehand
+// (softmax_rows_kernel).
+constexpr int kMixTok = 8;
+constexpr int kMixCoefLd = 40;  // LDS row stride of the coefficient operands (elements)
+constexpr int kMixCoefPer = 4;  // coefficient entries per thread (2kL <= 1024)
+
+__host__ __device__ static int mix_mfma_ldh(int D) { return D + 16; }  // LDS row stride of the staged states
+static size_t mix_mfma_smem(const Shape& sh) {
+  const int JT = (sh.k + 15) / 16;
+  return (size_t)sh.L * mix_mfma_ldh(sh.D) * 2 + 2 * 2 * 16 * JT * kMixCoefLd * 2 +
+         4 * 2 * 16 * JT * 4;
+}
+static bool mix_mfma_fits(const Shape& sh) {
+  return sh.L <= 32 && sh.k <= 32 && 2 * sh.k * sh.L <= 256 * kMixCoefPer && sh.D % 16 == 0 &&
+         mix_mfma_smem(sh) <= 65536;
+}
+
+template <int JT, int NCH>
+__global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __restrict__ H,
+                                                       const float* __restrict__ rinv,
+                                                       const bf16* __restrict__ g_pre,
+                                                       float* alpha, bf16* __restrict__ mixed,
+                                                       float* __restrict__ rinv_mid) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int L = sh.L, k = sh.k, D = sh.D, N = sh.N(), kL = k * L;
+  const int LDH = mix_mfma_ldh(D), DG = D / 8, chunks = L * DG;
+  bf16* Hs = (bf16*)smem;                                       // [L][LDH]
+  bf16* Cs = Hs + (size_t)L * LDH;                              // [2 br][2 hi/lo][16 JT][LD]
+  float* part = (float*)(Cs + 2 * 2 * 16 * JT * kMixCoefLd);    // [4 waves][2 br][16 JT]
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = lane >> 4, jj = lane & 15;
+  const int n_beg = blockIdx.x * kMixTok, n_end = min(N, n_beg + kMixTok);
+
+  // coefficient rows j >= k stay zero
+  for (int e = tid; e < 2 * 2 * 16 * JT * kMixCoefLd; e += 256) Cs[e] = (bf16)0.f;
+
+  // this thread's chunks: c = tid + 256 i -> layer c / DG, states 8 (c % DG) .. + 7
+  frag_t<bf16> hv[NCH];
+  // linear mixing: coefficient entries x = tid + 256 i -> (br, j, l), x < 2kL <= kMixCoefMax
+  float av[kMixCoefPer], rv[kMixCoefPer];
+  auto fetch = [&](long n) {
+    const auto view = make_view(H + n * L * D, (uint32_t)((long)L * D * 2));
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + 256 * i;
+      const int l = c / DG, eg = c - l * DG;
+      hv[i] = buf_frag<bf16>(view, c < chunks ? (uint32_t)(l * D + 8 * eg) * 2u : kOffOob);
+    }
+    {
+#pragma unroll
+      for (int i = 0; i < kMixCoefPer; ++i) {
+        const int x = min(tid + 256 * i, 2 * kL - 1);
+        const int br = x / kL, jl = x - br * kL, l = jl % L;
+        av[i] = alpha[((long)br * N + n) * kL + jl];
+        rv[i] = rinv[n * L + l];
+      }
+    }
+  };
+  if (n_beg < n_end) fetch(n_beg);
+  __syncthreads();
+
+  for (int n = n_beg; n < n_end; ++n) {
+    // coefficients of both branches (alpha is already normalised in softmax mode)
+    {
+#pragma unroll
+      for (int i = 0; i < kMixCoefPer; ++i) {
+        const int x = tid + 256 * i;
+        if (x < 2 * kL) {
+          const int br = x / kL, jl = x - br * kL, j = jl / L, l = jl - j * L;
+          const int slot = 8 * (l & 3) + (l >> 2);  // slot 8g + t holds layer g + 4t
+          const float c = av[i] * rv[i];
+          const bf16 ch = (bf16)c;
+          Cs[((br * 2 + 0) * 16 * JT + j) * kMixCoefLd + slot] = ch;
+          Cs[((br * 2 + 1) * 16 * JT + j) * kMixCoefLd + slot] = (bf16)(c - (float)ch);
+        }
+      }
+    }
+#pragma unroll 1
+    for (int br = 0; br < 2; ++br) {
+      // stage g_pre[br] * h as bf16. Branch-free, so the gain loads stay in flight
+      // together: chunks past the end read zeros and land in row 0's padding
+      // (columns D .. D+7, never read).
+      {
+        const auto gview = make_view(g_pre + (long)br * L * D, (uint32_t)((long)L * D * 2));
+        bf16x8 gv[NCH];
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+          const int c = tid + 256 * i;
+          const int l = c / DG, eg = c - l * DG;
+          gv[i] = buf_frag<bf16>(gview, c < chunks ? (uint32_t)(l * D + 8 * eg) * 2u : kOffOob);
+        }
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+          const int c = tid + 256 * i;
+          const int l = c / DG, eg = c - l * DG;
+          bf16x8 v;
+#pragma unroll
+          for (int t = 0; t < 8; ++t) v[t] = (bf16)((float)hv[i][t] * (float)gv[i][t]);
+          *(bf16x8*)(Hs + (c < chunks ? l * LDH + 8 * eg : D)) = v;
+        }
+      }
+      if (br == 1 && n + 1 < n_end) fetch(n + 1);  // the states are staged: refill
+      __syncthreads();
+
+      bf16x8 bh[JT], bl[JT];
+      float ss[JT];
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        bh[jt] = *(const bf16x8*)(Cs + ((br * 2 + 0) * 16 * JT + 16 * jt + jj) * kMixCoefLd + 8 * g);
+        bl[jt] = *(const bf16x8*)(Cs + ((br * 2 + 1) * 16 * JT + 16 * jt + jj) * kMixCoefLd + 8 * g);
+        ss[jt] = 0.f;
+      }
+#pragma unroll 3
+      for (int eb = w; eb < D / 16; eb += 4) {
+        bf16x8 a;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int l = g + 4 * t;
+          const bf16 v = Hs[min(l, L - 1) * LDH + 16 * eb + jj];
+          a[t] = l < L ? v : (bf16)0.f;
+        }
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh[jt], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl[jt], acc, 0, 0, 0);
+          // acc[t]: state 16 eb + 4 g + t of channel 16 jt + jj
+          const int j = 16 * jt + jj;
+          if (j < k) {
+            bf16x4 o;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              o[t] = (bf16)acc[t];
+              ss[jt] += acc[t] * acc[t];
+            }
+            *(bf16x4*)(mixed + (((long)br * k + j) * N + n) * D + 16 * eb + 4 * g) = o;
+          }
+        }
+      }
+      // sum of squares of channel j over the wave's states: the 4 lane groups hold parts
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        float v = ss[jt];
+        v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 32, 64);
+        if (g == 0) part[(w * 2 + br) * 16 * JT + 16 * jt + jj] = v;
+      }
+      __syncthreads();  // Hs is rewritten next; part is complete after the second branch
+    }
+    if (tid < 2 * k) {
+      const int br = tid / k, j = tid - br * k;
+      float v = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < 4; ++ww) v += part[(ww * 2 + br) * 16 * JT + j];
+      rinv_mid[((long)br * k + j) * N + n] = 1.0f / sqrtf(v / (float)D + sh.eps);
+    }
+  }
+}
+
+// alpha[r][0..L) <- softmax over the row, for rows r < rows (in place)
+__global__ __launch_bounds__(256) void softmax_rows_kernel(float* alpha, long rows, int L) {
+  const long r = (long)blockIdx.x * 256 + threadIdx.x;
+  if (r >= rows) return;
+  float* row = alpha + r * L;
+  float mx = row[0];
+  for (int l = 1; l < L; ++l) mx = fmaxf(mx, row[l]);
+  float z = 0.f;
+  for (int l = 0; l < L; ++l) z += expf(row[l] - mx);
+  const float iz = 1.0f / z;
+  for (int l = 0; l < L; ++l) row[l] = expf(row[l] - mx) * iz;
+}
+
+template <int JT>
+static void mix_mfma_launch(const Shape& sh, const bf16* H, const float* rinv, const bf16* g_pre,
+                            float* alpha, bf16* mixed, float* rinv_mid, hipStream_t s) {
+  const int nch = (sh.L * (sh.D / 8) + 255) / 256;
+  if (sh.mix_softmax) {
+    const long rows = 2L * sh.N() * sh.k;
+    hipLaunchKernelGGL(softmax_rows_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s,
+                       alpha, rows, sh.L);
+  }
+  const dim3 grid((sh.N() + kMixTok - 1) / kMixTok), block(256);
+  const size_t smem = mix_mfma_smem(sh);
+#define WM_MIX_GO(NC)                                                                          \
+  hipLaunchKernelGGL((mix_mfma_kernel<JT, NC>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, \
+                     mixed, rinv_mid)
+  if (nch <= 2) WM_MIX_GO(2);
+  else if (nch <= 4) WM_MIX_GO(4);
+  else if (nch <= 6) WM_MIX_GO(6);
+  else if (nch <= 8) WM_MIX_GO(8);
+  else if (nch <= 12) WM_MIX_GO(12);
+  else WM_MIX_GO(16);
+#undef WM_MIX_GO
+}
+
 template <typename T>
 void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
                 T* mixed, float* rinv_mid, hipStream_t s) {
   if (sh.N() <= 0) return;
+  if constexpr (sizeof(T) == 2) {
+    if (mix_mfma_fits(sh)) {
+      if (sh.k <= 16) mix_mfma_launch<1>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
+      else mix_mfma_launch<2>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
+      return;
+    }
+  }
   size_t smem = mix_smem_bytes(sh.L, sh.k, sh.D, sizeof(T));
   dim3 grid(sh.N()), block(128);
   switch (mix_chunk(sh.k)) {
