@@ -12,7 +12,8 @@
 // query's scores in registers (row max and sum need one cross-half exchange),
 // then O^T = V^T P^T with P^T taken straight from those registers (the MFMA
 // k-slot order is chosen to match; see wm_device.hpp). K blocks are staged
-// row-major and V blocks transposed in LDS.
+// row-major in LDS; bf16 V blocks too, read as V^T fragments with the transposing
+// LDS read (fp32 V is stored transposed).
 //
 // Decode form (attend_decode + combine): split-S over the cache, one
 // workgroup per (split, channel, sequence, KV head) serving every query row
@@ -60,12 +61,17 @@ template <typename T, int DH> struct PrefillCfg {
   static constexpr int BKV = 64;        // keys per block
   static constexpr int PAD = sizeof(T) == 2 ? 8 : 4;
   static constexpr int LDK = DH + PAD;   // Ks: [BKV][LDK]
-  static constexpr int LDV = BKV + PAD;  // Vt: [DH][LDV]
+  // bf16 V is staged row-major like K ([BKV][LDV], read transposed by ds_read_b64_tr_b16);
+  // fp32 V is stored transposed ([DH][LDV])
+  static constexpr bool VTR = sizeof(T) == 2;
+  static constexpr int LDV = VTR ? DH + 16 : BKV + PAD;
+  static constexpr int VS = VTR ? BKV * LDV : DH * LDV;  // V stage (elements)
   static constexpr int NKS = DH / 16;    // k16 steps of Q K^T
   static constexpr int NDT = DH / 32;    // 32-row tiles of O^T
   static constexpr int KIT = BKV * DH / 8;             // K fragments per block
   static constexpr int KFR = (KIT + NT - 1) / NT;      // ... per thread
-  static constexpr int VIT = (BKV / 2) * (DH / 8);     // (key pair, 8-column) items per block
+  static constexpr int VIT = VTR ? KIT : (BKV / 2) * (DH / 8);  // V items per block (16-B
+                                                                 // fragments, or key pairs)
   static constexpr int VPT = (VIT + NT - 1) / NT;      // ... per thread
   static constexpr float kRescale = 8.0f;              // log2 headroom before rescaling
 };
@@ -79,6 +85,21 @@ __device__ __forceinline__ void st_pair_t(float* vt, int ld, const f32x8& a, con
   typedef __attribute__((ext_vector_type(2))) float f32x2;
 #pragma unroll
   for (int i = 0; i < 8; ++i) *(f32x2*)(vt + i * ld) = f32x2{a[i], b[i]};
+}
+
+// V^T fragment for keys kb + 4h + {0..3, 8..11} and value column 32 dt + r from a
+// row-major bf16 V tile, with two transposing LDS reads: within each 16-lane group,
+// lane i's element t comes from element i % 4 of the 8-byte chunk addressed by lane
+// 4t + i / 4, so lane j addresses key (kb + 4h + 8s + j / 4), columns
+// 32 dt + 16 (group & 1) + 4 (j % 4) .. + 3, and receives 4 keys of its own column.
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x8 ld_vt_tr(const bf16* vs, int ldv, int kb, int dt, int lane) {
+  const int j = lane & 15, grp = lane >> 4, h = lane >> 5;
+  const bf16* p = vs + (kb + 4 * h + (j >> 2)) * ldv + 32 * dt + 16 * (grp & 1) + 4 * (j & 3);
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * ldv));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // One 64-key block for one wave (QT tiles of 32 queries): two 32-key halves, each
@@ -143,8 +164,13 @@ __device__ __forceinline__ void attend_block(
       const int kc = 32 * kt + 16 * hf + 4 * h;
 #pragma unroll
       for (int dt = 0; dt < C::NDT; ++dt) {
-        const T* vrow = vt_ + (32 * dt + r) * C::LDV;
-        frag_t<T> vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
+        frag_t<T> vf;
+        if constexpr (C::VTR) {
+          vf = ld_vt_tr(vt_, C::LDV, 32 * kt + 16 * hf, dt, 32 * h + r);
+        } else {
+          const T* vrow = vt_ + (32 * dt + r) * C::LDV;
+          vf = ld_frag_4_4<T>(vrow + kc, vrow + kc + 8);
+        }
 #pragma unroll
         for (int qt = 0; qt < C::QT; ++qt) o[dt][qt] = mma32(o[dt][qt], vf, pf[qt][hf]);
       }
@@ -157,7 +183,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   using C = PrefillCfg<T, DH>;
   constexpr int QT = C::QT;
   __shared__ __align__(16) T Ks[2][C::BKV * C::LDK];
-  __shared__ __align__(16) T Vt[2][DH * C::LDV];
+  __shared__ __align__(16) T Vt[2][C::VS];
 
   // 1-D grid over (consumer, sequence, head, query tile); each XCD takes a contiguous
   // run of heads, and a head's tiles run longest causal rows first on one L2
@@ -228,8 +254,9 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   const int wfree = ctx + qw0 + incl;                  // slots < wfree are visible to all its rows
   const int nblk = (kend + C::BKV - 1) / C::BKV;
 
-  // staged next block: K fragments (row-major copy) and V key pairs (transposed store)
-  frag_t<T> kreg[C::KFR], vreg[C::VPT][2];
+  // staged next block: K fragments (row-major copy) and V fragments (row-major, bf16)
+  // or V key pairs (transposed store, fp32)
+  frag_t<T> kreg[C::KFR], vreg[C::VPT][C::VTR ? 1 : 2];
   // the (channel, sequence, KV head) slice through buffer views: slots at or past kend
   // read as zeros without a branch
   const __amdgpu_buffer_rsrc_t kview = make_view(Kb, (uint32_t)a.S_cap * DH * sizeof(T));
@@ -246,10 +273,15 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
 #pragma unroll
     for (int i = 0; i < C::VPT; ++i) {
       int it = tid + C::NT * i;
-      int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2), s = k0 + 2 * kp;
       bool ok = it < C::VIT;
-      vreg[i][0] = buf_frag<T>(vview, ok ? slot_off(s, 8 * dg) : kOffOob);
-      vreg[i][1] = buf_frag<T>(vview, ok ? slot_off(s + 1, 8 * dg) : kOffOob);
+      if constexpr (C::VTR) {
+        int key = it / (DH / 8), dc = (it % (DH / 8)) * 8;
+        vreg[i][0] = buf_frag<T>(vview, ok ? slot_off(k0 + key, dc) : kOffOob);
+      } else {
+        int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2), s = k0 + 2 * kp;
+        vreg[i][0] = buf_frag<T>(vview, ok ? slot_off(s, 8 * dg) : kOffOob);
+        vreg[i][1] = buf_frag<T>(vview, ok ? slot_off(s + 1, 8 * dg) : kOffOob);
+      }
     }
   };
   auto stage = [&](int buf) {
@@ -262,8 +294,13 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
     for (int i = 0; i < C::VPT; ++i) {
       int it = tid + C::NT * i;
       if (it < C::VIT) {
-        int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2);
-        st_pair_t(&Vt[buf][(8 * dg) * C::LDV + 2 * kp], C::LDV, vreg[i][0], vreg[i][1]);
+        if constexpr (C::VTR) {
+          int key = it / (DH / 8), dc = (it % (DH / 8)) * 8;
+          st_frag<T>(&Vt[buf][key * C::LDV + dc], vreg[i][0]);
+        } else {
+          int kp = it % (C::BKV / 2), dg = it / (C::BKV / 2);
+          st_pair_t(&Vt[buf][(8 * dg) * C::LDV + 2 * kp], C::LDV, vreg[i][0], vreg[i][1]);
+        }
       }
     }
   };
