@@ -181,4 +181,142 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_kernel(int M, int Nout, int K
   epi.template finish<C>(g, ow0, nw0, acc, lane, est);
 }
 
+// bf16 variant whose K slices travel straight from memory into LDS
+// (buffer_load ... lds: each wave instruction fills 1 KB of LDS, lane l's 16 bytes
+// at 16 l), so nothing is staged in registers and the prefetch runs two slices
+// ahead through three LDS stages. A stage holds the W and X tiles as 64-byte rows
+// in the swizzled chunk order of ProjCfg::chunk_at; a lane of the instruction that
+// fills rows R .. R+15 fetches row R + l/4, logical chunk (l%4) ^ swizzle, so the
+// copy lands already swizzled. Loads past the matrix or past K read zeros.
+// The loads are issued from inline asm and waited for with an explicit vmcnt:
+// the compiler, seeing LDS DMA in flight, would otherwise wait for every
+// outstanding load (the prefetched slices too) before each barrier.
+template <class C> struct DmaCfg {
+  static constexpr int NS = 3;                              // LDS stages
+  static constexpr int ROWS = C::OT + C::NTOK;              // tile rows per stage
+  static constexpr int NW = C::NT / 64;
+  static constexpr int NI = (ROWS / 16 + NW - 1) / NW;      // 16-row instructions per wave
+  // Every wave issues exactly NI loads per slice (so one vmcnt fits all waves); blocks
+  // past the tile rows load zeros into padding rows that are never read.
+  static constexpr int ROWS_PAD = 16 * NW * NI;
+  static constexpr int STAGE_BYTES = ROWS_PAD * 64;
+  static_assert(C::SWZ && C::LDA == 32, "64-byte swizzled rows");
+  static_assert(C::OT % 16 == 0 && C::NTOK % 16 == 0, "16-row instruction blocks");
+  static_assert(NI <= 15, "vmcnt encodes at most 15 here");
+};
+
+__device__ __forceinline__ void lds_dma16(uint32_t lds_addr, uint32_t voff,
+                                          __amdgpu_buffer_rsrc_t rsrc) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone), n < 16
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+template <class C, typename T, class XLoad, class WLoad, class Epi>
+__global__ __launch_bounds__(C::NT) void proj_gemm_dma_kernel(int M, int Nout, int K, int groups,
+                                                              int seg_len, int kspan, XLoad xl,
+                                                              WLoad wl, Epi epi) {
+  using D = DmaCfg<C>;
+  __shared__ __align__(16) T smem[D::NS * D::ROWS_PAD * 32];
+
+  const int ot = (Nout + C::OT - 1) / C::OT, mt = (M + C::NTOK - 1) / C::NTOK;
+  const int tile = xcd_tile(blockIdx.x, groups * mt * ot);
+  const int g = tile / (mt * ot);
+  const int n0 = (tile / ot % mt) * C::NTOK, o0 = (tile % ot) * C::OT;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, held in an SGPR
+  const int wo = w % C::WGO, wn = w / C::WGO;
+  const int h = lane >> 5, r = lane & 31;
+
+  const RowsView xv = xl.view(g), wv = wl.view(g);
+  const int kbeg = kspan > 0 ? g * kspan : 0;
+  const int kend = kspan > 0 ? min(K, kbeg + kspan) : K;
+
+  // this lane's row offset (k = 0) and chunk for each of the wave's instructions;
+  // rows 0 .. OT-1 of a stage are W rows, the rest X rows
+  uint32_t roff[D::NI];
+#pragma unroll
+  for (int i = 0; i < D::NI; ++i) {
+    const int blk = w * D::NI + i, row = 16 * blk + lane / 4;
+    const int c = (lane & 3) ^ ((row >> 1) & 3);
+    bool ok;
+    uint32_t off;
+    if (row < C::OT) {
+      ok = o0 + row < Nout;
+      off = (uint32_t)(o0 + row) * wv.row_bytes;
+    } else {
+      ok = n0 + (row - C::OT) < M;
+      off = (uint32_t)(n0 + row - C::OT) * xv.row_bytes;
+    }
+    ok = ok && blk < D::ROWS / 16;
+    roff[i] = ok ? off + 16u * c : kOffOob;
+  }
+  const uint32_t smem_base = (uint32_t)(uintptr_t)smem;
+  auto issue = [&](int kb, int stage) {  // slice kb into LDS stage `stage`
+    const int k0 = kb * C::BK;
+    const bool kin = k0 < kend;
+    const uint32_t xs = kin ? xl.slice(k0) : 0u, ws = kin ? wl.slice(k0) : 0u;
+#pragma unroll
+    for (int i = 0; i < D::NI; ++i) {
+      const int blk = w * D::NI + i;  // wave-uniform
+      const bool wrow = 16 * blk < C::OT;
+      const uint32_t lds = __builtin_amdgcn_readfirstlane(smem_base + stage * D::STAGE_BYTES +
+                                                          blk * 1024);
+      const uint32_t off = kin && roff[i] != kOffOob ? roff[i] + (wrow ? ws : xs) : kOffOob;
+      lds_dma16(lds, off, wrow ? wv.rsrc : xv.rsrc);
+    }
+  };
+
+  f32x16 acc[C::WO][C::WN];
+#pragma unroll
+  for (int i = 0; i < C::WO; ++i)
+#pragma unroll
+    for (int j = 0; j < C::WN; ++j) acc[i][j] = zero16();
+
+  auto compute = [&](int stage) {
+    const T* Ws = smem + stage * D::ROWS_PAD * 32;
+    const T* Xs = Ws + C::OT * 32;
+#pragma unroll
+    for (int ks = 0; ks < C::BK / 16; ++ks) {
+      frag_t<T> a[C::WO], b[C::WN];
+#pragma unroll
+      for (int i = 0; i < C::WO; ++i)
+        a[i] = ld_frag<T>(Ws + C::chunk_at(32 * (wo * C::WO + i) + r, 2 * ks + h));
+#pragma unroll
+      for (int j = 0; j < C::WN; ++j)
+        b[j] = ld_frag<T>(Xs + C::chunk_at(32 * (wn * C::WN + j) + r, 2 * ks + h));
+#pragma unroll
+      for (int i = 0; i < C::WO; ++i)
+#pragma unroll
+        for (int j = 0; j < C::WN; ++j) acc[i][j] = mma32(acc[i][j], a[i], b[j]);
+    }
+  };
+
+  const int ow0 = o0 + 32 * C::WO * wo, nw0 = n0 + 32 * C::WN * wn;
+  typename Epi::State est;
+  epi.template begin<C>(g, nw0, lane, est);
+
+  const int kb_beg = kbeg / C::BK, kb_end = (kend + C::BK - 1) / C::BK;
+  issue(kb_beg, 0);
+  issue(kb_beg + 1, 1);
+  for (int kb = kb_beg, st = 0; kb < kb_end; ++kb, st = st == D::NS - 1 ? 0 : st + 1) {
+    // this wave's loads of slice kb are done once only the next slice's remain
+    wait_vmcnt<D::NI>();
+    __syncthreads();  // every wave's slice kb is in LDS, and slice kb-1 is consumed
+    issue(kb + 2, st == 0 ? 2 : st - 1);  // into the stage slice kb-1 used
+    compute(st);
+    if ((kb + 1) % seg_len == 0 && kb + 1 < kb_end)
+      epi.template segment<C>(g, (kb + 1) / seg_len, nw0, acc, lane, est);
+  }
+  wait_vmcnt<0>();  // the trailing prefetches (zeros) land before the block ends
+  epi.template finish<C>(g, ow0, nw0, acc, lane, est);
+}
+
 }  // namespace wm

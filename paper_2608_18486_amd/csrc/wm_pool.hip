@@ -371,16 +371,22 @@ template <class C> static unsigned proj_blocks(int M, int Nout, int groups) {
 template <class C, typename T, class XL, class WL, class Epi>
 static void launch_proj(int M, int Nout, int K, int groups, int seg_len, int kspan,
                         const XL& xl, const WL& wl, const Epi& e, hipStream_t s) {
-  hipLaunchKernelGGL((proj_gemm_kernel<C, T, XL, WL, Epi>), dim3(proj_blocks<C>(M, Nout, groups)),
-                     dim3(C::NT), 0, s, M, Nout, K, groups, seg_len, kspan, xl, wl, e);
+  if constexpr (C::SWZ) {
+    hipLaunchKernelGGL((proj_gemm_dma_kernel<C, T, XL, WL, Epi>),
+                       dim3(proj_blocks<C>(M, Nout, groups)), dim3(C::NT), 0, s, M, Nout, K,
+                       groups, seg_len, kspan, xl, wl, e);
+  } else {
+    hipLaunchKernelGGL((proj_gemm_kernel<C, T, XL, WL, Epi>), dim3(proj_blocks<C>(M, Nout, groups)),
+                       dim3(C::NT), 0, s, M, Nout, K, groups, seg_len, kspan, xl, wl, e);
+  }
 }
 constexpr int kNoSegments = 1 << 30;
 
-// Tile shapes. Large token counts: 128 channels x 256 tokens per block, 64 x 128
-// per wave (bf16). Few tokens (decode): 128 x 64. fp32 halves the token tile.
+// Tile shapes. Large token counts: 256 channels x 256 tokens per block of 8 waves,
+// 64 x 128 per wave (bf16). Few tokens (decode): 128 x 64. fp32: 128 x 128, 4 waves.
 template <typename T, bool FEW> struct ProjShape;
 #ifndef WM_PROJ_BF16
-#define WM_PROJ_BF16 32, 2, 2, 2, 4
+#define WM_PROJ_BF16 32, 4, 2, 2, 4
 #endif
 template <> struct ProjShape<bf16, false> { using C = ProjCfg<bf16, WM_PROJ_BF16>; };
 template <> struct ProjShape<bf16, true> { using C = ProjCfg<bf16, 32, 2, 2, 2, 1>; };
@@ -389,7 +395,10 @@ template <> struct ProjShape<float, true> { using C = ProjCfg<float, 32, 2, 2, 2
 // Router: 96 channels x 128 tokens per block (the channel count 2kL is small and
 // often a multiple of 96), 96 x 32 per wave.
 template <typename T, bool FEW> struct RouterShape;
-template <> struct RouterShape<bf16, false> { using C = ProjCfg<bf16, 32, 1, 4, 3, 1>; };
+#ifndef WM_ROUTER_BF16
+#define WM_ROUTER_BF16 32, 1, 4, 3, 1
+#endif
+template <> struct RouterShape<bf16, false> { using C = ProjCfg<bf16, WM_ROUTER_BF16>; };
 template <> struct RouterShape<bf16, true> { using C = ProjCfg<bf16, 32, 1, 2, 3, 1>; };
 template <> struct RouterShape<float, false> { using C = ProjCfg<float, 32, 1, 4, 3, 1>; };
 template <> struct RouterShape<float, true> { using C = ProjCfg<float, 32, 1, 2, 3, 1>; };
@@ -402,8 +411,11 @@ size_t router_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.L * sh.Lp * s
 // Layers per K split: enough blocks to cover the chip, splitting K at layer
 // boundaries when the token and channel tiles alone give few blocks.
 static int router_layers_per_split(const Shape& sh) {
-  const int tok = sh.N() <= kFewTokens ? 64 : 128;
-  const long blocks = (long)((sh.N() + tok - 1) / tok) * ((2 * sh.k * sh.L + 95) / 96);
+  using CF = RouterShape<bf16, false>::C;
+  using CD = RouterShape<bf16, true>::C;
+  const bool few = sh.N() <= kFewTokens;
+  const int tok = few ? CD::NTOK : CF::NTOK, och = few ? CD::OT : CF::OT;
+  const long blocks = (long)((sh.N() + tok - 1) / tok) * ((2 * sh.k * sh.L + och - 1) / och);
   int s = 1;
   while (s < sh.Lp && blocks * s < 512) s *= 2;
   return (sh.Lp + s - 1) / s;
