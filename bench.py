@@ -295,12 +295,14 @@ def main():
         achieved = b / t_dom / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    gemm = "proj_gemm_dma_kernel" if w.dtype == "bf16" else "proj_gemm_kernel"
+    mix = "mix_mfma_kernel" if (w.dtype == "bf16" and w.L <= 32 and w.k <= 32) else "mix_kernel"
     roof["kernel"] = {"attend": "attend_prefill_kernel" if w.T_new > 4 else
                       "attend_decode_kernel + attend_combine_kernel",
-                      "kv_project": "gemm_nt_kernel (K/V projection)",
-                      "q_project": "gemm_nt_kernel (Q projection)",
-                      "router": "gemm_nt_kernel (router)", "mix": "mix_kernel",
-                      "norms": "row_rms_kernel + rope_table_kernel"}[dom]
+                      "kv_project": gemm + " (K/V projection, after fold_gain_kernel)",
+                      "q_project": gemm + " (Q projection, after fold_gain_kernel)",
+                      "router": gemm + " (router, with router_fold/reduce kernels)",
+                      "mix": mix, "norms": "row_rms_kernel + rope_table_kernel"}[dom]
     roof["phase"] = dom
     roof["duration_ms"] = round(mean[dom], 4)
     roof["traffic"] = measured_traffic(w.name, dom)

@@ -399,8 +399,9 @@ __device__ __forceinline__ void merge_state(float& m, float& l, float* o, float 
 template <typename T, int DH, int NG>
 __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
   constexpr int LPS = DH / 8;    // lanes per cache slot (8 elements each)
-  constexpr int SPW = 64 / LPS;  // slots per wave per sweep
-  constexpr int U = 4;           // slots in flight per lane
+  constexpr int SPW = 64 / LPS;  // slots per wave per sweep step
+  constexpr int U = NG <= 2 ? 2 : 1;  // sweep steps per batch (U slots per lane)
+  constexpr int SPB = 4 * SPW * U;  // slots per batch of the 4 waves
   __shared__ float red[4][NG][DH + 2];
 
   const int split = blockIdx.x;
@@ -419,16 +420,20 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int sg = lane / LPS, c8 = lane % LPS;
   const float cl2 = a.scale_log2;
+  const float thresh = 8.0f / cl2;  // log2 headroom before a rescale
 
   const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
-  const T* Kb = a.Kc + cbase;
-  const T* Vb = a.Vc + cbase;
+  // the slice through buffer views: slots at or past s1 read zeros without a branch
+  const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)a.S_cap * DH * sizeof(T));
+  const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)a.S_cap * DH * sizeof(T));
+  auto slot_off = [&](int s) {
+    return s < s1 ? (uint32_t)(s * DH + 8 * c8) * (uint32_t)sizeof(T) : kOffOob;
+  };
 
   for (int g0 = 0; g0 < G; g0 += NG) {
     const int ng = min(NG, G - g0);
     float q[NG][8], m[NG], ls[NG], o[NG][8];
     int vis[NG];
-    long rowid[NG];
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       m[gi] = kNegBig;
@@ -439,51 +444,71 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
         int g = g0 + gi;
         int i = g % a.T_new, gq = (g / a.T_new) % grp, mi = g / (a.T_new * grp);
         int l = a.cg.members[off + mi], hq = kvh * grp + gq;
-        rowid[gi] = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + i;
-        load8(a.Q + rowid[gi] * DH + 8 * c8, q[gi]);
+        long rowid = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + i;
+        load8(a.Q + rowid * DH + 8 * c8, q[gi]);
         vis[gi] = ctx + i + incl;
       } else {
-        rowid[gi] = 0;
         vis[gi] = 0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) q[gi][i] = 0.f;
       }
     }
 
-    for (int sb = s0 + w * SPW * U; sb < s1; sb += 4 * SPW * U) {
-      float kv[U][8], vv[U][8];
-      int sl[U];
+    // raw K/V fragments of a batch (U slots per lane), double-buffered across batches
+    // (two batches per loop trip keep the buffer indices static)
+    frag_t<T> kr0[U], vr0[U], kr1[U], vr1[U];
+    auto fetch = [&](int sb, frag_t<T>* kr, frag_t<T>* vr) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        int s = sb + u * SPW + sg;
-        sl[u] = s;
-        if (s < s1) {
-          load8(Kb + (long)s * DH + 8 * c8, kv[u]);
-          load8(Vb + (long)s * DH + 8 * c8, vv[u]);
-        } else {
+        const uint32_t so = slot_off(sb + w * SPW * U + u * SPW + sg);
+        kr[u] = buf_frag<T>(kview, so);
+        vr[u] = buf_frag<T>(vview, so);
+      }
+    };
+    auto consume = [&](int sb, const frag_t<T>* kr, const frag_t<T>* vr) {
+      float p[U][NG];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) kv[u][i] = vv[u][i] = 0.f;
+      for (int u = 0; u < U; ++u) {
+        const int s = sb + w * SPW * U + u * SPW + sg;
+#pragma unroll
+        for (int gi = 0; gi < NG; ++gi) {
+          float d = 0.f;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) d += q[gi][i] * to_f32(kr[u][i]);
+#pragma unroll
+          for (int x = 1; x < LPS; x <<= 1) d += __shfl_xor(d, x, 64);
+          p[u][gi] = s < s1 && s < vis[gi] ? d : kNegBig;
         }
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+      for (int gi = 0; gi < NG; ++gi) {
+        float mx = p[0][gi];
 #pragma unroll
-        for (int gi = 0; gi < NG; ++gi) {
-          float p = 0.f;
+        for (int u = 1; u < U; ++u) mx = fmaxf(mx, p[u][gi]);
+        if (mx > m[gi] + thresh) {  // lazy rescale (per lane; merged exactly below)
+          const float al = fast_exp2((m[gi] - mx) * cl2);
+          ls[gi] *= al;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) p += q[gi][i] * kv[u][i];
-#pragma unroll
-          for (int x = 1; x < LPS; x <<= 1) p += __shfl_xor(p, x, 64);
-          const bool ok = sl[u] < s1 && sl[u] < vis[gi];
-          if (ok) {
-            float M = fmaxf(m[gi], p);
-            float al = fast_exp2((m[gi] - M) * cl2), pe = fast_exp2((p - M) * cl2);
-            ls[gi] = ls[gi] * al + pe;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) o[gi][i] = o[gi][i] * al + pe * vv[u][i];
-            m[gi] = M;
-          }
+          for (int i = 0; i < 8; ++i) o[gi][i] *= al;
+          m[gi] = mx;
         }
+        const float mc = m[gi] * cl2;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const float pe = p[u][gi] > 0.5f * kNegBig ? fast_exp2(p[u][gi] * cl2 - mc) : 0.f;
+          ls[gi] += pe;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) o[gi][i] += pe * to_f32(vr[u][i]);
+        }
+      }
+    };
+    // batches past the split read zeros (and are masked), so the loop runs in pairs
+    fetch(s0, kr0, vr0);
+    for (int sb = s0; sb < s1; sb += 2 * SPB) {
+      fetch(sb + SPB, kr1, vr1);
+      consume(sb, kr0, vr0);
+      fetch(sb + 2 * SPB, kr0, vr0);
+      consume(sb + SPB, kr1, vr1);
     }
     // merge the slot groups of the wave (lanes that share c8)
 #pragma unroll
