@@ -362,11 +362,24 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
 }
 
 // ------------------------------------------------------------------ decode
-constexpr int kSplitLen = 512;  // cache slots per split workgroup
+// Cache slots per split workgroup: long splits amortise a workgroup's set-up and its
+// partial-state write; they are halved (down to 256) while the grid of splits x
+// (channel, sequence, KV head) would hold fewer than kDecodeMinBlocks workgroups.
+constexpr int kSplitMax = 4096, kSplitMin = 256;
+constexpr long kDecodeMinBlocks = 4096;
+
+int decode_split_len(const Shape& sh) {
+  const long kend = (long)sh.ctx_max + sh.T_new;  // upper bound on visible slots
+  const long slices = (long)sh.k * sh.B * sh.Hkv;
+  int len = kSplitMax;
+  while (len > kSplitMin && slices * ((kend + len - 1) / len) < kDecodeMinBlocks) len /= 2;
+  return len;
+}
 
 int decode_splits(const Shape& sh) {
-  long kend = (long)sh.ctx_max + sh.T_new;  // upper bound on visible slots
-  int n = (int)((kend + kSplitLen - 1) / kSplitLen);
+  const long kend = (long)sh.ctx_max + sh.T_new;
+  const int len = decode_split_len(sh);
+  int n = (int)((kend + len - 1) / len);
   return n < 1 ? 1 : n;
 }
 
@@ -380,7 +393,7 @@ template <typename T> struct DecodeArgs {
   const int32_t* ctx_len;
   float* part;  // [L][B][Hq][T_new][nsplit][d + 2]: unnormalised o, m, l
   T* O;
-  int B, T_new, L, Hq, Hkv, S_cap, mask_paper, nsplit;
+  int B, T_new, L, Hq, Hkv, S_cap, mask_paper, nsplit, split_len;
   float scale_log2;
   LayerTable chan;
   ChannelGroups cg;
@@ -416,7 +429,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
   const int ctx = a.ctx_len ? a.ctx_len[b] : 0;
   const int incl = a.mask_paper ? 0 : 1;
   const int kend = min(ctx + a.T_new - 1 + incl, a.S_cap);
-  const int s0 = split * kSplitLen, s1 = min(s0 + kSplitLen, kend);
+  const int s0 = split * a.split_len, s1 = min(s0 + a.split_len, kend);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int sg = lane / LPS, c8 = lane % LPS;
   const float cl2 = a.scale_log2;
@@ -626,8 +639,8 @@ void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const Cha
                           const int32_t* ctx_len, float* partials, T* O, hipStream_t s) {
   if (sh.N() <= 0) return;
   DecodeArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, partials, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv,
-                  sh.S_cap, sh.mask_paper, decode_splits(sh), kLog2e / sqrtf((float)sh.d),
-                  chan_map, cg};
+                  sh.S_cap, sh.mask_paper, decode_splits(sh), decode_split_len(sh),
+                  kLog2e / sqrtf((float)sh.d), chan_map, cg};
   int maxmem = 0;
   for (int c = 0; c < sh.k; ++c) {
     int n = cg.offsets[c + 1] - cg.offsets[c];

@@ -13,6 +13,8 @@
 //                store happen in the epilogue
 //   q_project    the consumer's query (input norm, W^Q_l, q norm, RoPE), built
 //                the same way
+#include <algorithm>
+
 #include "wm_gemm.hpp"
 #include "wm_internal.hpp"
 
@@ -594,7 +596,7 @@ size_t mix_smem_bytes(int L, int k, int D, size_t es) {
 // coefficients keep about 16 significant bits. One 16x16x32 MFMA covers 16
 // states e, 16 channels j and all L <= 32 layers; lane group g of the operand
 // takes layers g + 4t (t = 0..7), which spreads its LDS gathers over all banks.
-// A block of 256 threads walks kMixTok consecutive tokens; the next token's
+// A block of 256 threads walks up to kMixTok consecutive tokens; the next token's
 // states and coefficients are fetched while the current token's second branch
 // is multiplied. In softmax mode alpha is normalised beforehand
 // (softmax_rows_kernel).
@@ -618,7 +620,7 @@ __global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __r
                                                        const float* __restrict__ rinv,
                                                        const bf16* __restrict__ g_pre,
                                                        float* alpha, bf16* __restrict__ mixed,
-                                                       float* __restrict__ rinv_mid) {
+                                                       float* __restrict__ rinv_mid, int tpb) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int L = sh.L, k = sh.k, D = sh.D, N = sh.N(), kL = k * L;
   const int LDH = mix_mfma_ldh(D), DG = D / 8, chunks = L * DG;
@@ -627,7 +629,7 @@ __global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __r
   float* part = (float*)(Cs + 2 * 2 * 16 * JT * kMixCoefLd);    // [4 waves][2 br][16 JT]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, jj = lane & 15;
-  const int n_beg = blockIdx.x * kMixTok, n_end = min(N, n_beg + kMixTok);
+  const int n_beg = blockIdx.x * tpb, n_end = min(N, n_beg + tpb);
 
   // coefficient rows j >= k stay zero
   for (int e = tid; e < 2 * 2 * 16 * JT * kMixCoefLd; e += 256) Cs[e] = (bf16)0.f;
@@ -777,11 +779,13 @@ static void mix_mfma_launch(const Shape& sh, const bf16* H, const float* rinv, c
     hipLaunchKernelGGL(softmax_rows_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s,
                        alpha, rows, sh.L);
   }
-  const dim3 grid((sh.N() + kMixTok - 1) / kMixTok), block(256);
+  // tokens per block: up to kMixTok, fewer when that would leave under ~2048 blocks
+  const int tpb = std::max(1, std::min(kMixTok, sh.N() / 2048));
+  const dim3 grid((sh.N() + tpb - 1) / tpb), block(256);
   const size_t smem = mix_mfma_smem(sh);
 #define WM_MIX_GO(NC)                                                                          \
   hipLaunchKernelGGL((mix_mfma_kernel<JT, NC>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, \
-                     mixed, rinv_mid)
+                     mixed, rinv_mid, tpb)
   if (nch <= 2) WM_MIX_GO(2);
   else if (nch <= 4) WM_MIX_GO(4);
   else if (nch <= 6) WM_MIX_GO(6);
