@@ -591,23 +591,25 @@ size_t mix_smem_bytes(int L, int k, int D, size_t es) {
 // ---------------------------------------------------------- mix (MFMA)
 // The bf16 mix as a batch of small matrix products on the matrix cores: for
 // token n and branch br, mixed^T[e][j] = sum_l Hh[l][e] C[j][l] with
-// Hh = g_pre[br] * h_n (rounded to bf16 once, staged in LDS) and
-// C[j][l] = alpha[br][n][j][l] / RMS(h_l), split into bf16 hi + lo parts so the
-// coefficients keep about 16 significant bits. One 16x16x32 MFMA covers 16
-// states e, 16 channels j and all L <= 32 layers; lane group g of the operand
-// takes layers g + 4t (t = 0..7), which spreads its LDS gathers over all banks.
+// Hh = g_pre[br] * h_n (rounded to bf16 once, staged in LDS row-major, one row
+// per layer) and C[j][l] = alpha[br][n][j][l] / RMS(h_l), split into bf16 hi + lo
+// parts so the coefficients keep about 16 significant bits. One 16x16x16 MFMA
+// covers 16 states e, 16 channels j and 16 layers; lane group g of its operand
+// takes layers 4g .. 4g+3 of its state column, which one transposing LDS read
+// (ds_read_b64_tr_b16) gathers from the row-major tile. The staged tile has L
+// rows plus one row of zeros that stands in for the layers past L.
 // A block of 256 threads walks up to kMixTok consecutive tokens; the next token's
 // states and coefficients are fetched while the current token's second branch
 // is multiplied. In softmax mode alpha is normalised beforehand
 // (softmax_rows_kernel).
 constexpr int kMixTok = 8;
-constexpr int kMixCoefLd = 40;  // LDS row stride of the coefficient operands (elements)
 constexpr int kMixCoefPer = 4;  // coefficient entries per thread (2kL <= 1024)
 
-__host__ __device__ static int mix_mfma_ldh(int D) { return D + 16; }  // LDS row stride of the staged states
+__host__ __device__ static int mix_mfma_ldh(int D) { return D + 16; }  // staged row stride
+__host__ __device__ static int mix_coef_ld(int LT) { return 16 * LT + 4; }
 static size_t mix_mfma_smem(const Shape& sh) {
-  const int JT = (sh.k + 15) / 16;
-  return (size_t)sh.L * mix_mfma_ldh(sh.D) * 2 + 2 * 2 * 16 * JT * kMixCoefLd * 2 +
+  const int JT = (sh.k + 15) / 16, LT = (sh.L + 15) / 16;
+  return (size_t)(sh.L + 1) * mix_mfma_ldh(sh.D) * 2 + 2 * 2 * 16 * JT * mix_coef_ld(LT) * 2 +
          4 * 2 * 16 * JT * 4;
 }
 static bool mix_mfma_fits(const Shape& sh) {
@@ -615,7 +617,10 @@ static bool mix_mfma_fits(const Shape& sh) {
          mix_mfma_smem(sh) <= 65536;
 }
 
-template <int JT, int NCH>
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <int JT, int LT, int NCH>
 __global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __restrict__ H,
                                                        const float* __restrict__ rinv,
                                                        const bf16* __restrict__ g_pre,
@@ -624,20 +629,31 @@ __global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __r
   extern __shared__ __align__(16) unsigned char smem[];
   const int L = sh.L, k = sh.k, D = sh.D, N = sh.N(), kL = k * L;
   const int LDH = mix_mfma_ldh(D), DG = D / 8, chunks = L * DG;
-  bf16* Hs = (bf16*)smem;                                       // [L][LDH]
-  bf16* Cs = Hs + (size_t)L * LDH;                              // [2 br][2 hi/lo][16 JT][LD]
-  float* part = (float*)(Cs + 2 * 2 * 16 * JT * kMixCoefLd);    // [4 waves][2 br][16 JT]
+  constexpr int CLD = 16 * LT + 4;
+  bf16* Hs = (bf16*)smem;                                     // [L + 1][LDH], row L zero
+  bf16* Cs = Hs + (size_t)(L + 1) * LDH;                      // [2 br][2 hi/lo][16 JT][CLD]
+  float* part = (float*)(Cs + 2 * 2 * 16 * JT * CLD);         // [4 waves][2 br][16 JT]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, jj = lane & 15;
   const int n_beg = blockIdx.x * tpb, n_end = min(N, n_beg + tpb);
 
-  // coefficient rows j >= k stay zero
-  for (int e = tid; e < 2 * 2 * 16 * JT * kMixCoefLd; e += 256) Cs[e] = (bf16)0.f;
+  // coefficient rows j >= k and slots l >= L, and the zero state row, stay zero
+  for (int e = tid; e < 2 * 2 * 16 * JT * CLD; e += 256) Cs[e] = (bf16)0.f;
+  for (int e = tid; e < LDH; e += 256) Hs[L * LDH + e] = (bf16)0.f;
 
   // this thread's chunks: c = tid + 256 i -> layer c / DG, states 8 (c % DG) .. + 7
   frag_t<bf16> hv[NCH];
-  // linear mixing: coefficient entries x = tid + 256 i -> (br, j, l), x < 2kL <= kMixCoefMax
+  // coefficient entries x = tid + 256 i -> (br, j, l); their LDS slot is fixed
   float av[kMixCoefPer], rv[kMixCoefPer];
+  int xin[kMixCoefPer], xcs[kMixCoefPer], xl[kMixCoefPer];
+#pragma unroll
+  for (int i = 0; i < kMixCoefPer; ++i) {
+    const int x = min(tid + 256 * i, 2 * kL - 1);
+    const int br = x / kL, jl = x - br * kL, j = jl / L, l = jl - j * L;
+    xin[i] = br * N * kL + jl;  // + n * kL
+    xcs[i] = ((br * 2) * 16 * JT + j) * CLD + l;
+    xl[i] = l;
+  }
   auto fetch = [&](long n) {
     const auto view = make_view(H + n * L * D, (uint32_t)((long)L * D * 2));
 #pragma unroll
@@ -646,33 +662,34 @@ __global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __r
       const int l = c / DG, eg = c - l * DG;
       hv[i] = buf_frag<bf16>(view, c < chunks ? (uint32_t)(l * D + 8 * eg) * 2u : kOffOob);
     }
-    {
 #pragma unroll
-      for (int i = 0; i < kMixCoefPer; ++i) {
-        const int x = min(tid + 256 * i, 2 * kL - 1);
-        const int br = x / kL, jl = x - br * kL, l = jl % L;
-        av[i] = alpha[((long)br * N + n) * kL + jl];
-        rv[i] = rinv[n * L + l];
-      }
+    for (int i = 0; i < kMixCoefPer; ++i) {
+      av[i] = alpha[(long)xin[i] + n * kL];
+      rv[i] = rinv[n * L + xl[i]];
     }
   };
   if (n_beg < n_end) fetch(n_beg);
   __syncthreads();
 
+  // per-lane LDS byte address of the transposing read: lane j of each 16-lane group
+  // addresses layer 16 lt + 4g + j/4 (the zero row past L) at states 4 (j % 4) .. + 3
+  // of the block's 16 columns
+  uint32_t tr_base[LT];
+#pragma unroll
+  for (int lt = 0; lt < LT; ++lt) {
+    const int row = min(16 * lt + 4 * g + (jj >> 2), L);
+    tr_base[lt] = (uint32_t)(uintptr_t)(Hs + row * LDH + 4 * (jj & 3));
+  }
+
   for (int n = n_beg; n < n_end; ++n) {
     // coefficients of both branches (alpha is already normalised in softmax mode)
-    {
 #pragma unroll
-      for (int i = 0; i < kMixCoefPer; ++i) {
-        const int x = tid + 256 * i;
-        if (x < 2 * kL) {
-          const int br = x / kL, jl = x - br * kL, j = jl / L, l = jl - j * L;
-          const int slot = 8 * (l & 3) + (l >> 2);  // slot 8g + t holds layer g + 4t
-          const float c = av[i] * rv[i];
-          const bf16 ch = (bf16)c;
-          Cs[((br * 2 + 0) * 16 * JT + j) * kMixCoefLd + slot] = ch;
-          Cs[((br * 2 + 1) * 16 * JT + j) * kMixCoefLd + slot] = (bf16)(c - (float)ch);
-        }
+    for (int i = 0; i < kMixCoefPer; ++i) {
+      if (tid + 256 * i < 2 * kL) {
+        const float c = av[i] * rv[i];
+        const bf16 ch = (bf16)c;
+        Cs[xcs[i]] = ch;
+        Cs[xcs[i] + 16 * JT * CLD] = (bf16)(c - (float)ch);
       }
     }
 #pragma unroll 1
@@ -702,39 +719,48 @@ __global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __r
       if (br == 1 && n + 1 < n_end) fetch(n + 1);  // the states are staged: refill
       __syncthreads();
 
-      bf16x8 bh[JT], bl[JT];
+      bf16x4 bh[JT][LT], bl[JT][LT];
       float ss[JT];
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
-        bh[jt] = *(const bf16x8*)(Cs + ((br * 2 + 0) * 16 * JT + 16 * jt + jj) * kMixCoefLd + 8 * g);
-        bl[jt] = *(const bf16x8*)(Cs + ((br * 2 + 1) * 16 * JT + 16 * jt + jj) * kMixCoefLd + 8 * g);
+#pragma unroll
+        for (int lt = 0; lt < LT; ++lt) {
+          const bf16* crow = Cs + ((br * 2) * 16 * JT + 16 * jt + jj) * CLD + 16 * lt + 4 * g;
+          bh[jt][lt] = *(const bf16x4*)crow;
+          bl[jt][lt] = *(const bf16x4*)(crow + 16 * JT * CLD);
+        }
         ss[jt] = 0.f;
       }
-#pragma unroll 3
       for (int eb = w; eb < D / 16; eb += 4) {
-        bf16x8 a;
+        bf16x4 a[LT];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          const int l = g + 4 * t;
-          const bf16 v = Hs[min(l, L - 1) * LDH + 16 * eb + jj];
-          a[t] = l < L ? v : (bf16)0.f;
+        for (int lt = 0; lt < LT; ++lt) {
+          typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+          const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(uintptr_t)(tr_base[lt] + (uint32_t)(16 * eb) * 2u));
+          a[lt] = __builtin_bit_cast(bf16x4, v);
         }
 #pragma unroll
         for (int jt = 0; jt < JT; ++jt) {
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh[jt], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl[jt], acc, 0, 0, 0);
+          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int lt = 0; lt < LT; ++lt) {
+            acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a[lt]),
+                                                           __builtin_bit_cast(i16x4_t, bh[jt][lt]),
+                                                           acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a[lt]),
+                                                           __builtin_bit_cast(i16x4_t, bl[jt][lt]),
+                                                           acc, 0, 0, 0);
+          }
           // acc[t]: state 16 eb + 4 g + t of channel 16 jt + jj
           const int j = 16 * jt + jj;
-          if (j < k) {
-            bf16x4 o;
+          bf16x4 o;
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              o[t] = (bf16)acc[t];
-              ss[jt] += acc[t] * acc[t];
-            }
-            *(bf16x4*)(mixed + (((long)br * k + j) * N + n) * D + 16 * eb + 4 * g) = o;
+          for (int t = 0; t < 4; ++t) {
+            o[t] = (bf16)acc[t];
+            ss[jt] += acc[t] * acc[t];
           }
+          if (j < k) *(bf16x4*)(mixed + (((long)br * k + j) * N + n) * D + 16 * eb + 4 * g) = o;
         }
       }
       // sum of squares of channel j over the wave's states: the 4 lane groups hold parts
@@ -770,7 +796,7 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(float* alpha, long ro
   for (int l = 0; l < L; ++l) row[l] = expf(row[l] - mx) * iz;
 }
 
-template <int JT>
+template <int JT, int LT>
 static void mix_mfma_launch(const Shape& sh, const bf16* H, const float* rinv, const bf16* g_pre,
                             float* alpha, bf16* mixed, float* rinv_mid, hipStream_t s) {
   const int nch = (sh.L * (sh.D / 8) + 255) / 256;
@@ -784,7 +810,7 @@ static void mix_mfma_launch(const Shape& sh, const bf16* H, const float* rinv, c
   const dim3 grid((sh.N() + tpb - 1) / tpb), block(256);
   const size_t smem = mix_mfma_smem(sh);
 #define WM_MIX_GO(NC)                                                                          \
-  hipLaunchKernelGGL((mix_mfma_kernel<JT, NC>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, \
+  hipLaunchKernelGGL((mix_mfma_kernel<JT, LT, NC>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, \
                      mixed, rinv_mid, tpb)
   if (nch <= 2) WM_MIX_GO(2);
   else if (nch <= 4) WM_MIX_GO(4);
@@ -801,8 +827,11 @@ void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, 
   if (sh.N() <= 0) return;
   if constexpr (sizeof(T) == 2) {
     if (mix_mfma_fits(sh)) {
-      if (sh.k <= 16) mix_mfma_launch<1>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
-      else mix_mfma_launch<2>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
+      const bool jt1 = sh.k <= 16, lt1 = sh.L <= 16;
+      if (jt1 && lt1) mix_mfma_launch<1, 1>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
+      else if (jt1) mix_mfma_launch<1, 2>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
+      else if (lt1) mix_mfma_launch<2, 1>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
+      else mix_mfma_launch<2, 2>(sh, H, rinv, g_pre, alpha, mixed, rinv_mid, s);
       return;
     }
   }
