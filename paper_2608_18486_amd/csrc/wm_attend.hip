@@ -39,6 +39,14 @@ __device__ __forceinline__ f32x8 ld_frag_4_4<float>(const float* p0, const float
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// A lane's sum of 16 softmax weights above this (some weight above 2^12) triggers the
+// rescale of the running state; `!(ps <= kGrowSum)` also catches inf and NaN.
+constexpr float kGrowSum = 65536.0f;
+// Reference of a row that has seen no slot yet, in log2 units. Finite and small, so
+// scores offset by it keep their digits; a row still at kNoRef always takes the
+// exact-max rescale, which then sets a real reference.
+constexpr float kNoRef = -100.0f;
+
 template <typename T> struct AttnArgs {
   const T *Q, *Kc, *Vc, *Kd, *Vd;
   const int32_t* ctx_len;
@@ -73,7 +81,6 @@ template <typename T, int DH> struct PrefillCfg {
   static constexpr int VIT = VTR ? KIT : (BKV / 2) * (DH / 8);  // V items per block (16-B
                                                                  // fragments, or key pairs)
   static constexpr int VPT = (VIT + NT - 1) / NT;      // ... per thread
-  static constexpr float kRescale = 8.0f;              // log2 headroom before rescaling
 };
 
 // Paired-key transposed store of two V rows' 8 columns: Vt[c][key], Vt[c][key+1].
@@ -110,14 +117,24 @@ __device__ __forceinline__ void attend_block(
     const T* __restrict__ ks_, const T* __restrict__ vt_,
     const frag_t<T> (&qf)[PrefillCfg<T, DH>::QT][DH / 16], float (&m)[PrefillCfg<T, DH>::QT],
     float (&lsum)[PrefillCfg<T, DH>::QT], f32x16 (&o)[DH / 32][PrefillCfg<T, DH>::QT], int k0,
-    int wkend, int tq0, int incl, int h, int r, float cl2, float thresh) {
+    int wkend, int tq0, int incl, int h, int r) {
   using C = PrefillCfg<T, DH>;
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
     if (MASK && k0 + 32 * kt >= wkend) break;  // this half is past every row of the wave
+    // Q is pre-scaled by log2(e)/sqrt(d): s' is the score in log2 units, m' the row's
+    // reference. In bf16 the scores start from -m', so the MFMAs leave s' - m' and the
+    // weight needs no subtraction; fp32 starts from 0 (summing on top of m' would cost
+    // fp32 parity a few ulps of m') and subtracts m' itself.
+    constexpr bool kOffsetInit = sizeof(T) == 2;
     f32x16 st[C::QT];
+    float off[C::QT];
 #pragma unroll
-    for (int qt = 0; qt < C::QT; ++qt) st[qt] = zero16();
+    for (int qt = 0; qt < C::QT; ++qt) {
+      off[qt] = kOffsetInit ? 0.f : m[qt];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) st[qt][q] = kOffsetInit ? -m[qt] : 0.f;
+    }
 #pragma unroll
     for (int ks = 0; ks < C::NKS; ++ks) {
       frag_t<T> kf = ld_frag<T>(ks_ + (32 * kt + r) * C::LDK + 16 * ks + 8 * h);
@@ -135,28 +152,35 @@ __device__ __forceinline__ void attend_block(
         for (int q = 0; q < 16; ++q)
           if (8 * (q >> 2) + (q & 3) >= lim) st[qt][q] = kNegBig;
       }
-      float mx = st[qt][0];
+      // Weights against the current reference m first: while every weight stays below
+      // 2^12 (so a lane's sum of 16 stays below 2^16) no rescale is needed. Otherwise
+      // (rare: a row's first block, or a score far above m) take the exact row max,
+      // rescale the running state to it and recompute. Masked slots hold -1e30: weight 0.
+      float pv[16], ps = 0.f;
 #pragma unroll
-      for (int q = 1; q < 16; ++q) mx = fmaxf(mx, st[qt][q]);
-      mx = halves_max(mx);
-      const bool grow = mx > m[qt] + thresh;
-      if (__any(grow)) {
-        const float mn = grow ? mx : m[qt];
-        const float alpha = fast_exp2((m[qt] - mn) * cl2);
-        m[qt] = mn;
+      for (int q = 0; q < 16; ++q) {
+        pv[q] = fast_exp2(st[qt][q] - off[qt]);
+        ps += pv[q];
+      }
+      if (__any(!(ps <= kGrowSum) || m[qt] == kNoRef)) {
+        float mx = st[qt][0];
+#pragma unroll
+        for (int q = 1; q < 16; ++q) mx = fmaxf(mx, st[qt][q]);
+        mx = fmaxf(halves_max(mx) - off[qt], 0.f);  // growth of the reference (never shrinks)
+        const float alpha = fast_exp2(-mx);
+        m[qt] += mx;
         lsum[qt] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] *= alpha;
-      }
-      const float mc = m[qt] * cl2;
-      float ps = 0.f;
+        ps = 0.f;
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        float p = fast_exp2(st[qt][q] * cl2 - mc);
-        if (MASK) p = st[qt][q] > 0.5f * kNegBig ? p : 0.f;
-        ps += p;
-        pf[qt][q >> 3][q & 7] = from_f32<T>(p);
+        for (int q = 0; q < 16; ++q) {
+          pv[q] = fast_exp2(st[qt][q] - off[qt] - mx);
+          ps += pv[q];
+        }
       }
+#pragma unroll
+      for (int q = 0; q < 16; ++q) pf[qt][q >> 3][q & 7] = from_f32<T>(pv[q]);
       lsum[qt] += ps;
     }
 #pragma unroll
@@ -200,7 +224,6 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   const int incl = a.mask_paper ? 0 : 1;
   const int q0 = qtile * C::BQ, qw0 = q0 + 32 * QT * w;
   const float cl2 = a.scale_log2;
-  const float thresh = C::kRescale / cl2;
 
   const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
   const T* Kb = a.Kc + cbase;
@@ -215,6 +238,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
     for (int ks = 0; ks < C::NKS; ++ks)
       qf[qt][ks] = qi < a.T_new ? ld_frag<T>(Qb + (long)qi * DH + 16 * ks + 8 * h) : zero_frag<T>();
   }
+  // queries in log2 units: the MFMAs then give s' = q.k log2(e) / sqrt(d), and the
+  // softmax weight of a slot is exp2(s' - m') with m' the row's running reference
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+    for (int ks = 0; ks < C::NKS; ++ks)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) qf[qt][ks][i] = from_f32<T>(to_f32(qf[qt][ks][i]) * cl2);
 
   // running state per query row (lanes r and r + 32 hold the same row): reference max,
   // partial row sum (each half-wave sums its own keys), and O^T
@@ -240,7 +271,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   } else {
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-      m[qt] = kNegBig;
+      m[qt] = kNoRef;
       lsum[qt] = 0.f;
 #pragma unroll
       for (int dt = 0; dt < C::NDT; ++dt) o[dt][qt] = zero16();
@@ -316,10 +347,10 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
     if (k0 < wkend) {
       if (k0 + C::BKV > wfree)
         attend_block<T, DH, true>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
-                                  h, r, cl2, thresh);
+                                  h, r);
       else
         attend_block<T, DH, false>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
-                                   h, r, cl2, thresh);
+                                   h, r);
     }
     stage(buf ^ 1);
     __syncthreads();
