@@ -19,6 +19,8 @@
 // workgroup per (split, channel, sequence, KV head) serving every query row
 // that reads that channel and head (all its consumer layers, grouped query
 // heads and new tokens), so each channel slice is streamed from HBM once.
+#include <type_traits>
+
 #include "wm_device.hpp"
 #include "wm_internal.hpp"
 
@@ -220,7 +222,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   const int c = a.chan.v[l];
   const int kvh = hq / (a.Hq / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, r = lane & 31;
-  const int ctx = a.ctx_len ? a.ctx_len[b] : 0;
+  const int ctx = __builtin_amdgcn_readfirstlane(a.ctx_len ? a.ctx_len[b] : 0);  // wave-uniform
   const int incl = a.mask_paper ? 0 : 1;
   const int q0 = qtile * C::BQ, qw0 = q0 + 32 * QT * w;
   const float cl2 = a.scale_log2;
@@ -375,6 +377,400 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   }
 }
 
+// ---------------------------------------------- prefill, bf16, head dim 64
+// K/V blocks of 64 slots are copied from HBM straight into LDS (no trip through
+// registers), one barrier per block. A slot row is 128 B; its 16-B chunk c sits at
+// chunk c ^ kv_swz(row) of the LDS row. That makes both readers free of bank
+// conflicts: the K fragment reads (16 rows, one chunk) and the transposing V reads
+// (4 rows x 4 chunks per 32 lanes).
+//
+// Each wave owns QT tiles of 32 queries and walks its keys in 32-slot steps. Step i
+// issues the MFMAs of S(i+1) = K Q^T and of O^T += V^T P(i-1)^T, and meanwhile computes
+// the softmax weights P(i) of S(i) on the vector ALUs, so the matrix cores and the ALUs
+// work on independent data. Every K or V fragment read from LDS feeds QT MFMAs.
+#ifndef WM_PF_NW
+#define WM_PF_NW 4
+#endif
+#ifndef WM_PF_NS
+#define WM_PF_NS 3
+#endif
+constexpr int kPfNs = WM_PF_NS;  // blocks per ring (3 or 4)
+template <int QT> struct PfDma {
+  static constexpr int NW = WM_PF_NW / QT, NT = 64 * NW;
+  static constexpr int BQ = 32 * QT * NW;              // queries per workgroup
+  static constexpr int BKV = 64, DH = 64;
+  static constexpr int ROW_BYTES = DH * 2;             // one slot row of K or V
+  static constexpr int BLK_BYTES = BKV * ROW_BYTES;    // one K (or V) block: 8 KB
+  static constexpr int RPW = BKV / NW;                 // block rows each wave copies
+  static constexpr int NI = RPW / 8;                   // ... in copy instructions of 8 rows
+  // Two rings of NS blocks. While block j is processed, K of j and j+1 and V of j-1 and
+  // j are read; K of j+2 and V of j+1 (and, with 4 blocks, K of j+3 and V of j+2) are
+  // in flight.
+  static constexpr int NS = kPfNs;
+  static constexpr int V_BASE = NS * BLK_BYTES;        // K ring first, then the V ring
+  static constexpr int SMEM_BYTES = 2 * NS * BLK_BYTES;
+  static_assert(RPW % 8 == 0 && (NS == 3 || NS == 4), "tile shapes");
+};
+constexpr int kPfRowBytes = 128, kPfBlkBytes = 64 * kPfRowBytes, kPfVBase = kPfNs * kPfBlkBytes;
+
+// Bit-reversal of (row / 2) mod 8: rows 2x and 2x+1 share a 256-B bank line, and rows
+// 4y, 4y+2 differ in bit 2, which keeps a transposing read's 4 chunks apart.
+__device__ __forceinline__ int kv_swz(int row) {
+  const int x = (row >> 1) & 7;
+  return ((x & 1) << 2) | (x & 2) | (x >> 2);
+}
+
+template <int QT> struct PfState {  // one wave's running softmax state (2 lanes per row)
+  f32x16 o[2][QT];   // O^T per value-column half and query tile
+  bf16x8 pf[2][QT];  // P(i-1)^T fragments (keys 0-15, 16-31 of the step)
+  float m[QT], lsum[QT];
+};
+
+// Byte offsets of one lane's fragment reads inside a half block (32 slot rows) of LDS:
+// k[ks] for the K fragment of k16 step ks, v[dt][s] for the s-th transposing read of the
+// V^T fragment of value tile dt (the second 16 rows of the half add 16 rows). They do
+// not depend on the ring stage, so the stage and half fold into the instructions'
+// offset fields.
+struct PfLane {
+  uint32_t k[4], v[2][2];
+};
+__device__ __forceinline__ PfLane pf_lane(int lane) {
+  const int h = lane >> 5, r = lane & 31, j = lane & 15, grp = lane >> 4;
+  PfLane o;
+  const int sw = kv_swz(r);
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) o.k[ks] = r * kPfRowBytes + 16 * ((2 * ks + h) ^ sw);
+#pragma unroll
+  for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int row = 4 * h + (j >> 2) + 8 * s;
+      const int chunk = 4 * dt + 2 * (grp & 1) + ((j & 3) >> 1);
+      o.v[dt][s] = row * kPfRowBytes + 16 * (chunk ^ kv_swz(row)) + 8 * (j & 1);
+    }
+  return o;
+}
+// byte offsets of the K and V ring half blocks: ring stage u, half hf
+constexpr uint32_t pf_kh(int u, int hf) { return u * kPfBlkBytes + hf * 32 * kPfRowBytes; }
+constexpr uint32_t pf_vh(int u, int hf) { return kPfVBase + u * kPfBlkBytes + hf * 32 * kPfRowBytes; }
+
+__device__ __forceinline__ bf16x8 pf_ldk(const char* sm, const PfLane& lo, uint32_t kh, int ks) {
+  return *(const bf16x8*)(sm + lo.k[ks] + kh);
+}
+// V^T fragment (value column 32 dt + r, keys 16 hf + 4h + {0..3, 8..11} of the half)
+__device__ __forceinline__ bf16x8 pf_ldv(const char* sm, const PfLane& lo, uint32_t vh, int hf,
+                                         int dt) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const uint32_t base = vh + hf * 16 * kPfRowBytes;
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sm + lo.v[dt][0] + base));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sm + lo.v[dt][1] + base));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// S^T fragment rows of one step for one query tile: the 32 K slots of the half block
+// at kh against the lane's query column, accumulated on top of acc.
+__device__ __forceinline__ f32x16 pf_scores(const char* sm, const PfLane& lo, uint32_t kh,
+                                            const bf16x8 (&qf)[4], f32x16 acc) {
+  bf16x8 kf[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) kf[ks] = pf_ldk(sm, lo, kh, ks);
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) acc = mma32(acc, kf[ks], qf[ks]);
+  return acc;
+}
+
+// Slots of step i that this lane's row must not see get the score -1e30 (weight 0):
+// slot 32 i + 8(q/4) + 4h + q%4 is visible iff it is below lim0 (row position + incl).
+__device__ __forceinline__ void pf_mask(f32x16& v, int i, int lim0, int lane) {
+  const int lim = lim0 - (32 * i + 4 * (lane >> 5));
+#pragma unroll
+  for (int q = 0; q < 16; ++q)
+    if (8 * (q >> 2) + (q & 3) >= lim) v[q] = kNegBig;
+}
+
+// Accumulator start for the scores of step i: -m (the row reference), or -1e30 for the
+// slots a masked step hides from this lane's row. -1e30 plus any score stays about
+// -1e30, so the MFMAs that follow need no masking afterwards.
+__device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int i, int lim0,
+                                        int lane) {
+  if (masked) {
+    const int lim = lim0 - (32 * i + 4 * (lane >> 5));
+#pragma unroll
+    for (int q = 0; q < 16; ++q) v[q] = 8 * (q >> 2) + (q & 3) >= lim ? kNegBig : init;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) v[q] = init;
+  }
+}
+
+// One step (see above), the same straight-line code for every step: the MFMAs of
+// PV(i-1) and S(i+1) and the exponentials of S(i) sit in one basic block, so they
+// interleave. sc holds S(i) in log2 units minus the row reference m, masked; sn
+// arrives holding the start value of S(i+1) (pf_init) and leaves holding S(i+1). Two
+// register sets alternate between consecutive steps, and sc is refilled with the start
+// value of S(i+2), so no step waits on the MFMAs it has just issued. lim0 is the first
+// tile's row limit; tile t's rows sit 32 t further.
+template <int QT>
+__device__ __forceinline__ void pf_step(const char* sm, const PfLane& lo, uint32_t kh_cur,
+                                        uint32_t kh_nxt, uint32_t vh_prv, int i,
+                                        const bf16x8 (&qf)[QT][4], PfState<QT>& st,
+                                        f32x16 (&sc)[QT], f32x16 (&sn)[QT], int lane, int lim0,
+                                        bool mask_cur, bool mask_n2) {
+  // Four groups k, each: the MFMAs of PV(i-1) for keys 16(k/2).. and value tile k%2 and
+  // of S(i+1) for k16 step k, plus the weights of 4 rows of S(i). The fragments of V^T
+  // (step i-1; before the first step a zeroed stage) and K (step i+1) are read one group
+  // ahead, and groups are not reordered, so at most two groups' fragments are live.
+  bf16x8 vf[2], kf[2];
+  vf[0] = pf_ldv(sm, lo, vh_prv, 0, 0);
+  kf[0] = pf_ldk(sm, lo, kh_nxt, 0);
+  // weights against the current reference, in place (S(i) is not needed again unless
+  // the rescale below runs, which recomputes it from the K block still in LDS)
+  float ps4[QT][4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (k < 3) {
+      vf[(k + 1) & 1] = pf_ldv(sm, lo, vh_prv, (k + 1) >> 1, (k + 1) & 1);
+      kf[(k + 1) & 1] = pf_ldk(sm, lo, kh_nxt, k + 1);
+    }
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      st.o[k & 1][t] = mma32(st.o[k & 1][t], vf[k & 1], st.pf[k >> 1][t]);
+      sn[t] = mma32(sn[t], kf[k & 1], qf[t][k]);
+    }
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+#pragma unroll
+      for (int q = 4 * k; q < 4 * k + 4; ++q) sc[t][q] = fast_exp2(sc[t][q]);
+      ps4[t][k] = (sc[t][4 * k] + sc[t][4 * k + 1]) + (sc[t][4 * k + 2] + sc[t][4 * k + 3]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    float ps = (ps4[t][0] + ps4[t][1]) + (ps4[t][2] + ps4[t][3]);
+    if (__any(!(ps <= kGrowSum) || st.m[t] == kNoRef)) {
+      // rare: move the reference up to the exact row max (never down) and rescale the
+      // state; S(i+1) was started from the old reference, so it moves too
+      f32x16 sr;
+      pf_init(sr, -st.m[t], mask_cur, i, lim0 + 32 * t, lane);
+      sr = pf_scores(sm, lo, kh_cur, qf[t], sr);
+      float mx = sr[0];
+#pragma unroll
+      for (int q = 1; q < 16; ++q) mx = fmaxf(mx, sr[q]);
+      mx = fmaxf(halves_max(mx), 0.f);
+      const float alpha = fast_exp2(-mx);
+      st.m[t] += mx;
+      st.lsum[t] *= alpha;
+      st.o[0][t] *= alpha;
+      st.o[1][t] *= alpha;
+      ps = 0.f;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        sn[t][q] -= mx;
+        sc[t][q] = fast_exp2(sr[q] - mx);
+        ps += sc[t][q];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) st.pf[q >> 3][t][q & 7] = (bf16)sc[t][q];
+    st.lsum[t] += ps;
+    pf_init(sc[t], -st.m[t], mask_n2, i + 2, lim0 + 32 * t, lane);  // accumulator of S(i+2)
+  }
+}
+
+#ifndef WM_PF_QT
+#define WM_PF_QT 1
+#endif
+constexpr int kPfQt = WM_PF_QT;  // query tiles per wave of the bf16 d = 64 prefill
+
+#ifndef WM_PF_OCC
+// waves per SIMD: two 8-wave or three 4-wave workgroups per CU
+#define WM_PF_OCC __attribute__((amdgpu_waves_per_eu(WM_PF_NW == 8 ? 4 : 3)))
+#endif
+template <int QT>
+__global__ __launch_bounds__(PfDma<QT>::NT) WM_PF_OCC
+void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
+  using P = PfDma<QT>;
+  __shared__ __align__(16) char smem[P::SMEM_BYTES];
+
+  // 1-D grid over (consumer, sequence, head, query tile), as in attend_prefill_kernel
+  const int tile = xcd_tile(blockIdx.x, a.n_qtiles * a.Hq * a.B * a.L);
+  const int qtile = a.n_qtiles - 1 - tile % a.n_qtiles;
+  int y = tile / a.n_qtiles;
+  const int hq = y % a.Hq;
+  y /= a.Hq;
+  const int b = y % a.B, l = y / a.B;
+  const int c = a.chan.v[l];
+  const int kvh = hq / (a.Hq / a.Hkv);
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ctx = __builtin_amdgcn_readfirstlane(a.ctx_len ? a.ctx_len[b] : 0);  // wave-uniform
+  const int incl = a.mask_paper ? 0 : 1;
+  const int q0 = qtile * P::BQ, qw0 = q0 + 32 * QT * w;
+  const float cl2 = a.scale_log2;
+
+  // zero the rings first: "block -1" feeds the first step's (weightless) PV, and slot
+  // rows past the visible range get weight 0, so every stage must hold finite values
+  {
+    const i32x4 z = {0, 0, 0, 0};
+#pragma unroll
+    for (int k = 0; k < P::SMEM_BYTES / (16 * P::NT); ++k)
+      *(i32x4*)(smem + 16 * (tid + P::NT * k)) = z;
+  }
+
+  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * P::DH;
+  bf16x8 qf[QT][4];
+  const bf16* Qb = a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * P::DH;
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int qi = qw0 + 32 * t + r;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      qf[t][ks] = qi < a.T_new ? *(const bf16x8*)(Qb + (long)qi * P::DH + 16 * ks + 8 * h)
+                               : zero_frag<bf16>();
+    // queries in log2 units: the MFMAs then give s' = q.k log2(e) / sqrt(d)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) qf[t][ks][i] = (bf16)((float)qf[t][ks][i] * cl2);
+  }
+
+  PfState<QT> st;
+  f32x16 sa[QT], sb[QT];  // score registers of even and odd steps
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    st.pf[0][t] = zero_frag<bf16>();
+    st.pf[1][t] = zero_frag<bf16>();
+    if (a.mask_paper) {
+      const bf16* kd = a.Kd + ((long)c * a.Hkv + kvh) * P::DH;
+      const bf16* vd = a.Vd + ((long)c * a.Hkv + kvh) * P::DH;
+      float part = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) part += (float)qf[t][ks][i] * (float)kd[16 * ks + 8 * h + i];
+      st.m[t] = halves_sum(part);
+      st.lsum[t] = h == 0 ? 1.f : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          st.o[dt][t][q] = (float)vd[32 * dt + 8 * (q >> 2) + 4 * h + (q & 3)];
+    } else {
+      st.m[t] = kNoRef;
+      st.lsum[t] = 0.f;
+      st.o[0][t] = zero16();
+      st.o[1][t] = zero16();
+    }
+  }
+
+  const int qlast = min(q0 + P::BQ, a.T_new) - 1;
+  const int kend = min(ctx + qlast + incl, a.S_cap);   // slots the workgroup may see
+  const int nblk = (kend + P::BKV - 1) / P::BKV;
+  const int wq_last = min(qw0 + 32 * QT - 1, a.T_new - 1);
+  const int wkend = wq_last >= qw0 ? ctx + wq_last + incl : 0;  // slots this wave may see
+  const int wfree = ctx + qw0 + incl;   // slots < wfree are visible to all its rows
+  const int ilast = (wkend + 31) / 32 - 1;  // the wave's last 32-slot step (-1: none)
+  const int lim0 = ctx + qw0 + r + incl;
+
+  // copies: wave w moves slot rows RPW w .. RPW w + RPW-1 of each K and V block
+  const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)a.S_cap * P::ROW_BYTES);
+  const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)a.S_cap * P::ROW_BYTES);
+  uint32_t dchunk[P::NI];
+#pragma unroll
+  for (int n = 0; n < P::NI; ++n)
+    dchunk[n] = 16u * (uint32_t)((lane & 7) ^ kv_swz(P::RPW * w + 8 * n + (lane >> 3)));
+  const uint32_t smem_base = (uint32_t)(uintptr_t)smem;
+  // NI copy instructions per wave move its rows of a K or V block; blocks past the
+  // visible range are copied too (as zeros), so every wave issues the same sequence
+  // (4-block rings: K0 K1 V0 K2 V1 | K3 V2 | K4 V3 | ..., 3-block rings: K0 K1 V0 |
+  // K2 V1 | K3 V2 | ...) and one vmcnt fits every iteration
+  auto issue = [&](int blk, bool v) {
+#pragma unroll
+    for (int n = 0; n < P::NI; ++n) {
+      const int row0 = P::RPW * w + 8 * n;
+      const int s = blk * P::BKV + row0 + (lane >> 3);
+      const uint32_t off = s < kend ? (uint32_t)s * P::ROW_BYTES + dchunk[n] : kOffOob;
+      const uint32_t lds = __builtin_amdgcn_readfirstlane(
+          smem_base + (v ? P::V_BASE : 0) + (blk % P::NS) * P::BLK_BYTES + row0 * P::ROW_BYTES);
+      lds_dma16(lds, off, v ? vview : kview);
+    }
+  };
+
+  __syncthreads();  // the zeroed rings are in place before any copy lands
+  constexpr int AHEAD = P::NS - 3;  // (K, V) pairs still in flight when block j starts
+  issue(0, false);
+  issue(1, false);
+  issue(0, true);
+  if (AHEAD) {
+    issue(2, false);
+    issue(1, true);
+  }
+  PfLane lo = pf_lane(lane);
+  // one block of the walk; u = j mod NS is a compile-time constant, so every ring
+  // address below is a lane offset plus a constant the LDS instructions carry
+  auto block = [&](const int j, auto uc) {
+    constexpr int u = decltype(uc)::value;
+    // keep the lane offsets as they are (not one precomputed address per use)
+    asm volatile("" : "+v"(lo.k[0]), "+v"(lo.k[1]), "+v"(lo.k[2]), "+v"(lo.k[3]),
+                 "+v"(lo.v[0][0]), "+v"(lo.v[0][1]), "+v"(lo.v[1][0]), "+v"(lo.v[1][1]));
+    wait_vmcnt<2 * P::NI * AHEAD>();  // this wave's copies of K(j+1) and V(j) have landed ...
+    __syncthreads();  // ... and every wave's; the stages of K(j-1) and V(j-2) are free
+    issue(j + P::NS - 1, false);
+    issue(j + P::NS - 2, true);
+    if (u == 0 && j == 0 && ilast >= 0) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        pf_init(sa[t], -st.m[t], 32 > wfree, 0, lim0 + 32 * t, lane);
+        sa[t] = pf_scores(smem, lo, pf_kh(0, 0), qf[t], sa[t]);
+        pf_init(sb[t], -st.m[t], 64 > wfree, 1, lim0 + 32 * t, lane);
+      }
+    }
+    // steps up to ilast + 1: the last one only adds PV(ilast) (its own slots are all
+    // past the wave's rows, so its weights are 0)
+    const int i = 2 * j;
+    if (i <= ilast + 1)
+      pf_step<QT>(smem, lo, pf_kh(u, 0), pf_kh(u, 1), pf_vh((u + P::NS - 1) % P::NS, 1), i, qf,
+                  st, sa, sb,
+                  lane, lim0, 32 * i + 32 > wfree, 32 * i + 96 > wfree);
+    if (i + 1 <= ilast + 1)
+      pf_step<QT>(smem, lo, pf_kh(u, 1), pf_kh((u + 1) % P::NS, 0), pf_vh(u, 0), i + 1, qf, st, sb,
+                  sa, lane, lim0, 32 * i + 64 > wfree, 32 * i + 128 > wfree);
+  };
+  for (int j = 0; j < nblk; j += P::NS) {
+    block(j, std::integral_constant<int, 0>());
+    if (j + 1 < nblk) block(j + 1, std::integral_constant<int, 1>());
+    if (j + 2 < nblk) block(j + 2, std::integral_constant<int, 2>());
+    if (P::NS == 4 && j + 3 < nblk) block(j + 3, std::integral_constant<int, 3 % P::NS>());
+  }
+  if (ilast + 1 == 2 * nblk) {
+    const int u = nblk % P::NS;
+    pf_step<QT>(smem, lo, pf_kh(u, 0), pf_kh(u, 1), pf_vh((u + P::NS - 1) % P::NS, 1), 2 * nblk,
+                qf, st, sa,
+                sb, lane, lim0, true, true);
+  }
+  wait_vmcnt<0>();  // no copy may land after the workgroup ends
+
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int qi = qw0 + 32 * t + r;
+    const float lt = halves_sum(st.lsum[t]);
+    if (qi < a.T_new) {
+      const float inv = 1.0f / lt;
+      bf16* dst = a.O + ((((long)l * a.B + b) * a.T_new + qi) * a.Hq + hq) * P::DH;
+#pragma unroll
+      for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float v[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = st.o[dt][t][4 * g + i] * inv;
+          store4(dst + 32 * dt + 8 * g + 4 * h, v);
+        }
+    }
+  }
+}
+
 template <typename T>
 void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q, const T* Kc,
                            const T* Vc, const T* Kd, const T* Vd, const int32_t* ctx_len, T* O,
@@ -386,7 +782,14 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
                 sh.mask_paper, (sh.T_new + BQ - 1) / BQ,
                 kLog2e / sqrtf((float)sh.d), chan_map};
   dim3 grid(a.n_qtiles * sh.Hq * sh.B * sh.L);
-  if (sh.d == 64)
+  if (sizeof(T) == 2 && sh.d == 64) {
+    constexpr int BQD = PfDma<kPfQt>::BQ;
+    AttnArgs<T> ad = a;
+    ad.n_qtiles = (sh.T_new + BQD - 1) / BQD;
+    hipLaunchKernelGGL(attend_prefill_dma_kernel<kPfQt>,
+                       dim3(ad.n_qtiles * sh.Hq * sh.B * sh.L), dim3(PfDma<kPfQt>::NT), 0, s,
+                       *reinterpret_cast<const AttnArgs<bf16>*>(&ad));
+  } else if (sh.d == 64)
     hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(NT), 0, s, a);
   else
     hipLaunchKernelGGL((attend_prefill_kernel<T, 32>), grid, dim3(NT), 0, s, a);
@@ -457,7 +860,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
   if (nmem == 0) return;
   const int grp = a.Hq / a.Hkv;
   const int G = nmem * grp * a.T_new;
-  const int ctx = a.ctx_len ? a.ctx_len[b] : 0;
+  const int ctx = __builtin_amdgcn_readfirstlane(a.ctx_len ? a.ctx_len[b] : 0);  // wave-uniform
   const int incl = a.mask_paper ? 0 : 1;
   const int kend = min(ctx + a.T_new - 1 + incl, a.S_cap);
   const int s0 = split * a.split_len, s1 = min(s0 + a.split_len, kend);

@@ -125,6 +125,24 @@ template <> __device__ __forceinline__ f32x8 buf_frag<float>(__amdgpu_buffer_rsr
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
+// Copy 16 bytes per lane from a buffer view straight into LDS: lane l's bytes land
+// at LDS byte address lds_addr + 16 l (lds_addr is wave-uniform and goes through
+// M0). Issued from inline assembly so that the compiler does not add a full
+// vmcnt(0) wait in front of every barrier; callers wait with wait_vmcnt.
+__device__ __forceinline__ void lds_dma16(uint32_t lds_addr, uint32_t voff,
+                                          __amdgpu_buffer_rsrc_t rsrc) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone), n < 16
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
 // Workgroups are dispatched round-robin over the chip's 8 XCDs (block i goes to
 // XCD i % 8), and each XCD has its own L2. Remap the linear block index so that
 // XCD x walks a contiguous share of the tile sequence: tiles that share

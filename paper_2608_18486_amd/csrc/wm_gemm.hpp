@@ -205,20 +205,6 @@ template <class C> struct DmaCfg {
   static_assert(NI <= 15, "vmcnt encodes at most 15 here");
 };
 
-__device__ __forceinline__ void lds_dma16(uint32_t lds_addr, uint32_t voff,
-                                          __amdgpu_buffer_rsrc_t rsrc) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :
-               : "s"(lds_addr), "v"(voff), "s"(rsrc)
-               : "memory", "m0");
-}
-
-// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone), n < 16
-template <int N> __device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 16, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
-}
-
 template <class C, typename T, class XLoad, class WLoad, class Epi>
 __global__ __launch_bounds__(C::NT) void proj_gemm_dma_kernel(int M, int Nout, int K, int groups,
                                                               int seg_len, int kspan, XLoad xl,
