@@ -388,15 +388,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
 // issues the MFMAs of S(i+1) = K Q^T and of O^T += V^T P(i-1)^T, and meanwhile computes
 // the softmax weights P(i) of S(i) on the vector ALUs, so the matrix cores and the ALUs
 // work on independent data. Every K or V fragment read from LDS feeds QT MFMAs.
-#ifndef WM_PF_NW
-#define WM_PF_NW 4
-#endif
-#ifndef WM_PF_NS
-#define WM_PF_NS 3
-#endif
-constexpr int kPfNs = WM_PF_NS;  // blocks per ring (3 or 4)
+// Workgroup shape: 4 waves of one 32-query tile each and rings of 3 blocks, i.e. 48 KB
+// of LDS and at most 168 registers per lane, so a CU holds three workgroups (3 waves per
+// SIMD, each from a different workgroup, so no two waves of a SIMD wait at the same
+// barrier). Measured on MI355X and slower: 8-wave workgroups (4 waves per SIMD, in
+// lock-step pairs; 128 registers), and 2 query tiles per wave (2 waves per SIMD).
+constexpr int kPfWaves = 4, kPfNs = 3, kPfQt = 1;
 template <int QT> struct PfDma {
-  static constexpr int NW = WM_PF_NW / QT, NT = 64 * NW;
+  static constexpr int NW = kPfWaves, NT = 64 * NW;
   static constexpr int BQ = 32 * QT * NW;              // queries per workgroup
   static constexpr int BKV = 64, DH = 64;
   static constexpr int ROW_BYTES = DH * 2;             // one slot row of K or V
@@ -578,17 +577,8 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane& lo, uint32
   }
 }
 
-#ifndef WM_PF_QT
-#define WM_PF_QT 1
-#endif
-constexpr int kPfQt = WM_PF_QT;  // query tiles per wave of the bf16 d = 64 prefill
-
-#ifndef WM_PF_OCC
-// waves per SIMD: two 8-wave or three 4-wave workgroups per CU
-#define WM_PF_OCC __attribute__((amdgpu_waves_per_eu(WM_PF_NW == 8 ? 4 : 3)))
-#endif
 template <int QT>
-__global__ __launch_bounds__(PfDma<QT>::NT) WM_PF_OCC
+__global__ __launch_bounds__(PfDma<QT>::NT) __attribute__((amdgpu_waves_per_eu(3)))
 void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   using P = PfDma<QT>;
   __shared__ __align__(16) char smem[P::SMEM_BYTES];
