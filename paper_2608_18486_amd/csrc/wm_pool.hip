@@ -598,77 +598,114 @@ size_t mix_smem_bytes(int L, int k, int D, size_t es) {
 // takes layers 4g .. 4g+3 of its state column, which one transposing LDS read
 // (ds_read_b64_tr_b16) gathers from the row-major tile. The staged tile has L
 // rows plus one row of zeros that stands in for the layers past L.
-// A block of 256 threads walks up to kMixTok consecutive tokens; the next token's
-// states and coefficients are fetched while the current token's second branch
-// is multiplied. In softmax mode alpha is normalised beforehand
+// A block of NT threads walks up to kMixTok consecutive tokens; the next token's
+// states and coefficients are fetched while the current token's second branch is
+// multiplied. NT is 256 when a token's states are at most 1536 chunks of 8 (six per
+// thread), else 512, which keeps the registers a thread holds for the prefetch low
+// enough for two or more blocks per CU (measured best for L12 D768 and L24 D1024). In softmax mode alpha is normalised beforehand
 // (softmax_rows_kernel).
 constexpr int kMixTok = 8;
-constexpr int kMixCoefPer = 4;  // coefficient entries per thread (2kL <= 1024)
+constexpr int kMixCoefMax = 1024;  // coefficient entries 2kL per token at most
+
+__host__ __device__ static int mix_threads(int L, int D) { return L * (D / 8) <= 1536 ? 256 : 512; }
 
 __host__ __device__ static int mix_mfma_ldh(int D) { return D + 16; }  // staged row stride
 __host__ __device__ static int mix_coef_ld(int LT) { return 16 * LT + 4; }
 static size_t mix_mfma_smem(const Shape& sh) {
   const int JT = (sh.k + 15) / 16, LT = (sh.L + 15) / 16;
   return (size_t)(sh.L + 1) * mix_mfma_ldh(sh.D) * 2 + 2 * 2 * 16 * JT * mix_coef_ld(LT) * 2 +
-         4 * 2 * 16 * JT * 4;
+         (mix_threads(sh.L, sh.D) / 64) * 2 * 16 * JT * 4;
 }
 static bool mix_mfma_fits(const Shape& sh) {
-  return sh.L <= 32 && sh.k <= 32 && 2 * sh.k * sh.L <= 256 * kMixCoefPer && sh.D % 16 == 0 &&
+  // (the kernel stores through a buffer view per branch, which must span under 2 GiB)
+  return sh.L <= 32 && sh.k <= 32 && 2 * sh.k * sh.L <= kMixCoefMax && sh.D % 16 == 0 &&
+         (long)sh.k * sh.N() * sh.D * 2 < (1L << 31) &&
          mix_mfma_smem(sh) <= 65536;
 }
 
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-template <int JT, int LT, int NCH>
-__global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __restrict__ H,
+// EB: column blocks of 16 states per wave and branch (D = 16 waves EB), or 0 for a runtime
+// count. With EB fixed every wave issues the same, static sequence of memory operations
+// per token (all stores go through buffer views, out-of-range lanes to an offset past
+// the view), so the waits for the next token's loads leave the current token's stores
+// in flight instead of draining them.
+template <int JT, int LT, int NCH, int EB, int NT>
+__global__ __launch_bounds__(NT) void mix_mfma_kernel(Shape sh, const bf16* __restrict__ H,
                                                        const float* __restrict__ rinv,
                                                        const bf16* __restrict__ g_pre,
                                                        float* alpha, bf16* __restrict__ mixed,
                                                        float* __restrict__ rinv_mid, int tpb) {
   extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int kMixThreads = NT, kMixWaves = NT / 64, kMixCoefPer = kMixCoefMax / NT;
   const int L = sh.L, k = sh.k, D = sh.D, N = sh.N(), kL = k * L;
   const int LDH = mix_mfma_ldh(D), DG = D / 8, chunks = L * DG;
   constexpr int CLD = 16 * LT + 4;
   bf16* Hs = (bf16*)smem;                                     // [L + 1][LDH], row L zero
   bf16* Cs = Hs + (size_t)(L + 1) * LDH;                      // [2 br][2 hi/lo][16 JT][CLD]
-  float* part = (float*)(Cs + 2 * 2 * 16 * JT * CLD);         // [4 waves][2 br][16 JT]
+  float* part = (float*)(Cs + 2 * 2 * 16 * JT * CLD);         // [waves][2 br][16 JT]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, jj = lane & 15;
   const int n_beg = blockIdx.x * tpb, n_end = min(N, n_beg + tpb);
 
   // coefficient rows j >= k and slots l >= L, and the zero state row, stay zero
-  for (int e = tid; e < 2 * 2 * 16 * JT * CLD; e += 256) Cs[e] = (bf16)0.f;
-  for (int e = tid; e < LDH; e += 256) Hs[L * LDH + e] = (bf16)0.f;
+  for (int e = tid; e < 2 * 2 * 16 * JT * CLD; e += kMixThreads) Cs[e] = (bf16)0.f;
+  for (int e = tid; e < LDH; e += kMixThreads) Hs[L * LDH + e] = (bf16)0.f;
 
-  // this thread's chunks: c = tid + 256 i -> layer c / DG, states 8 (c % DG) .. + 7
-  frag_t<bf16> hv[NCH];
-  // coefficient entries x = tid + 256 i -> (br, j, l); their LDS slot is fixed
+  // this thread's chunks: c = tid + kMixThreads i -> layer c / DG, states 8 (c % DG) .. + 7
+  frag_t<bf16> hv[NCH], gv[NCH];
+  uint32_t coff[NCH];  // byte offset of chunk i in an [L][D] array (past the end: out of range)
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const int c = tid + kMixThreads * i;
+    const int l = c / DG, eg = c - l * DG;
+    coff[i] = c < chunks ? (uint32_t)(l * D + 8 * eg) * 2u : kOffOob;
+  }
+  // coefficient entries x = tid + kMixThreads i -> (br, j, l); their LDS slot is fixed
   float av[kMixCoefPer], rv[kMixCoefPer];
   int xin[kMixCoefPer], xcs[kMixCoefPer], xl[kMixCoefPer];
 #pragma unroll
   for (int i = 0; i < kMixCoefPer; ++i) {
-    const int x = min(tid + 256 * i, 2 * kL - 1);
+    const int x = min(tid + kMixThreads * i, 2 * kL - 1);
     const int br = x / kL, jl = x - br * kL, j = jl / L, l = jl - j * L;
     xin[i] = br * N * kL + jl;  // + n * kL
     xcs[i] = ((br * 2) * 16 * JT + j) * CLD + l;
     xl[i] = l;
   }
-  auto fetch = [&](long n) {
+  const auto gview0 = make_view(g_pre, (uint32_t)((long)L * D * 2));
+  const auto gview1 = make_view(g_pre + (long)L * D, (uint32_t)((long)L * D * 2));
+  auto fetch = [&](long n) {  // the states and coefficients of token n
     const auto view = make_view(H + n * L * D, (uint32_t)((long)L * D * 2));
 #pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = tid + 256 * i;
-      const int l = c / DG, eg = c - l * DG;
-      hv[i] = buf_frag<bf16>(view, c < chunks ? (uint32_t)(l * D + 8 * eg) * 2u : kOffOob);
-    }
+    for (int i = 0; i < NCH; ++i) hv[i] = buf_frag<bf16>(view, coff[i]);
 #pragma unroll
     for (int i = 0; i < kMixCoefPer; ++i) {
       av[i] = alpha[(long)xin[i] + n * kL];
       rv[i] = rinv[n * L + xl[i]];
     }
   };
-  if (n_beg < n_end) fetch(n_beg);
+  auto fetch_gain = [&](const __amdgpu_buffer_rsrc_t& gview) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) gv[i] = buf_frag<bf16>(gview, coff[i]);
+  };
+  // stage g * h as bf16; chunks past the end land in row 0's padding (columns D .. D+7,
+  // never read)
+  auto stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + kMixThreads * i;
+      const int l = c / DG, eg = c - l * DG;
+      bf16x8 v;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = (bf16)((float)hv[i][t] * (float)gv[i][t]);
+      *(bf16x8*)(Hs + (c < chunks ? l * LDH + 8 * eg : D)) = v;
+    }
+  };
+  if (n_beg < n_end) {
+    fetch(n_beg);
+    fetch_gain(gview0);
+  }
   __syncthreads();
 
   // per-lane LDS byte address of the transposing read: lane j of each 16-lane group
@@ -680,105 +717,120 @@ __global__ __launch_bounds__(256) void mix_mfma_kernel(Shape sh, const bf16* __r
     const int row = min(16 * lt + 4 * g + (jj >> 2), L);
     tr_base[lt] = (uint32_t)(uintptr_t)(Hs + row * LDH + 4 * (jj & 3));
   }
+  // output views: mixed[br] ([k][N][D]) and rinv_mid; lane rows j >= k store out of range
+  const auto mview0 = make_view(mixed, (uint32_t)((long)k * N * D * 2));
+  const auto mview1 = make_view(mixed + (long)k * N * D, (uint32_t)((long)k * N * D * 2));
+  const auto rview = make_view(rinv_mid, (uint32_t)(2L * k * N * 4));
+
+  // One branch: O[j][e] = sum_l C[j][l] (g h)[l][e] on the matrix cores, stored as bf16,
+  // and the wave's sums of squares per channel into part.
+  auto branch = [&](const int br, const long n) {
+    bf16x4 bh[JT][LT], bl[JT][LT];
+    float ss[JT];
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+#pragma unroll
+      for (int lt = 0; lt < LT; ++lt) {
+        const bf16* crow = Cs + ((br * 2) * 16 * JT + 16 * jt + jj) * CLD + 16 * lt + 4 * g;
+        bh[jt][lt] = *(const bf16x4*)crow;
+        bl[jt][lt] = *(const bf16x4*)(crow + 16 * JT * CLD);
+      }
+      ss[jt] = 0.f;
+    }
+    uint32_t moff[JT];
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      const int j = 16 * jt + jj;
+      moff[jt] = j < k ? (uint32_t)(((long)j * N + n) * D + 4 * g) * 2u : kOffOob;
+    }
+    auto column = [&](const int eb) {
+      bf16x4 a[LT];
+#pragma unroll
+      for (int lt = 0; lt < LT; ++lt) {
+        typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+        const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4*)(uintptr_t)(tr_base[lt] + (uint32_t)(16 * eb) * 2u));
+        a[lt] = __builtin_bit_cast(bf16x4, v);
+      }
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int lt = 0; lt < LT; ++lt) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a[lt]),
+                                                         __builtin_bit_cast(i16x4_t, bh[jt][lt]),
+                                                         acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a[lt]),
+                                                         __builtin_bit_cast(i16x4_t, bl[jt][lt]),
+                                                         acc, 0, 0, 0);
+        }
+        // acc[t]: state 16 eb + 4 g + t of channel 16 jt + jj
+        bf16x4 o;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          o[t] = (bf16)acc[t];
+          ss[jt] += acc[t] * acc[t];
+        }
+        typedef int i32x2_t __attribute__((ext_vector_type(2)));
+        __builtin_amdgcn_raw_buffer_store_b64(
+            __builtin_bit_cast(i32x2_t, o), br ? mview1 : mview0,
+            moff[jt] == kOffOob ? kOffOob : moff[jt] + (uint32_t)(16 * eb) * 2u, 0, 0);
+      }
+    };
+    if constexpr (EB > 0) {
+#pragma unroll
+      for (int e = 0; e < EB; ++e) {
+        column(w + kMixWaves * e);
+        // with 8 waves, keep the columns in order (fewer values live at once)
+        if constexpr (NT == 512) __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      for (int eb = w; eb < D / 16; eb += kMixWaves) column(eb);
+    }
+    // sum of squares of channel j over the wave's states: the 4 lane groups hold parts
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      float v = ss[jt];
+      v += __shfl_xor(v, 16, 64);
+      v += __shfl_xor(v, 32, 64);
+      if (g == 0) part[(w * 2 + br) * 16 * JT + 16 * jt + jj] = v;
+    }
+  };
 
   for (int n = n_beg; n < n_end; ++n) {
     // coefficients of both branches (alpha is already normalised in softmax mode)
 #pragma unroll
     for (int i = 0; i < kMixCoefPer; ++i) {
-      if (tid + 256 * i < 2 * kL) {
+      if (tid + kMixThreads * i < 2 * kL) {
         const float c = av[i] * rv[i];
         const bf16 ch = (bf16)c;
         Cs[xcs[i]] = ch;
         Cs[xcs[i] + 16 * JT * CLD] = (bf16)(c - (float)ch);
       }
     }
-#pragma unroll 1
-    for (int br = 0; br < 2; ++br) {
-      // stage g_pre[br] * h as bf16. Branch-free, so the gain loads stay in flight
-      // together: chunks past the end read zeros and land in row 0's padding
-      // (columns D .. D+7, never read).
-      {
-        const auto gview = make_view(g_pre + (long)br * L * D, (uint32_t)((long)L * D * 2));
-        bf16x8 gv[NCH];
-#pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-          const int c = tid + 256 * i;
-          const int l = c / DG, eg = c - l * DG;
-          gv[i] = buf_frag<bf16>(gview, c < chunks ? (uint32_t)(l * D + 8 * eg) * 2u : kOffOob);
-        }
-#pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-          const int c = tid + 256 * i;
-          const int l = c / DG, eg = c - l * DG;
-          bf16x8 v;
-#pragma unroll
-          for (int t = 0; t < 8; ++t) v[t] = (bf16)((float)hv[i][t] * (float)gv[i][t]);
-          *(bf16x8*)(Hs + (c < chunks ? l * LDH + 8 * eg : D)) = v;
-        }
-      }
-      if (br == 1 && n + 1 < n_end) fetch(n + 1);  // the states are staged: refill
-      __syncthreads();
-
-      bf16x4 bh[JT][LT], bl[JT][LT];
-      float ss[JT];
-#pragma unroll
-      for (int jt = 0; jt < JT; ++jt) {
-#pragma unroll
-        for (int lt = 0; lt < LT; ++lt) {
-          const bf16* crow = Cs + ((br * 2) * 16 * JT + 16 * jt + jj) * CLD + 16 * lt + 4 * g;
-          bh[jt][lt] = *(const bf16x4*)crow;
-          bl[jt][lt] = *(const bf16x4*)(crow + 16 * JT * CLD);
-        }
-        ss[jt] = 0.f;
-      }
-      for (int eb = w; eb < D / 16; eb += 4) {
-        bf16x4 a[LT];
-#pragma unroll
-        for (int lt = 0; lt < LT; ++lt) {
-          typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
-          const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4*)(uintptr_t)(tr_base[lt] + (uint32_t)(16 * eb) * 2u));
-          a[lt] = __builtin_bit_cast(bf16x4, v);
-        }
-#pragma unroll
-        for (int jt = 0; jt < JT; ++jt) {
-          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int lt = 0; lt < LT; ++lt) {
-            acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a[lt]),
-                                                           __builtin_bit_cast(i16x4_t, bh[jt][lt]),
-                                                           acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a[lt]),
-                                                           __builtin_bit_cast(i16x4_t, bl[jt][lt]),
-                                                           acc, 0, 0, 0);
-          }
-          // acc[t]: state 16 eb + 4 g + t of channel 16 jt + jj
-          const int j = 16 * jt + jj;
-          bf16x4 o;
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            o[t] = (bf16)acc[t];
-            ss[jt] += acc[t] * acc[t];
-          }
-          if (j < k) *(bf16x4*)(mixed + (((long)br * k + j) * N + n) * D + 16 * eb + 4 * g) = o;
-        }
-      }
-      // sum of squares of channel j over the wave's states: the 4 lane groups hold parts
-#pragma unroll
-      for (int jt = 0; jt < JT; ++jt) {
-        float v = ss[jt];
-        v += __shfl_xor(v, 16, 64);
-        v += __shfl_xor(v, 32, 64);
-        if (g == 0) part[(w * 2 + br) * 16 * JT + 16 * jt + jj] = v;
-      }
-      __syncthreads();  // Hs is rewritten next; part is complete after the second branch
+    stage();             // branch 0 (waits for this token's states and the branch-0 gains)
+    fetch_gain(gview1);  // issued before branch 0's stores, so its wait leaves them in flight
+    __syncthreads();
+    branch(0, n);
+    __syncthreads();     // Hs is rewritten next
+    stage();             // branch 1
+    if (n + 1 < n_end) {  // next token's states and branch-0 gains, ahead of branch 1's stores
+      fetch(n + 1);
+      fetch_gain(gview0);
     }
-    if (tid < 2 * k) {
+    __syncthreads();
+    branch(1, n);
+    __syncthreads();     // Hs is rewritten next; part is complete
+    {
       const int br = tid / k, j = tid - br * k;
       float v = 0.f;
+      if (tid < 2 * k) {
 #pragma unroll
-      for (int ww = 0; ww < 4; ++ww) v += part[(ww * 2 + br) * 16 * JT + j];
-      rinv_mid[((long)br * k + j) * N + n] = 1.0f / sqrtf(v / (float)D + sh.eps);
+        for (int ww = 0; ww < kMixWaves; ++ww) v += part[(ww * 2 + br) * 16 * JT + j];
+      }
+      __builtin_amdgcn_raw_buffer_store_b32(
+          __float_as_uint(1.0f / sqrtf(v / (float)D + sh.eps)), rview,
+          tid < 2 * k ? (uint32_t)(((long)br * k + j) * N + n) * 4u : kOffOob, 0, 0);
     }
   }
 }
@@ -799,7 +851,8 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(float* alpha, long ro
 template <int JT, int LT>
 static void mix_mfma_launch(const Shape& sh, const bf16* H, const float* rinv, const bf16* g_pre,
                             float* alpha, bf16* mixed, float* rinv_mid, hipStream_t s) {
-  const int nch = (sh.L * (sh.D / 8) + 255) / 256;
+  const int nt = mix_threads(sh.L, sh.D);
+  const int nch = (sh.L * (sh.D / 8) + nt - 1) / nt;
   if (sh.mix_softmax) {
     const long rows = 2L * sh.N() * sh.k;
     hipLaunchKernelGGL(softmax_rows_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s,
@@ -807,17 +860,31 @@ static void mix_mfma_launch(const Shape& sh, const bf16* H, const float* rinv, c
   }
   // tokens per block: up to kMixTok, fewer when that would leave under ~2048 blocks
   const int tpb = std::max(1, std::min(kMixTok, sh.N() / 2048));
-  const dim3 grid((sh.N() + tpb - 1) / tpb), block(256);
+  const dim3 grid((sh.N() + tpb - 1) / tpb), block(nt);
   const size_t smem = mix_mfma_smem(sh);
-#define WM_MIX_GO(NC)                                                                          \
-  hipLaunchKernelGGL((mix_mfma_kernel<JT, LT, NC>), grid, block, smem, s, sh, H, rinv, g_pre, alpha, \
-                     mixed, rinv_mid, tpb)
-  if (nch <= 2) WM_MIX_GO(2);
-  else if (nch <= 4) WM_MIX_GO(4);
-  else if (nch <= 6) WM_MIX_GO(6);
-  else if (nch <= 8) WM_MIX_GO(8);
-  else if (nch <= 12) WM_MIX_GO(12);
-  else WM_MIX_GO(16);
+#define WM_MIX_GO(NC, NT)                                                                      \
+  do {                                                                                         \
+    if (sh.D == 768)                                                                           \
+      hipLaunchKernelGGL((mix_mfma_kernel<JT, LT, NC, 768 / 16 / (NT / 64), NT>), grid, block,  \
+                         smem, s, sh, H, rinv, g_pre, alpha, mixed, rinv_mid, tpb);            \
+    else if (sh.D == 1024)                                                                     \
+      hipLaunchKernelGGL((mix_mfma_kernel<JT, LT, NC, 1024 / 16 / (NT / 64), NT>), grid, block, \
+                         smem, s, sh, H, rinv, g_pre, alpha, mixed, rinv_mid, tpb);            \
+    else                                                                                       \
+      hipLaunchKernelGGL((mix_mfma_kernel<JT, LT, NC, 0, NT>), grid, block, smem, s, sh, H,    \
+                         rinv, g_pre, alpha, mixed, rinv_mid, tpb);                            \
+  } while (0)
+  if (nt == 256) {  // at most 6 chunks per thread
+    if (nch <= 2) WM_MIX_GO(2, 256);
+    else if (nch <= 4) WM_MIX_GO(4, 256);
+    else WM_MIX_GO(6, 256);
+  } else {
+    if (nch <= 4) WM_MIX_GO(4, 512);
+    else if (nch <= 6) WM_MIX_GO(6, 512);
+    else if (nch <= 8) WM_MIX_GO(8, 512);
+    else if (nch <= 12) WM_MIX_GO(12, 512);
+    else WM_MIX_GO(16, 512);
+  }
 #undef WM_MIX_GO
 }
 
