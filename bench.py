@@ -208,6 +208,42 @@ def cpu_baseline(w, P, H_cpu, cache_dev):
 
 # ------------------------------------------------------------ main
 
+def measure_ceilings(wm, torch, dev, stream):
+    """On-box ceilings reported beside the published peaks (best of several runs): the
+    library's read-only stream over 1 GiB, a plain 1 GiB device-to-device copy (bytes read
+    + written per second) and the library's matrix-core loop (bf16 flop per second on
+    every CU)."""
+    def timed(fn, reps):
+        best = float("inf")
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            best = min(best, a.elapsed_time(b) * 1e-3)
+        return best
+    n = 1 << 28
+    x = torch.ones(n, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    t_copy = timed(lambda: y.copy_(x), 6)
+    del x, y
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    xr = torch.ones(4 * n, dtype=torch.float32, device=dev)  # 4 GiB, far past the caches
+    t_read = timed(lambda: wm.calibrate_read(xr, sink, stream), 4)
+    del xr
+    blocks, iters = 2048, 16384
+    wm.calibrate_mfma(blocks, 64, sink, stream)
+    t_mfma = timed(lambda: wm.calibrate_mfma(blocks, iters, sink, stream), 4)
+    return {"hbm_read_gbs": round(16 * n / t_read / 1e9, 1),
+            "hbm_copy_gbs": round(2 * 4 * n / t_copy / 1e9, 1),
+            "mfma_bf16_tflops": round(blocks * iters * 2 ** 20 / t_mfma / 1e12, 1),
+            "method": "best of 4 runs of wm_calibrate_read over 4 GiB, of 6 copies of 1 GiB "
+                      "(read + written bytes) and of 4 launches of wm_calibrate_mfma(2048 "
+                      "blocks, 16384 iterations), event-timed"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -308,6 +344,13 @@ def main():
     roof["phase"] = dom
     roof["duration_ms"] = round(mean[dom], 4)
     roof["traffic"] = measured_traffic(w.name, dom)
+    ceilings = measure_ceilings(wm, torch, dev, stream)
+    if roof["bound"] == "hbm":
+        roof["measured_ceiling"] = ceilings["hbm_read_gbs"]
+    elif w.dtype == "bf16":
+        roof["measured_ceiling"] = ceilings["mfma_bf16_tflops"]
+    if "measured_ceiling" in roof:
+        roof["frac_of_measured_ceiling"] = round(achieved / roof["measured_ceiling"], 4)
 
     ms_per_step = wall / args.steps * 1e3
     tokens = w.N * args.steps
@@ -328,6 +371,7 @@ def main():
                    "ctx": w.ctx, "L": w.L, "k": w.k, "D": w.D, "Hq": w.Hq, "Hkv": w.Hkv,
                    "d": w.d, "p": w.p, "tokens_per_step": w.N},
         "roofline": roof,
+        "ceilings": ceilings,
         "step_roofline": {"gflop": round(flops / 1e9, 2), "min_hbm_gb": round(min_bytes / 1e9, 3),
                           "event_ms_per_step_median": round(float(np.median(step_ms)), 4),
                           "phases_ms": {k: round(v, 4) for k, v in mean.items()}},

@@ -205,6 +205,20 @@ int wm_init_bias(int32_t L, int32_t k, float *b);
 const char *wm_last_error(void);
 const char *wm_version(void);
 
+/* Measurement helper, not part of the method: launches `blocks` workgroups of 4
+ * waves on `stream`, each wave issuing 8 * iters independent 32x32x16 bf16 MFMAs
+ * (blocks * iters * 1048576 flop in all), so that a caller timing it with events
+ * reads the matrix-core ceiling of the device. sink: device float, caller-owned;
+ * written only in a case that does not occur, kept so the loop is not removed.
+ * WM_ERR_ARG for blocks or iters <= 0 (or above 2^20 / 2^24) or a NULL sink. */
+int wm_calibrate_mfma(int32_t blocks, int32_t iters, float *sink, wm_stream_t stream);
+
+/* Measurement helper, not part of the method: reads `bytes` of the device buffer buf
+ * once on `stream` (the HBM read ceiling when timed with events). buf: caller-owned,
+ * 16-byte aligned, bytes a positive multiple of 16; sink as above. WM_ERR_ARG
+ * otherwise. */
+int wm_calibrate_read(const void *buf, size_t bytes, float *sink, wm_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
         "wm_channel_groups": [ctypes.c_int32, ctypes.c_int32, _i32p, _i32p, _i32p],
         "wm_default_map": [ctypes.c_int32, ctypes.c_int32, _i32p],
         "wm_init_bias": [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_float)],
+        "wm_calibrate_mfma": [ctypes.c_int32, ctypes.c_int32, _vp, _vp],
+        "wm_calibrate_read": [_vp, _sz, _vp, _vp],
     }
     for name, argtypes in sig.items():
         fn = getattr(L, name)
@@ -240,3 +242,15 @@ def layer_step_profiled(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, eve
     _check(lib().wm_layer_step_profiled(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H),
                                         _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
                                         _ptr(O), wp, wn, _stream(stream), ev))
+
+
+def calibrate_mfma(blocks: int, iters: int, sink, stream=None):
+    """Launch the matrix-core ceiling loop (blocks * iters * 2**20 flop) on the stream;
+    sink is a device float tensor the kernel keeps but does not write."""
+    _check(lib().wm_calibrate_mfma(blocks, iters, _ptr(sink), _stream(stream)))
+
+
+def calibrate_read(buf, sink, stream=None):
+    """Launch the HBM read-ceiling loop over all bytes of the device tensor buf."""
+    _check(lib().wm_calibrate_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                                   _stream(stream)))

@@ -308,6 +308,22 @@ extern "C" {
 const char* wm_last_error(void) { return g_err; }
 const char* wm_version(void) { return "whitematter-gfx950 0.1.0"; }
 
+int wm_calibrate_mfma(int32_t blocks, int32_t iters, float* sink, wm_stream_t stream) {
+  if (blocks <= 0 || iters <= 0) return fail(WM_ERR_ARG, "blocks and iters must be positive");
+  if (blocks > (1 << 20) || iters > (1 << 24)) return fail(WM_ERR_ARG, "blocks or iters too large");
+  if (!sink) return fail(WM_ERR_ARG, "sink is NULL");
+  wm::launch_mfma_loop(blocks, iters, sink, (hipStream_t)stream);
+  return launched();
+}
+
+int wm_calibrate_read(const void* buf, size_t bytes, float* sink, wm_stream_t stream) {
+  if (!buf || !sink) return fail(WM_ERR_ARG, "buf or sink is NULL");
+  if ((uintptr_t)buf % 16 != 0 || bytes % 16 != 0 || bytes == 0)
+    return fail(WM_ERR_ARG, "buf must be 16-byte aligned and bytes a positive multiple of 16");
+  wm::launch_read_loop(buf, (long)(bytes / 16), sink, (hipStream_t)stream);
+  return launched();
+}
+
 int wm_validate(const wm_dims* dims, int op, const int32_t* chan_map) {
   return validate_dims(dims, op, chan_map);
 }

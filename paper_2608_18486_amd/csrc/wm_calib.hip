@@ -1,0 +1,59 @@
+// Measurement helper (not part of the method): a loop of independent bf16 MFMAs on
+// every CU, so that a benchmark can read the matrix-core ceiling of the device it runs
+// on and report kernels against it as well as against the published peak.
+#include "wm_device.hpp"
+#include "wm_internal.hpp"
+
+namespace wm {
+
+// Each wave keeps 8 independent 32x32 accumulators (no MFMA waits on the previous
+// one) and issues 8 * iters v_mfma_f32_32x32x16_bf16, i.e. 8 * iters * 32768 flop.
+__global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float* sink) {
+  bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {  // operands the compiler cannot fold
+    a[i] = (bf16)(1e-3f * (float)(threadIdx.x + i));
+    b[i] = (bf16)(1e-3f * (float)(blockIdx.x + i));
+  }
+  f32x16 acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = zero16();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = mma32(acc[j], a, b);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) s += acc[j][q];
+  if (s == 1.2345e-30f) sink[0] = s;  // never true for these operands; keeps the loop live
+}
+
+void launch_mfma_loop(int blocks, int iters, float* sink, hipStream_t s) {
+  hipLaunchKernelGGL(mfma_loop_kernel, dim3(blocks), dim3(256), 0, s, iters, sink);
+}
+
+// Streams n16 16-byte chunks once (grid-stride, eight loads in flight per thread) and
+// folds them into a value that is stored only in a case that does not occur.
+__global__ __launch_bounds__(256) void read_loop_kernel(const i32x4* __restrict__ p, long n16,
+                                                        float* sink) {
+  const long stride = (long)gridDim.x * 256;
+  i32x4 acc = {0, 0, 0, 0};
+  long i = (long)blockIdx.x * 256 + threadIdx.x;
+  for (; i + 7 * stride < n16; i += 8 * stride) {
+    i32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u];
+  }
+  for (; i < n16; i += stride) acc ^= p[i];
+  if ((acc.x & acc.y & acc.z & acc.w) == 0x7F123456) sink[0] = 1.f;
+}
+
+void launch_read_loop(const void* buf, long n16, float* sink, hipStream_t s) {
+  hipLaunchKernelGGL(read_loop_kernel, dim3(8192), dim3(256), 0, s, (const i32x4*)buf, n16, sink);
+}
+
+}  // namespace wm

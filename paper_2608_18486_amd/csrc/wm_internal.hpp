@@ -83,4 +83,10 @@ void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const Cha
                           const T* Q, const T* Kc, const T* Vc, const T* Kd, const T* Vd,
                           const int32_t* ctx_len, float* partials, T* O, hipStream_t s);
 
+// -- measurement helper ---------------------------------------------------------
+// blocks x 4 waves, each issuing 8 * iters independent 32x32x16 bf16 MFMAs.
+void launch_mfma_loop(int blocks, int iters, float* sink, hipStream_t s);
+// Reads n16 16-byte chunks of buf once.
+void launch_read_loop(const void* buf, long n16, float* sink, hipStream_t s);
+
 }  // namespace wm

@@ -177,3 +177,20 @@ def test_init_bias_and_default_map_match_oracle(wm, oracle_lib):
             assert wm.default_map(L, k) == [l % k for l in range(L)]
     with pytest.raises(wm.WMError):
         wm.init_bias(4, 5)
+
+
+def test_calibration_rejects_bad_arguments(wm):
+    L = wm.lib()
+    assert L.wm_calibrate_mfma(0, 10, None, None) == wm.ERR_ARG
+    assert L.wm_calibrate_mfma(10, 0, None, None) == wm.ERR_ARG
+    assert L.wm_calibrate_mfma(10, 10, None, None) == wm.ERR_ARG
+    assert "sink" in wm.last_error()
+
+
+def test_read_calibration_rejects_bad_arguments(wm):
+    L = wm.lib()
+    assert L.wm_calibrate_read(None, 16, None, None) == wm.ERR_ARG
+    # misaligned buffer: rejected on the host, nothing is launched or read
+    assert L.wm_calibrate_read(17, 16, 16, None) == wm.ERR_ARG
+    assert L.wm_calibrate_read(32, 0, 16, None) == wm.ERR_ARG
+    assert L.wm_calibrate_read(32, 24, 16, None) == wm.ERR_ARG

@@ -351,3 +351,22 @@ def test_decode_step_at_full_size(wm):
         Oo = oracle.channel_attend(dm, PP, Qo, w.chan_map, [w.ctx], Ko, Vo)
         check_close(O[:, b:b + 1], Oo, w.dtype, "decode O b=%d" % b)
         del Ko, Vo
+
+
+@pytest.mark.gpu
+def test_calibration_loop_runs(wm):
+    """The matrix-core ceiling loop launches, finishes and leaves its sink untouched."""
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    wm.calibrate_mfma(256, 16, sink, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert float(sink.item()) == 0.0
+
+
+@pytest.mark.gpu
+def test_read_calibration_runs(wm):
+    """The HBM read loop (ragged tail included) finishes and leaves its sink untouched."""
+    buf = torch.arange((1 << 20) + 12, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    wm.calibrate_read(buf, sink, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert float(sink.item()) == 0.0
