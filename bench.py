@@ -176,8 +176,8 @@ def measured_traffic(workload, kernel):
 # ------------------------------------------------------------ CPU baseline
 
 def cpu_baseline(w, P, H_cpu, cache_dev):
-    """The oracle, as it stands, on a bounded sample: one sequence of a full-sequence pass,
-    or two sequences of a decode step."""
+    """The oracle, as it stands, on a bounded sample: up to 8 sequences of the step (the
+    whole 2048-token pass of B = 8 takes about 15 s on 16 host threads)."""
     import numpy as np
     import torch
 
@@ -185,7 +185,7 @@ def cpu_baseline(w, P, H_cpu, cache_dev):
     from tests import synth
 
     oracle.build(force=False)
-    nseq = 1 if w.T_new > 1 else 2
+    nseq = min(w.B, 8)
     w1 = synth.Workload(w.name, nseq, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.ctx, w.dtype,
                         w.chan_map, w.p, w.seed)
     dm = oracle.Dims(B=nseq, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d,
@@ -201,7 +201,14 @@ def cpu_baseline(w, P, H_cpu, cache_dev):
     oracle.layer_step(dm, PP, Hs, w.chan_map, ctx, Kc, Vc)
     dt = time.perf_counter() - t0
     toks = nseq * w.T_new
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next(ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
     return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "cpu": cpu,
             "sample": "%d of %d sequences (%d tokens), whole step (pool, queries, attention over "
                       "%d cached + new slots), %.1f s" % (nseq, w.B, toks, w.ctx, dt)}
 
@@ -353,6 +360,9 @@ def main():
         roof["frac_of_measured_ceiling"] = round(achieved / roof["measured_ceiling"], 4)
 
     ms_per_step = wall / args.steps * 1e3
+    # the fused step's roofline: each phase at the slower of its flops and its bytes
+    t_roof = sum(max(f / (PEAK_TFLOPS[w.dtype] * 1e12), b / (PEAK_HBM_GBS * 1e9))
+                 for f, b in costs.values())
     tokens = w.N * args.steps
     line = {
         "metric": "tokens/s of mix+KV-proj+channel-attention step; % of HBM / MFMA roofline",
@@ -373,6 +383,8 @@ def main():
         "roofline": roof,
         "ceilings": ceilings,
         "step_roofline": {"gflop": round(flops / 1e9, 2), "min_hbm_gb": round(min_bytes / 1e9, 3),
+                          "t_roof_ms": round(t_roof * 1e3, 4),
+                          "frac": round(t_roof / (ms_per_step * 1e-3), 4),
                           "event_ms_per_step_median": round(float(np.median(step_ms)), 4),
                           "phases_ms": {k: round(v, 4) for k, v in mean.items()}},
     }
