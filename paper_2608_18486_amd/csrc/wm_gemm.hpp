@@ -20,6 +20,13 @@
 
 namespace wm {
 
+// LDS an epilogue may use once the main loop is done (one with kUsesLds set, in the
+// LDS-staged kernel): 32 x 32 WO elements of T per wave, at p + wave * that.
+struct EpiLds {
+  char* p;
+  int wave;
+};
+
 template <typename T, int BK_, int WGO_, int WGN_, int WO_, int WN_> struct ProjCfg {
   static constexpr int BK = BK_, WGO = WGO_, WGN = WGN_, WO = WO_, WN = WN_;
   static constexpr int NT = 64 * WGO * WGN;                 // threads
@@ -178,7 +185,7 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_kernel(int M, int Nout, int K
       __syncthreads();
     }
   }
-  epi.template finish<C>(g, ow0, nw0, acc, lane, est);
+  epi.template finish<C>(g, ow0, nw0, acc, lane, est, EpiLds{(char*)smem, w});
 }
 
 // bf16 variant whose K slices travel straight from memory into LDS
@@ -302,7 +309,14 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_dma_kernel(int M, int Nout, i
       epi.template segment<C>(g, (kb + 1) / seg_len, nw0, acc, lane, est);
   }
   wait_vmcnt<0>();  // the trailing prefetches (zeros) land before the block ends
-  epi.template finish<C>(g, ow0, nw0, acc, lane, est);
+  // an epilogue that stages its stores through the ring waits until every wave is past
+  // its last read of it
+  if constexpr (Epi::kUsesLds) {
+    static_assert(sizeof(smem) >= (size_t)(C::NT / 64) * 32 * 32 * C::WO * sizeof(T),
+                  "the epilogue's staging fits the ring");
+    __syncthreads();
+  }
+  epi.template finish<C>(g, ow0, nw0, acc, lane, est, EpiLds{(char*)smem, w});
 }
 
 }  // namespace wm

@@ -114,11 +114,25 @@ template <int DH> __device__ __forceinline__ int head_chan(int v, int h) {
   return 32 * (v >> 4) + 8 * ((v & 15) >> 2) + 4 * h + (v & 3);
 }
 
-template <typename T, int DH, int WO, int WN, class ScaleAt, class DstAt>
+// STAGE (bf16): stores go through the wave's LDS area so that each store instruction
+// writes whole head rows (measured faster for the cache writes of the K/V projection,
+// not for the query workspace).
+// Memory order: every load the epilogue needs for a column block (row scales, the
+// slot base of each token, the RoPE table entries) is issued before the previous
+// block's stores, and every store is issued whether or not its lane has a row to
+// write (lanes without one write to a small trash area of the workspace). So each
+// wave issues a fixed sequence of memory operations, and waiting for a load leaves
+// the earlier blocks' stores in flight instead of draining them.
+//   scale_at(n) -> float   the row's 1/RMS
+//   aux_at(n)   -> int     a per-token value the destination needs (or 0)
+//   dst_at(n, head, aux) -> T*   the row's destination, nullptr when there is none
+template <typename T, int DH, int WO, int WN, bool STAGE, class ScaleAt, class AuxAt,
+          class DstAt>
 __device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, int nw0, int lane,
                                               int M, bool rotate, const T* gain,
                                               const float* tab, float eps, ScaleAt scale_at,
-                                              DstAt dst_at) {
+                                              AuxAt aux_at, DstAt dst_at, T* trash,
+                                              const EpiLds& lds) {
   constexpr int NV = DH / 2;          // values of one head per lane
   constexpr int HPW = 32 * WO / DH;   // heads per wave
   static_assert(HPW * DH == 32 * WO, "a wave holds whole heads");
@@ -132,46 +146,65 @@ __device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, in
       for (int t = 0; t < 4; ++t) gv[4 * c + t] = to_f32(gp[t]);
     }
   }
+  int nn[WN];
+  bool in[WN];
+  float sc[WN];
+  int aux[WN];
 #pragma unroll
   for (int jn = 0; jn < WN; ++jn) {
     const int n = nw0 + 32 * jn + r;
-    const bool in = n < M;
-    const int nn = in ? n : M - 1;
-    const float sc = scale_at(nn);
-    f32x4 tb[DH / 16][2];  // (cos, sin) of angle indices 8g + 4h + t, t = 0..3
-    if (rotate) {
+    in[jn] = n < M;
+    nn[jn] = in[jn] ? n : M - 1;
+    sc[jn] = scale_at(nn[jn]);
+    aux[jn] = aux_at(nn[jn]);
+  }
+  f32x4 tb[DH / 16][2];  // (cos, sin) of angle indices 8g + 4h + t, t = 0..3
+  auto load_tab = [&](int jn) {
 #pragma unroll
-      for (int g = 0; g < DH / 16; ++g) {
-        const float* tp = tab + (long)nn * DH + 2 * (8 * g + 4 * h);
-        tb[g][0] = *(const f32x4*)tp;
-        tb[g][1] = *(const f32x4*)(tp + 4);
-      }
+    for (int g = 0; g < DH / 16; ++g) {
+      const float* tp = tab + (long)nn[jn] * DH + 2 * (8 * g + 4 * h);
+      tb[g][0] = *(const f32x4*)tp;
+      tb[g][1] = *(const f32x4*)(tp + 4);
     }
+  };
+  if (rotate) load_tab(0);
+#pragma unroll
+  for (int jn = 0; jn < WN; ++jn) {
+    float c[HPW][NV];
 #pragma unroll
     for (int hw = 0; hw < HPW; ++hw) {
-      float c[NV];
 #pragma unroll
-      for (int v = 0; v < NV; ++v) c[v] = acc[hw * (DH / 32) + (v >> 4)][jn][v & 15] * sc;
+      for (int v = 0; v < NV; ++v) c[hw][v] = acc[hw * (DH / 32) + (v >> 4)][jn][v & 15] * sc[jn];
       if (rotate) {
         float ss = 0.f;
 #pragma unroll
-        for (int v = 0; v < NV; ++v) ss += c[v] * c[v];
+        for (int v = 0; v < NV; ++v) ss += c[hw][v] * c[hw][v];
         ss = halves_sum(ss);
         const float rs = 1.0f / sqrtf(ss / (float)DH + eps);
 #pragma unroll
-        for (int v = 0; v < NV; ++v) c[v] *= rs * gv[v];
+        for (int v = 0; v < NV; ++v) c[hw][v] *= rs * gv[v];
 #pragma unroll
         for (int v = 0; v < NV / 2; ++v) {
           const int t = v & 3;
           const float cs = tb[v >> 2][t >> 1][2 * (t & 1)], sn = tb[v >> 2][t >> 1][2 * (t & 1) + 1];
-          const float x1 = c[v], x2 = c[v + NV / 2];
-          c[v] = x1 * cs - x2 * sn;
-          c[v + NV / 2] = x2 * cs + x1 * sn;
+          const float x1 = c[hw][v], x2 = c[hw][v + NV / 2];
+          c[hw][v] = x1 * cs - x2 * sn;
+          c[hw][v + NV / 2] = x2 * cs + x1 * sn;
         }
       }
-      T* dst = dst_at(nn, (ow0 + hw * DH) / DH);
-      const bool ok = in && dst != nullptr;
-      if constexpr (sizeof(T) == 2) {
+    }
+    // the next block's table entries, ahead of this block's stores
+    if (rotate && jn + 1 < WN) load_tab(jn + 1);
+    if constexpr (sizeof(T) == 2 && STAGE) {
+      // Stage the block (32 tokens x HPW heads, one head row of DH channels per token)
+      // in the wave's LDS area, then store it row by row: each store instruction writes
+      // whole head rows (CPR lanes of 16 bytes per row) instead of 32-byte pieces of 32
+      // rows. 16-byte chunk c of row t sits at chunk c ^ ((t / 2) mod CPR).
+      constexpr int CPR = DH / 8, RPI = 64 / CPR, ROWS = 32 * HPW;
+      char* reg = lds.p + lds.wave * (ROWS * DH * 2);
+#pragma unroll
+      for (int hw = 0; hw < HPW; ++hw) {
+        const int row = 32 * hw + r;
         // chunks 2p, 2p+1 (channels m0 + 4h + 0..3 and m0 + 8 + 4h + 0..3): one swap of
         // the middle quarters gives lane h the 8 contiguous channels m0 + 8h .. m0 + 8h + 7
 #pragma unroll
@@ -179,36 +212,78 @@ __device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, in
           uint32_t a[2], b[2];
 #pragma unroll
           for (int i = 0; i < 2; ++i) {
-            bf16x2 x = {(bf16)c[8 * p + 2 * i], (bf16)c[8 * p + 2 * i + 1]};
-            bf16x2 y = {(bf16)c[8 * p + 4 + 2 * i], (bf16)c[8 * p + 4 + 2 * i + 1]};
+            bf16x2 x = {(bf16)c[hw][8 * p + 2 * i], (bf16)c[hw][8 * p + 2 * i + 1]};
+            bf16x2 y = {(bf16)c[hw][8 * p + 4 + 2 * i], (bf16)c[hw][8 * p + 4 + 2 * i + 1]};
             a[i] = __builtin_bit_cast(uint32_t, x);
             b[i] = __builtin_bit_cast(uint32_t, y);
             auto sw = __builtin_amdgcn_permlane32_swap(a[i], b[i], false, false);
             a[i] = sw[0];
             b[i] = sw[1];
           }
-          if (ok) {
-            i32x4 o = {(int)a[0], (int)a[1], (int)b[0], (int)b[1]};
-            *(i32x4*)(dst + 32 * (p >> 1) + 16 * (p & 1) + 8 * h) = o;
-          }
+          const int ch = 4 * (p >> 1) + 2 * (p & 1) + h;  // 16-byte chunk of the row
+          const i32x4 o = {(int)a[0], (int)a[1], (int)b[0], (int)b[1]};
+          *(i32x4*)(reg + row * DH * 2 + 16 * (ch ^ ((row >> 1) & (CPR - 1)))) = o;
         }
-      } else {
-        if (ok) {
+      }
+      const int cl = lane % CPR;
 #pragma unroll
-          for (int q = 0; q < NV / 4; ++q) {
-            f32x4 o = {c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]};
-            *(f32x4*)(dst + head_chan<DH>(4 * q, h)) = o;
+      for (int it = 0; it < ROWS / RPI; ++it) {
+        const int row = RPI * it + lane / CPR, t = row & 31, hw = row >> 5;
+        const i32x4 o = *(const i32x4*)(reg + row * DH * 2 + 16 * (cl ^ ((row >> 1) & (CPR - 1))));
+        const int n = nw0 + 32 * jn + t;
+        const int ax = __shfl(aux[jn], t, 64);
+        T* dst = dst_at(n < M ? n : M - 1, (ow0 + hw * DH) / DH, ax);
+        if (!(n < M && dst != nullptr)) dst = trash;
+        *(i32x4*)(dst + 8 * cl) = o;
+      }
+    } else if constexpr (sizeof(T) == 2) {
+      // direct: each store writes 32 bytes of each of the block's 32 rows
+#pragma unroll
+      for (int hw = 0; hw < HPW; ++hw) {
+        T* dst = dst_at(nn[jn], (ow0 + hw * DH) / DH, aux[jn]);
+        if (!(in[jn] && dst != nullptr)) dst = trash;
+#pragma unroll
+        for (int p = 0; p < NV / 8; ++p) {
+          uint32_t a[2], b[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            bf16x2 x = {(bf16)c[hw][8 * p + 2 * i], (bf16)c[hw][8 * p + 2 * i + 1]};
+            bf16x2 y = {(bf16)c[hw][8 * p + 4 + 2 * i], (bf16)c[hw][8 * p + 4 + 2 * i + 1]};
+            a[i] = __builtin_bit_cast(uint32_t, x);
+            b[i] = __builtin_bit_cast(uint32_t, y);
+            auto sw = __builtin_amdgcn_permlane32_swap(a[i], b[i], false, false);
+            a[i] = sw[0];
+            b[i] = sw[1];
           }
+          i32x4 o = {(int)a[0], (int)a[1], (int)b[0], (int)b[1]};
+          *(i32x4*)(dst + 32 * (p >> 1) + 16 * (p & 1) + 8 * h) = o;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int hw = 0; hw < HPW; ++hw) {
+        T* dst = dst_at(nn[jn], (ow0 + hw * DH) / DH, aux[jn]);
+        if (!(in[jn] && dst != nullptr)) dst = trash;
+#pragma unroll
+        for (int q = 0; q < NV / 4; ++q) {
+          f32x4 o = {c[hw][4 * q], c[hw][4 * q + 1], c[hw][4 * q + 2], c[hw][4 * q + 3]};
+          *(f32x4*)(dst + head_chan<DH>(4 * q, h)) = o;
         }
       }
     }
   }
 }
 
+// Workspace elements (of T) after the folded weights that lanes without a row write
+// to: the bf16 stores reach 64 elements past the pointer, the fp32 ones DH.
+constexpr size_t kTrashElems = 512;
+
 struct NoState {};
 
 template <typename T, int DH> struct KVEpi {
+  static constexpr bool kUsesLds = sizeof(T) == 2;  // stages the cache writes
   T *Kc, *Vc;
+  T* trash;  // kTrashElems elements of workspace
   const float* rs;  // [2k][M] 1 / RMS of each mixed channel row (the mid RMSNorm)
   const T* g_knorm;
   const float* tab;
@@ -221,25 +296,29 @@ template <typename T, int DH> struct KVEpi {
   __device__ void segment(int, int, int, f32x16 (&)[C::WO][C::WN], int, State&) const {}
   template <class C>
   __device__ void finish(int g, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
-                         State&) const {
+                         State&, const EpiLds& lds) const {
     const int br = g / k, j = g - br * k;
     const bool key = br == 0;
     T* base = key ? Kc : Vc;
-    head_epilogue<T, DH, C::WO, C::WN>(
+    head_epilogue<T, DH, C::WO, C::WN, true>(
         acc, ow0, nw0, lane, M, key, g_knorm + (long)j * DH, tab, eps,
         [&](int n) { return rs[(long)g * M + n]; },
-        [&](int n, int head) -> T* {
+        [&](int n) { return ctx_len ? ctx_len[n / T_new] : 0; },
+        [&](int n, int head, int ctx) -> T* {
           if (head >= Hkv) return nullptr;
           const int b = n / T_new, i = n - b * T_new;
-          const long slot = (long)(ctx_len ? ctx_len[b] : 0) + i;
+          const long slot = (long)ctx + i;
           if (slot < 0 || slot >= S_cap) return nullptr;
           return base + ((((long)j * B + b) * Hkv + head) * S_cap + slot) * DH;
-        });
+        },
+        trash, lds);
   }
 };
 
 template <typename T, int DH> struct QEpi {
+  static constexpr bool kUsesLds = false;
   T* Q;
+  T* trash;  // kTrashElems elements of workspace
   const float* rs;  // [M][L] 1 / RMS of each consumer's input state (the input RMSNorm)
   const T* g_qnorm;
   const float* tab;
@@ -251,15 +330,16 @@ template <typename T, int DH> struct QEpi {
   __device__ void segment(int, int, int, f32x16 (&)[C::WO][C::WN], int, State&) const {}
   template <class C>
   __device__ void finish(int l, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
-                         State&) const {
-    head_epilogue<T, DH, C::WO, C::WN>(
+                         State&, const EpiLds& lds) const {
+    head_epilogue<T, DH, C::WO, C::WN, false>(
         acc, ow0, nw0, lane, M, true, g_qnorm + (long)l * DH, tab, eps,
-        [&](int n) { return rs[(long)n * L + l]; },
-        [&](int n, int head) -> T* {
+        [&](int n) { return rs[(long)n * L + l]; }, [](int) { return 0; },
+        [&](int n, int head, int) -> T* {
           if (head >= Hq) return nullptr;
           const int b = n / T_new, i = n - b * T_new;
           return Q + ((((long)l * B + b) * Hq + head) * T_new + i) * DH;
-        });
+        },
+        trash, lds);
   }
 };
 
@@ -270,6 +350,7 @@ template <typename T, int DH> struct QEpi {
 // block covers the layers [s * per, ...) and writes a partial sum for the
 // reduction; without it the bias is added and the logits are stored directly.
 template <typename T> struct RouterEpi {
+  static constexpr bool kUsesLds = false;
   float* out;        // splits == 1: logits [2][M][kL]; else partials [splits][M][2kL]
   const T* bias;     // [2kL]
   const float* rinv; // [M][L]
@@ -308,7 +389,7 @@ template <typename T> struct RouterEpi {
   }
   template <class C>
   __device__ void finish(int s, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
-                         State& st) const {
+                         State& st, const EpiLds&) const {
     const int h = lane >> 5, r = lane & 31;
 #pragma unroll
     for (int jn = 0; jn < C::WN; ++jn) {
@@ -944,8 +1025,9 @@ static void fold_gain(const T* W0, const T* W1, int split, const T* gain, T* Wf,
                      W0, W1, split, gain, Wf, groups, Nout, K);
 }
 
-size_t kv_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.Hkv * sh.d * sh.D; }
-size_t q_fold_elems(const Shape& sh) { return (size_t)sh.L * sh.Hq * sh.d * sh.D; }
+// folded weights, then the epilogue's trash area
+size_t kv_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.Hkv * sh.d * sh.D + kTrashElems; }
+size_t q_fold_elems(const Shape& sh) { return (size_t)sh.L * sh.Hq * sh.d * sh.D + kTrashElems; }
 
 template <typename T, int DH, bool FEW>
 static void kv_gemm(const Shape& sh, const T* mixed, const float* rinv_mid, const T* wfold,
@@ -955,8 +1037,9 @@ static void kv_gemm(const Shape& sh, const T* mixed, const float* rinv_mid, cons
   const int M = sh.N(), Nout = sh.Hkv * DH, K = sh.D;
   PlainRows<T> x{mixed, (long)M * K, K, M};
   PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
-  KVEpi<T, DH> e{Kc, Vc, rinv_mid, g_knorm, rope_tab, ctx_len, M, sh.T_new, sh.B, sh.Hkv,
-                 sh.S_cap, sh.k, sh.eps};
+  T* trash = const_cast<T*>(wfold) + (kv_fold_elems(sh) - kTrashElems);
+  KVEpi<T, DH> e{Kc, Vc, trash, rinv_mid, g_knorm, rope_tab, ctx_len, M, sh.T_new, sh.B,
+                 sh.Hkv, sh.S_cap, sh.k, sh.eps};
   launch_proj<C, T>(M, Nout, K, 2 * sh.k, kNoSegments, 0, x, w, e, s);
 }
 
@@ -984,7 +1067,8 @@ static void q_gemm(const Shape& sh, const T* H, const float* rinv, const T* wfol
   const int M = sh.N(), Nout = sh.Hq * DH, K = sh.D;
   PlainRows<T> x{H, K, (long)sh.L * K, M};
   PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
-  QEpi<T, DH> e{Q, rinv, g_qnorm, rope_tab, M, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
+  T* trash = const_cast<T*>(wfold) + (q_fold_elems(sh) - kTrashElems);
+  QEpi<T, DH> e{Q, trash, rinv, g_qnorm, rope_tab, M, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
   launch_proj<C, T>(M, Nout, K, sh.L, kNoSegments, 0, x, w, e, s);
 }
 
