@@ -38,6 +38,11 @@ WORKLOAD_LABEL = {
     "c4_T4096_L24_k12": "full-sequence pass, B4 T4096 L24 k12 D1024 16x64, bf16, map l->l%12",
     "c5_decode_S32768": "decode step, B64 ctx32768 L24 k12 D1024 16x64, bf16, map l->l%12",
 }
+for _k in (1, 2, 4, 8, 12, 16):
+    WORKLOAD_LABEL["paper_T2048_L16_k%d" % _k] = (
+        "full-sequence pass, the paper's model shape: B16 T2048 L16 k%d D512 6q/3kv x96, p2, "
+        "bf16, map l->l%%%d" % (_k, _k))
+del _k
 
 
 # ------------------------------------------------------------ cost model

@@ -72,7 +72,8 @@ enum wm_op {
 };
 
 /* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
- * D a multiple of 32, Hq a multiple of Hkv, d in {32, 64}, 1 <= p <= L,
+ * D a multiple of 32, Hq a multiple of Hkv, d in {32, 64} (either dtype) or d = 96
+ * (WM_BF16 only), 1 <= p <= L,
  * L * D * sizeof(dtype) <= 64 KiB. */
 typedef struct wm_dims {
   int32_t B;         /* sequences */

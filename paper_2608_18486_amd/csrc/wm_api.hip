@@ -105,7 +105,10 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (d.D < 32 || d.D % 32 != 0) return fail(WM_ERR_SHAPE, "D must be a positive multiple of 32");
   if (d.Hq < 1 || d.Hkv < 1 || d.Hq % d.Hkv != 0)
     return fail(WM_ERR_SHAPE, "Hq must be a positive multiple of Hkv");
-  if (d.d != 32 && d.d != 64) return fail(WM_ERR_SHAPE, "head dim d must be 32 or 64");
+  if (d.d != 32 && d.d != 64 && d.d != 96)
+    return fail(WM_ERR_SHAPE, "head dim d must be 32, 64 or 96");
+  if (d.d == 96 && d.dtype != WM_BF16)
+    return fail(WM_ERR_SHAPE, "head dim 96 is supported in bf16 only");
   if (d.p < 1 || d.p > d.L) return fail(WM_ERR_SHAPE, "p must be in [1, L]");
   if (!(d.eps > 0.f) || !std::isfinite(d.eps)) return fail(WM_ERR_ARG, "eps must be positive");
   if (!(d.rope_theta > 0.f) || !std::isfinite(d.rope_theta))

@@ -779,6 +779,9 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
     hipLaunchKernelGGL(attend_prefill_dma_kernel<kPfQt>,
                        dim3(ad.n_qtiles * sh.Hq * sh.B * sh.L), dim3(PfDma<kPfQt>::NT), 0, s,
                        *reinterpret_cast<const AttnArgs<bf16>*>(&ad));
+  } else if (sh.d == 96) {
+    if constexpr (sizeof(T) == 2)  // fp32 at d = 96 is rejected by validation
+      hipLaunchKernelGGL((attend_prefill_kernel<T, 96>), grid, dim3(NT), 0, s, a);
   } else if (sh.d == 64)
     hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(NT), 0, s, a);
   else
@@ -835,7 +838,12 @@ __device__ __forceinline__ void merge_state(float& m, float& l, float* o, float 
 
 template <typename T, int DH, int NG>
 __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
-  constexpr int LPS = DH / 8;    // lanes per cache slot (8 elements each)
+  // A cache slot is read by CPS lanes of 8 elements each, in a group of LPS lanes (CPS
+  // rounded up to a power of two, so the group's sums are butterflies); lanes c8 >= CPS
+  // of a group load nothing and hold zeros (head dim 96: 12 of 16 lanes work).
+  constexpr int CPS = DH / 8;
+  constexpr int LPS = CPS <= 4 ? 4 : CPS <= 8 ? 8 : 16;
+  static_assert(LPS >= CPS && DH % 8 == 0, "8-element chunks in a power-of-two group");
   constexpr int SPW = 64 / LPS;  // slots per wave per sweep step
   constexpr int U = NG <= 2 ? 2 : 1;  // sweep steps per batch (U slots per lane)
   constexpr int SPB = 4 * SPW * U;  // slots per batch of the 4 waves
@@ -863,8 +871,9 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
   // the slice through buffer views: slots at or past s1 read zeros without a branch
   const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)a.S_cap * DH * sizeof(T));
   const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)a.S_cap * DH * sizeof(T));
+  const bool chunk = c8 < CPS;  // the lane holds 8 channels of the head
   auto slot_off = [&](int s) {
-    return s < s1 ? (uint32_t)(s * DH + 8 * c8) * (uint32_t)sizeof(T) : kOffOob;
+    return s < s1 && chunk ? (uint32_t)(s * DH + 8 * c8) * (uint32_t)sizeof(T) : kOffOob;
   };
 
   for (int g0 = 0; g0 < G; g0 += NG) {
@@ -882,8 +891,12 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
         int i = g % a.T_new, gq = (g / a.T_new) % grp, mi = g / (a.T_new * grp);
         int l = a.cg.members[off + mi], hq = kvh * grp + gq;
         long rowid = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + i;
-        load8(a.Q + rowid * DH + 8 * c8, q[gi]);
         vis[gi] = ctx + i + incl;
+        if (chunk) load8(a.Q + rowid * DH + 8 * c8, q[gi]);
+        else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) q[gi][i] = 0.f;
+        }
       } else {
         vis[gi] = 0;
 #pragma unroll
@@ -957,7 +970,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
         for (int i = 0; i < 8; ++i) o2[i] = __shfl_xor(o[gi][i], msk, 64);
         merge_state(m[gi], ls[gi], o[gi], m2, l2, o2, 8, cl2);
       }
-    if (sg == 0) {
+    if (sg == 0 && chunk) {
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
 #pragma unroll
@@ -998,7 +1011,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
 // One wave per query row: fold the dummy slot and all split partials.
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void attend_combine_kernel(DecodeArgs<T> a) {
-  constexpr int EPL = DH / 64 > 0 ? DH / 64 : 1;  // elements per lane
+  constexpr int EPL = (DH + 63) / 64;  // elements per lane: channel 64 e + lane
   const long rows = (long)a.L * a.B * a.Hq * a.T_new;
   const long rid = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -1013,17 +1026,17 @@ __global__ __launch_bounds__(256) void attend_combine_kernel(DecodeArgs<T> a) {
   const float cl2 = a.scale_log2;
 
   float M, Lsum, o[EPL];
-  const bool active = lane * EPL < DH;
+  auto active = [&](int e) { return 64 * e + lane < DH; };
   if (a.mask_paper) {
     const T* q = a.Q + rid * DH;
     const T* kd = a.Kd + ((long)c * a.Hkv + kvh) * DH;
     const T* vd = a.Vd + ((long)c * a.Hkv + kvh) * DH;
     float part = 0.f;
     for (int e = 0; e < EPL; ++e)
-      if (active) part += to_f32(q[lane * EPL + e]) * to_f32(kd[lane * EPL + e]);
+      if (active(e)) part += to_f32(q[64 * e + lane]) * to_f32(kd[64 * e + lane]);
     M = wave_sum(part);
     Lsum = 1.f;
-    for (int e = 0; e < EPL; ++e) o[e] = active ? to_f32(vd[lane * EPL + e]) : 0.f;
+    for (int e = 0; e < EPL; ++e) o[e] = active(e) ? to_f32(vd[64 * e + lane]) : 0.f;
   } else {
     M = kNegBig;
     Lsum = 0.f;
@@ -1033,13 +1046,12 @@ __global__ __launch_bounds__(256) void attend_combine_kernel(DecodeArgs<T> a) {
   for (int sidx = 0; sidx < a.nsplit; ++sidx) {
     const float* ps = src + (long)sidx * (DH + 2);
     float o2[EPL];
-    for (int e = 0; e < EPL; ++e) o2[e] = active ? ps[lane * EPL + e] : 0.f;
+    for (int e = 0; e < EPL; ++e) o2[e] = active(e) ? ps[64 * e + lane] : 0.f;
     merge_state(M, Lsum, o, ps[DH], ps[DH + 1], o2, EPL, cl2);
   }
-  if (active) {
-    T* dst = a.O + ((((long)l * a.B + b) * a.T_new + i) * a.Hq + hq) * DH;
-    for (int e = 0; e < EPL; ++e) dst[lane * EPL + e] = from_f32<T>(o[e] / Lsum);
-  }
+  T* dst = a.O + ((((long)l * a.B + b) * a.T_new + i) * a.Hq + hq) * DH;
+  for (int e = 0; e < EPL; ++e)
+    if (active(e)) dst[64 * e + lane] = from_f32<T>(o[e] / Lsum);
 }
 
 template <typename T, int DH>
@@ -1072,7 +1084,9 @@ void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const Cha
   }
   int G = maxmem * (sh.Hq / sh.Hkv) * sh.T_new;
   dim3 grid(a.nsplit, sh.Hkv * sh.B * sh.k);
-  if (sh.d == 64)
+  if (sh.d == 96) {
+    if constexpr (sizeof(T) == 2) decode_dispatch<T, 96>(a, G, grid, s);
+  } else if (sh.d == 64)
     decode_dispatch<T, 64>(a, G, grid, s);
   else
     decode_dispatch<T, 32>(a, G, grid, s);

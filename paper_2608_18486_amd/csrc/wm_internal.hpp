@@ -10,7 +10,7 @@ namespace wm {
 
 typedef __bf16 bf16;
 constexpr int kMaxLayers = 64;  // L limit (kernel-argument tables are sized by it)
-constexpr int kMaxHeadDim = 64;  // head dims 32 and 64 are supported
+constexpr int kMaxHeadDim = 96;  // head dims 32 and 64 (fp32, bf16) and 96 (bf16)
 
 struct Shape {
   int B, T_new, L, k, D, Hq, Hkv, d, p, Lp, S_cap;

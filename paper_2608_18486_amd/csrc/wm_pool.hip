@@ -275,13 +275,15 @@ __device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, in
 }
 
 // Workspace elements (of T) after the folded weights that lanes without a row write
-// to: the bf16 stores reach 64 elements past the pointer, the fp32 ones DH.
+// to: the staged bf16 stores reach 64 elements past the pointer, the others DH.
 constexpr size_t kTrashElems = 512;
 
 struct NoState {};
 
 template <typename T, int DH> struct KVEpi {
-  static constexpr bool kUsesLds = sizeof(T) == 2;  // stages the cache writes
+  // bf16 stages the cache writes when a head row is a power-of-two count of 16-B chunks
+  // (head dims 32 and 64); head dim 96 stores directly
+  static constexpr bool kUsesLds = sizeof(T) == 2 && ((DH / 8) & (DH / 8 - 1)) == 0;
   T *Kc, *Vc;
   T* trash;  // kTrashElems elements of workspace
   const float* rs;  // [2k][M] 1 / RMS of each mixed channel row (the mid RMSNorm)
@@ -300,7 +302,7 @@ template <typename T, int DH> struct KVEpi {
     const int br = g / k, j = g - br * k;
     const bool key = br == 0;
     T* base = key ? Kc : Vc;
-    head_epilogue<T, DH, C::WO, C::WN, true>(
+    head_epilogue<T, DH, C::WO, C::WN, kUsesLds>(
         acc, ow0, nw0, lane, M, key, g_knorm + (long)j * DH, tab, eps,
         [&](int n) { return rs[(long)g * M + n]; },
         [&](int n) { return ctx_len ? ctx_len[n / T_new] : 0; },
@@ -475,6 +477,12 @@ template <> struct ProjShape<bf16, false> { using C = ProjCfg<bf16, WM_PROJ_BF16
 template <> struct ProjShape<bf16, true> { using C = ProjCfg<bf16, 32, 2, 2, 2, 1>; };
 template <> struct ProjShape<float, false> { using C = ProjCfg<float, 32, 2, 2, 2, 2>; };
 template <> struct ProjShape<float, true> { using C = ProjCfg<float, 32, 2, 2, 2, 1>; };
+// Head dim 96 (bf16): a wave holds one head (96 channels); 288 channels x 128 tokens per
+// block of 6 waves (64 tokens for few tokens), i.e. one K/V projection of 3 KV heads.
+template <typename T, bool FEW, int DH> struct ProjShapeD { using C = typename ProjShape<T, FEW>::C; };
+template <bool FEW> struct ProjShapeD<bf16, FEW, 96> {
+  using C = ProjCfg<bf16, 32, 3, 2, 3, FEW ? 1 : 2>;
+};
 // Router: 288 channels x 128 tokens per bf16 block on 6 waves, 96 x 64 per wave (the
 // channel count 2kL is small: 288 for L = k = 12, so a block covers all of it and the
 // stacked states are read once; measured 10% faster than 96-channel blocks at L = 24).
@@ -1034,7 +1042,7 @@ template <typename T, int DH, bool FEW>
 static void kv_gemm(const Shape& sh, const T* mixed, const float* rinv_mid, const T* wfold,
                     const T* g_knorm, const float* rope_tab, const int32_t* ctx_len, T* Kc, T* Vc,
                     hipStream_t s) {
-  using C = typename ProjShape<T, FEW>::C;
+  using C = typename ProjShapeD<T, FEW, DH>::C;
   const int M = sh.N(), Nout = sh.Hkv * DH, K = sh.D;
   PlainRows<T> x{mixed, (long)M * K, K, M};
   PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
@@ -1052,7 +1060,12 @@ void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, c
   if (M <= 0) return;
   fold_gain<T>(Wk, Wv, sh.k, g_mid, wfold, 2 * sh.k, sh.Hkv * sh.d, sh.D, s);
   const bool few = M <= kFewTokens;
-  if (sh.d == 64) {
+  if (sh.d == 96) {
+    if constexpr (sizeof(T) == 2) {  // fp32 at d = 96 is rejected by validation
+      if (few) kv_gemm<T, 96, true>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
+      else kv_gemm<T, 96, false>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
+    }
+  } else if (sh.d == 64) {
     if (few) kv_gemm<T, 64, true>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
     else kv_gemm<T, 64, false>(sh, mixed, rinv_mid, wfold, g_knorm, rope_tab, ctx_len, Kc, Vc, s);
   } else {
@@ -1064,7 +1077,7 @@ void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, c
 template <typename T, int DH, bool FEW>
 static void q_gemm(const Shape& sh, const T* H, const float* rinv, const T* wfold,
                    const T* g_qnorm, const float* rope_tab, T* Q, hipStream_t s) {
-  using C = typename ProjShape<T, FEW>::C;
+  using C = typename ProjShapeD<T, FEW, DH>::C;
   const int M = sh.N(), Nout = sh.Hq * DH, K = sh.D;
   PlainRows<T> x{H, K, (long)sh.L * K, M};
   PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
@@ -1081,7 +1094,12 @@ void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g
   if (M <= 0) return;
   fold_gain<T>(Wq, Wq, sh.L, g_in, wfold, sh.L, sh.Hq * sh.d, sh.D, s);
   const bool few = M <= kFewTokens;
-  if (sh.d == 64) {
+  if (sh.d == 96) {
+    if constexpr (sizeof(T) == 2) {
+      if (few) q_gemm<T, 96, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
+      else q_gemm<T, 96, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
+    }
+  } else if (sh.d == 64) {
     if (few) q_gemm<T, 64, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
     else q_gemm<T, 64, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
   } else {

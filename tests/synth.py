@@ -75,6 +75,15 @@ WORKLOADS = {
     "c5_decode_S32768": Workload("c5_decode_S32768", 64, 1, 24, 12, 1024, 16, 16, 64, 32768,
                                  "bf16", _map_mod(24, 12), seed=1005),
 }
+# The paper's own model shape (Section 5.1): L = 16, D = 512, 6 query and 3 KV heads of
+# dimension 96, routers reading every second source layer (p = 2), sequences packed to
+# 2048 tokens, 16 sequences (a global batch of 128 over 8 GPUs), fixed selection
+# l -> l mod k, for the channel counts of the compression study (Section 5.4).
+for _k in (1, 2, 4, 8, 12, 16):
+    WORKLOADS["paper_T2048_L16_k%d" % _k] = Workload(
+        "paper_T2048_L16_k%d" % _k, 16, 2048, 16, _k, 512, 6, 3, 96, 0, "bf16",
+        _map_mod(16, _k), p=2, seed=1100 + _k)
+del _k
 
 
 def small(name="small", B=2, T_new=40, L=5, k=3, D=96, Hq=4, Hkv=2, d=32, ctx=0,

@@ -47,7 +47,8 @@ def _dims(wm, **kw):
     (dict(L=0), "ERR_SHAPE"), (dict(L=65, k=2), "ERR_SHAPE"), (dict(k=5), "ERR_SHAPE"),
     (dict(k=0), "ERR_SHAPE"), (dict(D=48), "ERR_SHAPE"), (dict(D=0), "ERR_SHAPE"),
     (dict(Hq=3), "ERR_SHAPE"), (dict(Hkv=0), "ERR_SHAPE"), (dict(d=48), "ERR_SHAPE"),
-    (dict(d=128), "ERR_SHAPE"), (dict(p=0), "ERR_SHAPE"), (dict(p=5), "ERR_SHAPE"),
+    (dict(d=128), "ERR_SHAPE"), (dict(d=96, dtype=0), "ERR_SHAPE"), (dict(d=80), "ERR_SHAPE"),
+    (dict(p=0), "ERR_SHAPE"), (dict(p=5), "ERR_SHAPE"),
     (dict(dtype=7), "ERR_DTYPE"), (dict(mix_mode=2), "ERR_DTYPE"), (dict(mask_mode=-1), "ERR_DTYPE"),
     (dict(B=-1), "ERR_ARG"), (dict(T_new=-3), "ERR_ARG"), (dict(eps=0.0), "ERR_ARG"),
     (dict(rope_theta=-1.0), "ERR_ARG"), (dict(ctx_max=-1), "ERR_ARG"),
@@ -59,6 +60,14 @@ def test_validation_error_codes(wm, kw, code):
     chan_map = [l % 2 for l in range(max(d.L, 1))]
     assert wm.validate(d, wm.OP_LAYER_STEP, chan_map) == getattr(wm, code)
     assert wm.workspace_size(_dims(wm, **kw), wm.OP_LAYER_STEP) == 0
+
+
+@pytest.mark.parametrize("d,dtype", [(32, 0), (32, 1), (64, 0), (64, 1), (96, 1)])
+def test_supported_head_dims(wm, d, dtype):
+    """Head dims 32 and 64 in either dtype, 96 (the paper's model) in bf16."""
+    dims = _dims(wm, d=d, dtype=dtype)
+    assert wm.validate(dims, wm.OP_LAYER_STEP, [l % 2 for l in range(4)]) == wm.OK
+    assert wm.workspace_size(dims, wm.OP_LAYER_STEP) > 0
 
 
 def test_capacity_only_matters_for_cache_ops(wm):

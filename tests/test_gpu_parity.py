@@ -100,6 +100,11 @@ SMALL = {
                               dtype="f32"),
     "bf16_long_T300": synth.small("bf16_long_T300", B=1, T_new=300, L=2, k=2, D=64, Hq=2, Hkv=1,
                                   d=64),
+    # head dim 96 with grouped queries and router subsampling (the paper's head layout)
+    "bf16_d96_gqa_p2": synth.small("bf16_d96_gqa_p2", B=2, T_new=150, L=6, k=4, D=192, Hq=6,
+                                   Hkv=3, d=96, p=2),
+    "bf16_paper_shape": synth.small("bf16_paper_shape", B=1, T_new=70, L=16, k=8, D=512, Hq=6,
+                                    Hkv=3, d=96, p=2),
 }
 
 
@@ -160,6 +165,16 @@ def test_layer_step_with_context(wm, T_new, mask_mode):
         _layer_step_case(wm, w, mask_mode=mask_mode, ragged=True)
 
 
+@pytest.mark.parametrize("T_new", [1, 3, 33])
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_layer_step_with_context_d96(wm, T_new, mask_mode):
+    """Head dim 96: decode (12 of 16 lanes per slot group) and chunked prefill over a
+    ragged cached context."""
+    w = synth.small("ctx_d96_T%d" % T_new, B=3, T_new=T_new, L=6, k=3, D=192, Hq=6, Hkv=3,
+                    d=96, ctx=700, p=2)
+    _layer_step_case(wm, w, mask_mode=mask_mode, ragged=True)
+
+
 def test_layer_step_is_deterministic(wm):
     w = SMALL["bf16_ragged_gqa"]
     a = _layer_step_case(wm, w)
@@ -210,7 +225,8 @@ def test_router_zero_weights_give_bias_exactly(wm):
         assert torch.equal(alpha.cpu(), want)
 
 
-@pytest.mark.parametrize("name", ["c1_tiny_f32", "bf16_ragged_gqa", "f32_d64_kL"])
+@pytest.mark.parametrize("name", ["c1_tiny_f32", "bf16_ragged_gqa", "f32_d64_kL",
+                                  "bf16_d96_gqa_p2"])
 def test_kv_project(wm, name):
     w = SMALL[name]
     w = synth.Workload(w.name, w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, 50, w.dtype,
@@ -228,7 +244,8 @@ def test_kv_project(wm, name):
     _check_cache(Vg, Vo, V0, w, ctx.numpy(), w.dtype, name + " V")
 
 
-@pytest.mark.parametrize("name", ["c1_tiny_f32", "bf16_ragged_gqa", "bf16_d64_k1"])
+@pytest.mark.parametrize("name", ["c1_tiny_f32", "bf16_ragged_gqa", "bf16_d64_k1",
+                                  "bf16_d96_gqa_p2"])
 def test_q_project(wm, name):
     w = SMALL[name]
     P = synth.make_params(w, _bias(w), gains="random")
@@ -246,7 +263,7 @@ def test_q_project(wm, name):
 def test_channel_attend(wm, T_new, ctx, mask_mode):
     """Attention alone on seeded queries and a seeded cache, with a channel map where
     several consumers share a channel (and one channel has none)."""
-    for dtype, d in (("bf16", 64), ("f32", 32)):
+    for dtype, d in (("bf16", 64), ("f32", 32), ("bf16", 96)):
         w = synth.small("attn_%s" % dtype, B=2, T_new=T_new, L=5, k=3, D=64, Hq=4, Hkv=2, d=d,
                         ctx=ctx + T_new, dtype=dtype, chan_map=[2, 0, 2, 2, 0])
         P = synth.make_params(w, _bias(w))
@@ -260,12 +277,13 @@ def test_channel_attend(wm, T_new, ctx, mask_mode):
         wm.channel_attend(dims, _dev(P), Q.cuda(), w.chan_map, ctx_len.cuda(), Kc.cuda(),
                           Vc.cuda(), O)
         torch.cuda.synchronize()
-        check_close(O, Oo, dtype, "attend %s T%d ctx%d" % (dtype, T_new, ctx))
+        check_close(O, Oo, dtype, "attend %s d%d T%d ctx%d" % (dtype, d, T_new, ctx))
 
 
 # ------------------------------------------------------------ full workloads
 
-FULL = ["c2_T2048_L12_k12", "c3_T2048_L12_k6", "c4_T4096_L24_k12"]
+FULL = ["c2_T2048_L12_k12", "c3_T2048_L12_k6", "c4_T4096_L24_k12", "paper_T2048_L16_k8",
+        "paper_T2048_L16_k16"]
 
 
 def _sample_rows(w, b):
