@@ -345,7 +345,7 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
     gemm = "proj_gemm_dma_kernel" if w.dtype == "bf16" else "proj_gemm_kernel"
     mix = "mix_mfma_kernel" if (w.dtype == "bf16" and w.L <= 32 and w.k <= 32) else "mix_kernel"
-    prefill = "attend_prefill_dma_kernel" if (w.dtype == "bf16" and w.d == 64) else \
+    prefill = "attend_prefill_dma_kernel" if (w.dtype == "bf16" and w.d in (64, 96)) else \
         "attend_prefill_kernel"
     roof["kernel"] = {"attend": prefill if w.T_new > 4 else
                       "attend_decode_kernel + attend_combine_kernel",

@@ -377,51 +377,68 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   }
 }
 
-// ---------------------------------------------- prefill, bf16, head dim 64
+// ---------------------------------------------- prefill, bf16, head dims 64 and 96
 // K/V blocks of 64 slots are copied from HBM straight into LDS (no trip through
-// registers), one barrier per block. A slot row is 128 B; its 16-B chunk c sits at
-// chunk c ^ kv_swz(row) of the LDS row. That makes both readers free of bank
-// conflicts: the K fragment reads (16 rows, one chunk) and the transposing V reads
-// (4 rows x 4 chunks per 32 lanes).
+// registers), one barrier per block. A slot row is 2 DH bytes (8 or 12 chunks of 16 B);
+// its chunk c sits at chunk c ^ pf_swz(row) of the LDS row. That makes both readers
+// free of bank conflicts: the K fragment reads (16 rows, one chunk) and the transposing
+// V reads (4 rows x 4 chunks per 32 lanes).
 //
 // Each wave owns QT tiles of 32 queries and walks its keys in 32-slot steps. Step i
 // issues the MFMAs of S(i+1) = K Q^T and of O^T += V^T P(i-1)^T, and meanwhile computes
 // the softmax weights P(i) of S(i) on the vector ALUs, so the matrix cores and the ALUs
 // work on independent data. Every K or V fragment read from LDS feeds QT MFMAs.
-// Workgroup shape: 4 waves of one 32-query tile each and rings of 3 blocks, i.e. 48 KB
-// of LDS and at most 168 registers per lane, so a CU holds three workgroups (3 waves per
-// SIMD, each from a different workgroup, so no two waves of a SIMD wait at the same
-// barrier). Measured on MI355X and slower: 8-wave workgroups (4 waves per SIMD, in
-// lock-step pairs; 128 registers), and 2 query tiles per wave (2 waves per SIMD).
+// Workgroup shape: 4 waves of one 32-query tile each and rings of 3 blocks. Head dim
+// 64: 48 KB of LDS and at most 168 registers per lane, so a CU holds three workgroups
+// (3 waves per SIMD, each from a different workgroup, so no two waves of a SIMD wait at
+// the same barrier). Measured on MI355X and slower: 8-wave workgroups (4 waves per
+// SIMD, in lock-step pairs; 128 registers), and 2 query tiles per wave (2 waves per
+// SIMD). Head dim 96: 72 KB and two workgroups per CU; a step has 12 MFMAs (6 for the
+// scores, 6 for the output) against the same 16 exponentials per lane.
 constexpr int kPfWaves = 4, kPfNs = 3, kPfQt = 1;
-template <int QT> struct PfDma {
+template <int QT, int DH_> struct PfDma {
   static constexpr int NW = kPfWaves, NT = 64 * NW;
   static constexpr int BQ = 32 * QT * NW;              // queries per workgroup
-  static constexpr int BKV = 64, DH = 64;
+  static constexpr int BKV = 64, DH = DH_;
+  static constexpr int NKS = DH / 16;                  // k16 steps of S (= step groups)
+  static constexpr int NDT = DH / 32;                  // 32-column tiles of O^T
   static constexpr int ROW_BYTES = DH * 2;             // one slot row of K or V
-  static constexpr int BLK_BYTES = BKV * ROW_BYTES;    // one K (or V) block: 8 KB
+  static constexpr int CPR = ROW_BYTES / 16;           // 16-B chunks per row
+  static constexpr int BLK_BYTES = BKV * ROW_BYTES;    // one K (or V) block
   static constexpr int RPW = BKV / NW;                 // block rows each wave copies
-  static constexpr int NI = RPW / 8;                   // ... in copy instructions of 8 rows
+  static constexpr int NI = RPW * ROW_BYTES / 1024;    // ... in copy instructions of 1 KB
   // Two rings of NS blocks. While block j is processed, K of j and j+1 and V of j-1 and
   // j are read; K of j+2 and V of j+1 (and, with 4 blocks, K of j+3 and V of j+2) are
   // in flight.
   static constexpr int NS = kPfNs;
   static constexpr int V_BASE = NS * BLK_BYTES;        // K ring first, then the V ring
   static constexpr int SMEM_BYTES = 2 * NS * BLK_BYTES;
-  static_assert(RPW % 8 == 0 && (NS == 3 || NS == 4), "tile shapes");
+  static constexpr int WPE = DH == 64 ? 3 : 2;         // waves per SIMD
+  static_assert((DH == 64 || DH == 96) && NI * 1024 == RPW * ROW_BYTES && (NS == 3 || NS == 4),
+                "tile shapes");
+  static_assert(SMEM_BYTES % (16 * NT) == 0, "the rings are zeroed in whole passes");
 };
-constexpr int kPfRowBytes = 128, kPfBlkBytes = 64 * kPfRowBytes, kPfVBase = kPfNs * kPfBlkBytes;
 
-// Bit-reversal of (row / 2) mod 8: rows 2x and 2x+1 share a 256-B bank line, and rows
-// 4y, 4y+2 differ in bit 2, which keeps a transposing read's 4 chunks apart.
-__device__ __forceinline__ int kv_swz(int row) {
-  const int x = (row >> 1) & 7;
-  return ((x & 1) << 2) | (x & 2) | (x >> 2);
+// Chunk swizzle of slot row `row`.
+// Head dim 64 (128-B rows): bit-reversal of (row / 2) mod 8. Rows 2x and 2x+1 share a
+// 256-B bank line, and rows 4y, 4y+2 differ in bit 2, which keeps a transposing read's
+// 4 chunks apart.
+// Head dim 96 (192-B rows): (row / 4) mod 4, applied within aligned groups of 4 chunks.
+// Row 4a + b starts at 16-B bank group 12 b mod 16 (one of 0, 4, 8, 12 per b), and the
+// swizzle adds a distinct 0..3 per a, so 16 consecutive rows' chunk c, and 4 rows x one
+// aligned 4-chunk group, fall in 16 distinct bank groups.
+template <int DH> __device__ __forceinline__ int pf_swz(int row) {
+  if constexpr (DH == 64) {
+    const int x = (row >> 1) & 7;
+    return ((x & 1) << 2) | (x & 2) | (x >> 2);
+  } else {
+    return (row >> 2) & 3;
+  }
 }
 
-template <int QT> struct PfState {  // one wave's running softmax state (2 lanes per row)
-  f32x16 o[2][QT];   // O^T per value-column half and query tile
-  bf16x8 pf[2][QT];  // P(i-1)^T fragments (keys 0-15, 16-31 of the step)
+template <int QT, int DH> struct PfState {  // one wave's running softmax state (2 lanes per row)
+  f32x16 o[DH / 32][QT];  // O^T per 32-column tile of the values and query tile
+  bf16x8 pf[2][QT];       // P(i-1)^T fragments (keys 0-15, 16-31 of the step)
   float m[QT], lsum[QT];
 };
 
@@ -430,37 +447,45 @@ template <int QT> struct PfState {  // one wave's running softmax state (2 lanes
 // V^T fragment of value tile dt (the second 16 rows of the half add 16 rows). They do
 // not depend on the ring stage, so the stage and half fold into the instructions'
 // offset fields.
-struct PfLane {
-  uint32_t k[4], v[2][2];
+template <int DH> struct PfLane {
+  uint32_t k[DH / 16], v[DH / 32][2];
 };
-__device__ __forceinline__ PfLane pf_lane(int lane) {
+template <int DH> __device__ __forceinline__ PfLane<DH> pf_lane(int lane) {
+  constexpr int ROW = 2 * DH;
   const int h = lane >> 5, r = lane & 31, j = lane & 15, grp = lane >> 4;
-  PfLane o;
-  const int sw = kv_swz(r);
+  PfLane<DH> o;
+  const int sw = pf_swz<DH>(r);
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) o.k[ks] = r * kPfRowBytes + 16 * ((2 * ks + h) ^ sw);
+  for (int ks = 0; ks < DH / 16; ++ks) o.k[ks] = r * ROW + 16 * ((2 * ks + h) ^ sw);
 #pragma unroll
-  for (int dt = 0; dt < 2; ++dt)
+  for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int row = 4 * h + (j >> 2) + 8 * s;
       const int chunk = 4 * dt + 2 * (grp & 1) + ((j & 3) >> 1);
-      o.v[dt][s] = row * kPfRowBytes + 16 * (chunk ^ kv_swz(row)) + 8 * (j & 1);
+      o.v[dt][s] = row * ROW + 16 * (chunk ^ pf_swz<DH>(row)) + 8 * (j & 1);
     }
   return o;
 }
 // byte offsets of the K and V ring half blocks: ring stage u, half hf
-constexpr uint32_t pf_kh(int u, int hf) { return u * kPfBlkBytes + hf * 32 * kPfRowBytes; }
-constexpr uint32_t pf_vh(int u, int hf) { return kPfVBase + u * kPfBlkBytes + hf * 32 * kPfRowBytes; }
+template <int DH> constexpr uint32_t pf_kh(int u, int hf) {
+  return u * 64 * 2 * DH + hf * 32 * 2 * DH;
+}
+template <int DH> constexpr uint32_t pf_vh(int u, int hf) {
+  return kPfNs * 64 * 2 * DH + u * 64 * 2 * DH + hf * 32 * 2 * DH;
+}
 
-__device__ __forceinline__ bf16x8 pf_ldk(const char* sm, const PfLane& lo, uint32_t kh, int ks) {
+template <int DH>
+__device__ __forceinline__ bf16x8 pf_ldk(const char* sm, const PfLane<DH>& lo, uint32_t kh,
+                                         int ks) {
   return *(const bf16x8*)(sm + lo.k[ks] + kh);
 }
 // V^T fragment (value column 32 dt + r, keys 16 hf + 4h + {0..3, 8..11} of the half)
-__device__ __forceinline__ bf16x8 pf_ldv(const char* sm, const PfLane& lo, uint32_t vh, int hf,
-                                         int dt) {
+template <int DH>
+__device__ __forceinline__ bf16x8 pf_ldv(const char* sm, const PfLane<DH>& lo, uint32_t vh,
+                                         int hf, int dt) {
   typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-  const uint32_t base = vh + hf * 16 * kPfRowBytes;
+  const uint32_t base = vh + hf * 16 * 2 * DH;
   const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sm + lo.v[dt][0] + base));
   const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sm + lo.v[dt][1] + base));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -468,28 +493,21 @@ __device__ __forceinline__ bf16x8 pf_ldv(const char* sm, const PfLane& lo, uint3
 
 // S^T fragment rows of one step for one query tile: the 32 K slots of the half block
 // at kh against the lane's query column, accumulated on top of acc.
-__device__ __forceinline__ f32x16 pf_scores(const char* sm, const PfLane& lo, uint32_t kh,
-                                            const bf16x8 (&qf)[4], f32x16 acc) {
-  bf16x8 kf[4];
+template <int DH>
+__device__ __forceinline__ f32x16 pf_scores(const char* sm, const PfLane<DH>& lo, uint32_t kh,
+                                            const bf16x8 (&qf)[DH / 16], f32x16 acc) {
+  bf16x8 kf[DH / 16];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) kf[ks] = pf_ldk(sm, lo, kh, ks);
+  for (int ks = 0; ks < DH / 16; ++ks) kf[ks] = pf_ldk<DH>(sm, lo, kh, ks);
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) acc = mma32(acc, kf[ks], qf[ks]);
+  for (int ks = 0; ks < DH / 16; ++ks) acc = mma32(acc, kf[ks], qf[ks]);
   return acc;
 }
 
-// Slots of step i that this lane's row must not see get the score -1e30 (weight 0):
-// slot 32 i + 8(q/4) + 4h + q%4 is visible iff it is below lim0 (row position + incl).
-__device__ __forceinline__ void pf_mask(f32x16& v, int i, int lim0, int lane) {
-  const int lim = lim0 - (32 * i + 4 * (lane >> 5));
-#pragma unroll
-  for (int q = 0; q < 16; ++q)
-    if (8 * (q >> 2) + (q & 3) >= lim) v[q] = kNegBig;
-}
-
 // Accumulator start for the scores of step i: -m (the row reference), or -1e30 for the
-// slots a masked step hides from this lane's row. -1e30 plus any score stays about
-// -1e30, so the MFMAs that follow need no masking afterwards.
+// slots a masked step hides from this lane's row (slot 32 i + 8(q/4) + 4h + q%4 is
+// visible iff it is below lim0, the row position + incl). -1e30 plus any score stays
+// about -1e30, so the MFMAs that follow need no masking afterwards.
 __device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int i, int lim0,
                                         int lane) {
   if (masked) {
@@ -502,6 +520,27 @@ __device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int 
   }
 }
 
+// f(integral_constant<int, I>) for I = I0 .. N-1, in order.
+template <int I0, int N, class F> __device__ __forceinline__ void static_for(F& f) {
+  if constexpr (I0 < N) {
+    f(std::integral_constant<int, I0>());
+    static_for<I0 + 1, N>(f);
+  }
+}
+
+// Sum of v[Q0 .. Q1) as a balanced tree.
+template <int Q0, int Q1> __device__ __forceinline__ float tree_sum(const f32x16& v) {
+  if constexpr (Q1 - Q0 == 1) return v[Q0];
+  else {
+    constexpr int QM = Q0 + (Q1 - Q0) / 2;
+    return tree_sum<Q0, QM>(v) + tree_sum<QM, Q1>(v);
+  }
+}
+template <int N, int I0 = 0> __device__ __forceinline__ float tree_sum_arr(const float* p) {
+  if constexpr (N == 1) return p[I0];
+  else return tree_sum_arr<N / 2, I0>(p) + tree_sum_arr<N - N / 2, I0 + N / 2>(p);
+}
+
 // One step (see above), the same straight-line code for every step: the MFMAs of
 // PV(i-1) and S(i+1) and the exponentials of S(i) sit in one basic block, so they
 // interleave. sc holds S(i) in log2 units minus the row reference m, masked; sn
@@ -509,50 +548,54 @@ __device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int 
 // register sets alternate between consecutive steps, and sc is refilled with the start
 // value of S(i+2), so no step waits on the MFMAs it has just issued. lim0 is the first
 // tile's row limit; tile t's rows sit 32 t further.
-template <int QT>
-__device__ __forceinline__ void pf_step(const char* sm, const PfLane& lo, uint32_t kh_cur,
+template <int QT, int DH>
+__device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, uint32_t kh_cur,
                                         uint32_t kh_nxt, uint32_t vh_prv, int i,
-                                        const bf16x8 (&qf)[QT][4], PfState<QT>& st,
+                                        const bf16x8 (&qf)[QT][DH / 16], PfState<QT, DH>& st,
                                         f32x16 (&sc)[QT], f32x16 (&sn)[QT], int lane, int lim0,
                                         bool mask_cur, bool mask_n2) {
-  // Four groups k, each: the MFMAs of PV(i-1) for keys 16(k/2).. and value tile k%2 and
-  // of S(i+1) for k16 step k, plus the weights of 4 rows of S(i). The fragments of V^T
-  // (step i-1; before the first step a zeroed stage) and K (step i+1) are read one group
-  // ahead, and groups are not reordered, so at most two groups' fragments are live.
+  // NG groups g, each: the MFMAs of PV(i-1) for keys 16(g / NDT).. and value tile
+  // g % NDT and of S(i+1) for k16 step g, plus the weights of rows [q0(g), q0(g+1)) of
+  // S(i). The fragments of V^T (step i-1; before the first step a zeroed stage) and K
+  // (step i+1) are read one group ahead, and groups are not reordered, so at most two
+  // groups' fragments are live.
+  constexpr int NG = DH / 16, NDT = DH / 32;
   bf16x8 vf[2], kf[2];
-  vf[0] = pf_ldv(sm, lo, vh_prv, 0, 0);
-  kf[0] = pf_ldk(sm, lo, kh_nxt, 0);
+  vf[0] = pf_ldv<DH>(sm, lo, vh_prv, 0, 0);
+  kf[0] = pf_ldk<DH>(sm, lo, kh_nxt, 0);
   // weights against the current reference, in place (S(i) is not needed again unless
   // the rescale below runs, which recomputes it from the K block still in LDS)
-  float ps4[QT][4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (k < 3) {
-      vf[(k + 1) & 1] = pf_ldv(sm, lo, vh_prv, (k + 1) >> 1, (k + 1) & 1);
-      kf[(k + 1) & 1] = pf_ldk(sm, lo, kh_nxt, k + 1);
+  float psg[QT][NG];
+  auto group = [&](auto gc) {
+    constexpr int g = decltype(gc)::value;
+    constexpr int q0 = (16 * g + NG - 1) / NG, q1 = (16 * (g + 1) + NG - 1) / NG;
+    if constexpr (g + 1 < NG) {
+      vf[(g + 1) & 1] = pf_ldv<DH>(sm, lo, vh_prv, (g + 1) / NDT, (g + 1) % NDT);
+      kf[(g + 1) & 1] = pf_ldk<DH>(sm, lo, kh_nxt, g + 1);
     }
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
-      st.o[k & 1][t] = mma32(st.o[k & 1][t], vf[k & 1], st.pf[k >> 1][t]);
-      sn[t] = mma32(sn[t], kf[k & 1], qf[t][k]);
+      st.o[g % NDT][t] = mma32(st.o[g % NDT][t], vf[g & 1], st.pf[g / NDT][t]);
+      sn[t] = mma32(sn[t], kf[g & 1], qf[t][g]);
     }
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
 #pragma unroll
-      for (int q = 4 * k; q < 4 * k + 4; ++q) sc[t][q] = fast_exp2(sc[t][q]);
-      ps4[t][k] = (sc[t][4 * k] + sc[t][4 * k + 1]) + (sc[t][4 * k + 2] + sc[t][4 * k + 3]);
+      for (int q = q0; q < q1; ++q) sc[t][q] = fast_exp2(sc[t][q]);
+      psg[t][g] = tree_sum<q0, q1>(sc[t]);
     }
     __builtin_amdgcn_sched_barrier(0);
-  }
+  };
+  static_for<0, NG>(group);
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    float ps = (ps4[t][0] + ps4[t][1]) + (ps4[t][2] + ps4[t][3]);
+    float ps = tree_sum_arr<NG>(psg[t]);
     if (__any(!(ps <= kGrowSum) || st.m[t] == kNoRef)) {
       // rare: move the reference up to the exact row max (never down) and rescale the
       // state; S(i+1) was started from the old reference, so it moves too
       f32x16 sr;
       pf_init(sr, -st.m[t], mask_cur, i, lim0 + 32 * t, lane);
-      sr = pf_scores(sm, lo, kh_cur, qf[t], sr);
+      sr = pf_scores<DH>(sm, lo, kh_cur, qf[t], sr);
       float mx = sr[0];
 #pragma unroll
       for (int q = 1; q < 16; ++q) mx = fmaxf(mx, sr[q]);
@@ -560,8 +603,8 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane& lo, uint32
       const float alpha = fast_exp2(-mx);
       st.m[t] += mx;
       st.lsum[t] *= alpha;
-      st.o[0][t] *= alpha;
-      st.o[1][t] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) st.o[dt][t] *= alpha;
       ps = 0.f;
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
@@ -577,10 +620,12 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane& lo, uint32
   }
 }
 
-template <int QT>
-__global__ __launch_bounds__(PfDma<QT>::NT) __attribute__((amdgpu_waves_per_eu(3)))
+template <int QT, int DH>
+__global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(DH == 64 ? 3 : 2)))
 void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
-  using P = PfDma<QT>;
+  using P = PfDma<QT, DH>;
+  static_assert(P::NT == 64 * kPfWaves && P::WPE == (DH == 64 ? 3 : 2), "launch bounds");
+  constexpr int NKS = P::NKS, NDT = P::NDT;
   __shared__ __align__(16) char smem[P::SMEM_BYTES];
 
   // 1-D grid over (consumer, sequence, head, query tile), as in attend_prefill_kernel
@@ -608,49 +653,49 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
       *(i32x4*)(smem + 16 * (tid + P::NT * k)) = z;
   }
 
-  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * P::DH;
-  bf16x8 qf[QT][4];
-  const bf16* Qb = a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * P::DH;
+  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
+  bf16x8 qf[QT][NKS];
+  const bf16* Qb = a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * DH;
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     const int qi = qw0 + 32 * t + r;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-      qf[t][ks] = qi < a.T_new ? *(const bf16x8*)(Qb + (long)qi * P::DH + 16 * ks + 8 * h)
+    for (int ks = 0; ks < NKS; ++ks)
+      qf[t][ks] = qi < a.T_new ? *(const bf16x8*)(Qb + (long)qi * DH + 16 * ks + 8 * h)
                                : zero_frag<bf16>();
     // queries in log2 units: the MFMAs then give s' = q.k log2(e) / sqrt(d)
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
+    for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
       for (int i = 0; i < 8; ++i) qf[t][ks][i] = (bf16)((float)qf[t][ks][i] * cl2);
   }
 
-  PfState<QT> st;
+  PfState<QT, DH> st;
   f32x16 sa[QT], sb[QT];  // score registers of even and odd steps
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     st.pf[0][t] = zero_frag<bf16>();
     st.pf[1][t] = zero_frag<bf16>();
     if (a.mask_paper) {
-      const bf16* kd = a.Kd + ((long)c * a.Hkv + kvh) * P::DH;
-      const bf16* vd = a.Vd + ((long)c * a.Hkv + kvh) * P::DH;
+      const bf16* kd = a.Kd + ((long)c * a.Hkv + kvh) * DH;
+      const bf16* vd = a.Vd + ((long)c * a.Hkv + kvh) * DH;
       float part = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+      for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
         for (int i = 0; i < 8; ++i) part += (float)qf[t][ks][i] * (float)kd[16 * ks + 8 * h + i];
       st.m[t] = halves_sum(part);
       st.lsum[t] = h == 0 ? 1.f : 0.f;
 #pragma unroll
-      for (int dt = 0; dt < 2; ++dt)
+      for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int q = 0; q < 16; ++q)
           st.o[dt][t][q] = (float)vd[32 * dt + 8 * (q >> 2) + 4 * h + (q & 3)];
     } else {
       st.m[t] = kNoRef;
       st.lsum[t] = 0.f;
-      st.o[0][t] = zero16();
-      st.o[1][t] = zero16();
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) st.o[dt][t] = zero16();
     }
   }
 
@@ -663,13 +708,20 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   const int ilast = (wkend + 31) / 32 - 1;  // the wave's last 32-slot step (-1: none)
   const int lim0 = ctx + qw0 + r + incl;
 
-  // copies: wave w moves slot rows RPW w .. RPW w + RPW-1 of each K and V block
+  // copies: wave w moves slot rows RPW w .. RPW w + RPW-1 of each K and V block, 1 KB
+  // (64 chunks of 16 B) per instruction; lane x of instruction n fills LDS chunk
+  // 64 n + x of the wave's rows, i.e. row (64 n + x) / CPR, chunk (64 n + x) % CPR, with
+  // the chunk of the slot row that the swizzle puts there
   const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)a.S_cap * P::ROW_BYTES);
   const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)a.S_cap * P::ROW_BYTES);
+  int crow[P::NI];
   uint32_t dchunk[P::NI];
 #pragma unroll
-  for (int n = 0; n < P::NI; ++n)
-    dchunk[n] = 16u * (uint32_t)((lane & 7) ^ kv_swz(P::RPW * w + 8 * n + (lane >> 3)));
+  for (int n = 0; n < P::NI; ++n) {
+    const int ch = 64 * n + lane;
+    crow[n] = P::RPW * w + ch / P::CPR;
+    dchunk[n] = 16u * (uint32_t)((ch % P::CPR) ^ pf_swz<DH>(crow[n]));
+  }
   const uint32_t smem_base = (uint32_t)(uintptr_t)smem;
   // NI copy instructions per wave move its rows of a K or V block; blocks past the
   // visible range are copied too (as zeros), so every wave issues the same sequence
@@ -678,11 +730,11 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   auto issue = [&](int blk, bool v) {
 #pragma unroll
     for (int n = 0; n < P::NI; ++n) {
-      const int row0 = P::RPW * w + 8 * n;
-      const int s = blk * P::BKV + row0 + (lane >> 3);
+      const int s = blk * P::BKV + crow[n];
       const uint32_t off = s < kend ? (uint32_t)s * P::ROW_BYTES + dchunk[n] : kOffOob;
       const uint32_t lds = __builtin_amdgcn_readfirstlane(
-          smem_base + (v ? P::V_BASE : 0) + (blk % P::NS) * P::BLK_BYTES + row0 * P::ROW_BYTES);
+          smem_base + (v ? P::V_BASE : 0) + (blk % P::NS) * P::BLK_BYTES +
+          P::RPW * w * P::ROW_BYTES + 1024 * n);
       lds_dma16(lds, off, v ? vview : kview);
     }
   };
@@ -696,14 +748,16 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     issue(2, false);
     issue(1, true);
   }
-  PfLane lo = pf_lane(lane);
+  PfLane<DH> lo = pf_lane<DH>(lane);
   // one block of the walk; u = j mod NS is a compile-time constant, so every ring
   // address below is a lane offset plus a constant the LDS instructions carry
   auto block = [&](const int j, auto uc) {
     constexpr int u = decltype(uc)::value;
     // keep the lane offsets as they are (not one precomputed address per use)
-    asm volatile("" : "+v"(lo.k[0]), "+v"(lo.k[1]), "+v"(lo.k[2]), "+v"(lo.k[3]),
-                 "+v"(lo.v[0][0]), "+v"(lo.v[0][1]), "+v"(lo.v[1][0]), "+v"(lo.v[1][1]));
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) asm volatile("" : "+v"(lo.k[ks]));
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) asm volatile("" : "+v"(lo.v[dt][0]), "+v"(lo.v[dt][1]));
     wait_vmcnt<2 * P::NI * AHEAD>();  // this wave's copies of K(j+1) and V(j) have landed ...
     __syncthreads();  // ... and every wave's; the stages of K(j-1) and V(j-2) are free
     issue(j + P::NS - 1, false);
@@ -712,7 +766,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
 #pragma unroll
       for (int t = 0; t < QT; ++t) {
         pf_init(sa[t], -st.m[t], 32 > wfree, 0, lim0 + 32 * t, lane);
-        sa[t] = pf_scores(smem, lo, pf_kh(0, 0), qf[t], sa[t]);
+        sa[t] = pf_scores<DH>(smem, lo, pf_kh<DH>(0, 0), qf[t], sa[t]);
         pf_init(sb[t], -st.m[t], 64 > wfree, 1, lim0 + 32 * t, lane);
       }
     }
@@ -720,12 +774,13 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     // past the wave's rows, so its weights are 0)
     const int i = 2 * j;
     if (i <= ilast + 1)
-      pf_step<QT>(smem, lo, pf_kh(u, 0), pf_kh(u, 1), pf_vh((u + P::NS - 1) % P::NS, 1), i, qf,
-                  st, sa, sb,
-                  lane, lim0, 32 * i + 32 > wfree, 32 * i + 96 > wfree);
+      pf_step<QT, DH>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
+                      pf_vh<DH>((u + P::NS - 1) % P::NS, 1), i, qf, st, sa, sb, lane, lim0,
+                      32 * i + 32 > wfree, 32 * i + 96 > wfree);
     if (i + 1 <= ilast + 1)
-      pf_step<QT>(smem, lo, pf_kh(u, 1), pf_kh((u + 1) % P::NS, 0), pf_vh(u, 0), i + 1, qf, st, sb,
-                  sa, lane, lim0, 32 * i + 64 > wfree, 32 * i + 128 > wfree);
+      pf_step<QT, DH>(smem, lo, pf_kh<DH>(u, 1), pf_kh<DH>((u + 1) % P::NS, 0),
+                      pf_vh<DH>(u, 0), i + 1, qf, st, sb, sa, lane, lim0,
+                      32 * i + 64 > wfree, 32 * i + 128 > wfree);
   };
   for (int j = 0; j < nblk; j += P::NS) {
     block(j, std::integral_constant<int, 0>());
@@ -735,9 +790,9 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   }
   if (ilast + 1 == 2 * nblk) {
     const int u = nblk % P::NS;
-    pf_step<QT>(smem, lo, pf_kh(u, 0), pf_kh(u, 1), pf_vh((u + P::NS - 1) % P::NS, 1), 2 * nblk,
-                qf, st, sa,
-                sb, lane, lim0, true, true);
+    pf_step<QT, DH>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
+                    pf_vh<DH>((u + P::NS - 1) % P::NS, 1), 2 * nblk, qf, st, sa, sb, lane, lim0,
+                    true, true);
   }
   wait_vmcnt<0>();  // no copy may land after the workgroup ends
 
@@ -747,9 +802,9 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     const float lt = halves_sum(st.lsum[t]);
     if (qi < a.T_new) {
       const float inv = 1.0f / lt;
-      bf16* dst = a.O + ((((long)l * a.B + b) * a.T_new + qi) * a.Hq + hq) * P::DH;
+      bf16* dst = a.O + ((((long)l * a.B + b) * a.T_new + qi) * a.Hq + hq) * DH;
 #pragma unroll
-      for (int dt = 0; dt < 2; ++dt)
+      for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           float v[4];
@@ -772,16 +827,18 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
                 sh.mask_paper, (sh.T_new + BQ - 1) / BQ,
                 kLog2e / sqrtf((float)sh.d), chan_map};
   dim3 grid(a.n_qtiles * sh.Hq * sh.B * sh.L);
-  if (sizeof(T) == 2 && sh.d == 64) {
-    constexpr int BQD = PfDma<kPfQt>::BQ;
+  if (sizeof(T) == 2 && (sh.d == 64 || sh.d == 96)) {  // fp32 at d = 96 fails validation
+    constexpr int BQD = PfDma<kPfQt, 64>::BQ;
+    static_assert(BQD == PfDma<kPfQt, 96>::BQ && PfDma<kPfQt, 64>::NT == PfDma<kPfQt, 96>::NT,
+                  "tile shapes");
     AttnArgs<T> ad = a;
     ad.n_qtiles = (sh.T_new + BQD - 1) / BQD;
-    hipLaunchKernelGGL(attend_prefill_dma_kernel<kPfQt>,
-                       dim3(ad.n_qtiles * sh.Hq * sh.B * sh.L), dim3(PfDma<kPfQt>::NT), 0, s,
-                       *reinterpret_cast<const AttnArgs<bf16>*>(&ad));
-  } else if (sh.d == 96) {
-    if constexpr (sizeof(T) == 2)  // fp32 at d = 96 is rejected by validation
-      hipLaunchKernelGGL((attend_prefill_kernel<T, 96>), grid, dim3(NT), 0, s, a);
+    const AttnArgs<bf16>& ab = *reinterpret_cast<const AttnArgs<bf16>*>(&ad);
+    const dim3 gd(ad.n_qtiles * sh.Hq * sh.B * sh.L), bd(PfDma<kPfQt, 64>::NT);
+    if (sh.d == 64)
+      hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 64>), gd, bd, 0, s, ab);
+    else
+      hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 96>), gd, bd, 0, s, ab);
   } else if (sh.d == 64)
     hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(NT), 0, s, a);
   else
