@@ -42,6 +42,11 @@ for _k in (1, 2, 4, 8, 12, 16):
     WORKLOAD_LABEL["paper_T2048_L16_k%d" % _k] = (
         "full-sequence pass, the paper's model shape: B16 T2048 L16 k%d D512 6q/3kv x96, p2, "
         "bf16, map l->l%%%d" % (_k, _k))
+for _k in (8, 16):
+    WORKLOAD_LABEL["paper_T2048_L16_k%d_docs" % _k] = (
+        "full-sequence pass, the paper's model shape with the document mask (packed documents "
+        "of mean length 512): B16 T2048 L16 k%d D512 6q/3kv x96, p2, bf16, map l->l%%%d"
+        % (_k, _k))
 del _k
 
 
@@ -73,13 +78,18 @@ def attn_flops(L, Hq, d, visible_pairs):
     return 4 * d * Hq * L * visible_pairs
 
 
-def visible_pairs(w):
+def visible_pairs(w, docs=None):
     """Sum over queries of the slots each one reads: dummy + slots < t in the paper's
-    mask (t + 1 in total), the same count as slots <= t without the dummy."""
-    return w.B * sum(w.ctx + i + 1 for i in range(w.T_new))
+    mask (t + 1 in total), the same count as slots <= t without the dummy; with the
+    document mask, dummy + slots of the query's document before it."""
+    if docs is None:
+        return w.B * sum(w.ctx + i + 1 for i in range(w.T_new))
+    import numpy as np
+    pos = w.ctx + np.arange(w.T_new)[None, :]
+    return int((pos - np.asarray(docs) + 1).sum())
 
 
-def phase_costs(w):
+def phase_costs(w, docs=None):
     """Per-phase (flops, HBM bytes) of one step."""
     es = 4 if w.dtype == "f32" else 2
     N, L, k, D, Hq, Hkv, d, p = w.N, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.p
@@ -97,13 +107,13 @@ def phase_costs(w):
                        2 * k * N * D * es + 2 * k * Hkv * d * D * es + cache_write),
         "q_project": (N * q_flops_per_token(L, Hq, d, D),
                       H_bytes + L * Hq * d * D * es + L * N * Hq * d * es),
-        "attend": (attn_flops(L, Hq, d, visible_pairs(w)),
+        "attend": (attn_flops(L, Hq, d, visible_pairs(w, docs)),
                    L * N * Hq * d * es + cache_read + L * N * Hq * d * es),
     }
 
 
-def step_cost(w):
-    c = phase_costs(w)
+def step_cost(w, docs=None):
+    c = phase_costs(w, docs)
     min_bytes = (w.N * w.L * w.D + 2 * w.k * w.L * ((w.L + w.p - 1) // w.p) * w.D
                  + 2 * w.k * w.Hkv * w.d * w.D + w.L * w.Hq * w.d * w.D) * (
         4 if w.dtype == "f32" else 2)
@@ -180,7 +190,7 @@ def measured_traffic(workload, kernel):
 
 # ------------------------------------------------------------ CPU baseline
 
-def cpu_baseline(w, P, H_cpu, cache_dev):
+def cpu_baseline(w, P, H_cpu, cache_dev, docs=None):
     """The oracle, as it stands, on a bounded sample: up to 8 sequences of the step (the
     whole 2048-token pass of B = 8 takes about 15 s on 16 host threads)."""
     import numpy as np
@@ -203,7 +213,8 @@ def cpu_baseline(w, P, H_cpu, cache_dev):
     Hs = H_cpu[:nseq]
     ctx = np.full(nseq, w.ctx, dtype=np.int32)
     t0 = time.perf_counter()
-    oracle.layer_step(dm, PP, Hs, w.chan_map, ctx, Kc, Vc)
+    oracle.layer_step(dm, PP, Hs, w.chan_map, ctx, Kc, Vc,
+                      doc_start=None if docs is None else docs[:nseq])
     dt = time.perf_counter() - t0
     toks = nseq * w.T_new
     cpu = "unknown"
@@ -292,6 +303,9 @@ def main():
         Kc = torch.zeros((w.k, w.B, w.Hkv, w.S_cap, w.d), dtype=w.torch_dtype, device=dev)
         Vc = torch.zeros_like(Kc)
     ctx = torch.full((w.B,), w.ctx, dtype=torch.int32, device=dev)
+    docs_cpu = (synth.make_doc_start(w, mean_len=synth.DOC_MEAN[w.name])
+                if w.name in synth.DOC_MEAN else None)
+    docs = docs_cpu.to(dev) if docs_cpu is not None else None
     O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device=dev)
     dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p, S_cap=w.S_cap,
                         ctx_max=w.ctx, dtype=wm.dtype_code(w.torch_dtype))
@@ -301,14 +315,15 @@ def main():
     hip = HipEvents()
     events = [[hip.create() for _ in range(wm.PROFILE_EVENTS)] for _ in range(args.steps)]
     for _ in range(args.warmup):
-        wm.layer_step(dims, P, H, w.chan_map, ctx, Kc, Vc, O, ws=ws, stream=stream)
+        wm.layer_step(dims, P, H, w.chan_map, ctx, Kc, Vc, O, ws=ws, stream=stream,
+                      doc_start=docs)
     torch.cuda.synchronize()
     log("bench: warmup done, timing %d steps" % args.steps)
 
     t0 = time.perf_counter()
     for s in range(args.steps):
         wm.layer_step_profiled(dims, P, H, w.chan_map, ctx, Kc, Vc, O, events[s], ws=ws,
-                               stream=stream)
+                               stream=stream, doc_start=docs)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     wall = t1 - t0
@@ -323,8 +338,9 @@ def main():
         for e in ev:
             hip.destroy(e)
     mean = {k: float(np.mean(v)) for k, v in phase_ms.items()}
-    costs = phase_costs(w)
-    flops, min_bytes = step_cost(w)
+    docs_np = docs_cpu.numpy() if docs_cpu is not None else None
+    costs = phase_costs(w, docs_np)
+    flops, min_bytes = step_cost(w, docs_np)
     for name in wm.PHASES:
         f, b = costs[name]
         t = mean[name] * 1e-3
@@ -395,7 +411,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline ...")
-        line["cpu_baseline"] = cpu_baseline(w, P_cpu, H_cpu, (Kc, Vc))
+        line["cpu_baseline"] = cpu_baseline(w, P_cpu, H_cpu, (Kc, Vc), docs_np)
     print(json.dumps(line), flush=True)
 
 

@@ -171,18 +171,39 @@ int wm_layer_step(const wm_dims *dims, const wm_params *params, const void *H,
                   const int32_t *chan_map, const int32_t *ctx_len, void *Kc, void *Vc,
                   void *O, void *ws, size_t ws_bytes, wm_stream_t stream);
 
-/* wm_layer_step that also records caller-created HIP events (hipEvent_t,
+/* Document mask (Section 5.1: sequences packed from several documents, attention
+ * confined to each document). Same as wm_channel_attend / wm_layer_step, plus
+ *   doc_start device int32 [B][T_new], 4-byte aligned, not NULL: the position of
+ *             the first token of the document that holds token i of sequence b
+ *             (positions count from the start of the sequence, so token i sits at
+ *             ctx_len[b] + i). Nondecreasing in i within a sequence (documents are
+ *             contiguous). The row reads only cached slots at or after doc_start
+ *             (and below its own position, as the mask mode says); the dummy slot
+ *             stays visible in WM_MASK_PAPER. Values outside [0, position] are
+ *             clamped into it; a decreasing array gives unspecified rows but no
+ *             access outside the cache. */
+int wm_channel_attend_doc(const wm_dims *dims, const wm_params *params, const void *Q,
+                          const int32_t *chan_map, const int32_t *ctx_len,
+                          const int32_t *doc_start, const void *Kc, const void *Vc, void *O,
+                          void *ws, size_t ws_bytes, wm_stream_t stream);
+int wm_layer_step_doc(const wm_dims *dims, const wm_params *params, const void *H,
+                      const int32_t *chan_map, const int32_t *ctx_len, const int32_t *doc_start,
+                      void *Kc, void *Vc, void *O, void *ws, size_t ws_bytes,
+                      wm_stream_t stream);
+
+/* Measurement helper: wm_layer_step (doc_start NULL) or wm_layer_step_doc
+ * (doc_start not NULL) that also records caller-created HIP events (hipEvent_t,
  * passed as void*) on `stream` at its phase boundaries, for per-phase timing of
  * the fused step: events[0] before the row norms, [1] before the router, [2]
  * before the mix, [3] before the K/V projection, [4] before the Q projection,
  * [5] before the channel attention, [6] after it. The array holds
  * WM_PROFILE_EVENTS non-NULL handles, owned by the caller. Results and errors
- * are those of wm_layer_step. */
+ * are those of the step it runs. */
 #define WM_PROFILE_EVENTS 7
 int wm_layer_step_profiled(const wm_dims *dims, const wm_params *params, const void *H,
-                           const int32_t *chan_map, const int32_t *ctx_len, void *Kc, void *Vc,
-                           void *O, void *ws, size_t ws_bytes, wm_stream_t stream,
-                           void *const *events);
+                           const int32_t *chan_map, const int32_t *ctx_len,
+                           const int32_t *doc_start, void *Kc, void *Vc, void *O, void *ws,
+                           size_t ws_bytes, wm_stream_t stream, void *const *events);
 
 /* Bytes of device workspace the op needs for these dims (0 if dims invalid). */
 size_t wm_workspace_size(const wm_dims *dims, int op);

@@ -254,27 +254,41 @@ def q_project(dims: Dims, params, H, ctx_len=None, toks=None) -> np.ndarray:
     return Q
 
 
-def channel_attend(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, rows=None) -> np.ndarray:
+def _docs(dims: Dims, doc_start):
+    """doc_start [B, T_new] int32 (position of each token's document start), or None."""
+    if doc_start is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(doc_start, dtype=np.int32).reshape(dims.B, dims.T_new))
+    return a
+
+
+def channel_attend(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, rows=None,
+                   doc_start=None) -> np.ndarray:
+    """Consumer attention; doc_start (optional, [B, T_new]) applies the document mask."""
     P = _as_params(params)
     Q, Kc, Vc = _f64(Q), _f64(Kc), _f64(Vc)
     ctx = _ctx(dims, ctx_len)
     m = np.ascontiguousarray(np.asarray(chan_map, dtype=np.int32))
     O = np.zeros((dims.L, dims.B, dims.T_new, dims.Hq * dims.d))
     arr, n, p = _ilist(rows)
-    lib().wmo_channel_attend(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(Q), _ptr(m),
-                             _ptr(ctx), _ptr(Kc), _ptr(Vc), p, ctypes.c_int(n), _ptr(O))
+    ds = _docs(dims, doc_start)
+    lib().wmo_channel_attend_doc(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(Q), _ptr(m),
+                                 _ptr(ctx), _ptr(ds) if ds is not None else None, _ptr(Kc),
+                                 _ptr(Vc), p, ctypes.c_int(n), _ptr(O))
     return O
 
 
-def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc) -> np.ndarray:
+def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, doc_start=None) -> np.ndarray:
     """Fused step; Kc/Vc (float64, in place) gain the new tokens' slots."""
     P = _as_params(params)
     H = _f64(H)
     ctx = _ctx(dims, ctx_len)
     m = np.ascontiguousarray(np.asarray(chan_map, dtype=np.int32))
     O = np.zeros((dims.L, dims.B, dims.T_new, dims.Hq * dims.d))
-    lib().wmo_layer_step(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(H), _ptr(m), _ptr(ctx),
-                         _ptr(Kc), _ptr(Vc), _ptr(O))
+    ds = _docs(dims, doc_start)
+    lib().wmo_layer_step_doc(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(H), _ptr(m),
+                             _ptr(ctx), _ptr(ds) if ds is not None else None, _ptr(Kc),
+                             _ptr(Vc), _ptr(O))
     return O
 
 

@@ -466,10 +466,16 @@ void wmo_q_project(const wmo_dims *dm, const wmo_params *P, const double *H, con
 }
 
 /* Step 3: consumer l reads channel map[l]. A row r = (l*B + b)*T_new + i
- * produces O[l][b][i][0 .. Hq*d). */
-void wmo_channel_attend(const wmo_dims *dm, const wmo_params *P, const double *Q, const int *map,
-                        const int *ctx_len, const double *Kc, const double *Vc, const int *rows,
-                        int nrows, double *O)
+ * produces O[l][b][i][0 .. Hq*d).
+ * Document mask (Section 5.1, sequences packed from several documents): when
+ * doc_start is given ([B][T_new], the position of the first token of the
+ * document holding token i), the row reads only cached slots at or after that
+ * position; the learned dummy slot stays visible to every row. Values outside
+ * [0, position] are clamped into it. */
+void wmo_channel_attend_doc(const wmo_dims *dm, const wmo_params *P, const double *Q,
+                            const int *map, const int *ctx_len, const int *doc_start,
+                            const double *Kc, const double *Vc, const int *rows, int nrows,
+                            double *O)
 {
     int B = dm->B, T = dm->T_new, L = dm->L, Hq = dm->Hq, Hkv = dm->Hkv, d = dm->d;
     int grp = Hq / Hkv;
@@ -481,31 +487,50 @@ void wmo_channel_attend(const wmo_dims *dm, const wmo_params *P, const double *Q
         int c = map[l];
         long pos = (long)(ctx_len ? ctx_len[b] : 0) + i;
         int paper = dm->mask_mode == WMO_MASK_PAPER;
-        long nvis = paper ? pos : pos + 1;
+        long nvis = paper ? pos : pos + 1;  /* slots 0 .. nvis-1 before the document mask */
+        long lo = doc_start ? doc_start[(size_t)b * T + i] : 0;
+        if (lo < 0)
+            lo = 0;
+        if (lo > pos)
+            lo = pos;
         for (int hh = 0; hh < Hq; ++hh) {
             int kvh = hh / grp;
-            size_t base = (((size_t)c * B + b) * Hkv + kvh) * dm->S_cap * d;
+            size_t base = (((size_t)c * B + b) * Hkv + kvh) * dm->S_cap * d + (size_t)lo * d;
             const double *q = Q + ((((size_t)l * B + b) * Hq + hh) * T + i) * d;
             const double *kd = paper ? P->Kd + ((size_t)c * Hkv + kvh) * d : NULL;
             const double *vd = paper ? P->Vd + ((size_t)c * Hkv + kvh) * d : NULL;
-            wmo_attend_row(d, q, Kc + base, d, Vc + base, d, nvis, kd, vd,
+            wmo_attend_row(d, q, Kc + base, d, Vc + base, d, nvis - lo, kd, vd,
                            O + (((size_t)l * B + b) * T + i) * Hq * d + (size_t)hh * d);
         }
     }
 }
 
+void wmo_channel_attend(const wmo_dims *dm, const wmo_params *P, const double *Q, const int *map,
+                        const int *ctx_len, const double *Kc, const double *Vc, const int *rows,
+                        int nrows, double *O)
+{
+    wmo_channel_attend_doc(dm, P, Q, map, ctx_len, NULL, Kc, Vc, rows, nrows, O);
+}
+
 /* The fused step: pool the T_new new tokens into their slots, project the
  * consumer queries, then every consumer attends its channel. Slots below
  * ctx_len[b] must already hold the cached context. */
-void wmo_layer_step(const wmo_dims *dm, const wmo_params *P, const double *H, const int *map,
-                    const int *ctx_len, double *Kc, double *Vc, double *O)
+void wmo_layer_step_doc(const wmo_dims *dm, const wmo_params *P, const double *H, const int *map,
+                        const int *ctx_len, const int *doc_start, double *Kc, double *Vc,
+                        double *O)
 {
     size_t nq = (size_t)dm->L * dm->B * dm->Hq * dm->T_new * dm->d;
     double *Q = (double *)malloc(sizeof(double) * nq);
     wmo_pool(dm, P, H, ctx_len, NULL, 0, Kc, Vc);
     wmo_q_project(dm, P, H, ctx_len, NULL, 0, Q);
-    wmo_channel_attend(dm, P, Q, map, ctx_len, Kc, Vc, NULL, 0, O);
+    wmo_channel_attend_doc(dm, P, Q, map, ctx_len, doc_start, Kc, Vc, NULL, 0, O);
     free(Q);
+}
+
+void wmo_layer_step(const wmo_dims *dm, const wmo_params *P, const double *H, const int *map,
+                    const int *ctx_len, double *Kc, double *Vc, double *O)
+{
+    wmo_layer_step_doc(dm, P, H, map, ctx_len, NULL, Kc, Vc, O);
 }
 
 int wmo_num_threads(void)

@@ -69,7 +69,10 @@ def lib() -> ctypes.CDLL:
         "wm_q_project": [D, P, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_channel_attend": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_layer_step": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
-        "wm_layer_step_profiled": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp],
+        "wm_channel_attend_doc": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_layer_step_doc": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_layer_step_profiled": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp,
+                                   _vp],
         "wm_validate": [D, ctypes.c_int, _i32p],
         "wm_channel_groups": [ctypes.c_int32, ctypes.c_int32, _i32p, _i32p, _i32p],
         "wm_default_map": [ctypes.c_int32, ctypes.c_int32, _i32p],
@@ -212,20 +215,34 @@ def q_project(dims: Dims, params, H, ctx_len, Q, ws=None, stream=None):
                               _ptr(Q), wp, wn, _stream(stream)))
 
 
-def channel_attend(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, ws=None, stream=None):
+def channel_attend(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, ws=None, stream=None,
+                   doc_start=None):
+    """doc_start (device int32 [B, T_new]) selects the document-masked entry point."""
     P = _params(params)
     ws, wp, wn = _ws(dims, OP_CHANNEL_ATTEND, ws, getattr(Q, "device", None))
-    _check(lib().wm_channel_attend(ctypes.byref(dims), ctypes.byref(P.c), _ptr(Q),
-                                   _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O),
-                                   wp, wn, _stream(stream)))
+    if doc_start is None:
+        _check(lib().wm_channel_attend(ctypes.byref(dims), ctypes.byref(P.c), _ptr(Q),
+                                       _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O),
+                                       wp, wn, _stream(stream)))
+    else:
+        _check(lib().wm_channel_attend_doc(ctypes.byref(dims), ctypes.byref(P.c), _ptr(Q),
+                                           _map(chan_map), _ptr(ctx_len), _ptr(doc_start),
+                                           _ptr(Kc), _ptr(Vc), _ptr(O), wp, wn, _stream(stream)))
 
 
-def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws=None, stream=None):
+def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws=None, stream=None,
+               doc_start=None):
+    """doc_start (device int32 [B, T_new]) selects the document-masked entry point."""
     P = _params(params)
     ws, wp, wn = _ws(dims, OP_LAYER_STEP, ws, getattr(H, "device", None))
-    _check(lib().wm_layer_step(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H), _map(chan_map),
-                               _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O), wp, wn,
-                               _stream(stream)))
+    if doc_start is None:
+        _check(lib().wm_layer_step(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H), _map(chan_map),
+                                   _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O), wp, wn,
+                                   _stream(stream)))
+    else:
+        _check(lib().wm_layer_step_doc(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H),
+                                       _map(chan_map), _ptr(ctx_len), _ptr(doc_start), _ptr(Kc),
+                                       _ptr(Vc), _ptr(O), wp, wn, _stream(stream)))
 
 
 PROFILE_EVENTS = 7
@@ -233,14 +250,15 @@ PHASES = ("norms", "router", "mix", "kv_project", "q_project", "attend")
 
 
 def layer_step_profiled(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, events, ws=None,
-                        stream=None):
+                        stream=None, doc_start=None):
     """layer_step that records PROFILE_EVENTS caller-created hipEvent_t handles (ints) at
     its phase boundaries on the stream."""
     P = _params(params)
     ws, wp, wn = _ws(dims, OP_LAYER_STEP, ws, getattr(H, "device", None))
     ev = (ctypes.c_void_p * PROFILE_EVENTS)(*events)
     _check(lib().wm_layer_step_profiled(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H),
-                                        _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
+                                        _map(chan_map), _ptr(ctx_len), _ptr(doc_start),
+                                        _ptr(Kc), _ptr(Vc),
                                         _ptr(O), wp, wn, _stream(stream), ev))
 
 

@@ -241,21 +241,22 @@ void run_q_project(const wm_dims& d, const wm_params& P, const T* H, const int32
 
 template <typename T>
 void run_attend(const wm_dims& d, const wm_params& P, const T* Q, const int32_t* chan_map,
-                const int32_t* ctx_len, const T* Kc, const T* Vc, T* O, float* part,
-                hipStream_t s) {
+                const int32_t* ctx_len, const int32_t* doc, const T* Kc, const T* Vc, T* O,
+                float* part, hipStream_t s) {
   wm::Shape sh = make_shape(d);
   wm::LayerTable mt = map_table(d, chan_map);
   if (decode_path(d))
     wm::launch_attend_decode<T>(sh, mt, groups(d, chan_map), Q, Kc, Vc, (const T*)P.Kd,
-                                (const T*)P.Vd, ctx_len, part, O, s);
+                                (const T*)P.Vd, ctx_len, doc, part, O, s);
   else
-    wm::launch_attend_prefill<T>(sh, mt, Q, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len, O, s);
+    wm::launch_attend_prefill<T>(sh, mt, Q, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len, doc,
+                                 O, s);
 }
 
 template <typename T>
 void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int32_t* chan_map,
-                    const int32_t* ctx_len, T* Kc, T* Vc, T* O, void* ws, hipStream_t s,
-                    void* const* events) {
+                    const int32_t* ctx_len, const int32_t* doc, T* Kc, T* Vc, T* O, void* ws,
+                    hipStream_t s, void* const* events) {
   auto mark = [&](int i) {
     if (events) (void)hipEventRecord((hipEvent_t)events[i], s);
   };
@@ -284,7 +285,7 @@ void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int3
   wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
                           tab, Q, (T*)at(ws, Ly.wq), s);
   mark(5);
-  run_attend<T>(d, P, Q, chan_map, ctx_len, Kc, Vc, O, (float*)at(ws, Ly.part), s);
+  run_attend<T>(d, P, Q, chan_map, ctx_len, doc, Kc, Vc, O, (float*)at(ws, Ly.part), s);
   mark(6);
 }
 
@@ -431,9 +432,10 @@ int wm_q_project(const wm_dims* dims, const wm_params* params, const void* H,
   return launched();
 }
 
-int wm_channel_attend(const wm_dims* dims, const wm_params* params, const void* Q,
-                      const int32_t* chan_map, const int32_t* ctx_len, const void* Kc,
-                      const void* Vc, void* O, void* ws, size_t ws_bytes, wm_stream_t stream) {
+static int channel_attend_impl(const wm_dims* dims, const wm_params* params, const void* Q,
+                               const int32_t* chan_map, const int32_t* ctx_len,
+                               const int32_t* doc, const void* Kc, const void* Vc, void* O,
+                               void* ws, size_t ws_bytes, wm_stream_t stream) {
   if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
   WM_TRY(validate_dims(dims, WM_OP_CHANNEL_ATTEND, chan_map));
   const wm_dims& d = *dims;
@@ -449,18 +451,35 @@ int wm_channel_attend(const wm_dims* dims, const wm_params* params, const void* 
   hipStream_t s = (hipStream_t)stream;
   float* part = (float*)at(ws, layout(d, WM_OP_CHANNEL_ATTEND).part);
   if (d.dtype == WM_BF16)
-    run_attend<bf16>(d, *params, (const bf16*)Q, chan_map, ctx_len, (const bf16*)Kc,
+    run_attend<bf16>(d, *params, (const bf16*)Q, chan_map, ctx_len, doc, (const bf16*)Kc,
                      (const bf16*)Vc, (bf16*)O, part, s);
   else
-    run_attend<float>(d, *params, (const float*)Q, chan_map, ctx_len, (const float*)Kc,
+    run_attend<float>(d, *params, (const float*)Q, chan_map, ctx_len, doc, (const float*)Kc,
                       (const float*)Vc, (float*)O, part, s);
   return launched();
 }
 
+int wm_channel_attend(const wm_dims* dims, const wm_params* params, const void* Q,
+                      const int32_t* chan_map, const int32_t* ctx_len, const void* Kc,
+                      const void* Vc, void* O, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  return channel_attend_impl(dims, params, Q, chan_map, ctx_len, nullptr, Kc, Vc, O, ws,
+                             ws_bytes, stream);
+}
+
+int wm_channel_attend_doc(const wm_dims* dims, const wm_params* params, const void* Q,
+                          const int32_t* chan_map, const int32_t* ctx_len,
+                          const int32_t* doc_start, const void* Kc, const void* Vc, void* O,
+                          void* ws, size_t ws_bytes, wm_stream_t stream) {
+  if (!doc_start) return fail(WM_ERR_ARG, "doc_start is NULL");
+  if ((uintptr_t)doc_start % 4 != 0) return fail(WM_ERR_ARG, "doc_start is not 4-byte aligned");
+  return channel_attend_impl(dims, params, Q, chan_map, ctx_len, doc_start, Kc, Vc, O, ws,
+                             ws_bytes, stream);
+}
+
 static int layer_step_impl(const wm_dims* dims, const wm_params* params, const void* H,
-                           const int32_t* chan_map, const int32_t* ctx_len, void* Kc, void* Vc,
-                           void* O, void* ws, size_t ws_bytes, wm_stream_t stream,
-                           void* const* events) {
+                           const int32_t* chan_map, const int32_t* ctx_len, const int32_t* doc,
+                           void* Kc, void* Vc, void* O, void* ws, size_t ws_bytes,
+                           wm_stream_t stream, void* const* events) {
   if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
   WM_TRY(validate_dims(dims, WM_OP_LAYER_STEP, chan_map));
   const wm_dims& d = *dims;
@@ -475,30 +494,41 @@ static int layer_step_impl(const wm_dims* dims, const wm_params* params, const v
   (void)hipGetLastError();
   hipStream_t s = (hipStream_t)stream;
   if (d.dtype == WM_BF16)
-    run_layer_step<bf16>(d, *params, (const bf16*)H, chan_map, ctx_len, (bf16*)Kc, (bf16*)Vc,
-                         (bf16*)O, ws, s, events);
+    run_layer_step<bf16>(d, *params, (const bf16*)H, chan_map, ctx_len, doc, (bf16*)Kc,
+                         (bf16*)Vc, (bf16*)O, ws, s, events);
   else
-    run_layer_step<float>(d, *params, (const float*)H, chan_map, ctx_len, (float*)Kc, (float*)Vc,
-                          (float*)O, ws, s, events);
+    run_layer_step<float>(d, *params, (const float*)H, chan_map, ctx_len, doc, (float*)Kc,
+                          (float*)Vc, (float*)O, ws, s, events);
   return launched();
 }
 
 int wm_layer_step(const wm_dims* dims, const wm_params* params, const void* H,
                   const int32_t* chan_map, const int32_t* ctx_len, void* Kc, void* Vc, void* O,
                   void* ws, size_t ws_bytes, wm_stream_t stream) {
-  return layer_step_impl(dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws, ws_bytes, stream,
-                         nullptr);
+  return layer_step_impl(dims, params, H, chan_map, ctx_len, nullptr, Kc, Vc, O, ws, ws_bytes,
+                         stream, nullptr);
+}
+
+int wm_layer_step_doc(const wm_dims* dims, const wm_params* params, const void* H,
+                      const int32_t* chan_map, const int32_t* ctx_len, const int32_t* doc_start,
+                      void* Kc, void* Vc, void* O, void* ws, size_t ws_bytes,
+                      wm_stream_t stream) {
+  if (!doc_start) return fail(WM_ERR_ARG, "doc_start is NULL");
+  if ((uintptr_t)doc_start % 4 != 0) return fail(WM_ERR_ARG, "doc_start is not 4-byte aligned");
+  return layer_step_impl(dims, params, H, chan_map, ctx_len, doc_start, Kc, Vc, O, ws, ws_bytes,
+                         stream, nullptr);
 }
 
 int wm_layer_step_profiled(const wm_dims* dims, const wm_params* params, const void* H,
-                           const int32_t* chan_map, const int32_t* ctx_len, void* Kc, void* Vc,
-                           void* O, void* ws, size_t ws_bytes, wm_stream_t stream,
-                           void* const* events) {
+                           const int32_t* chan_map, const int32_t* ctx_len,
+                           const int32_t* doc_start, void* Kc, void* Vc, void* O, void* ws,
+                           size_t ws_bytes, wm_stream_t stream, void* const* events) {
   if (!events) return fail(WM_ERR_ARG, "events is NULL");
   for (int i = 0; i < WM_PROFILE_EVENTS; ++i)
     if (!events[i]) return fail(WM_ERR_ARG, "events[%d] is NULL", i);
-  return layer_step_impl(dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws, ws_bytes, stream,
-                         events);
+  if ((uintptr_t)doc_start % 4 != 0) return fail(WM_ERR_ARG, "doc_start is not 4-byte aligned");
+  return layer_step_impl(dims, params, H, chan_map, ctx_len, doc_start, Kc, Vc, O, ws, ws_bytes,
+                         stream, events);
 }
 
 }  // extern "C"

@@ -49,9 +49,29 @@ constexpr float kGrowSum = 65536.0f;
 // exact-max rescale, which then sets a real reference.
 constexpr float kNoRef = -100.0f;
 
+// Document mask (packed sequences, Section 5.1): query i of sequence b, at position
+// ctx + i, reads cached slots from its document's first position on (clamped into
+// [0, position]); the dummy slot stays visible. Without a document array every row
+// starts at slot 0.
+__device__ __forceinline__ int doc_first(const int32_t* doc, int b, int T_new, int i, int pos) {
+  if (!doc) return 0;
+  return min(max(doc[(long)b * T_new + i], 0), pos);
+}
+__device__ __forceinline__ int wave_min_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = min(v, __shfl_xor(v, m, 64));
+  return v;
+}
+__device__ __forceinline__ int wave_max_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = max(v, __shfl_xor(v, m, 64));
+  return v;
+}
+
 template <typename T> struct AttnArgs {
   const T *Q, *Kc, *Vc, *Kd, *Vd;
   const int32_t* ctx_len;
+  const int32_t* doc;  // [B][T_new] first position of each token's document, or null
   T* O;
   int B, T_new, L, Hq, Hkv, S_cap, mask_paper, n_qtiles;
   float scale_log2;  // log2(e) / sqrt(d)
@@ -119,7 +139,7 @@ __device__ __forceinline__ void attend_block(
     const T* __restrict__ ks_, const T* __restrict__ vt_,
     const frag_t<T> (&qf)[PrefillCfg<T, DH>::QT][DH / 16], float (&m)[PrefillCfg<T, DH>::QT],
     float (&lsum)[PrefillCfg<T, DH>::QT], f32x16 (&o)[DH / 32][PrefillCfg<T, DH>::QT], int k0,
-    int wkend, int tq0, int incl, int h, int r) {
+    int wkend, int tq0, int incl, const int (&dlo)[PrefillCfg<T, DH>::QT], int h, int r) {
   using C = PrefillCfg<T, DH>;
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
@@ -148,11 +168,14 @@ __device__ __forceinline__ void attend_block(
     for (int qt = 0; qt < C::QT; ++qt) {
       if (MASK) {
         // slot k0 + 32kt + 8(q/4) + 4h + q%4 is visible to the row at position t iff
-        // it is < t + incl
-        const int lim = tq0 + 32 * qt + r + incl - (k0 + 32 * kt + 4 * h);
+        // it is < t + incl and at least the row's document start
+        const int base = k0 + 32 * kt + 4 * h;
+        const int lim = tq0 + 32 * qt + r + incl - base, lo = dlo[qt] - base;
 #pragma unroll
-        for (int q = 0; q < 16; ++q)
-          if (8 * (q >> 2) + (q & 3) >= lim) st[qt][q] = kNegBig;
+        for (int q = 0; q < 16; ++q) {
+          const int off = 8 * (q >> 2) + (q & 3);
+          if (off >= lim || off < lo) st[qt][q] = kNegBig;
+        }
       }
       // Weights against the current reference m first: while every weight stays below
       // 2^12 (so a lane's sum of 16 stays below 2^16) no rescale is needed. Otherwise
@@ -227,7 +250,39 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   const int q0 = qtile * C::BQ, qw0 = q0 + 32 * QT * w;
   const float cl2 = a.scale_log2;
 
-  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
+  // document mask: each row's first readable slot; the walk starts at the block holding
+  // the workgroup's least one (base0), and slot indices below are relative to base0
+  __shared__ int s_lo[C::NW];
+  int dlo[QT], base0 = 0, wlo_max = 0, wlo_min = 0;  // wlo_min: blocks below it are skipped
+  if (a.doc) {
+    int wmin = 0x7fffffff;
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      const int qi = qw0 + 32 * qt + r;
+      dlo[qt] = qi < a.T_new ? doc_first(a.doc, b, a.T_new, qi, ctx + qi) : 0;
+      wmin = min(wmin, qi < a.T_new ? dlo[qt] : 0x7fffffff);
+      wlo_max = max(wlo_max, dlo[qt]);
+    }
+    wmin = __builtin_amdgcn_readfirstlane(wave_min_i(wmin));
+    wlo_max = __builtin_amdgcn_readfirstlane(wave_max_i(wlo_max));
+    if (lane == 0) s_lo[w] = wmin;
+    __syncthreads();
+    int gmin = s_lo[0];
+#pragma unroll
+    for (int k = 1; k < C::NW; ++k) gmin = min(gmin, s_lo[k]);
+    base0 = __builtin_amdgcn_readfirstlane(gmin / C::BKV * C::BKV);
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) dlo[qt] -= base0;
+    wlo_max -= base0;
+    wlo_min = wmin == 0x7fffffff ? 0 : wmin - base0;
+  } else {
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) dlo[qt] = 0;
+  }
+  const int ctxr = ctx - base0, scap = a.S_cap - base0;
+
+  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH +
+                     (long)base0 * DH;
   const T* Kb = a.Kc + cbase;
   const T* Vb = a.Vc + cbase;
 
@@ -281,10 +336,11 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   }
 
   const int qlast = min(q0 + C::BQ, a.T_new) - 1;
-  const int kend = min(ctx + qlast + incl, a.S_cap);   // slots the workgroup may see
+  const int kend = min(ctxr + qlast + incl, scap);    // slots the workgroup may see
   const int wq_last = min(qw0 + 32 * QT - 1, a.T_new - 1);
-  const int wkend = wq_last >= qw0 ? ctx + wq_last + incl : 0;  // slots this wave may see
-  const int wfree = ctx + qw0 + incl;                  // slots < wfree are visible to all its rows
+  const int wkend = wq_last >= qw0 ? ctxr + wq_last + incl : 0;  // slots this wave may see
+  // slots in [wlo_max, wfree) are visible to all its rows
+  const int wfree = ctxr + qw0 + incl;
   const int nblk = (kend + C::BKV - 1) / C::BKV;
 
   // staged next block: K fragments (row-major copy) and V fragments (row-major, bf16)
@@ -292,8 +348,8 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   frag_t<T> kreg[C::KFR], vreg[C::VPT][C::VTR ? 1 : 2];
   // the (channel, sequence, KV head) slice through buffer views: slots at or past kend
   // read as zeros without a branch
-  const __amdgpu_buffer_rsrc_t kview = make_view(Kb, (uint32_t)a.S_cap * DH * sizeof(T));
-  const __amdgpu_buffer_rsrc_t vview = make_view(Vb, (uint32_t)a.S_cap * DH * sizeof(T));
+  const __amdgpu_buffer_rsrc_t kview = make_view(Kb, (uint32_t)scap * DH * sizeof(T));
+  const __amdgpu_buffer_rsrc_t vview = make_view(Vb, (uint32_t)scap * DH * sizeof(T));
   auto slot_off = [&](int s, int col) {
     return s < kend ? (uint32_t)(s * DH + col) * (uint32_t)sizeof(T) : kOffOob;
   };
@@ -346,13 +402,13 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   for (int j = 0; j < nblk; ++j) {
     const int k0 = j * C::BKV, buf = j & 1;
     fetch(k0 + C::BKV);
-    if (k0 < wkend) {
-      if (k0 + C::BKV > wfree)
-        attend_block<T, DH, true>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
-                                  h, r);
+    if (k0 < wkend && k0 + C::BKV > wlo_min) {
+      if (k0 + C::BKV > wfree || k0 < wlo_max)
+        attend_block<T, DH, true>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctxr + qw0, incl,
+                                  dlo, h, r);
       else
-        attend_block<T, DH, false>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctx + qw0, incl,
-                                   h, r);
+        attend_block<T, DH, false>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctxr + qw0,
+                                   incl, dlo, h, r);
     }
     stage(buf ^ 1);
     __syncthreads();
@@ -506,14 +562,19 @@ __device__ __forceinline__ f32x16 pf_scores(const char* sm, const PfLane<DH>& lo
 
 // Accumulator start for the scores of step i: -m (the row reference), or -1e30 for the
 // slots a masked step hides from this lane's row (slot 32 i + 8(q/4) + 4h + q%4 is
-// visible iff it is below lim0, the row position + incl). -1e30 plus any score stays
-// about -1e30, so the MFMAs that follow need no masking afterwards.
+// visible iff it is at least lo0, the row's document start, and below lim0, the row
+// position + incl). -1e30 plus any score stays about -1e30, so the MFMAs that follow
+// need no masking afterwards.
+template <bool DOC>
 __device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int i, int lim0,
-                                        int lane) {
+                                        int lo0, int lane) {
   if (masked) {
-    const int lim = lim0 - (32 * i + 4 * (lane >> 5));
+    const int base = 32 * i + 4 * (lane >> 5), lim = lim0 - base, lo = lo0 - base;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) v[q] = 8 * (q >> 2) + (q & 3) >= lim ? kNegBig : init;
+    for (int q = 0; q < 16; ++q) {
+      const int off = 8 * (q >> 2) + (q & 3);
+      v[q] = off >= lim || (DOC && off < lo) ? kNegBig : init;
+    }
   } else {
 #pragma unroll
     for (int q = 0; q < 16; ++q) v[q] = init;
@@ -547,12 +608,13 @@ template <int N, int I0 = 0> __device__ __forceinline__ float tree_sum_arr(const
 // arrives holding the start value of S(i+1) (pf_init) and leaves holding S(i+1). Two
 // register sets alternate between consecutive steps, and sc is refilled with the start
 // value of S(i+2), so no step waits on the MFMAs it has just issued. lim0 is the first
-// tile's row limit; tile t's rows sit 32 t further.
-template <int QT, int DH>
+// tile's row limit; tile t's rows sit 32 t further; dlo[t] is tile t's document start.
+template <int QT, int DH, bool DOC>
 __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, uint32_t kh_cur,
                                         uint32_t kh_nxt, uint32_t vh_prv, int i,
                                         const bf16x8 (&qf)[QT][DH / 16], PfState<QT, DH>& st,
                                         f32x16 (&sc)[QT], f32x16 (&sn)[QT], int lane, int lim0,
+                                        const int (&dlo)[QT],
                                         bool mask_cur, bool mask_n2) {
   // NG groups g, each: the MFMAs of PV(i-1) for keys 16(g / NDT).. and value tile
   // g % NDT and of S(i+1) for k16 step g, plus the weights of rows [q0(g), q0(g+1)) of
@@ -594,7 +656,7 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
       // rare: move the reference up to the exact row max (never down) and rescale the
       // state; S(i+1) was started from the old reference, so it moves too
       f32x16 sr;
-      pf_init(sr, -st.m[t], mask_cur, i, lim0 + 32 * t, lane);
+      pf_init<DOC>(sr, -st.m[t], mask_cur, i, lim0 + 32 * t, dlo[t], lane);
       sr = pf_scores<DH>(sm, lo, kh_cur, qf[t], sr);
       float mx = sr[0];
 #pragma unroll
@@ -616,11 +678,13 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
 #pragma unroll
     for (int q = 0; q < 16; ++q) st.pf[q >> 3][t][q & 7] = (bf16)sc[t][q];
     st.lsum[t] += ps;
-    pf_init(sc[t], -st.m[t], mask_n2, i + 2, lim0 + 32 * t, lane);  // accumulator of S(i+2)
+    pf_init<DOC>(sc[t], -st.m[t], mask_n2, i + 2, lim0 + 32 * t, dlo[t], lane);  // S(i+2)
   }
 }
 
-template <int QT, int DH>
+// DOC: the document mask is on (a.doc is not null); the kernel without it keeps the
+// step loop free of the document bookkeeping.
+template <int QT, int DH, bool DOC>
 __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(DH == 64 ? 3 : 2)))
 void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   using P = PfDma<QT, DH>;
@@ -653,7 +717,41 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
       *(i32x4*)(smem + 16 * (tid + P::NT * k)) = z;
   }
 
-  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
+  // Document mask: each row's first readable slot; the walk starts at the 64-slot block
+  // holding the workgroup's least one (base0), and every slot index below is relative
+  // to base0. Blocks a wave's rows partly cannot read are masked like the causal edge.
+  __shared__ int s_lo[P::NW];
+  // (A wave's steps below its own rows' document starts are masked, not skipped:
+  // measured, skipping them and restarting the pipeline later is slower.)
+  int dlo[QT], base0 = 0, wlo_max = 0;
+  if constexpr (DOC) {
+    int wmin = 0x7fffffff;
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      const int qi = qw0 + 32 * t + r;
+      dlo[t] = qi < a.T_new ? doc_first(a.doc, b, a.T_new, qi, ctx + qi) : 0;
+      wmin = min(wmin, qi < a.T_new ? dlo[t] : 0x7fffffff);
+      wlo_max = max(wlo_max, dlo[t]);
+    }
+    wmin = __builtin_amdgcn_readfirstlane(wave_min_i(wmin));
+    wlo_max = __builtin_amdgcn_readfirstlane(wave_max_i(wlo_max));
+    if (lane == 0) s_lo[w] = wmin;
+    __syncthreads();
+    int gmin = s_lo[0];
+#pragma unroll
+    for (int k = 1; k < P::NW; ++k) gmin = min(gmin, s_lo[k]);
+    base0 = __builtin_amdgcn_readfirstlane(gmin / P::BKV * P::BKV);
+#pragma unroll
+    for (int t = 0; t < QT; ++t) dlo[t] -= base0;  // rows past T_new go negative: no mask
+    wlo_max -= base0;
+  } else {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) dlo[t] = 0;
+  }
+  const int ctxr = ctx - base0;  // the first new token's position relative to base0
+
+  const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH +
+                     (long)base0 * DH;
   bf16x8 qf[QT][NKS];
   const bf16* Qb = a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * DH;
 #pragma unroll
@@ -700,20 +798,23 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   }
 
   const int qlast = min(q0 + P::BQ, a.T_new) - 1;
-  const int kend = min(ctx + qlast + incl, a.S_cap);   // slots the workgroup may see
+  const int scap = a.S_cap - base0;
+  const int kend = min(ctxr + qlast + incl, scap);   // slots the workgroup may see
   const int nblk = (kend + P::BKV - 1) / P::BKV;
   const int wq_last = min(qw0 + 32 * QT - 1, a.T_new - 1);
-  const int wkend = wq_last >= qw0 ? ctx + wq_last + incl : 0;  // slots this wave may see
-  const int wfree = ctx + qw0 + incl;   // slots < wfree are visible to all its rows
+  const int wkend = wq_last >= qw0 ? ctxr + wq_last + incl : 0;  // slots this wave may see
+  const int wfree = ctxr + qw0 + incl;  // slots < wfree are visible to all its rows ...
+  // ... and at or past wlo_max (the document starts); a step is masked unless both hold
+  auto masked = [&](int i) { return 32 * i + 32 > wfree || (DOC && 32 * i < wlo_max); };
   const int ilast = (wkend + 31) / 32 - 1;  // the wave's last 32-slot step (-1: none)
-  const int lim0 = ctx + qw0 + r + incl;
+  const int lim0 = ctxr + qw0 + r + incl;
 
   // copies: wave w moves slot rows RPW w .. RPW w + RPW-1 of each K and V block, 1 KB
   // (64 chunks of 16 B) per instruction; lane x of instruction n fills LDS chunk
   // 64 n + x of the wave's rows, i.e. row (64 n + x) / CPR, chunk (64 n + x) % CPR, with
   // the chunk of the slot row that the swizzle puts there
-  const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)a.S_cap * P::ROW_BYTES);
-  const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)a.S_cap * P::ROW_BYTES);
+  const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)scap * P::ROW_BYTES);
+  const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)scap * P::ROW_BYTES);
   int crow[P::NI];
   uint32_t dchunk[P::NI];
 #pragma unroll
@@ -771,26 +872,26 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     if (u == 0 && j == 0 && ilast >= 0) {
 #pragma unroll
       for (int t = 0; t < QT; ++t) {
-        pf_init(sa[t], -st.m[t], 32 > wfree, 0, lim0 + 32 * t, lane);
+        pf_init<DOC>(sa[t], -st.m[t], masked(0), 0, lim0 + 32 * t, dlo[t], lane);
         sa[t] = pf_scores<DH>(smem, lo, pf_kh<DH>(0, 0), qf[t], sa[t]);
-        pf_init(sb[t], -st.m[t], 64 > wfree, 1, lim0 + 32 * t, lane);
+        pf_init<DOC>(sb[t], -st.m[t], masked(1), 1, lim0 + 32 * t, dlo[t], lane);
       }
     }
     // steps up to ilast + 1: the last one only adds PV(ilast) (its own slots are all
     // past the wave's rows, so its weights are 0)
     const int i = 2 * j;
     if (i <= ilast + 1)
-      pf_step<QT, DH>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
+      pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
                       pf_vh<DH>((u + P::NS - 1) % P::NS, 1), i, qf, st, sa, sb, lane, lim0,
-                      32 * i + 32 > wfree, 32 * i + 96 > wfree);
+                      dlo, masked(i), masked(i + 2));
     // the second step reads K(j+1) and V(j): only the copies issued above may still be
     // in flight
     wait_vmcnt<2 * P::NI * (1 + AHEAD)>();
     __syncthreads();
     if (i + 1 <= ilast + 1)
-      pf_step<QT, DH>(smem, lo, pf_kh<DH>(u, 1), pf_kh<DH>((u + 1) % P::NS, 0),
-                      pf_vh<DH>(u, 0), i + 1, qf, st, sb, sa, lane, lim0,
-                      32 * i + 64 > wfree, 32 * i + 128 > wfree);
+      pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 1), pf_kh<DH>((u + 1) % P::NS, 0),
+                      pf_vh<DH>(u, 0), i + 1, qf, st, sb, sa, lane, lim0, dlo,
+                      masked(i + 1), masked(i + 3));
   };
   for (int j = 0; j < nblk; j += P::NS) {
     block(j, std::integral_constant<int, 0>());
@@ -800,9 +901,9 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   }
   if (ilast + 1 == 2 * nblk) {
     const int u = nblk % P::NS;
-    pf_step<QT, DH>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
+    pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
                     pf_vh<DH>((u + P::NS - 1) % P::NS, 1), 2 * nblk, qf, st, sa, sb, lane, lim0,
-                    true, true);
+                    dlo, true, true);
   }
   wait_vmcnt<0>();  // no copy may land after the workgroup ends
 
@@ -828,12 +929,12 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
 
 template <typename T>
 void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q, const T* Kc,
-                           const T* Vc, const T* Kd, const T* Vd, const int32_t* ctx_len, T* O,
-                           hipStream_t s) {
+                           const T* Vc, const T* Kd, const T* Vd, const int32_t* ctx_len,
+                           const int32_t* doc, T* O, hipStream_t s) {
   if (sh.N() <= 0) return;
   constexpr int BQ = PrefillCfg<T, 64>::BQ, NT = PrefillCfg<T, 64>::NT;
   static_assert(BQ == PrefillCfg<T, 32>::BQ && NT == PrefillCfg<T, 32>::NT, "tile shapes");
-  AttnArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
+  AttnArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, doc, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
                 sh.mask_paper, (sh.T_new + BQ - 1) / BQ,
                 kLog2e / sqrtf((float)sh.d), chan_map};
   dim3 grid(a.n_qtiles * sh.Hq * sh.B * sh.L);
@@ -845,10 +946,13 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
     ad.n_qtiles = (sh.T_new + BQD - 1) / BQD;
     const AttnArgs<bf16>& ab = *reinterpret_cast<const AttnArgs<bf16>*>(&ad);
     const dim3 gd(ad.n_qtiles * sh.Hq * sh.B * sh.L), bd(PfDma<kPfQt, 64>::NT);
-    if (sh.d == 64)
-      hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 64>), gd, bd, 0, s, ab);
-    else
-      hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 96>), gd, bd, 0, s, ab);
+    if (sh.d == 64) {
+      if (doc) hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 64, true>), gd, bd, 0, s, ab);
+      else hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 64, false>), gd, bd, 0, s, ab);
+    } else {
+      if (doc) hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 96, true>), gd, bd, 0, s, ab);
+      else hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 96, false>), gd, bd, 0, s, ab);
+    }
   } else if (sh.d == 64)
     hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(NT), 0, s, a);
   else
@@ -885,6 +989,7 @@ size_t decode_partials_bytes(const Shape& sh) {
 template <typename T> struct DecodeArgs {
   const T *Q, *Kc, *Vc, *Kd, *Vd;
   const int32_t* ctx_len;
+  const int32_t* doc;  // [B][T_new] first position of each token's document, or null
   float* part;  // [L][B][Hq][T_new][nsplit][d + 2]: unnormalised o, m, l
   T* O;
   int B, T_new, L, Hq, Hkv, S_cap, mask_paper, nsplit, split_len;
@@ -946,7 +1051,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
   for (int g0 = 0; g0 < G; g0 += NG) {
     const int ng = min(NG, G - g0);
     float q[NG][8], m[NG], ls[NG], o[NG][8];
-    int vis[NG];
+    int vis[NG], lov[NG];  // the row reads slots lov <= s < vis
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi) {
       m[gi] = kNegBig;
@@ -959,6 +1064,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
         int l = a.cg.members[off + mi], hq = kvh * grp + gq;
         long rowid = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + i;
         vis[gi] = ctx + i + incl;
+        lov[gi] = doc_first(a.doc, b, a.T_new, i, ctx + i);
         if (chunk) load8(a.Q + rowid * DH + 8 * c8, q[gi]);
         else {
 #pragma unroll
@@ -966,6 +1072,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
         }
       } else {
         vis[gi] = 0;
+        lov[gi] = 0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) q[gi][i] = 0.f;
       }
@@ -994,7 +1101,7 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
           for (int i = 0; i < 8; ++i) d += q[gi][i] * to_f32(kr[u][i]);
 #pragma unroll
           for (int x = 1; x < LPS; x <<= 1) d += __shfl_xor(d, x, 64);
-          p[u][gi] = s < s1 && s < vis[gi] ? d : kNegBig;
+          p[u][gi] = s < s1 && s < vis[gi] && s >= lov[gi] ? d : kNegBig;
         }
       }
 #pragma unroll
@@ -1139,9 +1246,10 @@ static void decode_dispatch(const DecodeArgs<T>& a, int G, dim3 grid, hipStream_
 template <typename T>
 void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const ChannelGroups& cg,
                           const T* Q, const T* Kc, const T* Vc, const T* Kd, const T* Vd,
-                          const int32_t* ctx_len, float* partials, T* O, hipStream_t s) {
+                          const int32_t* ctx_len, const int32_t* doc, float* partials, T* O,
+                          hipStream_t s) {
   if (sh.N() <= 0) return;
-  DecodeArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, partials, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv,
+  DecodeArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, doc, partials, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv,
                   sh.S_cap, sh.mask_paper, decode_splits(sh), decode_split_len(sh),
                   kLog2e / sqrtf((float)sh.d), chan_map, cg};
   int maxmem = 0;
@@ -1161,11 +1269,11 @@ void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const Cha
 
 #define WM_INST(T)                                                                              \
   template void launch_attend_prefill<T>(const Shape&, const LayerTable&, const T*, const T*,   \
-                                         const T*, const T*, const T*, const int32_t*, T*,      \
-                                         hipStream_t);                                          \
+                                         const T*, const T*, const T*, const int32_t*,          \
+                                         const int32_t*, T*, hipStream_t);                      \
   template void launch_attend_decode<T>(const Shape&, const LayerTable&, const ChannelGroups&,  \
                                         const T*, const T*, const T*, const T*, const T*,       \
-                                        const int32_t*, float*, T*, hipStream_t);
+                                        const int32_t*, const int32_t*, float*, T*, hipStream_t);
 WM_INST(float)
 WM_INST(bf16)
 #undef WM_INST

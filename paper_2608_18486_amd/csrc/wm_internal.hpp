@@ -73,7 +73,7 @@ struct ChannelGroups {       // CSR inverse of the consumer -> channel map
 template <typename T>
 void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q,
                            const T* Kc, const T* Vc, const T* Kd, const T* Vd,
-                           const int32_t* ctx_len, T* O, hipStream_t s);
+                           const int32_t* ctx_len, const int32_t* doc, T* O, hipStream_t s);
 
 // Split-S decode for small T_new; partials live in the workspace.
 size_t decode_partials_bytes(const Shape& sh);
@@ -81,7 +81,8 @@ int decode_splits(const Shape& sh);
 template <typename T>
 void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const ChannelGroups& cg,
                           const T* Q, const T* Kc, const T* Vc, const T* Kd, const T* Vd,
-                          const int32_t* ctx_len, float* partials, T* O, hipStream_t s);
+                          const int32_t* ctx_len, const int32_t* doc, float* partials, T* O,
+                          hipStream_t s);
 
 // -- measurement helper ---------------------------------------------------------
 // blocks x 4 waves, each issuing 8 * iters independent 32x32x16 bf16 MFMAs.

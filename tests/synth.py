@@ -84,6 +84,17 @@ for _k in (1, 2, 4, 8, 12, 16):
         "paper_T2048_L16_k%d" % _k, 16, 2048, 16, _k, 512, 6, 3, 96, 0, "bf16",
         _map_mod(16, _k), p=2, seed=1100 + _k)
 del _k
+# The same passes with the document mask: each 2048-token row packs documents whose
+# lengths are 1 + an exponential draw of mean 511 (mean document 512 tokens), a seeded
+# stand-in for the paper's packed pretraining text (FineWeb-Edu, Section 5.1).
+DOC_MEAN = {}
+for _k in (8, 16):
+    _w = WORKLOADS["paper_T2048_L16_k%d" % _k]
+    _n = "paper_T2048_L16_k%d_docs" % _k
+    WORKLOADS[_n] = Workload(_n, _w.B, _w.T_new, _w.L, _w.k, _w.D, _w.Hq, _w.Hkv, _w.d, _w.ctx,
+                             _w.dtype, list(_w.chan_map), _w.p, _w.seed)
+    DOC_MEAN[_n] = 512.0
+del _k, _w, _n
 
 
 def small(name="small", B=2, T_new=40, L=5, k=3, D=96, Hq=4, Hkv=2, d=32, ctx=0,
@@ -163,6 +174,35 @@ def make_ctx_len(w: Workload, ragged: bool = False, sub: int = 23) -> torch.Tens
         return torch.full((w.B,), w.ctx, dtype=torch.int32)
     return torch.randint(0, w.ctx + 1, (w.B,), generator=_gen(w.seed * 100 + sub),
                          dtype=torch.int32)
+
+
+def make_doc_start(w: Workload, ctx_len=None, mean_len: float = 512.0, sub: int = 31,
+                   lengths=None) -> torch.Tensor:
+    """Packed documents: [B, T_new] int32, the position of the first token of the document
+    holding each new token (token i of sequence b sits at ctx_len[b] + i).
+
+    Each sequence is cut into documents from position 0 on, with lengths 1 + a seeded
+    exponential draw of mean `mean_len` - 1 (rounded down), or the given `lengths`
+    cycled (for hand-placed boundaries)."""
+    ctx = torch.zeros(w.B, dtype=torch.int32) if ctx_len is None else ctx_len.to(torch.int32)
+    g = _gen(w.seed * 100 + sub)
+    out = torch.empty((w.B, w.T_new), dtype=torch.int32)
+    for b in range(w.B):
+        end = int(ctx[b]) + w.T_new
+        starts = torch.empty(end, dtype=torch.int32)
+        pos, k = 0, 0
+        while pos < end:
+            if lengths is not None:
+                n = int(lengths[k % len(lengths)])
+            else:
+                e = torch.empty(1).exponential_(1.0 / max(mean_len - 1.0, 1e-6), generator=g)
+                n = 1 + int(e.item())
+            n = max(n, 1)
+            starts[pos:pos + n] = pos
+            pos += n
+            k += 1
+        out[b] = starts[int(ctx[b]):end]
+    return out
 
 
 def make_cache_cpu(w: Workload, sub: int = 24, fill=float("nan")):

@@ -129,6 +129,13 @@ def test_entry_points_reject_bad_pointers_before_launch(wm):
     assert _call(wm, "wm_q_project", d, good, None, None) == wm.ERR_ARG
     assert _call(wm, "wm_channel_attend", d, good, m, None, good, good, None) == wm.ERR_ARG
     assert _call(wm, "wm_layer_step", d, good, None, None, good, good, good) == wm.ERR_ARG
+    # document arrays: NULL or misaligned (the other arguments are valid)
+    assert _call(wm, "wm_channel_attend_doc", d, good, m, None, None, good, good, good) == \
+        wm.ERR_ARG
+    assert "doc_start" in wm.last_error()
+    assert _call(wm, "wm_layer_step_doc", d, good, m, None, good + 2, good, good, good) == \
+        wm.ERR_ARG
+    assert "doc_start" in wm.last_error()
     # NULL parameter
     bad = _fake_params(wm)
     bad["Wq"] = _FakeTensor(0)

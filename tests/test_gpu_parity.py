@@ -388,3 +388,112 @@ def test_read_calibration_runs(wm):
     wm.calibrate_read(buf, sink, torch.cuda.current_stream())
     torch.cuda.synchronize()
     assert float(sink.item()) == 0.0
+
+
+# ------------------------------------------------------------ document mask
+
+DOC_CASES = [  # (T_new, ctx, doc lengths or None for seeded lengths of mean 37)
+    (300, 0, None), (200, 0, [1]), (256, 0, [64]), (300, 0, [63, 65, 1, 128, 2]),
+    (129, 0, [300]), (40, 200, None), (3, 513, [100, 7]), (1, 1000, None), (1, 700, [1]),
+]
+
+
+@pytest.mark.parametrize("T_new,ctx,lengths", DOC_CASES)
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_channel_attend_doc(wm, T_new, ctx, lengths, mask_mode):
+    """Attention under the document mask (packed documents), every kernel path: bf16 head
+    dims 64 and 96 (the LDS-DMA prefill kernel), fp32 (the generic prefill kernel) and
+    decode (T_new <= 4), against the oracle row by row."""
+    for dtype, d in (("bf16", 64), ("f32", 32), ("bf16", 96)):
+        w = synth.small("doc_%s_d%d" % (dtype, d), B=2, T_new=T_new, L=5, k=3, D=64, Hq=4,
+                        Hkv=2, d=d, ctx=ctx + T_new, dtype=dtype, chan_map=[2, 0, 2, 2, 0])
+        print("doc case", dtype, d, T_new, ctx, lengths, mask_mode, flush=True)
+        P = synth.make_params(w, _bias(w))
+        Q = synth.make_queries(w)
+        Kc, Vc = synth.make_cache_cpu(w)
+        ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+        docs = synth.make_doc_start(w, ctx_len, mean_len=37.0, lengths=lengths)
+        Oo = oracle.channel_attend(_odims(w, mask_mode=mask_mode), P, Q, w.chan_map,
+                                   ctx_len.numpy(), _f64(Kc), _f64(Vc), doc_start=docs.numpy())
+        O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+        dims = _gdims(wm, w, mask_mode=mask_mode, ctx_max=ctx)
+        wm.channel_attend(dims, _dev(P), Q.cuda(), w.chan_map, ctx_len.cuda(), Kc.cuda(),
+                          Vc.cuda(), O, doc_start=docs.cuda())
+        torch.cuda.synchronize()
+        check_close(O, Oo, dtype, "doc %s d%d T%d ctx%d" % (dtype, d, T_new, ctx))
+
+
+@pytest.mark.parametrize("name", ["bf16_paper_shape", "c1_tiny_f32", "bf16_ragged_gqa"])
+def test_layer_step_doc(wm, name):
+    """The fused step with packed documents: the cache writes are the plain step's, the
+    outputs follow the document mask."""
+    w = SMALL[name]
+    rng = np.random.default_rng(w.seed)
+    P = synth.make_params(w, _bias(w) + rng.normal(0, 0.3, size=w.k * w.L))
+    H = synth.make_states(w)
+    docs = synth.make_doc_start(w, mean_len=9.0)
+    K0, V0 = synth.make_cache_cpu(w)
+    Ko, Vo = _f64(K0).copy(), _f64(V0).copy()
+    Oo = oracle.layer_step(_odims(w), P, H, w.chan_map, None, Ko, Vo, doc_start=docs.numpy())
+    Kg, Vg = K0.cuda(), V0.cuda()
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    wm.layer_step(_gdims(wm, w), _dev(P), H.cuda(), w.chan_map, None, Kg, Vg, O,
+                  doc_start=docs.cuda())
+    torch.cuda.synchronize()
+    ctx = np.zeros(w.B, dtype=np.int64)
+    _check_cache(Kg, Ko, K0, w, ctx, w.dtype, name + " doc K")
+    _check_cache(Vg, Vo, V0, w, ctx, w.dtype, name + " doc V")
+    check_close(O, Oo, w.dtype, name + " doc O")
+
+
+def test_doc_entry_points_reject_bad_doc_arrays(wm):
+    w = SMALL["bf16_ragged_gqa"]
+    dims = _gdims(wm, w)
+    P = _dev(synth.make_params(w, _bias(w)))
+    Q = torch.zeros((w.L, w.B, w.Hq, w.T_new, w.d), dtype=w.torch_dtype, device="cuda")
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    Kc = torch.zeros((w.k, w.B, w.Hkv, w.S_cap, w.d), dtype=w.torch_dtype, device="cuda")
+    raw = torch.zeros((4 * w.B * w.T_new + 4,), dtype=torch.uint8, device="cuda")
+    with pytest.raises(wm.WMError) as e:  # misaligned: no launch
+        wm.channel_attend(dims, P, Q, w.chan_map, None, Kc, Kc, O, doc_start=raw[1:])
+    assert e.value.code == wm.ERR_ARG
+
+
+@pytest.mark.parametrize("name", ["paper_T2048_L16_k8"])
+def test_full_sequence_doc_step_at_full_size(wm, name):
+    """The paper-shape pass with packed documents (mean length 512) as the benchmark runs
+    it; one sequence re-computed by the oracle (all its cache slots, sampled rows)."""
+    w = synth.WORKLOADS[name]
+    print("full doc", name, flush=True)
+    P = synth.make_params(w, _bias(w))
+    H = synth.make_states(w)
+    docs = synth.make_doc_start(w, mean_len=512.0)
+    Kg = torch.full((w.k, w.B, w.Hkv, w.S_cap, w.d), float("nan"), dtype=w.torch_dtype,
+                    device="cuda")
+    Vg = torch.full_like(Kg, float("nan"))
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    wm.layer_step(_gdims(wm, w), _dev(P), H.cuda(), w.chan_map, None, Kg, Vg, O,
+                  doc_start=docs.cuda())
+    torch.cuda.synchronize()
+    PP = oracle.Params(P)
+    b = w.B - 1
+    w1 = synth.Workload(w.name, 1, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, 0, w.dtype,
+                        w.chan_map, w.p, w.seed)
+    dm = _odims(w1)
+    Ko, Vo = oracle.empty_cache(dm)
+    oracle.pool(dm, PP, H[b:b + 1], None, Ko, Vo)
+    check_close(Kg[:, b:b + 1, :, :w.T_new], Ko[:, :, :, :w.T_new], w.dtype, name + " K")
+    rows = _sample_rows(w1, 0)
+    # rows at and just after each document start of the sequence, too
+    starts = sorted(set(docs[b].tolist()))
+    extra = sorted({t for s0 in starts for t in (s0, s0 + 1) if t < w.T_new})[:24]
+    rows = sorted(set(rows) | {(l * 1 + 0) * w.T_new + t for l in (0, w.L - 1) for t in extra})
+    toks = sorted({r % w.T_new for r in rows})
+    Qo = oracle.q_project(dm, PP, H[b:b + 1], None, toks)
+    Oo = oracle.channel_attend(dm, PP, Qo, w.chan_map, None, Ko, Vo, rows,
+                               doc_start=docs[b:b + 1].numpy())
+    g = O[:, b].float().cpu().numpy()
+    for l in sorted({r // w.T_new for r in rows}):
+        for t in toks:
+            if (l * w.T_new + t) in rows:
+                check_close(g[l, t], Oo[l, 0, t], w.dtype, "%s doc O l=%d t=%d" % (name, l, t))

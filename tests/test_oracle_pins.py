@@ -435,3 +435,86 @@ def test_inclusive_mask_is_shift_invariant(oracle_lib):
                                    V1[c, 0, kvh, 40:41 + t])
                 np.testing.assert_allclose(out, O0[l, 0, t, h * w.d:(h + 1) * w.d],
                                            rtol=1e-9, atol=1e-11)
+
+
+# ---------------------------------------------------------- document mask
+
+def _doc_case(o, mask_mode, ctx=0, lengths=None, mean_len=4.0, seed=21):
+    w = _small(L=3, k=2, T_new=13, B=2, Hq=4, Hkv=2, d=16, ctx=ctx, seed=seed)
+    P = synth.make_params(w, o.init_bias(w.L, w.k))
+    Q = synth.make_queries(w)
+    Kc, Vc = synth.make_cache_cpu(w, fill=0.0)
+    rng = np.random.default_rng(seed)
+    Kc = torch.as_tensor(rng.normal(size=Kc.shape))  # every slot finite and distinct
+    Vc = torch.as_tensor(rng.normal(size=Vc.shape))
+    ctx_len = np.array([ctx, max(ctx - 3, 0)], dtype=np.int32)
+    docs = synth.make_doc_start(w, torch.as_tensor(ctx_len), mean_len=mean_len,
+                                lengths=lengths).numpy()
+    dm = _dims(o, w, mask_mode=mask_mode)
+    return w, P, Q, Kc, Vc, ctx_len, docs, dm
+
+
+@pytest.mark.parametrize("mask_mode", [0, 1])
+@pytest.mark.parametrize("ctx", [0, 9])
+def test_document_mask_matches_sdpa_with_block_mask(oracle_lib, mask_mode, ctx):
+    """Packed documents (Section 5.1): each row against torch SDPA (float64) over the dummy
+    slot (paper mask) and the cached slots of its own document before (or at) it."""
+    o = oracle_lib
+    w, P, Q, Kc, Vc, ctx_len, docs, dm = _doc_case(o, mask_mode, ctx)
+    O = o.channel_attend(dm, P, Q, w.chan_map, ctx_len, Kc, Vc, doc_start=docs)
+    Qd, Kd, Vd = Q.double(), P["Kd"].double(), P["Vd"].double()
+    paper = mask_mode == 0
+    for l in range(w.L):
+        c = w.chan_map[l]
+        for b in range(w.B):
+            for i in range(w.T_new):
+                pos = int(ctx_len[b]) + i
+                for h in range(w.Hq):
+                    kv = h // (w.Hq // w.Hkv)
+                    K = Kc[c, b, kv].double()
+                    V = Vc[c, b, kv].double()
+                    mask = torch.zeros(w.S_cap, dtype=torch.bool)
+                    mask[docs[b, i]:pos + (0 if paper else 1)] = True
+                    if paper:
+                        K = torch.cat([Kd[c, kv][None], K])
+                        V = torch.cat([Vd[c, kv][None], V])
+                        mask = torch.cat([torch.ones(1, dtype=torch.bool), mask])
+                    ref = F.scaled_dot_product_attention(Qd[l, b, h, i][None, None], K[None],
+                                                         V[None], attn_mask=mask[None, None])
+                    np.testing.assert_allclose(O[l, b, i, h * w.d:(h + 1) * w.d],
+                                               ref[0, 0].numpy(), rtol=1e-12, atol=1e-13)
+
+
+def test_document_mask_with_one_document_is_no_mask(oracle_lib):
+    o = oracle_lib
+    w, P, Q, Kc, Vc, ctx_len, docs, dm = _doc_case(o, 0, ctx=9)
+    zero = np.zeros_like(docs)
+    np.testing.assert_array_equal(o.channel_attend(dm, P, Q, w.chan_map, ctx_len, Kc, Vc,
+                                                   doc_start=zero),
+                                  o.channel_attend(dm, P, Q, w.chan_map, ctx_len, Kc, Vc))
+
+
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_document_mask_ignores_other_documents(oracle_lib, mask_mode):
+    """Changing every cached slot before a row's document leaves the row unchanged, and
+    the first token of a document reads only the dummy (paper mask) or only itself."""
+    o = oracle_lib
+    w, P, Q, Kc, Vc, ctx_len, docs, dm = _doc_case(o, mask_mode, ctx=9, lengths=[5, 1, 7, 2])
+    O = o.channel_attend(dm, P, Q, w.chan_map, ctx_len, Kc, Vc, doc_start=docs)
+    rng = np.random.default_rng(5)
+    for b in range(w.B):
+        for i in range(w.T_new):
+            K2, V2 = Kc.clone(), Vc.clone()
+            lo = int(docs[b, i])
+            K2[:, b, :, :lo] = torch.as_tensor(rng.normal(size=K2[:, b, :, :lo].shape))
+            V2[:, b, :, :lo] = torch.as_tensor(rng.normal(size=V2[:, b, :, :lo].shape))
+            O2 = o.channel_attend(dm, P, Q, w.chan_map, ctx_len, K2, V2, doc_start=docs)
+            np.testing.assert_array_equal(O2[:, b, i], O[:, b, i])
+            if lo == int(ctx_len[b]) + i:  # first token of its document
+                for l in range(w.L):
+                    for h in range(w.Hq):
+                        kv = h // 2
+                        want = (P["Vd"][w.chan_map[l], kv] if mask_mode == 0
+                                else Vc[w.chan_map[l], b, kv, lo]).double().numpy()
+                        np.testing.assert_allclose(O[l, b, i, h * w.d:(h + 1) * w.d], want,
+                                                   rtol=1e-13, atol=1e-14)
