@@ -21,6 +21,7 @@ import ctypes
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -165,12 +166,22 @@ class HipEvents:
 
 # ------------------------------------------------------------ traffic
 
+def _strip_comments(src: str) -> str:
+    """The code of a C++/HIP source without its comments and blank lines (string literals
+    in these sources hold no comment markers)."""
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return "\n".join(ln.rstrip() for ln in src.splitlines() if ln.strip())
+
+
 def _kernel_source_hash():
+    """Hash of the library's code (comments and blank lines excluded), so counters taken on
+    one build stay attached to it until the code itself changes."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_18486_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode() + f.read())
+        with open(os.path.join(csrc, name), encoding="utf-8") as f:
+            h.update(name.encode() + _strip_comments(f.read()).encode())
     return h.hexdigest()[:16]
 
 

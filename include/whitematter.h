@@ -171,7 +171,7 @@ int wm_layer_step(const wm_dims *dims, const wm_params *params, const void *H,
                   const int32_t *chan_map, const int32_t *ctx_len, void *Kc, void *Vc,
                   void *O, void *ws, size_t ws_bytes, wm_stream_t stream);
 
-/* Document mask (Section 5.1: sequences packed from several documents, attention
+/* Document mask (Section 4.1: sequences packed from several documents, attention
  * confined to each document). Same as wm_channel_attend / wm_layer_step, plus
  *   doc_start device int32 [B][T_new], 4-byte aligned, not NULL: the position of
  *             the first token of the document that holds token i of sequence b

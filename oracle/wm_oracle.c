@@ -467,7 +467,7 @@ void wmo_q_project(const wmo_dims *dm, const wmo_params *P, const double *H, con
 
 /* Step 3: consumer l reads channel map[l]. A row r = (l*B + b)*T_new + i
  * produces O[l][b][i][0 .. Hq*d).
- * Document mask (Section 5.1, sequences packed from several documents): when
+ * Document mask (Section 4.1, sequences packed from several documents): when
  * doc_start is given ([B][T_new], the position of the first token of the
  * document holding token i), the row reads only cached slots at or after that
  * position; the learned dummy slot stays visible to every row. Values outside

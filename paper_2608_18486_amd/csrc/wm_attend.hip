@@ -49,7 +49,7 @@ constexpr float kGrowSum = 65536.0f;
 // exact-max rescale, which then sets a real reference.
 constexpr float kNoRef = -100.0f;
 
-// Document mask (packed sequences, Section 5.1): query i of sequence b, at position
+// Document mask (packed sequences, Section 4.1): query i of sequence b, at position
 // ctx + i, reads cached slots from its document's first position on (clamped into
 // [0, position]); the dummy slot stays visible. Without a document array every row
 // starts at slot 0.

@@ -75,10 +75,10 @@ WORKLOADS = {
     "c5_decode_S32768": Workload("c5_decode_S32768", 64, 1, 24, 12, 1024, 16, 16, 64, 32768,
                                  "bf16", _map_mod(24, 12), seed=1005),
 }
-# The paper's own model shape (Section 5.1): L = 16, D = 512, 6 query and 3 KV heads of
+# The paper's own model shape (Section 4.1): L = 16, D = 512, 6 query and 3 KV heads of
 # dimension 96, routers reading every second source layer (p = 2), sequences packed to
 # 2048 tokens, 16 sequences (a global batch of 128 over 8 GPUs), fixed selection
-# l -> l mod k, for the channel counts of the compression study (Section 5.4).
+# l -> l mod k, for the channel counts of the compression study (Section 5.2).
 for _k in (1, 2, 4, 8, 12, 16):
     WORKLOADS["paper_T2048_L16_k%d" % _k] = Workload(
         "paper_T2048_L16_k%d" % _k, 16, 2048, 16, _k, 512, 6, 3, 96, 0, "bf16",
@@ -86,7 +86,7 @@ for _k in (1, 2, 4, 8, 12, 16):
 del _k
 # The same passes with the document mask: each 2048-token row packs documents whose
 # lengths are 1 + an exponential draw of mean 511 (mean document 512 tokens), a seeded
-# stand-in for the paper's packed pretraining text (FineWeb-Edu, Section 5.1).
+# stand-in for the paper's packed pretraining text (FineWeb-Edu, Section 4.1).
 DOC_MEAN = {}
 for _k in (8, 16):
     _w = WORKLOADS["paper_T2048_L16_k%d" % _k]

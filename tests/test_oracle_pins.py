@@ -457,7 +457,7 @@ def _doc_case(o, mask_mode, ctx=0, lengths=None, mean_len=4.0, seed=21):
 @pytest.mark.parametrize("mask_mode", [0, 1])
 @pytest.mark.parametrize("ctx", [0, 9])
 def test_document_mask_matches_sdpa_with_block_mask(oracle_lib, mask_mode, ctx):
-    """Packed documents (Section 5.1): each row against torch SDPA (float64) over the dummy
+    """Packed documents (Section 4.1): each row against torch SDPA (float64) over the dummy
     slot (paper mask) and the cached slots of its own document before (or at) it."""
     o = oracle_lib
     w, P, Q, Kc, Vc, ctx_len, docs, dm = _doc_case(o, mask_mode, ctx)
