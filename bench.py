@@ -43,6 +43,13 @@ for _k in (1, 2, 4, 8, 12, 16):
     WORKLOAD_LABEL["paper_T2048_L16_k%d" % _k] = (
         "full-sequence pass, the paper's model shape: B16 T2048 L16 k%d D512 6q/3kv x96, p2, "
         "bf16, map l->l%%%d" % (_k, _k))
+for _k, _tag, _what in ((16, "static", "static mixing weights, no router"),
+                        (1, "static", "static mixing weights, no router"),
+                        (16, "nofeedback", "no deep-to-shallow feedback")):
+    WORKLOAD_LABEL["paper_T2048_L16_k%d_%s" % (_k, _tag)] = (
+        "full-sequence pass, the paper's model shape, ablation: %s: B16 T2048 L16 k%d D512 "
+        "6q/3kv x96, p2, bf16, map l->l%%%d" % (_what, _k, _k))
+del _tag, _what
 for _k in (8, 16):
     WORKLOAD_LABEL["paper_T2048_L16_k%d_docs" % _k] = (
         "full-sequence pass, the paper's model shape with the document mask (packed documents "
@@ -90,19 +97,32 @@ def visible_pairs(w, docs=None):
     return int((pos - np.asarray(docs) + 1).sum())
 
 
+def router_mode_of(w):
+    from tests import synth
+    return synth.ROUTER_MODE.get(w.name, 0)
+
+
 def phase_costs(w, docs=None):
     """Per-phase (flops, HBM bytes) of one step."""
     es = 4 if w.dtype == "f32" else 2
     N, L, k, D, Hq, Hkv, d, p = w.N, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.p
     Lp = (L + p - 1) // p
+    mode = router_mode_of(w)
+    if mode == 1:     # static weights: no router
+        router = (0, 0)
+    elif mode == 2:   # no feedback: channel j's router reads the stacked layers <= j
+        sel = [L - 1 - p * m for m in range(Lp)]
+        blocks = sum(sum(1 for s in sel if s <= j) for j in range(k))
+        router = (N * 4 * L * blocks * D, N * Lp * D * es + 2 * L * blocks * D * es)
+    else:
+        router = (N * router_flops_per_token(L, k, D, p), N * Lp * D * es + 2 * k * L * Lp * D * es)
     H_bytes = N * L * D * es
     cache_write = 2 * k * N * Hkv * d * es
     used = len(set(w.chan_map))
     cache_read = 2 * used * w.B * Hkv * (w.ctx + w.T_new) * d * es
     return {
         "norms": (0, H_bytes),
-        "router": (N * router_flops_per_token(L, k, D, p),
-                   N * Lp * D * es + 2 * k * L * Lp * D * es),
+        "router": router,
         "mix": (N * mix_flops_per_token(L, k, D), H_bytes + 2 * k * N * D * es),
         "kv_project": (N * kv_flops_per_token(k, Hkv, d, D),
                        2 * k * N * D * es + 2 * k * Hkv * d * D * es + cache_write),
@@ -115,7 +135,8 @@ def phase_costs(w, docs=None):
 
 def step_cost(w, docs=None):
     c = phase_costs(w, docs)
-    min_bytes = (w.N * w.L * w.D + 2 * w.k * w.L * ((w.L + w.p - 1) // w.p) * w.D
+    router_w = 0 if router_mode_of(w) == 1 else 2 * w.k * w.L * ((w.L + w.p - 1) // w.p) * w.D
+    min_bytes = (w.N * w.L * w.D + router_w
                  + 2 * w.k * w.Hkv * w.d * w.D + w.L * w.Hq * w.d * w.D) * (
         4 if w.dtype == "f32" else 2)
     es = 4 if w.dtype == "f32" else 2
@@ -215,7 +236,7 @@ def cpu_baseline(w, P, H_cpu, cache_dev, docs=None):
     w1 = synth.Workload(w.name, nseq, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.ctx, w.dtype,
                         w.chan_map, w.p, w.seed)
     dm = oracle.Dims(B=nseq, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d,
-                     p=w.p, S_cap=w.ctx + w.T_new)
+                     p=w.p, S_cap=w.ctx + w.T_new, router_mode=router_mode_of(w))
     PP = oracle.Params(P)
     Kc, Vc = oracle.empty_cache(dm)
     if w.ctx:
@@ -319,7 +340,8 @@ def main():
     docs = docs_cpu.to(dev) if docs_cpu is not None else None
     O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device=dev)
     dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p, S_cap=w.S_cap,
-                        ctx_max=w.ctx, dtype=wm.dtype_code(w.torch_dtype))
+                        ctx_max=w.ctx, dtype=wm.dtype_code(w.torch_dtype),
+                        router_mode=router_mode_of(w))
     ws = wm.workspace(dims, wm.OP_LAYER_STEP, dev)
     stream = torch.cuda.current_stream(dev)
 

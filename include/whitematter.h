@@ -63,6 +63,16 @@ enum wm_mix_mode { WM_MIX_LINEAR = 0, WM_MIX_SOFTMAX = 1 };
  * dummy). */
 enum wm_mask_mode { WM_MASK_PAPER = 0, WM_MASK_INCLUSIVE = 1 };
 
+/* Where the mixing weights come from (the ablations of Section 5.3):
+ *   WM_ROUTER_DYNAMIC    the paper's content-dependent router (Section 3.1 Step 1)
+ *   WM_ROUTER_STATIC     static learnable weights, no router: alpha[j][l] = b_alpha[j*L + l]
+ *                        for every token (W_alpha is not read)
+ *   WM_ROUTER_NOFEEDBACK no deep-to-shallow feedback: requires k = L; channel j mixes
+ *                        source layers 0..j only (weights on deeper layers are 0, or left
+ *                        out of the softmax), and its router reads only the stacked states
+ *                        of layers <= j (W_alpha entries on deeper layers are not used). */
+enum wm_router_mode { WM_ROUTER_DYNAMIC = 0, WM_ROUTER_STATIC = 1, WM_ROUTER_NOFEEDBACK = 2 };
+
 enum wm_op {
   WM_OP_ROUTER_MIX = 0,
   WM_OP_KV_PROJECT = 1,
@@ -90,6 +100,7 @@ typedef struct wm_dims {
   int32_t dtype;     /* enum wm_dtype */
   int32_t mix_mode;  /* enum wm_mix_mode */
   int32_t mask_mode; /* enum wm_mask_mode */
+  int32_t router_mode; /* enum wm_router_mode */
   float eps;         /* RMSNorm epsilon (e.g. 1e-6) */
   float rope_theta;  /* RoPE base (e.g. 1e6) */
 } wm_dims;

@@ -32,6 +32,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 MIX_LINEAR, MIX_SOFTMAX = 0, 1
 MASK_PAPER, MASK_INCLUSIVE = 0, 1
+ROUTER_DYNAMIC, ROUTER_STATIC, ROUTER_NOFEEDBACK = 0, 1, 2
 
 PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
                "Kd", "Vd", "g_in", "Wq", "g_qnorm")
@@ -50,7 +51,7 @@ def build(force: bool = True) -> str:
 class _Dims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in
                 ("B", "T_new", "L", "k", "D", "Hq", "Hkv", "d", "p", "S_cap",
-                 "mix_mode", "mask_mode")] + [("eps", ctypes.c_double),
+                 "mix_mode", "mask_mode", "router_mode")] + [("eps", ctypes.c_double),
                                               ("rope_theta", ctypes.c_double)]
 
 
@@ -84,6 +85,7 @@ class Dims:
     S_cap: int = 0
     mix_mode: int = MIX_LINEAR
     mask_mode: int = MASK_PAPER
+    router_mode: int = ROUTER_DYNAMIC
     eps: float = 1e-6
     rope_theta: float = 1e6
 
@@ -97,8 +99,8 @@ class Dims:
 
     def c(self) -> _Dims:
         return _Dims(self.B, self.T_new, self.L, self.k, self.D, self.Hq, self.Hkv, self.d,
-                     self.p, self.S_cap, self.mix_mode, self.mask_mode, self.eps,
-                     self.rope_theta)
+                     self.p, self.S_cap, self.mix_mode, self.mask_mode, self.router_mode,
+                     self.eps, self.rope_theta)
 
 
 def _f64(a) -> np.ndarray:

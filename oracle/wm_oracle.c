@@ -40,10 +40,17 @@
 #define WMO_MIX_SOFTMAX 1
 #define WMO_MASK_PAPER 0
 #define WMO_MASK_INCLUSIVE 1
+/* Router variants (Section 5.3, ablation studies): the paper's content-dependent router;
+ * static learnable mixing weights (alpha = b, no router); no deep-to-shallow feedback
+ * (k = L, channel j is built from source layers 0..j only, its router reading only
+ * those layers). */
+#define WMO_ROUTER_DYNAMIC 0
+#define WMO_ROUTER_STATIC 1
+#define WMO_ROUTER_NOFEEDBACK 2
 
 typedef struct {
     int B, T_new, L, k, D, Hq, Hkv, d, p, S_cap;
-    int mix_mode, mask_mode;
+    int mix_mode, mask_mode, router_mode;
     double eps, rope_theta;
 } wmo_dims;
 
@@ -171,27 +178,38 @@ void wmo_pool_mix_token(const wmo_dims *dm, const wmo_params *P, const double *h
         const double *W = P->W_alpha + (size_t)br * k * L * Lp * D;
         const double *bias = P->b_alpha + (size_t)br * k * L;
         double *al = alpha + (size_t)br * k * L;
+        int nofb = dm->router_mode == WMO_ROUTER_NOFEEDBACK;
         for (int o = 0; o < k * L; ++o) {
+            int j = o / L;
             double a = bias[o];
-            for (int m = 0; m < Lp; ++m) {
-                const double *x = hn + (size_t)sel[m] * D;
-                const double *w = W + (size_t)o * Lp * D + (size_t)m * D;
-                for (int e = 0; e < D; ++e)
-                    a += w[e] * x[e];
+            if (dm->router_mode != WMO_ROUTER_STATIC) {
+                for (int m = 0; m < Lp; ++m) {
+                    if (nofb && sel[m] > j)
+                        continue; /* channel j's router reads source layers <= j only */
+                    const double *x = hn + (size_t)sel[m] * D;
+                    const double *w = W + (size_t)o * Lp * D + (size_t)m * D;
+                    for (int e = 0; e < D; ++e)
+                        a += w[e] * x[e];
+                }
             }
             al[o] = a; /* alpha[j][l] with o = j*L + l */
         }
-        if (dm->mix_mode == WMO_MIX_SOFTMAX) {
-            for (int j = 0; j < k; ++j) {
-                double *row = al + (size_t)j * L, mx = row[0], s = 0.0;
-                for (int l = 1; l < L; ++l)
+        /* sources a channel may mix: all L, or 0..j without feedback */
+        for (int j = 0; j < k; ++j) {
+            int nl = nofb ? j + 1 : L;
+            double *row = al + (size_t)j * L;
+            if (dm->mix_mode == WMO_MIX_SOFTMAX) {
+                double mx = row[0], s = 0.0;
+                for (int l = 1; l < nl; ++l)
                     if (row[l] > mx)
                         mx = row[l];
-                for (int l = 0; l < L; ++l)
+                for (int l = 0; l < nl; ++l)
                     s += exp(row[l] - mx);
-                for (int l = 0; l < L; ++l)
+                for (int l = 0; l < nl; ++l)
                     row[l] = exp(row[l] - mx) / s;
             }
+            for (int l = nl; l < L; ++l)
+                row[l] = 0.0;
         }
         /* each channel is the alpha-weighted sum of the normed states */
         for (int j = 0; j < k; ++j) {

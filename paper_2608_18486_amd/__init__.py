@@ -22,6 +22,7 @@ OK, ERR_ARG, ERR_SHAPE, ERR_DTYPE, ERR_MAP, ERR_CAPACITY, ERR_WORKSPACE, ERR_LAU
 F32, BF16 = 0, 1
 MIX_LINEAR, MIX_SOFTMAX = 0, 1
 MASK_PAPER, MASK_INCLUSIVE = 0, 1
+ROUTER_DYNAMIC, ROUTER_STATIC, ROUTER_NOFEEDBACK = 0, 1, 2
 OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP = range(5)
 
 PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
@@ -37,7 +38,7 @@ class WMError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("B", "T_new", "L", "k", "D", "Hq", "Hkv", "d", "p", "S_cap", "ctx_max",
-                 "dtype", "mix_mode", "mask_mode")] + [("eps", ctypes.c_float),
+                 "dtype", "mix_mode", "mask_mode", "router_mode")] + [("eps", ctypes.c_float),
                                                        ("rope_theta", ctypes.c_float)]
 
     @property
@@ -106,9 +107,10 @@ def _check(rc: int):
 
 
 def make_dims(B, T_new, L, k, D, Hq, Hkv, d, p=1, S_cap=0, ctx_max=0, dtype=BF16,
-              mix_mode=MIX_LINEAR, mask_mode=MASK_PAPER, eps=1e-6, rope_theta=1e6) -> Dims:
+              mix_mode=MIX_LINEAR, mask_mode=MASK_PAPER, eps=1e-6, rope_theta=1e6,
+              router_mode=ROUTER_DYNAMIC) -> Dims:
     return Dims(B, T_new, L, k, D, Hq, Hkv, d, p, S_cap, ctx_max, dtype, mix_mode, mask_mode,
-                eps, rope_theta)
+                router_mode, eps, rope_theta)
 
 
 def dtype_code(t: torch.dtype) -> int:

@@ -50,6 +50,7 @@ wm::Shape make_shape(const wm_dims& d) {
   s.S_cap = d.S_cap;
   s.mix_softmax = d.mix_mode == WM_MIX_SOFTMAX;
   s.mask_paper = d.mask_mode == WM_MASK_PAPER;
+  s.router_mode = d.router_mode;
   s.eps = d.eps;
   s.rope_theta = d.rope_theta;
   s.ctx_max = d.ctx_max;
@@ -99,9 +100,13 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
     return fail(WM_ERR_DTYPE, "unknown mix_mode %d", d.mix_mode);
   if (d.mask_mode != WM_MASK_PAPER && d.mask_mode != WM_MASK_INCLUSIVE)
     return fail(WM_ERR_DTYPE, "unknown mask_mode %d", d.mask_mode);
+  if (d.router_mode < WM_ROUTER_DYNAMIC || d.router_mode > WM_ROUTER_NOFEEDBACK)
+    return fail(WM_ERR_DTYPE, "unknown router_mode %d", d.router_mode);
   if (d.B < 0 || d.T_new < 0) return fail(WM_ERR_ARG, "B and T_new must be >= 0");
   if (d.L < 1 || d.L > wm::kMaxLayers) return fail(WM_ERR_SHAPE, "L must be in [1, %d]", wm::kMaxLayers);
   if (d.k < 1 || d.k > d.L) return fail(WM_ERR_SHAPE, "k must be in [1, L]");
+  if (d.router_mode == WM_ROUTER_NOFEEDBACK && d.k != d.L)
+    return fail(WM_ERR_SHAPE, "router_mode WM_ROUTER_NOFEEDBACK needs k = L");
   if (d.D < 32 || d.D % 32 != 0) return fail(WM_ERR_SHAPE, "D must be a positive multiple of 32");
   if (d.Hq < 1 || d.Hkv < 1 || d.Hq % d.Hkv != 0)
     return fail(WM_ERR_SHAPE, "Hq must be a positive multiple of Hkv");
@@ -380,7 +385,8 @@ int wm_router_mix(const wm_dims* dims, const wm_params* params, const void* H, f
   WM_TRY(validate_dims(dims, WM_OP_ROUTER_MIX, nullptr));
   const wm_dims& d = *dims;
   if ((size_t)d.B * d.T_new == 0) return WM_OK;
-  WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA}));
+  if (d.router_mode == WM_ROUTER_STATIC) WM_TRY(check_params(params, {P_GPRE, P_BA}));
+  else WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA}));
   WM_TRY(need_ptr(H, "H"));
   WM_TRY(need_ptr(mixed_out, "mixed_out"));
   if (alpha_out && (uintptr_t)alpha_out % 16) return fail(WM_ERR_ARG, "alpha_out is not 16-byte aligned");
@@ -484,8 +490,12 @@ static int layer_step_impl(const wm_dims* dims, const wm_params* params, const v
   WM_TRY(validate_dims(dims, WM_OP_LAYER_STEP, chan_map));
   const wm_dims& d = *dims;
   if ((size_t)d.B * d.T_new == 0) return WM_OK;
-  WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD,
-                               P_GIN, P_WQ, P_GQN}));
+  if (d.router_mode == WM_ROUTER_STATIC)  // W_alpha is not read
+    WM_TRY(check_params(params, {P_GPRE, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD, P_GIN,
+                                 P_WQ, P_GQN}));
+  else
+    WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD,
+                                 P_GIN, P_WQ, P_GQN}));
   WM_TRY(need_ptr(H, "H"));
   WM_TRY(need_ptr(Kc, "Kc"));
   WM_TRY(need_ptr(Vc, "Vc"));

@@ -16,6 +16,7 @@ struct Shape {
   int B, T_new, L, k, D, Hq, Hkv, d, p, Lp, S_cap;
   int mix_softmax;   // 1: softmax over source layers per channel row
   int mask_paper;    // 1: dummy slot + strictly earlier slots; 0: slots <= own position
+  int router_mode;   // 0 content-dependent router, 1 static weights (alpha = b), 2 no feedback
   float eps, rope_theta;
   int ctx_max;       // host-side bound on ctx_len[b] (sizes the attention grid)
   __host__ __device__ int N() const { return B * T_new; }

@@ -431,10 +431,12 @@ __global__ __launch_bounds__(256) void router_reduce_kernel(const float* part, c
 
 // Router weights with the pre-mix gain folded in: Wf[o][m D + e] =
 // W_alpha[o][m D + e] * g_pre[o / kL][sel[m]][e], o over both branches.
+// Without feedback (nofb), the row of channel j = (o mod kL) / L reads only the stacked
+// blocks of layers <= j: the other blocks of its folded weights are zero.
 template <typename T>
 __global__ __launch_bounds__(256) void router_fold_kernel(const T* W, const T* g_pre,
                                                           LayerTable sel, int kL, int L, int Lp,
-                                                          int D, T* Wf) {
+                                                          int D, int nofb, T* Wf) {
   const long idx = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
   const long K = (long)Lp * D, total = 2 * kL * K;
   if (idx >= total) return;
@@ -444,9 +446,20 @@ __global__ __launch_bounds__(256) void router_fold_kernel(const T* W, const T* g
   float wv[8], gv[8];
   load8(W + idx, wv);
   load8(g_pre + ((long)(o / kL) * L + sel.v[m]) * D + e, gv);
+  const float keep = nofb && sel.v[m] > (o % kL) / L ? 0.f : 1.f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) wv[i] *= gv[i];
+  for (int i = 0; i < 8; ++i) wv[i] *= gv[i] * keep;
   store8(Wf + idx, wv);
+}
+
+// Static mixing weights: logits[br][n][o] = b_alpha[br][o] for every token.
+template <typename T>
+__global__ __launch_bounds__(256) void alpha_static_kernel(const T* b_alpha, int N, int kL,
+                                                           float* logits) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= 2L * N * kL) return;
+  const int o = (int)(idx % kL), br = (int)(idx / ((long)N * kL));
+  logits[idx] = to_f32(b_alpha[(long)br * kL + o]);
 }
 
 template <class C> static unsigned proj_blocks(int M, int Nout, int groups) {
@@ -555,9 +568,16 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
                    float* part, hipStream_t s) {
   const int M = sh.N();
   if (M <= 0) return;
+  if (sh.router_mode == 1) {  // static weights: no router, the logits are the bias
+    const long n = 2L * M * sh.k * sh.L;
+    hipLaunchKernelGGL(alpha_static_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       b_alpha, M, sh.k * sh.L, logits);
+    return;
+  }
   const long total = (long)router_fold_elems(sh) / 8;
   hipLaunchKernelGGL(router_fold_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
-                     s, W_alpha, g_pre, sel, sh.k * sh.L, sh.L, sh.Lp, sh.D, wfold);
+                     s, W_alpha, g_pre, sel, sh.k * sh.L, sh.L, sh.Lp, sh.D,
+                     sh.router_mode == 2 ? 1 : 0, wfold);
   if (M <= kFewTokens) router_gemm<T, true>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
   else router_gemm<T, false>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
 }
@@ -605,15 +625,7 @@ __global__ __launch_bounds__(128) void mix_kernel(Shape sh, const T* __restrict_
   __syncthreads();
   if (tid < 2 * k) {
     int br = tid / k, j = tid - br * k;
-    float* row = alpha + ((long)br * N + n) * k * L + (long)j * L;
-    if (sh.mix_softmax) {
-      float mx = row[0];
-      for (int l = 1; l < L; ++l) mx = fmaxf(mx, row[l]);
-      float z = 0.f;
-      for (int l = 0; l < L; ++l) z += expf(row[l] - mx);
-      float iz = 1.0f / z;
-      for (int l = 0; l < L; ++l) row[l] = expf(row[l] - mx) * iz;
-    }
+    const float* row = alpha + ((long)br * N + n) * k * L + (long)j * L;  // final weights
     for (int l = 0; l < L; ++l) coef[((long)br * L + l) * kp + j] = row[l] * rinv[n * L + l];
   }
   __syncthreads();
@@ -930,17 +942,33 @@ __global__ __launch_bounds__(NT) void mix_mfma_kernel(Shape sh, const bf16* __re
   }
 }
 
-// alpha[r][0..L) <- softmax over the row, for rows r < rows (in place)
-__global__ __launch_bounds__(256) void softmax_rows_kernel(float* alpha, long rows, int L) {
+// Mixing weights from the router logits, per channel row alpha[r][0..L) (r = (br N + n) k
+// + j), in place: without feedback the row keeps layers 0..j only (the rest set to 0);
+// in softmax mode the kept entries are normalised by a softmax.
+__global__ __launch_bounds__(256) void alpha_rows_kernel(float* alpha, long rows, int k, int L,
+                                                         int softmax, int nofb) {
   const long r = (long)blockIdx.x * 256 + threadIdx.x;
   if (r >= rows) return;
   float* row = alpha + r * L;
-  float mx = row[0];
-  for (int l = 1; l < L; ++l) mx = fmaxf(mx, row[l]);
-  float z = 0.f;
-  for (int l = 0; l < L; ++l) z += expf(row[l] - mx);
-  const float iz = 1.0f / z;
-  for (int l = 0; l < L; ++l) row[l] = expf(row[l] - mx) * iz;
+  const int nl = nofb ? (int)(r % k) + 1 : L;
+  if (softmax) {
+    float mx = row[0];
+    for (int l = 1; l < nl; ++l) mx = fmaxf(mx, row[l]);
+    float z = 0.f;
+    for (int l = 0; l < nl; ++l) z += expf(row[l] - mx);
+    const float iz = 1.0f / z;
+    for (int l = 0; l < nl; ++l) row[l] = expf(row[l] - mx) * iz;
+  }
+  for (int l = nl; l < L; ++l) row[l] = 0.f;
+}
+
+// The weights the mix applies, from the router output (see alpha_rows_kernel).
+static void finish_alpha(const Shape& sh, float* alpha, hipStream_t s) {
+  const bool nofb = sh.router_mode == 2;
+  if (!sh.mix_softmax && !nofb) return;
+  const long rows = 2L * sh.N() * sh.k;
+  hipLaunchKernelGGL(alpha_rows_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s,
+                     alpha, rows, sh.k, sh.L, sh.mix_softmax, nofb ? 1 : 0);
 }
 
 template <int JT, int LT>
@@ -948,11 +976,6 @@ static void mix_mfma_launch(const Shape& sh, const bf16* H, const float* rinv, c
                             float* alpha, bf16* mixed, float* rinv_mid, hipStream_t s) {
   const int nt = mix_threads(sh.L, sh.D);
   const int nch = (sh.L * (sh.D / 8) + nt - 1) / nt;
-  if (sh.mix_softmax) {
-    const long rows = 2L * sh.N() * sh.k;
-    hipLaunchKernelGGL(softmax_rows_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s,
-                       alpha, rows, sh.L);
-  }
   // tokens per block: up to kMixTok, fewer when that would leave under ~2048 blocks
   const int tpb = std::max(1, std::min(kMixTok, sh.N() / 2048));
   const dim3 grid((sh.N() + tpb - 1) / tpb), block(nt);
@@ -987,6 +1010,7 @@ template <typename T>
 void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
                 T* mixed, float* rinv_mid, hipStream_t s) {
   if (sh.N() <= 0) return;
+  finish_alpha(sh, alpha, s);
   if constexpr (sizeof(T) == 2) {
     if (mix_mfma_fits(sh)) {
       const bool jt1 = sh.k <= 16, lt1 = sh.L <= 16;

@@ -94,7 +94,16 @@ for _k in (8, 16):
     WORKLOADS[_n] = Workload(_n, _w.B, _w.T_new, _w.L, _w.k, _w.D, _w.Hq, _w.Hkv, _w.d, _w.ctx,
                              _w.dtype, list(_w.chan_map), _w.p, _w.seed)
     DOC_MEAN[_n] = 512.0
-del _k, _w, _n
+# The ablations of Section 5.3 at the paper's shape: static mixing weights (k = 16 and
+# k = 1) and no deep-to-shallow feedback (k = L = 16).
+ROUTER_MODE = {}
+for _k, _mode, _tag in ((16, 1, "static"), (1, 1, "static"), (16, 2, "nofeedback")):
+    _w = WORKLOADS["paper_T2048_L16_k%d" % _k]
+    _n = "paper_T2048_L16_k%d_%s" % (_k, _tag)
+    WORKLOADS[_n] = Workload(_n, _w.B, _w.T_new, _w.L, _w.k, _w.D, _w.Hq, _w.Hkv, _w.d, _w.ctx,
+                             _w.dtype, list(_w.chan_map), _w.p, _w.seed)
+    ROUTER_MODE[_n] = _mode
+del _k, _w, _n, _mode, _tag
 
 
 def small(name="small", B=2, T_new=40, L=5, k=3, D=96, Hq=4, Hkv=2, d=32, ctx=0,

@@ -50,6 +50,7 @@ def _dims(wm, **kw):
     (dict(d=128), "ERR_SHAPE"), (dict(d=96, dtype=0), "ERR_SHAPE"), (dict(d=80), "ERR_SHAPE"),
     (dict(p=0), "ERR_SHAPE"), (dict(p=5), "ERR_SHAPE"),
     (dict(dtype=7), "ERR_DTYPE"), (dict(mix_mode=2), "ERR_DTYPE"), (dict(mask_mode=-1), "ERR_DTYPE"),
+    (dict(router_mode=3), "ERR_DTYPE"), (dict(router_mode=2), "ERR_SHAPE"),
     (dict(B=-1), "ERR_ARG"), (dict(T_new=-3), "ERR_ARG"), (dict(eps=0.0), "ERR_ARG"),
     (dict(rope_theta=-1.0), "ERR_ARG"), (dict(ctx_max=-1), "ERR_ARG"),
     (dict(ctx_max=60, T_new=5), "ERR_CAPACITY"), (dict(S_cap=0), "ERR_SHAPE"),

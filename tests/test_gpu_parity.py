@@ -497,3 +497,63 @@ def test_full_sequence_doc_step_at_full_size(wm, name):
         for t in toks:
             if (l * w.T_new + t) in rows:
                 check_close(g[l, t], Oo[l, 0, t], w.dtype, "%s doc O l=%d t=%d" % (name, l, t))
+
+
+# -------------------------------------------- router variants (ablations, Section 5.3)
+
+VARIANT_CASES = {
+    "f32_kL": synth.small("f32_kL", B=2, T_new=37, L=4, k=4, D=64, Hq=2, Hkv=2, d=32,
+                          dtype="f32"),
+    "bf16_kL_p2": synth.small("bf16_kL_p2", B=2, T_new=70, L=6, k=6, D=128, Hq=4, Hkv=2, d=64,
+                              p=2),
+    "bf16_ragged_gqa": SMALL["bf16_ragged_gqa"],
+}
+
+
+@pytest.mark.parametrize("name,router_mode", [("f32_kL", 2), ("bf16_kL_p2", 2), ("f32_kL", 1),
+                                              ("bf16_ragged_gqa", 1)])
+@pytest.mark.parametrize("mix_mode", [0, 1])
+def test_router_mix_variants(wm, name, router_mode, mix_mode):
+    """Static weights (no router) and no deep-to-shallow feedback: mixing weights and mixed
+    channels against the oracle."""
+    w = VARIANT_CASES[name]
+    rng = np.random.default_rng(17)
+    P = synth.make_params(w, rng.normal(0, 1, size=(2, w.k * w.L)), gains="random")
+    P["W_alpha"] = (P["W_alpha"].float() * 10).to(P["W_alpha"].dtype)  # a router that matters
+    H = synth.make_states(w)
+    ao, mo = oracle.router_mix(_odims(w, mix_mode=mix_mode, router_mode=router_mode), P, H)
+    dims = _gdims(wm, w, mix_mode=mix_mode, router_mode=router_mode)
+    alpha = torch.empty((2, w.N, w.k, w.L), dtype=torch.float32, device="cuda")
+    mixed = torch.empty((2, w.k, w.N, w.D), dtype=w.torch_dtype, device="cuda")
+    ps = wm.ParamSet(_dev(P))
+    if router_mode == 1:
+        ps.c.W_alpha = None  # static weights do not read the router weights
+    wm.router_mix(dims, ps, H.cuda(), mixed, alpha)
+    torch.cuda.synchronize()
+    check_close(alpha, ao, w.dtype, "%s alpha" % name)
+    check_close(mixed, mo, w.dtype, "%s mixed" % name)
+    if router_mode == 2:
+        for j in range(w.k):
+            assert (alpha[:, :, j, j + 1:] == 0).all()
+
+
+
+@pytest.mark.parametrize("name,router_mode", [("bf16_kL_p2", 2), ("f32_kL", 2),
+                                              ("bf16_ragged_gqa", 1)])
+def test_layer_step_variants(wm, name, router_mode):
+    w = VARIANT_CASES[name]
+    rng = np.random.default_rng(19)
+    P = synth.make_params(w, rng.normal(0, 1, size=(2, w.k * w.L)), gains="random")
+    H = synth.make_states(w)
+    K0, V0 = synth.make_cache_cpu(w)
+    Ko, Vo = _f64(K0).copy(), _f64(V0).copy()
+    Oo = oracle.layer_step(_odims(w, router_mode=router_mode), P, H, w.chan_map, None, Ko, Vo)
+    Kg, Vg = K0.cuda(), V0.cuda()
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    wm.layer_step(_gdims(wm, w, router_mode=router_mode), _dev(P), H.cuda(), w.chan_map, None,
+                  Kg, Vg, O)
+    torch.cuda.synchronize()
+    ctx = np.zeros(w.B, dtype=np.int64)
+    _check_cache(Kg, Ko, K0, w, ctx, w.dtype, name + " K")
+    _check_cache(Vg, Vo, V0, w, ctx, w.dtype, name + " V")
+    check_close(O, Oo, w.dtype, name + " O")

@@ -518,3 +518,80 @@ def test_document_mask_ignores_other_documents(oracle_lib, mask_mode):
                                 else Vc[w.chan_map[l], b, kv, lo]).double().numpy()
                         np.testing.assert_allclose(O[l, b, i, h * w.d:(h + 1) * w.d], want,
                                                    rtol=1e-13, atol=1e-14)
+
+
+# ------------------------------------------- router variants (ablations, Section 5.3)
+
+@pytest.mark.parametrize("mix_mode", [0, 1])
+def test_static_router_is_the_bias_whatever_the_weights(oracle_lib, mix_mode):
+    """Static mixing weights: alpha = b for every token (before the optional softmax), the
+    same as the content-dependent router with W^alpha = 0, bit for bit."""
+    o = oracle_lib
+    w = _small(L=5, k=3, T_new=6, B=2, p=2)
+    rng = np.random.default_rng(41)
+    b = rng.normal(size=(2, w.k * w.L))
+    P = synth.make_params(w, b, gains="random")          # random W^alpha
+    Pz = synth.make_params(w, b, gains="random", zero_router=True)
+    H = synth.make_states(w)
+    a_s, m_s = o.router_mix(_dims(o, w, mix_mode=mix_mode, router_mode=o.ROUTER_STATIC), P, H)
+    a_z, m_z = o.router_mix(_dims(o, w, mix_mode=mix_mode), Pz, H)
+    np.testing.assert_array_equal(a_s, a_z)
+    np.testing.assert_array_equal(m_s, m_z)
+
+
+def _nofeedback_case(o, mix_mode, p=1):
+    w = _small(L=5, k=5, T_new=4, B=2, p=p)
+    rng = np.random.default_rng(42)
+    P = synth.make_params(w, rng.normal(size=(2, w.k * w.L)), gains="random")
+    P["W_alpha"] = P["W_alpha"] * 20.0   # a router that matters
+    H = synth.make_states(w)
+    dm = _dims(o, w, mix_mode=mix_mode, router_mode=o.ROUTER_NOFEEDBACK)
+    return w, P, H, dm
+
+
+@pytest.mark.parametrize("mix_mode", [0, 1])
+def test_nofeedback_channel_ignores_deeper_layers(oracle_lib, mix_mode):
+    """Without deep-to-shallow feedback, channel j (built at layer j) depends on source
+    layers 0..j only: changing the states of deeper layers leaves it bit-identical, its
+    weights on deeper layers are 0, and in softmax mode its weights on 0..j sum to 1."""
+    o = oracle_lib
+    w, P, H, dm = _nofeedback_case(o, mix_mode)
+    a, m = o.router_mix(dm, P, H)
+    for j in range(w.k):
+        assert (a[:, :, j, j + 1:] == 0).all()
+        if mix_mode == 1:
+            np.testing.assert_allclose(a[:, :, j, :j + 1].sum(-1), 1.0, rtol=1e-13)
+        H2 = H.clone()
+        H2[:, :, j + 1:] = torch.randn(H2[:, :, j + 1:].shape, dtype=H2.dtype)
+        a2, m2 = o.router_mix(dm, P, H2)
+        np.testing.assert_array_equal(m2[:, j], m[:, j])
+        np.testing.assert_array_equal(a2[:, :, j], a[:, :, j])
+    # and some channel does change with its own deepest layer
+    H3 = H.clone()
+    H3[:, :, w.L - 1] = torch.randn(H3[:, :, w.L - 1].shape, dtype=H3.dtype)
+    assert not np.array_equal(o.router_mix(dm, P, H3)[1][:, w.k - 1], m[:, w.k - 1])
+
+
+@pytest.mark.parametrize("p", [1, 2])
+def test_nofeedback_equals_router_with_masked_parameters(oracle_lib, p):
+    """Linear mode: the no-feedback mix equals the content-dependent one whose router
+    weights on deeper source layers, and whose weights and bias for deeper mixing
+    coefficients, are zero."""
+    o = oracle_lib
+    w, P, H, dm = _nofeedback_case(o, 0, p=p)
+    sel = o.router_layers(w.L, w.p)
+    Wm = P["W_alpha"].double().clone().reshape(2, w.k, w.L, len(sel), w.D)
+    bm = P["b_alpha"].double().clone().reshape(2, w.k, w.L)
+    for j in range(w.k):
+        for m, layer in enumerate(sel):
+            if layer > j:
+                Wm[:, j, :, m] = 0.0
+        Wm[:, j, j + 1:] = 0.0
+        bm[:, j, j + 1:] = 0.0
+    Pm = dict(P, W_alpha=Wm.reshape(2, w.k * w.L, -1), b_alpha=bm.reshape(2, -1))
+    Pm = {k: v.double() for k, v in Pm.items()}
+    Pd = {k: v.double() for k, v in P.items()}
+    a, m = o.router_mix(dm, Pd, H.double())
+    a0, m0 = o.router_mix(_dims(o, w), Pm, H.double())
+    np.testing.assert_array_equal(a, a0)
+    np.testing.assert_array_equal(m, m0)
