@@ -83,8 +83,10 @@ enum wm_op {
 
 /* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
  * D a multiple of 32, Hq a multiple of Hkv, d in {32, 64} (either dtype) or d = 96
- * (WM_BF16 only), 1 <= p <= L,
- * L * D * sizeof(dtype) <= 64 KiB. */
+ * (WM_BF16 only), 1 <= p <= L, and a token's L states plus its mixing coefficients
+ * within 64 KiB of LDS: L * D * sizeof(dtype) (rounded up to 16) + 8 * L * k4 + 16 * k
+ * bytes with k4 = k rounded up to a multiple of 4, e.g. L <= 31 at D = 1024 in bf16,
+ * L <= 15 in fp32. */
 typedef struct wm_dims {
   int32_t B;         /* sequences */
   int32_t T_new;     /* new tokens per sequence in this call */

@@ -148,6 +148,31 @@ def test_layer_step_modes(wm, mix_mode, mask_mode, gains):
     _layer_step_case(wm, SMALL["c1_tiny_f32"], mix_mode, mask_mode, gains)
 
 
+LIMITS = {
+    # the most layers (L = k = 64: 4096 router rows over 4096 stacked columns)
+    "L64_k64": synth.small("L64_k64", B=1, T_new=40, L=64, k=64, D=64, Hq=2, Hkv=1, d=32),
+    # the most layers sharing one channel, router reading the top layer only (p = L)
+    "L64_k1_p64": synth.small("L64_k1_p64", B=1, T_new=40, L=64, k=1, D=64, Hq=2, Hkv=1, d=32,
+                              p=64),
+    # the mix's LDS limit (a token's L states and its coefficients in 64 KiB): the most
+    # layers at D = 1024, bf16 and fp32
+    "L31_D1024_bf16": synth.small("L31_D1024_bf16", B=1, T_new=20, L=31, k=4, D=1024, Hq=4,
+                                  Hkv=4, d=64),
+    "L15_D1024_f32": synth.small("L15_D1024_f32", B=1, T_new=20, L=15, k=2, D=1024, Hq=4,
+                                 Hkv=2, d=32, dtype="f32"),
+    # a single new token with nothing cached: it reads only the dummy (or only itself)
+    "first_token": synth.small("first_token", B=3, T_new=1, L=3, k=2, D=64, Hq=2, Hkv=2,
+                               d=64),
+}
+
+
+@pytest.mark.parametrize("name", list(LIMITS))
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_layer_step_limits(wm, name, mask_mode):
+    """The largest supported layer counts and widths and the smallest step."""
+    _layer_step_case(wm, LIMITS[name], mask_mode=mask_mode)
+
+
 @pytest.mark.parametrize("p", [2, 3])
 def test_layer_step_router_subsampling(wm, p):
     _layer_step_case(wm, SMALL["bf16_ragged_gqa"], p=p)
