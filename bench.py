@@ -9,10 +9,12 @@ channel. The default workload is the 2048-token full-sequence (Jacobi) pass
 with B = 8, L = 12, k = 12, D = 768, 12 heads of 64 (bf16). Inputs are
 synthetic and already resident in HBM when the timed region starts.
 
-Prints one JSON line: tokens/s of the step, the roofline of the dominant
-kernel (timed with HIP events recorded by the library on its own stream at the
-phase boundaries of every timed step) and the CPU oracle's tokens/s on a
-bounded sample of the same workload.
+Prints one JSON line: tokens/s of the step (K timed steps of wm_layer_step,
+whose query projection overlaps the pool side on the library's second stream),
+the roofline of the dominant kernel (timed with HIP events that the library
+records at the phase boundaries of K more steps, run with the phases in
+sequence on the caller's stream) and the CPU oracle's tokens/s on a bounded
+sample of the same workload.
 """
 from __future__ import annotations
 
@@ -166,6 +168,7 @@ class HipEvents:
         self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
                                                  ctypes.c_void_p]
         self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
 
     def create(self) -> int:
         ev = ctypes.c_void_p()
@@ -173,6 +176,11 @@ class HipEvents:
         if rc != 0:
             raise RuntimeError("hipEventCreate failed: %d" % rc)
         return ev.value
+
+    def record(self, ev, stream) -> None:
+        rc = self.hip.hipEventRecord(ev, stream)
+        if rc != 0:
+            raise RuntimeError("hipEventRecord failed: %d" % rc)
 
     def elapsed_ms(self, a, b) -> float:
         ms = ctypes.c_float()
@@ -346,27 +354,43 @@ def main():
     stream = torch.cuda.current_stream(dev)
 
     hip = HipEvents()
-    events = [[hip.create() for _ in range(wm.PROFILE_EVENTS)] for _ in range(args.steps)]
     for _ in range(args.warmup):
         wm.layer_step(dims, P, H, w.chan_map, ctx, Kc, Vc, O, ws=ws, stream=stream,
                       doc_start=docs)
     torch.cuda.synchronize()
     log("bench: warmup done, timing %d steps" % args.steps)
 
+    # the timed steps: the fused step as a caller runs it (its query projection overlaps
+    # the pool side on the library's second stream), bracketed by synchronisations
+    step_ev = [hip.create() for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
+    hip.record(step_ev[0], stream.cuda_stream)
+    for s in range(args.steps):
+        wm.layer_step(dims, P, H, w.chan_map, ctx, Kc, Vc, O, ws=ws, stream=stream,
+                      doc_start=docs)
+        hip.record(step_ev[s + 1], stream.cuda_stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall = t1 - t0
+    step_ms = [hip.elapsed_ms(step_ev[s], step_ev[s + 1]) for s in range(args.steps)]
+    for e in step_ev:
+        hip.destroy(e)
+
+    # then the same number of steps with phase events (the phases run one after another on
+    # the caller's stream there), for the per-phase times and the roofline of each kernel
+    events = [[hip.create() for _ in range(wm.PROFILE_EVENTS)] for _ in range(args.steps)]
     for s in range(args.steps):
         wm.layer_step_profiled(dims, P, H, w.chan_map, ctx, Kc, Vc, O, events[s], ws=ws,
                                stream=stream, doc_start=docs)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    wall = t1 - t0
 
     phase_ms = {name: [] for name in wm.PHASES}
-    step_ms = []
+    serial_ms = []
     for ev in events:
         for i, name in enumerate(wm.PHASES):
             phase_ms[name].append(hip.elapsed_ms(ev[i], ev[i + 1]))
-        step_ms.append(hip.elapsed_ms(ev[0], ev[-1]))
+        serial_ms.append(hip.elapsed_ms(ev[0], ev[-1]))
     for ev in events:
         for e in ev:
             hip.destroy(e)
@@ -440,6 +464,7 @@ def main():
                           "t_roof_ms": round(t_roof * 1e3, 4),
                           "frac": round(t_roof / (ms_per_step * 1e-3), 4),
                           "event_ms_per_step_median": round(float(np.median(step_ms)), 4),
+                          "serial_phases_ms_per_step_median": round(float(np.median(serial_ms)), 4),
                           "phases_ms": {k: round(v, 4) for k, v in mean.items()}},
     }
     if not args.no_cpu_baseline:

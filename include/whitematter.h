@@ -174,6 +174,11 @@ int wm_channel_attend(const wm_dims *dims, const wm_params *params, const void *
  * then every consumer attends its channel (Step 3). With ctx_len = 0 and
  * T_new = T this is one full-sequence (Jacobi) pass, Section 3.3; with
  * T_new = 1 it is a decode step, Section 3.2.
+ * The query projection runs on a second stream that the library creates once per
+ * device (default priority, kept until the process ends): the call forks to it from
+ * `stream` with an event after the row norms and joins it before the attention, so to
+ * the caller the whole step is ordered on `stream` as usual (including under stream
+ * capture). If that stream cannot be created, everything runs on `stream`.
  *   H        device [B][T_new][L][D] in dtype
  *   chan_map host int32 [L]
  *   ctx_len  device int32 [B] or NULL

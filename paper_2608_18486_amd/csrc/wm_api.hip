@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "whitematter.h"
 #include "wm_internal.hpp"
@@ -175,6 +176,37 @@ int launched() {
   return WM_OK;
 }
 
+// A second stream per device for the fused step's query projection, which reads only the
+// layer states and runs beside the router, the mix and the K/V projection: the caller's
+// stream forks to it and joins it before the attention, through two events. Stream and
+// events are created on a device's first fused step (default priority) and kept for the
+// life of the process; a per-device lock orders the fork/join enqueues of calls made from
+// several host threads. Without them the step runs on the caller's stream alone.
+struct Aux {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool tried = false, ok = false;
+  std::mutex mu;
+};
+constexpr int kMaxDevices = 64;
+Aux g_aux[kMaxDevices];
+std::mutex g_aux_init;
+
+Aux* aux_stream() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  Aux& a = g_aux[dev];
+  std::lock_guard<std::mutex> lk(g_aux_init);
+  if (!a.tried) {
+    a.tried = true;
+    a.ok = hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking) == hipSuccess &&
+           hipEventCreateWithFlags(&a.fork, hipEventDisableTiming) == hipSuccess &&
+           hipEventCreateWithFlags(&a.join, hipEventDisableTiming) == hipSuccess;
+    (void)hipGetLastError();
+  }
+  return a.ok ? &a : nullptr;
+}
+
 #define WM_TRY(x)              \
   do {                         \
     int _rc = (x);             \
@@ -259,9 +291,9 @@ void run_attend(const wm_dims& d, const wm_params& P, const T* Q, const int32_t*
 }
 
 template <typename T>
-void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int32_t* chan_map,
-                    const int32_t* ctx_len, const int32_t* doc, T* Kc, T* Vc, T* O, void* ws,
-                    hipStream_t s, void* const* events) {
+int run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int32_t* chan_map,
+                   const int32_t* ctx_len, const int32_t* doc, T* Kc, T* Vc, T* O, void* ws,
+                   hipStream_t s, void* const* events) {
   auto mark = [&](int i) {
     if (events) (void)hipEventRecord((hipEvent_t)events[i], s);
   };
@@ -277,6 +309,22 @@ void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int3
   wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
   wm::launch_rope_table(sh, ctx_len, tab, s);
   mark(1);
+  // The query projection needs only H, the row norms and the angle table: unless the call
+  // is timing its phases, it goes to the auxiliary stream and overlaps the pool side.
+  Aux* ax = events ? nullptr : aux_stream();
+  std::unique_lock<std::mutex> lk;
+  hipStream_t qs = s;
+  if (ax) {
+    lk = std::unique_lock<std::mutex>(ax->mu);
+    if (hipEventRecord(ax->fork, s) != hipSuccess ||
+        hipStreamWaitEvent(ax->s, ax->fork, 0) != hipSuccess)
+      return fail(WM_ERR_LAUNCH, "fork to the auxiliary stream failed");
+    qs = ax->s;
+    wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
+                            tab, Q, (T*)at(ws, Ly.wq), qs);
+    if (hipEventRecord(ax->join, qs) != hipSuccess)
+      return fail(WM_ERR_LAUNCH, "join event on the auxiliary stream failed");
+  }
   wm::launch_router<T>(sh, router_layers(d), H, rinv, (const T*)P.g_pre, (const T*)P.W_alpha,
                        (const T*)P.b_alpha, alpha, (T*)at(ws, Ly.wa), (float*)at(ws, Ly.rpart),
                        s);
@@ -287,11 +335,17 @@ void run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int3
                            (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc,
                            (T*)at(ws, Ly.wkv), s);
   mark(4);
-  wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
-                          tab, Q, (T*)at(ws, Ly.wq), s);
+  if (qs != s) {
+    if (hipStreamWaitEvent(s, ax->join, 0) != hipSuccess)
+      return fail(WM_ERR_LAUNCH, "join of the auxiliary stream failed");
+  } else {
+    wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
+                            tab, Q, (T*)at(ws, Ly.wq), s);
+  }
   mark(5);
   run_attend<T>(d, P, Q, chan_map, ctx_len, doc, Kc, Vc, O, (float*)at(ws, Ly.part), s);
   mark(6);
+  return WM_OK;
 }
 
 int check_params(const wm_params* P, std::initializer_list<int> which) {
@@ -504,11 +558,11 @@ static int layer_step_impl(const wm_dims* dims, const wm_params* params, const v
   (void)hipGetLastError();
   hipStream_t s = (hipStream_t)stream;
   if (d.dtype == WM_BF16)
-    run_layer_step<bf16>(d, *params, (const bf16*)H, chan_map, ctx_len, doc, (bf16*)Kc,
-                         (bf16*)Vc, (bf16*)O, ws, s, events);
+    WM_TRY(run_layer_step<bf16>(d, *params, (const bf16*)H, chan_map, ctx_len, doc, (bf16*)Kc,
+                                (bf16*)Vc, (bf16*)O, ws, s, events));
   else
-    run_layer_step<float>(d, *params, (const float*)H, chan_map, ctx_len, doc, (float*)Kc,
-                          (float*)Vc, (float*)O, ws, s, events);
+    WM_TRY(run_layer_step<float>(d, *params, (const float*)H, chan_map, ctx_len, doc,
+                                 (float*)Kc, (float*)Vc, (float*)O, ws, s, events));
   return launched();
 }
 
