@@ -16,6 +16,8 @@
 // divergent branch and keeps exact wait counts), stored to the other half of a
 // double-buffered LDS stage, and multiplied with one barrier per slice.
 #pragma once
+#include <type_traits>
+
 #include "wm_device.hpp"
 
 namespace wm {
@@ -23,8 +25,18 @@ namespace wm {
 // LDS an epilogue may use once the main loop is done (one with kUsesLds set, in the
 // LDS-staged kernel): 32 x 32 WO elements of T per wave, at p + wave * that.
 struct EpiLds {
-  char* p;
-  int wave;
+  char* p;   // the block's LDS (free once the K loop is done)
+  int wave;  // this wave's index in the block
+  int n0;    // the block's first token
+};
+
+// Epilogues with kTabLds copy the block's rows of a per-token table into LDS before
+// finish() (stage_tab, all threads, then a barrier), so the waves that share tokens read
+// it there instead of each reading it from memory.
+template <class Epi, class = void> struct TabLds { static constexpr bool value = false; };
+template <class Epi>
+struct TabLds<Epi, std::void_t<decltype(Epi::kTabLds)>> {
+  static constexpr bool value = Epi::kTabLds;
 };
 
 template <typename T, int BK_, int WGO_, int WGN_, int WO_, int WN_> struct ProjCfg {
@@ -185,7 +197,12 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_kernel(int M, int Nout, int K
       __syncthreads();
     }
   }
-  epi.template finish<C>(g, ow0, nw0, acc, lane, est, EpiLds{(char*)smem, w});
+  if constexpr (TabLds<Epi>::value) {  // the loop ended at a barrier: the stages are free
+    static_assert(Epi::template tab_end<C>() <= sizeof(smem), "the table fits the stages");
+    epi.template stage_tab<C>(g, n0, (char*)smem, tid);
+    __syncthreads();
+  }
+  epi.template finish<C>(g, ow0, nw0, acc, lane, est, EpiLds{(char*)smem, w, n0});
 }
 
 // bf16 variant whose K slices travel straight from memory into LDS
@@ -311,12 +328,18 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_dma_kernel(int M, int Nout, i
   wait_vmcnt<0>();  // the trailing prefetches (zeros) land before the block ends
   // an epilogue that stages its stores through the ring waits until every wave is past
   // its last read of it
-  if constexpr (Epi::kUsesLds) {
-    static_assert(sizeof(smem) >= (size_t)(C::NT / 64) * 32 * 32 * C::WO * sizeof(T),
+  if constexpr (Epi::kUsesLds || TabLds<Epi>::value) {
+    static_assert(!Epi::kUsesLds ||
+                      sizeof(smem) >= (size_t)(C::NT / 64) * 32 * 32 * C::WO * sizeof(T),
                   "the epilogue's staging fits the ring");
     __syncthreads();
   }
-  epi.template finish<C>(g, ow0, nw0, acc, lane, est, EpiLds{(char*)smem, w});
+  if constexpr (TabLds<Epi>::value) {
+    static_assert(Epi::template tab_end<C>() <= sizeof(smem), "the table fits the ring");
+    epi.template stage_tab<C>(g, n0, (char*)smem, tid);
+    __syncthreads();
+  }
+  epi.template finish<C>(g, ow0, nw0, acc, lane, est, EpiLds{(char*)smem, w, n0});
 }
 
 }  // namespace wm

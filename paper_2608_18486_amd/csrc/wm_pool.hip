@@ -114,6 +114,11 @@ template <int DH> __device__ __forceinline__ int head_chan(int v, int h) {
   return 32 * (v >> 4) + 8 * ((v & 15) >> 2) + 4 * h + (v & 3);
 }
 
+// Chunk swizzle of the RoPE rows staged in LDS (see stage_rope_rows).
+template <int DH> __device__ __forceinline__ int rope_row_swz(int t) {
+  return DH == 64 ? (t & 15) : ((t >> 1) & 7);
+}
+
 // STAGE (bf16): stores go through the wave's LDS area so that each store instruction
 // writes whole head rows (measured faster for the cache writes of the K/V projection,
 // not for the query workspace).
@@ -126,11 +131,14 @@ template <int DH> __device__ __forceinline__ int head_chan(int v, int h) {
 //   scale_at(n) -> float   the row's 1/RMS
 //   aux_at(n)   -> int     a per-token value the destination needs (or 0)
 //   dst_at(n, head, aux) -> T*   the row's destination, nullptr when there is none
-template <typename T, int DH, int WO, int WN, bool STAGE, class ScaleAt, class AuxAt,
-          class DstAt>
+//   tab, tab_n0: the RoPE table rows of tokens tab_n0 .. : with TABLDS the block's rows
+//   in LDS, laid out by stage_rope_rows; else the whole table in memory (tab_n0 = 0)
+template <typename T, int DH, int WO, int WN, bool STAGE, bool TABLDS, class ScaleAt,
+          class AuxAt, class DstAt>
 __device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, int nw0, int lane,
                                               int M, bool rotate, const T* gain,
-                                              const float* tab, float eps, ScaleAt scale_at,
+                                              const float* tab, int tab_n0, float eps,
+                                              ScaleAt scale_at,
                                               AuxAt aux_at, DstAt dst_at, T* trash,
                                               const EpiLds& lds) {
   constexpr int NV = DH / 2;          // values of one head per lane
@@ -162,9 +170,10 @@ __device__ __forceinline__ void head_epilogue(f32x16 (&acc)[WO][WN], int ow0, in
   auto load_tab = [&](int jn) {
 #pragma unroll
     for (int g = 0; g < DH / 16; ++g) {
-      const float* tp = tab + (long)nn[jn] * DH + 2 * (8 * g + 4 * h);
-      tb[g][0] = *(const f32x4*)tp;
-      tb[g][1] = *(const f32x4*)(tp + 4);
+      const int t = nn[jn] - tab_n0, sw = TABLDS ? rope_row_swz<DH>(t) : 0;
+      const float* tp = tab + (long)t * DH;
+      tb[g][0] = *(const f32x4*)(tp + 4 * ((4 * g + 2 * h) ^ sw));
+      tb[g][1] = *(const f32x4*)(tp + 4 * ((4 * g + 2 * h + 1) ^ sw));
     }
   };
   if (rotate) load_tab(0);
@@ -280,10 +289,36 @@ constexpr size_t kTrashElems = 512;
 
 struct NoState {};
 
+// The block's rows [n0, n0 + NTOK) of the RoPE table (DH floats per token; rows past the
+// last token repeat it) copied into LDS at byte offset `off`, 16 bytes per thread and step.
+// 16-byte chunk c of row t sits at chunk c ^ rope_row_swz(t), so the 16 lanes of a read,
+// one token each, hit 16 distinct bank groups (the rows are 128, 256 or 384 bytes).
+template <class C, int DH>
+__device__ __forceinline__ void stage_rope_rows(const float* tab, int M, int n0, char* lds,
+                                                size_t off, int tid) {
+  static_assert(DH == 32 || DH == 64 || DH == 96, "swizzle shapes");
+  constexpr int CH = DH / 4, N = C::NTOK * CH;
+  float* dst = (float*)(lds + off);
+  for (int i = tid; i < N; i += C::NT) {
+    const int t = i / CH, c = i - t * CH, n = min(n0 + t, M - 1);
+    *(f32x4*)(dst + t * DH + 4 * (c ^ rope_row_swz<DH>(t))) =
+        *(const f32x4*)(tab + (long)n * DH + 4 * c);
+  }
+}
+
 template <typename T, int DH> struct KVEpi {
   // bf16 stages the cache writes when a head row is a power-of-two count of 16-B chunks
   // (head dims 32 and 64); head dim 96 stores directly
   static constexpr bool kUsesLds = sizeof(T) == 2 && ((DH / 8) & (DH / 8 - 1)) == 0;
+  // the key blocks' RoPE rows go to LDS after the output staging area (head dims 32 and
+  // 64; measured slower at 96, whose blocks read the table from memory)
+  static constexpr bool kTabLds = DH != 96;
+  template <class C> static constexpr size_t tab_off() {
+    return kUsesLds ? (size_t)(C::NT / 64) * 32 * 32 * C::WO * sizeof(T) : 0;
+  }
+  template <class C> static constexpr size_t tab_end() {
+    return tab_off<C>() + (size_t)C::NTOK * DH * sizeof(float);
+  }
   T *Kc, *Vc;
   T* trash;  // kTrashElems elements of workspace
   const float* rs;  // [2k][M] 1 / RMS of each mixed channel row (the mid RMSNorm)
@@ -296,14 +331,18 @@ template <typename T, int DH> struct KVEpi {
   template <class C> __device__ void begin(int, int, int, State&) const {}
   template <class C>
   __device__ void segment(int, int, int, f32x16 (&)[C::WO][C::WN], int, State&) const {}
+  template <class C> __device__ void stage_tab(int g, int n0, char* lds, int tid) const {
+    if (g < k) stage_rope_rows<C, DH>(tab, M, n0, lds, tab_off<C>(), tid);  // key branch
+  }
   template <class C>
   __device__ void finish(int g, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
                          State&, const EpiLds& lds) const {
     const int br = g / k, j = g - br * k;
     const bool key = br == 0;
     T* base = key ? Kc : Vc;
-    head_epilogue<T, DH, C::WO, C::WN, kUsesLds>(
-        acc, ow0, nw0, lane, M, key, g_knorm + (long)j * DH, tab, eps,
+    head_epilogue<T, DH, C::WO, C::WN, kUsesLds, kTabLds>(
+        acc, ow0, nw0, lane, M, key, g_knorm + (long)j * DH,
+        kTabLds ? (const float*)(lds.p + tab_off<C>()) : tab, kTabLds ? lds.n0 : 0, eps,
         [&](int n) { return rs[(long)g * M + n]; },
         [&](int n) { return ctx_len ? ctx_len[n / T_new] : 0; },
         [&](int n, int head, int ctx) -> T* {
@@ -319,6 +358,13 @@ template <typename T, int DH> struct KVEpi {
 
 template <typename T, int DH> struct QEpi {
   static constexpr bool kUsesLds = false;
+  static constexpr bool kTabLds = DH != 96;  // RoPE rows in LDS (as for the keys)
+  template <class C> static constexpr size_t tab_end() {
+    return (size_t)C::NTOK * DH * sizeof(float);
+  }
+  template <class C> __device__ void stage_tab(int, int n0, char* lds, int tid) const {
+    stage_rope_rows<C, DH>(tab, M, n0, lds, 0, tid);
+  }
   T* Q;
   T* trash;  // kTrashElems elements of workspace
   const float* rs;  // [M][L] 1 / RMS of each consumer's input state (the input RMSNorm)
@@ -333,8 +379,9 @@ template <typename T, int DH> struct QEpi {
   template <class C>
   __device__ void finish(int l, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
                          State&, const EpiLds& lds) const {
-    head_epilogue<T, DH, C::WO, C::WN, false>(
-        acc, ow0, nw0, lane, M, true, g_qnorm + (long)l * DH, tab, eps,
+    head_epilogue<T, DH, C::WO, C::WN, false, kTabLds>(
+        acc, ow0, nw0, lane, M, true, g_qnorm + (long)l * DH,
+        kTabLds ? (const float*)lds.p : tab, kTabLds ? lds.n0 : 0, eps,
         [&](int n) { return rs[(long)n * L + l]; }, [](int) { return 0; },
         [&](int n, int head, int) -> T* {
           if (head >= Hq) return nullptr;
