@@ -565,8 +565,9 @@ constexpr int kFewTokens = 64;
 // ------------------------------------------------------------------ router
 size_t router_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.L * sh.Lp * sh.D; }
 
-// Layers per K split: enough blocks to cover the chip, splitting K at layer
-// boundaries when the token and channel tiles alone give few blocks.
+// Layers per K split: enough blocks to cover the chip (one per CU), splitting K at layer
+// boundaries when the token and channel tiles alone give fewer. (Aiming at two blocks per
+// CU measured 6-21% slower: the extra partial sums cost more than the occupancy gains.)
 static int router_layers_per_split(const Shape& sh) {
   using CF = RouterShape<bf16, false>::C;
   using CD = RouterShape<bf16, true>::C;
@@ -574,7 +575,7 @@ static int router_layers_per_split(const Shape& sh) {
   const int tok = few ? CD::NTOK : CF::NTOK, och = few ? CD::OT : CF::OT;
   const long blocks = (long)((sh.N() + tok - 1) / tok) * ((2 * sh.k * sh.L + och - 1) / och);
   int s = 1;
-  while (s < sh.Lp && blocks * s < 512) s *= 2;
+  while (s < sh.Lp && blocks * s < 256) s *= 2;
   return (sh.Lp + s - 1) / s;
 }
 
