@@ -495,6 +495,7 @@ template <int DH> __device__ __forceinline__ int pf_swz(int row) {
 template <int QT, int DH> struct PfState {  // one wave's running softmax state (2 lanes per row)
   f32x16 o[DH / 32][QT];  // O^T per 32-column tile of the values and query tile
   bf16x8 pf[2][QT];       // P(i-1)^T fragments (keys 0-15, 16-31 of the step)
+  f32x16 nb[QT];          // -m in every element: the start value of each step's scores
   float m[QT], lsum[QT];
 };
 
@@ -581,6 +582,32 @@ __device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int 
   }
 }
 
+// Hides the slots a masked step hides from this lane's row (see pf_init) in finished
+// scores: they become -1e30, whose weight is 0.
+template <bool DOC>
+__device__ __forceinline__ void pf_mask(f32x16& v, int i, int lim0, int lo0, int lane) {
+  const int base = 32 * i + 4 * (lane >> 5), lim = lim0 - base, lo = lo0 - base;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int off = 8 * (q >> 2) + (q & 3);
+    v[q] = off >= lim || (DOC && off < lo) ? kNegBig : v[q];
+  }
+}
+
+// Sum of the 16 bf16 weights of a lane, two dot products against (1, 1) per pair of
+// fragments' halves: the normaliser then adds exactly the weights the PV products use.
+__device__ __forceinline__ float pf_wsum(const bf16x8& a, const bf16x8& b) {
+  const bf16x2 one = {(bf16)1.f, (bf16)1.f};
+  float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bf16x2 pa = {a[2 * e], a[2 * e + 1]}, pb = {b[2 * e], b[2 * e + 1]};
+    s0 = __builtin_amdgcn_fdot2_f32_bf16(pa, one, s0, false);
+    s1 = __builtin_amdgcn_fdot2_f32_bf16(pb, one, s1, false);
+  }
+  return s0 + s1;
+}
+
 // f(integral_constant<int, I>) for I = I0 .. N-1, in order.
 template <int I0, int N, class F> __device__ __forceinline__ void static_for(F& f) {
   if constexpr (I0 < N) {
@@ -604,18 +631,22 @@ template <int N, int I0 = 0> __device__ __forceinline__ float tree_sum_arr(const
 
 // One step (see above), the same straight-line code for every step: the MFMAs of
 // PV(i-1) and S(i+1) and the exponentials of S(i) sit in one basic block, so they
-// interleave. sc holds S(i) in log2 units minus the row reference m, masked; sn
-// arrives holding the start value of S(i+1) (pf_init) and leaves holding S(i+1). Two
-// register sets alternate between consecutive steps, and sc is refilled with the start
-// value of S(i+2), so no step waits on the MFMAs it has just issued. lim0 is the first
-// tile's row limit; tile t's rows sit 32 t further; dlo[t] is tile t's document start.
+// interleave. sc holds S(i) in log2 units minus the row reference m; a masked step hides
+// its slots here, before the exponentials. sn leaves holding S(i+1): its first MFMA
+// starts from st.nb (-m in every element), so no register is set per step. Two register
+// sets alternate between consecutive steps, so no step waits on the MFMAs it has just
+// issued. lim0 is the first tile's row limit; tile t's rows sit 32 t further; dlo[t] is
+// tile t's document start.
 template <int QT, int DH, bool DOC>
 __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, uint32_t kh_cur,
                                         uint32_t kh_nxt, uint32_t vh_prv, int i,
                                         const bf16x8 (&qf)[QT][DH / 16], PfState<QT, DH>& st,
                                         f32x16 (&sc)[QT], f32x16 (&sn)[QT], int lane, int lim0,
-                                        const int (&dlo)[QT],
-                                        bool mask_cur, bool mask_n2) {
+                                        const int (&dlo)[QT], bool mask_cur) {
+  if (mask_cur) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) pf_mask<DOC>(sc[t], i, lim0 + 32 * t, dlo[t], lane);
+  }
   // NG groups g, each: the MFMAs of PV(i-1) for keys 16(g / NDT).. and value tile
   // g % NDT and of S(i+1) for k16 step g, plus the weights of rows [q0(g), q0(g+1)) of
   // S(i). The fragments of V^T (step i-1; before the first step a zeroed stage) and K
@@ -627,7 +658,6 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
   kf[0] = pf_ldk<DH>(sm, lo, kh_nxt, 0);
   // weights against the current reference, in place (S(i) is not needed again unless
   // the rescale below runs, which recomputes it from the K block still in LDS)
-  float psg[QT][NG];
   auto group = [&](auto gc) {
     constexpr int g = decltype(gc)::value;
     constexpr int q0 = (16 * g + NG - 1) / NG, q1 = (16 * (g + 1) + NG - 1) / NG;
@@ -638,20 +668,20 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       st.o[g % NDT][t] = mma32(st.o[g % NDT][t], vf[g & 1], st.pf[g / NDT][t]);
-      sn[t] = mma32(sn[t], kf[g & 1], qf[t][g]);
+      sn[t] = mma32(g == 0 ? st.nb[t] : sn[t], kf[g & 1], qf[t][g]);
     }
 #pragma unroll
-    for (int t = 0; t < QT; ++t) {
+    for (int t = 0; t < QT; ++t)
 #pragma unroll
       for (int q = q0; q < q1; ++q) sc[t][q] = fast_exp2(sc[t][q]);
-      psg[t][g] = tree_sum<q0, q1>(sc[t]);
-    }
     __builtin_amdgcn_sched_barrier(0);
   };
   static_for<0, NG>(group);
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    float ps = tree_sum_arr<NG>(psg[t]);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) st.pf[q >> 3][t][q & 7] = (bf16)sc[t][q];
+    float ps = pf_wsum(st.pf[0][t], st.pf[1][t]);
     if (__any(!(ps <= kGrowSum) || st.m[t] == kNoRef)) {
       // rare: move the reference up to the exact row max (never down) and rescale the
       // state; S(i+1) was started from the old reference, so it moves too
@@ -667,18 +697,15 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
       st.lsum[t] *= alpha;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) st.o[dt][t] *= alpha;
-      ps = 0.f;
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
+        st.nb[t][q] = -st.m[t];
         sn[t][q] -= mx;
-        sc[t][q] = fast_exp2(sr[q] - mx);
-        ps += sc[t][q];
+        st.pf[q >> 3][t][q & 7] = (bf16)fast_exp2(sr[q] - mx);
       }
+      ps = pf_wsum(st.pf[0][t], st.pf[1][t]);
     }
-#pragma unroll
-    for (int q = 0; q < 16; ++q) st.pf[q >> 3][t][q & 7] = (bf16)sc[t][q];
     st.lsum[t] += ps;
-    pf_init<DOC>(sc[t], -st.m[t], mask_n2, i + 2, lim0 + 32 * t, dlo[t], lane);  // S(i+2)
   }
 }
 
@@ -795,6 +822,8 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) st.o[dt][t] = zero16();
     }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) st.nb[t][q] = -st.m[t];
   }
 
   const int qlast = min(q0 + P::BQ, a.T_new) - 1;
@@ -813,15 +842,14 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   // (64 chunks of 16 B) per instruction; lane x of instruction n fills LDS chunk
   // 64 n + x of the wave's rows, i.e. row (64 n + x) / CPR, chunk (64 n + x) % CPR, with
   // the chunk of the slot row that the swizzle puts there
-  const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)scap * P::ROW_BYTES);
-  const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)scap * P::ROW_BYTES);
-  int crow[P::NI];
-  uint32_t dchunk[P::NI];
+  // (the views end at slot kend, so rows past it read as zeros without a test per copy)
+  const __amdgpu_buffer_rsrc_t kview = make_view(a.Kc + cbase, (uint32_t)kend * P::ROW_BYTES);
+  const __amdgpu_buffer_rsrc_t vview = make_view(a.Vc + cbase, (uint32_t)kend * P::ROW_BYTES);
+  uint32_t coff[P::NI];  // byte offset of the lane's chunk within block 0
 #pragma unroll
   for (int n = 0; n < P::NI; ++n) {
-    const int ch = 64 * n + lane;
-    crow[n] = P::RPW * w + ch / P::CPR;
-    dchunk[n] = 16u * (uint32_t)((ch % P::CPR) ^ pf_swz<DH>(crow[n]));
+    const int ch = 64 * n + lane, crow = P::RPW * w + ch / P::CPR;
+    coff[n] = (uint32_t)crow * P::ROW_BYTES + 16u * (uint32_t)((ch % P::CPR) ^ pf_swz<DH>(crow));
   }
   const uint32_t smem_base = (uint32_t)(uintptr_t)smem;
   // NI copy instructions per wave move its rows of a K or V block; blocks past the
@@ -831,8 +859,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   auto issue = [&](int blk, bool v) {
 #pragma unroll
     for (int n = 0; n < P::NI; ++n) {
-      const int s = blk * P::BKV + crow[n];
-      const uint32_t off = s < kend ? (uint32_t)s * P::ROW_BYTES + dchunk[n] : kOffOob;
+      const uint32_t off = coff[n] + (uint32_t)blk * P::BLK_BYTES;
       const uint32_t lds = __builtin_amdgcn_readfirstlane(
           smem_base + (v ? P::V_BASE : 0) + (blk % P::NS) * P::BLK_BYTES +
           P::RPW * w * P::ROW_BYTES + 1024 * n);
@@ -871,11 +898,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     issue(j + P::NS - 2, true);
     if (u == 0 && j == 0 && ilast >= 0) {
 #pragma unroll
-      for (int t = 0; t < QT; ++t) {
-        pf_init<DOC>(sa[t], -st.m[t], masked(0), 0, lim0 + 32 * t, dlo[t], lane);
-        sa[t] = pf_scores<DH>(smem, lo, pf_kh<DH>(0, 0), qf[t], sa[t]);
-        pf_init<DOC>(sb[t], -st.m[t], masked(1), 1, lim0 + 32 * t, dlo[t], lane);
-      }
+      for (int t = 0; t < QT; ++t) sa[t] = pf_scores<DH>(smem, lo, pf_kh<DH>(0, 0), qf[t], st.nb[t]);
     }
     // steps up to ilast + 1: the last one only adds PV(ilast) (its own slots are all
     // past the wave's rows, so its weights are 0)
@@ -883,7 +906,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     if (i <= ilast + 1)
       pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
                       pf_vh<DH>((u + P::NS - 1) % P::NS, 1), i, qf, st, sa, sb, lane, lim0,
-                      dlo, masked(i), masked(i + 2));
+                      dlo, masked(i));
     // the second step reads K(j+1) and V(j): only the copies issued above may still be
     // in flight
     wait_vmcnt<2 * P::NI * (1 + AHEAD)>();
@@ -891,7 +914,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     if (i + 1 <= ilast + 1)
       pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 1), pf_kh<DH>((u + 1) % P::NS, 0),
                       pf_vh<DH>(u, 0), i + 1, qf, st, sb, sa, lane, lim0, dlo,
-                      masked(i + 1), masked(i + 3));
+                      masked(i + 1));
   };
   for (int j = 0; j < nblk; j += P::NS) {
     block(j, std::integral_constant<int, 0>());
@@ -903,7 +926,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     const int u = nblk % P::NS;
     pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
                     pf_vh<DH>((u + P::NS - 1) % P::NS, 1), 2 * nblk, qf, st, sa, sb, lane, lim0,
-                    dlo, true, true);
+                    dlo, true);
   }
   wait_vmcnt<0>();  // no copy may land after the workgroup ends
 
