@@ -643,7 +643,7 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
                                         const bf16x8 (&qf)[QT][DH / 16], PfState<QT, DH>& st,
                                         f32x16 (&sc)[QT], f32x16 (&sn)[QT], int lane, int lim0,
                                         const int (&dlo)[QT], bool mask_cur) {
-  if (mask_cur) {
+  if (__builtin_expect(mask_cur, 0)) {
 #pragma unroll
     for (int t = 0; t < QT; ++t) pf_mask<DOC>(sc[t], i, lim0 + 32 * t, dlo[t], lane);
   }
@@ -682,7 +682,7 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
 #pragma unroll
     for (int q = 0; q < 16; ++q) st.pf[q >> 3][t][q & 7] = (bf16)sc[t][q];
     float ps = pf_wsum(st.pf[0][t], st.pf[1][t]);
-    if (__any(!(ps <= kGrowSum) || st.m[t] == kNoRef)) {
+    if (__builtin_expect(__any(!(ps <= kGrowSum) || st.m[t] == kNoRef), 0)) {
       // rare: move the reference up to the exact row max (never down) and rescale the
       // state; S(i+1) was started from the old reference, so it moves too
       f32x16 sr;
