@@ -561,11 +561,11 @@ __device__ __forceinline__ f32x16 pf_scores(const char* sm, const PfLane<DH>& lo
   return acc;
 }
 
-// Accumulator start for the scores of step i: -m (the row reference), or -1e30 for the
-// slots a masked step hides from this lane's row (slot 32 i + 8(q/4) + 4h + q%4 is
-// visible iff it is at least lo0, the row's document start, and below lim0, the row
-// position + incl). -1e30 plus any score stays about -1e30, so the MFMAs that follow
-// need no masking afterwards.
+// Accumulator start for a recomputation of the scores of step i (the rescale path):
+// -m (the row reference), or -1e30 for the slots a masked step hides from this lane's
+// row (slot 32 i + 8(q/4) + 4h + q%4 is visible iff it is at least lo0, the row's
+// document start, and below lim0, the row position + incl). -1e30 plus any score stays
+// about -1e30, so the MFMAs that follow need no masking afterwards.
 template <bool DOC>
 __device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int i, int lim0,
                                         int lo0, int lane) {
