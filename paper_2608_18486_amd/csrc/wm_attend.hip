@@ -582,6 +582,11 @@ __device__ __forceinline__ void pf_init(f32x16& v, float init, bool masked, int 
   }
 }
 
+// 4 bf16 at byte offset off of a buffer view (zeros out of range)
+__device__ __forceinline__ bf16x4 buf_ld8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+
 // Hides the slots a masked step hides from this lane's row (see pf_init) in finished
 // scores: they become -1e30, whose weight is 0.
 template <bool DOC>
@@ -735,8 +740,40 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   const int q0 = qtile * P::BQ, qw0 = q0 + 32 * QT * w;
   const float cl2 = a.scale_log2;
 
-  // zero the rings first: "block -1" feeds the first step's (weightless) PV, and slot
-  // rows past the visible range get weight 0, so every stage must hold finite values
+  // The queries and the dummy slot are loaded first and used only once the first copies
+  // are issued, so their latency overlaps the ring set-up and the copies'.
+  // (buffer loads: rows past T_new, and the dummy when the mask has none, read as zeros)
+  bf16x8 qf[QT][NKS];
+  {
+    const auto qview = make_view(a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * DH,
+                                 (uint32_t)a.T_new * DH * 2u);
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      const int qi = qw0 + 32 * t + r;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+        qf[t][ks] = buf_frag<bf16>(qview, qi < a.T_new ? (uint32_t)(qi * DH + 16 * ks + 8 * h) * 2u
+                                                      : kOffOob);
+    }
+  }
+  bf16x8 kdv[NKS];      // the dummy's key at this lane's columns
+  bf16x4 vdv[NDT][4];   // and its value at this lane's rows of O^T
+  {
+    const long dof = ((long)c * a.Hkv + kvh) * DH;
+    const uint32_t dbytes = a.mask_paper ? DH * 2u : 0u;
+    const auto kdview = make_view(a.mask_paper ? a.Kd + dof : nullptr, dbytes);
+    const auto vdview = make_view(a.mask_paper ? a.Vd + dof : nullptr, dbytes);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) kdv[ks] = buf_frag<bf16>(kdview, (16 * ks + 8 * h) * 2u);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        vdv[dt][g4] = buf_ld8(vdview, (32 * dt + 8 * g4 + 4 * h) * 2u);
+  }
+
+  // zero the rings: "block -1" feeds the first step's (weightless) PV, and slot rows
+  // past the visible range get weight 0, so every stage must hold finite values
   {
     const i32x4 z = {0, 0, 0, 0};
 #pragma unroll
@@ -779,53 +816,6 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
 
   const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH +
                      (long)base0 * DH;
-  bf16x8 qf[QT][NKS];
-  const bf16* Qb = a.Q + (((long)l * a.B + b) * a.Hq + hq) * (long)a.T_new * DH;
-#pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    const int qi = qw0 + 32 * t + r;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-      qf[t][ks] = qi < a.T_new ? *(const bf16x8*)(Qb + (long)qi * DH + 16 * ks + 8 * h)
-                               : zero_frag<bf16>();
-    // queries in log2 units: the MFMAs then give s' = q.k log2(e) / sqrt(d)
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) qf[t][ks][i] = (bf16)((float)qf[t][ks][i] * cl2);
-  }
-
-  PfState<QT, DH> st;
-  f32x16 sa[QT], sb[QT];  // score registers of even and odd steps
-#pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    st.pf[0][t] = zero_frag<bf16>();
-    st.pf[1][t] = zero_frag<bf16>();
-    if (a.mask_paper) {
-      const bf16* kd = a.Kd + ((long)c * a.Hkv + kvh) * DH;
-      const bf16* vd = a.Vd + ((long)c * a.Hkv + kvh) * DH;
-      float part = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) part += (float)qf[t][ks][i] * (float)kd[16 * ks + 8 * h + i];
-      st.m[t] = halves_sum(part);
-      st.lsum[t] = h == 0 ? 1.f : 0.f;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int q = 0; q < 16; ++q)
-          st.o[dt][t][q] = (float)vd[32 * dt + 8 * (q >> 2) + 4 * h + (q & 3)];
-    } else {
-      st.m[t] = kNoRef;
-      st.lsum[t] = 0.f;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) st.o[dt][t] = zero16();
-    }
-#pragma unroll
-    for (int q = 0; q < 16; ++q) st.nb[t][q] = -st.m[t];
-  }
-
   const int qlast = min(q0 + P::BQ, a.T_new) - 1;
   const int scap = a.S_cap - base0;
   const int kend = min(ctxr + qlast + incl, scap);   // slots the workgroup may see
@@ -875,6 +865,41 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   if (AHEAD) {
     issue(2, false);
     issue(1, true);
+  }
+
+  // queries in log2 units: the MFMAs then give s' = q.k log2(e) / sqrt(d)
+#pragma unroll
+  for (int t = 0; t < QT; ++t)
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) qf[t][ks][i] = (bf16)((float)qf[t][ks][i] * cl2);
+  PfState<QT, DH> st;
+  f32x16 sa[QT], sb[QT];  // score registers of even and odd steps
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    st.pf[0][t] = zero_frag<bf16>();
+    st.pf[1][t] = zero_frag<bf16>();
+    if (a.mask_paper) {
+      float part = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) part += (float)qf[t][ks][i] * (float)kdv[ks][i];
+      st.m[t] = halves_sum(part);
+      st.lsum[t] = h == 0 ? 1.f : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) st.o[dt][t][q] = (float)vdv[dt][q >> 2][q & 3];
+    } else {
+      st.m[t] = kNoRef;
+      st.lsum[t] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) st.o[dt][t] = zero16();
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) st.nb[t][q] = -st.m[t];
   }
   // block 0's first step reads K(0) only (and the zeroed V stage before it)
   wait_vmcnt<P::NI * (2 + 2 * AHEAD)>();
