@@ -21,11 +21,12 @@
 namespace wm {
 
 // ----------------------------------------------------------------- row rms
+// One wave per row, any D.
 template <typename T>
-__global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int D, float eps,
-                                                      float* rinv) {
-  long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
-  int lane = threadIdx.x & 63;
+__global__ __launch_bounds__(256) void row_rms_loop_kernel(const T* X, long rows, int D,
+                                                           float eps, float* rinv) {
+  const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (row >= rows) return;
   const T* x = X + row * D;
   float ss = 0.f;
@@ -39,11 +40,59 @@ __global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int
   if (lane == 0) rinv[row] = 1.0f / sqrtf(ss / (float)D + eps);
 }
 
+// One wave per R rows of at most 512 NC elements; a lane loads its NC chunks of 8 from
+// each of them before any arithmetic, so a wave has R NC loads in flight (one row of
+// 1-1.5 KB per wave left the HBM read stream short of loads in flight).
+template <typename T, int R, int NC>
+__global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int D, float eps,
+                                                      float* rinv) {
+  const long row0 = ((long)blockIdx.x * 4 + (threadIdx.x >> 6)) * R;
+  const int lane = threadIdx.x & 63;
+  if (row0 >= rows) return;
+  float v[R][NC][8];
+#pragma unroll
+  for (int q = 0; q < R; ++q)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int e = lane * 8 + 512 * c;
+      if (row0 + q < rows && e < D) load8(X + (row0 + q) * D + e, v[q][c]);
+      else
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[q][c][i] = 0.f;
+    }
+#pragma unroll
+  for (int q = 0; q < R; ++q) {
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss += v[q][c][i] * v[q][c][i];
+    ss = wave_sum(ss);
+    if (lane == 0 && row0 + q < rows) rinv[row0 + q] = 1.0f / sqrtf(ss / (float)D + eps);
+  }
+}
+
+#ifndef WM_RMS_ROWS
+#define WM_RMS_ROWS 2
+#endif
+template <typename T, int NC>
+static void launch_row_rms_nc(const T* X, long rows, int D, float eps, float* rinv,
+                              hipStream_t s) {
+  constexpr int R = WM_RMS_ROWS;
+  hipLaunchKernelGGL((row_rms_kernel<T, R, NC>), dim3((unsigned)((rows + 4 * R - 1) / (4 * R))),
+                     dim3(256), 0, s, X, rows, D, eps, rinv);
+}
+
 template <typename T>
 void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(row_rms_kernel<T>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, X,
-                     rows, D, eps, rinv);
+  const int nc = (D + 511) / 512;  // chunks of 8 per lane (D is a multiple of 8)
+  if (nc <= 1) launch_row_rms_nc<T, 1>(X, rows, D, eps, rinv, s);
+  else if (nc == 2) launch_row_rms_nc<T, 2>(X, rows, D, eps, rinv, s);
+  else if (nc <= 4) launch_row_rms_nc<T, 4>(X, rows, D, eps, rinv, s);
+  else
+    hipLaunchKernelGGL(row_rms_loop_kernel<T>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
+                       X, rows, D, eps, rinv);
 }
 
 // -------------------------------------------------------------- rope table

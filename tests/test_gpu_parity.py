@@ -160,6 +160,12 @@ LIMITS = {
                                   Hkv=4, d=64),
     "L15_D1024_f32": synth.small("L15_D1024_f32", B=1, T_new=20, L=15, k=2, D=1024, Hq=4,
                                  Hkv=2, d=32, dtype="f32"),
+    # wide states: the row norms' 8-chunk-per-lane variant (D = 2560) and their loop over
+    # any width (D = 4608)
+    "D2560_bf16": synth.small("D2560_bf16", B=1, T_new=20, L=3, k=2, D=2560, Hq=2, Hkv=1,
+                              d=64),
+    "D4608_bf16": synth.small("D4608_bf16", B=1, T_new=12, L=2, k=2, D=4608, Hq=2, Hkv=1,
+                              d=32),
     # a single new token with nothing cached: it reads only the dummy (or only itself)
     "first_token": synth.small("first_token", B=3, T_new=1, L=3, k=2, D=64, Hq=2, Hkv=2,
                                d=64),
