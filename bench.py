@@ -307,6 +307,31 @@ def measure_ceilings(wm, torch, dev, stream):
                       "blocks, 16384 iterations), event-timed"}
 
 
+def blas_reference(w, log):
+    """Plain batched GEMMs of the projections' shapes through torch.bmm (no norms, RoPE or
+    cache layout), timed with events: what the vendor library reaches on these shapes."""
+    import torch
+
+    cases = [("K/V projection", 2 * w.k, w.B * w.T_new, w.Hkv * w.d, w.D),
+             ("Q projection", w.L, w.B * w.T_new, w.Hq * w.d, w.D)]
+    for name, G, M, N, K in cases:
+        x = torch.randn(G, M, K, device="cuda", dtype=torch.bfloat16)
+        wt = torch.randn(G, K, N, device="cuda", dtype=torch.bfloat16).contiguous()
+        o = torch.empty(G, M, N, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.bmm(x, wt, out=o)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(20):
+            torch.bmm(x, wt, out=o)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / 20
+        log("bench: torch.bmm reference, %s (%d x [%d x %d] x [%d x %d]): %.3f ms, %.1f TFLOP/s"
+            % (name, G, M, K, K, N, ms, 2.0 * G * M * N * K / ms / 1e9))
+        del x, wt, o
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -314,6 +339,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c2_T2048_L12_k12", choices=sorted(WORKLOAD_LABEL))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--blas-reference", action="store_true",
+                    help="also time torch.bmm (the vendor GEMM library) on the plain GEMMs of the "
+                         "K/V and query projections of this workload, for comparison (stderr)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the WhiteMatter step here runs on a single MI355X "
@@ -331,6 +359,8 @@ def main():
     torch.cuda.set_device(dev)
     log = lambda *a: print(*a, file=sys.stderr, flush=True)  # noqa: E731
     log("bench: workload %s (%s)" % (w.name, WORKLOAD_LABEL[w.name]))
+    if args.blas_reference and w.dtype == "bf16":
+        blas_reference(w, log)
 
     bias = np.asarray(wm.init_bias(w.L, w.k))
     P_cpu = synth.make_params(w, bias)
