@@ -96,21 +96,29 @@ void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStr
 }
 
 // -------------------------------------------------------------- rope table
+// tab[n][m] = (cos, sin)(pos(n) theta^(-2m/d)). The frequencies (one per m) are computed
+// once per block in double; each angle is formed and reduced modulo 2 pi in double, so
+// the float sincos that follows sees |r| <= pi and keeps float accuracy at any position.
 __global__ __launch_bounds__(256) void rope_table_kernel(const int32_t* ctx_len, int B,
                                                          int T_new, int d, double theta,
                                                          float* tab) {
-  int half = d / 2;
-  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  __shared__ double freq[kMaxHeadDim / 2];
+  const int half = d / 2;
+  for (int m = threadIdx.x; m < half; m += blockDim.x)
+    freq[m] = pow(theta, -2.0 * (double)m / (double)d);
+  __syncthreads();
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long)B * T_new * half) return;
-  int m = (int)(idx % half);
-  long n = idx / half;
-  int b = (int)(n / T_new), i = (int)(n % T_new);
-  double pos = (double)((ctx_len ? ctx_len[b] : 0) + i);
-  double freq = pow(theta, -2.0 * (double)m / (double)d);
-  double sn, cs;
-  sincos(pos * freq, &sn, &cs);
-  tab[2 * idx] = (float)cs;
-  tab[2 * idx + 1] = (float)sn;
+  const int m = (int)(idx % half);
+  const long n = idx / half;
+  const int b = (int)(n / T_new), i = (int)(n % T_new);
+  const double ang = (double)((ctx_len ? ctx_len[b] : 0) + i) * freq[m];
+  constexpr double kTwoPi = 6.283185307179586476925286766559;
+  const float r = (float)(ang - kTwoPi * rint(ang / kTwoPi));
+  float sn, cs;
+  sincosf(r, &sn, &cs);
+  tab[2 * idx] = cs;
+  tab[2 * idx + 1] = sn;
 }
 
 void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipStream_t s) {
