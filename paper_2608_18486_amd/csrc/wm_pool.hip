@@ -1143,29 +1143,29 @@ void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, 
 // from W0 = W^K, the rest from W1 = W^V).
 template <typename T>
 __global__ __launch_bounds__(256) void fold_gain_kernel(const T* W0, const T* W1, int split,
-                                                        const T* gain, T* Wf, int groups,
-                                                        int Nout, int K) {
-  long idx = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
-  long per = (long)Nout * K;
-  if (idx >= per * groups) return;
-  int grp = (int)(idx / per);
-  long rem = idx - (long)grp * per;
-  int e = (int)(rem % K);
-  const T* src = grp < split ? W0 + (long)grp * per + rem : W1 + (long)(grp - split) * per + rem;
+                                                        const T* gain, T* Wf, int Nout, int K) {
+  // one group per grid row; 32-bit offsets within it (a group holds under 2^31 elements)
+  const int grp = blockIdx.y;
+  const uint32_t per = (uint32_t)Nout * (uint32_t)K;
+  const uint32_t idx = (blockIdx.x * 256u + threadIdx.x) * 8u;
+  if (idx >= per) return;
+  const uint32_t e = idx % (uint32_t)K;
+  const T* src = grp < split ? W0 + (long)grp * per : W1 + (long)(grp - split) * per;
   float wv[8], gv[8];
-  load8(src, wv);
+  load8(src + idx, wv);
   load8(gain + (long)grp * K + e, gv);
 #pragma unroll
   for (int i = 0; i < 8; ++i) wv[i] *= gv[i];
-  store8(Wf + idx, wv);
+  store8(Wf + (long)grp * per + idx, wv);
 }
 
 template <typename T>
 static void fold_gain(const T* W0, const T* W1, int split, const T* gain, T* Wf, int groups,
                       int Nout, int K, hipStream_t s) {
-  long total = (long)groups * Nout * K / 8;
-  hipLaunchKernelGGL(fold_gain_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                     W0, W1, split, gain, Wf, groups, Nout, K);
+  const long per = (long)Nout * K;  // K is a multiple of 8
+  if (per <= 0 || groups <= 0) return;
+  hipLaunchKernelGGL(fold_gain_kernel<T>, dim3((unsigned)((per / 8 + 255) / 256), (unsigned)groups),
+                     dim3(256), 0, s, W0, W1, split, gain, Wf, Nout, K);
 }
 
 // folded weights, then the epilogue's trash area
