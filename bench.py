@@ -5,16 +5,16 @@ python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-
 One step = one wm_layer_step call: pool the new tokens into the channel cache
 (row norms, router, mix, per-channel K/V projection with key norm + RoPE),
 project every consumer's queries, and run every consumer's attention over its
-channel. The default workload is the 2048-token full-sequence (Jacobi) pass
-with B = 8, L = 12, k = 12, D = 768, 12 heads of 64 (bf16). Inputs are
-synthetic and already resident in HBM when the timed region starts.
+channel. The default workload is the largest full-sequence (Jacobi) pass that
+fits one GPU: B = 4 sequences of T = 4096 tokens, L = 24, k = 12, D = 1024, 16
+heads of 64 (bf16). Inputs are synthetic and already resident in HBM when the
+timed region starts.
 
-Prints one JSON line: tokens/s of the step (K timed steps of wm_layer_step,
-whose query projection overlaps the pool side on the library's second stream),
-the roofline of the dominant kernel (timed with HIP events that the library
-records at the phase boundaries of K more steps, run with the phases in
-sequence on the caller's stream) and the CPU oracle's tokens/s on a bounded
-sample of the same workload.
+Prints one JSON line: tokens/s of the step (K timed steps of wm_layer_step on
+one stream), the roofline of the dominant kernel (timed with HIP events that
+the library records at the phase boundaries of K more steps), the step against
+its fused minimum, the 32768-context decode step timed in the same run, and the
+CPU oracle's tokens/s on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -135,6 +135,30 @@ def phase_costs(w, docs=None):
     }
 
 
+def fused_min_ms(w, docs=None):
+    """The step's fused minimum: four phases, each at the slower of its flops at the bf16
+    (or fp32) matrix peak and its minimum HBM bytes at 8 TB/s, with the layer states read
+    once (by the pool side), the mixed channels and the queries kept on chip:
+      mix side   router + mix flops; H and the router weights
+      K/V        projection flops; its weights and the cache write
+      Q          projection flops; its weights
+      attention  flops; each channel's cache read once, O written."""
+    c = phase_costs(w, docs)
+    es = 4 if w.dtype == "f32" else 2
+    peak = PEAK_TFLOPS[w.dtype] * 1e12
+    bw = PEAK_HBM_GBS * 1e9
+    used = len(set(w.chan_map))
+    router_w = 0 if router_mode_of(w) == 1 else 2 * w.k * w.L * ((w.L + w.p - 1) // w.p) * w.D
+    phases = [
+        (c["router"][0] + c["mix"][0], (w.N * w.L * w.D + router_w) * es),
+        (c["kv_project"][0], (2 * w.k * w.Hkv * w.d * w.D + 2 * w.k * w.N * w.Hkv * w.d) * es),
+        (c["q_project"][0], w.L * w.Hq * w.d * w.D * es),
+        (c["attend"][0], (2 * used * w.B * w.Hkv * (w.ctx + w.T_new) * w.d
+                          + w.L * w.N * w.Hq * w.d) * es),
+    ]
+    return sum(max(f / peak, b / bw) for f, b in phases) * 1e3
+
+
 def step_cost(w, docs=None):
     c = phase_costs(w, docs)
     router_w = 0 if router_mode_of(w) == 1 else 2 * w.k * w.L * ((w.L + w.p - 1) // w.p) * w.D
@@ -230,17 +254,32 @@ def measured_traffic(workload, kernel):
 
 # ------------------------------------------------------------ CPU baseline
 
-def cpu_baseline(w, P, H_cpu, cache_dev, docs=None):
-    """The oracle, as it stands, on a bounded sample: up to 8 sequences of the step (the
-    whole 2048-token pass of B = 8 takes about 15 s on 16 host threads)."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next(ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name"))
+    except (OSError, StopIteration):
+        return "unknown"
+
+
+def cpu_baseline(w, P, H_cpu, cache_dev, docs=None, budget_tokens=2 * 2048):
+    """The oracle, as it stands, on a bounded sample (about 10-30 s on 16 host threads).
+
+    Small steps (at most budget_tokens tokens in up to 8 sequences) run whole. Larger
+    ones run one sequence: the pool of all its tokens (every query reads the whole cache
+    before it), then the queries and attention of 128 evenly spaced positions over all
+    consumers and heads; that part is scaled to all positions (a position's attention
+    cost grows linearly with it, so evenly spaced positions give its mean)."""
     import numpy as np
-    import torch
 
     import oracle
     from tests import synth
 
     oracle.build(force=False)
     nseq = min(w.B, 8)
+    whole = nseq * w.T_new <= budget_tokens or w.T_new <= 4
+    if not whole:
+        nseq = 1
     w1 = synth.Workload(w.name, nseq, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.ctx, w.dtype,
                         w.chan_map, w.p, w.seed)
     dm = oracle.Dims(B=nseq, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d,
@@ -252,21 +291,33 @@ def cpu_baseline(w, P, H_cpu, cache_dev, docs=None):
         Vc[:, :, :, :w.ctx] = cache_dev[1][:, :nseq, :, :w.ctx].double().cpu().numpy()
     Hs = H_cpu[:nseq]
     ctx = np.full(nseq, w.ctx, dtype=np.int32)
-    t0 = time.perf_counter()
-    oracle.layer_step(dm, PP, Hs, w.chan_map, ctx, Kc, Vc,
-                      doc_start=None if docs is None else docs[:nseq])
-    dt = time.perf_counter() - t0
-    toks = nseq * w.T_new
-    cpu = "unknown"
-    try:
-        with open("/proc/cpuinfo") as f:
-            cpu = next(ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name"))
-    except (OSError, StopIteration):
-        pass
-    return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "cpu": cpu,
-            "sample": "%d of %d sequences (%d tokens), whole step (pool, queries, attention over "
-                      "%d cached + new slots), %.1f s" % (nseq, w.B, toks, w.ctx, dt)}
+    dsub = None if docs is None else docs[:nseq]
+    if whole:
+        t0 = time.perf_counter()
+        oracle.layer_step(dm, PP, Hs, w.chan_map, ctx, Kc, Vc, doc_start=dsub)
+        dt = time.perf_counter() - t0
+        toks = nseq * w.T_new
+        sample = ("%d of %d sequences (%d tokens), whole step (pool, queries, attention over "
+                  "%d cached + new slots), %.1f s" % (nseq, w.B, toks, w.ctx, dt))
+        value = toks / dt
+    else:
+        npos = 128
+        pos = sorted({int(round(x)) for x in np.linspace(0, w.T_new - 1, npos)})
+        rows = [l * w.T_new + t for l in range(w.L) for t in pos]
+        t0 = time.perf_counter()
+        oracle.pool(dm, PP, Hs, ctx, Kc, Vc)
+        t1 = time.perf_counter()
+        Q = oracle.q_project(dm, PP, Hs, ctx, pos)
+        oracle.channel_attend(dm, PP, Q, w.chan_map, ctx, Kc, Vc, rows, doc_start=dsub)
+        t2 = time.perf_counter()
+        t_seq = (t1 - t0) + (t2 - t1) * w.T_new / len(pos)
+        value = w.T_new / t_seq
+        sample = ("1 of %d sequences: pool of all %d tokens (%.1f s), queries and attention of "
+                  "%d evenly spaced positions over all %d consumers and %d heads (%.1f s), "
+                  "scaled to %d positions: %.1f s per sequence"
+                  % (w.B, w.T_new, t1 - t0, len(pos), w.L, w.Hq, t2 - t1, w.T_new, t_seq))
+    return {"value": value, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "cpu": _cpu_model(), "sample": sample}
 
 
 # ------------------------------------------------------------ main
@@ -332,13 +383,67 @@ def blas_reference(w, log):
         del x, wt, o
 
 
+def decode_step(wm, torch, np, synth, hip, dev, stream, log, steps=10):
+    """The 32768-context decode step (B = 64 new tokens appended to 12 channels, 24
+    consumers attend; bf16), event-timed: ms per step, tokens/s and the attention's
+    share of the HBM peak over its algorithmic bytes (each channel's cache read once)."""
+    w = synth.WORKLOADS["c5_decode_S32768"]
+    log("bench: decode step %s" % w.name)
+    P = wm.ParamSet({k: v.to(dev) for k, v in
+                     synth.make_params(w, np.asarray(wm.init_bias(w.L, w.k))).items()})
+    H = synth.make_states(w).to(dev)
+    Kc, Vc = synth.make_cache_device(w, device=dev)
+    ctx = torch.full((w.B,), w.ctx, dtype=torch.int32, device=dev)
+    O = torch.empty((w.L, w.B, 1, w.Hq * w.d), dtype=w.torch_dtype, device=dev)
+    dims = wm.make_dims(w.B, 1, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p, S_cap=w.S_cap,
+                        ctx_max=w.ctx, dtype=wm.BF16)
+    ws = wm.workspace(dims, wm.OP_LAYER_STEP, dev)
+    for _ in range(3):
+        wm.layer_step(dims, P, H, w.chan_map, ctx, Kc, Vc, O, ws=ws, stream=stream)
+    torch.cuda.synchronize()
+    ev = [hip.create() for _ in range(steps + 1)]
+    hip.record(ev[0], stream.cuda_stream)
+    for s in range(steps):
+        wm.layer_step(dims, P, H, w.chan_map, ctx, Kc, Vc, O, ws=ws, stream=stream)
+        hip.record(ev[s + 1], stream.cuda_stream)
+    torch.cuda.synchronize()
+    ms = [hip.elapsed_ms(ev[s], ev[s + 1]) for s in range(steps)]
+    pev = [hip.create() for _ in range(wm.PROFILE_EVENTS)]
+    att = []
+    for _ in range(steps):
+        wm.layer_step_profiled(dims, P, H, w.chan_map, ctx, Kc, Vc, O, pev, ws=ws,
+                               stream=stream)
+        torch.cuda.synchronize()
+        att.append(hip.elapsed_ms(pev[5], pev[6]))
+    for e in ev + pev:
+        hip.destroy(e)
+    _, attn_bytes = phase_costs(w)["attend"]
+    t_step = float(np.median(ms))
+    t_att = float(np.median(att))
+    del Kc, Vc
+    torch.cuda.empty_cache()
+    out = {"workload": WORKLOAD_LABEL[w.name], "ms_per_step_median": round(t_step, 4),
+           "tokens_per_s": round(w.B / (t_step * 1e-3), 1),
+           "attend_ms_median": round(t_att, 4),
+           "attend_hbm_gb": round(attn_bytes / 1e9, 2),
+           "attend_hbm_frac": round(attn_bytes / (t_att * 1e-3) / (PEAK_HBM_GBS * 1e9), 4),
+           "step_hbm_frac": round(attn_bytes / (t_step * 1e-3) / (PEAK_HBM_GBS * 1e9), 4),
+           "per_consumer_hbm_gb": round(attn_bytes * w.L / len(set(w.chan_map)) / 1e9, 2),
+           "steps": steps}
+    log("bench: decode %.3f ms/step, attention %.3f ms (%.1f%% of HBM peak)"
+        % (t_step, t_att, 100 * out["attend_hbm_frac"]))
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2_T2048_L12_k12", choices=sorted(WORKLOAD_LABEL))
+    ap.add_argument("--workload", default="c4_T4096_L24_k12", choices=sorted(WORKLOAD_LABEL))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the 32768-context decode step timed after the main workload")
     ap.add_argument("--blas-reference", action="store_true",
                     help="also time torch.bmm (the vendor GEMM library) on the plain GEMMs of the "
                          "K/V and query projections of this workload, for comparison (stderr)")
@@ -390,8 +495,7 @@ def main():
     torch.cuda.synchronize()
     log("bench: warmup done, timing %d steps" % args.steps)
 
-    # the timed steps: the fused step as a caller runs it (its query projection overlaps
-    # the pool side on the library's second stream), bracketed by synchronisations
+    # the timed steps: the fused step as a caller runs it, bracketed by synchronisations
     step_ev = [hip.create() for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -407,8 +511,8 @@ def main():
     for e in step_ev:
         hip.destroy(e)
 
-    # then the same number of steps with phase events (the phases run one after another on
-    # the caller's stream there), for the per-phase times and the roofline of each kernel
+    # then the same number of steps with phase events, for the per-phase times and the
+    # roofline of each kernel
     events = [[hip.create() for _ in range(wm.PROFILE_EVENTS)] for _ in range(args.steps)]
     for s in range(args.steps):
         wm.layer_step_profiled(dims, P, H, w.chan_map, ctx, Kc, Vc, O, events[s], ws=ws,
@@ -468,9 +572,11 @@ def main():
         roof["frac_of_measured_ceiling"] = round(achieved / roof["measured_ceiling"], 4)
 
     ms_per_step = wall / args.steps * 1e3
-    # the fused step's roofline: each phase at the slower of its flops and its bytes
+    # this design's phase-wise roofline: each of its phases at the slower of its flops and
+    # its bytes, with the intermediates it keeps in HBM (row norms, mixed channels, Q)
     t_roof = sum(max(f / (PEAK_TFLOPS[w.dtype] * 1e12), b / (PEAK_HBM_GBS * 1e9))
                  for f, b in costs.values())
+    t_min = fused_min_ms(w, docs_np)
     tokens = w.N * args.steps
     line = {
         "metric": "tokens/s of mix+KV-proj+channel-attention step; % of HBM / MFMA roofline",
@@ -491,15 +597,21 @@ def main():
         "roofline": roof,
         "ceilings": ceilings,
         "step_roofline": {"gflop": round(flops / 1e9, 2), "min_hbm_gb": round(min_bytes / 1e9, 3),
-                          "t_roof_ms": round(t_roof * 1e3, 4),
-                          "frac": round(t_roof / (ms_per_step * 1e-3), 4),
+                          "fused_min_ms": round(t_min, 4),
+                          "frac": round(t_min / ms_per_step, 4),
+                          "this_design_roof_ms": round(t_roof * 1e3, 4),
+                          "frac_of_this_design_roof": round(t_roof / (ms_per_step * 1e-3), 4),
                           "event_ms_per_step_median": round(float(np.median(step_ms)), 4),
                           "serial_phases_ms_per_step_median": round(float(np.median(serial_ms)), 4),
                           "phases_ms": {k: round(v, 4) for k, v in mean.items()}},
     }
+    if not args.no_decode and w.name != "c5_decode_S32768":
+        del Kc, Vc, O, ws, H
+        torch.cuda.empty_cache()
+        line["decode_c5"] = decode_step(wm, torch, np, synth, hip, dev, stream, log)
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline ...")
-        line["cpu_baseline"] = cpu_baseline(w, P_cpu, H_cpu, (Kc, Vc), docs_np)
+        line["cpu_baseline"] = cpu_baseline(w, P_cpu, H_cpu, (Kc, Vc) if w.ctx else None, docs_np)
     print(json.dumps(line), flush=True)
 
 

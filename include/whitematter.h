@@ -21,11 +21,15 @@
  *  - Return value: WM_OK or one of the WM_ERR_* codes; wm_last_error() gives
  *    a message for the calling thread's last failure.
  *  - N = B * T_new new tokens; token n = b * T_new + i of sequence b sits at
- *    position ctx_len[b] + i and is cached at that slot.
+ *    position pos(b, i) = ctx_len[b] + q + g * i and is cached at that slot, where
+ *    g = dims->groups and q = dims->group select a strided token group of Section
+ *    3.3 (G_q = positions congruent to q mod g); g = 1, q = 0 (or g = 0) are
+ *    contiguous new tokens, pos(b, i) = ctx_len[b] + i.
  *  - ctx_len (device, int32 [B], NULL = all zero) must lie in [0, ctx_max];
- *    ctx_max + T_new <= S_cap is checked on the host. A ctx_len entry outside
- *    that range leaves that sequence's outputs unspecified but never causes an
- *    access outside the given buffers.
+ *    ctx_max + q + g * (T_new - 1) + 1 <= S_cap is checked on the host. The
+ *    kernels clamp each entry into [0, S_cap - (q + g * (T_new - 1) + 1)], so an
+ *    entry outside [0, ctx_max] leaves that sequence's outputs unspecified but
+ *    never causes an access outside the given buffers.
  */
 #ifndef WHITEMATTER_H
 #define WHITEMATTER_H
@@ -45,7 +49,7 @@ enum wm_status {
   WM_ERR_SHAPE = 2,       /* inconsistent or unsupported dimensions */
   WM_ERR_DTYPE = 3,       /* unknown dtype / mode value */
   WM_ERR_MAP = 4,         /* consumer->channel map entry outside [0, k) */
-  WM_ERR_CAPACITY = 5,    /* ctx_max + T_new > S_cap */
+  WM_ERR_CAPACITY = 5,    /* ctx_max + positions of the new tokens > S_cap */
   WM_ERR_WORKSPACE = 6,   /* ws NULL, misaligned or smaller than required */
   WM_ERR_LAUNCH = 7       /* the HIP runtime rejected a launch */
 };
@@ -105,6 +109,10 @@ typedef struct wm_dims {
   int32_t router_mode; /* enum wm_router_mode */
   float eps;         /* RMSNorm epsilon (e.g. 1e-6) */
   float rope_theta;  /* RoPE base (e.g. 1e6) */
+  int32_t groups;    /* g of Section 3.3: the call's tokens are the strided group q of a
+                        pass split into g groups (token i at position ctx_len[b] + q + g i);
+                        0 or 1: contiguous tokens */
+  int32_t group;     /* q, 0 <= q < max(g, 1) */
 } wm_dims;
 
 /* Parameters, device pointers, in dtype, row-major. L' = ceil(L / p). */
@@ -169,16 +177,13 @@ int wm_channel_attend(const wm_dims *dims, const wm_params *params, const void *
                       const void *Vc, void *O, void *ws, size_t ws_bytes,
                       wm_stream_t stream);
 
-/* The fused step: pool the T_new new tokens of every sequence into cache slots
- * [ctx_len[b], ctx_len[b] + T_new) (Steps 1-2), project the consumer queries,
- * then every consumer attends its channel (Step 3). With ctx_len = 0 and
- * T_new = T this is one full-sequence (Jacobi) pass, Section 3.3; with
- * T_new = 1 it is a decode step, Section 3.2.
- * The query projection runs on a second stream that the library creates once per
- * device (default priority, kept until the process ends): the call forks to it from
- * `stream` with an event after the row norms and joins it before the attention, so to
- * the caller the whole step is ordered on `stream` as usual (including under stream
- * capture). If that stream cannot be created, everything runs on `stream`.
+/* The fused step: pool the T_new new tokens of every sequence into their cache
+ * slots pos(b, i) (Steps 1-2), project the consumer queries, then every consumer
+ * attends its channel (Step 3). With ctx_len = 0 and T_new = T this is one
+ * full-sequence (Jacobi) pass, Section 3.3; with T_new = 1 it is a decode step,
+ * Section 3.2. Every kernel runs on `stream`, in order; the call keeps no state
+ * between calls (calls on different streams with their own buffers may overlap,
+ * and the step may be captured into a graph).
  *   H        device [B][T_new][L][D] in dtype
  *   chan_map host int32 [L]
  *   ctx_len  device int32 [B] or NULL

@@ -38,8 +38,9 @@ class WMError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("B", "T_new", "L", "k", "D", "Hq", "Hkv", "d", "p", "S_cap", "ctx_max",
-                 "dtype", "mix_mode", "mask_mode", "router_mode")] + [("eps", ctypes.c_float),
-                                                       ("rope_theta", ctypes.c_float)]
+                 "dtype", "mix_mode", "mask_mode", "router_mode")] + [
+        ("eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("groups", ctypes.c_int32),
+        ("group", ctypes.c_int32)]
 
     @property
     def N(self) -> int:
@@ -108,9 +109,11 @@ def _check(rc: int):
 
 def make_dims(B, T_new, L, k, D, Hq, Hkv, d, p=1, S_cap=0, ctx_max=0, dtype=BF16,
               mix_mode=MIX_LINEAR, mask_mode=MASK_PAPER, eps=1e-6, rope_theta=1e6,
-              router_mode=ROUTER_DYNAMIC) -> Dims:
+              router_mode=ROUTER_DYNAMIC, groups=1, group=0) -> Dims:
+    """groups/group: the call's tokens are the strided group q = group of a pass split into
+    g = groups groups (token i of sequence b at position ctx_len[b] + q + g i)."""
     return Dims(B, T_new, L, k, D, Hq, Hkv, d, p, S_cap, ctx_max, dtype, mix_mode, mask_mode,
-                router_mode, eps, rope_theta)
+                router_mode, eps, rope_theta, groups, group)
 
 
 def dtype_code(t: torch.dtype) -> int:

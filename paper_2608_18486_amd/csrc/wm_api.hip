@@ -4,11 +4,12 @@
 // the kernels on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <climits>
 #include <cstring>
-#include <mutex>
 
 #include "whitematter.h"
 #include "wm_internal.hpp"
@@ -36,6 +37,12 @@ struct Layout {
          wa = 0, rpart = 0, total = 0;
 };
 
+int group_stride(const wm_dims& d) { return d.groups > 1 ? d.groups : 1; }
+// positions covered by one sequence's new tokens (group + groups (T_new - 1) + 1)
+long long call_span(const wm_dims& d) {
+  return d.T_new > 0 ? (long long)d.group + (long long)group_stride(d) * (d.T_new - 1) + 1 : 0;
+}
+
 wm::Shape make_shape(const wm_dims& d) {
   wm::Shape s;
   s.B = d.B;
@@ -55,6 +62,12 @@ wm::Shape make_shape(const wm_dims& d) {
   s.eps = d.eps;
   s.rope_theta = d.rope_theta;
   s.ctx_max = d.ctx_max;
+  s.gs = group_stride(d);
+  s.gq = d.group;
+  // the device clamps ctx_len[b] into [0, ctx_hi]; without a cache (S_cap unused) only
+  // the lower bound applies
+  const long long hi = d.S_cap > 0 ? (long long)d.S_cap - call_span(d) : INT_MAX;
+  s.ctx_hi = (int)std::min<long long>(std::max<long long>(hi, 0), INT_MAX);
   return s;
 }
 
@@ -120,11 +133,16 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (!(d.rope_theta > 0.f) || !std::isfinite(d.rope_theta))
     return fail(WM_ERR_ARG, "rope_theta must be positive");
   if (d.ctx_max < 0) return fail(WM_ERR_ARG, "ctx_max must be >= 0");
+  if (d.groups < 0) return fail(WM_ERR_ARG, "groups must be >= 0");
+  if (d.group < 0 || d.group >= group_stride(d))
+    return fail(WM_ERR_ARG, "group must be in [0, groups)");
+  if ((long long)d.ctx_max + call_span(d) > INT_MAX / 2)
+    return fail(WM_ERR_SHAPE, "positions past the 32-bit range");
   if (uses_cache(op)) {
     if (d.S_cap < 1) return fail(WM_ERR_SHAPE, "S_cap must be >= 1");
-    if ((long long)d.ctx_max + d.T_new > d.S_cap)
-      return fail(WM_ERR_CAPACITY, "ctx_max + T_new = %lld exceeds S_cap = %d",
-                  (long long)d.ctx_max + d.T_new, d.S_cap);
+    if ((long long)d.ctx_max + call_span(d) > d.S_cap)
+      return fail(WM_ERR_CAPACITY, "ctx_max + the positions of the new tokens = %lld exceeds "
+                  "S_cap = %d", (long long)d.ctx_max + call_span(d), d.S_cap);
   }
   const long long N = (long long)d.B * d.T_new;
   if (N > (1LL << 30)) return fail(WM_ERR_SHAPE, "B * T_new too large");
@@ -174,37 +192,6 @@ int launched() {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(WM_ERR_LAUNCH, "launch failed: %s", hipGetErrorString(e));
   return WM_OK;
-}
-
-// A second stream per device for the fused step's query projection, which reads only the
-// layer states and runs beside the router, the mix and the K/V projection: the caller's
-// stream forks to it and joins it before the attention, through two events. Stream and
-// events are created on a device's first fused step (default priority) and kept for the
-// life of the process; a per-device lock orders the fork/join enqueues of calls made from
-// several host threads. Without them the step runs on the caller's stream alone.
-struct Aux {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-  bool tried = false, ok = false;
-  std::mutex mu;
-};
-constexpr int kMaxDevices = 64;
-Aux g_aux[kMaxDevices];
-std::mutex g_aux_init;
-
-Aux* aux_stream() {
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
-  Aux& a = g_aux[dev];
-  std::lock_guard<std::mutex> lk(g_aux_init);
-  if (!a.tried) {
-    a.tried = true;
-    a.ok = hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking) == hipSuccess &&
-           hipEventCreateWithFlags(&a.fork, hipEventDisableTiming) == hipSuccess &&
-           hipEventCreateWithFlags(&a.join, hipEventDisableTiming) == hipSuccess;
-    (void)hipGetLastError();
-  }
-  return a.ok ? &a : nullptr;
 }
 
 #define WM_TRY(x)              \
@@ -309,22 +296,6 @@ int run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int32
   wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
   wm::launch_rope_table(sh, ctx_len, tab, s);
   mark(1);
-  // The query projection needs only H, the row norms and the angle table: unless the call
-  // is timing its phases, it goes to the auxiliary stream and overlaps the pool side.
-  Aux* ax = events ? nullptr : aux_stream();
-  std::unique_lock<std::mutex> lk;
-  hipStream_t qs = s;
-  if (ax) {
-    lk = std::unique_lock<std::mutex>(ax->mu);
-    if (hipEventRecord(ax->fork, s) != hipSuccess ||
-        hipStreamWaitEvent(ax->s, ax->fork, 0) != hipSuccess)
-      return fail(WM_ERR_LAUNCH, "fork to the auxiliary stream failed");
-    qs = ax->s;
-    wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
-                            tab, Q, (T*)at(ws, Ly.wq), qs);
-    if (hipEventRecord(ax->join, qs) != hipSuccess)
-      return fail(WM_ERR_LAUNCH, "join event on the auxiliary stream failed");
-  }
   wm::launch_router<T>(sh, router_layers(d), H, rinv, (const T*)P.g_pre, (const T*)P.W_alpha,
                        (const T*)P.b_alpha, alpha, (T*)at(ws, Ly.wa), (float*)at(ws, Ly.rpart),
                        s);
@@ -335,13 +306,8 @@ int run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int32
                            (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc,
                            (T*)at(ws, Ly.wkv), s);
   mark(4);
-  if (qs != s) {
-    if (hipStreamWaitEvent(s, ax->join, 0) != hipSuccess)
-      return fail(WM_ERR_LAUNCH, "join of the auxiliary stream failed");
-  } else {
-    wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
-                            tab, Q, (T*)at(ws, Ly.wq), s);
-  }
+  wm::launch_q_project<T>(sh, H, rinv, (const T*)P.g_in, (const T*)P.Wq, (const T*)P.g_qnorm,
+                          tab, Q, (T*)at(ws, Ly.wq), s);
   mark(5);
   run_attend<T>(d, P, Q, chan_map, ctx_len, doc, Kc, Vc, O, (float*)at(ws, Ly.part), s);
   mark(6);

@@ -46,8 +46,22 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 constexpr float kGrowSum = 65536.0f;
 // Reference of a row that has seen no slot yet, in log2 units. Finite and small, so
 // scores offset by it keep their digits; a row still at kNoRef always takes the
-// exact-max rescale, which then sets a real reference.
+// exact-max rescale, which then sets the reference to the row's exact maximum (up or
+// down: its state is still zero). Only a step that hides every slot from the row
+// leaves it at kNoRef.
 constexpr float kNoRef = -100.0f;
+
+// Growth of a row's reference at a rescale, from the step's row maximum mx (in log2
+// units relative to the current reference m): never down once a slot has been read;
+// from kNoRef, exactly to the row maximum unless the step hid every slot from the row.
+__device__ __forceinline__ float ref_growth(float mx, float m) {
+  return m == kNoRef ? (mx > 0.5f * kNegBig ? mx : 0.f) : fmaxf(mx, 0.f);
+}
+// Factor of the running state at that rescale: a row still at kNoRef has a zero state,
+// and exp2(-growth) could overflow when the reference moves down.
+__device__ __forceinline__ float ref_rescale(float growth, float m) {
+  return m == kNoRef ? 0.f : fast_exp2(-growth);
+}
 
 // Document mask (packed sequences, Section 4.1): query i of sequence b, at position
 // ctx + i, reads cached slots from its document's first position on (clamped into
@@ -74,6 +88,7 @@ template <typename T> struct AttnArgs {
   const int32_t* doc;  // [B][T_new] first position of each token's document, or null
   T* O;
   int B, T_new, L, Hq, Hkv, S_cap, mask_paper, n_qtiles;
+  int gs, gq, ctx_hi;  // query i of sequence b sits at position ctx_len[b] + gq + gs i
   float scale_log2;  // log2(e) / sqrt(d)
   LayerTable chan;
 };
@@ -139,7 +154,8 @@ __device__ __forceinline__ void attend_block(
     const T* __restrict__ ks_, const T* __restrict__ vt_,
     const frag_t<T> (&qf)[PrefillCfg<T, DH>::QT][DH / 16], float (&m)[PrefillCfg<T, DH>::QT],
     float (&lsum)[PrefillCfg<T, DH>::QT], f32x16 (&o)[DH / 32][PrefillCfg<T, DH>::QT], int k0,
-    int wkend, int tq0, int incl, const int (&dlo)[PrefillCfg<T, DH>::QT], int h, int r) {
+    int wkend, int tq0, int gs, int incl, const int (&dlo)[PrefillCfg<T, DH>::QT], int h,
+    int r) {
   using C = PrefillCfg<T, DH>;
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
@@ -168,9 +184,10 @@ __device__ __forceinline__ void attend_block(
     for (int qt = 0; qt < C::QT; ++qt) {
       if (MASK) {
         // slot k0 + 32kt + 8(q/4) + 4h + q%4 is visible to the row at position t iff
-        // it is < t + incl and at least the row's document start
+        // it is < t + incl and at least the row's document start (row 32 qt + r of the
+        // wave sits at position tq0 + gs (32 qt + r))
         const int base = k0 + 32 * kt + 4 * h;
-        const int lim = tq0 + 32 * qt + r + incl - base, lo = dlo[qt] - base;
+        const int lim = tq0 + gs * (32 * qt + r) + incl - base, lo = dlo[qt] - base;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
           const int off = 8 * (q >> 2) + (q & 3);
@@ -191,8 +208,8 @@ __device__ __forceinline__ void attend_block(
         float mx = st[qt][0];
 #pragma unroll
         for (int q = 1; q < 16; ++q) mx = fmaxf(mx, st[qt][q]);
-        mx = fmaxf(halves_max(mx) - off[qt], 0.f);  // growth of the reference (never shrinks)
-        const float alpha = fast_exp2(-mx);
+        mx = ref_growth(halves_max(mx) - off[qt], m[qt]);  // growth of the reference
+        const float alpha = ref_rescale(mx, m[qt]);
         m[qt] += mx;
         lsum[qt] *= alpha;
 #pragma unroll
@@ -245,10 +262,11 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   const int c = a.chan.v[l];
   const int kvh = hq / (a.Hq / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, r = lane & 31;
-  const int ctx = __builtin_amdgcn_readfirstlane(a.ctx_len ? a.ctx_len[b] : 0);  // wave-uniform
+  const int ctx = __builtin_amdgcn_readfirstlane(ctx_at(a.ctx_len, b, a.ctx_hi));
   const int incl = a.mask_paper ? 0 : 1;
   const int q0 = qtile * C::BQ, qw0 = q0 + 32 * QT * w;
   const float cl2 = a.scale_log2;
+  const int gs = a.gs, pos0 = ctx + a.gq;  // query i sits at position pos0 + gs i
 
   // document mask: each row's first readable slot; the walk starts at the block holding
   // the workgroup's least one (base0), and slot indices below are relative to base0
@@ -259,7 +277,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       const int qi = qw0 + 32 * qt + r;
-      dlo[qt] = qi < a.T_new ? doc_first(a.doc, b, a.T_new, qi, ctx + qi) : 0;
+      dlo[qt] = qi < a.T_new ? doc_first(a.doc, b, a.T_new, qi, pos0 + gs * qi) : 0;
       wmin = min(wmin, qi < a.T_new ? dlo[qt] : 0x7fffffff);
       wlo_max = max(wlo_max, dlo[qt]);
     }
@@ -279,7 +297,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) dlo[qt] = 0;
   }
-  const int ctxr = ctx - base0, scap = a.S_cap - base0;
+  const int ctxr = pos0 - base0, scap = a.S_cap - base0;  // query 0's position from base0
 
   const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH +
                      (long)base0 * DH;
@@ -336,11 +354,11 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
   }
 
   const int qlast = min(q0 + C::BQ, a.T_new) - 1;
-  const int kend = min(ctxr + qlast + incl, scap);    // slots the workgroup may see
+  const int kend = min(ctxr + gs * qlast + incl, scap);    // slots the workgroup may see
   const int wq_last = min(qw0 + 32 * QT - 1, a.T_new - 1);
-  const int wkend = wq_last >= qw0 ? ctxr + wq_last + incl : 0;  // slots this wave may see
+  const int wkend = wq_last >= qw0 ? ctxr + gs * wq_last + incl : 0;  // slots this wave may see
   // slots in [wlo_max, wfree) are visible to all its rows
-  const int wfree = ctxr + qw0 + incl;
+  const int wfree = ctxr + gs * qw0 + incl;
   const int nblk = (kend + C::BKV - 1) / C::BKV;
 
   // staged next block: K fragments (row-major copy) and V fragments (row-major, bf16)
@@ -404,11 +422,11 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void attend_prefill_kernel(Attn
     fetch(k0 + C::BKV);
     if (k0 < wkend && k0 + C::BKV > wlo_min) {
       if (k0 + C::BKV > wfree || k0 < wlo_max)
-        attend_block<T, DH, true>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctxr + qw0, incl,
-                                  dlo, h, r);
+        attend_block<T, DH, true>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend,
+                                  ctxr + gs * qw0, gs, incl, dlo, h, r);
       else
-        attend_block<T, DH, false>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend, ctxr + qw0,
-                                   incl, dlo, h, r);
+        attend_block<T, DH, false>(Ks[buf], Vt[buf], qf, m, lsum, o, k0, wkend,
+                                   ctxr + gs * qw0, gs, incl, dlo, h, r);
     }
     stage(buf ^ 1);
     __syncthreads();
@@ -640,17 +658,17 @@ template <int N, int I0 = 0> __device__ __forceinline__ float tree_sum_arr(const
 // its slots here, before the exponentials. sn leaves holding S(i+1): its first MFMA
 // starts from st.nb (-m in every element), so no register is set per step. Two register
 // sets alternate between consecutive steps, so no step waits on the MFMAs it has just
-// issued. lim0 is the first tile's row limit; tile t's rows sit 32 t further; dlo[t] is
-// tile t's document start.
+// issued. lim0 is the first tile's row limit; tile t's rows sit tstride (32 times the
+// position stride between consecutive queries) further; dlo[t] is tile t's document start.
 template <int QT, int DH, bool DOC>
 __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, uint32_t kh_cur,
                                         uint32_t kh_nxt, uint32_t vh_prv, int i,
                                         const bf16x8 (&qf)[QT][DH / 16], PfState<QT, DH>& st,
                                         f32x16 (&sc)[QT], f32x16 (&sn)[QT], int lane, int lim0,
-                                        const int (&dlo)[QT], bool mask_cur) {
+                                        int tstride, const int (&dlo)[QT], bool mask_cur) {
   if (__builtin_expect(mask_cur, 0)) {
 #pragma unroll
-    for (int t = 0; t < QT; ++t) pf_mask<DOC>(sc[t], i, lim0 + 32 * t, dlo[t], lane);
+    for (int t = 0; t < QT; ++t) pf_mask<DOC>(sc[t], i, lim0 + tstride * t, dlo[t], lane);
   }
   // NG groups g, each: the MFMAs of PV(i-1) for keys 16(g / NDT).. and value tile
   // g % NDT and of S(i+1) for k16 step g, plus the weights of rows [q0(g), q0(g+1)) of
@@ -688,16 +706,17 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
     for (int q = 0; q < 16; ++q) st.pf[q >> 3][t][q & 7] = (bf16)sc[t][q];
     float ps = pf_wsum(st.pf[0][t], st.pf[1][t]);
     if (__builtin_expect(__any(!(ps <= kGrowSum) || st.m[t] == kNoRef), 0)) {
-      // rare: move the reference up to the exact row max (never down) and rescale the
-      // state; S(i+1) was started from the old reference, so it moves too
+      // rare: move the reference up to the exact row max (never down, but from kNoRef
+      // to it) and rescale the state; S(i+1) was started from the old reference, so it
+      // moves too
       f32x16 sr;
-      pf_init<DOC>(sr, -st.m[t], mask_cur, i, lim0 + 32 * t, dlo[t], lane);
+      pf_init<DOC>(sr, -st.m[t], mask_cur, i, lim0 + tstride * t, dlo[t], lane);
       sr = pf_scores<DH>(sm, lo, kh_cur, qf[t], sr);
       float mx = sr[0];
 #pragma unroll
       for (int q = 1; q < 16; ++q) mx = fmaxf(mx, sr[q]);
-      mx = fmaxf(halves_max(mx), 0.f);
-      const float alpha = fast_exp2(-mx);
+      mx = ref_growth(halves_max(mx), st.m[t]);
+      const float alpha = ref_rescale(mx, st.m[t]);
       st.m[t] += mx;
       st.lsum[t] *= alpha;
 #pragma unroll
@@ -735,10 +754,11 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
   const int kvh = hq / (a.Hq / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int ctx = __builtin_amdgcn_readfirstlane(a.ctx_len ? a.ctx_len[b] : 0);  // wave-uniform
+  const int ctx = __builtin_amdgcn_readfirstlane(ctx_at(a.ctx_len, b, a.ctx_hi));
   const int incl = a.mask_paper ? 0 : 1;
   const int q0 = qtile * P::BQ, qw0 = q0 + 32 * QT * w;
   const float cl2 = a.scale_log2;
+  const int gs = a.gs, pos0 = ctx + a.gq;  // query i sits at position pos0 + gs i
 
   // The queries and the dummy slot are loaded first and used only once the first copies
   // are issued, so their latency overlaps the ring set-up and the copies'.
@@ -793,7 +813,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       const int qi = qw0 + 32 * t + r;
-      dlo[t] = qi < a.T_new ? doc_first(a.doc, b, a.T_new, qi, ctx + qi) : 0;
+      dlo[t] = qi < a.T_new ? doc_first(a.doc, b, a.T_new, qi, pos0 + gs * qi) : 0;
       wmin = min(wmin, qi < a.T_new ? dlo[t] : 0x7fffffff);
       wlo_max = max(wlo_max, dlo[t]);
     }
@@ -812,21 +832,21 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
 #pragma unroll
     for (int t = 0; t < QT; ++t) dlo[t] = 0;
   }
-  const int ctxr = ctx - base0;  // the first new token's position relative to base0
+  const int ctxr = pos0 - base0;  // the first new token's position relative to base0
 
   const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH +
                      (long)base0 * DH;
   const int qlast = min(q0 + P::BQ, a.T_new) - 1;
   const int scap = a.S_cap - base0;
-  const int kend = min(ctxr + qlast + incl, scap);   // slots the workgroup may see
+  const int kend = min(ctxr + gs * qlast + incl, scap);   // slots the workgroup may see
   const int nblk = (kend + P::BKV - 1) / P::BKV;
   const int wq_last = min(qw0 + 32 * QT - 1, a.T_new - 1);
-  const int wkend = wq_last >= qw0 ? ctxr + wq_last + incl : 0;  // slots this wave may see
-  const int wfree = ctxr + qw0 + incl;  // slots < wfree are visible to all its rows ...
+  const int wkend = wq_last >= qw0 ? ctxr + gs * wq_last + incl : 0;  // slots this wave may see
+  const int wfree = ctxr + gs * qw0 + incl;  // slots < wfree are visible to all its rows ...
   // ... and at or past wlo_max (the document starts); a step is masked unless both hold
   auto masked = [&](int i) { return 32 * i + 32 > wfree || (DOC && 32 * i < wlo_max); };
   const int ilast = (wkend + 31) / 32 - 1;  // the wave's last 32-slot step (-1: none)
-  const int lim0 = ctxr + qw0 + r + incl;
+  const int lim0 = ctxr + gs * (qw0 + r) + incl, tstride = 32 * gs;
 
   // copies: wave w moves slot rows RPW w .. RPW w + RPW-1 of each K and V block, 1 KB
   // (64 chunks of 16 B) per instruction; lane x of instruction n fills LDS chunk
@@ -931,14 +951,14 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     if (i <= ilast + 1)
       pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
                       pf_vh<DH>((u + P::NS - 1) % P::NS, 1), i, qf, st, sa, sb, lane, lim0,
-                      dlo, masked(i));
+                      tstride, dlo, masked(i));
     // the second step reads K(j+1) and V(j): only the copies issued above may still be
     // in flight
     wait_vmcnt<2 * P::NI * (1 + AHEAD)>();
     __syncthreads();
     if (i + 1 <= ilast + 1)
       pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 1), pf_kh<DH>((u + 1) % P::NS, 0),
-                      pf_vh<DH>(u, 0), i + 1, qf, st, sb, sa, lane, lim0, dlo,
+                      pf_vh<DH>(u, 0), i + 1, qf, st, sb, sa, lane, lim0, tstride, dlo,
                       masked(i + 1));
   };
   for (int j = 0; j < nblk; j += P::NS) {
@@ -951,7 +971,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a) {
     const int u = nblk % P::NS;
     pf_step<QT, DH, DOC>(smem, lo, pf_kh<DH>(u, 0), pf_kh<DH>(u, 1),
                     pf_vh<DH>((u + P::NS - 1) % P::NS, 1), 2 * nblk, qf, st, sa, sb, lane, lim0,
-                    dlo, true);
+                    tstride, dlo, true);
   }
   wait_vmcnt<0>();  // no copy may land after the workgroup ends
 
@@ -983,7 +1003,7 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
   constexpr int BQ = PrefillCfg<T, 64>::BQ, NT = PrefillCfg<T, 64>::NT;
   static_assert(BQ == PrefillCfg<T, 32>::BQ && NT == PrefillCfg<T, 32>::NT, "tile shapes");
   AttnArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, doc, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
-                sh.mask_paper, (sh.T_new + BQ - 1) / BQ,
+                sh.mask_paper, (sh.T_new + BQ - 1) / BQ, sh.gs, sh.gq, sh.ctx_hi,
                 kLog2e / sqrtf((float)sh.d), chan_map};
   dim3 grid(a.n_qtiles * sh.Hq * sh.B * sh.L);
   if (sizeof(T) == 2 && (sh.d == 64 || sh.d == 96)) {  // fp32 at d = 96 fails validation
@@ -1015,7 +1035,7 @@ constexpr int kSplitMax = 4096, kSplitMin = 256;
 constexpr long kDecodeMinBlocks = 4096;
 
 int decode_split_len(const Shape& sh) {
-  const long kend = (long)sh.ctx_max + sh.T_new;  // upper bound on visible slots
+  const long kend = (long)sh.ctx_max + sh.span();  // upper bound on visible slots
   const long slices = (long)sh.k * sh.B * sh.Hkv;
   int len = kSplitMax;
   while (len > kSplitMin && slices * ((kend + len - 1) / len) < kDecodeMinBlocks) len /= 2;
@@ -1023,7 +1043,7 @@ int decode_split_len(const Shape& sh) {
 }
 
 int decode_splits(const Shape& sh) {
-  const long kend = (long)sh.ctx_max + sh.T_new;
+  const long kend = (long)sh.ctx_max + sh.span();
   const int len = decode_split_len(sh);
   int n = (int)((kend + len - 1) / len);
   return n < 1 ? 1 : n;
@@ -1041,6 +1061,7 @@ template <typename T> struct DecodeArgs {
   float* part;  // [L][B][Hq][T_new][nsplit][d + 2]: unnormalised o, m, l
   T* O;
   int B, T_new, L, Hq, Hkv, S_cap, mask_paper, nsplit, split_len;
+  int gs, gq, ctx_hi;  // query i of sequence b sits at position ctx_len[b] + gq + gs i
   float scale_log2;
   LayerTable chan;
   ChannelGroups cg;
@@ -1078,9 +1099,11 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
   if (nmem == 0) return;
   const int grp = a.Hq / a.Hkv;
   const int G = nmem * grp * a.T_new;
-  const int ctx = __builtin_amdgcn_readfirstlane(a.ctx_len ? a.ctx_len[b] : 0);  // wave-uniform
+  // position of query i: pos0 + gs i (wave-uniform)
+  const int pos0 = __builtin_amdgcn_readfirstlane(ctx_at(a.ctx_len, b, a.ctx_hi)) + a.gq;
+  const int gs = a.gs;
   const int incl = a.mask_paper ? 0 : 1;
-  const int kend = min(ctx + a.T_new - 1 + incl, a.S_cap);
+  const int kend = min(pos0 + gs * (a.T_new - 1) + incl, a.S_cap);
   const int s0 = split * a.split_len, s1 = min(s0 + a.split_len, kend);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int sg = lane / LPS, c8 = lane % LPS;
@@ -1111,8 +1134,8 @@ __global__ __launch_bounds__(256) void attend_decode_kernel(DecodeArgs<T> a) {
         int i = g % a.T_new, gq = (g / a.T_new) % grp, mi = g / (a.T_new * grp);
         int l = a.cg.members[off + mi], hq = kvh * grp + gq;
         long rowid = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + i;
-        vis[gi] = ctx + i + incl;
-        lov[gi] = doc_first(a.doc, b, a.T_new, i, ctx + i);
+        vis[gi] = pos0 + gs * i + incl;
+        lov[gi] = doc_first(a.doc, b, a.T_new, i, pos0 + gs * i);
         if (chunk) load8(a.Q + rowid * DH + 8 * c8, q[gi]);
         else {
 #pragma unroll
@@ -1298,8 +1321,8 @@ void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const Cha
                           hipStream_t s) {
   if (sh.N() <= 0) return;
   DecodeArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, doc, partials, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv,
-                  sh.S_cap, sh.mask_paper, decode_splits(sh), decode_split_len(sh),
-                  kLog2e / sqrtf((float)sh.d), chan_map, cg};
+                  sh.S_cap, sh.mask_paper, decode_splits(sh), decode_split_len(sh), sh.gs, sh.gq,
+                  sh.ctx_hi, kLog2e / sqrtf((float)sh.d), chan_map, cg};
   int maxmem = 0;
   for (int c = 0; c < sh.k; ++c) {
     int n = cg.offsets[c + 1] - cg.offsets[c];

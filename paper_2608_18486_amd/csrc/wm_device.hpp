@@ -173,6 +173,14 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// ctx_len[b] (NULL: 0) clamped into [0, hi]. The host checks that ctx_max plus the
+// positions a call's tokens span fits the cache and passes hi = S_cap minus that span, so
+// an entry outside its documented range [0, ctx_max] gives that sequence unspecified
+// results but never moves an access outside the cache.
+__device__ __forceinline__ int ctx_at(const int32_t* ctx_len, int b, int hi) {
+  return ctx_len ? min(max(ctx_len[b], 0), hi) : 0;
+}
+
 __device__ __forceinline__ f32x16 zero16() {
   f32x16 z;
 #pragma unroll

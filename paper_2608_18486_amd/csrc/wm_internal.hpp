@@ -19,7 +19,13 @@ struct Shape {
   int router_mode;   // 0 content-dependent router, 1 static weights (alpha = b), 2 no feedback
   float eps, rope_theta;
   int ctx_max;       // host-side bound on ctx_len[b] (sizes the attention grid)
+  // Token i of sequence b sits at position ctx_len[b] + gq + gs * i (a strided token
+  // group of Section 3.3: gs = g groups, gq = q; contiguous tokens: gs = 1, gq = 0).
+  int gs, gq;
+  int ctx_hi;        // device clamp of ctx_len[b]: S_cap minus the positions the call spans
   __host__ __device__ int N() const { return B * T_new; }
+  // positions covered by one sequence's new tokens: gq + gs (T_new - 1) + 1
+  __host__ __device__ long span() const { return T_new > 0 ? (long)gq + (long)gs * (T_new - 1) + 1 : 0; }
 };
 
 struct LayerTable {  // small per-call integer tables, passed by value
@@ -31,7 +37,7 @@ struct LayerTable {  // small per-call integer tables, passed by value
 template <typename T>
 void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStream_t s);
 
-// tab[n][m] = (cos, sin)(pos(n) * theta^(-2m/d)), pos(n) = ctx_len[b] + i, computed in fp64.
+// tab[n][m] = (cos, sin)(pos(n) * theta^(-2m/d)), pos(n) = ctx_len[b] + gq + gs i, in fp64.
 void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipStream_t s);
 
 // logits[br][n][o] = sum over stacked layers of W_alpha[br][o] . normed state + b_alpha[br][o]
@@ -50,7 +56,7 @@ template <typename T>
 void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, float* alpha,
                 T* mixed, float* rinv_mid, hipStream_t s);
 
-// mixed -> K (mid norm, W^K_j, key norm, RoPE) and V (mid norm, W^V_j) at slot ctx_len[b]+i.
+// mixed -> K (mid norm, W^K_j, key norm, RoPE) and V (mid norm, W^V_j) at slot pos(n).
 // wfold: workspace for the gain-folded weights, kv_fold_elems(sh) elements.
 size_t kv_fold_elems(const Shape& sh);
 template <typename T>

@@ -100,8 +100,8 @@ void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStr
 // once per block in double; each angle is formed and reduced modulo 2 pi in double, so
 // the float sincos that follows sees |r| <= pi and keeps float accuracy at any position.
 __global__ __launch_bounds__(256) void rope_table_kernel(const int32_t* ctx_len, int B,
-                                                         int T_new, int d, double theta,
-                                                         float* tab) {
+                                                         int T_new, int d, int gs, int gq,
+                                                         int ctx_hi, double theta, float* tab) {
   __shared__ double freq[kMaxHeadDim / 2];
   const int half = d / 2;
   for (int m = threadIdx.x; m < half; m += blockDim.x)
@@ -112,7 +112,8 @@ __global__ __launch_bounds__(256) void rope_table_kernel(const int32_t* ctx_len,
   const int m = (int)(idx % half);
   const long n = idx / half;
   const int b = (int)(n / T_new), i = (int)(n % T_new);
-  const double ang = (double)((ctx_len ? ctx_len[b] : 0) + i) * freq[m];
+  const long pos = (long)ctx_at(ctx_len, b, ctx_hi) + gq + (long)gs * i;
+  const double ang = (double)pos * freq[m];
   constexpr double kTwoPi = 6.283185307179586476925286766559;
   const float r = (float)(ang - kTwoPi * rint(ang / kTwoPi));
   float sn, cs;
@@ -125,7 +126,8 @@ void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipS
   long total = (long)sh.N() * (sh.d / 2);
   if (total <= 0) return;
   hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                     ctx_len, sh.B, sh.T_new, sh.d, (double)sh.rope_theta, tab);
+                     ctx_len, sh.B, sh.T_new, sh.d, sh.gs, sh.gq, sh.ctx_hi,
+                     (double)sh.rope_theta, tab);
 }
 
 // -------------------------------------------------------- GEMM operands
@@ -383,6 +385,7 @@ template <typename T, int DH> struct KVEpi {
   const float* tab;
   const int32_t* ctx_len;
   int M, T_new, B, Hkv, S_cap, k;
+  int gs, gq, ctx_hi;  // token i of sequence b goes to slot ctx_len[b] + gq + gs i
   float eps;
   using State = NoState;
   template <class C> __device__ void begin(int, int, int, State&) const {}
@@ -401,11 +404,11 @@ template <typename T, int DH> struct KVEpi {
         acc, ow0, nw0, lane, M, key, g_knorm + (long)j * DH,
         kTabLds ? (const float*)(lds.p + tab_off<C>()) : tab, kTabLds ? lds.n0 : 0, eps,
         [&](int n) { return rs[(long)g * M + n]; },
-        [&](int n) { return ctx_len ? ctx_len[n / T_new] : 0; },
-        [&](int n, int head, int ctx) -> T* {
+        [&](int n) { return ctx_at(ctx_len, n / T_new, ctx_hi) + gq; },
+        [&](int n, int head, int pos0) -> T* {
           if (head >= Hkv) return nullptr;
           const int b = n / T_new, i = n - b * T_new;
-          const long slot = (long)ctx + i;
+          const long slot = (long)pos0 + (long)gs * i;
           if (slot < 0 || slot >= S_cap) return nullptr;
           return base + ((((long)j * B + b) * Hkv + head) * S_cap + slot) * DH;
         },
@@ -1182,7 +1185,7 @@ static void kv_gemm(const Shape& sh, const T* mixed, const float* rinv_mid, cons
   PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
   T* trash = const_cast<T*>(wfold) + (kv_fold_elems(sh) - kTrashElems);
   KVEpi<T, DH> e{Kc, Vc, trash, rinv_mid, g_knorm, rope_tab, ctx_len, M, sh.T_new, sh.B,
-                 sh.Hkv, sh.S_cap, sh.k, sh.eps};
+                 sh.Hkv, sh.S_cap, sh.k, sh.gs, sh.gq, sh.ctx_hi, sh.eps};
   launch_proj<C, T>(M, Nout, K, 2 * sh.k, kNoSegments, 0, x, w, e, s);
 }
 

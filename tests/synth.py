@@ -241,3 +241,63 @@ def make_cache_device(w: Workload, device="cuda", sub: int = 24, fill=float("nan
                 T[j, b, :, :w.ctx].normal_(0.0, 1.0, generator=g)
                 T[j, b, :, w.ctx:].fill_(fill)
     return K, V
+
+
+def _unit_dirs(n, d, seed):
+    """n seeded unit vectors of length d (float64 rows)."""
+    u = torch.randn((n, d), generator=_gen(seed), dtype=torch.float64)
+    return u / u.norm(dim=1, keepdim=True)
+
+
+def make_peaked_attention(w: Workload, rise: float = 60.0, period: int = 256, a: float = 16.0,
+                          sub: int = 40):
+    """Queries and a cache whose attention scores climb steeply along the slots.
+
+    Q = a u + N(0, 1) and K[s] = beta(s) u + N(0, 1), with u a seeded unit vector per KV
+    head (query heads use their KV head's) and beta(s) a sawtooth over slots, rising
+    linearly through each `period` slots so that a beta(s) log2(e) / sqrt(d), the
+    score's trend in log2 units, climbs by `rise` per period. V ~ N(0, 1). Returns
+    Q [L, B, Hq, T_new, d] and Kc, Vc [k, B, Hkv, S_cap, d] with slots < w.ctx filled and
+    the rest NaN, in the workload dtype."""
+    s = w.seed * 100 + sub
+    u = _unit_dirs(w.Hkv, w.d, s)
+    grp = w.Hq // w.Hkv
+    beta_max = rise * w.d ** 0.5 / (a * 1.4426950408889634)
+    Q = torch.randn((w.L, w.B, w.Hq, w.T_new, w.d), generator=_gen(s + 1), dtype=torch.float64)
+    Q += a * u.repeat_interleave(grp, dim=0)[None, None, :, None, :]
+    shape = (w.k, w.B, w.Hkv, w.S_cap, w.d)
+    K = torch.full(shape, float("nan"), dtype=torch.float64)
+    V = torch.full(shape, float("nan"), dtype=torch.float64)
+    slots = torch.arange(w.ctx, dtype=torch.float64)
+    beta = beta_max * torch.remainder(slots, period) / (period - 1)
+    K[:, :, :, :w.ctx] = (torch.randn((w.k, w.B, w.Hkv, w.ctx, w.d), generator=_gen(s + 2),
+                                      dtype=torch.float64)
+                          + beta[None, None, None, :, None] * u[None, None, :, None, :])
+    V[:, :, :, :w.ctx] = torch.randn((w.k, w.B, w.Hkv, w.ctx, w.d), generator=_gen(s + 3),
+                                     dtype=torch.float64)
+    dt = w.torch_dtype
+    return Q.to(dt), K.to(dt), V.to(dt)
+
+
+def make_low_score_attention(w: Workload, level: float = -300.0, step: float = 4.0,
+                             floor: float = 40.0, a: float = 16.0, sub: int = 41):
+    """Queries and a cache whose scores all lie far below zero: Q = a u and K[s] =
+    -beta(s) u with u a seeded unit vector per KV head, beta(s) chosen so that the score
+    q.k log2(e) / sqrt(d) is `level` - min(step s, floor) log2 units (slot 0 the largest).
+    V ~ N(0, 1). Shapes and fill as make_peaked_attention."""
+    s = w.seed * 100 + sub
+    u = _unit_dirs(w.Hkv, w.d, s)
+    grp = w.Hq // w.Hkv
+    Q = (a * u.repeat_interleave(grp, dim=0))[None, None, :, None, :].expand(
+        w.L, w.B, w.Hq, w.T_new, w.d).clone()
+    shape = (w.k, w.B, w.Hkv, w.S_cap, w.d)
+    K = torch.full(shape, float("nan"), dtype=torch.float64)
+    V = torch.full(shape, float("nan"), dtype=torch.float64)
+    slots = torch.arange(w.ctx, dtype=torch.float64)
+    score = level - torch.clamp(step * slots, max=floor)
+    beta = -score * w.d ** 0.5 / (a * 1.4426950408889634)
+    K[:, :, :, :w.ctx] = -beta[None, None, None, :, None] * u[None, None, :, None, :]
+    V[:, :, :, :w.ctx] = torch.randn((w.k, w.B, w.Hkv, w.ctx, w.d), generator=_gen(s + 3),
+                                     dtype=torch.float64)
+    dt = w.torch_dtype
+    return Q.to(dt), K.to(dt), V.to(dt)

@@ -1,10 +1,11 @@
 """GPU parity: the HIP library (through its C ABI) against the fp64 CPU oracle.
 
 Tolerances (stated in the workloads' terms): fp32 max |gpu - ref| <= 1e-5;
-bf16 max |gpu - ref| / max |ref| <= 2e-2 per output tensor. Integer work (which
-slots are written, the channel each consumer reads) must match exactly: caches
-start as NaN sentinels and the set of slots the kernels wrote must equal the
-oracle's.
+bf16 max |gpu - ref| / max |ref| <= 2e-2 per output tensor and, per element,
+|gpu - ref| <= 2e-2 |ref| + 2e-2 rms(ref) for all but at most 0.1% of the elements
+(tests/parity.py). Integer work (which slots are written,
+the channel each consumer reads) must match exactly: caches start as NaN
+sentinels and the set of slots the kernels wrote must equal the oracle's.
 """
 import numpy as np
 import pytest
@@ -12,82 +13,10 @@ import torch
 
 import oracle
 from tests import synth
+from tests.parity import (TOL_BF16_REL, TOL_F32_ABS, _bias, _check_cache, _dev, _f64,  # noqa: F401
+                          _gdims, _odims, _written_mask, check_close, wm)
 
 pytestmark = pytest.mark.gpu
-
-TOL_F32_ABS = 1e-5
-TOL_BF16_REL = 2e-2
-
-
-@pytest.fixture(scope="module")
-def wm():
-    import paper_2608_18486_amd as wm
-    wm.lib()
-    assert torch.cuda.is_available(), "GPU tests need a GPU"
-    return wm
-
-
-def _f64(t):
-    return t.detach().to("cpu").double().numpy()
-
-
-def check_close(gpu, ref, dtype, name):
-    g = _f64(gpu) if torch.is_tensor(gpu) else np.asarray(gpu, dtype=np.float64)
-    r = np.asarray(ref, dtype=np.float64)
-    assert g.shape == r.shape, (name, g.shape, r.shape)
-    assert np.isfinite(g).all(), "%s: non-finite GPU output" % name
-    err = np.abs(g - r).max() if g.size else 0.0
-    if dtype == "f32":
-        assert err <= TOL_F32_ABS, "%s: max abs err %.3e > %.0e" % (name, err, TOL_F32_ABS)
-    else:
-        scale = np.abs(r).max() if r.size else 1.0
-        rel = err / max(scale, 1e-30)
-        assert rel <= TOL_BF16_REL, "%s: normwise rel err %.3e > %.0e" % (name, rel, TOL_BF16_REL)
-    return err
-
-
-def _odims(w, **kw):
-    base = dict(B=w.B, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d, p=w.p,
-                S_cap=w.S_cap)
-    base.update(kw)
-    return oracle.Dims(**base)
-
-
-def _gdims(wm, w, **kw):
-    base = dict(B=w.B, T_new=w.T_new, L=w.L, k=w.k, D=w.D, Hq=w.Hq, Hkv=w.Hkv, d=w.d, p=w.p,
-                S_cap=w.S_cap, ctx_max=w.ctx, dtype=wm.F32 if w.dtype == "f32" else wm.BF16)
-    base.update(kw)
-    return wm.make_dims(**base)
-
-
-def _dev(P):
-    return {k: v.cuda() for k, v in P.items()}
-
-
-def _bias(w):
-    return oracle.init_bias(w.L, w.k)
-
-
-def _written_mask(w, ctx):
-    """[B, S_cap] bool: the slots the step writes for each sequence."""
-    m = np.zeros((w.B, w.S_cap), dtype=bool)
-    for b in range(w.B):
-        m[b, ctx[b]:ctx[b] + w.T_new] = True
-    return m
-
-
-def _check_cache(Kg, Ko, Kin, w, ctx, dtype, name):
-    """Written slots within tolerance, every other slot bit-identical to the input, and
-    the NaN-sentinel write set equal to the oracle's."""
-    kg = _f64(Kg)
-    nan_g, nan_o = np.isnan(kg), np.isnan(Ko)
-    assert (nan_g == nan_o).all(), "%s: written slot set differs from the oracle's" % name
-    mask = _written_mask(w, ctx)[None, :, None, :, None]
-    mask = np.broadcast_to(mask, kg.shape)
-    check_close(kg[mask], Ko[mask], dtype, name + " (written slots)")
-    kin = _f64(Kin)
-    same = ~mask & ~np.isnan(kin)
-    assert (kg[same] == kin[same]).all(), "%s: a slot outside the write set changed" % name
 
 
 # ---------------------------------------------------------------- small cases
@@ -318,20 +247,27 @@ FULL = ["c2_T2048_L12_k12", "c3_T2048_L12_k6", "c4_T4096_L24_k12", "paper_T2048_
 
 
 def _sample_rows(w, b):
-    ls = sorted({0, w.L // 2, w.L - 1})
-    ts = sorted({0, 1, 63, 64, 255, 256, 1023, w.T_new // 2 + 7, w.T_new - 1})
+    ls = sorted({0, 1, w.L // 2, w.L - 2, w.L - 1})
+    ts = sorted({0, 1, 31, 63, 64, 255, 256, 1023, 1024, w.T_new // 2 + 7, w.T_new - 2,
+                 w.T_new - 1})
     return [(l * w.B + b) * w.T_new + t for l in ls for t in ts]
 
 
-@pytest.mark.parametrize("name", FULL)
-def test_full_sequence_step_at_full_size(wm, name):
+# (workload, mix mode, mask mode): every full-size pass in the paper's modes, and the
+# softmax-over-depth mix with the inclusive causal mask on the three bf16 passes
+FULL_CASES = [(n, 0, 0) for n in FULL] + [(n, 1, 1) for n in FULL[:3]]
+
+
+@pytest.mark.parametrize("name,mix_mode,mask_mode", FULL_CASES)
+def test_full_sequence_step_at_full_size(wm, name, mix_mode, mask_mode):
     """The full-size pass as the benchmark runs it; sampled sequences are re-computed by the
-    oracle (every cache slot of the sequence, sampled attention rows)."""
+    oracle (every cache slot of the sequence, sampled attention rows). The paper-mode pass
+    of the 24-layer 4096-token workload checks every one of its 4 sequences."""
     w = synth.WORKLOADS[name]
-    print("full", name, flush=True)
+    print("full", name, "mix", mix_mode, "mask", mask_mode, flush=True)
     P = synth.make_params(w, _bias(w))
     H = synth.make_states(w)
-    dims = _gdims(wm, w)
+    dims = _gdims(wm, w, mix_mode=mix_mode, mask_mode=mask_mode)
     Kg = torch.full((w.k, w.B, w.Hkv, w.S_cap, w.d), float("nan"), dtype=w.torch_dtype,
                     device="cuda")
     Vg = torch.full_like(Kg, float("nan"))
@@ -341,23 +277,30 @@ def test_full_sequence_step_at_full_size(wm, name):
     assert not torch.isnan(Kg[:, :, :, :w.T_new]).any()
     assert torch.isnan(Kg[:, :, :, w.T_new:]).all()
     PP = oracle.Params(P)
-    samples = (0, w.B - 1) if w.T_new * w.L <= 2048 * 12 else (w.B - 1,)
+    if name == "c4_T4096_L24_k12" and (mix_mode, mask_mode) == (0, 0):
+        samples = tuple(range(w.B))
+    elif w.T_new * w.L <= 2048 * 12 and (mix_mode, mask_mode) == (0, 0):
+        samples = (0, w.B - 1)
+    else:
+        samples = (w.B - 1,)
     for b in samples:
         w1 = synth.Workload(w.name, 1, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, 0, w.dtype,
                             w.chan_map, w.p, w.seed)
-        dm = _odims(w1)
+        dm = _odims(w1, mix_mode=mix_mode, mask_mode=mask_mode)
         Ko, Vo = oracle.empty_cache(dm)
         oracle.pool(dm, PP, H[b:b + 1], None, Ko, Vo)
-        check_close(Kg[:, b:b + 1, :, :w.T_new], Ko[:, :, :, :w.T_new], w.dtype, name + " K")
-        check_close(Vg[:, b:b + 1, :, :w.T_new], Vo[:, :, :, :w.T_new], w.dtype, name + " V")
+        check_close(Kg[:, b:b + 1, :, :w.T_new], Ko[:, :, :, :w.T_new], w.dtype,
+                    "%s K b=%d" % (name, b))
+        check_close(Vg[:, b:b + 1, :, :w.T_new], Vo[:, :, :, :w.T_new], w.dtype,
+                    "%s V b=%d" % (name, b))
         rows = _sample_rows(w1, 0)
         toks = sorted({r % w.T_new for r in rows})
         Qo = oracle.q_project(dm, PP, H[b:b + 1], None, toks)
         Oo = oracle.channel_attend(dm, PP, Qo, w.chan_map, None, Ko, Vo, rows)
         g = O[:, b].float().cpu().numpy()
-        for l in sorted({r // w.T_new for r in rows}):
-            for t in toks:
-                check_close(g[l, t], Oo[l, 0, t], w.dtype, "%s O l=%d t=%d b=%d" % (name, l, t, b))
+        ls = sorted({r // w.T_new for r in rows})
+        check_close(g[ls][:, toks], Oo[ls, 0][:, toks], w.dtype,
+                    "%s O b=%d (%d layers x %d positions)" % (name, b, len(ls), len(toks)))
 
 
 def test_decode_step_at_full_size(wm):

@@ -1,0 +1,189 @@
+"""GPU parity on peaked attention: inputs whose scores climb far above the running
+softmax reference while a row is walked, so every attention kernel must move its
+reference in the middle of a row and rescale the state it has accumulated (Section 3.1
+Step 3: a standard softmax over the visible slots; Section 3.2: the dummy slot starts
+the row).
+
+Each case first checks, from its own inputs (scores in fp64 from the same bf16/fp32
+values the kernels read), that the rescale condition occurs: a checked row's largest
+score exceeds every reference the kernel can hold after its first 32-slot step (the
+dummy score in the paper mask, the first 32 visible slots' maximum in both masks) by
+more than 17 log2 units, so some weight exceeds 2^16 against that reference and the
+kernel's rescale test must fire. The decode cases check it per 256-slot window (the
+split-S kernel restarts its state at every split, and splits are multiples of 256 slots).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests import synth
+from tests.parity import _bias, _dev, _f64, _gdims, _odims, check_close, wm  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+LOG2E = 1.4426950408889634
+RISE = 17.0   # log2 units above the first reference that a checked row must reach
+
+
+def _scores(Q, Kc, Kd, w, l, b, h, i, pos, mask_mode, lo):
+    """Row scores in log2 units: the dummy's (None in the inclusive mask) and the visible
+    slots' in order."""
+    c = w.chan_map[l]
+    kvh = h // (w.Hq // w.Hkv)
+    q = Q[l, b, h, i]
+    hi = pos + (1 if mask_mode == 1 else 0)
+    s = Kc[c, b, kvh, lo:hi] @ q * (LOG2E / np.sqrt(w.d))
+    dummy = float(Kd[c, kvh] @ q * (LOG2E / np.sqrt(w.d))) if mask_mode == 0 else None
+    return dummy, s
+
+
+def _rising_rows(Q, Kc, Kd, w, ctx, mask_mode, docs=None, rows=None):
+    """(rows checked, rows whose maximum is RISE above every first-step reference, the
+    largest |score| of those rows in log2 units)."""
+    n = hit = 0
+    smax = 0.0
+    for l in range(w.L):
+        for b in range(w.B):
+            for h in range(w.Hq):
+                for i in range(w.T_new):
+                    if rows is not None and (l, b, i) not in rows:
+                        continue
+                    pos = int(ctx[b]) + i
+                    lo = 0 if docs is None else min(max(int(docs[b, i]), 0), pos)
+                    dummy, s = _scores(Q, Kc, Kd, w, l, b, h, i, pos, mask_mode, lo)
+                    if s.size == 0:
+                        continue
+                    ref0 = s[:32].max() if dummy is None else max(dummy, s[:32].max())
+                    n += 1
+                    hit += s.max() - ref0 > RISE
+                    smax = max(smax, float(np.abs(s).max()))
+    return n, hit, smax
+
+
+def _windows_rise(Q, Kc, w, ctx, mask_mode):
+    """Decode rows: (the smallest, over rows and fully visible 256-slot windows, of the
+    window's maximum past its first 64 slots minus the maximum of those 64; the largest
+    |score| in log2 units)."""
+    worst = np.inf
+    smax = 0.0
+    for l in range(w.L):
+        for b in range(w.B):
+            for h in range(w.Hq):
+                for i in range(w.T_new):
+                    pos = int(ctx[b]) + i
+                    _, s = _scores(Q, Kc, np.zeros((w.k, w.Hkv, w.d)), w, l, b, h, i, pos, 1, 0)
+                    smax = max(smax, float(np.abs(s).max()))
+                    for w0 in range(0, pos - 255, 256):
+                        win = s[w0:w0 + 256]
+                        worst = min(worst, win[64:].max() - win[:64].max())
+    return worst, smax
+
+
+@pytest.mark.parametrize("T_new,ctx,lengths,period", [
+    (300, 0, None, 256),            # prefill, no cached context
+    (300, 0, [63, 65, 1, 128, 43], 64),  # prefill with packed documents
+    (70, 600, None, 256),           # chunked prefill over a cached context
+    (1, 9000, None, 256),           # decode: split-S over many splits, then the combine
+    (3, 9000, [5000, 4003], 256),   # decode with a document boundary inside the context
+])
+@pytest.mark.parametrize("mask_mode", [0, 1])
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 96), ("f32", 32)])
+def test_channel_attend_peaked(wm, T_new, ctx, lengths, period, mask_mode, dtype, d):
+    """Every attention kernel against the oracle on keys whose scores climb in a sawtooth
+    by 60 log2 units per period (the LDS-DMA prefill kernel at head dims 64 and 96, the
+    generic prefill kernel in fp32, the split-S decode kernels and their combine)."""
+    w = synth.small("peak_%s_d%d" % (dtype, d), B=2, T_new=T_new, L=5, k=3, D=64, Hq=4, Hkv=2,
+                    d=d, ctx=ctx + T_new, dtype=dtype, chan_map=[2, 0, 2, 2, 0])
+    print("peaked", dtype, d, T_new, ctx, lengths, mask_mode, flush=True)
+    P = synth.make_params(w, _bias(w))
+    Q, Kc, Vc = synth.make_peaked_attention(w, rise=60.0, period=period)
+    ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+    docs = (synth.make_doc_start(w, ctx_len, lengths=lengths) if lengths is not None else None)
+    Qn, Kn, Kdn = _f64(Q), _f64(Kc), _f64(P["Kd"])
+    dn = docs.numpy() if docs is not None else None
+    if T_new <= 4:
+        rise, smax = _windows_rise(Qn, Kn, w, ctx_len.numpy(), mask_mode)
+        assert rise > 9.0, "decode windows rise only %.1f log2 units" % rise
+    else:
+        n, hit, smax = _rising_rows(Qn, Kn, Kdn, w, ctx_len.numpy(), mask_mode, dn)
+        assert hit >= 0.2 * n, "only %d of %d rows rise %.0f log2 units" % (hit, n, RISE)
+    # fp32: the 1e-5 bound holds for scores no larger than unit-norm queries and keys give
+    # (sqrt(d)); rounding in a score grows with its size, so the bound scales with it
+    f32_scale = max(1.0, smax / LOG2E / np.sqrt(d))
+    Oo = oracle.channel_attend(_odims(w, mask_mode=mask_mode), P, Q, w.chan_map,
+                               ctx_len.numpy(), Kn, _f64(Vc), doc_start=dn)
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    dims = _gdims(wm, w, mask_mode=mask_mode, ctx_max=ctx)
+    wm.channel_attend(dims, _dev(P), Q.cuda(), w.chan_map, ctx_len.cuda(), Kc.cuda(),
+                      Vc.cuda(), O, doc_start=None if docs is None else docs.cuda())
+    torch.cuda.synchronize()
+    check_close(O, Oo, dtype, "peaked %s d%d T%d ctx%d mask%d" % (dtype, d, T_new, ctx,
+                                                                  mask_mode),
+                f32_scale=f32_scale)
+
+
+@pytest.mark.parametrize("name", ["bf16_d64", "bf16_d96_gqa", "f32_d32"])
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_layer_step_peaked(wm, name, mask_mode):
+    """The fused step with q-norm and key-norm gains of 4: the consumers' own queries and
+    the pooled keys give peaked attention (score spread about 23 log2 units)."""
+    w = {"bf16_d64": synth.small("pk_bf16_d64", B=2, T_new=300, L=4, k=2, D=128, Hq=2, Hkv=2,
+                                 d=64),
+         "bf16_d96_gqa": synth.small("pk_bf16_d96", B=2, T_new=260, L=4, k=3, D=192, Hq=6,
+                                     Hkv=3, d=96, p=2),
+         "f32_d32": synth.small("pk_f32_d32", B=1, T_new=200, L=3, k=2, D=64, Hq=2, Hkv=1,
+                                d=32, dtype="f32")}[name]
+    print("peaked step", name, mask_mode, flush=True)
+    P = synth.make_params(w, _bias(w))
+    P["g_qnorm"] = torch.full_like(P["g_qnorm"], 4.0)
+    P["g_knorm"] = torch.full_like(P["g_knorm"], 4.0)
+    H = synth.make_states(w)
+    dm = _odims(w, mask_mode=mask_mode)
+    PP = oracle.Params(P)
+    Ko, Vo = oracle.empty_cache(dm)
+    Oo = oracle.layer_step(dm, PP, H, w.chan_map, None, Ko, Vo)
+    Qo = oracle.q_project(dm, PP, H)
+    n, hit, smax = _rising_rows(Qo, Ko, PP.arrays["Kd"], w, np.zeros(w.B, dtype=np.int64),
+                                mask_mode)
+    assert hit >= 0.15 * n, "only %d of %d rows rise %.0f log2 units" % (hit, n, RISE)
+    # Peaked attention magnifies the rounding of the stored queries, keys and values to
+    # bf16 (the library keeps them in the workload dtype): the oracle alone measures that
+    # sensitivity by attending with its own Q, K, V rounded to bf16, and twice it is
+    # allowed on top of the usual bound. fp32 rounding in a score grows with its size.
+    slack = None
+    if w.dtype == "bf16":
+        rb = lambda a: torch.from_numpy(a).to(torch.bfloat16).double().numpy()  # noqa: E731
+        Or = oracle.channel_attend(dm, PP, rb(Qo), w.chan_map, None, rb(Ko), rb(Vo))
+        slack = 2.0 * np.abs(Or - Oo)
+    f32_scale = max(1.0, smax / LOG2E / np.sqrt(w.d))
+    Kg = torch.full((w.k, w.B, w.Hkv, w.S_cap, w.d), float("nan"), dtype=w.torch_dtype,
+                    device="cuda")
+    Vg = torch.full_like(Kg, float("nan"))
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+    wm.layer_step(_gdims(wm, w, mask_mode=mask_mode), _dev(P), H.cuda(), w.chan_map, None, Kg,
+                  Vg, O)
+    torch.cuda.synchronize()
+    check_close(Kg[:, :, :, :w.T_new], Ko[:, :, :, :w.T_new], w.dtype, name + " K")
+    check_close(O, Oo, w.dtype, "%s peaked O mask%d" % (name, mask_mode), slack=slack,
+                f32_scale=f32_scale)
+
+
+def test_inclusive_mask_very_low_scores(wm):
+    """Inclusive mask, every score of a row far below the kernels' initial reference
+    (about -300 log2 units): the first step must set the reference to the row's own
+    maximum, so the weights do not underflow to an all-zero row."""
+    for dtype, d in (("bf16", 64), ("bf16", 96), ("f32", 32)):
+        w = synth.small("low_%s_d%d" % (dtype, d), B=1, T_new=150, L=2, k=1, D=64, Hq=2, Hkv=1,
+                        d=d, ctx=150, dtype=dtype)
+        P = synth.make_params(w, _bias(w))
+        Q, Kc, Vc = synth.make_low_score_attention(w, level=-300.0)
+        Qn, Kn = _f64(Q), _f64(Kc)
+        _, s = _scores(Qn, Kn, None, w, 0, 0, 0, 100, 100, 1, 0)
+        assert s.max() < -250.0, s.max()
+        Oo = oracle.channel_attend(_odims(w, mask_mode=1), P, Q, w.chan_map, None, Kn, _f64(Vc))
+        O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=w.torch_dtype, device="cuda")
+        wm.channel_attend(_gdims(wm, w, mask_mode=1, ctx_max=0), _dev(P), Q.cuda(), w.chan_map,
+                          None, Kc.cuda(), Vc.cuda(), O)
+        torch.cuda.synchronize()
+        check_close(O, Oo, dtype, "low scores %s d%d" % (dtype, d))
