@@ -16,6 +16,15 @@ Arrays are numpy float64, C-contiguous, in the layouts below (N = B*T_new):
                                     is stored at slot ctx_len[b] + i
     Q       [L, B, Hq, T_new, d]    consumer queries after q-norm and RoPE
     O       [L, B, T_new, Hq*d]     attention output per consumer layer
+
+The fixed-point passes of Section 3.3 (jacobi, gauss_seidel, autoregressive) run
+on sequences that start empty (T = T_new positions) with a stand-in for the
+rest of each decoder block, h_{l+1} = h_l + W_o[l] o_l:
+
+    X       [B, T, D]               the state entering layer 0 (embedding)
+    W_o     [L, D, Hq*d]            the stand-in block's output projection
+    H       [B, T, L, D]            states entering every layer after the passes
+    h_top   [B, T, D]               the state leaving the top layer
 """
 from __future__ import annotations
 
@@ -296,3 +305,61 @@ def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, doc_start=None)
 
 def num_threads() -> int:
     return int(lib().wmo_num_threads())
+
+
+# ----------------------------------------------- Section 3.3: fixed-point passes
+
+def _pass_outputs(dims: Dims):
+    H = np.zeros((dims.B, dims.T_new, dims.L, dims.D))
+    top = np.zeros((dims.B, dims.T_new, dims.D))
+    Kc, Vc = empty_cache(dims)
+    return H, top, Kc, Vc
+
+
+def _pass_args(dims, params, W_o, chan_map, X):
+    assert dims.S_cap >= dims.T_new
+    P = _as_params(params)
+    W = _f64(W_o)
+    assert W.shape == (dims.L, dims.D, dims.Hq * dims.d)
+    X = _f64(X)
+    assert X.shape == (dims.B, dims.T_new, dims.D)
+    m = np.ascontiguousarray(np.asarray(chan_map, dtype=np.int32))
+    return P, W, m, X
+
+
+def jacobi(dims: Dims, params, W_o, chan_map, X, passes: int):
+    """Jacobi iteration (Section 3.3) with the stand-in decoder block
+    h_{l+1} = h_l + W_o[l] o_l: returns (H [B, T, L, D], h_top [B, T, D], Kc, Vc)."""
+    P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)
+    H, top, Kc, Vc = _pass_outputs(dims)
+    lib().wmo_jacobi(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(m), _ptr(X),
+                     ctypes.c_int(passes), _ptr(H), _ptr(top), _ptr(Kc), _ptr(Vc))
+    return H, top, Kc, Vc
+
+
+def gauss_seidel(dims: Dims, params, W_o, chan_map, X, g: int, passes: int):
+    """Cyclic Gauss-Seidel iteration over g strided groups (Section 3.3)."""
+    P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)
+    H, top, Kc, Vc = _pass_outputs(dims)
+    lib().wmo_gauss_seidel(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(m), _ptr(X),
+                           ctypes.c_int(g), ctypes.c_int(passes), _ptr(H), _ptr(top), _ptr(Kc),
+                           _ptr(Vc))
+    return H, top, Kc, Vc
+
+
+def autoregressive(dims: Dims, params, W_o, chan_map, X):
+    """Exact left-to-right evaluation (Section 3.2 order), the fixed point's solution."""
+    P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)
+    H, top, Kc, Vc = _pass_outputs(dims)
+    lib().wmo_autoregressive(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(m),
+                             _ptr(X), _ptr(H), _ptr(top), _ptr(Kc), _ptr(Vc))
+    return H, top, Kc, Vc
+
+
+def block_residual(dims: Dims, W_o, l: int, h, o) -> np.ndarray:
+    """The stand-in decoder block: h + W_o[l] o."""
+    W, h, o = _f64(W_o), _f64(h), _f64(o)
+    out = np.zeros(dims.D)
+    lib().wmo_block_residual(ctypes.byref(dims.c()), _ptr(W), ctypes.c_int(l), _ptr(h), _ptr(o),
+                             _ptr(out))
+    return out

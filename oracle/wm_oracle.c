@@ -560,3 +560,171 @@ int wmo_num_threads(void)
     return 1;
 #endif
 }
+
+/* ======================================= Section 3.3: the fixed-point passes
+ *
+ * The paper writes the exact solution as P = Pool(H), H = States(X; P): Pool
+ * is Steps 1-2 applied at every position, States the decoder stack applied at
+ * every position with each layer reading its channel of P. Here sequences
+ * start empty (positions 0 .. T-1, one document per sequence), T = T_new and
+ * S_cap >= T. Layouts: X[B][T][D] (the state entering layer 0 of each token,
+ * i.e. its embedding), H[B][T][L][D] (states entering every layer), h_top[B][T][D]
+ * (the state leaving the top layer), W_o[L][D][Hq*d].
+ *
+ * States needs the rest of each decoder block, which the method leaves
+ * unchanged. A stand-in stands for it: h_{l+1} = h_l + W_o[l] o_l, the output
+ * projection and residual of the attention sublayer, with o_l layer l's channel
+ * attention (query from h_l, Qwen3 query side) and no MLP.
+ */
+
+/* The stand-in block: h_next = h_l + W_o[l] o_l, o_l of length Hq*d. */
+void wmo_block_residual(const wmo_dims *dm, const double *W_o, int l, const double *h_l,
+                        const double *o_l, double *h_next)
+{
+    int D = dm->D, HD = dm->Hq * dm->d;
+    const double *W = W_o + (size_t)l * D * HD;
+    for (int e = 0; e < D; ++e) {
+        double a = 0.0;
+        for (int c = 0; c < HD; ++c)
+            a += W[(size_t)e * HD + c] * o_l[c];
+        h_next[e] = h_l[e] + a;
+    }
+}
+
+/* States at position i of sequence b: layers 0 .. L-1 in depth order, each
+ * attending channel map[l] over the cache as it stands (dummy + slots < i, or
+ * slots <= i in the inclusive mask). Writes the L states entering the layers to
+ * Hrow[L][D] and the state leaving the top layer to top[D]. */
+static void states_position(const wmo_dims *dm, const wmo_params *P, const double *W_o,
+                            const int *map, const double *x, int b, int i, const double *Kc,
+                            const double *Vc, double *Hrow, double *top)
+{
+    int L = dm->L, D = dm->D, Hq = dm->Hq, Hkv = dm->Hkv, d = dm->d, grp = Hq / Hkv;
+    int paper = dm->mask_mode == WMO_MASK_PAPER;
+    long nvis = paper ? i : i + 1;
+    double *q = (double *)malloc(sizeof(double) * Hq * d);
+    double *o = (double *)malloc(sizeof(double) * Hq * d);
+    memcpy(Hrow, x, sizeof(double) * D);
+    for (int l = 0; l < L; ++l) {
+        const double *h = Hrow + (size_t)l * D;
+        double *next = l + 1 < L ? Hrow + (size_t)(l + 1) * D : top;
+        int c = map[l];
+        wmo_query_token(dm, P, h, l, (double)i, q);
+        for (int hh = 0; hh < Hq; ++hh) {
+            int kvh = hh / grp;
+            size_t base = (((size_t)c * dm->B + b) * Hkv + kvh) * dm->S_cap * d;
+            const double *kd = paper ? P->Kd + ((size_t)c * Hkv + kvh) * d : NULL;
+            const double *vd = paper ? P->Vd + ((size_t)c * Hkv + kvh) * d : NULL;
+            wmo_attend_row(d, q + (size_t)hh * d, Kc + base, d, Vc + base, d, nvis, kd, vd,
+                           o + (size_t)hh * d);
+        }
+        wmo_block_residual(dm, W_o, l, h, o, next);
+    }
+    free(o);
+    free(q);
+}
+
+/* Pool at position i of sequence b (Steps 1-2): its L states -> cache slot i. */
+static void pool_position(const wmo_dims *dm, const wmo_params *P, const double *Hrow, int b,
+                          int i, double *Kc, double *Vc)
+{
+    int L = dm->L, k = dm->k, D = dm->D, KV = dm->k * dm->Hkv * dm->d;
+    double *al = (double *)malloc(sizeof(double) * 2 * k * L);
+    double *mx = (double *)malloc(sizeof(double) * 2 * k * D);
+    double *kt = (double *)malloc(sizeof(double) * KV);
+    double *vt = (double *)malloc(sizeof(double) * KV);
+    wmo_pool_mix_token(dm, P, Hrow, al, mx);
+    wmo_project_token(dm, P, mx, (double)i, kt, vt);
+    store_cache_rows(dm, b, i, kt, vt, Kc, Vc);
+    free(vt);
+    free(kt);
+    free(mx);
+    free(al);
+}
+
+/* H^(0): every layer's state is the token's embedding. */
+static void initial_states(const wmo_dims *dm, const double *X, double *H)
+{
+    int B = dm->B, T = dm->T_new, L = dm->L, D = dm->D;
+    for (int b = 0; b < B; ++b)
+        for (int i = 0; i < T; ++i)
+            for (int l = 0; l < L; ++l)
+                memcpy(H + (((size_t)b * T + i) * L + l) * D, X + ((size_t)b * T + i) * D,
+                       sizeof(double) * D);
+}
+
+/* Jacobi iteration, Section 3.3: H^(0) = embeddings; for t = 1 .. passes,
+ * P^(t) = Pool(H^(t-1)) at every position, then H^(t) = States(X; P^(t)) at
+ * every position. Returns H^(passes), its top states, and the cache P^(passes). */
+void wmo_jacobi(const wmo_dims *dm, const wmo_params *P, const double *W_o, const int *map,
+                const double *X, int passes, double *H, double *h_top, double *Kc, double *Vc)
+{
+    int B = dm->B, T = dm->T_new, L = dm->L, D = dm->D;
+    initial_states(dm, X, H);
+    for (int t = 1; t <= passes; ++t) {
+#pragma omp parallel for schedule(dynamic)
+        for (int n = 0; n < B * T; ++n)
+            pool_position(dm, P, H + (size_t)n * L * D, n / T, n % T, Kc, Vc);
+#pragma omp parallel for schedule(dynamic)
+        for (int n = 0; n < B * T; ++n)
+            states_position(dm, P, W_o, map, X + (size_t)n * D, n / T, n % T, Kc, Vc,
+                            H + (size_t)n * L * D, h_top + (size_t)n * D);
+    }
+}
+
+/* Cyclic Gauss-Seidel iteration, Section 3.3: the positions split into g
+ * strided groups G_q = {i : i mod g = q}. The cache starts as Pool(H^(0)); each
+ * pass evaluates G_0 .. G_{g-1} in order, and group q first recomputes the
+ * states of all its positions from the cache as it stands (so it reads the
+ * current pass's updates of groups < q and the previous pass's of the rest,
+ * its own included: a parallel Jacobi update within the group), then pools
+ * them into its slots. g = 1 reproduces Jacobi iteration (its cache ends one
+ * pool later: Pool(H^(passes))); g = T is autoregressive decoding. */
+void wmo_gauss_seidel(const wmo_dims *dm, const wmo_params *P, const double *W_o,
+                      const int *map, const double *X, int g, int passes, double *H,
+                      double *h_top, double *Kc, double *Vc)
+{
+    int B = dm->B, T = dm->T_new, L = dm->L, D = dm->D;
+    initial_states(dm, X, H);
+#pragma omp parallel for schedule(dynamic)
+    for (int n = 0; n < B * T; ++n)
+        pool_position(dm, P, H + (size_t)n * L * D, n / T, n % T, Kc, Vc);
+    for (int t = 1; t <= passes; ++t) {
+        for (int q = 0; q < g; ++q) {
+            int per = (T - q + g - 1) / g; /* positions q, q + g, ... below T */
+#pragma omp parallel for schedule(dynamic)
+            for (int u = 0; u < B * per; ++u) {
+                int b = u / per, i = q + g * (u % per);
+                size_t n = (size_t)b * T + i;
+                states_position(dm, P, W_o, map, X + n * D, b, i, Kc, Vc, H + n * L * D,
+                                h_top + n * D);
+            }
+#pragma omp parallel for schedule(dynamic)
+            for (int u = 0; u < B * per; ++u) {
+                int b = u / per, i = q + g * (u % per);
+                pool_position(dm, P, H + ((size_t)b * T + i) * L * D, b, i, Kc, Vc);
+            }
+        }
+    }
+}
+
+/* Exact left-to-right evaluation (Section 3.2): position by position, all L
+ * layers in depth order against the cache of the earlier positions, then one
+ * pool evaluation appends the position's channels. Defined in the paper's mask
+ * only: with the inclusive mask a position would read its own slot before its
+ * pool writes it. */
+void wmo_autoregressive(const wmo_dims *dm, const wmo_params *P, const double *W_o,
+                        const int *map, const double *X, double *H, double *h_top, double *Kc,
+                        double *Vc)
+{
+    int B = dm->B, T = dm->T_new, L = dm->L, D = dm->D;
+    for (int i = 0; i < T; ++i) {
+#pragma omp parallel for schedule(dynamic)
+        for (int b = 0; b < B; ++b) {
+            size_t n = (size_t)b * T + i;
+            states_position(dm, P, W_o, map, X + n * D, b, i, Kc, Vc, H + n * L * D,
+                            h_top + n * D);
+            pool_position(dm, P, H + n * L * D, b, i, Kc, Vc);
+        }
+    }
+}

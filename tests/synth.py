@@ -301,3 +301,13 @@ def make_low_score_attention(w: Workload, level: float = -300.0, step: float = 4
                                      dtype=torch.float64)
     dt = w.torch_dtype
     return Q.to(dt), K.to(dt), V.to(dt)
+
+
+def make_embeddings(w: Workload, sub: int = 50) -> torch.Tensor:
+    """Token states entering layer 0 (stand-ins for embeddings) X[B, T_new, D] ~ N(0, 1)."""
+    return _normal((w.B, w.T_new, w.D), 1.0, w.seed * 100 + sub, w.torch_dtype)
+
+
+def make_out_proj(w: Workload, sub: int = 51) -> torch.Tensor:
+    """Output projection of the stand-in decoder block, W_o[L, D, Hq*d] ~ N(0, 0.02)."""
+    return _normal((w.L, w.D, w.Hq * w.d), 0.02, w.seed * 100 + sub, w.torch_dtype)
