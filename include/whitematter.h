@@ -82,7 +82,10 @@ enum wm_op {
   WM_OP_KV_PROJECT = 1,
   WM_OP_Q_PROJECT = 2,
   WM_OP_CHANNEL_ATTEND = 3,
-  WM_OP_LAYER_STEP = 4
+  WM_OP_LAYER_STEP = 4,
+  WM_OP_POOL = 5,          /* wm_pool */
+  WM_OP_LAYER_ATTEND = 6,  /* wm_layer_attend */
+  WM_OP_PASSES = 7         /* wm_prefill_passes */
 };
 
 /* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
@@ -212,6 +215,60 @@ int wm_channel_attend_doc(const wm_dims *dims, const wm_params *params, const vo
 int wm_layer_step_doc(const wm_dims *dims, const wm_params *params, const void *H,
                       const int32_t *chan_map, const int32_t *ctx_len, const int32_t *doc_start,
                       void *Kc, void *Vc, void *O, void *ws, size_t ws_bytes,
+                      wm_stream_t stream);
+
+/* Section 3.1 Steps 1-2 fused: the pool of the call's tokens into their cache slots
+ * pos(b, i) (row norms, router, mix, mid norm, K/V projection, key norm, RoPE), with
+ * the mixed channels kept in the workspace. The same cache writes as wm_layer_step.
+ *   H        device [B][T_new][L][D] in dtype
+ *   ctx_len  device int32 [B] or NULL
+ *   Kc, Vc   device [k][B][Hkv][S_cap][d] in dtype (only the new slots are written)
+ * Uses g_pre, W_alpha (not with WM_ROUTER_STATIC), b_alpha, g_mid, Wk, Wv, g_knorm. */
+int wm_pool(const wm_dims *dims, const wm_params *params, const void *H, const int32_t *ctx_len,
+            void *Kc, void *Vc, void *ws, size_t ws_bytes, wm_stream_t stream);
+
+/* One consumer layer of Section 3.1 Step 3 on its own, as a depth-sequential decoder
+ * runs it (Sections 3.2, 3.3): the query of `layer` from h_layer = H[b][i][layer][:]
+ * (input norm, W^Q, q norm, RoPE at pos(b, i)), then attention over channel
+ * chan_map[layer] in the mask mode (dummy + slots < pos, or slots <= pos).
+ *   layer    0 <= layer < L
+ *   H        device [B][T_new][L][D] in dtype (only layer `layer` is read)
+ *   chan_map host int32 [L]
+ *   ctx_len  device int32 [B] or NULL
+ *   Kc, Vc   device [k][B][Hkv][S_cap][d] in dtype (read only)
+ *   O_l      device [B][T_new][Hq*d] in dtype
+ * Uses g_in, Wq, g_qnorm and (paper mask) Kd, Vd. */
+int wm_layer_attend(const wm_dims *dims, const wm_params *params, int32_t layer, const void *H,
+                    const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
+                    const void *Vc, void *O_l, void *ws, size_t ws_bytes, wm_stream_t stream);
+
+/* The fixed-point passes of Section 3.3 over sequences that start empty: P = Pool(H),
+ * H = States(X; P), solved by cyclic Gauss-Seidel iteration over g = dims->groups strided
+ * groups G_q = {i : i mod g = q} (g = 1: Jacobi iteration; g = T: one pass is exact
+ * left-to-right evaluation). H^(0) takes every layer's state to be the token's embedding
+ * and the cache starts as Pool(H^(0)); each pass evaluates G_0 .. G_{g-1} in order, and
+ * group q first recomputes the states of all its positions, layer by layer, from the
+ * cache as it stands (current-pass slots of groups < q, previous-pass slots of the rest),
+ * then pools them into its slots. States needs the rest of each decoder block, which the
+ * method leaves unchanged; a stand-in takes its place: h_{l+1} = h_l + W_o[l] o_l, the
+ * attention sublayer's output projection and residual, o_l = layer l's channel attention
+ * (wm_layer_attend), no MLP.
+ *   dims     T_new = T, the sequence length, a multiple of groups; group = 0; ctx_max = 0;
+ *            S_cap >= T. Every mode of dims applies (mask, mix, router).
+ *   W_o      device [L][D][Hq*d] in dtype: the stand-in block's output projections
+ *   X        device [B][T][D] in dtype: the state entering layer 0 (the embedding)
+ *   chan_map host int32 [L]
+ *   passes   >= 1
+ *   Kc, Vc   device [k][B][Hkv][S_cap][d] in dtype: slots [0, T) are written; at return
+ *            they hold Pool(H) of the returned states
+ *   H        device [B][T][L][D] in dtype: the states entering every layer after the passes
+ *   h_top    device [B][T][D] in dtype or NULL: the state leaving the top layer
+ * The workspace (wm_workspace_size(dims, WM_OP_PASSES)) holds the states group by group,
+ * B T L D elements, plus one group's scratch. Only the paper's mask has an exact
+ * left-to-right solution: with WM_MASK_INCLUSIVE a position reads its own slot. */
+int wm_prefill_passes(const wm_dims *dims, const wm_params *params, const void *W_o,
+                      const void *X, const int32_t *chan_map, int32_t passes, void *Kc,
+                      void *Vc, void *H, void *h_top, void *ws, size_t ws_bytes,
                       wm_stream_t stream);
 
 /* Measurement helper: wm_layer_step (doc_start NULL) or wm_layer_step_doc

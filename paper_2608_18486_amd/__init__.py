@@ -23,7 +23,8 @@ F32, BF16 = 0, 1
 MIX_LINEAR, MIX_SOFTMAX = 0, 1
 MASK_PAPER, MASK_INCLUSIVE = 0, 1
 ROUTER_DYNAMIC, ROUTER_STATIC, ROUTER_NOFEEDBACK = 0, 1, 2
-OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP = range(5)
+(OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP, OP_POOL,
+ OP_LAYER_ATTEND, OP_PASSES) = range(8)
 
 PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
                "Kd", "Vd", "g_in", "Wq", "g_qnorm")
@@ -75,6 +76,10 @@ def lib() -> ctypes.CDLL:
         "wm_layer_step_doc": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_layer_step_profiled": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp,
                                    _vp],
+        "wm_pool": [D, P, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_layer_attend": [D, P, ctypes.c_int32, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_prefill_passes": [D, P, _vp, _vp, _i32p, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp,
+                              _sz, _vp],
         "wm_validate": [D, ctypes.c_int, _i32p],
         "wm_channel_groups": [ctypes.c_int32, ctypes.c_int32, _i32p, _i32p, _i32p],
         "wm_default_map": [ctypes.c_int32, ctypes.c_int32, _i32p],
@@ -137,8 +142,10 @@ def _map(chan_map):
     return arr
 
 
-def _stream(stream) -> int:
+def _stream(stream) -> int | None:
     if stream is None:
+        if not torch.cuda.is_available():
+            return None  # the null stream: only calls that validation rejects get here
         stream = torch.cuda.current_stream()
     return stream.cuda_stream
 
@@ -155,6 +162,11 @@ def _params(params) -> ParamSet:
     return params if isinstance(params, ParamSet) else ParamSet(params)
 
 
+def _pref(params):
+    """ctypes reference to the parameters (None passes a NULL wm_params*)."""
+    return None if params is None else ctypes.byref(_params(params).c)
+
+
 def workspace_size(dims: Dims, op: int) -> int:
     return int(lib().wm_workspace_size(ctypes.byref(dims), op))
 
@@ -166,6 +178,8 @@ def workspace(dims: Dims, op: int, device="cuda") -> torch.Tensor:
 
 
 def _ws(dims, op, ws, device):
+    if device is None and ws is None and not torch.cuda.is_available():
+        return None, None, 0  # a call that validation rejects before any launch
     if device is None:
         device = "cuda"
     if ws is None:
@@ -248,6 +262,33 @@ def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws=None, str
         _check(lib().wm_layer_step_doc(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H),
                                        _map(chan_map), _ptr(ctx_len), _ptr(doc_start), _ptr(Kc),
                                        _ptr(Vc), _ptr(O), wp, wn, _stream(stream)))
+
+
+def pool(dims: Dims, params, H, ctx_len, Kc, Vc, ws=None, stream=None):
+    """Steps 1-2 fused: the call's tokens pooled into their cache slots."""
+    ws, wp, wn = _ws(dims, OP_POOL, ws, getattr(H, "device", None))
+    _check(lib().wm_pool(ctypes.byref(dims), _pref(params), _ptr(H), _ptr(ctx_len), _ptr(Kc),
+                         _ptr(Vc), wp, wn, _stream(stream)))
+
+
+def layer_attend(dims: Dims, params, layer: int, H, chan_map, ctx_len, Kc, Vc, O_l, ws=None,
+                 stream=None):
+    """One consumer layer: its query from H[:, :, layer] and its channel attention into
+    O_l [B, T_new, Hq*d]."""
+    ws, wp, wn = _ws(dims, OP_LAYER_ATTEND, ws, getattr(H, "device", None))
+    _check(lib().wm_layer_attend(ctypes.byref(dims), _pref(params), int(layer), _ptr(H),
+                                 _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O_l),
+                                 wp, wn, _stream(stream)))
+
+
+def prefill_passes(dims: Dims, params, W_o, X, chan_map, passes: int, Kc, Vc, H, h_top=None,
+                   ws=None, stream=None):
+    """Cyclic Gauss-Seidel passes (dims.groups groups; 1 = Jacobi) over sequences that start
+    empty, with the stand-in decoder block h_{l+1} = h_l + W_o[l] o_l."""
+    ws, wp, wn = _ws(dims, OP_PASSES, ws, getattr(X, "device", None))
+    _check(lib().wm_prefill_passes(ctypes.byref(dims), _pref(params), _ptr(W_o), _ptr(X),
+                                   _map(chan_map), int(passes), _ptr(Kc), _ptr(Vc), _ptr(H),
+                                   _ptr(h_top), wp, wn, _stream(stream)))
 
 
 PROFILE_EVENTS = 7

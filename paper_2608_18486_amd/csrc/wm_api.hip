@@ -34,7 +34,7 @@ bool decode_path(const wm_dims& d) { return d.T_new <= 4; }
 
 struct Layout {
   size_t rinv = 0, alpha = 0, mixed = 0, rinv_mid = 0, tab = 0, q = 0, part = 0, wkv = 0, wq = 0,
-         wa = 0, rpart = 0, total = 0;
+         wa = 0, rpart = 0, hg = 0, topg = 0, ol = 0, total = 0;
 };
 
 int group_stride(const wm_dims& d) { return d.groups > 1 ? d.groups : 1; }
@@ -71,9 +71,29 @@ wm::Shape make_shape(const wm_dims& d) {
   return s;
 }
 
+// The dims of one strided group of a pass-driver call (T_new = T / g tokens per sequence).
+wm_dims group_dims(const wm_dims& d, int q) {
+  wm_dims dg = d;
+  dg.T_new = d.T_new / group_stride(d);
+  dg.groups = group_stride(d);
+  dg.group = q;
+  dg.ctx_max = 0;
+  return dg;
+}
+
+// The shape of one consumer's attention: a single layer reading channel map[l].
+wm::Shape one_layer(wm::Shape sh) {
+  sh.L = 1;
+  return sh;
+}
+
 // Workspace regions for an op (offsets in bytes, each 256-byte aligned).
-Layout layout(const wm_dims& d, int op) {
+Layout layout(const wm_dims& dd, int op) {
   Layout Ly;
+  const bool passes = op == WM_OP_PASSES;
+  // the pass driver works on one group at a time: its scratch is sized by a group (the
+  // last one, whose positions reach furthest: the decode partials grow with them)
+  const wm_dims d = passes ? group_dims(dd, group_stride(dd) - 1) : dd;
   const size_t N = (size_t)d.B * d.T_new, es = elem_size(d);
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -82,18 +102,29 @@ Layout layout(const wm_dims& d, int op) {
     return at;
   };
   const bool all = op == WM_OP_LAYER_STEP;
-  if (op == WM_OP_ROUTER_MIX || op == WM_OP_Q_PROJECT || all) Ly.rinv = take(N * d.L * 4);
-  if (op == WM_OP_ROUTER_MIX || all) Ly.alpha = take(2 * N * d.k * d.L * 4);
-  if (all) Ly.mixed = take(2 * (size_t)d.k * N * d.D * es);
-  if (op == WM_OP_ROUTER_MIX || op == WM_OP_KV_PROJECT || all)
+  const bool pool = op == WM_OP_POOL || passes;  // the fused Steps 1-2
+  const bool layer = op == WM_OP_LAYER_ATTEND || passes;  // one consumer at a time
+  if (passes) {
+    Ly.hg = take((size_t)dd.B * dd.T_new * d.L * d.D * es);
+    Ly.topg = take((size_t)dd.B * dd.T_new * d.D * es);
+    Ly.ol = take(N * d.Hq * d.d * es);
+  }
+  if (op == WM_OP_ROUTER_MIX || op == WM_OP_Q_PROJECT || all || pool || layer)
+    Ly.rinv = take(N * d.L * 4);
+  if (op == WM_OP_ROUTER_MIX || all || pool) Ly.alpha = take(2 * N * d.k * d.L * 4);
+  if (all || pool) Ly.mixed = take(2 * (size_t)d.k * N * d.D * es);
+  if (op == WM_OP_ROUTER_MIX || op == WM_OP_KV_PROJECT || all || pool)
     Ly.rinv_mid = take(2 * (size_t)d.k * N * 4);
-  if (op == WM_OP_KV_PROJECT || op == WM_OP_Q_PROJECT || all) Ly.tab = take(N * d.d * 4);
+  if (op == WM_OP_KV_PROJECT || op == WM_OP_Q_PROJECT || all || pool || layer)
+    Ly.tab = take(N * d.d * 4);
   if (all) Ly.q = take((size_t)d.L * N * d.Hq * d.d * es);
+  if (layer) Ly.q = take(N * d.Hq * d.d * es);
   if ((op == WM_OP_CHANNEL_ATTEND || all) && decode_path(d))
     Ly.part = take(wm::decode_partials_bytes(make_shape(d)));
-  if (op == WM_OP_KV_PROJECT || all) Ly.wkv = take(wm::kv_fold_elems(make_shape(d)) * es);
-  if (op == WM_OP_Q_PROJECT || all) Ly.wq = take(wm::q_fold_elems(make_shape(d)) * es);
-  if (op == WM_OP_ROUTER_MIX || all) {
+  if (layer && decode_path(d)) Ly.part = take(wm::decode_partials_bytes(one_layer(make_shape(d))));
+  if (op == WM_OP_KV_PROJECT || all || pool) Ly.wkv = take(wm::kv_fold_elems(make_shape(d)) * es);
+  if (op == WM_OP_Q_PROJECT || all || layer) Ly.wq = take(wm::q_fold_elems(make_shape(d)) * es);
+  if (op == WM_OP_ROUTER_MIX || all || pool) {
     Ly.wa = take(wm::router_fold_elems(make_shape(d)) * es);
     Ly.rpart = take(wm::router_partials_bytes(make_shape(d)));
   }
@@ -102,13 +133,14 @@ Layout layout(const wm_dims& d, int op) {
 }
 
 bool uses_cache(int op) {
-  return op == WM_OP_KV_PROJECT || op == WM_OP_CHANNEL_ATTEND || op == WM_OP_LAYER_STEP;
+  return op == WM_OP_KV_PROJECT || op == WM_OP_CHANNEL_ATTEND || op == WM_OP_LAYER_STEP ||
+         op == WM_OP_POOL || op == WM_OP_LAYER_ATTEND || op == WM_OP_PASSES;
 }
 
 int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (!dp) return fail(WM_ERR_ARG, "dims is NULL");
   const wm_dims& d = *dp;
-  if (op < WM_OP_ROUTER_MIX || op > WM_OP_LAYER_STEP) return fail(WM_ERR_ARG, "unknown op %d", op);
+  if (op < WM_OP_ROUTER_MIX || op > WM_OP_PASSES) return fail(WM_ERR_ARG, "unknown op %d", op);
   if (d.dtype != WM_F32 && d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "unknown dtype %d", d.dtype);
   if (d.mix_mode != WM_MIX_LINEAR && d.mix_mode != WM_MIX_SOFTMAX)
     return fail(WM_ERR_DTYPE, "unknown mix_mode %d", d.mix_mode);
@@ -136,13 +168,16 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (d.groups < 0) return fail(WM_ERR_ARG, "groups must be >= 0");
   if (d.group < 0 || d.group >= group_stride(d))
     return fail(WM_ERR_ARG, "group must be in [0, groups)");
-  if ((long long)d.ctx_max + call_span(d) > INT_MAX / 2)
+  // positions the call covers: the pass driver's T_new is the whole sequence, the other
+  // calls place their tokens at group + groups i
+  const long long span = op == WM_OP_PASSES ? (long long)d.T_new : call_span(d);
+  if ((long long)d.ctx_max + span > INT_MAX / 2)
     return fail(WM_ERR_SHAPE, "positions past the 32-bit range");
   if (uses_cache(op)) {
     if (d.S_cap < 1) return fail(WM_ERR_SHAPE, "S_cap must be >= 1");
-    if ((long long)d.ctx_max + call_span(d) > d.S_cap)
+    if ((long long)d.ctx_max + span > d.S_cap)
       return fail(WM_ERR_CAPACITY, "ctx_max + the positions of the new tokens = %lld exceeds "
-                  "S_cap = %d", (long long)d.ctx_max + call_span(d), d.S_cap);
+                  "S_cap = %d", (long long)d.ctx_max + span, d.S_cap);
   }
   const long long N = (long long)d.B * d.T_new;
   if (N > (1LL << 30)) return fail(WM_ERR_SHAPE, "B * T_new too large");
@@ -161,7 +196,14 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
     for (double v : views)
       if (v >= lim) return fail(WM_ERR_SHAPE, "an operand spans more than 2 GiB (%.0f B)", v);
   }
-  if (op == WM_OP_ROUTER_MIX || op == WM_OP_LAYER_STEP) {
+  if (op == WM_OP_PASSES) {
+    if (d.group != 0) return fail(WM_ERR_ARG, "the pass driver runs every group: group must be 0");
+    if (d.T_new % group_stride(d) != 0)
+      return fail(WM_ERR_SHAPE, "the pass driver needs T_new a multiple of groups");
+    if (d.ctx_max != 0) return fail(WM_ERR_ARG, "the pass driver starts empty sequences: ctx_max 0");
+  }
+  if (op == WM_OP_ROUTER_MIX || op == WM_OP_LAYER_STEP || op == WM_OP_POOL ||
+      op == WM_OP_PASSES) {
     size_t lds = wm::mix_smem_bytes(d.L, d.k, d.D, elem_size(d));
     if (lds > 65536) return fail(WM_ERR_SHAPE, "L * D too large for the mix kernel (%zu B of LDS)", lds);
   }
@@ -312,6 +354,107 @@ int run_layer_step(const wm_dims& d, const wm_params& P, const T* H, const int32
   run_attend<T>(d, P, Q, chan_map, ctx_len, doc, Kc, Vc, O, (float*)at(ws, Ly.part), s);
   mark(6);
   return WM_OK;
+}
+
+// Steps 1-2 for the call's tokens: row norms (unless have_rinv), angle table (unless
+// have_tab), router, mix, K/V projection into the cache. prefolded: the workspace already
+// holds the gain-folded router and K/V weights.
+template <typename T>
+void run_pool(const wm_dims& d, const wm_params& P, const T* H, const int32_t* ctx_len, T* Kc,
+              T* Vc, const Layout& Ly, void* ws, hipStream_t s, bool have_rinv, bool have_tab,
+              bool prefolded) {
+  wm::Shape sh = make_shape(d);
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* alpha = (float*)at(ws, Ly.alpha);
+  T* mixed = (T*)at(ws, Ly.mixed);
+  float* rinv_mid = (float*)at(ws, Ly.rinv_mid);
+  float* tab = (float*)at(ws, Ly.tab);
+  if (!have_rinv) wm::launch_row_rms<T>(H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
+  if (!have_tab) wm::launch_rope_table(sh, ctx_len, tab, s);
+  wm::launch_router<T>(sh, router_layers(d), H, rinv, (const T*)P.g_pre, (const T*)P.W_alpha,
+                       (const T*)P.b_alpha, alpha, (T*)at(ws, Ly.wa), (float*)at(ws, Ly.rpart),
+                       s, prefolded);
+  wm::launch_mix<T>(sh, H, rinv, (const T*)P.g_pre, alpha, mixed, rinv_mid, s);
+  wm::launch_kv_project<T>(sh, mixed, rinv_mid, (const T*)P.g_mid, (const T*)P.Wk,
+                           (const T*)P.Wv, (const T*)P.g_knorm, tab, ctx_len, Kc, Vc,
+                           (T*)at(ws, Ly.wkv), s, prefolded);
+}
+
+// Consumer l alone: input norm of h_l = H[..][l][..], W^Q_l, q norm, RoPE (angle table
+// unless have_tab), then attention over channel chan_map[l] into O_l [B][T_new][Hq d].
+// q_prefolded: the workspace already holds the gain-folded query weights of every layer.
+template <typename T>
+void run_layer_attend(const wm_dims& d, const wm_params& P, int l, const T* H,
+                      const int32_t* chan_map, const int32_t* ctx_len, const T* Kc, const T* Vc,
+                      T* O_l, const Layout& Ly, void* ws, hipStream_t s, bool have_tab,
+                      bool q_prefolded) {
+  wm::Shape sh = make_shape(d);
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* tab = (float*)at(ws, Ly.tab);
+  T* Q = (T*)at(ws, Ly.q);
+  T* wq = (T*)at(ws, Ly.wq);
+  wm::launch_row_rms_strided<T>(H + (long)l * sh.D, sh.N(), sh.D, (long)sh.L * sh.D, sh.L, sh.eps,
+                                rinv + l, s);
+  if (!have_tab) wm::launch_rope_table(sh, ctx_len, tab, s);
+  if (!q_prefolded) wm::launch_q_fold<T>(sh, (const T*)P.g_in, (const T*)P.Wq, wq, l, 1, s);
+  wm::launch_q_layers<T>(sh, H, rinv, (const T*)P.g_qnorm, tab, Q, wq, l, 1, s);
+  const wm::Shape sh1 = one_layer(sh);
+  wm::LayerTable mt{};
+  mt.v[0] = chan_map[l];
+  if (decode_path(d)) {
+    wm::ChannelGroups cg{};
+    wm_channel_groups(1, d.k, &chan_map[l], cg.offsets, cg.members);
+    wm::launch_attend_decode<T>(sh1, mt, cg, Q, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len,
+                                nullptr, (float*)at(ws, Ly.part), O_l, s);
+  } else {
+    wm::launch_attend_prefill<T>(sh1, mt, Q, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len,
+                                 nullptr, O_l, s);
+  }
+}
+
+// Section 3.3: the cache starts as Pool(H^(0)) (every layer's state the embedding X);
+// each pass runs the g strided groups in order, and group q first recomputes the states
+// of its positions layer by layer (its consumers' attention over the cache as it stands,
+// then the stand-in block h_{l+1} = h_l + W_o[l] o_l), then pools them into its slots.
+template <typename T>
+void run_passes(const wm_dims& d, const wm_params& P, const T* W_o, const T* X,
+                const int32_t* chan_map, int passes, T* Kc, T* Vc, T* H, T* h_top, void* ws,
+                hipStream_t s) {
+  const int g = group_stride(d), Tg = d.T_new / g, L = d.L, D = d.D, HD = d.Hq * d.d;
+  const Layout Ly = layout(d, WM_OP_PASSES);
+  const wm::Shape sh0 = make_shape(group_dims(d, 0));
+  T* Hg = (T*)at(ws, Ly.hg);
+  T* topg = (T*)at(ws, Ly.topg);
+  T* Ol = (T*)at(ws, Ly.ol);
+  const long gsz = (long)d.B * Tg * L * D;  // one group's states
+  wm::launch_router_fold<T>(sh0, router_layers(d), (const T*)P.g_pre, (const T*)P.W_alpha,
+                            (T*)at(ws, Ly.wa), s);
+  wm::launch_kv_fold<T>(sh0, (const T*)P.g_mid, (const T*)P.Wk, (const T*)P.Wv,
+                        (T*)at(ws, Ly.wkv), s);
+  wm::launch_q_fold<T>(sh0, (const T*)P.g_in, (const T*)P.Wq, (T*)at(ws, Ly.wq), 0, L, s);
+  wm::launch_group_gather<T>(X, Hg, d.B, d.T_new, g, L, D, s);
+  for (int q = 0; q < g; ++q)
+    run_pool<T>(group_dims(d, q), P, Hg + q * gsz, nullptr, Kc, Vc, Ly, ws, s, false, false,
+                true);
+  for (int t = 0; t < passes; ++t) {
+    for (int q = 0; q < g; ++q) {
+      const wm_dims dq = group_dims(d, q);
+      T* Hq = Hg + q * gsz;
+      wm::launch_rope_table(make_shape(dq), nullptr, (float*)at(ws, Ly.tab), s);
+      for (int l = 0; l < L; ++l) {
+        run_layer_attend<T>(dq, P, l, Hq, chan_map, nullptr, Kc, Vc, Ol, Ly, ws, s, true, true);
+        const bool last = l + 1 == L;
+        wm::launch_block_residual<T>(d.B * Tg, D, HD, Ol, W_o + (long)l * D * HD,
+                                     Hq + (long)l * D, (long)L * D,
+                                     last ? topg + (long)q * d.B * Tg * D : Hq + (long)(l + 1) * D,
+                                     last ? D : (long)L * D, s);
+      }
+      // every layer's row norms are already current: only the pool remains
+      run_pool<T>(dq, P, Hq, nullptr, Kc, Vc, Ly, ws, s, true, true, true);
+    }
+  }
+  wm::launch_group_scatter<T>(Hg, H, d.B, d.T_new, g, (long)L * D, s);
+  if (h_top) wm::launch_group_scatter<T>(topg, h_top, d.B, d.T_new, g, D, s);
 }
 
 int check_params(const wm_params* P, std::initializer_list<int> which) {
@@ -559,6 +702,91 @@ int wm_layer_step_profiled(const wm_dims* dims, const wm_params* params, const v
   if ((uintptr_t)doc_start % 4 != 0) return fail(WM_ERR_ARG, "doc_start is not 4-byte aligned");
   return layer_step_impl(dims, params, H, chan_map, ctx_len, doc_start, Kc, Vc, O, ws, ws_bytes,
                          stream, events);
+}
+
+int wm_pool(const wm_dims* dims, const wm_params* params, const void* H, const int32_t* ctx_len,
+            void* Kc, void* Vc, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  WM_TRY(validate_dims(dims, WM_OP_POOL, nullptr));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  if (d.router_mode == WM_ROUTER_STATIC)
+    WM_TRY(check_params(params, {P_GPRE, P_BA, P_GMID, P_WK, P_WV, P_GKN}));
+  else
+    WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN}));
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(check_ws(d, WM_OP_POOL, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  const Layout Ly = layout(d, WM_OP_POOL);
+  if (d.dtype == WM_BF16)
+    run_pool<bf16>(d, *params, (const bf16*)H, ctx_len, (bf16*)Kc, (bf16*)Vc, Ly, ws, s, false,
+                   false, false);
+  else
+    run_pool<float>(d, *params, (const float*)H, ctx_len, (float*)Kc, (float*)Vc, Ly, ws, s,
+                    false, false, false);
+  return launched();
+}
+
+int wm_layer_attend(const wm_dims* dims, const wm_params* params, int32_t layer, const void* H,
+                    const int32_t* chan_map, const int32_t* ctx_len, const void* Kc,
+                    const void* Vc, void* O_l, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_LAYER_ATTEND, chan_map));
+  const wm_dims& d = *dims;
+  if (layer < 0 || layer >= d.L) return fail(WM_ERR_ARG, "layer %d is outside [0, L)", layer);
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_GIN, P_WQ, P_GQN, P_KD, P_VD}));
+  else WM_TRY(check_params(params, {P_GIN, P_WQ, P_GQN}));
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(need_ptr(O_l, "O_l"));
+  WM_TRY(check_ws(d, WM_OP_LAYER_ATTEND, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  const Layout Ly = layout(d, WM_OP_LAYER_ATTEND);
+  if (d.dtype == WM_BF16)
+    run_layer_attend<bf16>(d, *params, layer, (const bf16*)H, chan_map, ctx_len, (const bf16*)Kc,
+                           (const bf16*)Vc, (bf16*)O_l, Ly, ws, s, false, false);
+  else
+    run_layer_attend<float>(d, *params, layer, (const float*)H, chan_map, ctx_len,
+                            (const float*)Kc, (const float*)Vc, (float*)O_l, Ly, ws, s, false,
+                            false);
+  return launched();
+}
+
+int wm_prefill_passes(const wm_dims* dims, const wm_params* params, const void* W_o,
+                      const void* X, const int32_t* chan_map, int32_t passes, void* Kc, void* Vc,
+                      void* H, void* h_top, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_PASSES, chan_map));
+  const wm_dims& d = *dims;
+  if (passes < 1) return fail(WM_ERR_ARG, "passes must be >= 1");
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  if (d.router_mode == WM_ROUTER_STATIC)
+    WM_TRY(check_params(params, {P_GPRE, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD, P_GIN,
+                                 P_WQ, P_GQN}));
+  else
+    WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD,
+                                 P_GIN, P_WQ, P_GQN}));
+  WM_TRY(need_ptr(W_o, "W_o"));
+  WM_TRY(need_ptr(X, "X"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(need_ptr(H, "H"));
+  if (h_top && (uintptr_t)h_top % 16 != 0) return fail(WM_ERR_ARG, "h_top is not 16-byte aligned");
+  WM_TRY(check_ws(d, WM_OP_PASSES, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  if (d.dtype == WM_BF16)
+    run_passes<bf16>(d, *params, (const bf16*)W_o, (const bf16*)X, chan_map, passes, (bf16*)Kc,
+                     (bf16*)Vc, (bf16*)H, (bf16*)h_top, ws, s);
+  else
+    run_passes<float>(d, *params, (const float*)W_o, (const float*)X, chan_map, passes,
+                      (float*)Kc, (float*)Vc, (float*)H, (float*)h_top, ws, s);
+  return launched();
 }
 
 }  // extern "C"

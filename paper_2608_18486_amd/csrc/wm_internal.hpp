@@ -36,6 +36,10 @@ struct LayerTable {  // small per-call integer tables, passed by value
 // rinv[r] = 1 / sqrt(mean(X[r][:]^2) + eps) for rows of length D.
 template <typename T>
 void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStream_t s);
+// rows at X + r * xs, results at rinv[r * os]
+template <typename T>
+void launch_row_rms_strided(const T* X, long rows, int D, long xs, long os, float eps,
+                            float* rinv, hipStream_t s);
 
 // tab[n][m] = (cos, sin)(pos(n) * theta^(-2m/d)), pos(n) = ctx_len[b] + gq + gs i, in fp64.
 void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipStream_t s);
@@ -45,10 +49,14 @@ void launch_rope_table(const Shape& sh, const int32_t* ctx_len, float* tab, hipS
 // part: router_partials_bytes(sh) bytes of split-K partial sums (may be 0).
 size_t router_fold_elems(const Shape& sh);
 size_t router_partials_bytes(const Shape& sh);
+// prefolded: wfold already holds launch_router_fold's output for these weights
+template <typename T>
+void launch_router_fold(const Shape& sh, const LayerTable& sel, const T* g_pre, const T* W_alpha,
+                        T* wfold, hipStream_t s);
 template <typename T>
 void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
                    const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits, T* wfold,
-                   float* part, hipStream_t s);
+                   float* part, hipStream_t s, bool prefolded = false);
 
 // alpha (in: logits [2][N][k*L], out: mixing weights) -> mixed[2][k][N][D], rinv_mid[2][k][N]
 size_t mix_smem_bytes(int L, int k, int D, size_t elem_bytes);
@@ -60,9 +68,13 @@ void launch_mix(const Shape& sh, const T* H, const float* rinv, const T* g_pre, 
 // wfold: workspace for the gain-folded weights, kv_fold_elems(sh) elements.
 size_t kv_fold_elems(const Shape& sh);
 template <typename T>
+void launch_kv_fold(const Shape& sh, const T* g_mid, const T* Wk, const T* Wv, T* wfold,
+                    hipStream_t s);
+template <typename T>
 void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, const T* g_mid,
                        const T* Wk, const T* Wv, const T* g_knorm, const float* rope_tab,
-                       const int32_t* ctx_len, T* Kc, T* Vc, T* wfold, hipStream_t s);
+                       const int32_t* ctx_len, T* Kc, T* Vc, T* wfold, hipStream_t s,
+                       bool prefolded = false);
 
 // H -> Q[L][B][Hq][T_new][d] (input norm, W^Q_l, q norm, RoPE); wfold: q_fold_elems(sh).
 size_t q_fold_elems(const Shape& sh);
@@ -70,6 +82,28 @@ template <typename T>
 void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g_in,
                       const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q, T* wfold,
                       hipStream_t s);
+// the same in two parts: fold the input-norm gains of layers l0 .. l0 + nl - 1 into their
+// slots of wfold (layer l at l Hq d D), then project layers l0 .. l0 + nl - 1 into
+// Q[nl][B][Hq][T_new][d]
+template <typename T>
+void launch_q_fold(const Shape& sh, const T* g_in, const T* Wq, T* wfold, int l0, int nl,
+                   hipStream_t s);
+template <typename T>
+void launch_q_layers(const Shape& sh, const T* H, const float* rinv, const T* g_qnorm,
+                     const float* rope_tab, T* Q, const T* wfold, int l0, int nl, hipStream_t s);
+
+// -- pass driver (Section 3.3) --------------------------------------------------
+// The stand-in decoder block: out[n] = h[n] + W o_l[n] (W [D][HD], o_l [M][HD]); rows of h
+// and out strided by hs and os elements.
+template <typename T>
+void launch_block_residual(int M, int D, int HD, const T* o_l, const T* W, const T* h, long hs,
+                           T* out, long os, hipStream_t s);
+// Group-major states: Hg[q][b][m][l][e] for position q + g m (T a multiple of g).
+template <typename T>
+void launch_group_gather(const T* X, T* Hg, int B, int T_len, int g, int L, int D,
+                         hipStream_t s);
+template <typename T>
+void launch_group_scatter(const T* Yg, T* Y, int B, int T_len, int g, long row, hipStream_t s);
 
 // -- consumer side (Step 3) ---------------------------------------------------
 struct ChannelGroups {       // CSR inverse of the consumer -> channel map

@@ -21,14 +21,15 @@
 namespace wm {
 
 // ----------------------------------------------------------------- row rms
+// Row r of length D starts at X + r * xs; its 1/RMS goes to rinv[r * os].
 // One wave per row, any D.
 template <typename T>
-__global__ __launch_bounds__(256) void row_rms_loop_kernel(const T* X, long rows, int D,
-                                                           float eps, float* rinv) {
+__global__ __launch_bounds__(256) void row_rms_loop_kernel(const T* X, long rows, int D, long xs,
+                                                           long os, float eps, float* rinv) {
   const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
-  const T* x = X + row * D;
+  const T* x = X + row * xs;
   float ss = 0.f;
   for (int e = lane * 8; e < D; e += 512) {
     float v[8];
@@ -37,15 +38,15 @@ __global__ __launch_bounds__(256) void row_rms_loop_kernel(const T* X, long rows
     for (int i = 0; i < 8; ++i) ss += v[i] * v[i];
   }
   ss = wave_sum(ss);
-  if (lane == 0) rinv[row] = 1.0f / sqrtf(ss / (float)D + eps);
+  if (lane == 0) rinv[row * os] = 1.0f / sqrtf(ss / (float)D + eps);
 }
 
 // One wave per R rows of at most 512 NC elements; a lane loads its NC chunks of 8 from
 // each of them before any arithmetic, so a wave has R NC loads in flight (one row of
 // 1-1.5 KB per wave left the HBM read stream short of loads in flight).
 template <typename T, int R, int NC>
-__global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int D, float eps,
-                                                      float* rinv) {
+__global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int D, long xs,
+                                                      long os, float eps, float* rinv) {
   const long row0 = ((long)blockIdx.x * 4 + (threadIdx.x >> 6)) * R;
   const int lane = threadIdx.x & 63;
   if (row0 >= rows) return;
@@ -55,7 +56,7 @@ __global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int e = lane * 8 + 512 * c;
-      if (row0 + q < rows && e < D) load8(X + (row0 + q) * D + e, v[q][c]);
+      if (row0 + q < rows && e < D) load8(X + (row0 + q) * xs + e, v[q][c]);
       else
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[q][c][i] = 0.f;
@@ -68,7 +69,7 @@ __global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int
 #pragma unroll
       for (int i = 0; i < 8; ++i) ss += v[q][c][i] * v[q][c][i];
     ss = wave_sum(ss);
-    if (lane == 0 && row0 + q < rows) rinv[row0 + q] = 1.0f / sqrtf(ss / (float)D + eps);
+    if (lane == 0 && row0 + q < rows) rinv[(row0 + q) * os] = 1.0f / sqrtf(ss / (float)D + eps);
   }
 }
 
@@ -76,23 +77,29 @@ __global__ __launch_bounds__(256) void row_rms_kernel(const T* X, long rows, int
 #define WM_RMS_ROWS 2
 #endif
 template <typename T, int NC>
-static void launch_row_rms_nc(const T* X, long rows, int D, float eps, float* rinv,
-                              hipStream_t s) {
+static void launch_row_rms_nc(const T* X, long rows, int D, long xs, long os, float eps,
+                              float* rinv, hipStream_t s) {
   constexpr int R = WM_RMS_ROWS;
   hipLaunchKernelGGL((row_rms_kernel<T, R, NC>), dim3((unsigned)((rows + 4 * R - 1) / (4 * R))),
-                     dim3(256), 0, s, X, rows, D, eps, rinv);
+                     dim3(256), 0, s, X, rows, D, xs, os, eps, rinv);
+}
+
+template <typename T>
+void launch_row_rms_strided(const T* X, long rows, int D, long xs, long os, float eps,
+                            float* rinv, hipStream_t s) {
+  if (rows <= 0) return;
+  const int nc = (D + 511) / 512;  // chunks of 8 per lane (D is a multiple of 8)
+  if (nc <= 1) launch_row_rms_nc<T, 1>(X, rows, D, xs, os, eps, rinv, s);
+  else if (nc == 2) launch_row_rms_nc<T, 2>(X, rows, D, xs, os, eps, rinv, s);
+  else if (nc <= 4) launch_row_rms_nc<T, 4>(X, rows, D, xs, os, eps, rinv, s);
+  else
+    hipLaunchKernelGGL(row_rms_loop_kernel<T>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
+                       X, rows, D, xs, os, eps, rinv);
 }
 
 template <typename T>
 void launch_row_rms(const T* X, long rows, int D, float eps, float* rinv, hipStream_t s) {
-  if (rows <= 0) return;
-  const int nc = (D + 511) / 512;  // chunks of 8 per lane (D is a multiple of 8)
-  if (nc <= 1) launch_row_rms_nc<T, 1>(X, rows, D, eps, rinv, s);
-  else if (nc == 2) launch_row_rms_nc<T, 2>(X, rows, D, eps, rinv, s);
-  else if (nc <= 4) launch_row_rms_nc<T, 4>(X, rows, D, eps, rinv, s);
-  else
-    hipLaunchKernelGGL(row_rms_loop_kernel<T>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
-                       X, rows, D, eps, rinv);
+  launch_row_rms_strided<T>(X, rows, D, D, 1, eps, rinv, s);
 }
 
 // -------------------------------------------------------------- rope table
@@ -431,6 +438,7 @@ template <typename T, int DH> struct QEpi {
   const T* g_qnorm;
   const float* tab;
   int M, T_new, B, Hq, L;
+  int l0;  // group g of the launch is consumer layer l0 + g; Q holds the launch's layers
   float eps;
   using State = NoState;
   template <class C> __device__ void begin(int, int, int, State&) const {}
@@ -440,9 +448,9 @@ template <typename T, int DH> struct QEpi {
   __device__ void finish(int l, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane,
                          State&, const EpiLds& lds) const {
     head_epilogue<T, DH, C::WO, C::WN, false, kTabLds>(
-        acc, ow0, nw0, lane, M, true, g_qnorm + (long)l * DH,
+        acc, ow0, nw0, lane, M, true, g_qnorm + (long)(l0 + l) * DH,
         kTabLds ? (const float*)lds.p : tab, kTabLds ? lds.n0 : 0, eps,
-        [&](int n) { return rs[(long)n * L + l]; }, [](int) { return 0; },
+        [&](int n) { return rs[(long)n * L + l0 + l]; }, [](int) { return 0; },
         [&](int n, int head, int) -> T* {
           if (head >= Hq) return nullptr;
           const int b = n / T_new, i = n - b * T_new;
@@ -671,9 +679,19 @@ static void router_gemm(const Shape& sh, const LayerTable& sel, const T* H, cons
 }
 
 template <typename T>
+void launch_router_fold(const Shape& sh, const LayerTable& sel, const T* g_pre, const T* W_alpha,
+                        T* wfold, hipStream_t s) {
+  if (sh.router_mode == 1) return;  // static weights: no router
+  const long total = (long)router_fold_elems(sh) / 8;
+  hipLaunchKernelGGL(router_fold_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                     s, W_alpha, g_pre, sel, sh.k * sh.L, sh.L, sh.Lp, sh.D,
+                     sh.router_mode == 2 ? 1 : 0, wfold);
+}
+
+template <typename T>
 void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
                    const T* g_pre, const T* W_alpha, const T* b_alpha, float* logits, T* wfold,
-                   float* part, hipStream_t s) {
+                   float* part, hipStream_t s, bool prefolded) {
   const int M = sh.N();
   if (M <= 0) return;
   if (sh.router_mode == 1) {  // static weights: no router, the logits are the bias
@@ -682,10 +700,7 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
                        b_alpha, M, sh.k * sh.L, logits);
     return;
   }
-  const long total = (long)router_fold_elems(sh) / 8;
-  hipLaunchKernelGGL(router_fold_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
-                     s, W_alpha, g_pre, sel, sh.k * sh.L, sh.L, sh.Lp, sh.D,
-                     sh.router_mode == 2 ? 1 : 0, wfold);
+  if (!prefolded) launch_router_fold<T>(sh, sel, g_pre, W_alpha, wfold, s);
   if (M <= kFewTokens) router_gemm<T, true>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
   else router_gemm<T, false>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
 }
@@ -1190,12 +1205,19 @@ static void kv_gemm(const Shape& sh, const T* mixed, const float* rinv_mid, cons
 }
 
 template <typename T>
+void launch_kv_fold(const Shape& sh, const T* g_mid, const T* Wk, const T* Wv, T* wfold,
+                    hipStream_t s) {
+  fold_gain<T>(Wk, Wv, sh.k, g_mid, wfold, 2 * sh.k, sh.Hkv * sh.d, sh.D, s);
+}
+
+template <typename T>
 void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, const T* g_mid,
                        const T* Wk, const T* Wv, const T* g_knorm, const float* rope_tab,
-                       const int32_t* ctx_len, T* Kc, T* Vc, T* wfold, hipStream_t s) {
+                       const int32_t* ctx_len, T* Kc, T* Vc, T* wfold, hipStream_t s,
+                       bool prefolded) {
   const int M = sh.N();
   if (M <= 0) return;
-  fold_gain<T>(Wk, Wv, sh.k, g_mid, wfold, 2 * sh.k, sh.Hkv * sh.d, sh.D, s);
+  if (!prefolded) launch_kv_fold<T>(sh, g_mid, Wk, Wv, wfold, s);
   const bool few = M <= kFewTokens;
   if (sh.d == 96) {
     if constexpr (sizeof(T) == 2) {  // fp32 at d = 96 is rejected by validation
@@ -1211,52 +1233,203 @@ void launch_kv_project(const Shape& sh, const T* mixed, const float* rinv_mid, c
   }
 }
 
+// Layers l0 .. l0 + nl - 1; wfold holds the folded weights of all L layers (layer l at
+// l * Hq d * D) followed by the trash area; Q receives [nl][B][Hq][T_new][d].
 template <typename T, int DH, bool FEW>
 static void q_gemm(const Shape& sh, const T* H, const float* rinv, const T* wfold,
-                   const T* g_qnorm, const float* rope_tab, T* Q, hipStream_t s) {
+                   const T* g_qnorm, const float* rope_tab, T* Q, int l0, int nl, hipStream_t s) {
   using C = typename ProjShapeD<T, FEW, DH, true>::C;
   const int M = sh.N(), Nout = sh.Hq * DH, K = sh.D;
-  PlainRows<T> x{H, K, (long)sh.L * K, M};
-  PlainRows<T> w{wfold, (long)Nout * K, K, Nout};
+  PlainRows<T> x{H + (long)l0 * K, K, (long)sh.L * K, M};
+  PlainRows<T> w{wfold + (long)l0 * Nout * K, (long)Nout * K, K, Nout};
   T* trash = const_cast<T*>(wfold) + (q_fold_elems(sh) - kTrashElems);
-  QEpi<T, DH> e{Q, trash, rinv, g_qnorm, rope_tab, M, sh.T_new, sh.B, sh.Hq, sh.L, sh.eps};
-  launch_proj<C, T>(M, Nout, K, sh.L, kNoSegments, 0, x, w, e, s);
+  QEpi<T, DH> e{Q, trash, rinv, g_qnorm, rope_tab, M, sh.T_new, sh.B, sh.Hq, sh.L, l0, sh.eps};
+  launch_proj<C, T>(M, Nout, K, nl, kNoSegments, 0, x, w, e, s);
+}
+
+template <typename T>
+void launch_q_fold(const Shape& sh, const T* g_in, const T* Wq, T* wfold, int l0, int nl,
+                   hipStream_t s) {
+  const long per = (long)sh.Hq * sh.d * sh.D;
+  fold_gain<T>(Wq + l0 * per, Wq + l0 * per, nl, g_in + (long)l0 * sh.D, wfold + l0 * per, nl,
+               sh.Hq * sh.d, sh.D, s);
+}
+
+template <typename T>
+void launch_q_layers(const Shape& sh, const T* H, const float* rinv, const T* g_qnorm,
+                     const float* rope_tab, T* Q, const T* wfold, int l0, int nl,
+                     hipStream_t s) {
+  const int M = sh.N();
+  if (M <= 0 || nl <= 0) return;
+  // few tokens, or a grid of large tiles that would not cover the chip: small tiles
+  using CL = typename ProjShape<T, false>::C;
+  const long big = (long)nl * ((M + CL::NTOK - 1) / CL::NTOK) *
+                   ((sh.Hq * sh.d + CL::OT - 1) / CL::OT);
+  const bool few = M <= kFewTokens || big < 128;
+  if (sh.d == 96) {
+    if constexpr (sizeof(T) == 2) {
+      if (few) q_gemm<T, 96, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, l0, nl, s);
+      else q_gemm<T, 96, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, l0, nl, s);
+    }
+  } else if (sh.d == 64) {
+    if (few) q_gemm<T, 64, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, l0, nl, s);
+    else q_gemm<T, 64, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, l0, nl, s);
+  } else {
+    if (few) q_gemm<T, 32, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, l0, nl, s);
+    else q_gemm<T, 32, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, l0, nl, s);
+  }
 }
 
 template <typename T>
 void launch_q_project(const Shape& sh, const T* H, const float* rinv, const T* g_in,
                       const T* Wq, const T* g_qnorm, const float* rope_tab, T* Q, T* wfold,
                       hipStream_t s) {
-  const int M = sh.N();
-  if (M <= 0) return;
-  fold_gain<T>(Wq, Wq, sh.L, g_in, wfold, sh.L, sh.Hq * sh.d, sh.D, s);
-  const bool few = M <= kFewTokens;
-  if (sh.d == 96) {
-    if constexpr (sizeof(T) == 2) {
-      if (few) q_gemm<T, 96, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
-      else q_gemm<T, 96, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
+  if (sh.N() <= 0) return;
+  launch_q_fold<T>(sh, g_in, Wq, wfold, 0, sh.L, s);
+  launch_q_layers<T>(sh, H, rinv, g_qnorm, rope_tab, Q, wfold, 0, sh.L, s);
+}
+
+// ------------------------------------------------- pass driver (Section 3.3)
+// The stand-in for the rest of a decoder block: h_{l+1} = h_l + W_o[l] o_l (output
+// projection and residual of the attention sublayer). GEMM C^T = W_o o_l^T; lane (h, r)
+// of a 32 x 32 block holds token n and output channels o = 32 i + 8 (q/4) + 4h + q%4,
+// 4 consecutive channels per register quad, added to h_l and stored 4 at a time.
+template <typename T> __device__ __forceinline__ void load4(const T* p, float* out);
+template <> __device__ __forceinline__ void load4<bf16>(const bf16* p, float* out) {
+  const bf16x4 v = *(const bf16x4*)p;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = (float)v[i];
+}
+template <> __device__ __forceinline__ void load4<float>(const float* p, float* out) {
+  const f32x4 v = *(const f32x4*)p;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = v[i];
+}
+
+template <typename T> struct ResidEpi {
+  static constexpr bool kUsesLds = false;
+  const T* h;   // h_l, row n at h + n * hs
+  T* out;       // h_{l+1}, row n at out + n * os
+  long hs, os;
+  int M, Nout;
+  using State = NoState;
+  template <class C> __device__ void begin(int, int, int, State&) const {}
+  template <class C>
+  __device__ void segment(int, int, int, f32x16 (&)[C::WO][C::WN], int, State&) const {}
+  template <class C>
+  __device__ void finish(int, int ow0, int nw0, f32x16 (&acc)[C::WO][C::WN], int lane, State&,
+                         const EpiLds&) const {
+    const int hh = lane >> 5, r = lane & 31;
+#pragma unroll
+    for (int jn = 0; jn < C::WN; ++jn) {
+      const int n = nw0 + 32 * jn + r;
+      if (n >= M) continue;
+#pragma unroll
+      for (int i = 0; i < C::WO; ++i)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int o = ow0 + 32 * i + 8 * q4 + 4 * hh;
+          if (o >= Nout) continue;
+          float v[4];
+          load4<T>(h + (long)n * hs + o, v);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] += acc[i][jn][4 * q4 + t];
+          store4(out + (long)n * os + o, v);
+        }
     }
-  } else if (sh.d == 64) {
-    if (few) q_gemm<T, 64, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
-    else q_gemm<T, 64, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
-  } else {
-    if (few) q_gemm<T, 32, true>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
-    else q_gemm<T, 32, false>(sh, H, rinv, wfold, g_qnorm, rope_tab, Q, s);
   }
+};
+
+template <typename T>
+void launch_block_residual(int M, int D, int HD, const T* o_l, const T* W, const T* h, long hs,
+                           T* out, long os, hipStream_t s) {
+  if (M <= 0) return;
+  PlainRows<T> x{o_l, 0, HD, M};
+  PlainRows<T> w{W, 0, HD, D};
+  ResidEpi<T> e{h, out, hs, os, M, D};
+  using CL = typename ProjShape<T, false>::C;
+  using CS = typename ProjShape<T, true>::C;
+  const long big = (long)((M + CL::NTOK - 1) / CL::NTOK) * ((D + CL::OT - 1) / CL::OT);
+  if (big >= 128) launch_proj<CL, T>(M, D, HD, 1, kNoSegments, 0, x, w, e, s);
+  else launch_proj<CS, T>(M, D, HD, 1, kNoSegments, 0, x, w, e, s);
+}
+
+// The pass driver keeps the states of a group contiguous: Hg[q][b][m][l][e] is the state
+// entering layer l at position i = q + g m of sequence b (T a multiple of g, Tg = T / g).
+// gather: Hg[q][b][m][l] = X[b][i] for every layer l (H^(0): each token's embedding).
+template <typename T>
+__global__ __launch_bounds__(256) void group_gather_kernel(const T* X, T* Hg, int B, int T_len,
+                                                           int g, int L, int D) {
+  const int Tg = T_len / g, c8 = D / 8;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)B * T_len * L * c8) return;
+  long r = idx;
+  const int e = (int)(r % c8) * 8;
+  r /= c8;
+  r /= L;  // the layer: every layer gets the same state
+  const int m = (int)(r % Tg);
+  r /= Tg;
+  const int b = (int)(r % B), q = (int)(r / B);
+  st_frag<T>(Hg + idx * 8, ld_frag<T>(X + ((long)b * T_len + q + (long)g * m) * D + e));
+}
+// scatter: Y[b][i][row] = Yg[q][b][m][row] for rows of R * D elements (R = L for the
+// states, 1 for the top states).
+template <typename T>
+__global__ __launch_bounds__(256) void group_scatter_kernel(const T* Yg, T* Y, int B, int T_len,
+                                                            int g, long row) {
+  const int Tg = T_len / g;
+  const long c8 = row / 8;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)B * T_len * c8) return;
+  long r = idx;
+  const long e = (r % c8) * 8;
+  r /= c8;
+  const int m = (int)(r % Tg);
+  r /= Tg;
+  const int b = (int)(r % B), q = (int)(r / B);
+  st_frag<T>(Y + ((long)b * T_len + q + (long)g * m) * row + e, ld_frag<T>(Yg + idx * 8));
+}
+
+template <typename T>
+void launch_group_gather(const T* X, T* Hg, int B, int T_len, int g, int L, int D,
+                         hipStream_t s) {
+  const long n = (long)B * T_len * L * (D / 8);
+  if (n <= 0) return;
+  hipLaunchKernelGGL(group_gather_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     X, Hg, B, T_len, g, L, D);
+}
+template <typename T>
+void launch_group_scatter(const T* Yg, T* Y, int B, int T_len, int g, long row, hipStream_t s) {
+  const long n = (long)B * T_len * (row / 8);
+  if (n <= 0) return;
+  hipLaunchKernelGGL(group_scatter_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     Yg, Y, B, T_len, g, row);
 }
 
 #define WM_INST(T)                                                                             \
   template void launch_row_rms<T>(const T*, long, int, float, float*, hipStream_t);            \
+  template void launch_row_rms_strided<T>(const T*, long, int, long, long, float, float*,      \
+                                          hipStream_t);                                        \
+  template void launch_router_fold<T>(const Shape&, const LayerTable&, const T*, const T*, T*, \
+                                      hipStream_t);                                            \
   template void launch_router<T>(const Shape&, const LayerTable&, const T*, const float*,      \
                                  const T*, const T*, const T*, float*, T*, float*,             \
-                                 hipStream_t);                                                 \
+                                 hipStream_t, bool);                                           \
   template void launch_mix<T>(const Shape&, const T*, const float*, const T*, float*, T*,      \
                               float*, hipStream_t);                                            \
+  template void launch_kv_fold<T>(const Shape&, const T*, const T*, const T*, T*, hipStream_t); \
   template void launch_kv_project<T>(const Shape&, const T*, const float*, const T*, const T*, \
                                      const T*, const T*, const float*, const int32_t*, T*, T*, \
-                                     T*, hipStream_t);                                         \
+                                     T*, hipStream_t, bool);                                   \
+  template void launch_q_fold<T>(const Shape&, const T*, const T*, T*, int, int, hipStream_t); \
+  template void launch_q_layers<T>(const Shape&, const T*, const float*, const T*,             \
+                                   const float*, T*, const T*, int, int, hipStream_t);         \
   template void launch_q_project<T>(const Shape&, const T*, const float*, const T*, const T*,  \
-                                    const T*, const float*, T*, T*, hipStream_t);
+                                    const T*, const float*, T*, T*, hipStream_t);              \
+  template void launch_block_residual<T>(int, int, int, const T*, const T*, const T*, long,    \
+                                         T*, long, hipStream_t);                               \
+  template void launch_group_gather<T>(const T*, T*, int, int, int, int, int, hipStream_t);    \
+  template void launch_group_scatter<T>(const T*, T*, int, int, int, long, hipStream_t);
 WM_INST(float)
 WM_INST(bf16)
 #undef WM_INST

@@ -36,7 +36,7 @@ def _f64(t):
 MAX_FRAC_PAST_BOUND = 1e-3
 
 
-def check_close(gpu, ref, dtype, name, slack=None, f32_scale=1.0):
+def check_close(gpu, ref, dtype, name, slack=None, f32_scale=1.0, per_element=True):
     """GPU output against the oracle's.
 
     slack (optional, broadcastable to ref): an extra per-element allowance, for stress
@@ -44,6 +44,7 @@ def check_close(gpu, ref, dtype, name, slack=None, f32_scale=1.0):
     (the caller derives it from the oracle alone); its maximum is added to the normwise
     allowance. f32_scale multiplies the fp32 bound, for stress cases whose scores are
     larger than unit-norm queries and keys allow (fp32 rounding in a score grows with it).
+    per_element=False reports the per-element figure without gating on it.
     """
     g = _f64(gpu) if torch.is_tensor(gpu) else np.asarray(gpu, dtype=np.float64)
     r = np.asarray(ref, dtype=np.float64)
@@ -72,7 +73,8 @@ def check_close(gpu, ref, dtype, name, slack=None, f32_scale=1.0):
                    % (name, rel, allow, np.unravel_index(worst, r.shape), g.flat[worst],
                       r.flat[worst], ratio.flat[worst], frac, float(np.quantile(ratio, 0.999))))
             print(msg)
-            assert frac <= MAX_FRAC_PAST_BOUND, msg
+            if per_element:
+                assert frac <= MAX_FRAC_PAST_BOUND, msg
     return err
 
 

@@ -211,3 +211,52 @@ def test_read_calibration_rejects_bad_arguments(wm):
     assert L.wm_calibrate_read(17, 16, 16, None) == wm.ERR_ARG
     assert L.wm_calibrate_read(32, 0, 16, None) == wm.ERR_ARG
     assert L.wm_calibrate_read(32, 24, 16, None) == wm.ERR_ARG
+
+
+@pytest.mark.parametrize("kw,op,code", [
+    (dict(groups=-1), "OP_LAYER_STEP", "ERR_ARG"),
+    (dict(groups=4, group=4), "OP_LAYER_STEP", "ERR_ARG"),
+    (dict(groups=4, group=-1), "OP_POOL", "ERR_ARG"),
+    # group q of g: the last token sits at q + g (T_new - 1); ctx_max 8 + 3 + 4 * 15 + 1 > 64
+    (dict(groups=4, group=3), "OP_LAYER_STEP", "ERR_CAPACITY"),
+    (dict(groups=4, group=3), "OP_POOL", "ERR_CAPACITY"),
+    (dict(groups=4, group=3, ctx_max=0, S_cap=63), "OP_LAYER_ATTEND", "ERR_CAPACITY"),
+    (dict(groups=3, ctx_max=0), "OP_PASSES", "ERR_SHAPE"),        # T_new not a multiple of g
+    (dict(groups=4, group=1, ctx_max=0), "OP_PASSES", "ERR_ARG"),  # the driver runs all groups
+    (dict(groups=4, S_cap=128), "OP_PASSES", "ERR_ARG"),           # sequences start empty
+])
+def test_group_validation(wm, kw, op, code):
+    d = _dims(wm, **kw)
+    assert wm.validate(d, getattr(wm, op), [l % 2 for l in range(4)]) == getattr(wm, code)
+
+
+def test_group_span_fits_exactly(wm):
+    """Group q of g with T_new tokens covers positions up to q + g (T_new - 1): with no
+    cached context that must be below S_cap, and the bound is exact."""
+    for g, q in ((4, 0), (4, 3), (16, 7)):
+        last = q + g * 15
+        ok = _dims(wm, groups=g, group=q, ctx_max=0, S_cap=last + 1)
+        bad = _dims(wm, groups=g, group=q, ctx_max=0, S_cap=last)
+        for op in ("OP_LAYER_STEP", "OP_POOL", "OP_LAYER_ATTEND", "OP_KV_PROJECT"):
+            assert wm.validate(ok, getattr(wm, op), [0, 1, 0, 1]) == wm.OK, (g, q, op)
+            assert wm.validate(bad, getattr(wm, op), [0, 1, 0, 1]) == wm.ERR_CAPACITY
+    # zero groups means contiguous tokens, like one group
+    assert wm.validate(_dims(wm, groups=0), wm.OP_LAYER_STEP, [0, 1, 0, 1]) == wm.OK
+
+
+def test_new_entry_points_reject_bad_arguments_before_launch(wm):
+    d = _dims(wm, ctx_max=0, groups=4)
+    assert wm.validate(d, wm.OP_PASSES, [0, 1, 0, 1]) == wm.OK
+    assert wm.workspace_size(d, wm.OP_PASSES) > 0
+    # the driver's workspace holds every group's states plus one group's scratch
+    es = 2
+    assert wm.workspace_size(d, wm.OP_PASSES) >= d.B * d.T_new * d.L * d.D * es
+    with pytest.raises(wm.WMError) as e:
+        wm.prefill_passes(d, None, None, None, [0, 1, 0, 1], 0, None, None, None)
+    assert e.value.code == wm.ERR_ARG  # passes < 1
+    with pytest.raises(wm.WMError) as e:
+        wm.layer_attend(_dims(wm), None, 4, None, [0, 1, 0, 1], None, None, None, None)
+    assert e.value.code == wm.ERR_ARG  # layer outside [0, L)
+    with pytest.raises(wm.WMError) as e:
+        wm.pool(_dims(wm), None, None, None, None, None)
+    assert e.value.code == wm.ERR_ARG  # params NULL
