@@ -197,6 +197,19 @@ int wm_layer_step(const wm_dims *dims, const wm_params *params, const void *H,
                   const int32_t *chan_map, const int32_t *ctx_len, void *Kc, void *Vc,
                   void *O, void *ws, size_t ws_bytes, wm_stream_t stream);
 
+/* wm_channel_attend for callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): no workspace argument. Its only
+ * scratch, the split-S decode partials (T_new <= 4; the full-sequence kernels need none),
+ * lives in a fixed array of 64 MiB of device memory inside the library; each device holds
+ * its own copy until the process ends. The call itself allocates nothing. Calls on one
+ * device share that array, so calls that overlap on one device race; serialise them (one
+ * stream, or events). A call needing more scratch than the array holds (its
+ * wm_workspace_size(dims, WM_OP_CHANNEL_ATTEND)) fails with WM_ERR_WORKSPACE before any
+ * launch. Arguments, results and errors otherwise as wm_channel_attend. */
+int wm_channel_attend_static(const wm_dims *dims, const wm_params *params, const void *Q,
+                             const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
+                             const void *Vc, void *O, wm_stream_t stream);
+
 /* Document mask (Section 4.1: sequences packed from several documents, attention
  * confined to each document). Same as wm_channel_attend / wm_layer_step, plus
  *   doc_start device int32 [B][T_new], 4-byte aligned, not NULL: the position of

@@ -77,6 +77,7 @@ def lib() -> ctypes.CDLL:
         "wm_layer_step_profiled": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp,
                                    _vp],
         "wm_pool": [D, P, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_channel_attend_static": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp],
         "wm_layer_attend": [D, P, ctypes.c_int32, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_prefill_passes": [D, P, _vp, _vp, _i32p, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp,
                               _sz, _vp],
@@ -262,6 +263,14 @@ def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws=None, str
         _check(lib().wm_layer_step_doc(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H),
                                        _map(chan_map), _ptr(ctx_len), _ptr(doc_start), _ptr(Kc),
                                        _ptr(Vc), _ptr(O), wp, wn, _stream(stream)))
+
+
+def channel_attend_static(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, stream=None):
+    """wm_channel_attend without a workspace: the decode partials live in the library's
+    fixed scratch array (calls on one device must not overlap)."""
+    _check(lib().wm_channel_attend_static(ctypes.byref(dims), _pref(params), _ptr(Q),
+                                          _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
+                                          _ptr(O), _stream(stream)))
 
 
 def pool(dims: Dims, params, H, ctx_len, Kc, Vc, ws=None, stream=None):

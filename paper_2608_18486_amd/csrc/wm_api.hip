@@ -10,11 +10,19 @@
 #include <cstdio>
 #include <climits>
 #include <cstring>
+#include <mutex>
 
 #include "whitematter.h"
 #include "wm_internal.hpp"
 
 using wm::bf16;
+
+// Scratch of wm_channel_attend_static, for callers that cannot allocate: the decode
+// kernels' split partials live in this array instead of a caller workspace. Every device
+// the library runs on holds its own copy until the process ends; calls that overlap on
+// one device share it and race.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -473,6 +481,29 @@ int check_params(const wm_params* P, std::initializer_list<int> which) {
 
 enum { P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN, P_KD, P_VD, P_GIN, P_WQ, P_GQN };
 
+// The array's device address, looked up once per device with that device current (in host
+// code the array's name is only a stand-in, never a device address).
+constexpr int kMaxDevices = 64;
+struct ScratchAddr {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t rc = hipSuccess;
+};
+ScratchAddr g_scratch_addr[kMaxDevices];
+
+int static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(WM_ERR_LAUNCH, "no current HIP device below %d", kMaxDevices);
+  ScratchAddr& a = g_scratch_addr[dev];
+  std::call_once(a.once, [&] { a.rc = hipGetSymbolAddress(&a.ptr, HIP_SYMBOL(scratch)); });
+  if (a.rc != hipSuccess || !a.ptr)
+    return fail(WM_ERR_LAUNCH, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev,
+                hipGetErrorString(a.rc));
+  *out = a.ptr;
+  return WM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -633,6 +664,21 @@ int wm_channel_attend(const wm_dims* dims, const wm_params* params, const void* 
                       const void* Vc, void* O, void* ws, size_t ws_bytes, wm_stream_t stream) {
   return channel_attend_impl(dims, params, Q, chan_map, ctx_len, nullptr, Kc, Vc, O, ws,
                              ws_bytes, stream);
+}
+
+int wm_channel_attend_static(const wm_dims* dims, const wm_params* params, const void* Q,
+                             const int32_t* chan_map, const int32_t* ctx_len, const void* Kc,
+                             const void* Vc, void* O, wm_stream_t stream) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_CHANNEL_ATTEND, chan_map));
+  const size_t need = layout(*dims, WM_OP_CHANNEL_ATTEND).total;
+  if (need > kStaticScratchBytes)
+    return fail(WM_ERR_WORKSPACE, "the call needs %zu bytes of scratch, more than the %zu the "
+                "library holds for wm_channel_attend_static", need, kStaticScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) WM_TRY(static_scratch(&ws));
+  return channel_attend_impl(dims, params, Q, chan_map, ctx_len, nullptr, Kc, Vc, O, ws, need,
+                             stream);
 }
 
 int wm_channel_attend_doc(const wm_dims* dims, const wm_params* params, const void* Q,
