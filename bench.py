@@ -435,6 +435,51 @@ def decode_step(wm, torch, np, synth, hip, dev, stream, log, steps=10):
     return out
 
 
+def passes_bench(wm, torch, np, synth, hip, dev, stream, log):
+    """The fixed-point passes of Section 3.3 at the paper's model shape (B16 T2048 L16 k8
+    D512, 6 query / 3 KV heads of 96, p = 2, bf16) with the stand-in decoder block:
+    cyclic Gauss-Seidel with the paper's g = 8 groups and with g = 16, Jacobi (g = 1), 3
+    passes each, and one pass of g = T (exact left-to-right evaluation), event-timed."""
+    w0 = synth.WORKLOADS["paper_T2048_L16_k8"]
+    w = synth.Workload("paper_passes", w0.B, w0.T_new, w0.L, w0.k, w0.D, w0.Hq, w0.Hkv, w0.d, 0,
+                       w0.dtype, list(w0.chan_map), w0.p, w0.seed)
+    P = wm.ParamSet({k: v.to(dev) for k, v in
+                     synth.make_params(w, np.asarray(wm.init_bias(w.L, w.k)) + 0.2).items()})
+    X = synth.make_embeddings(w).to(dev)
+    W_o = synth.make_out_proj(w).to(dev)
+    Kc = torch.zeros((w.k, w.B, w.Hkv, w.T_new, w.d), dtype=w.torch_dtype, device=dev)
+    Vc = torch.zeros_like(Kc)
+    H = torch.empty((w.B, w.T_new, w.L, w.D), dtype=w.torch_dtype, device=dev)
+    top = torch.empty((w.B, w.T_new, w.D), dtype=w.torch_dtype, device=dev)
+    out = {"workload": "fixed-point passes, the paper's model shape: B16 T2048 L16 k8 D512 "
+                       "6q/3kv x96, p2, bf16, map l->l%8, stand-in block h + W_o o"}
+    for g, passes, reps in ((8, 3, 5), (16, 3, 5), (1, 3, 5), (w.T_new, 1, 1)):
+        dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p,
+                            S_cap=w.T_new, ctx_max=0, dtype=wm.BF16, groups=g)
+        ws = wm.workspace(dims, wm.OP_PASSES, dev)
+        run = lambda: wm.prefill_passes(dims, P, W_o, X, w.chan_map, passes, Kc, Vc, H, top,  # noqa: E731
+                                        ws=ws, stream=stream)
+        run()
+        torch.cuda.synchronize()
+        ev = [hip.create() for _ in range(reps + 1)]
+        hip.record(ev[0], stream.cuda_stream)
+        for r in range(reps):
+            run()
+            hip.record(ev[r + 1], stream.cuda_stream)
+        torch.cuda.synchronize()
+        ms = float(np.median([hip.elapsed_ms(ev[r], ev[r + 1]) for r in range(reps)]))
+        for e in ev:
+            hip.destroy(e)
+        key = "g%d" % g if g < w.T_new else "g_T"
+        out[key] = {"passes": passes, "ms": round(ms, 3), "ms_per_pass": round(ms / passes, 3),
+                    "tokens_per_s": round(w.B * w.T_new / (ms * 1e-3), 1),
+                    "s_per_sequence": round(ms * 1e-3 / w.B, 6)}
+        log("bench: passes g=%d x %d: %.3f ms (%.3f ms per pass, %.0f tokens/s)"
+            % (g, passes, ms, ms / passes, w.B * w.T_new / (ms * 1e-3)))
+        del ws
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -444,6 +489,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the 32768-context decode step timed after the main workload")
+    ap.add_argument("--no-passes", action="store_true",
+                    help="skip the fixed-point pass driver timed at the paper's model shape")
     ap.add_argument("--blas-reference", action="store_true",
                     help="also time torch.bmm (the vendor GEMM library) on the plain GEMMs of the "
                          "K/V and query projections of this workload, for comparison (stderr)")
@@ -609,6 +656,9 @@ def main():
         del Kc, Vc, O, ws, H
         torch.cuda.empty_cache()
         line["decode_c5"] = decode_step(wm, torch, np, synth, hip, dev, stream, log)
+    if not args.no_passes:
+        torch.cuda.empty_cache()
+        line["prefill_passes"] = passes_bench(wm, torch, np, synth, hip, dev, stream, log)
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline ...")
         line["cpu_baseline"] = cpu_baseline(w, P_cpu, H_cpu, (Kc, Vc) if w.ctx else None, docs_np)
