@@ -43,17 +43,18 @@ template <typename T, int BK_, int WGO_, int WGN_, int WO_, int WN_> struct Proj
   static constexpr int BK = BK_, WGO = WGO_, WGN = WGN_, WO = WO_, WN = WN_;
   static constexpr int NT = 64 * WGO * WGN;                 // threads
   static constexpr int OT = 32 * WO * WGO, NTOK = 32 * WN * WGN;
-  // bf16 with BK = 32: 64-B LDS rows whose four 16-B chunks are XOR-swizzled
-  // (chunk c of row r at c ^ ((r / 2) % 4)), so the 8 lanes of a 128-B LDS cycle
-  // hit distinct banks both when a wave stages two rows of 4 chunks and when it
-  // reads one chunk of 8 consecutive rows. Otherwise rows are padded.
+  // bf16 with BK = 32: 64-B LDS rows whose four 16-B chunks are XOR-swizzled (chunk c of
+  // row r at c ^ swz(r)), so that a fragment read -- 16 lanes reading one chunk of 16
+  // consecutive rows, served 256 B per LDS cycle -- hits 16 distinct 16-B bank groups;
+  // the same holds 8 rows at a time at 128 B per cycle. Otherwise rows are padded.
   static constexpr bool SWZ = sizeof(T) == 2 && BK == 32;
   static constexpr int PAD = SWZ ? 0 : sizeof(T) == 2 ? 8 : 4;  // keeps 16-B row alignment
   static constexpr int LDA = BK + PAD;                       // LDS row stride (elements)
   static constexpr int CPR = BK / 8;                         // fragments per tile row
+  __device__ static int swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
   // element offset of 8-element chunk ch of tile row row
   __device__ static int chunk_at(int row, int ch) {
-    return row * LDA + 8 * (SWZ ? ch ^ ((row >> 1) & 3) : ch);
+    return row * LDA + 8 * (SWZ ? ch ^ swz(row) : ch);
   }
   static constexpr int FW = (OT * CPR + NT - 1) / NT;        // W fragments per thread
   static constexpr int FX = (NTOK * CPR + NT - 1) / NT;      // X fragments per thread
@@ -255,7 +256,7 @@ __global__ __launch_bounds__(C::NT) void proj_gemm_dma_kernel(int M, int Nout, i
 #pragma unroll
   for (int i = 0; i < D::NI; ++i) {
     const int blk = w * D::NI + i, row = 16 * blk + lane / 4;
-    const int c = (lane & 3) ^ ((row >> 1) & 3);
+    const int c = (lane & 3) ^ C::swz(row);
     bool ok;
     uint32_t off;
     if (row < C::OT) {

@@ -153,17 +153,20 @@ template <typename T> struct PlainRows {
 // Router operand: token n's row is the stack of the selected layers' raw states,
 // column k = m * D + e reading H[n][sel[m]][e] (the 1/RMS is applied to the
 // accumulators, the gain is folded into the weights).
+// The stacked layers are affine in m: sel[m] = s0 + p m (every p-th layer counting down
+// from L-1, in ascending order), so a slice's offset needs no table read; with p = 1 the
+// stack is the whole row.
 template <typename T> struct StackedRows {
   const T* H;
-  LayerTable sel;
-  int L, D, M;
+  int s0, p, L, D, M;
   __device__ RowsView view(int) const {
     return {make_view(H, (uint32_t)((long)M * L * D * sizeof(T))),
             (uint32_t)((long)L * D * sizeof(T))};
   }
   __device__ uint32_t slice(int k0) const {
+    if (p == 1) return (uint32_t)(s0 * D + k0) * (uint32_t)sizeof(T);
     const int m = k0 / D, e = k0 - m * D;
-    return (uint32_t)(sel.v[m] * D + e) * (uint32_t)sizeof(T);
+    return (uint32_t)((s0 + p * m) * D + e) * (uint32_t)sizeof(T);
   }
 };
 
@@ -636,6 +639,9 @@ size_t router_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.L * sh.Lp * s
 // Layers per K split: enough blocks to cover the chip (one per CU), splitting K at layer
 // boundaries when the token and channel tiles alone give fewer. (Aiming at two blocks per
 // CU measured 6-21% slower: the extra partial sums cost more than the occupancy gains.)
+#ifndef WM_ROUTER_MIN_BLOCKS
+#define WM_ROUTER_MIN_BLOCKS 256
+#endif
 static int router_layers_per_split(const Shape& sh) {
   using CF = RouterShape<bf16, false>::C;
   using CD = RouterShape<bf16, true>::C;
@@ -643,7 +649,7 @@ static int router_layers_per_split(const Shape& sh) {
   const int tok = few ? CD::NTOK : CF::NTOK, och = few ? CD::OT : CF::OT;
   const long blocks = (long)((sh.N() + tok - 1) / tok) * ((2 * sh.k * sh.L + och - 1) / och);
   int s = 1;
-  while (s < sh.Lp && blocks * s < 256) s *= 2;
+  while (s < sh.Lp && blocks * s < WM_ROUTER_MIN_BLOCKS) s *= 2;
   return (sh.Lp + s - 1) / s;
 }
 
@@ -665,7 +671,7 @@ static void router_gemm(const Shape& sh, const LayerTable& sel, const T* H, cons
   const int M = sh.N(), kL = sh.k * sh.L, Nout = 2 * kL, K = sh.Lp * sh.D;
   const int seg = sh.D / C::BK, splits = router_splits(sh);
   const int per = router_layers_per_split(sh);
-  StackedRows<T> x{H, sel, sh.L, sh.D, M};
+  StackedRows<T> x{H, sel.v[0], sh.p, sh.L, sh.D, M};
   PlainRows<T> w{wf, 0, K, Nout};
   RouterEpi<T> e{splits > 1 ? part : logits, b_alpha, rinv, sel, M, Nout, kL, sh.L, sh.Lp, per,
                  splits};
