@@ -363,3 +363,18 @@ def block_residual(dims: Dims, W_o, l: int, h, o) -> np.ndarray:
     lib().wmo_block_residual(ctypes.byref(dims.c()), _ptr(W), ctypes.c_int(l), _ptr(h), _ptr(o),
                              _ptr(out))
     return out
+
+
+def channel_attend_dense(dims: Dims, params, read_w, Q, ctx_len, Kc, Vc, rows=None) -> np.ndarray:
+    """The dense soft read (Section 3.1 Step 3 variant): layer l attends the channels mixed
+    with its weights read_w[l] ([L, k])."""
+    P = _as_params(params)
+    W = _f64(read_w)
+    assert W.shape == (dims.L, dims.k)
+    Q, Kc, Vc = _f64(Q), _f64(Kc), _f64(Vc)
+    ctx = _ctx(dims, ctx_len)
+    O = np.zeros((dims.L, dims.B, dims.T_new, dims.Hq * dims.d))
+    arr, n, p = _ilist(rows)
+    lib().wmo_channel_attend_dense(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(Q),
+                                   _ptr(ctx), _ptr(Kc), _ptr(Vc), p, ctypes.c_int(n), _ptr(O))
+    return O

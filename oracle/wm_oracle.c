@@ -728,3 +728,63 @@ void wmo_autoregressive(const wmo_dims *dm, const wmo_params *P, const double *W
         }
     }
 }
+
+/* ============================ Section 3.1 Step 3: the dense soft read (variant)
+ *
+ * The paper contrasts its fixed one-channel selection with a dense read over all
+ * channels that would permit learned soft assignments (and would stream all k
+ * channels per layer). Read here as: layer l attends a soft mix of the channels,
+ * K^_l[s] = sum_c w[l][c] K~_c[s], V^_l[s] = sum_c w[l][c] V_c[s], and likewise
+ * for the dummy slot, with w[L][k] the layer's assignment weights as given (the
+ * fixed selection is the one-hot row w[l][c] = [c == map[l]]). The attention is
+ * then the standard one over the mixed slots. */
+void wmo_channel_attend_dense(const wmo_dims *dm, const wmo_params *P, const double *w,
+                              const double *Q, const int *ctx_len, const double *Kc,
+                              const double *Vc, const int *rows, int nrows, double *O)
+{
+    int B = dm->B, T = dm->T_new, L = dm->L, k = dm->k, Hq = dm->Hq, Hkv = dm->Hkv, d = dm->d;
+    int grp = Hq / Hkv;
+    int cnt = list_len(rows, nrows, L * B * T);
+#pragma omp parallel for schedule(dynamic)
+    for (int t = 0; t < cnt; ++t) {
+        int r = rows ? rows[t] : t;
+        int l = r / (B * T), b = (r / T) % B, i = r % T;
+        long pos = (long)(ctx_len ? ctx_len[b] : 0) + i;
+        int paper = dm->mask_mode == WMO_MASK_PAPER;
+        long nvis = paper ? pos : pos + 1;
+        double *Km = (double *)malloc(sizeof(double) * (nvis > 0 ? nvis : 1) * d);
+        double *Vm = (double *)malloc(sizeof(double) * (nvis > 0 ? nvis : 1) * d);
+        double *kd = (double *)malloc(sizeof(double) * d);
+        double *vd = (double *)malloc(sizeof(double) * d);
+        for (int hh = 0; hh < Hq; ++hh) {
+            int kvh = hh / grp;
+            for (long s = 0; s < nvis; ++s)
+                for (int e = 0; e < d; ++e) {
+                    double a = 0.0, v = 0.0;
+                    for (int c = 0; c < k; ++c) {
+                        size_t off = ((((size_t)c * B + b) * Hkv + kvh) * dm->S_cap + s) * d + e;
+                        a += w[(size_t)l * k + c] * Kc[off];
+                        v += w[(size_t)l * k + c] * Vc[off];
+                    }
+                    Km[s * d + e] = a;
+                    Vm[s * d + e] = v;
+                }
+            for (int e = 0; e < d; ++e) {
+                double a = 0.0, v = 0.0;
+                for (int c = 0; c < k; ++c) {
+                    a += w[(size_t)l * k + c] * P->Kd[((size_t)c * Hkv + kvh) * d + e];
+                    v += w[(size_t)l * k + c] * P->Vd[((size_t)c * Hkv + kvh) * d + e];
+                }
+                kd[e] = a;
+                vd[e] = v;
+            }
+            const double *q = Q + ((((size_t)l * B + b) * Hq + hh) * T + i) * d;
+            wmo_attend_row(d, q, Km, d, Vm, d, nvis, paper ? kd : NULL, paper ? vd : NULL,
+                           O + (((size_t)l * B + b) * T + i) * Hq * d + (size_t)hh * d);
+        }
+        free(vd);
+        free(kd);
+        free(Vm);
+        free(Km);
+    }
+}

@@ -595,3 +595,76 @@ def test_nofeedback_equals_router_with_masked_parameters(oracle_lib, p):
     a0, m0 = o.router_mix(_dims(o, w), Pm, H.double())
     np.testing.assert_array_equal(a, a0)
     np.testing.assert_array_equal(m, m0)
+
+
+# ------------------------------------------------ dense soft read (Section 3.1 Step 3)
+
+def _dense_case(o, mask_mode=0, ctx=30):
+    w = _small(B=2, T_new=12, L=5, k=3, Hq=4, Hkv=2, ctx=ctx + 12)
+    w = synth.Workload(w.name, w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, w.ctx, "f32",
+                       [2, 0, 2, 1, 0], w.p, w.seed)
+    P = synth.make_params(w, o.init_bias(w.L, w.k))
+    Q = synth.make_queries(w)
+    Kc, Vc = synth.make_cache_cpu(w)
+    ctx_len = np.array([ctx, ctx // 3], dtype=np.int32)
+    return w, P, Q, Kc.double().numpy(), Vc.double().numpy(), ctx_len, _dims(o, w,
+                                                                             mask_mode=mask_mode)
+
+
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_dense_read_with_one_hot_weights_is_the_fixed_selection(oracle_lib, mask_mode):
+    o = oracle_lib
+    w, P, Q, Kc, Vc, ctx, dm = _dense_case(o, mask_mode)
+    onehot = np.zeros((w.L, w.k))
+    onehot[np.arange(w.L), w.chan_map] = 1.0
+    Od = o.channel_attend_dense(dm, P, onehot, Q, ctx, Kc, Vc)
+    Os = o.channel_attend(dm, P, Q, w.chan_map, ctx, Kc, Vc)
+    assert np.array_equal(Od, Os)
+
+
+def test_dense_read_matches_sdpa_over_mixed_channels(oracle_lib):
+    """Soft weights: the mixed keys and values formed with einsum, the dummy slot mixed the
+    same way, then torch's scaled_dot_product_attention (float64)."""
+    o = oracle_lib
+    w, P, Q, Kc, Vc, ctx, dm = _dense_case(o)
+    rng = np.random.default_rng(21)
+    sw = rng.normal(size=(w.L, w.k))
+    sw = np.exp(sw) / np.exp(sw).sum(axis=1, keepdims=True)
+    Od = o.channel_attend_dense(dm, P, sw, Q, ctx, Kc, Vc)
+    Qn = Q.double().numpy()
+    Kd, Vd = P["Kd"].double().numpy(), P["Vd"].double().numpy()
+    grp = w.Hq // w.Hkv
+    for l in range(w.L):
+        Km = np.einsum("c,cbhsd->bhsd", sw[l], Kc)
+        Vm = np.einsum("c,cbhsd->bhsd", sw[l], Vc)
+        kd, vd = np.einsum("c,chd->hd", sw[l], Kd), np.einsum("c,chd->hd", sw[l], Vd)
+        for b in range(w.B):
+            for i in range(w.T_new):
+                pos = int(ctx[b]) + i
+                for h in range(w.Hq):
+                    kv = h // grp
+                    K = np.vstack([kd[kv], Km[b, kv, :pos]])
+                    V = np.vstack([vd[kv], Vm[b, kv, :pos]])
+                    ref = F.scaled_dot_product_attention(_t(Qn[l, b, h, i])[None, None],
+                                                         _t(K)[None], _t(V)[None])[0, 0]
+                    np.testing.assert_allclose(Od[l, b, i, h * w.d:(h + 1) * w.d], ref.numpy(),
+                                               rtol=1e-11, atol=1e-12)
+
+
+def test_dense_read_splitting_a_weight_over_equal_channels(oracle_lib):
+    """Two channels holding the same cache and dummy: weights 0.3 / 0.7 on them read the
+    same as 1.0 on one."""
+    o = oracle_lib
+    w, P, Q, Kc, Vc, ctx, dm = _dense_case(o)
+    Kc[1], Vc[1] = Kc[0], Vc[0]
+    P = dict(P)
+    P["Kd"] = P["Kd"].clone()
+    P["Vd"] = P["Vd"].clone()
+    P["Kd"][1], P["Vd"][1] = P["Kd"][0], P["Vd"][0]
+    split = np.zeros((w.L, w.k))
+    split[:, 0], split[:, 1] = 0.3, 0.7
+    one = np.zeros((w.L, w.k))
+    one[:, 0] = 1.0
+    np.testing.assert_allclose(o.channel_attend_dense(dm, P, split, Q, ctx, Kc, Vc),
+                               o.channel_attend_dense(dm, P, one, Q, ctx, Kc, Vc),
+                               rtol=1e-12, atol=1e-12)
