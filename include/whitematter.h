@@ -85,7 +85,8 @@ enum wm_op {
   WM_OP_LAYER_STEP = 4,
   WM_OP_POOL = 5,          /* wm_pool */
   WM_OP_LAYER_ATTEND = 6,  /* wm_layer_attend */
-  WM_OP_PASSES = 7         /* wm_prefill_passes */
+  WM_OP_PASSES = 7,        /* wm_prefill_passes */
+  WM_OP_DENSE_ATTEND = 8   /* wm_channel_attend_dense */
 };
 
 /* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
@@ -196,6 +197,22 @@ int wm_channel_attend(const wm_dims *dims, const wm_params *params, const void *
 int wm_layer_step(const wm_dims *dims, const wm_params *params, const void *H,
                   const int32_t *chan_map, const int32_t *ctx_len, void *Kc, void *Vc,
                   void *O, void *ws, size_t ws_bytes, wm_stream_t stream);
+
+/* The dense soft read of Section 3.1 Step 3, the variant the paper contrasts with its
+ * fixed selection: every consumer reads all k channels, mixed with its own weights,
+ * K^_l[s] = sum_c read_w[l][c] K~_c[s] and V^_l[s] = sum_c read_w[l][c] V_c[s] (the dummy
+ * slot likewise), then attends them as wm_channel_attend does. The fixed selection is
+ * the one-hot row read_w[l][c] = (c == chan_map[l]).
+ *   read_w  device float [L][k], 16-byte aligned: the weights as given (apply a softmax
+ *           beforehand for a soft assignment)
+ *   other arguments as wm_channel_attend (no chan_map)
+ * The mixed channels go to the workspace first (2 L B Hkv S_cap d elements in dtype, the
+ * mix summed in fp32 and rounded to dtype): each consumer streams the k channels' slots it
+ * may see, k times the bytes of the fixed selection, which is the cost the paper names. */
+int wm_channel_attend_dense(const wm_dims *dims, const wm_params *params, const float *read_w,
+                            const void *Q, const int32_t *ctx_len, const void *Kc,
+                            const void *Vc, void *O, void *ws, size_t ws_bytes,
+                            wm_stream_t stream);
 
 /* wm_channel_attend for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument. Its only

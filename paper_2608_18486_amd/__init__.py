@@ -24,7 +24,7 @@ MIX_LINEAR, MIX_SOFTMAX = 0, 1
 MASK_PAPER, MASK_INCLUSIVE = 0, 1
 ROUTER_DYNAMIC, ROUTER_STATIC, ROUTER_NOFEEDBACK = 0, 1, 2
 (OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP, OP_POOL,
- OP_LAYER_ATTEND, OP_PASSES) = range(8)
+ OP_LAYER_ATTEND, OP_PASSES, OP_DENSE_ATTEND) = range(9)
 
 PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
                "Kd", "Vd", "g_in", "Wq", "g_qnorm")
@@ -78,6 +78,7 @@ def lib() -> ctypes.CDLL:
                                    _vp],
         "wm_pool": [D, P, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_channel_attend_static": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp],
+        "wm_channel_attend_dense": [D, P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_layer_attend": [D, P, ctypes.c_int32, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_prefill_passes": [D, P, _vp, _vp, _i32p, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp,
                               _sz, _vp],
@@ -263,6 +264,16 @@ def layer_step(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, ws=None, str
         _check(lib().wm_layer_step_doc(ctypes.byref(dims), ctypes.byref(P.c), _ptr(H),
                                        _map(chan_map), _ptr(ctx_len), _ptr(doc_start), _ptr(Kc),
                                        _ptr(Vc), _ptr(O), wp, wn, _stream(stream)))
+
+
+def channel_attend_dense(dims: Dims, params, read_w, Q, ctx_len, Kc, Vc, O, ws=None,
+                         stream=None):
+    """The dense soft read: consumer l attends all channels mixed with read_w[l] (device
+    float32 [L, k])."""
+    ws, wp, wn = _ws(dims, OP_DENSE_ATTEND, ws, getattr(Q, "device", None))
+    _check(lib().wm_channel_attend_dense(ctypes.byref(dims), _pref(params), _ptr(read_w),
+                                         _ptr(Q), _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O),
+                                         wp, wn, _stream(stream)))
 
 
 def channel_attend_static(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, stream=None):

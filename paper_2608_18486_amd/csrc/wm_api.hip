@@ -42,7 +42,7 @@ bool decode_path(const wm_dims& d) { return d.T_new <= 4; }
 
 struct Layout {
   size_t rinv = 0, alpha = 0, mixed = 0, rinv_mid = 0, tab = 0, q = 0, part = 0, wkv = 0, wq = 0,
-         wa = 0, rpart = 0, hg = 0, topg = 0, ol = 0, total = 0;
+         wa = 0, rpart = 0, hg = 0, topg = 0, ol = 0, kl = 0, vl = 0, kdl = 0, vdl = 0, total = 0;
 };
 
 int group_stride(const wm_dims& d) { return d.groups > 1 ? d.groups : 1; }
@@ -95,6 +95,12 @@ wm::Shape one_layer(wm::Shape sh) {
   return sh;
 }
 
+// The dense soft read attends L mixed channels, one per consumer layer.
+wm::Shape dense_shape(wm::Shape sh) {
+  sh.k = sh.L;
+  return sh;
+}
+
 // Workspace regions for an op (offsets in bytes, each 256-byte aligned).
 Layout layout(const wm_dims& dd, int op) {
   Layout Ly;
@@ -129,6 +135,14 @@ Layout layout(const wm_dims& dd, int op) {
   if (layer) Ly.q = take(N * d.Hq * d.d * es);
   if ((op == WM_OP_CHANNEL_ATTEND || all) && decode_path(d))
     Ly.part = take(wm::decode_partials_bytes(make_shape(d)));
+  if (op == WM_OP_DENSE_ATTEND) {
+    const size_t cache = (size_t)d.L * d.B * d.Hkv * d.S_cap * d.d * es;
+    Ly.kl = take(cache);
+    Ly.vl = take(cache);
+    Ly.kdl = take((size_t)d.L * d.Hkv * d.d * es);
+    Ly.vdl = take((size_t)d.L * d.Hkv * d.d * es);
+    if (decode_path(d)) Ly.part = take(wm::decode_partials_bytes(dense_shape(make_shape(d))));
+  }
   if (layer && decode_path(d)) Ly.part = take(wm::decode_partials_bytes(one_layer(make_shape(d))));
   if (op == WM_OP_KV_PROJECT || all || pool) Ly.wkv = take(wm::kv_fold_elems(make_shape(d)) * es);
   if (op == WM_OP_Q_PROJECT || all || layer) Ly.wq = take(wm::q_fold_elems(make_shape(d)) * es);
@@ -142,13 +156,14 @@ Layout layout(const wm_dims& dd, int op) {
 
 bool uses_cache(int op) {
   return op == WM_OP_KV_PROJECT || op == WM_OP_CHANNEL_ATTEND || op == WM_OP_LAYER_STEP ||
-         op == WM_OP_POOL || op == WM_OP_LAYER_ATTEND || op == WM_OP_PASSES;
+         op == WM_OP_POOL || op == WM_OP_LAYER_ATTEND || op == WM_OP_PASSES ||
+         op == WM_OP_DENSE_ATTEND;
 }
 
 int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (!dp) return fail(WM_ERR_ARG, "dims is NULL");
   const wm_dims& d = *dp;
-  if (op < WM_OP_ROUTER_MIX || op > WM_OP_PASSES) return fail(WM_ERR_ARG, "unknown op %d", op);
+  if (op < WM_OP_ROUTER_MIX || op > WM_OP_DENSE_ATTEND) return fail(WM_ERR_ARG, "unknown op %d", op);
   if (d.dtype != WM_F32 && d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "unknown dtype %d", d.dtype);
   if (d.mix_mode != WM_MIX_LINEAR && d.mix_mode != WM_MIX_SOFTMAX)
     return fail(WM_ERR_DTYPE, "unknown mix_mode %d", d.mix_mode);
@@ -192,6 +207,8 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if ((N + 127) / 128 > 65535) return fail(WM_ERR_SHAPE, "B * T_new exceeds the grid limit");
   if ((long long)d.Hq * d.B * d.L > 65535 || (long long)d.Hkv * d.B * d.k > 65535)
     return fail(WM_ERR_SHAPE, "heads x sequences x layers exceeds the grid limit");
+  if (op == WM_OP_DENSE_ATTEND && (long long)d.L * d.B * d.Hkv > 65535)
+    return fail(WM_ERR_SHAPE, "layers x sequences x KV heads exceeds the grid limit");
   {
     // tiles are read through 32-bit buffer views: every operand view must span < 2 GiB
     const double es = (double)elem_size(d), lim = 2147483647.0;
@@ -463,6 +480,35 @@ void run_passes(const wm_dims& d, const wm_params& P, const T* W_o, const T* X,
   }
   wm::launch_group_scatter<T>(Hg, H, d.B, d.T_new, g, (long)L * D, s);
   if (h_top) wm::launch_group_scatter<T>(topg, h_top, d.B, d.T_new, g, D, s);
+}
+
+// The dense soft read: every consumer's mix of the k channels into the workspace, then the
+// attention of L consumers over L mixed channels (consumer l reads its own).
+template <typename T>
+void run_attend_dense(const wm_dims& d, const wm_params& P, const float* read_w, const T* Q,
+                      const int32_t* ctx_len, const T* Kc, const T* Vc, T* O, void* ws,
+                      hipStream_t s) {
+  const Layout Ly = layout(d, WM_OP_DENSE_ATTEND);
+  const wm::Shape sh = make_shape(d);
+  T* Kl = (T*)at(ws, Ly.kl);
+  T* Vl = (T*)at(ws, Ly.vl);
+  T* Kdl = (T*)at(ws, Ly.kdl);
+  T* Vdl = (T*)at(ws, Ly.vdl);
+  wm::launch_soft_read<T>(sh, read_w, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len, Kl, Vl,
+                          Kdl, Vdl, s);
+  const wm::Shape shd = dense_shape(sh);
+  wm::LayerTable ident{};
+  for (int l = 0; l < d.L; ++l) ident.v[l] = l;
+  if (decode_path(d)) {
+    wm::ChannelGroups cg{};
+    int32_t map[wm::kMaxLayers];
+    for (int l = 0; l < d.L; ++l) map[l] = l;
+    wm_channel_groups(d.L, d.L, map, cg.offsets, cg.members);
+    wm::launch_attend_decode<T>(shd, ident, cg, Q, Kl, Vl, Kdl, Vdl, ctx_len, nullptr,
+                                (float*)at(ws, Ly.part), O, s);
+  } else {
+    wm::launch_attend_prefill<T>(shd, ident, Q, Kl, Vl, Kdl, Vdl, ctx_len, nullptr, O, s);
+  }
 }
 
 int check_params(const wm_params* P, std::initializer_list<int> which) {
@@ -748,6 +794,32 @@ int wm_layer_step_profiled(const wm_dims* dims, const wm_params* params, const v
   if ((uintptr_t)doc_start % 4 != 0) return fail(WM_ERR_ARG, "doc_start is not 4-byte aligned");
   return layer_step_impl(dims, params, H, chan_map, ctx_len, doc_start, Kc, Vc, O, ws, ws_bytes,
                          stream, events);
+}
+
+int wm_channel_attend_dense(const wm_dims* dims, const wm_params* params, const float* read_w,
+                            const void* Q, const int32_t* ctx_len, const void* Kc,
+                            const void* Vc, void* O, void* ws, size_t ws_bytes,
+                            wm_stream_t stream) {
+  WM_TRY(validate_dims(dims, WM_OP_DENSE_ATTEND, nullptr));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_KD, P_VD}));
+  else if (!params) return fail(WM_ERR_ARG, "params is NULL");
+  WM_TRY(need_ptr(read_w, "read_w"));
+  WM_TRY(need_ptr(Q, "Q"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(need_ptr(O, "O"));
+  WM_TRY(check_ws(d, WM_OP_DENSE_ATTEND, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  if (d.dtype == WM_BF16)
+    run_attend_dense<bf16>(d, *params, read_w, (const bf16*)Q, ctx_len, (const bf16*)Kc,
+                           (const bf16*)Vc, (bf16*)O, ws, s);
+  else
+    run_attend_dense<float>(d, *params, read_w, (const float*)Q, ctx_len, (const float*)Kc,
+                            (const float*)Vc, (float*)O, ws, s);
+  return launched();
 }
 
 int wm_pool(const wm_dims* dims, const wm_params* params, const void* H, const int32_t* ctx_len,

@@ -1338,13 +1338,90 @@ void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const Cha
     decode_dispatch<T, 32>(a, G, grid, s);
 }
 
+// ------------------------------------------------------------ dense soft read
+// Layer l's soft mix of the k channels (the dense read of Section 3.1 Step 3):
+// Kl[l][b][h][s] = sum_c w[l][c] Kc[c][b][h][s], the same for V, over the slots the
+// call's rows may see (below min(S_cap, ctx + span)), and the dummy slots
+// Kdl[l][h] = sum_c w[l][c] Kd[c][h] (blockIdx.y = L B Hkv for those). Sums in fp32,
+// one 8-element chunk per thread.
+template <typename T>
+__global__ __launch_bounds__(256) void soft_read_kernel(const T* __restrict__ Kc,
+                                                        const T* __restrict__ Vc,
+                                                        const T* __restrict__ Kd,
+                                                        const T* __restrict__ Vd,
+                                                        const float* __restrict__ w, int B,
+                                                        int Hkv, int S_cap, int k, int d,
+                                                        const int32_t* ctx_len, int ctx_hi,
+                                                        long span, T* Kl, T* Vl, T* Kdl,
+                                                        T* Vdl) {
+  const int c8 = d / 8;
+  const int y = blockIdx.y;  // (l, b, h) slice, or the dummies of layer l
+  const long x = (long)blockIdx.x * 256 + threadIdx.x;
+  const int L = gridDim.y / (B * Hkv + 1);  // the grid's rows: L B Hkv slices, L dummy rows
+  if (y < L * B * Hkv) {
+    const int h = y % Hkv, b = (y / Hkv) % B, l = y / (Hkv * B);
+    const long lim = min((long)S_cap, (long)ctx_at(ctx_len, b, ctx_hi) + span);
+    if (x >= lim * c8) return;
+    const long s = x / c8, e = (x % c8) * 8;
+    float ka[8] = {0, 0, 0, 0, 0, 0, 0, 0}, va[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int c = 0; c < k; ++c) {
+      const float wc = w[(long)l * k + c];
+      const long off = (((long)c * B + b) * Hkv + h) * S_cap * d + s * d + e;
+      float kv[8], vv[8];
+      load8(Kc + off, kv);
+      load8(Vc + off, vv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        ka[i] += wc * kv[i];
+        va[i] += wc * vv[i];
+      }
+    }
+    const long o = (((long)l * B + b) * Hkv + h) * S_cap * d + s * d + e;
+    store8(Kl + o, ka);
+    store8(Vl + o, va);
+  } else {
+    const int l = y - L * B * Hkv;
+    if (x >= (long)Hkv * c8) return;
+    const long h = x / c8, e = (x % c8) * 8;
+    float ka[8] = {0, 0, 0, 0, 0, 0, 0, 0}, va[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int c = 0; c < k; ++c) {
+      const float wc = w[(long)l * k + c];
+      float kv[8], vv[8];
+      load8(Kd + ((long)c * Hkv + h) * d + e, kv);
+      load8(Vd + ((long)c * Hkv + h) * d + e, vv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        ka[i] += wc * kv[i];
+        va[i] += wc * vv[i];
+      }
+    }
+    store8(Kdl + ((long)l * Hkv + h) * d + e, ka);
+    store8(Vdl + ((long)l * Hkv + h) * d + e, va);
+  }
+}
+
+template <typename T>
+void launch_soft_read(const Shape& sh, const float* w, const T* Kc, const T* Vc, const T* Kd,
+                      const T* Vd, const int32_t* ctx_len, T* Kl, T* Vl, T* Kdl, T* Vdl,
+                      hipStream_t s) {
+  const long incl = sh.mask_paper ? 0 : 1;
+  const long span = sh.span() - 1 + incl;  // slots below ctx + span are visible to some row
+  const long rows = min((long)sh.S_cap, (long)sh.ctx_max + span) * (sh.d / 8);
+  const long n = max(rows, (long)sh.Hkv * (sh.d / 8));
+  dim3 grid((unsigned)((n + 255) / 256), (unsigned)(sh.L * sh.B * sh.Hkv + sh.L));
+  hipLaunchKernelGGL(soft_read_kernel<T>, grid, dim3(256), 0, s, Kc, Vc, Kd, Vd, w, sh.B, sh.Hkv,
+                     sh.S_cap, sh.k, sh.d, ctx_len, sh.ctx_hi, span, Kl, Vl, Kdl, Vdl);
+}
+
 #define WM_INST(T)                                                                              \
   template void launch_attend_prefill<T>(const Shape&, const LayerTable&, const T*, const T*,   \
                                          const T*, const T*, const T*, const int32_t*,          \
                                          const int32_t*, T*, hipStream_t);                      \
   template void launch_attend_decode<T>(const Shape&, const LayerTable&, const ChannelGroups&,  \
                                         const T*, const T*, const T*, const T*, const T*,       \
-                                        const int32_t*, const int32_t*, float*, T*, hipStream_t);
+                                        const int32_t*, const int32_t*, float*, T*, hipStream_t); \
+  template void launch_soft_read<T>(const Shape&, const float*, const T*, const T*, const T*,   \
+                                    const T*, const int32_t*, T*, T*, T*, T*, hipStream_t);
 WM_INST(float)
 WM_INST(bf16)
 #undef WM_INST

@@ -125,6 +125,13 @@ void launch_attend_decode(const Shape& sh, const LayerTable& chan_map, const Cha
                           const int32_t* ctx_len, const int32_t* doc, float* partials, T* O,
                           hipStream_t s);
 
+// The dense soft read: Kl/Vl[l][B][Hkv][S_cap][d] = sum_c w[l][c] Kc/Vc[c], over the slots the
+// call's rows may see, and Kdl/Vdl[l][Hkv][d] from the dummies.
+template <typename T>
+void launch_soft_read(const Shape& sh, const float* w, const T* Kc, const T* Vc, const T* Kd,
+                      const T* Vd, const int32_t* ctx_len, T* Kl, T* Vl, T* Kdl, T* Vdl,
+                      hipStream_t s);
+
 // -- measurement helper ---------------------------------------------------------
 // blocks x 4 waves, each issuing 8 * iters independent 32x32x16 bf16 MFMAs.
 void launch_mfma_loop(int blocks, int iters, float* sink, hipStream_t s);
