@@ -227,12 +227,20 @@ def _strip_comments(src: str) -> str:
     return "\n".join(ln.rstrip() for ln in src.splitlines() if ln.strip())
 
 
-def _kernel_source_hash():
-    """Hash of the library's code (comments and blank lines excluded), so counters taken on
-    one build stay attached to it until the code itself changes."""
+KERNEL_SOURCES = {
+    "attend": ("wm_attend.hip", "wm_device.hpp"),
+}
+POOL_SOURCES = ("wm_pool.hip", "wm_gemm.hpp", "wm_device.hpp")
+
+
+def _kernel_source_hash(phase=None):
+    """Hash of the code a phase's kernels are built from (comments and blank lines
+    excluded), so counters taken on one build stay attached to that kernel until its own
+    code changes. phase=None hashes the whole library."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_18486_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    names = sorted(os.listdir(csrc)) if phase is None else KERNEL_SOURCES.get(phase, POOL_SOURCES)
+    for name in names:
         with open(os.path.join(csrc, name), encoding="utf-8") as f:
             h.update(name.encode() + _strip_comments(f.read()).encode())
     return h.hexdigest()[:16]
@@ -247,7 +255,7 @@ def measured_traffic(workload, kernel):
     with open(path) as f:
         rec = json.load(f)
     ent = rec.get(workload, {}).get(kernel)
-    if not ent or ent.get("source_hash") != _kernel_source_hash():
+    if not ent or ent.get("source_hash") != _kernel_source_hash(kernel):
         return None
     return ent.get("bytes_per_launch")
 
@@ -350,12 +358,18 @@ def measure_ceilings(wm, torch, dev, stream):
     blocks, iters = 2048, 16384
     wm.calibrate_mfma(blocks, 64, sink, stream)
     t_mfma = timed(lambda: wm.calibrate_mfma(blocks, iters, sink, stream), 4)
+    wm.calibrate_mfma(blocks, 64, sink, stream, random_operands=True)
+    t_mfma_r = timed(lambda: wm.calibrate_mfma(blocks, iters, sink, stream,
+                                               random_operands=True), 4)
     return {"hbm_read_gbs": round(16 * n / t_read / 1e9, 1),
             "hbm_copy_gbs": round(2 * 4 * n / t_copy / 1e9, 1),
             "mfma_bf16_tflops": round(blocks * iters * 2 ** 20 / t_mfma / 1e12, 1),
+            "mfma_bf16_tflops_random_operands": round(blocks * iters * 2 ** 20 / t_mfma_r / 1e12,
+                                                      1),
             "method": "best of 4 runs of wm_calibrate_read over 4 GiB, of 6 copies of 1 GiB "
                       "(read + written bytes) and of 4 launches of wm_calibrate_mfma(2048 "
-                      "blocks, 16384 iterations), event-timed"}
+                      "blocks, 16384 iterations) on constant and on random operands, "
+                      "event-timed"}
 
 
 def blas_reference(w, log):
@@ -435,7 +449,7 @@ def decode_step(wm, torch, np, synth, hip, dev, stream, log, steps=10):
     return out
 
 
-def passes_bench(wm, torch, np, synth, hip, dev, stream, log):
+def passes_bench(wm, torch, np, synth, hip, dev, stream, log, groups=("8", "16", "1", "T")):
     """The fixed-point passes of Section 3.3 at the paper's model shape (B16 T2048 L16 k8
     D512, 6 query / 3 KV heads of 96, p = 2, bf16) with the stand-in decoder block:
     cyclic Gauss-Seidel with the paper's g = 8 groups and with g = 16, Jacobi (g = 1), 3
@@ -453,7 +467,8 @@ def passes_bench(wm, torch, np, synth, hip, dev, stream, log):
     top = torch.empty((w.B, w.T_new, w.D), dtype=w.torch_dtype, device=dev)
     out = {"workload": "fixed-point passes, the paper's model shape: B16 T2048 L16 k8 D512 "
                        "6q/3kv x96, p2, bf16, map l->l%8, stand-in block h + W_o o"}
-    for g, passes, reps in ((8, 3, 5), (16, 3, 5), (1, 3, 5), (w.T_new, 1, 1)):
+    runs = [(w.T_new, 1, 1) if g == "T" else (int(g), 3, 5) for g in groups]
+    for g, passes, reps in runs:
         dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p,
                             S_cap=w.T_new, ctx_max=0, dtype=wm.BF16, groups=g)
         ws = wm.workspace(dims, wm.OP_PASSES, dev)
@@ -491,6 +506,8 @@ def main():
                     help="skip the 32768-context decode step timed after the main workload")
     ap.add_argument("--no-passes", action="store_true",
                     help="skip the fixed-point pass driver timed at the paper's model shape")
+    ap.add_argument("--pass-groups", default="8,16,1,T",
+                    help="group counts g of the timed pass-driver runs (T: one exact pass)")
     ap.add_argument("--blas-reference", action="store_true",
                     help="also time torch.bmm (the vendor GEMM library) on the plain GEMMs of the "
                          "K/V and query projections of this workload, for comparison (stderr)")
@@ -615,6 +632,10 @@ def main():
         roof["measured_ceiling"] = ceilings["hbm_read_gbs"]
     elif w.dtype == "bf16":
         roof["measured_ceiling"] = ceilings["mfma_bf16_tflops"]
+        # the same loop on changing random operands: the rate real data gets
+        roof["measured_ceiling_random_operands"] = ceilings["mfma_bf16_tflops_random_operands"]
+        roof["frac_of_measured_ceiling_random_operands"] = round(
+            achieved / roof["measured_ceiling_random_operands"], 4)
     if "measured_ceiling" in roof:
         roof["frac_of_measured_ceiling"] = round(achieved / roof["measured_ceiling"], 4)
 
@@ -658,7 +679,8 @@ def main():
         line["decode_c5"] = decode_step(wm, torch, np, synth, hip, dev, stream, log)
     if not args.no_passes:
         torch.cuda.empty_cache()
-        line["prefill_passes"] = passes_bench(wm, torch, np, synth, hip, dev, stream, log)
+        line["prefill_passes"] = passes_bench(wm, torch, np, synth, hip, dev, stream, log,
+                                              args.pass_groups.split(","))
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline ...")
         line["cpu_baseline"] = cpu_baseline(w, P_cpu, H_cpu, (Kc, Vc) if w.ctx else None, docs_np)

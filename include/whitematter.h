@@ -175,7 +175,9 @@ int wm_q_project(const wm_dims *dims, const wm_params *params, const void *H,
  *   O        device [L][B][T_new][Hq*d] in dtype: softmax(q K^T / sqrt(d)) V over
  *            the visible slots of the mask mode (dummy Kd/Vd of the channel
  *            included in WM_MASK_PAPER)
- * Uses Kd, Vd. T_new <= 4 takes the split-S decode kernels. */
+ * Uses Kd, Vd. T_new <= 4 takes the split-S decode kernels (their partial sums go to the
+ * workspace); longer calls take the full-sequence kernels, whose workgroups take query tiles
+ * from a 512-byte work queue in the workspace, reset on `stream` before each launch. */
 int wm_channel_attend(const wm_dims *dims, const wm_params *params, const void *Q,
                       const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
                       const void *Vc, void *O, void *ws, size_t ws_bytes,
@@ -216,8 +218,8 @@ int wm_channel_attend_dense(const wm_dims *dims, const wm_params *params, const 
 
 /* wm_channel_attend for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument. Its only
- * scratch, the split-S decode partials (T_new <= 4; the full-sequence kernels need none),
- * lives in a fixed array of 64 MiB of device memory inside the library; each device holds
+ * scratch, the split-S decode partials (T_new <= 4) or the full-sequence kernels' 512-byte
+ * work queue, lives in a fixed array of 64 MiB of device memory inside the library; each device holds
  * its own copy until the process ends. The call itself allocates nothing. Calls on one
  * device share that array, so calls that overlap on one device race; serialise them (one
  * stream, or events). A call needing more scratch than the array holds (its
@@ -340,10 +342,15 @@ const char *wm_version(void);
 /* Measurement helper, not part of the method: launches `blocks` workgroups of 4
  * waves on `stream`, each wave issuing 8 * iters independent 32x32x16 bf16 MFMAs
  * (blocks * iters * 1048576 flop in all), so that a caller timing it with events
- * reads the matrix-core ceiling of the device. sink: device float, caller-owned;
- * written only in a case that does not occur, kept so the loop is not removed.
- * WM_ERR_ARG for blocks or iters <= 0 (or above 2^20 / 2^24) or a NULL sink. */
-int wm_calibrate_mfma(int32_t blocks, int32_t iters, float *sink, wm_stream_t stream);
+ * reads the matrix-core ceiling of the device. operands: 0 = small constants, the same
+ * for every MFMA (the unthrottled issue rate); 1 = pseudo-random values in [-1, 1) that
+ * change from one MFMA to the next, as real data does (the matrix cores then draw more
+ * power and the clock may drop). sink: device float, caller-owned; written only in a case
+ * that does not occur, kept so the loop is not removed.
+ * WM_ERR_ARG for blocks or iters <= 0 (or above 2^20 / 2^24), operands not 0 or 1, or a
+ * NULL sink. */
+int wm_calibrate_mfma(int32_t blocks, int32_t iters, int32_t operands, float *sink,
+                      wm_stream_t stream);
 
 /* Measurement helper, not part of the method: reads `bytes` of the device buffer buf
  * once on `stream` (the HBM read ceiling when timed with events). buf: caller-owned,

@@ -86,7 +86,7 @@ def lib() -> ctypes.CDLL:
         "wm_channel_groups": [ctypes.c_int32, ctypes.c_int32, _i32p, _i32p, _i32p],
         "wm_default_map": [ctypes.c_int32, ctypes.c_int32, _i32p],
         "wm_init_bias": [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_float)],
-        "wm_calibrate_mfma": [ctypes.c_int32, ctypes.c_int32, _vp, _vp],
+        "wm_calibrate_mfma": [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp],
         "wm_calibrate_read": [_vp, _sz, _vp, _vp],
     }
     for name, argtypes in sig.items():
@@ -328,10 +328,12 @@ def layer_step_profiled(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, eve
                                         _ptr(O), wp, wn, _stream(stream), ev))
 
 
-def calibrate_mfma(blocks: int, iters: int, sink, stream=None):
-    """Launch the matrix-core ceiling loop (blocks * iters * 2**20 flop) on the stream;
-    sink is a device float tensor the kernel keeps but does not write."""
-    _check(lib().wm_calibrate_mfma(blocks, iters, _ptr(sink), _stream(stream)))
+def calibrate_mfma(blocks: int, iters: int, sink, stream=None, random_operands=False):
+    """Launch the matrix-core ceiling loop (blocks * iters * 2**20 flop) on the stream, on
+    small constant operands or (random_operands) on changing pseudo-random ones; sink is a
+    device float tensor the kernel keeps but does not write."""
+    _check(lib().wm_calibrate_mfma(blocks, iters, 1 if random_operands else 0, _ptr(sink),
+                                   _stream(stream)))
 
 
 def calibrate_read(buf, sink, stream=None):

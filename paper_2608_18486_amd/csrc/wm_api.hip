@@ -144,6 +144,9 @@ Layout layout(const wm_dims& dd, int op) {
     if (decode_path(d)) Ly.part = take(wm::decode_partials_bytes(dense_shape(make_shape(d))));
   }
   if (layer && decode_path(d)) Ly.part = take(wm::decode_partials_bytes(one_layer(make_shape(d))));
+  // the full-sequence attention's work queue takes the decode partials' place
+  if (!decode_path(d) && (op == WM_OP_CHANNEL_ATTEND || all || layer || op == WM_OP_DENSE_ATTEND))
+    Ly.part = take(wm::kPrefillQueueBytes);
   if (op == WM_OP_KV_PROJECT || all || pool) Ly.wkv = take(wm::kv_fold_elems(make_shape(d)) * es);
   if (op == WM_OP_Q_PROJECT || all || layer) Ly.wq = take(wm::q_fold_elems(make_shape(d)) * es);
   if (op == WM_OP_ROUTER_MIX || all || pool) {
@@ -341,7 +344,7 @@ void run_attend(const wm_dims& d, const wm_params& P, const T* Q, const int32_t*
                                 (const T*)P.Vd, ctx_len, doc, part, O, s);
   else
     wm::launch_attend_prefill<T>(sh, mt, Q, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len, doc,
-                                 O, s);
+                                 O, (uint32_t*)part, s);
 }
 
 template <typename T>
@@ -433,7 +436,7 @@ void run_layer_attend(const wm_dims& d, const wm_params& P, int l, const T* H,
                                 nullptr, (float*)at(ws, Ly.part), O_l, s);
   } else {
     wm::launch_attend_prefill<T>(sh1, mt, Q, Kc, Vc, (const T*)P.Kd, (const T*)P.Vd, ctx_len,
-                                 nullptr, O_l, s);
+                                 nullptr, O_l, (uint32_t*)at(ws, Ly.part), s);
   }
 }
 
@@ -507,7 +510,8 @@ void run_attend_dense(const wm_dims& d, const wm_params& P, const float* read_w,
     wm::launch_attend_decode<T>(shd, ident, cg, Q, Kl, Vl, Kdl, Vdl, ctx_len, nullptr,
                                 (float*)at(ws, Ly.part), O, s);
   } else {
-    wm::launch_attend_prefill<T>(shd, ident, Q, Kl, Vl, Kdl, Vdl, ctx_len, nullptr, O, s);
+    wm::launch_attend_prefill<T>(shd, ident, Q, Kl, Vl, Kdl, Vdl, ctx_len, nullptr, O,
+                                 (uint32_t*)at(ws, Ly.part), s);
   }
 }
 
@@ -557,11 +561,13 @@ extern "C" {
 const char* wm_last_error(void) { return g_err; }
 const char* wm_version(void) { return "whitematter-gfx950 0.1.0"; }
 
-int wm_calibrate_mfma(int32_t blocks, int32_t iters, float* sink, wm_stream_t stream) {
+int wm_calibrate_mfma(int32_t blocks, int32_t iters, int32_t operands, float* sink,
+                      wm_stream_t stream) {
   if (blocks <= 0 || iters <= 0) return fail(WM_ERR_ARG, "blocks and iters must be positive");
   if (blocks > (1 << 20) || iters > (1 << 24)) return fail(WM_ERR_ARG, "blocks or iters too large");
+  if (operands != 0 && operands != 1) return fail(WM_ERR_ARG, "operands must be 0 or 1");
   if (!sink) return fail(WM_ERR_ARG, "sink is NULL");
-  wm::launch_mfma_loop(blocks, iters, sink, (hipStream_t)stream);
+  wm::launch_mfma_loop(blocks, iters, operands == 1, sink, (hipStream_t)stream);
   return launched();
 }
 

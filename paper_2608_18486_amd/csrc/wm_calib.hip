@@ -8,19 +8,36 @@ namespace wm {
 
 // Each wave keeps 8 independent 32x32 accumulators (no MFMA waits on the previous
 // one) and issues 8 * iters v_mfma_f32_32x32x16_bf16, i.e. 8 * iters * 32768 flop.
+// RANDOM: operands drawn per lane from a hash, four sets used in turn so the inputs of
+// consecutive MFMAs differ, as in a real GEMM or attention (the matrix cores draw more
+// power on such data than on the small constants of the other form, and the clock
+// drops accordingly).
+template <bool RANDOM>
 __global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float* sink) {
-  bf16x8 a, b;
+  constexpr int NS = RANDOM ? 4 : 1;
+  bf16x8 a[NS], b[NS];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {  // operands the compiler cannot fold
-    a[i] = (bf16)(1e-3f * (float)(threadIdx.x + i));
-    b[i] = (bf16)(1e-3f * (float)(blockIdx.x + i));
-  }
+  for (int u = 0; u < NS; ++u)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {  // operands the compiler cannot fold
+      if (RANDOM) {
+        uint32_t z = (uint32_t)((threadIdx.x * 64 + blockIdx.x * 7 + 8 * u + i)) * 2654435761u;
+        z ^= z >> 15;
+        z *= 2246822519u;
+        z ^= z >> 13;
+        a[u][i] = (bf16)((float)((int)(z & 0xFFFFu) - 32768) * (1.0f / 32768.0f));
+        b[u][i] = (bf16)((float)((int)(z >> 16) - 32768) * (1.0f / 32768.0f));
+      } else {
+        a[u][i] = (bf16)(1e-3f * (float)(threadIdx.x + i));
+        b[u][i] = (bf16)(1e-3f * (float)(blockIdx.x + i));
+      }
+    }
   f32x16 acc[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) acc[j] = zero16();
   for (int it = 0; it < iters; ++it) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = mma32(acc[j], a, b);
+    for (int j = 0; j < 8; ++j) acc[j] = mma32(acc[j], a[j % NS], b[(j + 1) % NS]);
   }
   float s = 0.f;
 #pragma unroll
@@ -30,8 +47,9 @@ __global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float* sink) 
   if (s == 1.2345e-30f) sink[0] = s;  // never true for these operands; keeps the loop live
 }
 
-void launch_mfma_loop(int blocks, int iters, float* sink, hipStream_t s) {
-  hipLaunchKernelGGL(mfma_loop_kernel, dim3(blocks), dim3(256), 0, s, iters, sink);
+void launch_mfma_loop(int blocks, int iters, bool random, float* sink, hipStream_t s) {
+  if (random) hipLaunchKernelGGL(mfma_loop_kernel<true>, dim3(blocks), dim3(256), 0, s, iters, sink);
+  else hipLaunchKernelGGL(mfma_loop_kernel<false>, dim3(blocks), dim3(256), 0, s, iters, sink);
 }
 
 // Streams n16 16-byte chunks once (grid-stride, eight loads in flight per thread) and

@@ -111,10 +111,14 @@ struct ChannelGroups {       // CSR inverse of the consumer -> channel map
   int members[kMaxLayers];
 };
 
+// queue: kPrefillQueueBytes of device memory the bf16 kernels take their tiles from
+// (reset on the stream before each launch); other paths ignore it.
+constexpr size_t kPrefillQueueBytes = 512;
 template <typename T>
 void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q,
                            const T* Kc, const T* Vc, const T* Kd, const T* Vd,
-                           const int32_t* ctx_len, const int32_t* doc, T* O, hipStream_t s);
+                           const int32_t* ctx_len, const int32_t* doc, T* O, uint32_t* queue,
+                           hipStream_t s);
 
 // Split-S decode for small T_new; partials live in the workspace.
 size_t decode_partials_bytes(const Shape& sh);
@@ -133,8 +137,9 @@ void launch_soft_read(const Shape& sh, const float* w, const T* Kc, const T* Vc,
                       hipStream_t s);
 
 // -- measurement helper ---------------------------------------------------------
-// blocks x 4 waves, each issuing 8 * iters independent 32x32x16 bf16 MFMAs.
-void launch_mfma_loop(int blocks, int iters, float* sink, hipStream_t s);
+// blocks x 4 waves, each issuing 8 * iters independent 32x32x16 bf16 MFMAs on small
+// constant operands, or (random) on hashed operands that change from one MFMA to the next.
+void launch_mfma_loop(int blocks, int iters, bool random, float* sink, hipStream_t s);
 // Reads n16 16-byte chunks of buf once.
 void launch_read_loop(const void* buf, long n16, float* sink, hipStream_t s);
 

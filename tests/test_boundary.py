@@ -198,9 +198,11 @@ def test_init_bias_and_default_map_match_oracle(wm, oracle_lib):
 
 def test_calibration_rejects_bad_arguments(wm):
     L = wm.lib()
-    assert L.wm_calibrate_mfma(0, 10, None, None) == wm.ERR_ARG
-    assert L.wm_calibrate_mfma(10, 0, None, None) == wm.ERR_ARG
-    assert L.wm_calibrate_mfma(10, 10, None, None) == wm.ERR_ARG
+    assert L.wm_calibrate_mfma(0, 10, 0, None, None) == wm.ERR_ARG
+    assert L.wm_calibrate_mfma(10, 0, 0, None, None) == wm.ERR_ARG
+    assert L.wm_calibrate_mfma(10, 10, 2, None, None) == wm.ERR_ARG
+    assert "operands" in wm.last_error()
+    assert L.wm_calibrate_mfma(10, 10, 1, None, None) == wm.ERR_ARG
     assert "sink" in wm.last_error()
 
 

@@ -240,6 +240,40 @@ def test_channel_attend(wm, T_new, ctx, mask_mode):
         check_close(O, Oo, dtype, "attend %s d%d T%d ctx%d" % (dtype, d, T_new, ctx))
 
 
+@pytest.mark.parametrize("d,L,Hq,Hkv,mask_mode,docs", [(64, 12, 16, 4, 0, False),
+                                                       (64, 12, 16, 4, 1, True),
+                                                       (96, 16, 6, 3, 0, False),
+                                                       (96, 16, 6, 3, 0, True)])
+def test_channel_attend_work_queue(wm, d, L, Hq, Hkv, mask_mode, docs):
+    """More query tiles (128 queries of one consumer, sequence and head) than the CUs hold at
+    once, so the bf16 kernels run persistent workgroups that take tiles from the work queue;
+    every output element against the oracle, with a ragged last tile and cached context."""
+    T_new, ctx = 300, 40
+    w = synth.small("queue_d%d" % d, B=2, T_new=T_new, L=L, k=4, D=64, Hq=Hq, Hkv=Hkv, d=d,
+                    ctx=ctx + T_new, dtype="bf16", chan_map=[l % 4 for l in range(L)])
+    tiles = (T_new + 127) // 128 * Hq * w.B * L
+    resident = torch.cuda.get_device_properties(0).multi_processor_count * (3 if d == 64 else 2)
+    assert tiles > resident, (tiles, resident)
+    print("queue case d%d tiles %d resident %d mask %d docs %s" % (d, tiles, resident, mask_mode,
+                                                                   docs), flush=True)
+    P = synth.make_params(w, _bias(w))
+    Q = synth.make_queries(w)
+    Kc, Vc = synth.make_cache_cpu(w)
+    ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+    doc = synth.make_doc_start(w, ctx_len, mean_len=37.0) if docs else None
+    Oo = oracle.channel_attend(_odims(w, mask_mode=mask_mode), P, Q, w.chan_map, ctx_len.numpy(),
+                               _f64(Kc), _f64(Vc),
+                               doc_start=doc.numpy() if docs else None)
+    O = torch.full((w.L, w.B, w.T_new, w.Hq * w.d), float("nan"), dtype=w.torch_dtype,
+                   device="cuda")
+    dims = _gdims(wm, w, mask_mode=mask_mode, ctx_max=ctx)
+    wm.channel_attend(dims, _dev(P), Q.cuda(), w.chan_map, ctx_len.cuda(), Kc.cuda(), Vc.cuda(),
+                      O, doc_start=doc.cuda() if docs else None)
+    torch.cuda.synchronize()
+    assert not torch.isnan(O.float()).any(), "a query tile was never computed"
+    check_close(O, Oo, "bf16", "queue d%d mask%d docs%d" % (d, mask_mode, docs))
+
+
 # ------------------------------------------------------------ full workloads
 
 FULL = ["c2_T2048_L12_k12", "c3_T2048_L12_k6", "c4_T4096_L24_k12", "paper_T2048_L16_k8",
@@ -349,9 +383,10 @@ def test_decode_step_at_full_size(wm):
 def test_calibration_loop_runs(wm):
     """The matrix-core ceiling loop launches, finishes and leaves its sink untouched."""
     sink = torch.zeros(1, dtype=torch.float32, device="cuda")
-    wm.calibrate_mfma(256, 16, sink, torch.cuda.current_stream())
-    torch.cuda.synchronize()
-    assert float(sink.item()) == 0.0
+    for random_operands in (False, True):
+        wm.calibrate_mfma(256, 16, sink, torch.cuda.current_stream(), random_operands)
+        torch.cuda.synchronize()
+        assert float(sink.item()) == 0.0
 
 
 @pytest.mark.gpu
