@@ -622,16 +622,27 @@ template <bool Q> struct ProjShapeD<bf16, true, 96, Q> { using C = ProjCfg<bf16,
 // Router: 288 channels x 128 tokens per bf16 block on 6 waves, 96 x 64 per wave (the
 // channel count 2kL is small: 288 for L = k = 12, so a block covers all of it and the
 // stacked states are read once; measured 10% faster than 96-channel blocks at L = 24).
-template <typename T, bool FEW> struct RouterShape;
+// Long K (the stacked states of many wide layers, L' D >= kRouterWideK) in bf16: 288 x 256
+// on 12 waves, 3 per SIMD (the 6-wave block leaves two of the four SIMDs one wave each),
+// its grid filled by splitting K. Measured: 21% faster at L = 24, D = 1024; no change at
+// L = 12, D = 768; 12% slower at the paper's L' = 8, D = 512 (a short K, whose split
+// doubles the fixed costs), so the 6-wave block stays there.
+template <typename T, bool FEW, bool WIDE = false> struct RouterShape;
 #ifndef WM_ROUTER_BF16
 #define WM_ROUTER_BF16 32, 3, 2, 3, 2
 #endif
 template <> struct RouterShape<bf16, false> { using C = ProjCfg<bf16, WM_ROUTER_BF16>; };
+template <> struct RouterShape<bf16, false, true> { using C = ProjCfg<bf16, 32, 3, 4, 3, 2>; };
 template <> struct RouterShape<bf16, true> { using C = ProjCfg<bf16, 32, 1, 2, 3, 1>; };
 template <> struct RouterShape<float, false> { using C = ProjCfg<float, 32, 1, 4, 3, 1>; };
+template <> struct RouterShape<float, false, true> { using C = ProjCfg<float, 32, 1, 4, 3, 1>; };
 template <> struct RouterShape<float, true> { using C = ProjCfg<float, 32, 1, 2, 3, 1>; };
 
 constexpr int kFewTokens = 64;
+constexpr int kRouterWideK = 16384;
+static bool router_wide(const Shape& sh) {
+  return sh.N() > kFewTokens && (long)sh.Lp * sh.D >= kRouterWideK;
+}
 
 // ------------------------------------------------------------------ router
 size_t router_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.L * sh.Lp * sh.D; }
@@ -644,9 +655,11 @@ size_t router_fold_elems(const Shape& sh) { return 2ul * sh.k * sh.L * sh.Lp * s
 #endif
 static int router_layers_per_split(const Shape& sh) {
   using CF = RouterShape<bf16, false>::C;
+  using CW = RouterShape<bf16, false, true>::C;
   using CD = RouterShape<bf16, true>::C;
-  const bool few = sh.N() <= kFewTokens;
-  const int tok = few ? CD::NTOK : CF::NTOK, och = few ? CD::OT : CF::OT;
+  const bool few = sh.N() <= kFewTokens, wide = router_wide(sh);
+  const int tok = few ? CD::NTOK : wide ? CW::NTOK : CF::NTOK;
+  const int och = few ? CD::OT : wide ? CW::OT : CF::OT;
   const long blocks = (long)((sh.N() + tok - 1) / tok) * ((2 * sh.k * sh.L + och - 1) / och);
   int s = 1;
   while (s < sh.Lp && blocks * s < WM_ROUTER_MIN_BLOCKS) s *= 2;
@@ -663,11 +676,11 @@ size_t router_partials_bytes(const Shape& sh) {
   return s > 1 ? (size_t)s * sh.N() * 2 * sh.k * sh.L * sizeof(float) : 0;
 }
 
-template <typename T, bool FEW>
+template <typename T, bool FEW, bool WIDE>
 static void router_gemm(const Shape& sh, const LayerTable& sel, const T* H, const float* rinv,
                         const T* wf, const T* b_alpha, float* logits, float* part,
                         hipStream_t s) {
-  using C = typename RouterShape<T, FEW>::C;
+  using C = typename RouterShape<T, FEW, WIDE>::C;
   const int M = sh.N(), kL = sh.k * sh.L, Nout = 2 * kL, K = sh.Lp * sh.D;
   const int seg = sh.D / C::BK, splits = router_splits(sh);
   const int per = router_layers_per_split(sh);
@@ -707,8 +720,12 @@ void launch_router(const Shape& sh, const LayerTable& sel, const T* H, const flo
     return;
   }
   if (!prefolded) launch_router_fold<T>(sh, sel, g_pre, W_alpha, wfold, s);
-  if (M <= kFewTokens) router_gemm<T, true>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
-  else router_gemm<T, false>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
+  if (M <= kFewTokens)
+    router_gemm<T, true, false>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
+  else if (router_wide(sh))
+    router_gemm<T, false, true>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
+  else
+    router_gemm<T, false, false>(sh, sel, H, rinv, wfold, b_alpha, logits, part, s);
 }
 
 // --------------------------------------------------------------------- mix

@@ -171,6 +171,28 @@ def test_router_mix(wm, name, mix_mode):
         assert torch.allclose(s, torch.ones_like(s), atol=1e-5) and (alpha > 0).all()
 
 
+@pytest.mark.parametrize("L,k,p,T_new", [(16, 4, 1, 200), (24, 3, 1, 70), (20, 8, 1, 300)])
+def test_router_mix_long_k(wm, L, k, p, T_new):
+    """The router's long-K path (stacked states of at least 16384 elements: the 12-wave block
+    with K split at layer boundaries and the partial sums reduced), every weight and mixed
+    channel against the oracle, ragged token tiles."""
+    w = synth.small("router_long_L%d" % L, B=2, T_new=T_new, L=L, k=k, D=1024, Hq=4, Hkv=2,
+                    d=64, dtype="bf16", p=p)
+    assert (L + p - 1) // p * w.D >= 16384 and w.N > 64
+    print("router long K: L%d k%d p%d N%d" % (L, k, p, w.N), flush=True)
+    rng = np.random.default_rng(5)
+    P = synth.make_params(w, rng.normal(0, 1, size=(2, w.k * w.L)), gains="random")
+    H = synth.make_states(w)
+    ao, mo = oracle.router_mix(_odims(w), P, H)
+    dims = _gdims(wm, w)
+    alpha = torch.empty((2, w.N, w.k, w.L), dtype=torch.float32, device="cuda")
+    mixed = torch.empty((2, w.k, w.N, w.D), dtype=w.torch_dtype, device="cuda")
+    wm.router_mix(dims, _dev(P), H.cuda(), mixed, alpha)
+    torch.cuda.synchronize()
+    check_close(alpha, ao, "bf16", "long-K alpha")
+    check_close(mixed, mo, "bf16", "long-K mixed")
+
+
 def test_router_zero_weights_give_bias_exactly(wm):
     """W_alpha = 0: the mixing weights are the bias, exactly (fp32 and bf16)."""
     for name in ("c1_tiny_f32", "bf16_ragged_gqa"):
