@@ -92,6 +92,7 @@ template <typename T> struct AttnArgs {
   int gs, gq, ctx_hi;  // query i of sequence b sits at position ctx_len[b] + gq + gs i
   float scale_log2;  // log2(e) / sqrt(d)
   LayerTable chan;
+  LayerTable lord;  // the consumers in channel order (the bf16 kernels' tile order)
 };
 
 #ifndef WM_PREFILL_WAVES
@@ -745,13 +746,20 @@ __device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile,
                                         int* s_lo) {
   using P = PfDma<QT, DH>;
   constexpr int NKS = P::NKS, NDT = P::NDT;
+  // Tile order: sequence, KV head, consumer (in channel order), query head of the KV
+  // head's group, query tile (longest first). Consecutive tiles read one channel's K/V
+  // slice: every query tile and grouped head of a consumer, then the next consumer of
+  // the same channel, so an XCD's L2 serves a slice to all its readers.
+  const int G = a.Hq / a.Hkv;
   const int qtile = a.n_qtiles - 1 - tile % a.n_qtiles;
   int y = tile / a.n_qtiles;
-  const int hq = y % a.Hq;
-  y /= a.Hq;
-  const int b = y % a.B, l = y / a.B;
+  const int hg = y % G;
+  y /= G;
+  const int li = y % a.L;
+  y /= a.L;
+  const int kvh = y % a.Hkv, b = y / a.Hkv;
+  const int hq = kvh * G + hg, l = a.lord.v[li];
   const int c = a.chan.v[l];
-  const int kvh = hq / (a.Hq / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ctx = __builtin_amdgcn_readfirstlane(ctx_at(a.ctx_len, b, a.ctx_hi));
@@ -1061,9 +1069,13 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
   if (sh.N() <= 0) return;
   constexpr int BQ = PrefillCfg<T, 64>::BQ, NT = PrefillCfg<T, 64>::NT;
   static_assert(BQ == PrefillCfg<T, 32>::BQ && NT == PrefillCfg<T, 32>::NT, "tile shapes");
+  LayerTable lord{};  // consumers sorted by channel, stable
+  for (int c = 0, n = 0; c < kMaxLayers && n < sh.L; ++c)
+    for (int l = 0; l < sh.L; ++l)
+      if (chan_map.v[l] == c) lord.v[n++] = l;
   AttnArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, doc, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
                 sh.mask_paper, (sh.T_new + BQ - 1) / BQ, sh.gs, sh.gq, sh.ctx_hi,
-                kLog2e / sqrtf((float)sh.d), chan_map};
+                kLog2e / sqrtf((float)sh.d), chan_map, lord};
   dim3 grid(a.n_qtiles * sh.Hq * sh.B * sh.L);
   if (sizeof(T) == 2 && (sh.d == 64 || sh.d == 96)) {  // fp32 at d = 96 fails validation
     constexpr int BQD = PfDma<kPfQt, 64>::BQ;
