@@ -228,7 +228,7 @@ def _strip_comments(src: str) -> str:
 
 
 KERNEL_SOURCES = {
-    "attend": ("wm_attend.hip", "wm_device.hpp"),
+    "attend": ("wm_attend.hip", "wm_device.hpp", "wm_frag.hpp"),
 }
 POOL_SOURCES = ("wm_pool.hip", "wm_gemm.hpp", "wm_device.hpp")
 

@@ -86,7 +86,8 @@ enum wm_op {
   WM_OP_POOL = 5,          /* wm_pool */
   WM_OP_LAYER_ATTEND = 6,  /* wm_layer_attend */
   WM_OP_PASSES = 7,        /* wm_prefill_passes */
-  WM_OP_DENSE_ATTEND = 8   /* wm_channel_attend_dense */
+  WM_OP_DENSE_ATTEND = 8,  /* wm_channel_attend_dense */
+  WM_OP_ATTEND_BACKWARD = 9 /* wm_channel_attend_backward */
 };
 
 /* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
@@ -215,6 +216,33 @@ int wm_channel_attend_dense(const wm_dims *dims, const wm_params *params, const 
                             const void *Q, const int32_t *ctx_len, const void *Kc,
                             const void *Vc, void *O, void *ws, size_t ws_bytes,
                             wm_stream_t stream);
+
+/* Gradients of wm_channel_attend (Section 3.1 Step 3 with the dummy slot of Section 3.2),
+ * the attention part of the backward pass that training runs through its last n_g passes
+ * (Section 3.3, truncated backpropagation). For the loss gradient dO of the output, with
+ * scores s_j = q.k_j / sqrt(d) over a row's visible slots and the dummy, P = softmax(s),
+ * dS_j = P_j (dO.v_j - dO.O): dQ = sum_j dS_j k_j / sqrt(d); every slot's dK sums
+ * dS_j q / sqrt(d) and its dV sums P_j dO over all rows that read it (every consumer of
+ * its channel and every query head of its KV head); the dummy's likewise.
+ * bf16 only, head dims 64 and 96, full-sequence calls (T_new > 4) of contiguous tokens
+ * (dims.groups <= 1), no document mask.
+ *   Q, chan_map, ctx_len, Kc, Vc  as wm_channel_attend
+ *   O        device [L][B][T_new][Hq*d] bf16: that call's output
+ *   dO       device [L][B][T_new][Hq*d] bf16: the gradient of the loss in O
+ *   dQ       device float [L][B][Hq][T_new][d]
+ *   dKc, dVc device float [k][B][Hkv][S_cap][d]: slots below ctx_len[b] + T_new of every
+ *            (channel, sequence, KV head) are written (zero where no row reads the slot);
+ *            the others are left as they are
+ *   dKd, dVd device float [k][Hkv][d] (written; zero in WM_MASK_INCLUSIVE)
+ * Workspace: wm_workspace_size(dims, WM_OP_ATTEND_BACKWARD) bytes (four floats per query
+ * row: the row's log-sum-exp, dO.O and the dummy's weight and dS). Errors: WM_ERR_DTYPE for
+ * fp32, WM_ERR_SHAPE for other head dims or T_new <= 4, WM_ERR_ARG for groups > 1 or a
+ * NULL pointer, otherwise as wm_channel_attend. */
+int wm_channel_attend_backward(const wm_dims *dims, const wm_params *params, const void *Q,
+                               const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
+                               const void *Vc, const void *O, const void *dO, float *dQ,
+                               float *dKc, float *dVc, float *dKd, float *dVd, void *ws,
+                               size_t ws_bytes, wm_stream_t stream);
 
 /* wm_channel_attend for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument. Its only

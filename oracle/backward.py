@@ -25,6 +25,8 @@ F64 = torch.float64
 
 
 def _t(a, grad=False):
+    if hasattr(a, "detach"):  # a torch tensor (any dtype): exact widening to float64
+        a = a.detach().to("cpu").double().numpy()
     t = torch.as_tensor(np.ascontiguousarray(np.asarray(a, dtype=np.float64)), dtype=F64)
     return t.clone().requires_grad_(grad)
 
@@ -142,8 +144,7 @@ def attend(dims: Dims, Kd, Vd, Q, chan_map, ctx, K, V):
 
 def _params(params, grad):
     arrays = params.arrays if hasattr(params, "arrays") else params
-    return {n: _t(arrays[n].detach().cpu().double().numpy() if hasattr(arrays[n], "detach")
-                  else arrays[n], grad) for n in PARAM_NAMES}
+    return {n: _t(arrays[n], grad) for n in PARAM_NAMES}
 
 
 def _ctx(dims, ctx_len):

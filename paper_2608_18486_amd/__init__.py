@@ -24,7 +24,7 @@ MIX_LINEAR, MIX_SOFTMAX = 0, 1
 MASK_PAPER, MASK_INCLUSIVE = 0, 1
 ROUTER_DYNAMIC, ROUTER_STATIC, ROUTER_NOFEEDBACK = 0, 1, 2
 (OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP, OP_POOL,
- OP_LAYER_ATTEND, OP_PASSES, OP_DENSE_ATTEND) = range(9)
+ OP_LAYER_ATTEND, OP_PASSES, OP_DENSE_ATTEND, OP_ATTEND_BACKWARD) = range(10)
 
 PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
                "Kd", "Vd", "g_in", "Wq", "g_qnorm")
@@ -79,6 +79,8 @@ def lib() -> ctypes.CDLL:
         "wm_pool": [D, P, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_channel_attend_static": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp],
         "wm_channel_attend_dense": [D, P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_channel_attend_backward": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_layer_attend": [D, P, ctypes.c_int32, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_prefill_passes": [D, P, _vp, _vp, _i32p, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp,
                               _sz, _vp],
@@ -274,6 +276,17 @@ def channel_attend_dense(dims: Dims, params, read_w, Q, ctx_len, Kc, Vc, O, ws=N
     _check(lib().wm_channel_attend_dense(ctypes.byref(dims), _pref(params), _ptr(read_w),
                                          _ptr(Q), _ptr(ctx_len), _ptr(Kc), _ptr(Vc), _ptr(O),
                                          wp, wn, _stream(stream)))
+
+
+def channel_attend_backward(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, dO, dQ, dKc,
+                            dVc, dKd, dVd, ws=None, stream=None):
+    """Gradients of channel_attend for the output gradient dO: dQ, dKc, dVc, dKd, dVd
+    (device float32 tensors, written)."""
+    ws, wp, wn = _ws(dims, OP_ATTEND_BACKWARD, ws, getattr(Q, "device", None))
+    _check(lib().wm_channel_attend_backward(ctypes.byref(dims), _pref(params), _ptr(Q),
+                                            _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
+                                            _ptr(O), _ptr(dO), _ptr(dQ), _ptr(dKc), _ptr(dVc),
+                                            _ptr(dKd), _ptr(dVd), wp, wn, _stream(stream)))
 
 
 def channel_attend_static(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, stream=None):

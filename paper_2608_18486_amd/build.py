@@ -19,6 +19,7 @@ SOURCES = {
     "wm_api.hip": [],
     "wm_pool.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "wm_attend.hip": [],
+    "wm_backward.hip": [],
     "wm_calib.hip": [],
 }
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

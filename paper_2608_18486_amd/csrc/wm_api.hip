@@ -144,6 +144,7 @@ Layout layout(const wm_dims& dd, int op) {
     if (decode_path(d)) Ly.part = take(wm::decode_partials_bytes(dense_shape(make_shape(d))));
   }
   if (layer && decode_path(d)) Ly.part = take(wm::decode_partials_bytes(one_layer(make_shape(d))));
+  if (op == WM_OP_ATTEND_BACKWARD) Ly.part = take(wm::attend_backward_rows_bytes(make_shape(d)));
   // the full-sequence attention's work queue takes the decode partials' place
   if (!decode_path(d) && (op == WM_OP_CHANNEL_ATTEND || all || layer || op == WM_OP_DENSE_ATTEND))
     Ly.part = take(wm::kPrefillQueueBytes);
@@ -160,13 +161,13 @@ Layout layout(const wm_dims& dd, int op) {
 bool uses_cache(int op) {
   return op == WM_OP_KV_PROJECT || op == WM_OP_CHANNEL_ATTEND || op == WM_OP_LAYER_STEP ||
          op == WM_OP_POOL || op == WM_OP_LAYER_ATTEND || op == WM_OP_PASSES ||
-         op == WM_OP_DENSE_ATTEND;
+         op == WM_OP_DENSE_ATTEND || op == WM_OP_ATTEND_BACKWARD;
 }
 
 int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (!dp) return fail(WM_ERR_ARG, "dims is NULL");
   const wm_dims& d = *dp;
-  if (op < WM_OP_ROUTER_MIX || op > WM_OP_DENSE_ATTEND) return fail(WM_ERR_ARG, "unknown op %d", op);
+  if (op < WM_OP_ROUTER_MIX || op > WM_OP_ATTEND_BACKWARD) return fail(WM_ERR_ARG, "unknown op %d", op);
   if (d.dtype != WM_F32 && d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "unknown dtype %d", d.dtype);
   if (d.mix_mode != WM_MIX_LINEAR && d.mix_mode != WM_MIX_SOFTMAX)
     return fail(WM_ERR_DTYPE, "unknown mix_mode %d", d.mix_mode);
@@ -825,6 +826,45 @@ int wm_channel_attend_dense(const wm_dims* dims, const wm_params* params, const 
   else
     run_attend_dense<float>(d, *params, read_w, (const float*)Q, ctx_len, (const float*)Kc,
                             (const float*)Vc, (float*)O, ws, s);
+  return launched();
+}
+
+int wm_channel_attend_backward(const wm_dims* dims, const wm_params* params, const void* Q,
+                               const int32_t* chan_map, const int32_t* ctx_len, const void* Kc,
+                               const void* Vc, const void* O, const void* dO, float* dQ,
+                               float* dKc, float* dVc, float* dKd, float* dVd, void* ws,
+                               size_t ws_bytes, wm_stream_t stream) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_ATTEND_BACKWARD, chan_map));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  if (d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "the attention gradients are built for bf16");
+  if (d.d != 64 && d.d != 96)
+    return fail(WM_ERR_SHAPE, "the attention gradients support head dims 64 and 96");
+  if (decode_path(d))
+    return fail(WM_ERR_SHAPE, "the attention gradients need a full-sequence call (T_new > 4)");
+  if (group_stride(d) > 1)
+    return fail(WM_ERR_ARG, "the attention gradients need contiguous new tokens (groups <= 1)");
+  if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_KD, P_VD}));
+  else if (!params) return fail(WM_ERR_ARG, "params is NULL");
+  WM_TRY(need_ptr(Q, "Q"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(need_ptr(O, "O"));
+  WM_TRY(need_ptr(dO, "dO"));
+  WM_TRY(need_ptr(dQ, "dQ"));
+  WM_TRY(need_ptr(dKc, "dKc"));
+  WM_TRY(need_ptr(dVc, "dVc"));
+  WM_TRY(need_ptr(dKd, "dKd"));
+  WM_TRY(need_ptr(dVd, "dVd"));
+  WM_TRY(check_ws(d, WM_OP_ATTEND_BACKWARD, ws, ws_bytes));
+  (void)hipGetLastError();
+  const Layout Ly = layout(d, WM_OP_ATTEND_BACKWARD);
+  wm::launch_attend_backward(make_shape(d), map_table(d, chan_map), groups(d, chan_map),
+                             (const bf16*)Q, (const bf16*)Kc, (const bf16*)Vc,
+                             (const bf16*)params->Kd, (const bf16*)params->Vd, (const bf16*)O,
+                             (const bf16*)dO, ctx_len, dQ, dKc, dVc, dKd, dVd,
+                             (float*)at(ws, Ly.part), (hipStream_t)stream);
   return launched();
 }
 

@@ -23,6 +23,7 @@
 #include <type_traits>
 
 #include "wm_device.hpp"
+#include "wm_frag.hpp"
 #include "wm_internal.hpp"
 
 namespace wm {
@@ -138,7 +139,6 @@ __device__ __forceinline__ void st_pair_t(float* vt, int ld, const f32x8& a, con
 // lane i's element t comes from element i % 4 of the 8-byte chunk addressed by lane
 // 4t + i / 4, so lane j addresses key (kb + 4h + 8s + j / 4), columns
 // 32 dt + 16 (group & 1) + 4 (j % 4) .. + 3, and receives 4 keys of its own column.
-typedef short i16x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ bf16x8 ld_vt_tr(const bf16* vs, int ldv, int kb, int dt, int lane) {
   const int j = lane & 15, grp = lane >> 4, h = lane >> 5;
   const bf16* p = vs + (kb + 4 * h + (j >> 2)) * ldv + 32 * dt + 16 * (grp & 1) + 4 * (j & 3);
@@ -498,23 +498,6 @@ template <int QT, int DH_> struct PfDma {
   static_assert(SMEM_BYTES % (16 * NT) == 0, "the rings are zeroed in whole passes");
 };
 
-// Chunk swizzle of slot row `row`.
-// Head dim 64 (128-B rows): bit-reversal of (row / 2) mod 8. Rows 2x and 2x+1 share a
-// 256-B bank line, and rows 4y, 4y+2 differ in bit 2, which keeps a transposing read's
-// 4 chunks apart.
-// Head dim 96 (192-B rows): (row / 4) mod 4, applied within aligned groups of 4 chunks.
-// Row 4a + b starts at 16-B bank group 12 b mod 16 (one of 0, 4, 8, 12 per b), and the
-// swizzle adds a distinct 0..3 per a, so 16 consecutive rows' chunk c, and 4 rows x one
-// aligned 4-chunk group, fall in 16 distinct bank groups.
-template <int DH> __device__ __forceinline__ int pf_swz(int row) {
-  if constexpr (DH == 64) {
-    const int x = (row >> 1) & 7;
-    return ((x & 1) << 2) | (x & 2) | (x >> 2);
-  } else {
-    return (row >> 2) & 3;
-  }
-}
-
 template <int QT, int DH> struct PfState {  // one wave's running softmax state (2 lanes per row)
   f32x16 o[DH / 32][QT];  // O^T per 32-column tile of the values and query tile
   bf16x8 pf[2][QT];       // P(i-1)^T fragments (keys 0-15, 16-31 of the step)
@@ -522,53 +505,12 @@ template <int QT, int DH> struct PfState {  // one wave's running softmax state 
   float m[QT], lsum[QT];
 };
 
-// Byte offsets of one lane's fragment reads inside a half block (32 slot rows) of LDS:
-// k[ks] for the K fragment of k16 step ks, v[dt][s] for the s-th transposing read of the
-// V^T fragment of value tile dt (the second 16 rows of the half add 16 rows). They do
-// not depend on the ring stage, so the stage and half fold into the instructions'
-// offset fields.
-template <int DH> struct PfLane {
-  uint32_t k[DH / 16], v[DH / 32][2];
-};
-template <int DH> __device__ __forceinline__ PfLane<DH> pf_lane(int lane) {
-  constexpr int ROW = 2 * DH;
-  const int h = lane >> 5, r = lane & 31, j = lane & 15, grp = lane >> 4;
-  PfLane<DH> o;
-  const int sw = pf_swz<DH>(r);
-#pragma unroll
-  for (int ks = 0; ks < DH / 16; ++ks) o.k[ks] = r * ROW + 16 * ((2 * ks + h) ^ sw);
-#pragma unroll
-  for (int dt = 0; dt < DH / 32; ++dt)
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int row = 4 * h + (j >> 2) + 8 * s;
-      const int chunk = 4 * dt + 2 * (grp & 1) + ((j & 3) >> 1);
-      o.v[dt][s] = row * ROW + 16 * (chunk ^ pf_swz<DH>(row)) + 8 * (j & 1);
-    }
-  return o;
-}
 // byte offsets of the K and V ring half blocks: ring stage u, half hf
 template <int DH> constexpr uint32_t pf_kh(int u, int hf) {
   return u * 64 * 2 * DH + hf * 32 * 2 * DH;
 }
 template <int DH> constexpr uint32_t pf_vh(int u, int hf) {
   return kPfNs * 64 * 2 * DH + u * 64 * 2 * DH + hf * 32 * 2 * DH;
-}
-
-template <int DH>
-__device__ __forceinline__ bf16x8 pf_ldk(const char* sm, const PfLane<DH>& lo, uint32_t kh,
-                                         int ks) {
-  return *(const bf16x8*)(sm + lo.k[ks] + kh);
-}
-// V^T fragment (value column 32 dt + r, keys 16 hf + 4h + {0..3, 8..11} of the half)
-template <int DH>
-__device__ __forceinline__ bf16x8 pf_ldv(const char* sm, const PfLane<DH>& lo, uint32_t vh,
-                                         int hf, int dt) {
-  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-  const uint32_t base = vh + hf * 16 * 2 * DH;
-  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sm + lo.v[dt][0] + base));
-  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sm + lo.v[dt][1] + base));
-  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // S^T fragment rows of one step for one query tile: the 32 K slots of the half block

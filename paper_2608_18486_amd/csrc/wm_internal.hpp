@@ -120,6 +120,16 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
                            const int32_t* ctx_len, const int32_t* doc, T* O, uint32_t* queue,
                            hipStream_t s);
 
+// Gradients of the full-sequence channel attention (bf16, head dims 64 and 96): dQ
+// [L][B][Hq][T][d], dKc / dVc [k][B][Hkv][S_cap][d] (slots below ctx_len[b] + T written),
+// dKd / dVd [k][Hkv][d], all fp32; rows: attend_backward_rows_bytes of workspace.
+size_t attend_backward_rows_bytes(const Shape& sh);
+void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
+                            const ChannelGroups& groups, const bf16* Q, const bf16* Kc,
+                            const bf16* Vc, const bf16* Kd, const bf16* Vd, const bf16* O,
+                            const bf16* dO, const int32_t* ctx_len, float* dQ, float* dKc,
+                            float* dVc, float* dKd, float* dVd, float* rows, hipStream_t s);
+
 // Split-S decode for small T_new; partials live in the workspace.
 size_t decode_partials_bytes(const Shape& sh);
 int decode_splits(const Shape& sh);

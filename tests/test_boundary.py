@@ -262,3 +262,24 @@ def test_new_entry_points_reject_bad_arguments_before_launch(wm):
     with pytest.raises(wm.WMError) as e:
         wm.pool(_dims(wm), None, None, None, None, None)
     assert e.value.code == wm.ERR_ARG  # params NULL
+
+
+def test_attention_backward_rejects_unsupported_calls_before_launch(wm):
+    """The attention gradients cover bf16 full-sequence calls at head dims 64 and 96 with
+    contiguous tokens; everything else is refused on the host with its own code."""
+    cmap = [0, 1, 0, 1]
+    args = (None, None, cmap, None, None, None, None, None, None, None, None, None, None)
+
+    def call(**kw):
+        with pytest.raises(wm.WMError) as e:
+            wm.channel_attend_backward(_dims(wm, **kw), *args)
+        return e.value.code
+
+    assert call(d=64, dtype=wm.F32) == wm.ERR_DTYPE
+    assert call(d=32) == wm.ERR_SHAPE
+    assert call(d=64, T_new=4) == wm.ERR_SHAPE
+    assert call(d=64, groups=2) == wm.ERR_ARG
+    assert call(d=64) == wm.ERR_ARG            # params NULL
+    # four floats per query row of workspace
+    d = _dims(wm, d=64)
+    assert wm.workspace_size(d, wm.OP_ATTEND_BACKWARD) >= 16 * d.L * d.B * d.Hq * d.T_new
