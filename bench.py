@@ -449,6 +449,58 @@ def decode_step(wm, torch, np, synth, hip, dev, stream, log, steps=10):
     return out
 
 
+def attend_backward_bench(wm, torch, np, synth, hip, dev, stream, log, w, reps=5):
+    """The attention gradients of the headline pass (wm_channel_attend_backward), the part
+    of the backward pass that runs through the attention: seeded queries, cache and output
+    gradient (as in the parity test), O from the forward kernel, event-timed. TFLOP/s count
+    the five gradient products of the standard tally (S = QK^T, dP = dO V^T, dQ = dS K,
+    dK = dS^T Q, dV = P^T dO: 10 d flops per visible pair, 2.5 times the forward's); the
+    kernels also recompute S for the row log-sum-exp and S, dP in both the query-major and
+    the slot-major kernel (16 d flops per pair executed)."""
+    log("bench: attention gradients %s" % w.name)
+    P = wm.ParamSet({k: v.to(dev) for k, v in
+                     synth.make_params(w, np.asarray(wm.init_bias(w.L, w.k))).items()})
+    bf = torch.bfloat16
+    Q = synth._normal((w.L, w.B, w.Hq, w.T_new, w.d), 1.0, 9100, bf).to(dev)
+    shape = (w.k, w.B, w.Hkv, w.T_new, w.d)
+    Kc = synth._normal(shape, 1.0, 9101, bf).to(dev)
+    Vc = synth._normal(shape, 1.0, 9102, bf).to(dev)
+    dO = synth._normal((w.L, w.B, w.T_new, w.Hq * w.d), 1.0, 9103, bf).to(dev)
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=bf, device=dev)
+    dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p, S_cap=w.T_new,
+                        ctx_max=0, dtype=wm.BF16)
+    wm.channel_attend(dims, P, Q, w.chan_map, None, Kc, Vc, O, stream=stream)
+    f32 = dict(dtype=torch.float32, device=dev)
+    g = [torch.empty(tuple(Q.shape), **f32), torch.empty(shape, **f32),
+         torch.empty(shape, **f32), torch.empty((w.k, w.Hkv, w.d), **f32),
+         torch.empty((w.k, w.Hkv, w.d), **f32)]
+    ws = wm.workspace(dims, wm.OP_ATTEND_BACKWARD, dev)
+    for _ in range(2):
+        wm.channel_attend_backward(dims, P, Q, w.chan_map, None, Kc, Vc, O, dO, *g, ws=ws,
+                                   stream=stream)
+    torch.cuda.synchronize()
+    ev = [hip.create() for _ in range(reps + 1)]
+    hip.record(ev[0], stream.cuda_stream)
+    for r in range(reps):
+        wm.channel_attend_backward(dims, P, Q, w.chan_map, None, Kc, Vc, O, dO, *g, ws=ws,
+                                   stream=stream)
+        hip.record(ev[r + 1], stream.cuda_stream)
+    torch.cuda.synchronize()
+    ms = float(np.median([hip.elapsed_ms(ev[r], ev[r + 1]) for r in range(reps)]))
+    for e in ev:
+        hip.destroy(e)
+    flops = 2.5 * attn_flops(w.L, w.Hq, w.d, visible_pairs(w))
+    tf = flops / (ms * 1e-3) / 1e12
+    del Q, Kc, Vc, dO, O, g, ws
+    torch.cuda.empty_cache()
+    log("bench: attention gradients %.3f ms, %.1f TFLOP/s (%.1f%% of the bf16 peak)"
+        % (ms, tf, 100 * tf / PEAK_TFLOPS["bf16"]))
+    return {"workload": WORKLOAD_LABEL[w.name], "ms_median": round(ms, 4),
+            "gflop": round(flops / 1e9, 1), "tflops": round(tf, 1),
+            "frac_of_bf16_peak": round(tf / PEAK_TFLOPS["bf16"], 4),
+            "executed_gflop": round(flops * 16 / 10 / 1e9, 1), "reps": reps}
+
+
 def passes_bench(wm, torch, np, synth, hip, dev, stream, log, groups=("8", "16", "1", "T")):
     """The fixed-point passes of Section 3.3 at the paper's model shape (B16 T2048 L16 k8
     D512, 6 query / 3 KV heads of 96, p = 2, bf16) with the stand-in decoder block:
@@ -504,6 +556,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the 32768-context decode step timed after the main workload")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the attention gradients timed on the main workload")
     ap.add_argument("--no-passes", action="store_true",
                     help="skip the fixed-point pass driver timed at the paper's model shape")
     ap.add_argument("--pass-groups", default="8,16,1,T",
@@ -677,6 +731,11 @@ def main():
         del Kc, Vc, O, ws, H
         torch.cuda.empty_cache()
         line["decode_c5"] = decode_step(wm, torch, np, synth, hip, dev, stream, log)
+    if not args.no_backward and w.dtype == "bf16" and w.d in (64, 96) and w.T_new > 4 \
+            and w.ctx == 0:
+        torch.cuda.empty_cache()
+        line["attention_backward"] = attend_backward_bench(wm, torch, np, synth, hip, dev,
+                                                           stream, log, w)
     if not args.no_passes:
         torch.cuda.empty_cache()
         line["prefill_passes"] = passes_bench(wm, torch, np, synth, hip, dev, stream, log,

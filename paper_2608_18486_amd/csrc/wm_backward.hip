@@ -14,7 +14,7 @@
 //                          and KV head and walks every query that reads them (all
 //                          consumers of the channel, all grouped query heads), so each
 //                          slot's dk and dv are summed in registers and written once.
-//   attend_bwd_dummy_kernel  the dummy's dk, dv: a sum over every row of its readers.
+//   attend_bwd_dummy_*     the dummy's dk, dv: a sum over every row of its readers.
 // Products run on the matrix cores in bf16 (P and dS rounded to bf16 as operands), sums
 // in fp32; gradients leave in fp32.
 #include "wm_device.hpp"
@@ -38,17 +38,24 @@ constexpr int kBwdThreads = 256;
 
 __device__ __forceinline__ float bwd_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Copies rows row0 .. row0 + ROWS - 1 (DH bf16 each, row_bytes apart in the view) into an
-// LDS block with the fragment readers' chunk swizzle; rows at or past nvalid read zeros.
+// Copies rows row0 .. row0 + ROWS - 1 (DH bf16 each, row_bytes apart in the view) into the
+// LDS block at lds_base with LDS DMA, in the fragment readers' chunk swizzle: wave w's
+// n-th instruction fills LDS chunks 64 (NI w + n) + lane, and each lane fetches the chunk
+// the swizzle puts there. Rows at or past nvalid arrive as zeros. Every wave issues NI
+// copies; the caller waits for them (vmcnt) before the barrier that publishes the block.
 template <int DH, int ROWS>
-__device__ __forceinline__ void bwd_stage(char* dst, __amdgpu_buffer_rsrc_t view,
-                                          uint32_t row_bytes, int row0, int nvalid, int tid) {
-  constexpr int CPR = DH * 2 / 16;
+__device__ __forceinline__ void bwd_dma(uint32_t lds_base, __amdgpu_buffer_rsrc_t view,
+                                        uint32_t row_bytes, int row0, int nvalid, int w,
+                                        int lane) {
+  constexpr int CPR = DH * 2 / 16, NI = ROWS * CPR / 256;
+  static_assert(NI * 256 == ROWS * CPR, "whole instructions per wave");
 #pragma unroll
-  for (int ch = tid; ch < ROWS * CPR; ch += kBwdThreads) {
-    const int r = ch / CPR, c = ch - r * CPR, gr = row0 + r;
-    const uint32_t off = gr < nvalid ? (uint32_t)gr * row_bytes + 16u * c : kOffOob;
-    *(i32x4*)(dst + r * 2 * DH + 16 * (c ^ pf_swz<DH>(r))) = buf_ld16(view, off);
+  for (int n = 0; n < NI; ++n) {
+    const int pos = (NI * w + n) * 64 + lane, row = pos / CPR, cc = pos - row * CPR;
+    const int gr = row0 + row;
+    const uint32_t off = gr < nvalid ? (uint32_t)gr * row_bytes + 16u * (uint32_t)(cc ^ pf_swz<DH>(row))
+                                     : kOffOob;
+    lds_dma16(__builtin_amdgcn_readfirstlane(lds_base + (NI * w + n) * 1024), off, view);
   }
 }
 
@@ -64,7 +71,9 @@ __device__ __forceinline__ bf16x4 bwd_ld8(__amdgpu_buffer_rsrc_t r, uint32_t off
 template <int DH>
 __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
   constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, BLK = 64;
-  __shared__ __align__(16) char smem[2 * BLK * ROW];  // K block, then V block
+  // two buffers, each a K block then a V block (pass 1 uses the K blocks only)
+  __shared__ __align__(16) char smem[4 * BLK * ROW];
+  const uint32_t lbase = (uint32_t)(uintptr_t)smem;
   const int tile = blockIdx.x;
   const int qtile = a.n_qtiles - 1 - tile % a.n_qtiles;
   int y = tile / a.n_qtiles;
@@ -133,16 +142,21 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
   // two lanes of a row share the running maximum and keep partial sums
   float m = a.mask_paper ? sd : kNegBig;
   float sum = a.mask_paper && h == 0 ? 1.f : 0.f;
+  // blocks are double-buffered: block j + 1 is copied while block j is multiplied
+  if (nblk > 0) bwd_dma<DH, BLK>(lbase, kv, ROW, 0, kend, w, lane);
   for (int j = 0; j < nblk; ++j) {
-    bwd_stage<DH, BLK>(smem, kv, ROW, j * BLK, kend, tid);
-    __syncthreads();
+    const uint32_t kb = (uint32_t)(j & 1) * 2 * BLK * ROW;
+    wait_vmcnt<0>();
+    __syncthreads();  // block j is in LDS; every wave is done with block j - 1
+    if (j + 1 < nblk) bwd_dma<DH, BLK>(lbase + (kb ^ (2 * BLK * ROW)), kv, ROW, (j + 1) * BLK, kend, w, lane);
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const int s0 = j * BLK + 32 * hf;
       if (s0 < wkend) {
         f32x16 sc = zero16();
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) sc = mma32(sc, pf_ldk<DH>(smem, lo, hf * 32 * ROW, ks), qf[ks]);
+        for (int ks = 0; ks < NKS; ++ks)
+          sc = mma32(sc, pf_ldk<DH>(smem, lo, kb + hf * 32 * ROW, ks), qf[ks]);
         float mx = kNegBig;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
@@ -158,18 +172,27 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
         m = mn;
       }
     }
-    __syncthreads();
   }
+  __syncthreads();  // pass 2 reuses the buffers
   const float lse = m + __log2f(halves_sum(sum));
 
   // pass 2: dS and dq^T += K^T dS^T
   f32x16 dq[NDT];
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) dq[dt] = zero16();
+  if (nblk > 0) {
+    bwd_dma<DH, BLK>(lbase, kv, ROW, 0, kend, w, lane);
+    bwd_dma<DH, BLK>(lbase + BLK * ROW, vv, ROW, 0, kend, w, lane);
+  }
   for (int j = 0; j < nblk; ++j) {
-    bwd_stage<DH, BLK>(smem, kv, ROW, j * BLK, kend, tid);
-    bwd_stage<DH, BLK>(smem + BLK * ROW, vv, ROW, j * BLK, kend, tid);
+    const uint32_t kb = (uint32_t)(j & 1) * 2 * BLK * ROW;
+    wait_vmcnt<0>();
     __syncthreads();
+    if (j + 1 < nblk) {
+      const uint32_t nb = lbase + (kb ^ (2 * BLK * ROW));
+      bwd_dma<DH, BLK>(nb, kv, ROW, (j + 1) * BLK, kend, w, lane);
+      bwd_dma<DH, BLK>(nb + BLK * ROW, vv, ROW, (j + 1) * BLK, kend, w, lane);
+    }
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const int s0 = j * BLK + 32 * hf;
@@ -177,8 +200,8 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
         f32x16 sc = zero16(), dp = zero16();
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-          sc = mma32(sc, pf_ldk<DH>(smem, lo, hf * 32 * ROW, ks), qf[ks]);
-          dp = mma32(dp, pf_ldk<DH>(smem, lo, BLK * ROW + hf * 32 * ROW, ks), df[ks]);
+          sc = mma32(sc, pf_ldk<DH>(smem, lo, kb + hf * 32 * ROW, ks), qf[ks]);
+          dp = mma32(dp, pf_ldk<DH>(smem, lo, kb + BLK * ROW + hf * 32 * ROW, ks), df[ks]);
         }
         bf16x8 ds[2];
 #pragma unroll
@@ -191,10 +214,9 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
           for (int kh = 0; kh < 2; ++kh)
-            dq[dt] = mma32(dq[dt], pf_ldv<DH>(smem, lo, hf * 32 * ROW, kh, dt), ds[kh]);
+            dq[dt] = mma32(dq[dt], pf_ldv<DH>(smem, lo, kb + hf * 32 * ROW, kh, dt), ds[kh]);
       }
     }
-    __syncthreads();
   }
 
   // the dummy's term, then dq / sqrt(d) out
@@ -224,15 +246,20 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
 
 // ------------------------------------------------------------------- dk, dv
 // Tile: 128 slots of one (channel, sequence, KV head), 32 per wave; the wave's K and V
-// rows stay in registers as the column operand. For each 32-row query block (staged in
-// LDS with its LSE and D): S = Q K^T and dP = dO V^T put one slot in a lane, and
-// dv^T += dO^T P and dk^T += Q^T dS take P and dS from those registers through the
-// transposing reads of the dO and Q blocks.
+// rows stay in registers as the column operand. The tile walks every query block of 64
+// rows that may read its slots, for every consumer of the channel and every query head of
+// the KV head, as one flat sequence, so the next block (queries and dO by LDS DMA, the
+// rows' LSE and D through registers) is fetched while the current one is multiplied. For
+// each 32-row half: S = Q K^T and dP = dO V^T put one slot in a lane, and dv^T += dO^T P
+// and dk^T += Q^T dS take P and dS from those registers through the transposing reads
+// of the dO and Q blocks.
 template <int DH>
 __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) {
-  constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, QB = 32;
-  __shared__ __align__(16) char smem[2 * QB * ROW];  // Q block, then dO block
-  __shared__ __align__(16) float s_lse[QB], s_dlt[QB];
+  constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, QB = 64;
+  constexpr uint32_t BUF = 2 * QB * ROW;  // one buffer: a Q block, then a dO block
+  __shared__ __align__(16) char smem[2 * BUF];
+  __shared__ __align__(16) float s_lse[2][QB], s_dlt[2][QB];
+  const uint32_t lbase = (uint32_t)(uintptr_t)smem;
   const int tile = blockIdx.x;
   const int stile = tile % a.n_stiles;
   int y = tile / a.n_stiles;
@@ -269,57 +296,83 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) 
   const PfLane<DH> lo = pf_lane<DH>(lane);
   // the first query that sees slot sbase sits at position sbase + 1 - incl
   const int i_first = max(0, sbase + 1 - incl - pos0);
+  const int qb0 = i_first / QB, nqb = (a.T + QB - 1) / QB - qb0;
+  const int nmem = a.grp.offsets[c + 1] - a.grp.offsets[c];
+  const int nit = nqb > 0 ? nmem * G * nqb : 0;
   const uint32_t ostride = (uint32_t)a.Hq * DH * 2u;
 
-  for (int mi = a.grp.offsets[c]; mi < a.grp.offsets[c + 1]; ++mi) {
-    const int l = a.grp.members[mi];
-    for (int hg = 0; hg < G; ++hg) {
-      const int hq = kvh * G + hg;
-      const long rows0 = (((long)l * a.B + b) * a.Hq + hq) * a.T;  // (l, b, hq, 0) in [L][B][Hq][T]
-      const long rowl = ((long)l * a.B + b) * a.T;                 // (l, b, 0) in [L][B][T][Hq d]
-      const auto qv = make_view(a.Q + rows0 * DH, (uint32_t)a.T * DH * 2u);
-      const auto dov = make_view(a.dO + rowl * a.Hq * DH + (long)hq * DH, (uint32_t)a.T * ostride);
-      for (int qb = i_first / QB; qb * QB < a.T; ++qb) {
-        bwd_stage<DH, QB>(smem, qv, DH * 2u, qb * QB, a.T, tid);
-        bwd_stage<DH, QB>(smem + QB * ROW, dov, ostride, qb * QB, a.T, tid);
-        if (tid < QB) {
-          const int qr = qb * QB + tid;
-          s_lse[tid] = qr < a.T ? a.lse[rows0 + qr] : 1.0e30f;  // a row past T weighs 0
-          s_dlt[tid] = qr < a.T ? a.dlt[rows0 + qr] : 0.f;
+  // iteration it -> (consumer, query head, query block)
+  auto where = [&](int it, int& l, int& hq, int& qb) {
+    qb = qb0 + it % nqb;
+    const int x = it / nqb;
+    hq = kvh * G + x % G;
+    l = a.grp.members[a.grp.offsets[c] + x / G];
+  };
+  float lse_n = 0.f, dlt_n = 0.f;  // the next block's row statistics (threads < QB)
+  auto fetch = [&](int it, uint32_t buf) {
+    int l, hq, qb;
+    where(it, l, hq, qb);
+    const long rows0 = (((long)l * a.B + b) * a.Hq + hq) * a.T;
+    const long rowl = ((long)l * a.B + b) * a.T;
+    const auto qv = make_view(a.Q + rows0 * DH, (uint32_t)a.T * DH * 2u);
+    const auto dov = make_view(a.dO + rowl * a.Hq * DH + (long)hq * DH, (uint32_t)a.T * ostride);
+    bwd_dma<DH, QB>(buf, qv, DH * 2u, qb * QB, a.T, w, lane);
+    bwd_dma<DH, QB>(buf + QB * ROW, dov, ostride, qb * QB, a.T, w, lane);
+    if (tid < QB) {
+      const int qr = qb * QB + tid;
+      lse_n = qr < a.T ? a.lse[rows0 + qr] : 1.0e30f;  // a row past T weighs 0
+      dlt_n = qr < a.T ? a.dlt[rows0 + qr] : 0.f;
+    }
+  };
+  if (nit > 0) fetch(0, lbase);
+  for (int it = 0; it < nit; ++it) {
+    const int u = it & 1;
+    const uint32_t kb = (uint32_t)u * BUF;
+    if (tid < QB) {
+      s_lse[u][tid] = lse_n;
+      s_dlt[u][tid] = dlt_n;
+    }
+    wait_vmcnt<0>();
+    __syncthreads();  // block it is in LDS; every wave is done with block it - 1
+    int l, hq, qb;
+    where(it, l, hq, qb);
+    (void)l;
+    (void)hq;
+    if (it + 1 < nit) fetch(it + 1, lbase + (kb ^ BUF));
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int q0 = qb * QB + 32 * hf;
+      // the half's last row (position pos0 + q0 + 31) sees slots below that + incl: skip
+      // the half when the wave's first slot is not among them, or when it is past T
+      if (q0 < a.T && pos0 + min(q0 + 31, a.T - 1) + incl > ws0) {
+        const uint32_t qo = kb + hf * 32 * ROW, doo = kb + QB * ROW + hf * 32 * ROW;
+        f32x16 sc = zero16(), dp = zero16();
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+          sc = mma32(sc, pf_ldk<DH>(smem, lo, qo, ks), kf[ks]);
+          dp = mma32(dp, pf_ldk<DH>(smem, lo, doo, ks), vf[ks]);
         }
-        __syncthreads();
-        // the block's last row, at position pos0 + qb QB + QB - 1, sees slots below
-        // that + incl: skip when the wave's first slot is not among them
-        if (pos0 + min(qb * QB + QB - 1, a.T - 1) + incl > ws0) {
-          f32x16 sc = zero16(), dp = zero16();
+        // lane (h, r): slot r of the wave, query rows 8 (i / 4) + 4 h + i % 4 of the half
+        bf16x8 pp[2], pds[2];
 #pragma unroll
-          for (int ks = 0; ks < NKS; ++ks) {
-            sc = mma32(sc, pf_ldk<DH>(smem, lo, 0, ks), kf[ks]);
-            dp = mma32(dp, pf_ldk<DH>(smem, lo, QB * ROW, ks), vf[ks]);
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 lz = *(const f32x4*)(&s_lse[u][32 * hf + 8 * g + 4 * h]);
+          const f32x4 dz = *(const f32x4*)(&s_dlt[u][32 * hf + 8 * g + 4 * h]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int i = 4 * g + e, qr = q0 + 8 * g + 4 * h + e;
+            const float p = slot < pos0 + qr + incl ? bwd_exp2(sc[i] * cl2 - lz[e]) : 0.f;
+            pp[i >> 3][i & 7] = (bf16)p;
+            pds[i >> 3][i & 7] = (bf16)(p * (dp[i] - dz[e]));
           }
-          // lane (h, r): slot r of the wave, query rows 8 (i / 4) + 4 h + i % 4 of the block
-          bf16x8 pp[2], pds[2];
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 lz = *(const f32x4*)(s_lse + 8 * g + 4 * h);
-            const f32x4 dz = *(const f32x4*)(s_dlt + 8 * g + 4 * h);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int i = 4 * g + e, qr = qb * QB + 8 * g + 4 * h + e;
-              const float p = slot < pos0 + qr + incl ? bwd_exp2(sc[i] * cl2 - lz[e]) : 0.f;
-              pp[i >> 3][i & 7] = (bf16)p;
-              pds[i >> 3][i & 7] = (bf16)(p * (dp[i] - dz[e]));
-            }
-          }
-#pragma unroll
-          for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int kh = 0; kh < 2; ++kh) {
-              dv[dt] = mma32(dv[dt], pf_ldv<DH>(smem, lo, QB * ROW, kh, dt), pp[kh]);
-              dk[dt] = mma32(dk[dt], pf_ldv<DH>(smem, lo, 0, kh, dt), pds[kh]);
-            }
         }
-        __syncthreads();
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+          for (int kh = 0; kh < 2; ++kh) {
+            dv[dt] = mma32(dv[dt], pf_ldv<DH>(smem, lo, doo, kh, dt), pp[kh]);
+            dk[dt] = mma32(dk[dt], pf_ldv<DH>(smem, lo, qo, kh, dt), pds[kh]);
+          }
       }
     }
   }
@@ -343,43 +396,59 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) 
 }
 
 // -------------------------------------------------------------------- dummy
-// One workgroup per (channel, KV head), 4 DH threads: thread (rl, e) sums column e over
-// every fourth row of the channel's readers, then the four partial sums are added.
+// The dummy's gradients sum over every row that reads its channel and KV head: the rows
+// (consumer, query head, sequence, position) are split into kDummyChunks contiguous
+// chunks, one workgroup of 4 DH threads each (thread (rl, e) sums column e over every
+// fourth row of the chunk), and a second kernel adds the chunks in order.
+constexpr int kDummyChunks = 32;
+
 template <int DH>
-__global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_kernel(BwdArgs a) {
+__global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_part_kernel(BwdArgs a, float* part) {
   __shared__ float s_v[4 * DH], s_k[4 * DH];
-  const int c = blockIdx.x / a.Hkv, kvh = blockIdx.x % a.Hkv;
+  const int ck = blockIdx.x / kDummyChunks, chunk = blockIdx.x % kDummyChunks;
+  const int c = ck / a.Hkv, kvh = ck % a.Hkv;
   const int tid = threadIdx.x, e = tid % DH, rl = tid / DH;
   const int G = a.Hq / a.Hkv;
+  const long per_b = a.T, per_h = (long)a.B * per_b, per_m = G * per_h;
+  const long nrow = (long)(a.grp.offsets[c + 1] - a.grp.offsets[c]) * per_m;
+  const long r0 = nrow * chunk / kDummyChunks, r1 = nrow * (chunk + 1) / kDummyChunks;
   float av = 0.f, ak = 0.f;
   if (a.mask_paper) {
-    for (int mi = a.grp.offsets[c]; mi < a.grp.offsets[c + 1]; ++mi) {
-      const int l = a.grp.members[mi];
-      for (int hg = 0; hg < G; ++hg) {
-        const int hq = kvh * G + hg;
-        for (int b = 0; b < a.B; ++b) {
-          const long rows0 = (((long)l * a.B + b) * a.Hq + hq) * a.T;
-          const long rowl = ((long)l * a.B + b) * a.T;
-          for (int i = rl; i < a.T; i += 4) {
-            av += a.pd[rows0 + i] * (float)a.dO[(rowl + i) * a.Hq * DH + (long)hq * DH + e];
-            ak += a.dsd[rows0 + i] * (float)a.Q[(rows0 + i) * DH + e];
-          }
-        }
-      }
+    for (long rr = r0 + rl; rr < r1; rr += 4) {
+      const int mi = (int)(rr / per_m), hg = (int)(rr / per_h % G), b = (int)(rr / per_b % a.B);
+      const int i = (int)(rr % per_b);
+      const int l = a.grp.members[a.grp.offsets[c] + mi], hq = kvh * G + hg;
+      const long row = (((long)l * a.B + b) * a.Hq + hq) * a.T + i;
+      av += a.pd[row] * (float)a.dO[(((long)l * a.B + b) * a.T + i) * a.Hq * DH + (long)hq * DH + e];
+      ak += a.dsd[row] * (float)a.Q[row * DH + e];
     }
   }
   s_v[tid] = av;
   s_k[tid] = ak;
   __syncthreads();
   if (rl == 0) {
-    const long o = ((long)c * a.Hkv + kvh) * DH + e;
-    a.dVd[o] = (s_v[e] + s_v[DH + e]) + (s_v[2 * DH + e] + s_v[3 * DH + e]);
-    a.dKd[o] = ((s_k[e] + s_k[DH + e]) + (s_k[2 * DH + e] + s_k[3 * DH + e])) * a.scale;
+    float* o = part + (long)blockIdx.x * 2 * DH;
+    o[e] = (s_v[e] + s_v[DH + e]) + (s_v[2 * DH + e] + s_v[3 * DH + e]);
+    o[DH + e] = (s_k[e] + s_k[DH + e]) + (s_k[2 * DH + e] + s_k[3 * DH + e]);
   }
 }
 
+template <int DH>
+__global__ __launch_bounds__(DH) void attend_bwd_dummy_sum_kernel(BwdArgs a, const float* part) {
+  const int ck = blockIdx.x, e = threadIdx.x;
+  float v = 0.f, k = 0.f;
+  for (int ch = 0; ch < kDummyChunks; ++ch) {
+    const float* p = part + ((long)ck * kDummyChunks + ch) * 2 * DH;
+    v += p[e];
+    k += p[DH + e];
+  }
+  a.dVd[(long)ck * DH + e] = v;
+  a.dKd[(long)ck * DH + e] = k * a.scale;
+}
+
 size_t attend_backward_rows_bytes(const Shape& sh) {
-  return 4ul * sh.L * sh.B * sh.Hq * sh.T_new * sizeof(float);
+  return (4ul * sh.L * sh.B * sh.Hq * sh.T_new + 2ul * sh.k * sh.Hkv * kDummyChunks * sh.d) *
+         sizeof(float);
 }
 
 void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
@@ -395,15 +464,18 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
             (int)(((long)sh.ctx_max + sh.T_new + 127) / 128), kLog2e / sqrtf((float)sh.d),
             1.0f / sqrtf((float)sh.d), chan_map, groups};
   const dim3 ga(a.n_qtiles * sh.Hq * sh.B * sh.L), gb(a.n_stiles * sh.Hkv * sh.B * sh.k),
-      gc(sh.k * sh.Hkv);
+      gp(sh.k * sh.Hkv * kDummyChunks), gs(sh.k * sh.Hkv);
+  float* part = rows + 4 * nrow;
   if (sh.d == 64) {
     hipLaunchKernelGGL(attend_bwd_dq_kernel<64>, ga, dim3(kBwdThreads), 0, s, a);
     hipLaunchKernelGGL(attend_bwd_dkv_kernel<64>, gb, dim3(kBwdThreads), 0, s, a);
-    hipLaunchKernelGGL(attend_bwd_dummy_kernel<64>, gc, dim3(4 * 64), 0, s, a);
+    hipLaunchKernelGGL(attend_bwd_dummy_part_kernel<64>, gp, dim3(4 * 64), 0, s, a, part);
+    hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<64>, gs, dim3(64), 0, s, a, (const float*)part);
   } else {
     hipLaunchKernelGGL(attend_bwd_dq_kernel<96>, ga, dim3(kBwdThreads), 0, s, a);
     hipLaunchKernelGGL(attend_bwd_dkv_kernel<96>, gb, dim3(kBwdThreads), 0, s, a);
-    hipLaunchKernelGGL(attend_bwd_dummy_kernel<96>, gc, dim3(4 * 96), 0, s, a);
+    hipLaunchKernelGGL(attend_bwd_dummy_part_kernel<96>, gp, dim3(4 * 96), 0, s, a, part);
+    hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<96>, gs, dim3(96), 0, s, a, (const float*)part);
   }
 }
 

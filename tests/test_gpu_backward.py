@@ -81,3 +81,80 @@ def test_channel_attend_backward_is_deterministic(wm):
         outs.append(r)
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+def _sub_dims(w, L, Hq, mask_mode):
+    return oracle.Dims(B=1, T_new=w.T_new, L=L, k=1, D=w.D, Hq=Hq, Hkv=1, d=w.d, p=1,
+                       S_cap=w.T_new, mask_mode=mask_mode)
+
+
+@pytest.mark.parametrize("name", ["c4_T4096_L24_k12", "paper_T2048_L16_k8"])
+def test_channel_attend_backward_at_full_size(wm, name):
+    """The full-size pass's attention gradients in the launch configuration a training step
+    uses (the forward's output O from the GPU forward, persistent grids): sampled query rows'
+    dQ, sampled channel slices' dK and dV (every reader of the slice), and one dummy's dK,
+    dV, each against the oracle on the sub-problem that determines it."""
+    w = synth.WORKLOADS[name]
+    print("attention backward full size %s" % name, flush=True)
+    G, c_of = w.Hq // w.Hkv, w.chan_map
+    P = synth.make_params(w, _bias(w))
+    Q = synth.make_queries(w)
+    shape = (w.k, w.B, w.Hkv, w.T_new, w.d)
+    Kc = synth._normal(shape, 1.0, 9001, torch.bfloat16)
+    Vc = synth._normal(shape, 1.0, 9002, torch.bfloat16)
+    dO = synth._normal((w.L, w.B, w.T_new, w.Hq * w.d), 1.0, 9003, torch.bfloat16)
+    dims = _gdims(wm, w, S_cap=w.T_new, ctx_max=0)
+    Pd, Qd, Kd_, Vd_ = _dev(P), Q.cuda(), Kc.cuda(), Vc.cuda()
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=torch.bfloat16, device="cuda")
+    wm.channel_attend(dims, Pd, Qd, w.chan_map, None, Kd_, Vd_, O)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    dQ, dKc, dVc = torch.empty(tuple(Q.shape), **f32), torch.empty(shape, **f32), \
+        torch.empty(shape, **f32)
+    dKd, dVd = torch.empty(tuple(P["Kd"].shape), **f32), torch.empty(tuple(P["Vd"].shape), **f32)
+    wm.channel_attend_backward(dims, Pd, Qd, w.chan_map, None, Kd_, Vd_, O, dO.cuda(), dQ, dKc,
+                               dVc, dKd, dVd)
+    torch.cuda.synchronize()
+    del O, Pd, Qd, Kd_, Vd_
+    dQ, dKc, dVc, dKd, dVd = (t.cpu() for t in (dQ, dKc, dVc, dKd, dVd))
+
+    def sub_params(c, kvh):
+        return {**{n: P[n] for n in oracle.PARAM_NAMES},
+                "Kd": P["Kd"][c, kvh].reshape(1, 1, w.d), "Vd": P["Vd"][c, kvh].reshape(1, 1, w.d)}
+
+    # dQ of sampled (consumer, sequence, query head) rows: the sub-problem of that row set
+    for l, b, hq in ((0, 0, 0), (w.L - 1, w.B - 1, w.Hq - 1), (w.L // 2, 1, w.Hq // 2)):
+        c, kvh = c_of[l], hq // G
+        g = ob.channel_attend_grads(_sub_dims(w, 1, 1, 0), sub_params(c, kvh),
+                                    Q[l, b, hq].reshape(1, 1, 1, w.T_new, w.d), [0], None,
+                                    _f64(Kc[c, b, kvh]).reshape(1, 1, 1, w.T_new, w.d),
+                                    _f64(Vc[c, b, kvh]).reshape(1, 1, 1, w.T_new, w.d),
+                                    _f64(dO[l, b, :, hq * w.d:(hq + 1) * w.d]).reshape(
+                                        1, 1, w.T_new, w.d))
+        check_close(dQ[l, b, hq], g["dQ"][0, 0, 0], "bf16", "%s dQ l%d b%d h%d" % (name, l, b, hq))
+
+    # dK, dV of sampled channel slices: every consumer of the channel, every grouped head
+    def slice_grads(c, b, kvh):
+        ls = [l for l in range(w.L) if c_of[l] == c]
+        hs = list(range(kvh * G, (kvh + 1) * G))
+        Qs = Q[ls][:, b, hs].reshape(len(ls), 1, G, w.T_new, w.d)
+        dOs = dO[ls][:, b].reshape(len(ls), w.T_new, w.Hq, w.d)[:, :, hs].reshape(
+            len(ls), 1, w.T_new, G * w.d)
+        return ob.channel_attend_grads(_sub_dims(w, len(ls), G, 0), sub_params(c, kvh), Qs,
+                                       [0] * len(ls), None,
+                                       _f64(Kc[c, b, kvh]).reshape(1, 1, 1, w.T_new, w.d),
+                                       _f64(Vc[c, b, kvh]).reshape(1, 1, 1, w.T_new, w.d),
+                                       _f64(dOs))
+
+    for c, b, kvh in ((0, 0, 0), (w.k - 1, w.B - 1, w.Hkv - 1)):
+        g = slice_grads(c, b, kvh)
+        check_close(dKc[c, b, kvh], g["dKc"][0, 0, 0], "bf16", "%s dK c%d b%d" % (name, c, b))
+        check_close(dVc[c, b, kvh], g["dVc"][0, 0, 0], "bf16", "%s dV c%d b%d" % (name, c, b))
+    # the dummy of channel 1, KV head 0: its readers in every sequence
+    kd = np.zeros(w.d)
+    vd = np.zeros(w.d)
+    for b in range(w.B):
+        g = slice_grads(1, b, 0)
+        kd += g["dKd"][0, 0]
+        vd += g["dVd"][0, 0]
+    check_close(dKd[1, 0], kd, "bf16", "%s dKd" % name)
+    check_close(dVd[1, 0], vd, "bf16", "%s dVd" % name)
