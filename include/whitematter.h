@@ -87,7 +87,10 @@ enum wm_op {
   WM_OP_LAYER_ATTEND = 6,  /* wm_layer_attend */
   WM_OP_PASSES = 7,        /* wm_prefill_passes */
   WM_OP_DENSE_ATTEND = 8,  /* wm_channel_attend_dense */
-  WM_OP_ATTEND_BACKWARD = 9 /* wm_channel_attend_backward */
+  WM_OP_ATTEND_BACKWARD = 9, /* wm_channel_attend_backward */
+  WM_OP_Q_BACKWARD = 10,      /* wm_q_project_backward */
+  WM_OP_POOL_BACKWARD = 11,   /* wm_pool_backward */
+  WM_OP_STEP_BACKWARD = 12    /* wm_layer_step_backward */
 };
 
 /* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
@@ -136,6 +139,15 @@ typedef struct wm_params {
   const void *Wq;      /* [L][Hq*d][D]     consumer query projections */
   const void *g_qnorm; /* [L][d]           consumer q-norm gains (shared by query heads) */
 } wm_params;
+
+/* Gradients of the parameters, device fp32 pointers in the shapes and layouts of the
+ * wm_params entries of the same names (4-byte aligned). The backward entry points ADD
+ * their contribution, so that the gradient passes of a training step (Section 3.3) sum
+ * into one set: zero the buffers before the first call. Each entry point names the
+ * entries it uses; the others may be NULL. */
+typedef struct wm_grads {
+  float *g_pre, *W_alpha, *b_alpha, *g_mid, *Wk, *Wv, *g_knorm, *Kd, *Vd, *g_in, *Wq, *g_qnorm;
+} wm_grads;
 
 /* Section 3.1 Step 1 (mix L states into k channels), both branches.
  *   H         device [B][T_new][L][D] in dtype: state entering each layer
@@ -243,6 +255,65 @@ int wm_channel_attend_backward(const wm_dims *dims, const wm_params *params, con
                                const void *Vc, const void *O, const void *dO, float *dQ,
                                float *dKc, float *dVc, float *dKd, float *dVd, void *ws,
                                size_t ws_bytes, wm_stream_t stream);
+
+/* Gradients of the consumer queries (wm_q_project) for a loss gradient dQ in the
+ * queries: back through RoPE (the transposed rotation), the q norm, W^Q_l and the input
+ * norm, with the forward's intermediate values recomputed from H.
+ * bf16, head dims 64 and 96, contiguous tokens (dims.groups <= 1), D <= 4608.
+ *   H        device [B][T_new][L][D] bf16, ctx_len device int32 [B] or NULL: as the forward
+ *   dQ       device float [L][B][Hq][T_new][d]
+ *   dH       device float [B][T_new][L][D]: the gradient in H is ADDED
+ *   grads    g_in, Wq, g_qnorm: ADDED
+ * Workspace: wm_workspace_size(dims, WM_OP_Q_BACKWARD). Errors as wm_q_project, plus
+ * WM_ERR_DTYPE for fp32 and WM_ERR_SHAPE / WM_ERR_ARG for what the gradients do not support
+ * or a NULL gradient pointer. */
+int wm_q_project_backward(const wm_dims *dims, const wm_params *params, const void *H,
+                          const int32_t *ctx_len, const float *dQ, float *dH,
+                          const wm_grads *grads, void *ws, size_t ws_bytes, wm_stream_t stream);
+
+/* Gradients of the pool (wm_pool, Section 3.1 Steps 1-2) for loss gradients in the cache
+ * rows the call wrote: back through RoPE and the key norm (key branch), W^K_j / W^V_j, the
+ * mid norm, the mix (dh_l gets sum_j alpha_jl dh~_j; the weights' gradient dh~_j . h_l goes
+ * through the softmax over depth, or the no-feedback mask, to the router's logits), the
+ * router (W_alpha, b_alpha) and the pre-mix norm. The router, mix and norms of the forward
+ * are recomputed from H with the forward's kernels.
+ * bf16, head dims 64 and 96, contiguous tokens, D <= 4608; every router mode and mix mode.
+ *   H, ctx_len  as wm_pool
+ *   dKc, dVc device float [k][B][Hkv][S_cap][d]: slot ctx_len[b] + i of every (channel,
+ *            sequence, KV head) is read (the call's new rows); no other slot is read
+ *   dH       device float [B][T_new][L][D]: ADDED
+ *   grads    g_pre, W_alpha (not with WM_ROUTER_STATIC), b_alpha, g_mid, Wk, Wv, g_knorm:
+ *            ADDED. Without feedback the router entries a channel never reads get nothing.
+ * Workspace: wm_workspace_size(dims, WM_OP_POOL_BACKWARD). Errors as wm_q_project_backward. */
+int wm_pool_backward(const wm_dims *dims, const wm_params *params, const void *H,
+                     const int32_t *ctx_len, const float *dKc, const float *dVc, float *dH,
+                     const wm_grads *grads, void *ws, size_t ws_bytes, wm_stream_t stream);
+
+/* Gradients of the fused step (wm_layer_step) for a loss gradient dO in its output and,
+ * optionally, gradients already reaching its cache rows: the step's backward that training
+ * runs in each gradient-carrying pass (Section 3.3). Recomputes the queries, then runs
+ * wm_channel_attend_backward (its slot and dummy gradients ADDED into dKc, dVc and
+ * grads->Kd, grads->Vd), wm_q_project_backward and wm_pool_backward on the new slots'
+ * total gradient.
+ *   H, chan_map, ctx_len  as wm_layer_step
+ *   Kc, Vc   device [k][B][Hkv][S_cap][d] bf16: the caches as the forward step left them
+ *   O        device [L][B][T_new][Hq*d] bf16: the forward step's output
+ *   dO       device [L][B][T_new][Hq*d] bf16
+ *   dKc, dVc device float [k][B][Hkv][S_cap][d], 16-byte aligned, in/out: on entry the
+ *            gradient that reaches the caches from elsewhere (zero if none); the attention's
+ *            gradient is added to slots below ctx_len[b] + T_new, and the new slots' total
+ *            is what the pool's backward receives. On return the context slots (below
+ *            ctx_len[b]) hold the gradient for the step that wrote them.
+ *   dH       device float [B][T_new][L][D]: ADDED
+ *   grads    every entry (Kd, Vd only with WM_MASK_PAPER; W_alpha not with static
+ *            weights): ADDED
+ * Workspace: wm_workspace_size(dims, WM_OP_STEP_BACKWARD). Errors as
+ * wm_channel_attend_backward and wm_pool_backward. */
+int wm_layer_step_backward(const wm_dims *dims, const wm_params *params, const void *H,
+                           const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
+                           const void *Vc, const void *O, const void *dO, float *dKc,
+                           float *dVc, float *dH, const wm_grads *grads, void *ws,
+                           size_t ws_bytes, wm_stream_t stream);
 
 /* wm_channel_attend for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument. Its only

@@ -225,3 +225,47 @@ def layer_step_grads(dims: Dims, params, H, chan_map, dO, ctx_len=None, Kc=None,
     if have_ctx:
         out["dKc_ctx"], out["dVc_ctx"] = g[-2].numpy(), g[-1].numpy()
     return out
+
+
+POOL_PARAMS = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm")
+QUERY_PARAMS = ("g_in", "Wq", "g_qnorm")
+
+
+def pool_grads(dims: Dims, params, H, dK, dV, ctx_len=None) -> dict:
+    """Gradients of <dK, K_new> + <dV, V_new> through the pool of the call's tokens (Steps
+    1-2): dK, dV in the new rows' layout [k, B, Hkv, T, d]. Returns dH [B, T, L, D] and
+    d + name for the pool's parameters."""
+    P = _params(params, True)
+    ctx = _ctx(dims, ctx_len)
+    Ht = _t(H, True)
+    Kn, Vn = pool(dims, P, Ht, ctx)
+    loss = (Kn * _t(dK)).sum() + (Vn * _t(dV)).sum()
+    leaves = [Ht] + [P[n] for n in POOL_PARAMS]
+    g = torch.autograd.grad(loss, leaves, allow_unused=True)
+    out = {"dH": g[0].numpy()}
+    for n, x in zip(POOL_PARAMS, g[1:]):
+        out["d" + n] = (x if x is not None else torch.zeros_like(P[n])).numpy()
+    return out
+
+
+def q_project_grads(dims: Dims, params, H, dQ, ctx_len=None) -> dict:
+    """Gradients of <dQ, Q> through the consumer queries (input norm, W^Q, q norm, RoPE):
+    dQ [L, B, Hq, T, d]. Returns dH and d + name for g_in, Wq, g_qnorm."""
+    P = _params(params, True)
+    ctx = _ctx(dims, ctx_len)
+    Ht = _t(H, True)
+    loss = (queries(dims, P, Ht, ctx) * _t(dQ)).sum()
+    leaves = [Ht] + [P[n] for n in QUERY_PARAMS]
+    g = torch.autograd.grad(loss, leaves)
+    out = {"dH": g[0].numpy()}
+    for n, x in zip(QUERY_PARAMS, g[1:]):
+        out["d" + n] = x.numpy()
+    return out
+
+
+def new_rows(dims: Dims, cache, ctx_len=None):
+    """The call's new rows [k, B, Hkv, T, d] of a cache-layout array (slots ctx_len[b] + i)."""
+    ctx = np.zeros(dims.B, dtype=np.int64) if ctx_len is None else np.asarray(ctx_len)
+    c = np.asarray(cache)
+    return np.stack([c[:, b, :, int(ctx[b]):int(ctx[b]) + dims.T_new] for b in range(dims.B)],
+                    axis=1)

@@ -24,7 +24,8 @@ MIX_LINEAR, MIX_SOFTMAX = 0, 1
 MASK_PAPER, MASK_INCLUSIVE = 0, 1
 ROUTER_DYNAMIC, ROUTER_STATIC, ROUTER_NOFEEDBACK = 0, 1, 2
 (OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP, OP_POOL,
- OP_LAYER_ATTEND, OP_PASSES, OP_DENSE_ATTEND, OP_ATTEND_BACKWARD) = range(10)
+ OP_LAYER_ATTEND, OP_PASSES, OP_DENSE_ATTEND, OP_ATTEND_BACKWARD, OP_Q_BACKWARD,
+ OP_POOL_BACKWARD, OP_STEP_BACKWARD) = range(13)
 
 PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
                "Kd", "Vd", "g_in", "Wq", "g_qnorm")
@@ -52,6 +53,11 @@ class Params(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in PARAM_NAMES]
 
 
+class Grads(ctypes.Structure):
+    """wm_grads: fp32 device pointers named like the parameters (NULL where unused)."""
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_NAMES]
+
+
 _lib = None
 _vp, _i32p, _sz = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_size_t
 
@@ -65,7 +71,7 @@ def lib() -> ctypes.CDLL:
         raise ImportError("libwhitematter.so is not built (%s); run "
                           "`python -m paper_2608_18486_amd.build`" % LIB_PATH)
     L = ctypes.CDLL(LIB_PATH)
-    D, P = ctypes.POINTER(Dims), ctypes.POINTER(Params)
+    D, P, G = ctypes.POINTER(Dims), ctypes.POINTER(Params), ctypes.POINTER(Grads)
     sig = {
         "wm_router_mix": [D, P, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_kv_project": [D, P, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
@@ -81,6 +87,10 @@ def lib() -> ctypes.CDLL:
         "wm_channel_attend_dense": [D, P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_channel_attend_backward": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _vp, _vp, _vp, _vp, _sz, _vp],
+        "wm_q_project_backward": [D, P, _vp, _vp, _vp, _vp, G, _vp, _sz, _vp],
+        "wm_pool_backward": [D, P, _vp, _vp, _vp, _vp, _vp, G, _vp, _sz, _vp],
+        "wm_layer_step_backward": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, G,
+                                   _vp, _sz, _vp],
         "wm_layer_attend": [D, P, ctypes.c_int32, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_prefill_passes": [D, P, _vp, _vp, _i32p, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp,
                               _sz, _vp],
@@ -287,6 +297,41 @@ def channel_attend_backward(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O,
                                             _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
                                             _ptr(O), _ptr(dO), _ptr(dQ), _ptr(dKc), _ptr(dVc),
                                             _ptr(dKd), _ptr(dVd), wp, wn, _stream(stream)))
+
+
+def _grads(grads):
+    """ctypes reference to a wm_grads from a dict of float32 tensors (missing names: NULL)."""
+    if grads is None:
+        return None
+    return ctypes.byref(Grads(*[_ptr(grads.get(n)) for n in PARAM_NAMES]))
+
+
+def q_project_backward(dims: Dims, params, H, ctx_len, dQ, dH, grads, ws=None, stream=None):
+    """Gradients of q_project for dQ: added into dH and grads (dict of float32 tensors)."""
+    ws, wp, wn = _ws(dims, OP_Q_BACKWARD, ws, getattr(H, "device", None))
+    _check(lib().wm_q_project_backward(ctypes.byref(dims), _pref(params), _ptr(H), _ptr(ctx_len),
+                                       _ptr(dQ), _ptr(dH), _grads(grads), wp, wn,
+                                       _stream(stream)))
+
+
+def pool_backward(dims: Dims, params, H, ctx_len, dKc, dVc, dH, grads, ws=None, stream=None):
+    """Gradients of pool for the new cache rows' gradients dKc, dVc: added into dH and
+    grads."""
+    ws, wp, wn = _ws(dims, OP_POOL_BACKWARD, ws, getattr(H, "device", None))
+    _check(lib().wm_pool_backward(ctypes.byref(dims), _pref(params), _ptr(H), _ptr(ctx_len),
+                                  _ptr(dKc), _ptr(dVc), _ptr(dH), _grads(grads), wp, wn,
+                                  _stream(stream)))
+
+
+def layer_step_backward(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, dO, dKc, dVc, dH,
+                        grads, ws=None, stream=None):
+    """Gradients of layer_step for dO (and the gradients already in dKc, dVc): the cache
+    gradients added in dKc, dVc; the state and parameter gradients added into dH, grads."""
+    ws, wp, wn = _ws(dims, OP_STEP_BACKWARD, ws, getattr(H, "device", None))
+    _check(lib().wm_layer_step_backward(ctypes.byref(dims), _pref(params), _ptr(H),
+                                        _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
+                                        _ptr(O), _ptr(dO), _ptr(dKc), _ptr(dVc), _ptr(dH),
+                                        _grads(grads), wp, wn, _stream(stream)))
 
 
 def channel_attend_static(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, stream=None):

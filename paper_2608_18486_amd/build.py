@@ -20,6 +20,7 @@ SOURCES = {
     "wm_pool.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "wm_attend.hip": [],
     "wm_backward.hip": [],
+    "wm_grad.hip": [],
     "wm_calib.hip": [],
 }
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

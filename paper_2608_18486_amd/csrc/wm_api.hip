@@ -43,6 +43,11 @@ bool decode_path(const wm_dims& d) { return d.T_new <= 4; }
 struct Layout {
   size_t rinv = 0, alpha = 0, mixed = 0, rinv_mid = 0, tab = 0, q = 0, part = 0, wkv = 0, wq = 0,
          wa = 0, rpart = 0, hg = 0, topg = 0, ol = 0, kl = 0, vl = 0, kdl = 0, vdl = 0, total = 0;
+  // gradients: dQ, gain partial rows, dummy scratch, the Q side's normed input, pre-norm
+  // projection and its gradient, the pool side's normed states, mid-normed channels,
+  // K/V pre-norm values and gradients, channel gradients, state gradients, logit gradients
+  size_t dq = 0, dgp = 0, gkd = 0, x = 0, yq = 0, dx = 0, hn = 0, u = 0, ydy = 0, du = 0,
+         dhn = 0, dlog = 0;
 };
 
 int group_stride(const wm_dims& d) { return d.groups > 1 ? d.groups : 1; }
@@ -101,8 +106,64 @@ wm::Shape dense_shape(wm::Shape sh) {
   return sh;
 }
 
+// Partial rows per gain or bias gradient: fixed, so every sum has one order on any device.
+constexpr int kGradChunks = 64;
+
+// Workspace of the backward ops. The step's backward recomputes Q into q, takes the
+// attention gradients (dQ into dq), then runs the Q side and the pool side one after the
+// other in the same region: both start at the offset after the shared rows.
+Layout grad_layout(const wm_dims& d, int op) {
+  Layout Ly;
+  const size_t N = (size_t)d.B * d.T_new, L = d.L, k = d.k, D = d.D;
+  const size_t HQ = (size_t)d.Hq * d.d, HK = (size_t)d.Hkv * d.d;
+  const wm::Shape sh = make_shape(d);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += al256(bytes);
+    return at;
+  };
+  if (op == WM_OP_STEP_BACKWARD) {
+    Ly.q = take(L * N * HQ * 2);
+    Ly.dq = take(L * N * HQ * 4);
+    Ly.part = take(wm::attend_backward_rows_bytes(sh));
+    Ly.gkd = take(2 * k * HK * 4);
+    Ly.wq = take(wm::q_fold_elems(sh) * 2);
+  }
+  Ly.rinv = take(N * L * 4);
+  Ly.tab = take(N * d.d * 4);
+  Ly.dgp = take(std::max(std::max(L, k) * kGradChunks * D, kGradChunks * k * L) * 4);
+  const size_t base = off;
+  size_t end = off;
+  if (op == WM_OP_Q_BACKWARD || op == WM_OP_STEP_BACKWARD) {
+    Ly.x = take(N * L * D * 2);
+    Ly.yq = take(L * N * HQ * 4);
+    Ly.dx = take(N * L * D * 4);
+    end = std::max(end, off);
+    off = base;
+  }
+  if (op == WM_OP_POOL_BACKWARD || op == WM_OP_STEP_BACKWARD) {
+    Ly.alpha = take(2 * N * k * L * 4);
+    Ly.mixed = take(2 * k * N * D * 2);
+    Ly.rinv_mid = take(2 * k * N * 4);
+    Ly.wa = take(wm::router_fold_elems(sh) * 2);
+    Ly.rpart = take(wm::router_partials_bytes(sh));
+    Ly.hn = take(N * L * D * 2);
+    Ly.u = take(k * N * D * 2);
+    Ly.ydy = take(k * N * HK * 4);
+    Ly.du = take(k * N * D * 4);
+    Ly.dhn = take(N * L * D * 4);
+    Ly.dlog = take(N * k * L * 4);
+    end = std::max(end, off);
+  }
+  Ly.total = N == 0 ? 0 : end;
+  return Ly;
+}
+
 // Workspace regions for an op (offsets in bytes, each 256-byte aligned).
 Layout layout(const wm_dims& dd, int op) {
+  if (op == WM_OP_Q_BACKWARD || op == WM_OP_POOL_BACKWARD || op == WM_OP_STEP_BACKWARD)
+    return grad_layout(dd, op);
   Layout Ly;
   const bool passes = op == WM_OP_PASSES;
   // the pass driver works on one group at a time: its scratch is sized by a group (the
@@ -161,13 +222,14 @@ Layout layout(const wm_dims& dd, int op) {
 bool uses_cache(int op) {
   return op == WM_OP_KV_PROJECT || op == WM_OP_CHANNEL_ATTEND || op == WM_OP_LAYER_STEP ||
          op == WM_OP_POOL || op == WM_OP_LAYER_ATTEND || op == WM_OP_PASSES ||
-         op == WM_OP_DENSE_ATTEND || op == WM_OP_ATTEND_BACKWARD;
+         op == WM_OP_DENSE_ATTEND || op == WM_OP_ATTEND_BACKWARD || op == WM_OP_POOL_BACKWARD ||
+         op == WM_OP_STEP_BACKWARD;
 }
 
 int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (!dp) return fail(WM_ERR_ARG, "dims is NULL");
   const wm_dims& d = *dp;
-  if (op < WM_OP_ROUTER_MIX || op > WM_OP_ATTEND_BACKWARD) return fail(WM_ERR_ARG, "unknown op %d", op);
+  if (op < WM_OP_ROUTER_MIX || op > WM_OP_STEP_BACKWARD) return fail(WM_ERR_ARG, "unknown op %d", op);
   if (d.dtype != WM_F32 && d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "unknown dtype %d", d.dtype);
   if (d.mix_mode != WM_MIX_LINEAR && d.mix_mode != WM_MIX_SOFTMAX)
     return fail(WM_ERR_DTYPE, "unknown mix_mode %d", d.mix_mode);
@@ -232,7 +294,7 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
     if (d.ctx_max != 0) return fail(WM_ERR_ARG, "the pass driver starts empty sequences: ctx_max 0");
   }
   if (op == WM_OP_ROUTER_MIX || op == WM_OP_LAYER_STEP || op == WM_OP_POOL ||
-      op == WM_OP_PASSES) {
+      op == WM_OP_PASSES || op == WM_OP_POOL_BACKWARD || op == WM_OP_STEP_BACKWARD) {
     size_t lds = wm::mix_smem_bytes(d.L, d.k, d.D, elem_size(d));
     if (lds > 65536) return fail(WM_ERR_SHAPE, "L * D too large for the mix kernel (%zu B of LDS)", lds);
   }
@@ -553,6 +615,181 @@ int static_scratch(void** out) {
                 hipGetErrorString(a.rc));
   *out = a.ptr;
   return WM_OK;
+}
+
+
+// ------------------------------------------------------------------ gradients
+wm::GemmOperand opnd(const void* p, long s_row, long s_k, long s_z, bool f32) {
+  return wm::GemmOperand{p, s_row, s_k, s_z, f32 ? 1 : 0, 0};
+}
+
+// C[z] (+)= A[z] B[z]^T over `batches`; see GemmArgs for the k / row limits.
+void gemm(const wm::GemmOperand& A, const wm::GemmOperand& B, float* C, long c_row, long c_col,
+          long c_z, int M, int N, int K, int batches, bool acc, hipStream_t s, long klo0 = 0,
+          long klo_dz = 0, long mlo0 = 0, long mlo_dz = 0) {
+  wm::GemmArgs g{A, B, C, c_row, c_col, c_z, M, N, K, acc ? 1 : 0, klo0, klo_dz, mlo0, mlo_dz};
+  wm::launch_grad_gemm(g, batches, s);
+}
+
+// RMSNorm backward over rows (o, i) of D, gain rows o < nouter; dg partials in dgp.
+void rms_backward(const float* dy, long dy_o, long dy_i, const bf16* x, long x_o, long x_i,
+                  float* out, long out_o, long out_i, const float* rinv, long r_o, long r_i,
+                  const bf16* g, int D, int nouter, int ninner, bool acc, float* dgp,
+                  hipStream_t s) {
+  wm::RmsArgs a;
+  a.dy = dy, a.dy_o = dy_o, a.dy_i = dy_i;
+  a.x = x, a.x_o = x_o, a.x_i = x_i;
+  a.out = out, a.out_o = out_o, a.out_i = out_i;
+  a.rinv = rinv, a.r_o = r_o, a.r_i = r_i;
+  a.g = g, a.dgp = dgp;
+  a.D = D, a.ninner = ninner, a.chunks = kGradChunks, a.accumulate = acc ? 1 : 0;
+  wm::launch_grad_rms(a, nouter, s);
+}
+
+int grad_ptr(const float* p, const char* name) {
+  if (!p) return fail(WM_ERR_ARG, "grads->%s is NULL", name);
+  if ((uintptr_t)p % 4 != 0) return fail(WM_ERR_ARG, "grads->%s is not 4-byte aligned", name);
+  return WM_OK;
+}
+
+// What every gradient op supports: bf16, head dims 64 and 96, contiguous tokens, rows of
+// at most 4608 for the norms' backward, and the mix gradient's LDS.
+int check_backward(const wm_dims& d) {
+  if (d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "the gradients are built for bf16");
+  if (d.d != 64 && d.d != 96) return fail(WM_ERR_SHAPE, "the gradients support head dims 64 and 96");
+  if (group_stride(d) > 1)
+    return fail(WM_ERR_ARG, "the gradients need contiguous new tokens (groups <= 1)");
+  if (d.D > 4608) return fail(WM_ERR_SHAPE, "the gradients support D <= 4608");
+  if (wm::grad_mix_smem(d.L, d.k, d.D) > 65536)
+    return fail(WM_ERR_SHAPE, "L and k too large for the mix gradient's LDS");
+  return WM_OK;
+}
+
+// Gradients of the queries (input norm, W^Q, q norm, RoPE) for dQ [L][B][Hq][T][d]: into
+// dH [N][L][D] and the gradients of g_in, Wq, g_qnorm (all added).
+void run_q_backward(const wm_dims& d, const wm_params& P, const bf16* H, const int32_t* ctx_len,
+                    const float* dQ, float* dH, const wm_grads& G, const Layout& Ly, void* ws,
+                    hipStream_t s) {
+  const wm::Shape sh = make_shape(d);
+  const int N = sh.N(), L = d.L, D = d.D, HQ = d.Hq * d.d;
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* tab = (float*)at(ws, Ly.tab);
+  float* dgp = (float*)at(ws, Ly.dgp);
+  bf16* x = (bf16*)at(ws, Ly.x);
+  float* yq = (float*)at(ws, Ly.yq);
+  float* dx = (float*)at(ws, Ly.dx);
+  const bf16* Wq = (const bf16*)P.Wq;
+  wm::launch_row_rms<bf16>(H, (long)N * L, D, sh.eps, rinv, s);
+  wm::launch_rope_table(sh, ctx_len, tab, s);
+  // x[n][l] = g_in[l] h[n][l] / rms (bf16), then y_l = x_l Wq_l^T [N][HQ] per layer
+  wm::launch_grad_norm_apply(H, (const bf16*)P.g_in, rinv, (long)N * L, 1, L, D, x, s);
+  gemm(opnd(x, (long)L * D, 1, D, false), opnd(Wq, D, 1, (long)HQ * D, false), yq, HQ, 1,
+       (long)N * HQ, N, HQ, D, L, false, s);
+  // RoPE and q norm backward: y's gradient in place
+  wm::HeadArgs h{};
+  h.src = dQ, h.sZ = (long)d.B * d.Hq * d.T_new, h.sB = (long)d.Hq * d.T_new, h.sH = d.T_new;
+  h.slot_ctx = 0, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
+  h.y = yq, h.dy = yq, h.g = (const bf16*)P.g_qnorm, h.tab = tab, h.dgp = dgp;
+  h.B = d.B, h.H = d.Hq, h.T = d.T_new, h.chunks = kGradChunks, h.eps = d.eps;
+  wm::launch_grad_head(h, L, d.d, s);
+  wm::launch_grad_sum(dgp, L, kGradChunks, d.d, G.g_qnorm, 1.f, 1, s);
+  // dx_l = dy_l Wq_l [N][D] (into [N][L][D]); dWq_l += dy_l^T x_l [HQ][D]
+  gemm(opnd(yq, HQ, 1, (long)N * HQ, true), opnd(Wq, 1, D, (long)HQ * D, false), dx,
+       (long)L * D, 1, D, N, D, HQ, L, false, s);
+  gemm(opnd(yq, 1, HQ, (long)N * HQ, true), opnd(x, 1, (long)L * D, D, false), G.Wq, D, 1,
+       (long)HQ * D, HQ, D, N, L, true, s);
+  // input norm backward: rows (l, n) at n L + l
+  rms_backward(dx, 1, L, H, 1, L, dH, 1, L, rinv, 1, L, (const bf16*)P.g_in, D, L, N, true, dgp,
+               s);
+  wm::launch_grad_sum(dgp, L, kGradChunks, D, G.g_in, 1.f, 1, s);
+}
+
+// Gradients of the pool (Steps 1-2) for the gradients of the call's new cache slots
+// (dKc, dVc at slot ctx_len[b] + i): into dH and the gradients of g_pre, W_alpha (not with
+// static weights), b_alpha, g_mid, Wk, Wv, g_knorm (all added). The forward's router, mix
+// and norms are recomputed with the forward kernels.
+void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
+                       const int32_t* ctx_len, const float* dKc, const float* dVc, float* dH,
+                       const wm_grads& G, const Layout& Ly, void* ws, hipStream_t s) {
+  const wm::Shape sh = make_shape(d);
+  const int N = sh.N(), L = d.L, k = d.k, D = d.D, HK = d.Hkv * d.d, Lp = sh.Lp;
+  const int kL = k * L;
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* tab = (float*)at(ws, Ly.tab);
+  float* dgp = (float*)at(ws, Ly.dgp);
+  float* alpha = (float*)at(ws, Ly.alpha);
+  bf16* mixed = (bf16*)at(ws, Ly.mixed);
+  float* rinv_mid = (float*)at(ws, Ly.rinv_mid);
+  bf16* hn = (bf16*)at(ws, Ly.hn);
+  bf16* u = (bf16*)at(ws, Ly.u);
+  float* ydy = (float*)at(ws, Ly.ydy);
+  float* du = (float*)at(ws, Ly.du);
+  float* dhn = (float*)at(ws, Ly.dhn);
+  float* dlog = (float*)at(ws, Ly.dlog);
+  const wm::LayerTable sel = router_layers(d);
+  const bool dynamic = d.router_mode != WM_ROUTER_STATIC;
+  const bool nofb = d.router_mode == WM_ROUTER_NOFEEDBACK;
+  wm::launch_row_rms<bf16>(H, (long)N * L, D, sh.eps, rinv, s);
+  wm::launch_rope_table(sh, ctx_len, tab, s);
+  wm::launch_router<bf16>(sh, sel, H, rinv, (const bf16*)P.g_pre, (const bf16*)P.W_alpha,
+                          (const bf16*)P.b_alpha, alpha, (bf16*)at(ws, Ly.wa),
+                          (float*)at(ws, Ly.rpart), s);
+  wm::launch_mix<bf16>(sh, H, rinv, (const bf16*)P.g_pre, alpha, mixed, rinv_mid, s);
+  for (int br = 0; br < 2; ++br) {
+    const bf16* gpre = (const bf16*)P.g_pre + (long)br * L * D;
+    const bf16* gmid = (const bf16*)P.g_mid + (long)br * k * D;
+    const bf16* W = (const bf16*)(br ? P.Wv : P.Wk);
+    const bf16* mix_b = mixed + (long)br * k * N * D;
+    const float* rmid = rinv_mid + (long)br * k * N;
+    // u_j = g_mid[j] mixed_j / rms (bf16 [k][N][D])
+    wm::launch_grad_norm_apply(mix_b, gmid, rmid, (long)k * N, N, k, D, u, s);
+    if (br == 0) {
+      // y_j = u_j Wk_j^T [N][HK], then RoPE and key norm backward (y's gradient in place)
+      gemm(opnd(u, D, 1, (long)N * D, false), opnd(W, D, 1, (long)HK * D, false), ydy, HK, 1,
+           (long)N * HK, N, HK, D, k, false, s);
+      wm::HeadArgs h{};
+      h.src = dKc, h.sZ = (long)d.B * d.Hkv * d.S_cap, h.sB = (long)d.Hkv * d.S_cap;
+      h.sH = d.S_cap, h.slot_ctx = 1, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
+      h.y = ydy, h.dy = ydy, h.g = (const bf16*)P.g_knorm, h.tab = tab, h.dgp = dgp;
+      h.B = d.B, h.H = d.Hkv, h.T = d.T_new, h.chunks = kGradChunks, h.eps = d.eps;
+      wm::launch_grad_head(h, k, d.d, s);
+      wm::launch_grad_sum(dgp, k, kGradChunks, d.d, G.g_knorm, 1.f, 1, s);
+    } else {
+      wm::launch_grad_gather(dVc, k, d.B, d.Hkv, d.T_new, d.S_cap, d.d, ctx_len, sh.ctx_hi, ydy,
+                             s);
+    }
+    // du_j = dy_j W_j [N][D]; dW_j += dy_j^T u_j [HK][D]
+    gemm(opnd(ydy, HK, 1, (long)N * HK, true), opnd(W, 1, D, (long)HK * D, false), du, D, 1,
+         (long)N * D, N, D, HK, k, false, s);
+    gemm(opnd(ydy, 1, HK, (long)N * HK, true), opnd(u, 1, D, (long)N * D, false),
+         br ? G.Wv : G.Wk, D, 1, (long)HK * D, HK, D, N, k, true, s);
+    // mid norm backward in place: du becomes the mixed channels' gradient
+    rms_backward(du, N, 1, mix_b, N, 1, du, N, 1, rmid, N, 1, gmid, D, k, N, false, dgp, s);
+    wm::launch_grad_sum(dgp, k, kGradChunks, D, G.g_mid + (long)br * k * D, 1.f, 1, s);
+    // mix backward: dhn (written) and the logits' gradient
+    wm::MixGradArgs m{H, gpre, rinv, du, alpha + (long)br * N * kL, dhn, dlog, N, L, k, D,
+                      d.mix_mode == WM_MIX_SOFTMAX ? 1 : 0, nofb ? 1 : 0};
+    wm::launch_grad_mix(m, s);
+    wm::launch_grad_colsum(dlog, N, kL, kGradChunks, dgp, s);
+    wm::launch_grad_sum(dgp, 1, kGradChunks, kL, G.b_alpha + (long)br * kL, 1.f, 1, s);
+    if (dynamic) {
+      wm::launch_grad_norm_apply(H, gpre, rinv, (long)N * L, 1, L, D, hn, s);
+      // stacked source m is layer sel[m] = sel[0] + p m. dhn[n][sel[m]] += dlog[n] W_alpha[:, m]
+      // and dW_alpha[:, m] += dlog^T hn[:, sel[m]], batched over m; without feedback, router
+      // row o reads source m only when sel[m] <= o / L
+      const bf16* Wa = (const bf16*)P.W_alpha + (long)br * kL * Lp * D;
+      const long s0 = sel.v[0];
+      const long klo0 = nofb ? (long)L * s0 : 0, klo_dz = nofb ? (long)L * d.p : 0;
+      gemm(opnd(dlog, kL, 1, 0, true), opnd(Wa, 1, (long)Lp * D, D, false), dhn + s0 * D,
+           (long)L * D, 1, (long)d.p * D, N, D, kL, Lp, true, s, klo0, klo_dz);
+      gemm(opnd(dlog, 1, kL, 0, true), opnd(hn + s0 * D, 1, (long)L * D, (long)d.p * D, false),
+           G.W_alpha + (long)br * kL * Lp * D, (long)Lp * D, 1, D, kL, D, N, Lp, true, s, 0, 0,
+           klo0, klo_dz);
+    }
+    // pre-mix norm backward into dH: rows (l, n) at n L + l
+    rms_backward(dhn, 1, L, H, 1, L, dH, 1, L, rinv, 1, L, gpre, D, L, N, true, dgp, s);
+    wm::launch_grad_sum(dgp, L, kGradChunks, D, G.g_pre + (long)br * L * D, 1.f, 1, s);
+  }
 }
 
 }  // namespace
@@ -950,6 +1187,122 @@ int wm_prefill_passes(const wm_dims* dims, const wm_params* params, const void* 
   else
     run_passes<float>(d, *params, (const float*)W_o, (const float*)X, chan_map, passes,
                       (float*)Kc, (float*)Vc, (float*)H, (float*)h_top, ws, s);
+  return launched();
+}
+
+int wm_q_project_backward(const wm_dims* dims, const wm_params* params, const void* H,
+                          const int32_t* ctx_len, const float* dQ, float* dH,
+                          const wm_grads* grads, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  WM_TRY(validate_dims(dims, WM_OP_Q_BACKWARD, nullptr));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_backward(d));
+  WM_TRY(check_params(params, {P_GIN, P_WQ, P_GQN}));
+  if (!grads) return fail(WM_ERR_ARG, "grads is NULL");
+  WM_TRY(grad_ptr(grads->g_in, "g_in"));
+  WM_TRY(grad_ptr(grads->Wq, "Wq"));
+  WM_TRY(grad_ptr(grads->g_qnorm, "g_qnorm"));
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(grad_ptr(dQ, "(dQ)"));
+  WM_TRY(grad_ptr(dH, "(dH)"));
+  WM_TRY(check_ws(d, WM_OP_Q_BACKWARD, ws, ws_bytes));
+  (void)hipGetLastError();
+  run_q_backward(d, *params, (const bf16*)H, ctx_len, dQ, dH, *grads,
+                 layout(d, WM_OP_Q_BACKWARD), ws, (hipStream_t)stream);
+  return launched();
+}
+
+static int check_pool_grads(const wm_dims& d, const wm_params* params, const wm_grads* grads) {
+  if (d.router_mode == WM_ROUTER_STATIC)
+    WM_TRY(check_params(params, {P_GPRE, P_BA, P_GMID, P_WK, P_WV, P_GKN}));
+  else
+    WM_TRY(check_params(params, {P_GPRE, P_WA, P_BA, P_GMID, P_WK, P_WV, P_GKN}));
+  if (!grads) return fail(WM_ERR_ARG, "grads is NULL");
+  WM_TRY(grad_ptr(grads->g_pre, "g_pre"));
+  if (d.router_mode != WM_ROUTER_STATIC) WM_TRY(grad_ptr(grads->W_alpha, "W_alpha"));
+  WM_TRY(grad_ptr(grads->b_alpha, "b_alpha"));
+  WM_TRY(grad_ptr(grads->g_mid, "g_mid"));
+  WM_TRY(grad_ptr(grads->Wk, "Wk"));
+  WM_TRY(grad_ptr(grads->Wv, "Wv"));
+  WM_TRY(grad_ptr(grads->g_knorm, "g_knorm"));
+  return WM_OK;
+}
+
+int wm_pool_backward(const wm_dims* dims, const wm_params* params, const void* H,
+                     const int32_t* ctx_len, const float* dKc, const float* dVc, float* dH,
+                     const wm_grads* grads, void* ws, size_t ws_bytes, wm_stream_t stream) {
+  WM_TRY(validate_dims(dims, WM_OP_POOL_BACKWARD, nullptr));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_backward(d));
+  WM_TRY(check_pool_grads(d, params, grads));
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(grad_ptr(dKc, "(dKc)"));
+  WM_TRY(grad_ptr(dVc, "(dVc)"));
+  WM_TRY(grad_ptr(dH, "(dH)"));
+  WM_TRY(check_ws(d, WM_OP_POOL_BACKWARD, ws, ws_bytes));
+  (void)hipGetLastError();
+  run_pool_backward(d, *params, (const bf16*)H, ctx_len, dKc, dVc, dH, *grads,
+                    layout(d, WM_OP_POOL_BACKWARD), ws, (hipStream_t)stream);
+  return launched();
+}
+
+int wm_layer_step_backward(const wm_dims* dims, const wm_params* params, const void* H,
+                           const int32_t* chan_map, const int32_t* ctx_len, const void* Kc,
+                           const void* Vc, const void* O, const void* dO, float* dKc,
+                           float* dVc, float* dH, const wm_grads* grads, void* ws,
+                           size_t ws_bytes, wm_stream_t stream) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_STEP_BACKWARD, chan_map));
+  const wm_dims& d = *dims;
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_backward(d));
+  if (decode_path(d))
+    return fail(WM_ERR_SHAPE, "the step's gradients need a full-sequence call (T_new > 4)");
+  WM_TRY(check_pool_grads(d, params, grads));
+  WM_TRY(check_params(params, {P_GIN, P_WQ, P_GQN}));
+  if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_KD, P_VD}));
+  WM_TRY(grad_ptr(grads->g_in, "g_in"));
+  WM_TRY(grad_ptr(grads->Wq, "Wq"));
+  WM_TRY(grad_ptr(grads->g_qnorm, "g_qnorm"));
+  if (d.mask_mode == WM_MASK_PAPER) {
+    WM_TRY(grad_ptr(grads->Kd, "Kd"));
+    WM_TRY(grad_ptr(grads->Vd, "Vd"));
+  }
+  WM_TRY(need_ptr(H, "H"));
+  WM_TRY(need_ptr(Kc, "Kc"));
+  WM_TRY(need_ptr(Vc, "Vc"));
+  WM_TRY(need_ptr(O, "O"));
+  WM_TRY(need_ptr(dO, "dO"));
+  WM_TRY(need_ptr(dKc, "dKc"));
+  WM_TRY(need_ptr(dVc, "dVc"));
+  WM_TRY(grad_ptr(dH, "(dH)"));
+  WM_TRY(check_ws(d, WM_OP_STEP_BACKWARD, ws, ws_bytes));
+  (void)hipGetLastError();
+  hipStream_t s = (hipStream_t)stream;
+  const wm::Shape sh = make_shape(d);
+  const Layout Ly = layout(d, WM_OP_STEP_BACKWARD);
+  const wm_params& P = *params;
+  // the forward's queries, with the forward's kernels
+  bf16* Q = (bf16*)at(ws, Ly.q);
+  float* rinv = (float*)at(ws, Ly.rinv);
+  float* tab = (float*)at(ws, Ly.tab);
+  wm::launch_row_rms<bf16>((const bf16*)H, (long)sh.N() * sh.L, sh.D, sh.eps, rinv, s);
+  wm::launch_rope_table(sh, ctx_len, tab, s);
+  wm::launch_q_project<bf16>(sh, (const bf16*)H, rinv, (const bf16*)P.g_in, (const bf16*)P.Wq,
+                             (const bf16*)P.g_qnorm, tab, Q, (bf16*)at(ws, Ly.wq), s);
+  // attention gradients: dQ, and the slots' and dummy's gradients added to the caller's
+  float* dQ = (float*)at(ws, Ly.dq);
+  float* gkd = (float*)at(ws, Ly.gkd);
+  const bool paper = d.mask_mode == WM_MASK_PAPER;
+  const long nd = (long)d.k * d.Hkv * d.d;
+  wm::launch_attend_backward(sh, map_table(d, chan_map), groups(d, chan_map), Q,
+                             (const bf16*)Kc, (const bf16*)Vc, (const bf16*)P.Kd,
+                             (const bf16*)P.Vd, (const bf16*)O, (const bf16*)dO, ctx_len, dQ,
+                             dKc, dVc, paper ? grads->Kd : gkd, paper ? grads->Vd : gkd + nd,
+                             (float*)at(ws, Ly.part), s, true);
+  run_q_backward(d, P, (const bf16*)H, ctx_len, dQ, dH, *grads, Ly, ws, s);
+  run_pool_backward(d, P, (const bf16*)H, ctx_len, dKc, dVc, dH, *grads, Ly, ws, s);
   return launched();
 }
 

@@ -32,6 +32,7 @@ struct BwdArgs {
   float scale_log2, scale;  // log2(e) / sqrt(d), 1 / sqrt(d)
   LayerTable chan;
   ChannelGroups grp;
+  int accumulate;  // add the slot and dummy gradients into dKc, dVc, dKd, dVd
 };
 
 constexpr int kBwdThreads = 256;
@@ -389,6 +390,10 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) 
           kq[i] = dk[dt][4 * g + i] * a.scale;
           vq[i] = dv[dt][4 * g + i];
         }
+        if (a.accumulate) {
+          kq += *(const f32x4*)(dkd + 32 * dt + 8 * g + 4 * h);
+          vq += *(const f32x4*)(dvd + 32 * dt + 8 * g + 4 * h);
+        }
         *(f32x4*)(dkd + 32 * dt + 8 * g + 4 * h) = kq;
         *(f32x4*)(dvd + 32 * dt + 8 * g + 4 * h) = vq;
       }
@@ -442,8 +447,10 @@ __global__ __launch_bounds__(DH) void attend_bwd_dummy_sum_kernel(BwdArgs a, con
     v += p[e];
     k += p[DH + e];
   }
-  a.dVd[(long)ck * DH + e] = v;
-  a.dKd[(long)ck * DH + e] = k * a.scale;
+  float* pv = a.dVd + (long)ck * DH + e;
+  float* pk = a.dKd + (long)ck * DH + e;
+  *pv = a.accumulate ? *pv + v : v;
+  *pk = a.accumulate ? *pk + k * a.scale : k * a.scale;
 }
 
 size_t attend_backward_rows_bytes(const Shape& sh) {
@@ -455,14 +462,15 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
                             const ChannelGroups& groups, const bf16* Q, const bf16* Kc,
                             const bf16* Vc, const bf16* Kd, const bf16* Vd, const bf16* O,
                             const bf16* dO, const int32_t* ctx_len, float* dQ, float* dKc,
-                            float* dVc, float* dKd, float* dVd, float* rows, hipStream_t s) {
+                            float* dVc, float* dKd, float* dVd, float* rows, hipStream_t s,
+                            bool accumulate) {
   if (sh.N() <= 0) return;
   const long nrow = (long)sh.L * sh.B * sh.Hq * sh.T_new;
   BwdArgs a{Q, Kc, Vc, Kd, Vd, O, dO, ctx_len, dQ, dKc, dVc, dKd, dVd, rows, rows + nrow,
             rows + 2 * nrow, rows + 3 * nrow, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
             sh.mask_paper, sh.ctx_hi, (sh.T_new + 127) / 128,
             (int)(((long)sh.ctx_max + sh.T_new + 127) / 128), kLog2e / sqrtf((float)sh.d),
-            1.0f / sqrtf((float)sh.d), chan_map, groups};
+            1.0f / sqrtf((float)sh.d), chan_map, groups, accumulate ? 1 : 0};
   const dim3 ga(a.n_qtiles * sh.Hq * sh.B * sh.L), gb(a.n_stiles * sh.Hkv * sh.B * sh.k),
       gp(sh.k * sh.Hkv * kDummyChunks), gs(sh.k * sh.Hkv);
   float* part = rows + 4 * nrow;

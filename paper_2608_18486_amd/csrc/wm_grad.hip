@@ -1,0 +1,570 @@
+// Gradients of the pool (Section 3.1 Steps 1-2) and of the consumer queries (Step 7):
+// the backward pass through the norms, the router, the mix and the projections, which
+// training runs through its gradient-carrying passes (Section 3.3). bf16 operands, fp32
+// gradients.
+//
+//   grad_gemm_kernel       C (+)= A B for strided, batched operands (bf16 or fp32, staged
+//                          to LDS as bf16), MFMA 32x32x16, fp32 accumulation: every
+//                          projection and router gradient (dX = dY W, dW = dY^T X) and the
+//                          recomputed pre-norm projections.
+//   grad_norm_apply_kernel g x / rms(x) rows as bf16 (the normed operands the GEMMs need).
+//   grad_head_kernel       per head: the transposed RoPE rotation, then the head RMSNorm's
+//                          backward (query and key norms), with the gain gradient's partial
+//                          sums.
+//   grad_rms_kernel        RMSNorm backward over rows of D (input, pre-mix and mid norms),
+//                          with the gain gradient's partial sums.
+//   grad_mix_kernel        per token: dĥ_l = sum_j alpha_jl dh~_j and dalpha_jl =
+//                          dh~_j . ĥ_l (fp32), then the softmax (or masking) backward into
+//                          the router logits' gradient.
+//   grad_sum_kernel        deterministic sums of partial rows (gain and bias gradients).
+#include "wm_device.hpp"
+#include "wm_frag.hpp"
+#include "wm_internal.hpp"
+
+namespace wm {
+
+// ------------------------------------------------------------------------ GEMM
+// 128 x 128 output tiles, 4 waves of 64 x 64, K-steps of 32 staged to LDS as bf16 (the
+// next step's global loads in flight during this step's MFMAs). Each operand is staged in
+// one of two layouts, chosen from its strides:
+//   N (k contiguous in memory): LDS [128 rows][32 k], 64-byte rows with a chunk swizzle;
+//     lane (h, r) reads row r, k 16 ks + 8 h .. + 7 as one 16-byte word.
+//   T (rows contiguous, k strided: the transposed operands of dW = dY^T X and dX = dY W):
+//     LDS [32 k][kLdt] (rows padded), filled by 8-row vector loads along the rows; lane
+//     (h, r) gathers the same fragment with two transposing reads (ds_read_b64_tr_b16).
+constexpr int kGT = 256;        // threads per GEMM workgroup
+constexpr int kLdt = 144;       // T layout row pitch in elements (128 + 16: the four k rows
+                                // one 16-lane group reads fall in disjoint banks)
+constexpr int kGTile = 32 * kLdt * 2;  // bytes per staged operand tile (>= 128 * 64)
+
+__device__ __forceinline__ int grad_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+
+// N layout: this thread's 16 elements (row r, k = k0 + 16 half .. + 15) of the tile;
+// elements with k < klo are zero. VEC: vector loads (the operands' strides allow them);
+// otherwise element by element (kept out of the vector kernels: it needs many registers).
+template <bool VEC>
+__device__ __forceinline__ void gemm_load_n(const GemmOperand& o, long zoff, int row0, int k0,
+                                            int nrows, int K, int klo, int tid, bf16x8 (&v)[2]) {
+  const int r = tid & 127, half = tid >> 7;
+  const int row = row0 + r, kb = k0 + 16 * half;
+  if constexpr (VEC) {  // k contiguous, rows and batches 8-aligned: two 8-element loads
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const int k = kb + 8 * g;
+      const bool ok = row < nrows && k < K;  // K is a multiple of 8 on this path
+      if (o.f32) {
+        const float* p = (const float*)o.p + zoff + (long)row * o.s_row + k;
+        f32x4 a = ok ? *(const f32x4*)p : f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 b = ok ? *(const f32x4*)(p + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[g][e] = (bf16)a[e];
+          v[g][4 + e] = (bf16)b[e];
+        }
+      } else {
+        const bf16* p = (const bf16*)o.p + zoff + (long)row * o.s_row + k;
+        v[g] = ok ? *(const bf16x8*)p : zero_frag<bf16>();
+      }
+      if (klo > k) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (k + e < klo) v[g][e] = (bf16)0.f;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int k = kb + e;
+      float x = 0.f;
+      if (row < nrows && k < K && k >= klo) {
+        const long off = zoff + (long)row * o.s_row + (long)k * o.s_k;
+        x = o.f32 ? ((const float*)o.p)[off] : (float)((const bf16*)o.p)[off];
+      }
+      v[e >> 3][e & 7] = (bf16)x;
+    }
+  }
+}
+
+__device__ __forceinline__ void gemm_store_n(char* tile, int tid, const bf16x8 (&v)[2]) {
+  const int r = tid & 127, half = tid >> 7;
+#pragma unroll
+  for (int g = 0; g < 2; ++g)
+    *(bf16x8*)(tile + r * 64 + 16 * ((2 * half + g) ^ grad_swz(r))) = v[g];
+}
+
+// T layout: item g of this thread is k = k0 + idx / 16, rows row0 + 8 (idx % 16) .. + 7
+// with idx = tid + 256 g.
+template <bool VEC>
+__device__ __forceinline__ void gemm_load_t(const GemmOperand& o, long zoff, int row0, int k0,
+                                            int nrows, int K, int klo, int tid, bf16x8 (&v)[2]) {
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    const int idx = tid + 256 * g, k = k0 + (idx >> 4), row = row0 + 8 * (idx & 15);
+    const bool kok = k < K && k >= klo;
+    if constexpr (VEC) {  // rows contiguous, nrows and strides 8-aligned
+      const bool ok = kok && row < nrows;
+      if (o.f32) {
+        const float* p = (const float*)o.p + zoff + (long)k * o.s_k + row;
+        f32x4 a = ok ? *(const f32x4*)p : f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 b = ok ? *(const f32x4*)(p + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[g][e] = (bf16)a[e];
+          v[g][4 + e] = (bf16)b[e];
+        }
+      } else {
+        const bf16* p = (const bf16*)o.p + zoff + (long)k * o.s_k + row;
+        v[g] = ok ? *(const bf16x8*)p : zero_frag<bf16>();
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float x = 0.f;
+        if (kok && row + e < nrows) {
+          const long off = zoff + (long)(row + e) * o.s_row + (long)k * o.s_k;
+          x = o.f32 ? ((const float*)o.p)[off] : (float)((const bf16*)o.p)[off];
+        }
+        v[g][e] = (bf16)x;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void gemm_store_t(char* tile, int tid, const bf16x8 (&v)[2]) {
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    const int idx = tid + 256 * g;
+    *(bf16x8*)(tile + ((idx >> 4) * kLdt + 8 * (idx & 15)) * 2) = v[g];
+  }
+}
+
+// Fragment of rows rb .. rb + 31 (lane row r), k 16 ks + 8 h .. + 7, from either layout.
+// T layout: within a 16-lane group, lane j addresses k row 16 ks + 8 h + 4 s + j / 4 and
+// rows rb + 16 (group & 1) + 4 (j % 4) .. + 3; the transposing read hands lane i the four
+// k values of row rb + 16 (group & 1) + i, so s = 0, 1 give k 8 h + 0..3 and 4..7.
+template <bool T>
+__device__ __forceinline__ bf16x8 gemm_frag(const char* tile, int rb, int ks, int lane) {
+  if constexpr (T) {
+    const int j = lane & 15, grp = lane >> 4, h = lane >> 5;
+    const char* p =
+        tile + ((16 * ks + 8 * h + (j >> 2)) * kLdt + rb + 16 * (grp & 1) + 4 * (j & 3)) * 2;
+    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+    const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+    const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * kLdt * 2));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+  } else {
+    const int h = lane >> 5, row = rb + (lane & 31);
+    return *(const bf16x8*)(tile + row * 64 + 16 * ((2 * ks + h) ^ grad_swz(row)));
+  }
+}
+
+template <bool TA, bool TB, bool VEC>
+__global__ __launch_bounds__(kGT) void grad_gemm_kernel(GemmArgs a) {
+  __shared__ __align__(16) char smem[2][2][kGTile];  // [buffer][A, B]
+  const int tm = (a.M + 127) / 128, tn = (a.N + 127) / 128;
+  const int z = blockIdx.x / (tm * tn), t = blockIdx.x % (tm * tn);
+  const int m0 = (t / tn) * 128, n0 = (t % tn) * 128;
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
+  const int w = tid >> 6, wm = w & 1, wn = w >> 1;
+  const long za = (long)z * a.A.s_z, zb = (long)z * a.B.s_z;
+  const int klo = (int)(a.k_lo0 + a.k_lo_dz * z);
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
+  bf16x8 va[2], vb[2];
+  const int nk = (a.K + 31) / 32;
+  auto load = [&](int k0) {
+    if constexpr (TA) gemm_load_t<VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
+    else gemm_load_n<VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
+    if constexpr (TB) gemm_load_t<VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
+    else gemm_load_n<VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
+  };
+  load(0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int u = kt & 1;
+    if constexpr (TA) gemm_store_t(smem[u][0], tid, va);
+    else gemm_store_n(smem[u][0], tid, va);
+    if constexpr (TB) gemm_store_t(smem[u][1], tid, vb);
+    else gemm_store_n(smem[u][1], tid, vb);
+    __syncthreads();  // tile kt in LDS; every wave is done with tile kt - 1
+    if (kt + 1 < nk) load(32 * (kt + 1));
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = gemm_frag<TA>(smem[u][0], 64 * wm + 32 * i, ks, lane);
+        fb[i] = gemm_frag<TB>(smem[u][1], 64 * wn + 32 * i, ks, lane);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mma32(acc[i][j], fa[i], fb[j]);
+    }
+  }
+  // lane (h, r): column n0 + 64 wn + 32 j + r, rows m0 + 64 wm + 32 i + 8 (q / 4) + 4 h + q % 4
+  float* C = a.C + (long)z * a.c_z;
+  const int mlo = (int)(a.m_lo0 + a.m_lo_dz * z);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = n0 + 64 * wn + 32 * j + r;
+    if (n >= a.N) continue;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int m = m0 + 64 * wm + 32 * i + 8 * (q >> 2) + 4 * h + (q & 3);
+        if (m < a.M && m >= mlo) {
+          float* p = C + (long)m * a.c_row + (long)n * a.c_col;
+          *p = a.accumulate ? *p + acc[i][j][q] : acc[i][j][q];
+        }
+      }
+  }
+}
+
+static bool operand_t(const GemmOperand& o) { return o.s_row == 1 && o.s_k != 1; }
+
+static bool operand_vec(const GemmOperand& o, int nrows, int K) {
+  if ((uintptr_t)o.p % 16 != 0 || o.s_z % 8 != 0) return false;
+  if (operand_t(o)) return o.s_k % 8 == 0 && nrows % 8 == 0;
+  return o.s_k == 1 && o.s_row % 8 == 0 && K % 8 == 0;
+}
+
+template <bool TA, bool TB>
+static void launch_gemm_t(const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
+  if (vec) hipLaunchKernelGGL((grad_gemm_kernel<TA, TB, true>), grid, dim3(kGT), 0, s, a);
+  else hipLaunchKernelGGL((grad_gemm_kernel<TA, TB, false>), grid, dim3(kGT), 0, s, a);
+}
+
+void launch_grad_gemm(GemmArgs a, int batches, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0 || batches <= 0) return;
+  a.A.vec = operand_vec(a.A, a.M, a.K);
+  a.B.vec = operand_vec(a.B, a.N, a.K);
+  const bool vec = a.A.vec && a.B.vec;
+  const long tiles = (long)((a.M + 127) / 128) * ((a.N + 127) / 128) * batches;
+  const bool ta = operand_t(a.A), tb = operand_t(a.B);
+  const dim3 grid((unsigned)tiles);
+  if (ta && tb) launch_gemm_t<true, true>(a, grid, vec, s);
+  else if (ta) launch_gemm_t<true, false>(a, grid, vec, s);
+  else if (tb) launch_gemm_t<false, true>(a, grid, vec, s);
+  else launch_gemm_t<false, false>(a, grid, vec, s);
+}
+
+// --------------------------------------------------------------- row kernels
+// out[r][e] = g[(r / gdiv) % gmod][e] * x[r][e] * rinv[r], as bf16; one block per row.
+__global__ __launch_bounds__(256) void grad_norm_apply_kernel(const bf16* x, const bf16* g,
+                                                              const float* rinv, long gdiv,
+                                                              int gmod, int D, bf16* out) {
+  const long r = blockIdx.x;
+  const bf16* gr = g + ((r / gdiv) % gmod) * (long)D;
+  const float ri = rinv[r];
+  for (int e = threadIdx.x; e < D; e += 256)
+    out[r * D + e] = (bf16)((float)gr[e] * (float)x[r * D + e] * ri);
+}
+
+void launch_grad_norm_apply(const bf16* x, const bf16* g, const float* rinv, long rows, long gdiv,
+                            int gmod, int D, bf16* out, hipStream_t s) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(grad_norm_apply_kernel, dim3((unsigned)rows), dim3(256), 0, s, x, g, rinv,
+                     gdiv, gmod, D, out);
+}
+
+// Head RMSNorm + RoPE backward. Row (z, b, h, i): the gradient dR of the rotated output at
+// src[z][b][h][slot] (slot = i, or ctx_len[b] + i for the cache; rows of d floats), the
+// pre-norm values y at y[z][b T + i][h d] (fp32), the gain g[z][d] and the angle table
+// tab[b T + i][d / 2] (cos, sin) of the forward; writes dy (the gradient of y, y's layout)
+// and adds each row's dg contribution into the workgroup's partial row
+// dgp[z][blockIdx.x % chunks][d]. One wave per row.
+template <int DH>
+__global__ __launch_bounds__(256) void grad_head_kernel(HeadArgs a) {
+  constexpr int PER = (DH + 63) / 64;
+  const int chunk = blockIdx.x % a.chunks, z = blockIdx.x / a.chunks;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long rows = (long)a.B * a.H * a.T;  // rows of one z
+  const long r0 = rows * chunk / a.chunks, r1 = rows * (chunk + 1) / a.chunks;
+  float dg[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) dg[q] = 0.f;
+  const bf16* g = a.g + (long)z * DH;
+  for (long rr = r0 + w; rr < r1; rr += 4) {
+    const int i = (int)(rr % a.T), hh = (int)(rr / a.T % a.H), b = (int)(rr / ((long)a.T * a.H));
+    const int slot = a.slot_ctx ? ctx_at(a.ctx_len, b, a.ctx_hi) + i : i;
+    const float* src = a.src + ((long)z * a.sZ + (long)b * a.sB + (long)hh * a.sH + slot) * DH;
+    const long yrow = ((long)z * a.B * a.T + (long)b * a.T + i) * a.H * DH + (long)hh * DH;
+    const float* tab = a.tab + ((long)b * a.T + i) * DH;  // DH / 2 (cos, sin) pairs
+    // RoPE^T: (da, db) = (c dx_m + s dx_{m+d/2}, -s dx_m + c dx_{m+d/2})
+    float yv[PER], gy[PER], dr[PER];
+    float ss = 0.f;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int e = lane + 64 * q;
+      yv[q] = gy[q] = dr[q] = 0.f;
+      if (e < DH) {
+        const int m = e < DH / 2 ? e : e - DH / 2;
+        const float cs = tab[2 * m], sn = tab[2 * m + 1];
+        const float dx = src[e], dp = src[e < DH / 2 ? e + DH / 2 : e - DH / 2];
+        dr[q] = e < DH / 2 ? cs * dx + sn * dp : cs * dx - sn * dp;
+        yv[q] = a.y[yrow + e];
+        gy[q] = (float)g[e] * dr[q];
+        ss += yv[q] * yv[q];
+      }
+    }
+    ss = wave_sum(ss);
+    const float ri = 1.0f / sqrtf(ss / DH + a.eps);
+    float dot = 0.f;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) dot += gy[q] * yv[q];
+    dot = wave_sum(dot);
+    const float c2 = ri * ri * dot / DH;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int e = lane + 64 * q;
+      if (e < DH) {
+        a.dy[yrow + e] = ri * (gy[q] - yv[q] * c2);
+        dg[q] += dr[q] * yv[q] * ri;
+      }
+    }
+  }
+  __shared__ float s_dg[4][DH];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = lane + 64 * q;
+    if (e < DH) s_dg[w][e] = dg[q];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < DH; e += 256)
+    a.dgp[((long)z * a.chunks + chunk) * DH + e] =
+        (s_dg[0][e] + s_dg[1][e]) + (s_dg[2][e] + s_dg[3][e]);
+}
+
+void launch_grad_head(const HeadArgs& a, int Z, int d, hipStream_t s) {
+  if (Z <= 0 || (long)a.B * a.H * a.T == 0) return;
+  const dim3 grid(Z * a.chunks);
+  if (d == 64) hipLaunchKernelGGL(grad_head_kernel<64>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(grad_head_kernel<96>, grid, dim3(256), 0, s, a);
+}
+
+// RMSNorm backward over rows of D: row (o, i) for gain row o (0 <= o < nouter) and
+// i < ninner; tensors addressed as base + (o s_o + i s_i) D. With y = g x / rms(x):
+// dx = rinv (g dy - x rinv^2 (g dy . x) / D), dg += dy x rinv. dx is added into out (or
+// written when accumulate is 0); dg partial rows per workgroup.
+__global__ __launch_bounds__(256) void grad_rms_kernel(RmsArgs a) {
+  constexpr int MAXP = 18;  // D <= 4608
+  const int chunk = blockIdx.x % a.chunks, o = blockIdx.x / a.chunks;
+  const long i0 = (long)a.ninner * chunk / a.chunks, i1 = (long)a.ninner * (chunk + 1) / a.chunks;
+  const int tid = threadIdx.x;
+  __shared__ float s_red[2][4];
+  float dg[MAXP];
+#pragma unroll
+  for (int q = 0; q < MAXP; ++q) dg[q] = 0.f;
+  const bf16* g = a.g + (long)o * a.D;
+  int par = 0;
+  for (long i = i0; i < i1; ++i, par ^= 1) {
+    const float* dy = a.dy + ((long)o * a.dy_o + i * a.dy_i) * a.D;
+    const bf16* x = a.x + ((long)o * a.x_o + i * a.x_i) * a.D;
+    float* out = a.out + ((long)o * a.out_o + i * a.out_i) * a.D;
+    const float ri = a.rinv[(long)o * a.r_o + i * a.r_i];
+    float dv[MAXP], xv[MAXP], dot = 0.f;
+#pragma unroll
+    for (int q = 0; q < MAXP; ++q) {
+      const int e = tid + 256 * q;
+      dv[q] = xv[q] = 0.f;
+      if (e < a.D) {
+        dv[q] = dy[e];
+        xv[q] = (float)x[e];
+        dot += (float)g[e] * dv[q] * xv[q];
+      }
+    }
+    dot = wave_sum(dot);
+    if ((tid & 63) == 0) s_red[par][tid >> 6] = dot;
+    __syncthreads();  // (alternating halves of s_red: one barrier per row)
+    dot = (s_red[par][0] + s_red[par][1]) + (s_red[par][2] + s_red[par][3]);
+    const float c2 = ri * ri * dot / a.D;
+#pragma unroll
+    for (int q = 0; q < MAXP; ++q) {
+      const int e = tid + 256 * q;
+      if (e < a.D) {
+        const float dx = ri * ((float)g[e] * dv[q] - xv[q] * c2);
+        out[e] = a.accumulate ? out[e] + dx : dx;
+        dg[q] += dv[q] * xv[q] * ri;
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < MAXP; ++q) {
+    const int e = tid + 256 * q;
+    if (e < a.D) a.dgp[((long)o * a.chunks + chunk) * a.D + e] = dg[q];
+  }
+}
+
+void launch_grad_rms(const RmsArgs& a, int nouter, hipStream_t s) {
+  if (nouter <= 0 || a.ninner <= 0) return;
+  hipLaunchKernelGGL(grad_rms_kernel, dim3(nouter * a.chunks), dim3(256), 0, s, a);
+}
+
+// out[o][e] (+)= scale * sum over c < chunks of part[(o chunks + c) n + e] (fixed order).
+__global__ __launch_bounds__(256) void grad_sum_kernel(const float* part, int chunks, long n,
+                                                       float* out, float scale, int accumulate) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long o = blockIdx.y;
+  if (idx >= n) return;
+  float v = 0.f;
+  for (int c = 0; c < chunks; ++c) v += part[(o * chunks + c) * n + idx];
+  out[o * n + idx] = accumulate ? out[o * n + idx] + v * scale : v * scale;
+}
+
+void launch_grad_sum(const float* part, int outer, int chunks, long n, float* out, float scale,
+                     int accumulate, hipStream_t s) {
+  if (outer <= 0 || n <= 0) return;
+  hipLaunchKernelGGL(grad_sum_kernel, dim3((unsigned)((n + 255) / 256), outer), dim3(256), 0, s,
+                     part, chunks, n, out, scale, accumulate);
+}
+
+// Per token and branch: the normed states hn[l] = g[l] h[l] / rms(h[l]) (recomputed in fp32
+// from the bf16 states H [N][L][D], the branch's gains g [L][D] and rinv [N][L], as the
+// forward mix computes them), the channels' gradient dmix [k][N][D] (fp32) and the final
+// mixing weights alpha [N][k][L] (fp32) give dhn[n][l][e] = sum_j alpha[j][l] dmix[j][e]
+// (written, fp32) and dalpha[j][l] = dmix[j] . hn[l]; then the softmax-over-depth backward
+// (or the mask of the sources a channel may not mix) gives the router logits' gradient
+// dlog [N][k L] (fp32). Everything stays fp32: dalpha[j][l] is a small difference when
+// one source dominates a channel (the mid norm's gradient is orthogonal to the mixed
+// channel), which bf16 operands would swamp. The states go through LDS in column chunks
+// of kMixGradCols, the dalpha sums accumulating across chunks (each (j, l) pair stays
+// with one wave).
+constexpr int kMixGradCols = 64;
+
+__global__ __launch_bounds__(256) void grad_mix_kernel(MixGradArgs a) {
+  extern __shared__ __align__(16) unsigned char gsm[];
+  const int L = a.L, k = a.k, D = a.D;
+  const long n = blockIdx.x;
+  constexpr int DC = kMixGradCols;
+  float* hs = (float*)gsm;                        // [L][DC]
+  float* ds = hs + L * DC;                        // [k][DC]
+  float* al = ds + k * DC;                        // [k][L]
+  float* da = al + k * L;                         // [k][L]
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int e = tid; e < k * L; e += 256) {
+    al[e] = a.alpha[n * k * L + e];
+    da[e] = 0.f;
+  }
+  for (int c0 = 0; c0 < D; c0 += DC) {
+    __syncthreads();  // the previous chunk is consumed (and al, da are in place)
+    for (int e = tid; e < L * DC; e += 256) {
+      const int l = e / DC, c = c0 + e % DC;
+      hs[e] = c < D ? (float)a.g[(long)l * D + c] * (float)a.H[(n * L + l) * D + c] *
+                          a.rinv[n * L + l]
+                    : 0.f;
+    }
+    for (int e = tid; e < k * DC; e += 256) {
+      const int j = e / DC, c = c0 + e % DC;
+      ds[e] = c < D ? a.dmix[((long)j * a.N + n) * D + c] : 0.f;
+    }
+    __syncthreads();
+    for (int pr = w; pr < k * L; pr += 4) {
+      const int j = pr / L, l = pr % L;
+      float s = 0.f;
+      for (int c = lane; c < DC; c += 64) s += ds[j * DC + c] * hs[l * DC + c];
+      s = wave_sum(s);
+      if (lane == 0) da[pr] += s;
+    }
+    for (int e = tid; e < L * DC; e += 256) {
+      const int l = e / DC, c = e % DC;
+      if (c0 + c < D) {
+        float s = 0.f;
+        for (int j = 0; j < k; ++j) s += al[j * L + l] * ds[j * DC + c];
+        a.dhn[(n * L + l) * D + c0 + c] = s;
+      }
+    }
+  }
+  __syncthreads();
+  // logits' gradient per channel row
+  for (int j = tid; j < k; j += 256) {
+    const int nl = a.nofeedback ? j + 1 : L;
+    float dot = 0.f;
+    if (a.softmax)
+      for (int l = 0; l < nl; ++l) dot += al[j * L + l] * da[j * L + l];
+    for (int l = 0; l < L; ++l) {
+      float v = 0.f;
+      if (l < nl) v = a.softmax ? al[j * L + l] * (da[j * L + l] - dot) : da[j * L + l];
+      a.dlog[n * k * L + j * L + l] = v;
+    }
+  }
+}
+
+size_t grad_mix_smem(int L, int k, int D) {
+  (void)D;
+  return (size_t)(L + k) * kMixGradCols * 4 + (size_t)2 * k * L * 4;
+}
+
+void launch_grad_mix(const MixGradArgs& a, hipStream_t s) {
+  if (a.N <= 0) return;
+  hipLaunchKernelGGL(grad_mix_kernel, dim3((unsigned)a.N), dim3(256),
+                     grad_mix_smem(a.L, a.k, a.D), s, a);
+}
+
+// dst[j][b T + i][h d + e] = src[j][b][h][ctx_len[b] + i][e]: the new slots' rows of a
+// cache-layout gradient, token-major for the projection GEMMs.
+__global__ __launch_bounds__(256) void grad_gather_kernel(const float* src, int k, int B, int H,
+                                                          int T, int S_cap, int d,
+                                                          const int32_t* ctx_len, int ctx_hi,
+                                                          float* dst) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long n = (long)k * B * T * H * d;
+  if (idx >= n) return;
+  const int e = (int)(idx % d), hh = (int)(idx / d % H);
+  const long t = idx / ((long)d * H);  // (j, b, i)
+  const int i = (int)(t % T), b = (int)(t / T % B), j = (int)(t / ((long)T * B));
+  const int slot = ctx_at(ctx_len, b, ctx_hi) + i;
+  dst[idx] = src[((((long)j * B + b) * H + hh) * S_cap + slot) * d + e];
+}
+
+void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,
+                        const int32_t* ctx_len, int ctx_hi, float* dst, hipStream_t s) {
+  const long n = (long)k * B * T * H * d;
+  if (n <= 0) return;
+  hipLaunchKernelGGL(grad_gather_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,
+                     k, B, H, T, S_cap, d, ctx_len, ctx_hi, dst);
+}
+
+// part[c][o] = sum over rows r in chunk c of x[r][o] (x [rows][n]); chunks = gridDim.y.
+__global__ __launch_bounds__(256) void grad_colsum_kernel(const float* x, long rows, int n,
+                                                          float* part) {
+  const int o = blockIdx.x * 256 + threadIdx.x, c = blockIdx.y, nc = gridDim.y;
+  if (o >= n) return;
+  const long r0 = rows * c / nc, r1 = rows * (c + 1) / nc;
+  float v = 0.f;
+  for (long r = r0; r < r1; ++r) v += x[r * n + o];
+  part[(long)c * n + o] = v;
+}
+
+void launch_grad_colsum(const float* x, long rows, int n, int chunks, float* part, hipStream_t s) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(grad_colsum_kernel, dim3((n + 255) / 256, chunks), dim3(256), 0, s, x, rows,
+                     n, part);
+}
+
+// Zeroes the router weight entries (o, m) whose source layer sel[m] lies above channel
+// o / L (the no-feedback ablation's mask): W [kL][Lp D] rows, in place (bf16 or fp32).
+template <typename T>
+__global__ __launch_bounds__(256) void grad_mask_kernel(T* W, int kL, int L, int Lp, int D,
+                                                        LayerTable sel) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long n = (long)kL * Lp * D;
+  if (idx >= n) return;
+  const int o = (int)(idx / ((long)Lp * D)), m = (int)(idx / D % Lp);
+  if (sel.v[m] > o / L) W[idx] = (T)0.f;
+}
+
+template <typename T>
+void launch_grad_mask(T* W, int kL, int L, int Lp, int D, const LayerTable& sel, hipStream_t s) {
+  const long n = (long)kL * Lp * D;
+  if (n <= 0) return;
+  hipLaunchKernelGGL(grad_mask_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, W,
+                     kL, L, Lp, D, sel);
+}
+template void launch_grad_mask<bf16>(bf16*, int, int, int, int, const LayerTable&, hipStream_t);
+template void launch_grad_mask<float>(float*, int, int, int, int, const LayerTable&, hipStream_t);
+
+}  // namespace wm

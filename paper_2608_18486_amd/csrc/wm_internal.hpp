@@ -128,7 +128,80 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
                             const ChannelGroups& groups, const bf16* Q, const bf16* Kc,
                             const bf16* Vc, const bf16* Kd, const bf16* Vd, const bf16* O,
                             const bf16* dO, const int32_t* ctx_len, float* dQ, float* dKc,
-                            float* dVc, float* dKd, float* dVd, float* rows, hipStream_t s);
+                            float* dVc, float* dKd, float* dVd, float* rows, hipStream_t s,
+                            bool accumulate = false);
+
+// -- gradients of the pool and the queries (wm_grad.hip) ----------------------
+// Operand element (row, k) of batch z at p + z s_z + row s_row + k s_k (bf16 or fp32).
+struct GemmOperand {
+  const void* p;
+  long s_row, s_k, s_z;
+  int f32;
+  int vec;  // set by launch_grad_gemm
+};
+// C[z][m][n] (+)= sum_k A(m, k) B(n, k) over batches z; C at C + z c_z + m c_row + n c_col.
+// Batch z uses only k >= k_lo0 + k_lo_dz z of B and stores only rows m >= m_lo0 + m_lo_dz z
+// (the no-feedback router's triangular weights); zero both for a plain GEMM.
+struct GemmArgs {
+  GemmOperand A, B;
+  float* C;
+  long c_row, c_col, c_z;
+  int M, N, K, accumulate;
+  long k_lo0, k_lo_dz, m_lo0, m_lo_dz;
+};
+void launch_grad_gemm(GemmArgs a, int batches, hipStream_t s);
+// out[r] = g[(r / gdiv) % gmod] * x[r] * rinv[r] (bf16 rows of D)
+void launch_grad_norm_apply(const bf16* x, const bf16* g, const float* rinv, long rows, long gdiv,
+                            int gmod, int D, bf16* out, hipStream_t s);
+struct HeadArgs {
+  const float* src;       // rotated output's gradient, rows of d at (z sZ + b sB + h sH + slot)
+  long sZ, sB, sH;
+  int slot_ctx;           // slot = ctx_len[b] + i (cache layout) or i
+  const int32_t* ctx_len;
+  int ctx_hi;
+  const float* y;         // pre-norm values [Z][B T][H d]
+  float* dy;              // their gradient, same layout
+  const bf16* g;          // [Z][d]
+  const float* tab;       // RoPE table [B T][d / 2] (cos, sin)
+  float* dgp;             // gain gradient partials [Z][chunks][d]
+  int B, H, T, chunks;
+  float eps;
+};
+void launch_grad_head(const HeadArgs& a, int Z, int d, hipStream_t s);
+struct RmsArgs {           // rows (o, i); offsets in rows of D
+  const float* dy;
+  long dy_o, dy_i;
+  const bf16* x;
+  long x_o, x_i;
+  float* out;
+  long out_o, out_i;
+  const float* rinv;       // per row, at o r_o + i r_i
+  long r_o, r_i;
+  const bf16* g;           // [nouter][D]
+  float* dgp;              // [nouter][chunks][D]
+  int D, ninner, chunks, accumulate;
+};
+void launch_grad_rms(const RmsArgs& a, int nouter, hipStream_t s);
+// out[o][e] (+)= scale * sum_c part[(o chunks + c) n + e]
+void launch_grad_sum(const float* part, int outer, int chunks, long n, float* out, float scale,
+                     int accumulate, hipStream_t s);
+void launch_grad_colsum(const float* x, long rows, int n, int chunks, float* part, hipStream_t s);
+void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,
+                        const int32_t* ctx_len, int ctx_hi, float* dst, hipStream_t s);
+struct MixGradArgs {
+  const bf16* H;           // [N][L][D] states
+  const bf16* g;           // [L][D] the branch's pre-mix gains
+  const float* rinv;       // [N][L] 1 / rms of each state
+  const float* dmix;       // [k][N][D] gradient of that branch's mixed channels
+  const float* alpha;      // [N][k][L] final mixing weights
+  float* dhn;              // [N][L][D]
+  float* dlog;             // [N][k L] gradient of the router logits
+  int N, L, k, D, softmax, nofeedback;
+};
+size_t grad_mix_smem(int L, int k, int D);
+void launch_grad_mix(const MixGradArgs& a, hipStream_t s);
+template <typename T>
+void launch_grad_mask(T* W, int kL, int L, int Lp, int D, const LayerTable& sel, hipStream_t s);
 
 // Split-S decode for small T_new; partials live in the workspace.
 size_t decode_partials_bytes(const Shape& sh);

@@ -283,3 +283,29 @@ def test_attention_backward_rejects_unsupported_calls_before_launch(wm):
     # four floats per query row of workspace
     d = _dims(wm, d=64)
     assert wm.workspace_size(d, wm.OP_ATTEND_BACKWARD) >= 16 * d.L * d.B * d.Hq * d.T_new
+
+
+def test_step_gradients_reject_unsupported_calls_before_launch(wm):
+    """The queries', pool's and step's gradients: bf16, head dims 64 and 96, contiguous
+    tokens, D <= 4608, the step's only with T_new > 4; NULL parameters or gradient pointers
+    are refused on the host."""
+    def code(fn, *args, **kw):
+        with pytest.raises(wm.WMError) as e:
+            fn(_dims(wm, **kw), *args)
+        return e.value.code
+
+    q = (None, None, None, None, None, None)
+    p = (None, None, None, None, None, None, None)
+    s = (None, None, [0, 1, 0, 1], None, None, None, None, None, None, None, None, None)
+    for fn, args in ((wm.q_project_backward, q), (wm.pool_backward, p),
+                     (wm.layer_step_backward, s)):
+        assert code(fn, *args, d=64, dtype=wm.F32) == wm.ERR_DTYPE
+        assert code(fn, *args, d=32) == wm.ERR_SHAPE
+        assert code(fn, *args, d=64, groups=2) == wm.ERR_ARG
+        assert code(fn, *args, d=64) == wm.ERR_ARG  # params NULL
+    assert code(wm.layer_step_backward, *s, d=64, T_new=4) == wm.ERR_SHAPE
+    # the workspace grows with the tokens and holds at least the recomputed queries
+    d = _dims(wm, d=64)
+    for op in (wm.OP_Q_BACKWARD, wm.OP_POOL_BACKWARD, wm.OP_STEP_BACKWARD):
+        assert wm.workspace_size(d, op) > 0
+    assert wm.workspace_size(d, wm.OP_STEP_BACKWARD) >= 6 * d.L * d.B * d.Hq * d.T_new * d.d

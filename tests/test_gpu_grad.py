@@ -1,0 +1,178 @@
+"""GPU parity of the step's remaining gradients against the gradient oracle: the queries'
+backward (wm_q_project_backward), the pool's backward (wm_pool_backward) and the whole
+step's backward (wm_layer_step_backward), element by element on small shapes that span
+several GEMM tiles and a ragged tail. The entry points add into their outputs: every test
+starts the outputs at seeded nonzero values and compares the difference."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import backward as ob
+from tests import synth
+from tests.parity import TOL_BF16_REL, _bias, _dev, _f64, _gdims, _odims, check_close, wm  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+F32 = dict(dtype=torch.float32, device="cuda")
+
+
+def _grads_like(P, names, seed):
+    """Seeded nonzero starting values for the gradients (the calls add into them)."""
+    return {n: synth._normal(tuple(P[n].shape), 0.5, seed + i, torch.float32).cuda()
+            for i, n in enumerate(names)}
+
+
+def _chain_slack(ref):
+    """The step's gradients pass through two bf16 stages in a row (the attention gradients,
+    then the projections' and norms' gradients of their result), each within the bf16
+    bound on its own: the per-element floor of the bound, TOL rms(ref), is doubled."""
+    return TOL_BF16_REL * float(np.sqrt(np.mean(np.square(ref))))
+
+
+def _check_grads(name, g_gpu, g_start, ref, names, chain=False):
+    for n in names:
+        got = (g_gpu[n] - g_start[n]).cpu()
+        r = ref["d" + n]
+        check_close(got, r, "bf16", "%s d%s" % (name, n), slack=_chain_slack(r) if chain else None)
+
+
+def _workload(name, d, Hq, Hkv, T_new, ctx, L=5, k=3, D=160, p=1):
+    return synth.small(name, B=2, T_new=T_new, L=L, k=k, D=D, Hq=Hq, Hkv=Hkv, d=d,
+                       ctx=ctx + T_new, dtype="bf16", p=p)
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(64, 4, 2), (96, 3, 3)])
+@pytest.mark.parametrize("T_new,ctx", [(150, 0), (37, 90)])
+def test_q_project_backward(wm, d, Hq, Hkv, T_new, ctx):
+    w = _workload("qb_d%d" % d, d, Hq, Hkv, T_new, ctx)
+    print("q backward d%d %d/%d T%d ctx%d" % (d, Hq, Hkv, T_new, ctx), flush=True)
+    P = synth.make_params(w, _bias(w), gains="random")
+    H = synth.make_states(w)
+    ctx_len = torch.tensor([ctx, ctx // 3], dtype=torch.int32)
+    dQ = synth._normal((w.L, w.B, w.Hq, w.T_new, w.d), 1.0, 501, torch.float32)
+    ref = ob.q_project_grads(_odims(w), P, H, dQ.double().numpy(), ctx_len.numpy())
+    dH0 = synth._normal(tuple(H.shape), 1.0, 502, torch.float32).cuda()
+    dH = dH0.clone()
+    g0 = _grads_like(P, ob.QUERY_PARAMS, 503)
+    g = {n: t.clone() for n, t in g0.items()}
+    dims = _gdims(wm, w, ctx_max=ctx)
+    wm.q_project_backward(dims, _dev(P), H.cuda(), ctx_len.cuda(), dQ.cuda(), dH, g)
+    torch.cuda.synchronize()
+    check_close((dH - dH0).cpu(), ref["dH"], "bf16", "dH")
+    _check_grads("q", g, g0, ref, ob.QUERY_PARAMS)
+
+
+POOL_CASES = [
+    dict(),
+    dict(mix_mode=1),
+    dict(p=2, L=6, k=4),
+    dict(router_mode=2, L=4, k=4),
+    dict(router_mode=2, L=4, k=4, mix_mode=1),
+    dict(router_mode=1),
+    dict(d=96, Hq=3, Hkv=3, k=2),
+]
+
+
+@pytest.mark.parametrize("case", range(len(POOL_CASES)))
+@pytest.mark.parametrize("T_new,ctx", [(150, 0), (37, 90)])
+def test_pool_backward(wm, case, T_new, ctx):
+    kw = dict(POOL_CASES[case])
+    modes = {m: kw.pop(m) for m in ("mix_mode", "router_mode") if m in kw}
+    shape = dict(d=64, Hq=4, Hkv=2)
+    shape.update(kw)
+    w = _workload("pb%d" % case, T_new=T_new, ctx=ctx, **shape)
+    print("pool backward case %d %s T%d ctx%d" % (case, modes, T_new, ctx), flush=True)
+    bias = _bias(w)
+    if modes.get("router_mode") == 2:
+        # the default bias puts channel j on layer j + 1, a source the no-feedback router may
+        # not mix; that leaves channel 0 with a router-only weight near zero and its mid norm
+        # near its singular point, where any rounding of the mixed channel is amplified by
+        # 1 / rms. Here channel j starts on layer j instead, and the router's weights are
+        # scaled down so that its logits (std ~0.5 at this width) keep the single-source
+        # weight of channel 0 away from zero in the linear mix.
+        bias = np.eye(w.k, w.L).reshape(-1)
+    P = synth.make_params(w, bias, gains="random")
+    if modes.get("router_mode") == 2:
+        P["W_alpha"] = (P["W_alpha"].float() * 0.1).to(torch.bfloat16)
+    H = synth.make_states(w)
+    ctx_len = torch.tensor([ctx, ctx // 3], dtype=torch.int32)
+    dK = synth._normal((w.k, w.B, w.Hkv, w.T_new, w.d), 1.0, 601, torch.float32)
+    dV = synth._normal((w.k, w.B, w.Hkv, w.T_new, w.d), 1.0, 602, torch.float32)
+    od = _odims(w, **modes)
+    ref = ob.pool_grads(od, P, H, dK.double().numpy(), dV.double().numpy(), ctx_len.numpy())
+    # the cache-layout gradients hold the rows at the new slots, NaN elsewhere (never read)
+    shape_c = (w.k, w.B, w.Hkv, w.S_cap, w.d)
+    dKc = torch.full(shape_c, float("nan"), dtype=torch.float32)
+    dVc = dKc.clone()
+    for b, c0 in enumerate(ctx_len.tolist()):
+        dKc[:, b, :, c0:c0 + w.T_new] = dK[:, b]
+        dVc[:, b, :, c0:c0 + w.T_new] = dV[:, b]
+    names = [n for n in ob.POOL_PARAMS if not (n == "W_alpha" and modes.get("router_mode") == 1)]
+    dH0 = synth._normal(tuple(H.shape), 1.0, 603, torch.float32).cuda()
+    dH = dH0.clone()
+    g0 = _grads_like(P, names, 604)
+    g = {n: t.clone() for n, t in g0.items()}
+    dims = _gdims(wm, w, ctx_max=ctx, **modes)
+    wm.pool_backward(dims, _dev(P), H.cuda(), ctx_len.cuda(), dKc.cuda(), dVc.cuda(), dH, g)
+    torch.cuda.synchronize()
+    check_close((dH - dH0).cpu(), ref["dH"], "bf16", "dH")
+    _check_grads("pool", g, g0, ref, names)
+    if modes.get("router_mode") == 2:
+        # without feedback, router rows never read a source above their channel: untouched
+        Wg = (g["W_alpha"] - g0["W_alpha"]).cpu().numpy().reshape(2, w.k * w.L, -1, w.D)
+        sel = [w.L - 1 - w.p * m for m in range((w.L + w.p - 1) // w.p)][::-1]
+        for o in range(w.k * w.L):
+            for m, l in enumerate(sel):
+                if l > o // w.L:
+                    assert not np.any(Wg[:, o, m]), (o, m)
+
+
+@pytest.mark.parametrize("mask_mode", [0, 1])
+@pytest.mark.parametrize("d,Hq,Hkv", [(64, 4, 2), (96, 6, 3)])
+@pytest.mark.parametrize("T_new,ctx", [(150, 0), (70, 60)])
+def test_layer_step_backward(wm, mask_mode, d, Hq, Hkv, T_new, ctx):
+    """The whole step: forward on the GPU (its caches and output), then the backward with a
+    gradient already on the new slots; every gradient against the oracle's autograd of
+    the step."""
+    w = synth.small("sb_d%d" % d, B=2, T_new=T_new, L=5, k=3, D=128, Hq=Hq, Hkv=Hkv, d=d,
+                    ctx=ctx + T_new, dtype="bf16", chan_map=[2, 0, 2, 1, 0])
+    print("step backward d%d %d/%d T%d ctx%d mask%d" % (d, Hq, Hkv, T_new, ctx, mask_mode),
+          flush=True)
+    P = synth.make_params(w, _bias(w), gains="random")
+    H = synth.make_states(w)
+    ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+    Kc, Vc = synth.make_cache_cpu(w)
+    dO = synth._normal((w.L, w.B, w.T_new, w.Hq * w.d), 1.0, 701, torch.bfloat16)
+    dKe = synth._normal((w.k, w.B, w.Hkv, w.T_new, w.d), 0.3, 702, torch.float32)
+    dVe = synth._normal((w.k, w.B, w.Hkv, w.T_new, w.d), 0.3, 703, torch.float32)
+    od = _odims(w, mask_mode=mask_mode)
+    ref = ob.layer_step_grads(od, P, H, w.chan_map, _f64(dO), ctx_len.numpy(), _f64(Kc),
+                              _f64(Vc), dKe.double().numpy(), dVe.double().numpy())
+
+    dims = _gdims(wm, w, ctx_max=ctx, mask_mode=mask_mode)
+    Pd, Hd, cl = _dev(P), H.cuda(), ctx_len.cuda()
+    Kd_, Vd_ = Kc.cuda(), Vc.cuda()
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=torch.bfloat16, device="cuda")
+    wm.layer_step(dims, Pd, Hd, w.chan_map, cl, Kd_, Vd_, O)
+    dKc = torch.zeros(tuple(Kc.shape), **F32)
+    dVc = torch.zeros(tuple(Kc.shape), **F32)
+    for b, c0 in enumerate(ctx_len.tolist()):
+        dKc[:, b, :, c0:c0 + w.T_new] = dKe[:, b].cuda()
+        dVc[:, b, :, c0:c0 + w.T_new] = dVe[:, b].cuda()
+    names = list(ob.POOL_PARAMS) + list(ob.QUERY_PARAMS) + (["Kd", "Vd"] if mask_mode == 0
+                                                            else [])
+    dH0 = synth._normal(tuple(H.shape), 1.0, 704, torch.float32).cuda()
+    dH = dH0.clone()
+    g0 = _grads_like(P, names, 705)
+    g = {n: t.clone() for n, t in g0.items()}
+    wm.layer_step_backward(dims, Pd, Hd, w.chan_map, cl, Kd_, Vd_, O, dO.cuda(), dKc, dVc, dH, g)
+    torch.cuda.synchronize()
+    check_close((dH - dH0).cpu(), ref["dH"], "bf16", "dH", slack=_chain_slack(ref["dH"]))
+    _check_grads("step", g, g0, ref, names, chain=True)
+    dKc_h, dVc_h = dKc.cpu().numpy(), dVc.cpu().numpy()
+    for b, c0 in enumerate(ctx_len.tolist()):
+        if c0:  # one stage: the attention gradients alone
+            check_close(dKc_h[:, b, :, :c0], ref["dKc_ctx"][:, b, :, :c0], "bf16", "dKc ctx b%d" % b)
+            check_close(dVc_h[:, b, :, :c0], ref["dVc_ctx"][:, b, :, :c0], "bf16", "dVc ctx b%d" % b)
+        # slots past the call's span are never written
+        assert not np.any(dKc_h[:, b, :, c0 + w.T_new:]) and not np.any(dVc_h[:, b, :, c0 + w.T_new:])

@@ -217,3 +217,100 @@ def test_attention_gradients_closed_forms():
         w = (Vc[0, b, 0, :n] @ dO[0, b, 0] - o @ dO[0, b, 0]) / n
         want = (w[:, None] * Kc[0, b, 0, :n]).sum(0) / np.sqrt(dm.d)
         assert np.allclose(g["dQ"][0, b, 0, 0], want, atol=1e-13)
+
+
+# ------------------------------------------------------- the step's parts alone
+
+@pytest.mark.parametrize("kw", CASES)
+def test_pool_gradients_match_finite_differences(kw):
+    """pool_grads against central differences of the C oracle's pool rows (wmo_pool_rows)."""
+    dm = _dims(**kw)
+    ctxs = (2, 5)
+    P = _params(dm, seed=11)
+    rng = np.random.default_rng(12)
+    H = rng.standard_normal((dm.B, dm.T_new, dm.L, dm.D))
+    dK = rng.standard_normal((dm.k, dm.B, dm.Hkv, dm.T_new, dm.d))
+    dV = rng.standard_normal((dm.k, dm.B, dm.Hkv, dm.T_new, dm.d))
+    g = ob.pool_grads(dm, P, H, dK, dV, ctxs)
+
+    def rows(x):  # [N, k, Hkv, d] -> [k, B, Hkv, T, d]
+        return x.reshape(dm.B, dm.T_new, dm.k, dm.Hkv, dm.d).transpose(2, 0, 3, 1, 4)
+
+    def loss(Hx, Px):
+        K, V = oracle.pool_rows(dm, Px, Hx, ctxs)
+        return (rows(K) * dK).sum() + (rows(V) * dV).sum()
+
+    checks = [("dH", lambda x: loss(x, P), H)]
+    for n in ob.POOL_PARAMS:
+        checks.append(("d" + n, lambda x, n=n: loss(H, {**P, n: x}), P[n]))
+    for name, f, x in checks:
+        v = rng.standard_normal(x.shape)
+        # a small step: without feedback, channel 0 mixes one source with a signed weight
+        # that can sit near zero, where the mid norm's curvature is large
+        num = _fd(f, x, v, eps=2e-5)
+        ana = (g[name] * v).sum()
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(num)), (name, num, ana)
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(Hq=2, Hkv=1, d=16), dict(L=2, k=1)])
+def test_query_gradients_match_finite_differences(kw):
+    """q_project_grads against central differences of the C oracle's queries."""
+    dm = _dims(**kw)
+    ctxs = (0, 7)
+    P = _params(dm, seed=13)
+    rng = np.random.default_rng(14)
+    H = rng.standard_normal((dm.B, dm.T_new, dm.L, dm.D))
+    dQ = rng.standard_normal((dm.L, dm.B, dm.Hq, dm.T_new, dm.d))
+    g = ob.q_project_grads(dm, P, H, dQ, ctxs)
+
+    def loss(Hx, Px):
+        return (oracle.q_project(dm, Px, Hx, ctxs) * dQ).sum()
+
+    checks = [("dH", lambda x: loss(x, P), H)]
+    for n in ob.QUERY_PARAMS:
+        checks.append(("d" + n, lambda x, n=n: loss(H, {**P, n: x}), P[n]))
+    for name, f, x in checks:
+        v = rng.standard_normal(x.shape)
+        num = _fd(f, x, v)
+        ana = (g[name] * v).sum()
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(num)), (name, num, ana)
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(mask_mode=oracle.MASK_INCLUSIVE),
+                                dict(router_mode=oracle.ROUTER_NOFEEDBACK, L=3, k=3)])
+def test_step_gradient_is_the_sum_of_its_parts(kw):
+    """The decomposition the GPU step's backward runs: attention gradients first, then the
+    queries' backward of dQ and the pool's backward of the new slots' total gradient (the
+    attention's plus what reaches them from elsewhere). The parts' sum equals the whole
+    step's gradient (computed as one autograd graph)."""
+    dm = _dims(**kw)
+    ctxs = (3, 1)
+    dm.S_cap = max(ctxs) + dm.T_new + 1
+    P = _params(dm, seed=15)
+    rng = np.random.default_rng(16)
+    H = rng.standard_normal((dm.B, dm.T_new, dm.L, dm.D))
+    cmap = [(l + 1) % dm.k for l in range(dm.L)]
+    Kc, Vc = _cache(dm, ctxs)
+    dO = rng.standard_normal((dm.L, dm.B, dm.T_new, dm.Hq * dm.d))
+    dKe = rng.standard_normal((dm.k, dm.B, dm.Hkv, dm.T_new, dm.d))
+    dVe = rng.standard_normal((dm.k, dm.B, dm.Hkv, dm.T_new, dm.d))
+    whole = ob.layer_step_grads(dm, P, H, cmap, dO, ctxs, Kc, Vc, dKe, dVe)
+    _, K, V = _c_step(dm, P, H, cmap, ctxs, Kc, Vc)
+    K, V = np.nan_to_num(K), np.nan_to_num(V)
+    Q = oracle.q_project(dm, P, H, ctxs)
+    ga = ob.channel_attend_grads(dm, P, Q, cmap, ctxs, K, V, dO)
+    gq = ob.q_project_grads(dm, P, H, ga["dQ"], ctxs)
+    gp = ob.pool_grads(dm, P, H, dKe + ob.new_rows(dm, ga["dKc"], ctxs),
+                       dVe + ob.new_rows(dm, ga["dVc"], ctxs), ctxs)
+    tol = 1e-10
+    assert np.abs(gq["dH"] + gp["dH"] - whole["dH"]).max() < tol
+    for n in ob.QUERY_PARAMS:
+        assert np.abs(gq["d" + n] - whole["d" + n]).max() < tol, n
+    for n in ob.POOL_PARAMS:
+        assert np.abs(gp["d" + n] - whole["d" + n]).max() < tol, n
+    assert np.abs(ga["dKd"] - whole["dKd"]).max() < tol
+    assert np.abs(ga["dVd"] - whole["dVd"]).max() < tol
+    for b in range(dm.B):
+        c0 = ctxs[b]
+        assert np.abs(ga["dKc"][:, b, :, :c0] - whole["dKc_ctx"][:, b, :, :c0]).max() < tol
+        assert np.abs(ga["dVc"][:, b, :, :c0] - whole["dVc_ctx"][:, b, :, :c0]).max() < tol
