@@ -501,6 +501,74 @@ def attend_backward_bench(wm, torch, np, synth, hip, dev, stream, log, w, reps=5
             "executed_gflop": round(flops * 16 / 10 / 1e9, 1), "reps": reps}
 
 
+def step_backward_bench(wm, torch, np, synth, hip, dev, stream, log, w, reps=3):
+    """The whole step's gradients for the headline pass (wm_layer_step_backward: the
+    queries recomputed, the attention gradients, then the queries' and the pool's
+    backward), plus the queries' and the pool's backward alone, event-timed, from the
+    forward step's own caches and output. GFLOP count the MFMA products the backward
+    executes outside the attention: recomputed pre-norm projections, dX = dY W and
+    dW = dY^T X for W^Q, W^K (three each), W^V (two), and the router's forward and its two
+    gradient products per branch."""
+    log("bench: step gradients %s" % w.name)
+    P = wm.ParamSet({k: v.to(dev) for k, v in
+                     synth.make_params(w, np.asarray(wm.init_bias(w.L, w.k)),
+                                       gains="random").items()})
+    bf = torch.bfloat16
+    f32 = dict(dtype=torch.float32, device=dev)
+    H = synth.make_states(w).to(dev)
+    dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p, S_cap=w.T_new,
+                        ctx_max=0, dtype=wm.BF16)
+    shape = (w.k, w.B, w.Hkv, w.T_new, w.d)
+    Kc = torch.empty(shape, dtype=bf, device=dev)
+    Vc = torch.empty(shape, dtype=bf, device=dev)
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=bf, device=dev)
+    wm.layer_step(dims, P, H, w.chan_map, None, Kc, Vc, O, stream=stream)
+    dO = synth._normal(tuple(O.shape), 1.0, 9201, bf).to(dev)
+    dKc, dVc = torch.zeros(shape, **f32), torch.zeros(shape, **f32)
+    dH = torch.zeros(tuple(H.shape), **f32)
+    grads = {n: torch.zeros(tuple(P.tensors[n].shape), **f32) for n in wm.PARAM_NAMES}
+    dQ = synth._normal((w.L, w.B, w.Hq, w.T_new, w.d), 1.0, 9202, torch.float32).to(dev)
+    calls = {
+        "step": (wm.OP_STEP_BACKWARD, lambda ws: wm.layer_step_backward(
+            dims, P, H, w.chan_map, None, Kc, Vc, O, dO, dKc, dVc, dH, grads, ws=ws,
+            stream=stream)),
+        "queries": (wm.OP_Q_BACKWARD, lambda ws: wm.q_project_backward(
+            dims, P, H, None, dQ, dH, grads, ws=ws, stream=stream)),
+        "pool": (wm.OP_POOL_BACKWARD, lambda ws: wm.pool_backward(
+            dims, P, H, None, dKc, dVc, dH, grads, ws=ws, stream=stream)),
+    }
+    out = {"workload": WORKLOAD_LABEL[w.name], "reps": reps}
+    for name, (op, fn) in calls.items():
+        ws = wm.workspace(dims, op, dev)
+        fn(ws)
+        torch.cuda.synchronize()
+        ev = [hip.create() for _ in range(reps + 1)]
+        hip.record(ev[0], stream.cuda_stream)
+        for r in range(reps):
+            fn(ws)
+            hip.record(ev[r + 1], stream.cuda_stream)
+        torch.cuda.synchronize()
+        out[name + "_ms_median"] = round(float(np.median(
+            [hip.elapsed_ms(ev[r], ev[r + 1]) for r in range(reps)])), 4)
+        for e in ev:
+            hip.destroy(e)
+        del ws
+        torch.cuda.empty_cache()
+    N, HQ, HK, kL, Lp = w.N, w.Hq * w.d, w.Hkv * w.d, w.k * w.L, (w.L + w.p - 1) // w.p
+    q_gf = 3 * 2.0 * N * w.L * HQ * w.D
+    kv_gf = 5 * 2.0 * N * w.k * HK * w.D
+    r_gf = 3 * 2 * 2.0 * N * kL * Lp * w.D
+    out["queries_gflop"] = round(q_gf / 1e9, 1)
+    out["pool_gflop"] = round((kv_gf + r_gf) / 1e9, 1)
+    out["queries_tflops"] = round(q_gf / (out["queries_ms_median"] * 1e-3) / 1e12, 1)
+    out["pool_tflops"] = round((kv_gf + r_gf) / (out["pool_ms_median"] * 1e-3) / 1e12, 1)
+    log("bench: step gradients %.3f ms (queries %.3f ms, pool %.3f ms)"
+        % (out["step_ms_median"], out["queries_ms_median"], out["pool_ms_median"]))
+    del H, Kc, Vc, O, dO, dKc, dVc, dH, grads, dQ, P
+    torch.cuda.empty_cache()
+    return out
+
+
 def passes_bench(wm, torch, np, synth, hip, dev, stream, log, groups=("8", "16", "1", "T")):
     """The fixed-point passes of Section 3.3 at the paper's model shape (B16 T2048 L16 k8
     D512, 6 query / 3 KV heads of 96, p = 2, bf16) with the stand-in decoder block:
@@ -736,6 +804,8 @@ def main():
         torch.cuda.empty_cache()
         line["attention_backward"] = attend_backward_bench(wm, torch, np, synth, hip, dev,
                                                            stream, log, w)
+        line["step_backward"] = step_backward_bench(wm, torch, np, synth, hip, dev, stream,
+                                                    log, w)
     if not args.no_passes:
         torch.cuda.empty_cache()
         line["prefill_passes"] = passes_bench(wm, torch, np, synth, hip, dev, stream, log,

@@ -46,8 +46,8 @@ struct Layout {
   // gradients: dQ, gain partial rows, dummy scratch, the Q side's normed input, pre-norm
   // projection and its gradient, the pool side's normed states, mid-normed channels,
   // K/V pre-norm values and gradients, channel gradients, state gradients, logit gradients
-  size_t dq = 0, dgp = 0, gkd = 0, x = 0, yq = 0, dx = 0, hn = 0, u = 0, ydy = 0, du = 0,
-         dhn = 0, dlog = 0;
+  size_t dq = 0, dgp = 0, gkd = 0, x = 0, yq = 0, dyq = 0, dx = 0, hn = 0, u = 0, ydy = 0,
+         dyb = 0, du = 0, dhn = 0, dlog = 0, dlogb = 0;
 };
 
 int group_stride(const wm_dims& d) { return d.groups > 1 ? d.groups : 1; }
@@ -138,6 +138,7 @@ Layout grad_layout(const wm_dims& d, int op) {
   if (op == WM_OP_Q_BACKWARD || op == WM_OP_STEP_BACKWARD) {
     Ly.x = take(N * L * D * 2);
     Ly.yq = take(L * N * HQ * 4);
+    Ly.dyq = take(L * N * HQ * 2);
     Ly.dx = take(N * L * D * 4);
     end = std::max(end, off);
     off = base;
@@ -151,9 +152,11 @@ Layout grad_layout(const wm_dims& d, int op) {
     Ly.hn = take(N * L * D * 2);
     Ly.u = take(k * N * D * 2);
     Ly.ydy = take(k * N * HK * 4);
+    Ly.dyb = take(k * N * HK * 2);
     Ly.du = take(k * N * D * 4);
     Ly.dhn = take(N * L * D * 4);
     Ly.dlog = take(N * k * L * 4);
+    Ly.dlogb = take(N * ((k * L + 7) & ~(size_t)7) * 2);
     end = std::max(end, off);
   }
   Ly.total = N == 0 ? 0 : end;
@@ -619,8 +622,8 @@ int static_scratch(void** out) {
 
 
 // ------------------------------------------------------------------ gradients
-wm::GemmOperand opnd(const void* p, long s_row, long s_k, long s_z, bool f32) {
-  return wm::GemmOperand{p, s_row, s_k, s_z, f32 ? 1 : 0, 0};
+wm::GemmOperand opnd(const void* p, long s_row, long s_k, long s_z, bool f32, bool pad8 = false) {
+  return wm::GemmOperand{p, s_row, s_k, s_z, f32 ? 1 : 0, pad8 ? 1 : 0};
 }
 
 // C[z] (+)= A[z] B[z]^T over `batches`; see GemmArgs for the k / row limits.
@@ -677,6 +680,7 @@ void run_q_backward(const wm_dims& d, const wm_params& P, const bf16* H, const i
   float* dgp = (float*)at(ws, Ly.dgp);
   bf16* x = (bf16*)at(ws, Ly.x);
   float* yq = (float*)at(ws, Ly.yq);
+  bf16* dyq = (bf16*)at(ws, Ly.dyq);
   float* dx = (float*)at(ws, Ly.dx);
   const bf16* Wq = (const bf16*)P.Wq;
   wm::launch_row_rms<bf16>(H, (long)N * L, D, sh.eps, rinv, s);
@@ -685,18 +689,18 @@ void run_q_backward(const wm_dims& d, const wm_params& P, const bf16* H, const i
   wm::launch_grad_norm_apply(H, (const bf16*)P.g_in, rinv, (long)N * L, 1, L, D, x, s);
   gemm(opnd(x, (long)L * D, 1, D, false), opnd(Wq, D, 1, (long)HQ * D, false), yq, HQ, 1,
        (long)N * HQ, N, HQ, D, L, false, s);
-  // RoPE and q norm backward: y's gradient in place
+  // RoPE and q norm backward: y's gradient (bf16)
   wm::HeadArgs h{};
   h.src = dQ, h.sZ = (long)d.B * d.Hq * d.T_new, h.sB = (long)d.Hq * d.T_new, h.sH = d.T_new;
   h.slot_ctx = 0, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
-  h.y = yq, h.dy = yq, h.g = (const bf16*)P.g_qnorm, h.tab = tab, h.dgp = dgp;
+  h.y = yq, h.dy = dyq, h.g = (const bf16*)P.g_qnorm, h.tab = tab, h.dgp = dgp;
   h.B = d.B, h.H = d.Hq, h.T = d.T_new, h.chunks = kGradChunks, h.eps = d.eps;
   wm::launch_grad_head(h, L, d.d, s);
   wm::launch_grad_sum(dgp, L, kGradChunks, d.d, G.g_qnorm, 1.f, 1, s);
   // dx_l = dy_l Wq_l [N][D] (into [N][L][D]); dWq_l += dy_l^T x_l [HQ][D]
-  gemm(opnd(yq, HQ, 1, (long)N * HQ, true), opnd(Wq, 1, D, (long)HQ * D, false), dx,
+  gemm(opnd(dyq, HQ, 1, (long)N * HQ, false), opnd(Wq, 1, D, (long)HQ * D, false), dx,
        (long)L * D, 1, D, N, D, HQ, L, false, s);
-  gemm(opnd(yq, 1, HQ, (long)N * HQ, true), opnd(x, 1, (long)L * D, D, false), G.Wq, D, 1,
+  gemm(opnd(dyq, 1, HQ, (long)N * HQ, false), opnd(x, 1, (long)L * D, D, false), G.Wq, D, 1,
        (long)HQ * D, HQ, D, N, L, true, s);
   // input norm backward: rows (l, n) at n L + l
   rms_backward(dx, 1, L, H, 1, L, dH, 1, L, rinv, 1, L, (const bf16*)P.g_in, D, L, N, true, dgp,
@@ -723,9 +727,12 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
   bf16* hn = (bf16*)at(ws, Ly.hn);
   bf16* u = (bf16*)at(ws, Ly.u);
   float* ydy = (float*)at(ws, Ly.ydy);
+  bf16* dyb = (bf16*)at(ws, Ly.dyb);
   float* du = (float*)at(ws, Ly.du);
   float* dhn = (float*)at(ws, Ly.dhn);
   float* dlog = (float*)at(ws, Ly.dlog);
+  bf16* dlogb = (bf16*)at(ws, Ly.dlogb);
+  const int kLp = (kL + 7) & ~7;
   const wm::LayerTable sel = router_layers(d);
   const bool dynamic = d.router_mode != WM_ROUTER_STATIC;
   const bool nofb = d.router_mode == WM_ROUTER_NOFEEDBACK;
@@ -744,31 +751,31 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
     // u_j = g_mid[j] mixed_j / rms (bf16 [k][N][D])
     wm::launch_grad_norm_apply(mix_b, gmid, rmid, (long)k * N, N, k, D, u, s);
     if (br == 0) {
-      // y_j = u_j Wk_j^T [N][HK], then RoPE and key norm backward (y's gradient in place)
+      // y_j = u_j Wk_j^T [N][HK], then RoPE and key norm backward (y's gradient, bf16)
       gemm(opnd(u, D, 1, (long)N * D, false), opnd(W, D, 1, (long)HK * D, false), ydy, HK, 1,
            (long)N * HK, N, HK, D, k, false, s);
       wm::HeadArgs h{};
       h.src = dKc, h.sZ = (long)d.B * d.Hkv * d.S_cap, h.sB = (long)d.Hkv * d.S_cap;
       h.sH = d.S_cap, h.slot_ctx = 1, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
-      h.y = ydy, h.dy = ydy, h.g = (const bf16*)P.g_knorm, h.tab = tab, h.dgp = dgp;
+      h.y = ydy, h.dy = dyb, h.g = (const bf16*)P.g_knorm, h.tab = tab, h.dgp = dgp;
       h.B = d.B, h.H = d.Hkv, h.T = d.T_new, h.chunks = kGradChunks, h.eps = d.eps;
       wm::launch_grad_head(h, k, d.d, s);
       wm::launch_grad_sum(dgp, k, kGradChunks, d.d, G.g_knorm, 1.f, 1, s);
     } else {
-      wm::launch_grad_gather(dVc, k, d.B, d.Hkv, d.T_new, d.S_cap, d.d, ctx_len, sh.ctx_hi, ydy,
+      wm::launch_grad_gather(dVc, k, d.B, d.Hkv, d.T_new, d.S_cap, d.d, ctx_len, sh.ctx_hi, dyb,
                              s);
     }
     // du_j = dy_j W_j [N][D]; dW_j += dy_j^T u_j [HK][D]
-    gemm(opnd(ydy, HK, 1, (long)N * HK, true), opnd(W, 1, D, (long)HK * D, false), du, D, 1,
+    gemm(opnd(dyb, HK, 1, (long)N * HK, false), opnd(W, 1, D, (long)HK * D, false), du, D, 1,
          (long)N * D, N, D, HK, k, false, s);
-    gemm(opnd(ydy, 1, HK, (long)N * HK, true), opnd(u, 1, D, (long)N * D, false),
+    gemm(opnd(dyb, 1, HK, (long)N * HK, false), opnd(u, 1, D, (long)N * D, false),
          br ? G.Wv : G.Wk, D, 1, (long)HK * D, HK, D, N, k, true, s);
     // mid norm backward in place: du becomes the mixed channels' gradient
     rms_backward(du, N, 1, mix_b, N, 1, du, N, 1, rmid, N, 1, gmid, D, k, N, false, dgp, s);
     wm::launch_grad_sum(dgp, k, kGradChunks, D, G.g_mid + (long)br * k * D, 1.f, 1, s);
     // mix backward: dhn (written) and the logits' gradient
-    wm::MixGradArgs m{H, gpre, rinv, du, alpha + (long)br * N * kL, dhn, dlog, N, L, k, D,
-                      d.mix_mode == WM_MIX_SOFTMAX ? 1 : 0, nofb ? 1 : 0};
+    wm::MixGradArgs m{H, gpre, rinv, du, alpha + (long)br * N * kL, dhn, dlog, dlogb, N, L, k,
+                      D, d.mix_mode == WM_MIX_SOFTMAX ? 1 : 0, nofb ? 1 : 0, kLp};
     wm::launch_grad_mix(m, s);
     wm::launch_grad_colsum(dlog, N, kL, kGradChunks, dgp, s);
     wm::launch_grad_sum(dgp, 1, kGradChunks, kL, G.b_alpha + (long)br * kL, 1.f, 1, s);
@@ -780,9 +787,10 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
       const bf16* Wa = (const bf16*)P.W_alpha + (long)br * kL * Lp * D;
       const long s0 = sel.v[0];
       const long klo0 = nofb ? (long)L * s0 : 0, klo_dz = nofb ? (long)L * d.p : 0;
-      gemm(opnd(dlog, kL, 1, 0, true), opnd(Wa, 1, (long)Lp * D, D, false), dhn + s0 * D,
-           (long)L * D, 1, (long)d.p * D, N, D, kL, Lp, true, s, klo0, klo_dz);
-      gemm(opnd(dlog, 1, kL, 0, true), opnd(hn + s0 * D, 1, (long)L * D, (long)d.p * D, false),
+      gemm(opnd(dlogb, kLp, 1, 0, false, true), opnd(Wa, 1, (long)Lp * D, D, false),
+           dhn + s0 * D, (long)L * D, 1, (long)d.p * D, N, D, kL, Lp, true, s, klo0, klo_dz);
+      gemm(opnd(dlogb, 1, kLp, 0, false, true),
+           opnd(hn + s0 * D, 1, (long)L * D, (long)d.p * D, false),
            G.W_alpha + (long)br * kL * Lp * D, (long)Lp * D, 1, D, kL, D, N, Lp, true, s, 0, 0,
            klo0, klo_dz);
     }

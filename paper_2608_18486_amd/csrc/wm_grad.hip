@@ -24,98 +24,88 @@
 namespace wm {
 
 // ------------------------------------------------------------------------ GEMM
-// 128 x 128 output tiles, 4 waves of 64 x 64, K-steps of 32 staged to LDS as bf16 (the
-// next step's global loads in flight during this step's MFMAs). Each operand is staged in
-// one of two layouts, chosen from its strides:
-//   N (k contiguous in memory): LDS [128 rows][32 k], 64-byte rows with a chunk swizzle;
+// Tiles of BM x BN = (32 WM WGM) x (32 WN WGN) on WGM x WGN waves, each owning WM x WN
+// blocks of 32 x 32, K-steps of 32 staged to LDS as bf16 (the next step's global loads in
+// flight during this step's MFMAs, one barrier per step). 256 x 256 tiles on 8 waves for
+// the large products (128 FLOP per staged byte), 128 x 128 on 4 waves when the large
+// tiles would leave CUs idle. Each operand is staged in one of two layouts, chosen from
+// its strides:
+//   N (k contiguous in memory): LDS [BM rows][32 k], 64-byte rows with a chunk swizzle;
 //     lane (h, r) reads row r, k 16 ks + 8 h .. + 7 as one 16-byte word.
 //   T (rows contiguous, k strided: the transposed operands of dW = dY^T X and dX = dY W):
-//     LDS [32 k][kLdt] (rows padded), filled by 8-row vector loads along the rows; lane
-//     (h, r) gathers the same fragment with two transposing reads (ds_read_b64_tr_b16).
-constexpr int kGT = 256;        // threads per GEMM workgroup
-constexpr int kLdt = 144;       // T layout row pitch in elements (128 + 16: the four k rows
-                                // one 16-lane group reads fall in disjoint banks)
-constexpr int kGTile = 32 * kLdt * 2;  // bytes per staged operand tile (>= 128 * 64)
+//     LDS [32 k][BM + 16], filled by 8-row vector loads along the rows; lane (h, r)
+//     gathers the same fragment with two transposing reads (ds_read_b64_tr_b16).
+// VEC: 16-byte vector loads of bf16 operands (the strides allow them); otherwise element
+// by element (bf16 or fp32), kept out of the vector kernels since it needs many registers.
+template <int WGM_, int WGN_, int WM_, int WN_> struct GemmCfg {
+  static constexpr int WGM = WGM_, WGN = WGN_, WM = WM_, WN = WN_;
+  static constexpr int NT = 64 * WGM * WGN;
+  static constexpr int BM = 32 * WM * WGM, BN = 32 * WN * WGN;
+  static constexpr int VA = BM * 4 / NT, VB = BN * 4 / NT;  // 16-byte chunks per thread
+  static constexpr int LDTA = BM + 16, LDTB = BN + 16;      // T layout pitches (elements)
+  // bytes per staged tile: the larger of the two layouts
+  static constexpr int TA_BYTES = (BM * 64 > 32 * LDTA * 2) ? BM * 64 : 32 * LDTA * 2;
+  static constexpr int TB_BYTES = (BN * 64 > 32 * LDTB * 2) ? BN * 64 : 32 * LDTB * 2;
+};
+typedef GemmCfg<2, 4, 4, 2> GemmBig;    // 256 x 256, 8 waves
+typedef GemmCfg<2, 2, 2, 2> GemmSmall;  // 128 x 128, 4 waves
 
 __device__ __forceinline__ int grad_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
 
-// N layout: this thread's 16 elements (row r, k = k0 + 16 half .. + 15) of the tile;
-// elements with k < klo are zero. VEC: vector loads (the operands' strides allow them);
-// otherwise element by element (kept out of the vector kernels: it needs many registers).
-template <bool VEC>
+// N layout: chunk v of this thread is row idx / 4, k = k0 + 8 (idx % 4) .. + 7 with
+// idx = tid + NT v; elements with k < klo are zero.
+template <int BM, int NT, int V, bool VEC>
 __device__ __forceinline__ void gemm_load_n(const GemmOperand& o, long zoff, int row0, int k0,
-                                            int nrows, int K, int klo, int tid, bf16x8 (&v)[2]) {
-  const int r = tid & 127, half = tid >> 7;
-  const int row = row0 + r, kb = k0 + 16 * half;
-  if constexpr (VEC) {  // k contiguous, rows and batches 8-aligned: two 8-element loads
+                                            int nrows, int K, int klo, int tid, bf16x8 (&v)[V]) {
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      const int k = kb + 8 * g;
-      const bool ok = row < nrows && k < K;  // K is a multiple of 8 on this path
-      if (o.f32) {
-        const float* p = (const float*)o.p + zoff + (long)row * o.s_row + k;
-        f32x4 a = ok ? *(const f32x4*)p : f32x4{0.f, 0.f, 0.f, 0.f};
-        f32x4 b = ok ? *(const f32x4*)(p + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[g][e] = (bf16)a[e];
-          v[g][4 + e] = (bf16)b[e];
-        }
-      } else {
-        const bf16* p = (const bf16*)o.p + zoff + (long)row * o.s_row + k;
-        v[g] = ok ? *(const bf16x8*)p : zero_frag<bf16>();
-      }
+  for (int c = 0; c < V; ++c) {
+    const int idx = tid + NT * c, row = row0 + (idx >> 2), k = k0 + 8 * (idx & 3);
+    if constexpr (VEC) {  // bf16, k contiguous, rows 8-aligned; K rounded up to 8 readable
+      const bool ok = row < nrows && k < K;
+      v[c] = ok ? *(const bf16x8*)((const bf16*)o.p + zoff + (long)row * o.s_row + k)
+                : zero_frag<bf16>();
       if (klo > k) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          if (k + e < klo) v[g][e] = (bf16)0.f;
+          if (k + e < klo) v[c][e] = (bf16)0.f;
       }
-    }
-  } else {
+    } else {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int k = kb + e;
-      float x = 0.f;
-      if (row < nrows && k < K && k >= klo) {
-        const long off = zoff + (long)row * o.s_row + (long)k * o.s_k;
-        x = o.f32 ? ((const float*)o.p)[off] : (float)((const bf16*)o.p)[off];
+      for (int e = 0; e < 8; ++e) {
+        float x = 0.f;
+        if (row < nrows && k + e < K && k + e >= klo) {
+          const long off = zoff + (long)row * o.s_row + (long)(k + e) * o.s_k;
+          x = o.f32 ? ((const float*)o.p)[off] : (float)((const bf16*)o.p)[off];
+        }
+        v[c][e] = (bf16)x;
       }
-      v[e >> 3][e & 7] = (bf16)x;
     }
   }
 }
 
-__device__ __forceinline__ void gemm_store_n(char* tile, int tid, const bf16x8 (&v)[2]) {
-  const int r = tid & 127, half = tid >> 7;
+template <int NT, int V>
+__device__ __forceinline__ void gemm_store_n(char* tile, int tid, const bf16x8 (&v)[V]) {
 #pragma unroll
-  for (int g = 0; g < 2; ++g)
-    *(bf16x8*)(tile + r * 64 + 16 * ((2 * half + g) ^ grad_swz(r))) = v[g];
+  for (int c = 0; c < V; ++c) {
+    const int idx = tid + NT * c, r = idx >> 2;
+    *(bf16x8*)(tile + r * 64 + 16 * ((idx & 3) ^ grad_swz(r))) = v[c];
+  }
 }
 
-// T layout: item g of this thread is k = k0 + idx / 16, rows row0 + 8 (idx % 16) .. + 7
-// with idx = tid + 256 g.
-template <bool VEC>
+// T layout: chunk v of this thread is k = k0 + idx / (BM / 8), rows row0 + 8 (idx % (BM / 8))
+// .. + 7 with idx = tid + NT v.
+template <int BM, int NT, int V, bool VEC>
 __device__ __forceinline__ void gemm_load_t(const GemmOperand& o, long zoff, int row0, int k0,
-                                            int nrows, int K, int klo, int tid, bf16x8 (&v)[2]) {
+                                            int nrows, int K, int klo, int tid, bf16x8 (&v)[V]) {
+  constexpr int RC = BM / 8;  // row chunks per k row
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    const int idx = tid + 256 * g, k = k0 + (idx >> 4), row = row0 + 8 * (idx & 15);
+  for (int c = 0; c < V; ++c) {
+    const int idx = tid + NT * c, k = k0 + idx / RC, row = row0 + 8 * (idx % RC);
     const bool kok = k < K && k >= klo;
-    if constexpr (VEC) {  // rows contiguous, nrows and strides 8-aligned
+    if constexpr (VEC) {  // bf16, rows contiguous and readable in whole groups of 8
       const bool ok = kok && row < nrows;
-      if (o.f32) {
-        const float* p = (const float*)o.p + zoff + (long)k * o.s_k + row;
-        f32x4 a = ok ? *(const f32x4*)p : f32x4{0.f, 0.f, 0.f, 0.f};
-        f32x4 b = ok ? *(const f32x4*)(p + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[g][e] = (bf16)a[e];
-          v[g][4 + e] = (bf16)b[e];
-        }
-      } else {
-        const bf16* p = (const bf16*)o.p + zoff + (long)k * o.s_k + row;
-        v[g] = ok ? *(const bf16x8*)p : zero_frag<bf16>();
-      }
+      v[c] = ok ? *(const bf16x8*)((const bf16*)o.p + zoff + (long)k * o.s_k + row)
+                : zero_frag<bf16>();
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -124,17 +114,19 @@ __device__ __forceinline__ void gemm_load_t(const GemmOperand& o, long zoff, int
           const long off = zoff + (long)(row + e) * o.s_row + (long)k * o.s_k;
           x = o.f32 ? ((const float*)o.p)[off] : (float)((const bf16*)o.p)[off];
         }
-        v[g][e] = (bf16)x;
+        v[c][e] = (bf16)x;
       }
     }
   }
 }
 
-__device__ __forceinline__ void gemm_store_t(char* tile, int tid, const bf16x8 (&v)[2]) {
+template <int BM, int NT, int V>
+__device__ __forceinline__ void gemm_store_t(char* tile, int tid, const bf16x8 (&v)[V]) {
+  constexpr int RC = BM / 8, LDT = BM + 16;
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    const int idx = tid + 256 * g;
-    *(bf16x8*)(tile + ((idx >> 4) * kLdt + 8 * (idx & 15)) * 2) = v[g];
+  for (int c = 0; c < V; ++c) {
+    const int idx = tid + NT * c;
+    *(bf16x8*)(tile + ((idx / RC) * LDT + 8 * (idx % RC)) * 2) = v[c];
   }
 }
 
@@ -142,15 +134,15 @@ __device__ __forceinline__ void gemm_store_t(char* tile, int tid, const bf16x8 (
 // T layout: within a 16-lane group, lane j addresses k row 16 ks + 8 h + 4 s + j / 4 and
 // rows rb + 16 (group & 1) + 4 (j % 4) .. + 3; the transposing read hands lane i the four
 // k values of row rb + 16 (group & 1) + i, so s = 0, 1 give k 8 h + 0..3 and 4..7.
-template <bool T>
+template <bool T, int LDT>
 __device__ __forceinline__ bf16x8 gemm_frag(const char* tile, int rb, int ks, int lane) {
   if constexpr (T) {
     const int j = lane & 15, grp = lane >> 4, h = lane >> 5;
     const char* p =
-        tile + ((16 * ks + 8 * h + (j >> 2)) * kLdt + rb + 16 * (grp & 1) + 4 * (j & 3)) * 2;
+        tile + ((16 * ks + 8 * h + (j >> 2)) * LDT + rb + 16 * (grp & 1) + 4 * (j & 3)) * 2;
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
     const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-    const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * kLdt * 2));
+    const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * LDT * 2));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
   } else {
     const int h = lane >> 5, row = rb + (lane & 31);
@@ -158,66 +150,69 @@ __device__ __forceinline__ bf16x8 gemm_frag(const char* tile, int rb, int ks, in
   }
 }
 
-template <bool TA, bool TB, bool VEC>
-__global__ __launch_bounds__(kGT) void grad_gemm_kernel(GemmArgs a) {
-  __shared__ __align__(16) char smem[2][2][kGTile];  // [buffer][A, B]
-  const int tm = (a.M + 127) / 128, tn = (a.N + 127) / 128;
-  const int z = blockIdx.x / (tm * tn), t = blockIdx.x % (tm * tn);
-  const int m0 = (t / tn) * 128, n0 = (t % tn) * 128;
+template <class C, bool TA, bool TB, bool VEC>
+__global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
+  __shared__ __align__(16) char smem[2][C::TA_BYTES + C::TB_BYTES];  // [buffer][A | B]
+  const int tm = (a.M + C::BM - 1) / C::BM, tn = (a.N + C::BN - 1) / C::BN;
+  const int tile = xcd_tile(blockIdx.x, (int)gridDim.x);
+  const int z = tile / (tm * tn), t = tile % (tm * tn);
+  const int m0 = (t / tn) * C::BM, n0 = (t % tn) * C::BN;
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
-  const int w = tid >> 6, wm = w & 1, wn = w >> 1;
+  const int w = tid >> 6, wm = w % C::WGM, wn = w / C::WGM;
   const long za = (long)z * a.A.s_z, zb = (long)z * a.B.s_z;
   const int klo = (int)(a.k_lo0 + a.k_lo_dz * z);
-  f32x16 acc[2][2];
+  f32x16 acc[C::WM][C::WN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < C::WM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
-  bf16x8 va[2], vb[2];
+    for (int j = 0; j < C::WN; ++j) acc[i][j] = zero16();
+  bf16x8 va[C::VA], vb[C::VB];
   const int nk = (a.K + 31) / 32;
   auto load = [&](int k0) {
-    if constexpr (TA) gemm_load_t<VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
-    else gemm_load_n<VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
-    if constexpr (TB) gemm_load_t<VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
-    else gemm_load_n<VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
+    if constexpr (TA) gemm_load_t<C::BM, C::NT, C::VA, VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
+    else gemm_load_n<C::BM, C::NT, C::VA, VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
+    if constexpr (TB) gemm_load_t<C::BN, C::NT, C::VB, VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
+    else gemm_load_n<C::BN, C::NT, C::VB, VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
   };
   load(0);
   for (int kt = 0; kt < nk; ++kt) {
-    const int u = kt & 1;
-    if constexpr (TA) gemm_store_t(smem[u][0], tid, va);
-    else gemm_store_n(smem[u][0], tid, va);
-    if constexpr (TB) gemm_store_t(smem[u][1], tid, vb);
-    else gemm_store_n(smem[u][1], tid, vb);
+    char* sa = smem[kt & 1];
+    char* sb = sa + C::TA_BYTES;
+    if constexpr (TA) gemm_store_t<C::BM, C::NT, C::VA>(sa, tid, va);
+    else gemm_store_n<C::NT, C::VA>(sa, tid, va);
+    if constexpr (TB) gemm_store_t<C::BN, C::NT, C::VB>(sb, tid, vb);
+    else gemm_store_n<C::NT, C::VB>(sb, tid, vb);
     __syncthreads();  // tile kt in LDS; every wave is done with tile kt - 1
     if (kt + 1 < nk) load(32 * (kt + 1));
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 fa[2], fb[2];
+      bf16x8 fa[C::WM], fb[C::WN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        fa[i] = gemm_frag<TA>(smem[u][0], 64 * wm + 32 * i, ks, lane);
-        fb[i] = gemm_frag<TB>(smem[u][1], 64 * wn + 32 * i, ks, lane);
-      }
+      for (int i = 0; i < C::WM; ++i)
+        fa[i] = gemm_frag<TA, C::LDTA>(sa, 32 * (C::WM * wm + i), ks, lane);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int j = 0; j < C::WN; ++j)
+        fb[j] = gemm_frag<TB, C::LDTB>(sb, 32 * (C::WN * wn + j), ks, lane);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mma32(acc[i][j], fa[i], fb[j]);
+      for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::WN; ++j) acc[i][j] = mma32(acc[i][j], fa[i], fb[j]);
     }
   }
-  // lane (h, r): column n0 + 64 wn + 32 j + r, rows m0 + 64 wm + 32 i + 8 (q / 4) + 4 h + q % 4
-  float* C = a.C + (long)z * a.c_z;
+  // lane (h, r): column n0 + 32 (WN wn + j) + r, rows m0 + 32 (WM wm + i) + 8 (q / 4) + 4 h + q % 4
+  float* Cz = a.C + (long)z * a.c_z;
   const int mlo = (int)(a.m_lo0 + a.m_lo_dz * z);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = n0 + 64 * wn + 32 * j + r;
+  for (int j = 0; j < C::WN; ++j) {
+    const int n = n0 + 32 * (C::WN * wn + j) + r;
     if (n >= a.N) continue;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < C::WM; ++i)
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        const int m = m0 + 64 * wm + 32 * i + 8 * (q >> 2) + 4 * h + (q & 3);
+        const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
         if (m < a.M && m >= mlo) {
-          float* p = C + (long)m * a.c_row + (long)n * a.c_col;
+          float* p = Cz + (long)m * a.c_row + (long)n * a.c_col;
           *p = a.accumulate ? *p + acc[i][j][q] : acc[i][j][q];
         }
       }
@@ -226,30 +221,38 @@ __global__ __launch_bounds__(kGT) void grad_gemm_kernel(GemmArgs a) {
 
 static bool operand_t(const GemmOperand& o) { return o.s_row == 1 && o.s_k != 1; }
 
+// Vector loads need bf16, 16-byte alignment and strides in whole 8-element groups, with
+// the last group of rows (T) or of k (N) readable in full (a multiple of 8, or pad8).
 static bool operand_vec(const GemmOperand& o, int nrows, int K) {
-  if ((uintptr_t)o.p % 16 != 0 || o.s_z % 8 != 0) return false;
-  if (operand_t(o)) return o.s_k % 8 == 0 && nrows % 8 == 0;
-  return o.s_k == 1 && o.s_row % 8 == 0 && K % 8 == 0;
+  if (o.f32 || (uintptr_t)o.p % 16 != 0 || o.s_z % 8 != 0) return false;
+  if (operand_t(o)) return o.s_k % 8 == 0 && (nrows % 8 == 0 || o.pad8);
+  return o.s_k == 1 && o.s_row % 8 == 0 && (K % 8 == 0 || o.pad8);
+}
+
+template <class C, bool TA, bool TB, bool VEC>
+static void launch_gemm_cfg(const GemmArgs& a, int batches, hipStream_t s) {
+  const long tiles = (long)((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN) * batches;
+  hipLaunchKernelGGL((grad_gemm_kernel<C, TA, TB, VEC>), dim3((unsigned)tiles), dim3(C::NT), 0, s,
+                     a);
 }
 
 template <bool TA, bool TB>
-static void launch_gemm_t(const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
-  if (vec) hipLaunchKernelGGL((grad_gemm_kernel<TA, TB, true>), grid, dim3(kGT), 0, s, a);
-  else hipLaunchKernelGGL((grad_gemm_kernel<TA, TB, false>), grid, dim3(kGT), 0, s, a);
+static void launch_gemm_t(const GemmArgs& a, int batches, bool vec, hipStream_t s) {
+  // the large tiles (vector operands only) when they still give every CU at least two
+  const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256) * batches;
+  if (vec && big >= 2L * device_cus()) launch_gemm_cfg<GemmBig, TA, TB, true>(a, batches, s);
+  else if (vec) launch_gemm_cfg<GemmSmall, TA, TB, true>(a, batches, s);
+  else launch_gemm_cfg<GemmSmall, TA, TB, false>(a, batches, s);
 }
 
 void launch_grad_gemm(GemmArgs a, int batches, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || batches <= 0) return;
-  a.A.vec = operand_vec(a.A, a.M, a.K);
-  a.B.vec = operand_vec(a.B, a.N, a.K);
-  const bool vec = a.A.vec && a.B.vec;
-  const long tiles = (long)((a.M + 127) / 128) * ((a.N + 127) / 128) * batches;
+  const bool vec = operand_vec(a.A, a.M, a.K) && operand_vec(a.B, a.N, a.K);
   const bool ta = operand_t(a.A), tb = operand_t(a.B);
-  const dim3 grid((unsigned)tiles);
-  if (ta && tb) launch_gemm_t<true, true>(a, grid, vec, s);
-  else if (ta) launch_gemm_t<true, false>(a, grid, vec, s);
-  else if (tb) launch_gemm_t<false, true>(a, grid, vec, s);
-  else launch_gemm_t<false, false>(a, grid, vec, s);
+  if (ta && tb) launch_gemm_t<true, true>(a, batches, vec, s);
+  else if (ta) launch_gemm_t<true, false>(a, batches, vec, s);
+  else if (tb) launch_gemm_t<false, true>(a, batches, vec, s);
+  else launch_gemm_t<false, false>(a, batches, vec, s);
 }
 
 // --------------------------------------------------------------- row kernels
@@ -322,7 +325,7 @@ __global__ __launch_bounds__(256) void grad_head_kernel(HeadArgs a) {
     for (int q = 0; q < PER; ++q) {
       const int e = lane + 64 * q;
       if (e < DH) {
-        a.dy[yrow + e] = ri * (gy[q] - yv[q] * c2);
+        a.dy[yrow + e] = (bf16)(ri * (gy[q] - yv[q] * c2));
         dg[q] += dr[q] * yv[q] * ri;
       }
     }
@@ -399,9 +402,101 @@ __global__ __launch_bounds__(256) void grad_rms_kernel(RmsArgs a) {
   }
 }
 
+// The same with one wave per row (no workgroup barrier between rows, four rows in flight
+// per workgroup): lane t takes elements 4 t + 256 q .. + 3 (q < PER / 4), so D <= 64 PER;
+// the waves' gain partials are added in wave order at the end.
+template <int PER>
+__global__ __launch_bounds__(256) void grad_rms_wave_kernel(RmsArgs a) {
+  constexpr int NV = PER / 4;
+  const int chunk = blockIdx.x % a.chunks, o = blockIdx.x / a.chunks;
+  const long i0 = (long)a.ninner * chunk / a.chunks, i1 = (long)a.ninner * (chunk + 1) / a.chunks;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, D = a.D;
+  __shared__ float s_dg[64 * PER];  // the gain partials, summed over the waves
+  const bf16* g = a.g + (long)o * D;
+  float gv[PER], dg[PER];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int e = 4 * lane + 256 * v;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      gv[4 * v + u] = e + u < D ? (float)g[e + u] : 0.f;
+      dg[4 * v + u] = 0.f;
+    }
+  }
+  for (long i = i0 + w; i < i1; i += 4) {
+    const float* dy = a.dy + ((long)o * a.dy_o + i * a.dy_i) * D;
+    const bf16* x = a.x + ((long)o * a.x_o + i * a.x_i) * D;
+    float* out = a.out + ((long)o * a.out_o + i * a.out_i) * D;
+    const float ri = a.rinv[(long)o * a.r_o + i * a.r_i];
+    float dv[PER], xv[PER], dot = 0.f;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int e = 4 * lane + 256 * v;
+      if (e < D) {  // D is a multiple of 32: a lane's four elements are all in or all out
+        const f32x4 d4 = *(const f32x4*)(dy + e);
+        const bf16x4 x4 = *(const bf16x4*)(x + e);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          dv[4 * v + u] = d4[u];
+          xv[4 * v + u] = (float)x4[u];
+          dot += gv[4 * v + u] * d4[u] * xv[4 * v + u];
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) dv[4 * v + u] = xv[4 * v + u] = 0.f;
+      }
+    }
+    dot = wave_sum(dot);
+    const float c2 = ri * ri * dot / D;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int e = 4 * lane + 256 * v;
+      if (e < D) {
+        f32x4 r4;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int q = 4 * v + u;
+          r4[u] = ri * (gv[q] * dv[q] - xv[q] * c2);
+          dg[q] += dv[q] * xv[q] * ri;
+        }
+        if (a.accumulate) r4 += *(const f32x4*)(out + e);
+        *(f32x4*)(out + e) = r4;
+      }
+    }
+  }
+  for (int ww = 0; ww < 4; ++ww) {
+    if (w == ww) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int e = 4 * lane + 256 * v;
+        if (e < D)
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            s_dg[e + u] = ww == 0 ? dg[4 * v + u] : s_dg[e + u] + dg[4 * v + u];
+      }
+    }
+    __syncthreads();
+  }
+  for (int e = tid; e < D; e += 256) a.dgp[((long)o * a.chunks + chunk) * D + e] = s_dg[e];
+}
+
+static bool rms_wave_ok(const RmsArgs& a) {
+  // vector access: row bases and the tensors 16-byte (fp32) / 8-byte (bf16) aligned
+  const long rows[] = {a.dy_o, a.dy_i, a.out_o, a.out_i, a.x_o, a.x_i};
+  for (long r : rows)
+    if ((r * a.D) % 4 != 0) return false;
+  return (uintptr_t)a.dy % 16 == 0 && (uintptr_t)a.out % 16 == 0 && (uintptr_t)a.x % 8 == 0;
+}
+
 void launch_grad_rms(const RmsArgs& a, int nouter, hipStream_t s) {
   if (nouter <= 0 || a.ninner <= 0) return;
-  hipLaunchKernelGGL(grad_rms_kernel, dim3(nouter * a.chunks), dim3(256), 0, s, a);
+  const dim3 grid(nouter * a.chunks), blk(256);
+  if (rms_wave_ok(a) && a.D <= 512) hipLaunchKernelGGL(grad_rms_wave_kernel<8>, grid, blk, 0, s, a);
+  else if (rms_wave_ok(a) && a.D <= 1024)
+    hipLaunchKernelGGL(grad_rms_wave_kernel<16>, grid, blk, 0, s, a);
+  else if (rms_wave_ok(a) && a.D <= 2048)
+    hipLaunchKernelGGL(grad_rms_wave_kernel<32>, grid, blk, 0, s, a);
+  else hipLaunchKernelGGL(grad_rms_kernel, grid, blk, 0, s, a);
 }
 
 // out[o][e] (+)= scale * sum over c < chunks of part[(o chunks + c) n + e] (fixed order).
@@ -422,64 +517,115 @@ void launch_grad_sum(const float* part, int outer, int chunks, long n, float* ou
                      part, chunks, n, out, scale, accumulate);
 }
 
-// Per token and branch: the normed states hn[l] = g[l] h[l] / rms(h[l]) (recomputed in fp32
-// from the bf16 states H [N][L][D], the branch's gains g [L][D] and rinv [N][L], as the
-// forward mix computes them), the channels' gradient dmix [k][N][D] (fp32) and the final
-// mixing weights alpha [N][k][L] (fp32) give dhn[n][l][e] = sum_j alpha[j][l] dmix[j][e]
-// (written, fp32) and dalpha[j][l] = dmix[j] . hn[l]; then the softmax-over-depth backward
-// (or the mask of the sources a channel may not mix) gives the router logits' gradient
-// dlog [N][k L] (fp32). Everything stays fp32: dalpha[j][l] is a small difference when
-// one source dominates a channel (the mid norm's gradient is orthogonal to the mixed
-// channel), which bf16 operands would swamp. The states go through LDS in column chunks
-// of kMixGradCols, the dalpha sums accumulating across chunks (each (j, l) pair stays
-// with one wave).
-constexpr int kMixGradCols = 64;
-
+// Per token and branch, with hn[l] = g[l] h[l] / rms(h[l]) recomputed in fp32 from the
+// bf16 states H [N][L][D], the branch's gains g [L][D] and rinv [N][L] (as the forward mix
+// computes them), the channels' gradient dmix [k][N][D] (fp32) and the final mixing
+// weights alpha [N][k][L]:
+//   dhn[n][l][e] = sum_j alpha[j][l] dmix[j][e]   (written, fp32): each thread takes whole
+//     columns e, holding the k values dmix[.][e] in registers against alpha^T in LDS;
+//   dalpha[j][l] = dmix[j] . hn[l]: a k x L product over the D columns on the fp32 matrix
+//     cores (32 x 32 x 2 steps, the four waves taking every fourth 16-column step, their
+//     partial tiles summed in a fixed order). It stays fp32 because dalpha[j][l] is a
+//     small difference when one source dominates a channel (the mid norm's gradient is
+//     orthogonal to the mixed channel), which bf16 operands would swamp;
+// then the softmax-over-depth backward (or the mask of the sources a channel may not mix)
+// gives the router logits' gradient dlog [N][k L]. MAXK >= k (16, 32 or 64).
+template <int MAXK>
 __global__ __launch_bounds__(256) void grad_mix_kernel(MixGradArgs a) {
   extern __shared__ __align__(16) unsigned char gsm[];
   const int L = a.L, k = a.k, D = a.D;
+  const int KP = (k + 3) & ~3;
   const long n = blockIdx.x;
-  constexpr int DC = kMixGradCols;
-  float* hs = (float*)gsm;                        // [L][DC]
-  float* ds = hs + L * DC;                        // [k][DC]
-  float* al = ds + k * DC;                        // [k][L]
-  float* da = al + k * L;                         // [k][L]
+  float* alT = (float*)gsm;        // [L][KP] alpha transposed, zero-padded
+  float* al = alT + L * KP;        // [k][L]
+  float* da = al + k * L;          // [k][L]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int e = tid; e < k * L; e += 256) {
-    al[e] = a.alpha[n * k * L + e];
-    da[e] = 0.f;
+  for (int e = tid; e < L * KP; e += 256) {
+    const int l = e / KP, j = e % KP;
+    alT[e] = j < k ? a.alpha[(n * k + j) * L + l] : 0.f;
   }
-  for (int c0 = 0; c0 < D; c0 += DC) {
-    __syncthreads();  // the previous chunk is consumed (and al, da are in place)
-    for (int e = tid; e < L * DC; e += 256) {
-      const int l = e / DC, c = c0 + e % DC;
-      hs[e] = c < D ? (float)a.g[(long)l * D + c] * (float)a.H[(n * L + l) * D + c] *
-                          a.rinv[n * L + l]
-                    : 0.f;
-    }
-    for (int e = tid; e < k * DC; e += 256) {
-      const int j = e / DC, c = c0 + e % DC;
-      ds[e] = c < D ? a.dmix[((long)j * a.N + n) * D + c] : 0.f;
-    }
-    __syncthreads();
-    for (int pr = w; pr < k * L; pr += 4) {
-      const int j = pr / L, l = pr % L;
+  for (int e = tid; e < k * L; e += 256) al[e] = a.alpha[n * k * L + e];
+  __syncthreads();
+  // dhn, one column per thread at a time
+  for (int c = tid; c < D; c += 256) {
+    float dm[MAXK];
+#pragma unroll
+    for (int j = 0; j < MAXK; ++j) dm[j] = j < k ? a.dmix[((long)j * a.N + n) * D + c] : 0.f;
+    float* out = a.dhn + n * L * D + c;
+    for (int l = 0; l < L; ++l) {
+      const float* ar = alT + l * KP;
       float s = 0.f;
-      for (int c = lane; c < DC; c += 64) s += ds[j * DC + c] * hs[l * DC + c];
-      s = wave_sum(s);
-      if (lane == 0) da[pr] += s;
+#pragma unroll
+      for (int j = 0; j < MAXK; j += 4) {
+        if (j < KP) {
+          const f32x4 av = *(const f32x4*)(ar + j);
+          s += av[0] * dm[j] + av[1] * dm[j + 1] + av[2] * dm[j + 2] + av[3] * dm[j + 3];
+        }
+      }
+      out[(long)l * D] = s;
     }
-    for (int e = tid; e < L * DC; e += 256) {
-      const int l = e / DC, c = e % DC;
-      if (c0 + c < D) {
-        float s = 0.f;
-        for (int j = 0; j < k; ++j) s += al[j * L + l] * ds[j * DC + c];
-        a.dhn[(n * L + l) * D + c0 + c] = s;
+  }
+  // dalpha on the fp32 matrix cores: tile (tj, tl) rows j = 32 tj + .., columns l = 32 tl + ..
+  // lane (h, r) supplies columns 16 s + 8 h .. + 7 of row r of both operands
+  constexpr int TJ = MAXK > 32 ? 2 : 1;
+  const int tj_n = (k + 31) / 32, tl_n = (L + 31) / 32;
+  const int h = lane >> 5, r = lane & 31;
+  f32x16 acc[TJ][2];
+#pragma unroll
+  for (int tj = 0; tj < TJ; ++tj)
+#pragma unroll
+    for (int tl = 0; tl < 2; ++tl) acc[tj][tl] = zero16();
+  const float* rinv = a.rinv + n * L;
+  for (int st = w; st < D / 16; st += 4) {
+    const int c0 = 16 * st + 8 * h;
+    f32x8 av[TJ], bv[2];
+#pragma unroll
+    for (int tj = 0; tj < TJ; ++tj) {
+      const int j = 32 * tj + r;
+      if (tj < tj_n && j < k) {
+        const float* p = a.dmix + ((long)j * a.N + n) * D + c0;
+        const f32x4 x = *(const f32x4*)p, y = *(const f32x4*)(p + 4);
+        av[tj] = f32x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+      } else {
+        av[tj] = f32x8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
       }
     }
+#pragma unroll
+    for (int tl = 0; tl < 2; ++tl) {
+      const int l = 32 * tl + r;
+      if (tl < tl_n && l < L) {
+        const bf16x8 hv = *(const bf16x8*)(a.H + (n * L + l) * D + c0);
+        const bf16x8 gv = *(const bf16x8*)(a.g + (long)l * D + c0);
+        const float ri = rinv[l];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) bv[tl][i] = (float)gv[i] * (float)hv[i] * ri;
+      } else {
+        bv[tl] = f32x8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int tj = 0; tj < TJ; ++tj)
+#pragma unroll
+      for (int tl = 0; tl < 2; ++tl)
+        if (tj < tj_n && tl < tl_n) acc[tj][tl] = mma32(acc[tj][tl], av[tj], bv[tl]);
   }
-  __syncthreads();
-  // logits' gradient per channel row
+  // the four waves' partial tiles, added in wave order
+  for (int ww = 0; ww < 4; ++ww) {
+    if (w == ww) {
+#pragma unroll
+      for (int tj = 0; tj < TJ; ++tj)
+#pragma unroll
+        for (int tl = 0; tl < 2; ++tl)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const int j = 32 * tj + 8 * (q >> 2) + 4 * h + (q & 3), l = 32 * tl + r;
+            if (tj < tj_n && tl < tl_n && j < k && l < L)
+              da[j * L + l] = ww == 0 ? acc[tj][tl][q] : da[j * L + l] + acc[tj][tl][q];
+          }
+    }
+    __syncthreads();
+  }
+  // logits' gradient per channel row (fp32, and a bf16 copy padded to kLp for the GEMMs)
   for (int j = tid; j < k; j += 256) {
     const int nl = a.nofeedback ? j + 1 : L;
     float dot = 0.f;
@@ -489,19 +635,24 @@ __global__ __launch_bounds__(256) void grad_mix_kernel(MixGradArgs a) {
       float v = 0.f;
       if (l < nl) v = a.softmax ? al[j * L + l] * (da[j * L + l] - dot) : da[j * L + l];
       a.dlog[n * k * L + j * L + l] = v;
+      a.dlogb[n * a.kLp + j * L + l] = (bf16)v;
     }
   }
+  for (int e = k * L + tid; e < a.kLp; e += 256) a.dlogb[n * a.kLp + e] = (bf16)0.f;
 }
 
 size_t grad_mix_smem(int L, int k, int D) {
   (void)D;
-  return (size_t)(L + k) * kMixGradCols * 4 + (size_t)2 * k * L * 4;
+  return ((size_t)L * ((k + 3) & ~3) + (size_t)2 * k * L) * 4;
 }
 
 void launch_grad_mix(const MixGradArgs& a, hipStream_t s) {
   if (a.N <= 0) return;
-  hipLaunchKernelGGL(grad_mix_kernel, dim3((unsigned)a.N), dim3(256),
-                     grad_mix_smem(a.L, a.k, a.D), s, a);
+  const dim3 grid((unsigned)a.N), blk(256);
+  const size_t sm = grad_mix_smem(a.L, a.k, a.D);
+  if (a.k <= 16) hipLaunchKernelGGL(grad_mix_kernel<16>, grid, blk, sm, s, a);
+  else if (a.k <= 32) hipLaunchKernelGGL(grad_mix_kernel<32>, grid, blk, sm, s, a);
+  else hipLaunchKernelGGL(grad_mix_kernel<64>, grid, blk, sm, s, a);
 }
 
 // dst[j][b T + i][h d + e] = src[j][b][h][ctx_len[b] + i][e]: the new slots' rows of a
@@ -509,7 +660,7 @@ void launch_grad_mix(const MixGradArgs& a, hipStream_t s) {
 __global__ __launch_bounds__(256) void grad_gather_kernel(const float* src, int k, int B, int H,
                                                           int T, int S_cap, int d,
                                                           const int32_t* ctx_len, int ctx_hi,
-                                                          float* dst) {
+                                                          bf16* dst) {
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   const long n = (long)k * B * T * H * d;
   if (idx >= n) return;
@@ -517,11 +668,11 @@ __global__ __launch_bounds__(256) void grad_gather_kernel(const float* src, int 
   const long t = idx / ((long)d * H);  // (j, b, i)
   const int i = (int)(t % T), b = (int)(t / T % B), j = (int)(t / ((long)T * B));
   const int slot = ctx_at(ctx_len, b, ctx_hi) + i;
-  dst[idx] = src[((((long)j * B + b) * H + hh) * S_cap + slot) * d + e];
+  dst[idx] = (bf16)src[((((long)j * B + b) * H + hh) * S_cap + slot) * d + e];
 }
 
 void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,
-                        const int32_t* ctx_len, int ctx_hi, float* dst, hipStream_t s) {
+                        const int32_t* ctx_len, int ctx_hi, bf16* dst, hipStream_t s) {
   const long n = (long)k * B * T * H * d;
   if (n <= 0) return;
   hipLaunchKernelGGL(grad_gather_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,

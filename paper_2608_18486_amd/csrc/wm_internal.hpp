@@ -131,13 +131,17 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
                             float* dVc, float* dKd, float* dVd, float* rows, hipStream_t s,
                             bool accumulate = false);
 
+// compute units of the current device (cached per device)
+int device_cus();
+
 // -- gradients of the pool and the queries (wm_grad.hip) ----------------------
 // Operand element (row, k) of batch z at p + z s_z + row s_row + k s_k (bf16 or fp32).
 struct GemmOperand {
   const void* p;
   long s_row, s_k, s_z;
   int f32;
-  int vec;  // set by launch_grad_gemm
+  int pad8;  // the operand's memory extends to a whole group of 8 past its last row (rows
+             // contiguous) or k (k contiguous), zero-filled: vector loads may read it
 };
 // C[z][m][n] (+)= sum_k A(m, k) B(n, k) over batches z; C at C + z c_z + m c_row + n c_col.
 // Batch z uses only k >= k_lo0 + k_lo_dz z of B and stores only rows m >= m_lo0 + m_lo_dz z
@@ -160,7 +164,7 @@ struct HeadArgs {
   const int32_t* ctx_len;
   int ctx_hi;
   const float* y;         // pre-norm values [Z][B T][H d]
-  float* dy;              // their gradient, same layout
+  bf16* dy;               // their gradient, same layout (bf16: the GEMMs' operand)
   const bf16* g;          // [Z][d]
   const float* tab;       // RoPE table [B T][d / 2] (cos, sin)
   float* dgp;             // gain gradient partials [Z][chunks][d]
@@ -187,7 +191,7 @@ void launch_grad_sum(const float* part, int outer, int chunks, long n, float* ou
                      int accumulate, hipStream_t s);
 void launch_grad_colsum(const float* x, long rows, int n, int chunks, float* part, hipStream_t s);
 void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,
-                        const int32_t* ctx_len, int ctx_hi, float* dst, hipStream_t s);
+                        const int32_t* ctx_len, int ctx_hi, bf16* dst, hipStream_t s);
 struct MixGradArgs {
   const bf16* H;           // [N][L][D] states
   const bf16* g;           // [L][D] the branch's pre-mix gains
@@ -196,7 +200,8 @@ struct MixGradArgs {
   const float* alpha;      // [N][k][L] final mixing weights
   float* dhn;              // [N][L][D]
   float* dlog;             // [N][k L] gradient of the router logits
-  int N, L, k, D, softmax, nofeedback;
+  bf16* dlogb;             // [N][kLp] the same in bf16, rows padded with zeros to kLp
+  int N, L, k, D, softmax, nofeedback, kLp;
 };
 size_t grad_mix_smem(int L, int k, int D);
 void launch_grad_mix(const MixGradArgs& a, hipStream_t s);
