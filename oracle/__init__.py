@@ -337,6 +337,17 @@ def jacobi(dims: Dims, params, W_o, chan_map, X, passes: int):
     return H, top, Kc, Vc
 
 
+def jacobi_from(dims: Dims, params, W_o, chan_map, X, H0, passes: int):
+    """Jacobi iteration from given states H0 [B, T, L, D] in place of the embeddings."""
+    P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)
+    H0 = _f64(H0)
+    assert H0.shape == (dims.B, dims.T_new, dims.L, dims.D)
+    H, top, Kc, Vc = _pass_outputs(dims)
+    lib().wmo_jacobi_from(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(m), _ptr(X),
+                          _ptr(H0), ctypes.c_int(passes), _ptr(H), _ptr(top), _ptr(Kc), _ptr(Vc))
+    return H, top, Kc, Vc
+
+
 def gauss_seidel(dims: Dims, params, W_o, chan_map, X, g: int, passes: int):
     """Cyclic Gauss-Seidel iteration over g strided groups (Section 3.3)."""
     P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)

@@ -16,6 +16,8 @@ gradients have the shapes of what they differentiate.
 """
 from __future__ import annotations
 
+import dataclasses
+
 import numpy as np
 import torch
 
@@ -269,3 +271,59 @@ def new_rows(dims: Dims, cache, ctx_len=None):
     c = np.asarray(cache)
     return np.stack([c[:, b, :, int(ctx[b]):int(ctx[b]) + dims.T_new] for b in range(dims.B)],
                     axis=1)
+
+
+# ------------------------------------------- Section 3.3: passes, truncated backprop
+
+def _states(dims: Dims, P: dict, W_o, X, chan_map, K, V):
+    """States(X; P) with the stand-in block h_{l+1} = h_l + W_o[l] o_l: layer l's query from
+    h_l, its attention over channel chan_map[l] of the caches K, V [k, B, Hkv, T, d] (every
+    position's slot written by the pool). Returns (H [B, T, L, D], h_top [B, T, D])."""
+    L = dims.L
+    one = dataclasses.replace(dims, L=1)
+    ctx = torch.zeros(dims.B, dtype=torch.long)
+    h = X
+    Hs = []
+    for l in range(L):
+        Hs.append(h)
+        sub = {**P, "g_in": P["g_in"][l:l + 1], "Wq": P["Wq"][l:l + 1],
+               "g_qnorm": P["g_qnorm"][l:l + 1]}
+        q = queries(one, sub, h.unsqueeze(2), ctx)                         # [1, B, Hq, T, d]
+        o = attend(one, P["Kd"], P["Vd"], q, [chan_map[l]], ctx, K, V)[0]  # [B, T, Hq d]
+        h = h + o @ W_o[l].T
+    return torch.stack(Hs, dim=2), h
+
+
+def passes_forward(dims: Dims, P: dict, W_o, X, chan_map, passes: int, n_grad: int):
+    """Jacobi passes (Section 3.3) as the C oracle runs them: H^(0) = X in every layer; pass
+    t pools H^(t-1) into the caches and recomputes H^(t) = States(X; caches). The states
+    entering the last n_grad passes are detached (truncated backpropagation): only those
+    passes carry gradients; with n_grad = passes nothing is cut and H^(0) stays a function
+    of X. Returns (H^(passes), h_top^(passes))."""
+    B, T, L, D = dims.B, dims.T_new, dims.L, dims.D
+    H = X.unsqueeze(2).expand(B, T, L, D)
+    ctx = torch.zeros(B, dtype=torch.long)
+    top = None
+    for t in range(1, passes + 1):
+        if t == passes - n_grad + 1 and n_grad < passes:
+            H = H.detach()
+        K, V = pool(dims, P, H, ctx)
+        H, top = _states(dims, P, W_o, X, chan_map, K, V)
+    return H, top
+
+
+def passes_grads(dims: Dims, params, W_o, X, chan_map, passes: int, n_grad: int, dh_top) -> dict:
+    """Gradients of <dh_top, h_top> after `passes` Jacobi passes with backpropagation
+    truncated to the last n_grad (1 <= n_grad <= passes): dX, dW_o and d + name for every
+    parameter."""
+    assert 1 <= n_grad <= passes
+    P = _params(params, True)
+    Xt, Wt = _t(X, True), _t(W_o, True)
+    _, top = passes_forward(dims, P, Wt, Xt, chan_map, passes, n_grad)
+    loss = (top * _t(dh_top)).sum()
+    leaves = [Xt, Wt] + [P[n] for n in PARAM_NAMES]
+    g = torch.autograd.grad(loss, leaves, allow_unused=True)
+    out = {"dX": g[0].numpy(), "dW_o": g[1].numpy()}
+    for n, x in zip(PARAM_NAMES, g[2:]):
+        out["d" + n] = (x if x is not None else torch.zeros_like(P[n])).numpy()
+    return out

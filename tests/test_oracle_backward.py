@@ -314,3 +314,61 @@ def test_step_gradient_is_the_sum_of_its_parts(kw):
         c0 = ctxs[b]
         assert np.abs(ga["dKc"][:, b, :, :c0] - whole["dKc_ctx"][:, b, :, :c0]).max() < tol
         assert np.abs(ga["dVc"][:, b, :, :c0] - whole["dVc_ctx"][:, b, :, :c0]).max() < tol
+
+
+# ------------------------------------------------ passes and truncated backprop
+
+def _pass_inputs(dm, seed=21):
+    rng = np.random.default_rng(seed)
+    P = _params(dm, seed=seed)
+    W_o = 0.3 * rng.standard_normal((dm.L, dm.D, dm.Hq * dm.d)) / np.sqrt(dm.Hq * dm.d)
+    X = rng.standard_normal((dm.B, dm.T_new, dm.D))
+    dh = rng.standard_normal((dm.B, dm.T_new, dm.D))
+    return P, W_o, X, dh, rng
+
+
+PASS_CASES = [dict(), dict(mask_mode=oracle.MASK_INCLUSIVE, mix_mode=oracle.MIX_SOFTMAX),
+              dict(p=2, L=5, k=3)]
+
+
+@pytest.mark.parametrize("kw", PASS_CASES)
+def test_passes_forward_matches_c_oracle(kw):
+    dm = _dims(T_new=6, **kw)
+    dm.S_cap = dm.T_new
+    P, W_o, X, _, _ = _pass_inputs(dm)
+    cmap = [(l + 1) % dm.k for l in range(dm.L)]
+    H, top, _, _ = oracle.jacobi(dm, P, W_o, cmap, X, 3)
+    Pt = {n: ob._t(P[n]) for n in oracle.PARAM_NAMES}
+    Ht, topt = ob.passes_forward(dm, Pt, ob._t(W_o), ob._t(X), cmap, 3, 3)
+    assert np.abs(Ht.detach().numpy() - H).max() < 1e-12
+    assert np.abs(topt.detach().numpy() - top).max() < 1e-12
+
+
+@pytest.mark.parametrize("kw", PASS_CASES)
+@pytest.mark.parametrize("passes,n_grad", [(2, 2), (3, 1), (3, 2)])
+def test_truncated_pass_gradients_match_finite_differences(kw, passes, n_grad):
+    """Full backpropagation (n_grad = passes) against central differences of the C oracle's
+    Jacobi passes; truncated backpropagation against central differences of the last
+    n_grad passes run from the states entering them, held fixed at their value (the C
+    oracle's passes from given states)."""
+    dm = _dims(T_new=5, **kw)
+    dm.S_cap = dm.T_new
+    P, W_o, X, dh, rng = _pass_inputs(dm)
+    cmap = [(2 * l + 1) % dm.k for l in range(dm.L)]
+    g = ob.passes_grads(dm, P, W_o, X, cmap, passes, n_grad, dh)
+    if n_grad == passes:
+        def top(Px, Wx, Xx):
+            return (oracle.jacobi(dm, Px, Wx, cmap, Xx, passes)[1] * dh).sum()
+    else:
+        H0 = oracle.jacobi(dm, P, W_o, cmap, X, passes - n_grad)[0]
+
+        def top(Px, Wx, Xx):
+            return (oracle.jacobi_from(dm, Px, Wx, cmap, Xx, H0, n_grad)[1] * dh).sum()
+    checks = [("dX", lambda x: top(P, W_o, x), X), ("dW_o", lambda x: top(P, x, X), W_o)]
+    for n in oracle.PARAM_NAMES:
+        checks.append(("d" + n, lambda x, n=n: top({**P, n: x}, W_o, X), P[n]))
+    for name, f, x in checks:
+        v = rng.standard_normal(x.shape)
+        num = _fd(f, x, v, eps=2e-5)
+        ana = (g[name] * v).sum()
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(num)), (name, num, ana)
