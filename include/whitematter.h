@@ -90,7 +90,9 @@ enum wm_op {
   WM_OP_ATTEND_BACKWARD = 9, /* wm_channel_attend_backward */
   WM_OP_Q_BACKWARD = 10,      /* wm_q_project_backward */
   WM_OP_POOL_BACKWARD = 11,   /* wm_pool_backward */
-  WM_OP_STEP_BACKWARD = 12    /* wm_layer_step_backward */
+  WM_OP_STEP_BACKWARD = 12,   /* wm_layer_step_backward */
+  WM_OP_PASSES_BACKWARD = 13  /* wm_prefill_passes_backward (size: see
+                                 wm_passes_backward_workspace) */
 };
 
 /* Problem dimensions (paper notation). Supported: 1 <= L <= 64, 1 <= k <= L,
@@ -401,6 +403,40 @@ int wm_prefill_passes(const wm_dims *dims, const wm_params *params, const void *
                       const void *X, const int32_t *chan_map, int32_t passes, void *Kc,
                       void *Vc, void *H, void *h_top, void *ws, size_t ws_bytes,
                       wm_stream_t stream);
+
+/* A training step's passes with truncated backpropagation (Section 3.3): the Jacobi
+ * passes of wm_prefill_passes (dims->groups <= 1), then the gradients of the loss through
+ * the last n_grad of them only. Pass t pools H^(t-1) into the caches and recomputes
+ * H^(t) = States(X; caches) with the stand-in block h_{l+1} = h_l + W_o[l] o_l; the
+ * states entering pass passes - n_grad + 1 are held fixed (no gradient flows into them or
+ * the passes before), except with n_grad = passes, where they are H^(0) = X in every layer
+ * and their gradient goes to X. Each window pass is differentiated whole: its pool (the
+ * router, mix, projections and norms that wrote the caches), then every layer from the
+ * top down (the block's W_o, the consumer's attention over its channel with the dummy,
+ * its query), the residual stream carrying the gradient down to X. The window's states,
+ * caches and per-layer attention outputs are kept in the workspace; the queries are
+ * recomputed.
+ * bf16, head dims 64 and 96, T_new = T > 4, D <= 4608, every mask, mix and router mode.
+ *   dims, params, W_o, X, chan_map, passes  as wm_prefill_passes
+ *   n_grad   1 <= n_grad <= passes: the passes that carry gradients
+ *   dh_top   device float [B][T][D]: the loss gradient in the state leaving the top layer
+ *            after the last pass
+ *   h_top    device [B][T][D] bf16 or NULL: that state (the forward's output)
+ *   dX       device float [B][T][D]: ADDED
+ *   dW_o     device float [L][D][Hq*d]: ADDED
+ *   grads    every entry (Kd, Vd only with WM_MASK_PAPER; W_alpha not with static
+ *            weights): ADDED
+ * Workspace: wm_passes_backward_workspace(dims, n_grad) bytes, 256-byte aligned (it grows
+ * with n_grad: three state-sized arrays per window pass). Errors as wm_prefill_passes and
+ * wm_layer_step_backward; WM_ERR_ARG for n_grad outside [1, passes] or groups > 1. */
+int wm_prefill_passes_backward(const wm_dims *dims, const wm_params *params, const void *W_o,
+                               const void *X, const int32_t *chan_map, int32_t passes,
+                               int32_t n_grad, const float *dh_top, void *h_top, float *dX,
+                               float *dW_o, const wm_grads *grads, void *ws, size_t ws_bytes,
+                               wm_stream_t stream);
+/* Bytes of workspace wm_prefill_passes_backward needs for a window of n_grad passes; 0 when
+ * dims are invalid (see wm_validate) or n_grad < 1. */
+size_t wm_passes_backward_workspace(const wm_dims *dims, int32_t n_grad);
 
 /* Measurement helper: wm_layer_step (doc_start NULL) or wm_layer_step_doc
  * (doc_start not NULL) that also records caller-created HIP events (hipEvent_t,

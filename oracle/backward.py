@@ -33,6 +33,16 @@ def _t(a, grad=False):
     return t.clone().requires_grad_(grad)
 
 
+def _same(t):
+    return t
+
+
+def bf16_store(t):
+    """The value rounded to bfloat16 (round to nearest even), the gradient passed through
+    unchanged: a tensor stored in bf16 between two steps of the computation."""
+    return t + (t.detach().to(torch.bfloat16).to(F64) - t.detach())
+
+
 def _rms(x, g, eps):
     """RMSNorm over the last axis (Section 3.1 Step 1 and Step 2)."""
     return g * x / torch.sqrt((x * x).mean(-1, keepdim=True) + eps)
@@ -54,9 +64,10 @@ def _router_layers(L, p):
     return [L - 1 - p * m for m in range(Lp)][::-1]
 
 
-def pool(dims: Dims, P: dict, H, ctx):
+def pool(dims: Dims, P: dict, H, ctx, store=_same):
     """Steps 1-2 for every new token: H [B, T, L, D] -> the new cache rows
-    K, V [k, B, Hkv, T, d] (key norm and RoPE applied to K)."""
+    K, V [k, B, Hkv, T, d] (key norm and RoPE applied to K). store: applied to the mixed
+    channels and to the rows (bf16_store: as a path that keeps them in bf16)."""
     B, T, L, k, D = dims.B, dims.T_new, dims.L, dims.k, dims.D
     Hkv, d = dims.Hkv, dims.d
     N = B * T
@@ -88,14 +99,14 @@ def pool(dims: Dims, P: dict, H, ctx):
             alpha = torch.softmax(alpha.masked_fill(~allowed, float("-inf")), dim=-1)
         else:
             alpha = alpha.masked_fill(~allowed, 0.0)
-        mixed = torch.einsum("nkl,nld->nkd", alpha, hn)                   # [N, k, D]
+        mixed = store(torch.einsum("nkl,nld->nkd", alpha, hn))            # [N, k, D]
         u = _rms(mixed, P["g_mid"][br], dims.eps)
         W = (P["Wk"] if br == 0 else P["Wv"]).reshape(k, Hkv * d, D)
         y = torch.einsum("nkd,kod->nko", u, W).reshape(N, k, Hkv, d)
         if br == 0:
             y = _rms(y, P["g_knorm"].reshape(1, k, 1, d), dims.eps)
             y = _rope(y, pos.reshape(N, 1, 1).expand(N, k, Hkv), dims.rope_theta)
-        out.append(y.reshape(B, T, k, Hkv, d).permute(2, 0, 3, 1, 4))
+        out.append(store(y.reshape(B, T, k, Hkv, d).permute(2, 0, 3, 1, 4)))
     return out[0], out[1]
 
 
@@ -275,10 +286,11 @@ def new_rows(dims: Dims, cache, ctx_len=None):
 
 # ------------------------------------------- Section 3.3: passes, truncated backprop
 
-def _states(dims: Dims, P: dict, W_o, X, chan_map, K, V):
+def _states(dims: Dims, P: dict, W_o, X, chan_map, K, V, store=_same):
     """States(X; P) with the stand-in block h_{l+1} = h_l + W_o[l] o_l: layer l's query from
     h_l, its attention over channel chan_map[l] of the caches K, V [k, B, Hkv, T, d] (every
-    position's slot written by the pool). Returns (H [B, T, L, D], h_top [B, T, D])."""
+    position's slot written by the pool). Returns (H [B, T, L, D], h_top [B, T, D]). store:
+    applied to each query, attention output and state."""
     L = dims.L
     one = dataclasses.replace(dims, L=1)
     ctx = torch.zeros(dims.B, dtype=torch.long)
@@ -288,13 +300,14 @@ def _states(dims: Dims, P: dict, W_o, X, chan_map, K, V):
         Hs.append(h)
         sub = {**P, "g_in": P["g_in"][l:l + 1], "Wq": P["Wq"][l:l + 1],
                "g_qnorm": P["g_qnorm"][l:l + 1]}
-        q = queries(one, sub, h.unsqueeze(2), ctx)                         # [1, B, Hq, T, d]
-        o = attend(one, P["Kd"], P["Vd"], q, [chan_map[l]], ctx, K, V)[0]  # [B, T, Hq d]
-        h = h + o @ W_o[l].T
+        q = store(queries(one, sub, h.unsqueeze(2), ctx))                  # [1, B, Hq, T, d]
+        o = store(attend(one, P["Kd"], P["Vd"], q, [chan_map[l]], ctx, K, V)[0])
+        h = store(h + o @ W_o[l].T)
     return torch.stack(Hs, dim=2), h
 
 
-def passes_forward(dims: Dims, P: dict, W_o, X, chan_map, passes: int, n_grad: int):
+def passes_forward(dims: Dims, P: dict, W_o, X, chan_map, passes: int, n_grad: int,
+                   store=_same):
     """Jacobi passes (Section 3.3) as the C oracle runs them: H^(0) = X in every layer; pass
     t pools H^(t-1) into the caches and recomputes H^(t) = States(X; caches). The states
     entering the last n_grad passes are detached (truncated backpropagation): only those
@@ -307,19 +320,24 @@ def passes_forward(dims: Dims, P: dict, W_o, X, chan_map, passes: int, n_grad: i
     for t in range(1, passes + 1):
         if t == passes - n_grad + 1 and n_grad < passes:
             H = H.detach()
-        K, V = pool(dims, P, H, ctx)
-        H, top = _states(dims, P, W_o, X, chan_map, K, V)
+        K, V = pool(dims, P, H, ctx, store)
+        H, top = _states(dims, P, W_o, X, chan_map, K, V, store)
     return H, top
 
 
-def passes_grads(dims: Dims, params, W_o, X, chan_map, passes: int, n_grad: int, dh_top) -> dict:
+def passes_grads(dims: Dims, params, W_o, X, chan_map, passes: int, n_grad: int, dh_top,
+                 bf16_storage: bool = False) -> dict:
     """Gradients of <dh_top, h_top> after `passes` Jacobi passes with backpropagation
     truncated to the last n_grad (1 <= n_grad <= passes): dX, dW_o and d + name for every
-    parameter."""
+    parameter. bf16_storage: the forward rounds what a bf16 path stores between its steps
+    (mixed channels, cache rows, queries, attention outputs, states) to bf16, the
+    derivatives passing through the rounding; how far that moves the gradients measures
+    their sensitivity to the storage precision."""
     assert 1 <= n_grad <= passes
     P = _params(params, True)
     Xt, Wt = _t(X, True), _t(W_o, True)
-    _, top = passes_forward(dims, P, Wt, Xt, chan_map, passes, n_grad)
+    _, top = passes_forward(dims, P, Wt, Xt, chan_map, passes, n_grad,
+                            bf16_store if bf16_storage else _same)
     loss = (top * _t(dh_top)).sum()
     leaves = [Xt, Wt] + [P[n] for n in PARAM_NAMES]
     g = torch.autograd.grad(loss, leaves, allow_unused=True)

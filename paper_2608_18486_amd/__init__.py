@@ -25,7 +25,7 @@ MASK_PAPER, MASK_INCLUSIVE = 0, 1
 ROUTER_DYNAMIC, ROUTER_STATIC, ROUTER_NOFEEDBACK = 0, 1, 2
 (OP_ROUTER_MIX, OP_KV_PROJECT, OP_Q_PROJECT, OP_CHANNEL_ATTEND, OP_LAYER_STEP, OP_POOL,
  OP_LAYER_ATTEND, OP_PASSES, OP_DENSE_ATTEND, OP_ATTEND_BACKWARD, OP_Q_BACKWARD,
- OP_POOL_BACKWARD, OP_STEP_BACKWARD) = range(13)
+ OP_POOL_BACKWARD, OP_STEP_BACKWARD, OP_PASSES_BACKWARD) = range(14)
 
 PARAM_NAMES = ("g_pre", "W_alpha", "b_alpha", "g_mid", "Wk", "Wv", "g_knorm",
                "Kd", "Vd", "g_in", "Wq", "g_qnorm")
@@ -91,6 +91,8 @@ def lib() -> ctypes.CDLL:
         "wm_pool_backward": [D, P, _vp, _vp, _vp, _vp, _vp, G, _vp, _sz, _vp],
         "wm_layer_step_backward": [D, P, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, G,
                                    _vp, _sz, _vp],
+        "wm_prefill_passes_backward": [D, P, _vp, _vp, _i32p, ctypes.c_int32, ctypes.c_int32,
+                                       _vp, _vp, _vp, _vp, G, _vp, _sz, _vp],
         "wm_layer_attend": [D, P, ctypes.c_int32, _vp, _i32p, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
         "wm_prefill_passes": [D, P, _vp, _vp, _i32p, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp,
                               _sz, _vp],
@@ -107,6 +109,8 @@ def lib() -> ctypes.CDLL:
         fn.restype = ctypes.c_int
     L.wm_workspace_size.argtypes = [D, ctypes.c_int]
     L.wm_workspace_size.restype = ctypes.c_size_t
+    L.wm_passes_backward_workspace.argtypes = [D, ctypes.c_int32]
+    L.wm_passes_backward_workspace.restype = ctypes.c_size_t
     L.wm_last_error.restype = ctypes.c_char_p
     L.wm_version.restype = ctypes.c_char_p
     _lib = L
@@ -332,6 +336,25 @@ def layer_step_backward(dims: Dims, params, H, chan_map, ctx_len, Kc, Vc, O, dO,
                                         _map(chan_map), _ptr(ctx_len), _ptr(Kc), _ptr(Vc),
                                         _ptr(O), _ptr(dO), _ptr(dKc), _ptr(dVc), _ptr(dH),
                                         _grads(grads), wp, wn, _stream(stream)))
+
+
+def passes_backward_workspace(dims: Dims, n_grad: int) -> int:
+    return int(lib().wm_passes_backward_workspace(ctypes.byref(dims), n_grad))
+
+
+def prefill_passes_backward(dims: Dims, params, W_o, X, chan_map, passes: int, n_grad: int,
+                            dh_top, dX, dW_o, grads, h_top=None, ws=None, stream=None):
+    """Jacobi passes, then the gradients of <dh_top, h_top> through the last n_grad passes:
+    added into dX, dW_o and grads (float32 tensors); h_top (bf16, optional) receives the
+    forward's top state."""
+    if ws is None and getattr(X, "device", None) is not None:
+        ws = torch.empty(max(passes_backward_workspace(dims, n_grad), 256), dtype=torch.uint8,
+                         device=X.device)
+    wp, wn = (ws.data_ptr(), ws.numel()) if ws is not None else (None, 0)
+    _check(lib().wm_prefill_passes_backward(ctypes.byref(dims), _pref(params), _ptr(W_o), _ptr(X),
+                                            _map(chan_map), passes, n_grad, _ptr(dh_top),
+                                            _ptr(h_top), _ptr(dX), _ptr(dW_o), _grads(grads), wp,
+                                            wn, _stream(stream)))
 
 
 def channel_attend_static(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, O, stream=None):

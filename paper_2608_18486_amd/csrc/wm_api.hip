@@ -164,9 +164,22 @@ Layout grad_layout(const wm_dims& d, int op) {
 }
 
 // Workspace regions for an op (offsets in bytes, each 256-byte aligned).
+struct PassBwdLayout {
+  size_t fw = 0, hs = 0, kp = 0, op = 0, gcur = 0, gb = 0, dof = 0, dob = 0, dql = 0, h1 = 0,
+         rows = 0, gkd = 0, dpk = 0, dpv = 0, dhn = 0, sub = 0, total = 0;
+  size_t state = 0, cache = 0, outs = 0;  // bytes of one state array, cache, output set
+};
+
+PassBwdLayout passes_bwd_layout(const wm_dims& d, int n_grad);
+
 Layout layout(const wm_dims& dd, int op) {
   if (op == WM_OP_Q_BACKWARD || op == WM_OP_POOL_BACKWARD || op == WM_OP_STEP_BACKWARD)
     return grad_layout(dd, op);
+  if (op == WM_OP_PASSES_BACKWARD) {  // the size with a one-pass window
+    Layout Ly;
+    Ly.total = passes_bwd_layout(dd, 1).total;
+    return Ly;
+  }
   Layout Ly;
   const bool passes = op == WM_OP_PASSES;
   // the pass driver works on one group at a time: its scratch is sized by a group (the
@@ -226,13 +239,13 @@ bool uses_cache(int op) {
   return op == WM_OP_KV_PROJECT || op == WM_OP_CHANNEL_ATTEND || op == WM_OP_LAYER_STEP ||
          op == WM_OP_POOL || op == WM_OP_LAYER_ATTEND || op == WM_OP_PASSES ||
          op == WM_OP_DENSE_ATTEND || op == WM_OP_ATTEND_BACKWARD || op == WM_OP_POOL_BACKWARD ||
-         op == WM_OP_STEP_BACKWARD;
+         op == WM_OP_STEP_BACKWARD || op == WM_OP_PASSES_BACKWARD;
 }
 
 int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
   if (!dp) return fail(WM_ERR_ARG, "dims is NULL");
   const wm_dims& d = *dp;
-  if (op < WM_OP_ROUTER_MIX || op > WM_OP_STEP_BACKWARD) return fail(WM_ERR_ARG, "unknown op %d", op);
+  if (op < WM_OP_ROUTER_MIX || op > WM_OP_PASSES_BACKWARD) return fail(WM_ERR_ARG, "unknown op %d", op);
   if (d.dtype != WM_F32 && d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "unknown dtype %d", d.dtype);
   if (d.mix_mode != WM_MIX_LINEAR && d.mix_mode != WM_MIX_SOFTMAX)
     return fail(WM_ERR_DTYPE, "unknown mix_mode %d", d.mix_mode);
@@ -262,7 +275,8 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
     return fail(WM_ERR_ARG, "group must be in [0, groups)");
   // positions the call covers: the pass driver's T_new is the whole sequence, the other
   // calls place their tokens at group + groups i
-  const long long span = op == WM_OP_PASSES ? (long long)d.T_new : call_span(d);
+  const bool pass_op = op == WM_OP_PASSES || op == WM_OP_PASSES_BACKWARD;
+  const long long span = pass_op ? (long long)d.T_new : call_span(d);
   if ((long long)d.ctx_max + span > INT_MAX / 2)
     return fail(WM_ERR_SHAPE, "positions past the 32-bit range");
   if (uses_cache(op)) {
@@ -290,14 +304,17 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
     for (double v : views)
       if (v >= lim) return fail(WM_ERR_SHAPE, "an operand spans more than 2 GiB (%.0f B)", v);
   }
-  if (op == WM_OP_PASSES) {
+  if (op == WM_OP_PASSES_BACKWARD && group_stride(d) > 1)
+    return fail(WM_ERR_ARG, "the pass gradients run Jacobi passes: groups must be <= 1");
+  if (pass_op) {
     if (d.group != 0) return fail(WM_ERR_ARG, "the pass driver runs every group: group must be 0");
     if (d.T_new % group_stride(d) != 0)
       return fail(WM_ERR_SHAPE, "the pass driver needs T_new a multiple of groups");
     if (d.ctx_max != 0) return fail(WM_ERR_ARG, "the pass driver starts empty sequences: ctx_max 0");
   }
   if (op == WM_OP_ROUTER_MIX || op == WM_OP_LAYER_STEP || op == WM_OP_POOL ||
-      op == WM_OP_PASSES || op == WM_OP_POOL_BACKWARD || op == WM_OP_STEP_BACKWARD) {
+      op == WM_OP_PASSES || op == WM_OP_POOL_BACKWARD || op == WM_OP_STEP_BACKWARD ||
+      op == WM_OP_PASSES_BACKWARD) {
     size_t lds = wm::mix_smem_bytes(d.L, d.k, d.D, elem_size(d));
     if (lds > 65536) return fail(WM_ERR_SHAPE, "L * D too large for the mix kernel (%zu B of LDS)", lds);
   }
@@ -797,6 +814,186 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
     // pre-mix norm backward into dH: rows (l, n) at n L + l
     rms_backward(dhn, 1, L, H, 1, L, dH, 1, L, rinv, 1, L, gpre, D, L, N, true, dgp, s);
     wm::launch_grad_sum(dgp, L, kGradChunks, D, G.g_pre + (long)br * L * D, 1.f, 1, s);
+  }
+}
+
+
+// ------------------------------------------- Section 3.3: truncated backpropagation
+// Workspace of wm_prefill_passes_backward: the forward's scratch, what the gradient
+// window keeps of its passes (the states H^(t) for t = passes - n_grad .. passes, the
+// caches and the per-layer attention outputs of the window's passes), and the backward's
+// scratch (the Q-side and pool-side gradient workspaces share one region).
+
+wm_dims one_consumer(const wm_dims& d) {
+  wm_dims d1 = d;
+  d1.L = 1;
+  d1.k = 1;
+  d1.p = 1;
+  return d1;
+}
+
+PassBwdLayout passes_bwd_layout(const wm_dims& d, int n_grad) {
+  PassBwdLayout Ly;
+  const size_t N = (size_t)d.B * d.T_new, L = d.L, D = d.D, HQ = (size_t)d.Hq * d.d;
+  Ly.state = N * L * D * 2;
+  Ly.cache = (size_t)d.k * d.B * d.Hkv * d.S_cap * d.d * 2;
+  Ly.outs = L * N * HQ * 2;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += al256(bytes);
+    return at;
+  };
+  Ly.fw = take(layout(d, WM_OP_PASSES).total);
+  Ly.hs = take(al256(Ly.state) * (n_grad + 1));
+  Ly.kp = take(al256(Ly.cache) * 2 * n_grad);
+  Ly.op = take(al256(Ly.outs) * n_grad);
+  Ly.gcur = take(N * D * 4);
+  Ly.gb = take(N * D * 2);
+  Ly.dof = take(N * HQ * 4);
+  Ly.dob = take(N * HQ * 2);
+  Ly.dql = take(N * HQ * 4);
+  Ly.h1 = take(N * D * 2);
+  Ly.rows = take(wm::attend_backward_rows_bytes(make_shape(one_consumer(d))));
+  Ly.gkd = take(2 * (size_t)d.Hkv * d.d * 4);
+  Ly.dpk = take(Ly.cache * 2);
+  Ly.dpv = take(Ly.cache * 2);
+  Ly.dhn = take(N * L * D * 4);
+  wm_dims dq = d;
+  dq.L = 1;
+  Ly.sub = take(std::max(layout(dq, WM_OP_Q_BACKWARD).total, layout(d, WM_OP_POOL_BACKWARD).total));
+  Ly.total = N == 0 ? 0 : off;
+  return Ly;
+}
+
+// Jacobi passes (groups <= 1) as the fixed point's iteration: H^(0) = X in every layer; pass
+// t pools H^(t-1) into the caches, then recomputes H^(t) = States(X; caches) layer by
+// layer. The passes before the gradient window run in scratch; the window's passes keep
+// their input states, caches and per-layer outputs. Then the backward, pass by pass from
+// the last: the stand-in blocks and the consumers' attention and queries layer by layer
+// from the top (the residual stream's gradient in gcur), then the pool of the pass's
+// caches into the gradient of the states it read, which the pass before receives; the
+// states entering the window are held fixed (their gradient is dropped) unless the window
+// starts at H^(0), whose gradient goes to X.
+void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, const bf16* X,
+                         const int32_t* chan_map, int passes, int n_grad, const float* dh_top,
+                         bf16* h_top, float* dX, float* dW_o, const wm_grads& G, void* ws,
+                         hipStream_t s) {
+  const PassBwdLayout Ly = passes_bwd_layout(d, n_grad);
+  const Layout Lf = layout(d, WM_OP_PASSES);
+  void* fw = at(ws, Ly.fw);
+  const wm::Shape sh = make_shape(d);
+  const int L = d.L, D = d.D, HQ = d.Hq * d.d, N = sh.N();
+  const long cslice = (long)d.B * d.Hkv * d.S_cap * d.d;  // one channel of a cache
+  auto Hs = [&](int i) { return (bf16*)at(ws, Ly.hs + al256(Ly.state) * i); };
+  auto Kp = [&](int i) { return (bf16*)at(ws, Ly.kp + al256(Ly.cache) * (2 * (i - 1))); };
+  auto Vp = [&](int i) { return (bf16*)at(ws, Ly.kp + al256(Ly.cache) * (2 * (i - 1) + 1)); };
+  auto Os = [&](int i) { return (bf16*)at(ws, Ly.op + al256(Ly.outs) * (i - 1)); };
+  bf16* top = h_top ? h_top : (bf16*)at(fw, Lf.topg);
+  wm::launch_router_fold<bf16>(sh, router_layers(d), (const bf16*)P.g_pre, (const bf16*)P.W_alpha,
+                               (bf16*)at(fw, Lf.wa), s);
+  wm::launch_kv_fold<bf16>(sh, (const bf16*)P.g_mid, (const bf16*)P.Wk, (const bf16*)P.Wv,
+                           (bf16*)at(fw, Lf.wkv), s);
+  wm::launch_q_fold<bf16>(sh, (const bf16*)P.g_in, (const bf16*)P.Wq, (bf16*)at(fw, Lf.wq), 0, L,
+                          s);
+  wm::launch_rope_table(sh, nullptr, (float*)at(fw, Lf.tab), s);
+  // one pass: pool H_in into (K, V), then the states into H_out (layer 0 = X) and top,
+  // the layers' attention outputs into O (layer l at l N HQ) or scratch
+  auto pass = [&](const bf16* H_in, bf16* K, bf16* V, bf16* H_out, bf16* O) {
+    run_pool<bf16>(d, P, H_in, nullptr, K, V, Lf, fw, s, false, true, true);
+    if (H_out != H_in) wm::launch_group_gather<bf16>(X, H_out, d.B, d.T_new, 1, L, D, s);
+    for (int l = 0; l < L; ++l) {
+      bf16* Ol = O ? O + (long)l * N * HQ : (bf16*)at(fw, Lf.ol);
+      run_layer_attend<bf16>(d, P, l, H_out, chan_map, nullptr, K, V, Ol, Lf, fw, s, true, true);
+      const bool last = l + 1 == L;
+      wm::launch_block_residual<bf16>(N, D, HQ, Ol, W_o + (long)l * D * HQ, H_out + (long)l * D,
+                                      (long)L * D, last ? top : H_out + (long)(l + 1) * D,
+                                      last ? D : (long)L * D, s);
+    }
+  };
+  // H^(0), then the passes before the window (in place in Hs(0), caches in slot 1)
+  wm::launch_group_gather<bf16>(X, Hs(0), d.B, d.T_new, 1, L, D, s);
+  for (int t = 1; t <= passes - n_grad; ++t) pass(Hs(0), Kp(1), Vp(1), Hs(0), nullptr);
+  for (int i = 1; i <= n_grad; ++i) pass(Hs(i - 1), Kp(i), Vp(i), Hs(i), Os(i));
+
+  // backward
+  float* gcur = (float*)at(ws, Ly.gcur);
+  bf16* gb = (bf16*)at(ws, Ly.gb);
+  float* dof = (float*)at(ws, Ly.dof);
+  bf16* dob = (bf16*)at(ws, Ly.dob);
+  float* dql = (float*)at(ws, Ly.dql);
+  bf16* h1 = (bf16*)at(ws, Ly.h1);
+  float* dpk = (float*)at(ws, Ly.dpk);
+  float* dpv = (float*)at(ws, Ly.dpv);
+  float* dhn = (float*)at(ws, Ly.dhn);
+  float* gkd = (float*)at(ws, Ly.gkd);
+  void* sub = at(ws, Ly.sub);
+  const wm_dims d1 = one_consumer(d);
+  const wm::Shape sh1 = make_shape(d1);
+  wm::LayerTable m0{};
+  wm::ChannelGroups cg0{};
+  cg0.offsets[1] = 1;
+  wm_dims dq = d;
+  dq.L = 1;
+  const Layout Lq = layout(dq, WM_OP_Q_BACKWARD), Lp = layout(d, WM_OP_POOL_BACKWARD);
+  const bool paper = d.mask_mode == WM_MASK_PAPER;
+  const long cache_elems = (long)d.k * cslice;
+  bool have_dhn = false;
+  for (int i = n_grad; i >= 1; --i) {
+    const bf16* H = Hs(i);
+    const bf16* O = Os(i);
+    if (i == n_grad) {
+      wm::launch_grad_fill(gcur, (long)N * D, 0.f, s);
+      wm::launch_grad_add_rows(gcur, dh_top, N, D, D, 1, s);
+    } else {
+      wm::launch_grad_fill(gcur, (long)N * D, 0.f, s);
+    }
+    wm::launch_grad_fill(dpk, cache_elems, 0.f, s);
+    wm::launch_grad_fill(dpv, cache_elems, 0.f, s);
+    for (int l = L - 1; l >= 0; --l) {
+      const int c = chan_map[l];
+      const bf16* Ol = O + (long)l * N * HQ;
+      // gcur: the gradient in h_{l+1}. do_l = W_o[l]^T gcur, dW_o[l] += gcur^T o_l
+      wm::launch_grad_cast(gcur, gb, (long)N * D, s);
+      gemm(opnd(gb, D, 1, 0, false), opnd(W_o + (long)l * D * HQ, 1, HQ, 0, false), dof, HQ, 1, 0,
+           N, HQ, D, 1, false, s);
+      wm::launch_grad_cast(dof, dob, (long)N * HQ, s);
+      gemm(opnd(gb, 1, D, 0, false), opnd(Ol, 1, HQ, 0, false), dW_o + (long)l * D * HQ, HQ, 1, 0,
+           D, HQ, N, 1, true, s);
+      // layer l's queries again, then its attention gradients on channel c alone
+      bf16* Ql = (bf16*)at(fw, Lf.q);
+      float* rinv = (float*)at(fw, Lf.rinv);
+      wm::launch_row_rms_strided<bf16>(H + (long)l * D, N, D, (long)L * D, L, sh.eps, rinv + l, s);
+      wm::launch_q_layers<bf16>(sh, H, rinv, (const bf16*)P.g_qnorm, (const float*)at(fw, Lf.tab),
+                                Ql, (const bf16*)at(fw, Lf.wq), l, 1, s);
+      const long dofs = ((long)c * d.Hkv) * d.d;
+      wm::launch_attend_backward(sh1, m0, cg0, Ql, Kp(i) + c * cslice, Vp(i) + c * cslice,
+                                 (const bf16*)P.Kd + dofs, (const bf16*)P.Vd + dofs, Ol, dob,
+                                 nullptr, dql, dpk + c * cslice, dpv + c * cslice,
+                                 paper ? G.Kd + dofs : gkd,
+                                 paper ? G.Vd + dofs : gkd + (long)d.Hkv * d.d,
+                                 (float*)at(ws, Ly.rows), s, true);
+      // the queries' backward of layer l adds its h_l gradient into gcur
+      wm::launch_grad_copy_rows(H + (long)l * D, (long)L * D, h1, N, D, s);
+      wm_params P1 = P;
+      P1.g_in = (const bf16*)P.g_in + (long)l * D;
+      P1.Wq = (const bf16*)P.Wq + (long)l * HQ * D;
+      P1.g_qnorm = (const bf16*)P.g_qnorm + (long)l * d.d;
+      wm_grads G1 = G;
+      G1.g_in = G.g_in + (long)l * D;
+      G1.Wq = G.Wq + (long)l * HQ * D;
+      G1.g_qnorm = G.g_qnorm + (long)l * d.d;
+      run_q_backward(dq, P1, h1, nullptr, dql, gcur, G1, Lq, sub, s);
+      // and the gradient the next pass's pool sent to h_l
+      if (have_dhn) wm::launch_grad_add_rows(gcur, dhn + (long)l * D, N, D, (long)L * D, 1, s);
+    }
+    wm::launch_grad_add_rows(dX, gcur, N, D, D, 1, s);  // h_0 = X
+    // the pool that made this pass's caches from the states of the pass before
+    wm::launch_grad_fill(dhn, (long)N * L * D, 0.f, s);
+    run_pool_backward(d, P, Hs(i - 1), nullptr, dpk, dpv, dhn, G, Lp, sub, s);
+    have_dhn = i > 1;
+    if (i == 1 && n_grad == passes)  // H^(0) = X in every layer
+      wm::launch_grad_add_rows(dX, dhn, N, D, (long)L * D, L, s);
   }
 }
 
@@ -1311,6 +1508,51 @@ int wm_layer_step_backward(const wm_dims* dims, const wm_params* params, const v
                              (float*)at(ws, Ly.part), s, true);
   run_q_backward(d, P, (const bf16*)H, ctx_len, dQ, dH, *grads, Ly, ws, s);
   run_pool_backward(d, P, (const bf16*)H, ctx_len, dKc, dVc, dH, *grads, Ly, ws, s);
+  return launched();
+}
+
+size_t wm_passes_backward_workspace(const wm_dims* dims, int32_t n_grad) {
+  if (validate_dims(dims, WM_OP_PASSES_BACKWARD, nullptr) != WM_OK || n_grad < 1) return 0;
+  return passes_bwd_layout(*dims, n_grad).total;
+}
+
+int wm_prefill_passes_backward(const wm_dims* dims, const wm_params* params, const void* W_o,
+                               const void* X, const int32_t* chan_map, int32_t passes,
+                               int32_t n_grad, const float* dh_top, void* h_top, float* dX,
+                               float* dW_o, const wm_grads* grads, void* ws, size_t ws_bytes,
+                               wm_stream_t stream) {
+  if (!chan_map) return fail(WM_ERR_ARG, "chan_map is NULL");
+  WM_TRY(validate_dims(dims, WM_OP_PASSES_BACKWARD, chan_map));
+  const wm_dims& d = *dims;
+  if (passes < 1) return fail(WM_ERR_ARG, "passes must be >= 1");
+  if (n_grad < 1 || n_grad > passes) return fail(WM_ERR_ARG, "n_grad must be in [1, passes]");
+  if ((size_t)d.B * d.T_new == 0) return WM_OK;
+  WM_TRY(check_backward(d));
+  if (decode_path(d)) return fail(WM_ERR_SHAPE, "the pass gradients need T_new > 4");
+  WM_TRY(check_pool_grads(d, params, grads));
+  WM_TRY(check_params(params, {P_GIN, P_WQ, P_GQN}));
+  if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_KD, P_VD}));
+  WM_TRY(grad_ptr(grads->g_in, "g_in"));
+  WM_TRY(grad_ptr(grads->Wq, "Wq"));
+  WM_TRY(grad_ptr(grads->g_qnorm, "g_qnorm"));
+  if (d.mask_mode == WM_MASK_PAPER) {
+    WM_TRY(grad_ptr(grads->Kd, "Kd"));
+    WM_TRY(grad_ptr(grads->Vd, "Vd"));
+  }
+  WM_TRY(need_ptr(W_o, "W_o"));
+  WM_TRY(need_ptr(X, "X"));
+  if (h_top) WM_TRY(need_ptr(h_top, "h_top"));
+  WM_TRY(grad_ptr(dh_top, "(dh_top)"));
+  WM_TRY(grad_ptr(dX, "(dX)"));
+  WM_TRY(grad_ptr(dW_o, "(dW_o)"));
+  const size_t need = passes_bwd_layout(d, n_grad).total;
+  if (!ws) return fail(WM_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if ((uintptr_t)ws % 256 != 0) return fail(WM_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(WM_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+  (void)hipGetLastError();
+  run_passes_backward(d, *params, (const bf16*)W_o, (const bf16*)X, chan_map, passes, n_grad,
+                      dh_top, (bf16*)h_top, dX, dW_o, *grads, ws, (hipStream_t)stream);
   return launched();
 }
 

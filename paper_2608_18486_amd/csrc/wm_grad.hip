@@ -696,6 +696,62 @@ void launch_grad_colsum(const float* x, long rows, int n, int chunks, float* par
                      n, part);
 }
 
+// ------------------------------------------------- small elementwise helpers
+__global__ __launch_bounds__(256) void grad_fill_kernel(float* p, long n, float v) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+void launch_grad_fill(float* p, long n, float v, hipStream_t s) {
+  if (n > 0)
+    hipLaunchKernelGGL(grad_fill_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n,
+                       v);
+}
+
+__global__ __launch_bounds__(256) void grad_cast_kernel(const float* src, bf16* dst, long n) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = (bf16)src[i];
+}
+void launch_grad_cast(const float* src, bf16* dst, long n, hipStream_t s) {
+  if (n > 0)
+    hipLaunchKernelGGL(grad_cast_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,
+                       dst, n);
+}
+
+// dst[r][e] += sum over l < nsrc of src[r * src_stride + l * D + e] (rows of D)
+__global__ __launch_bounds__(256) void grad_add_rows_kernel(float* dst, const float* src,
+                                                            long rows, int D, long src_stride,
+                                                            int nsrc) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * D) return;
+  const long r = i / D;
+  const int e = (int)(i % D);
+  float v = 0.f;
+  for (int l = 0; l < nsrc; ++l) v += src[r * src_stride + (long)l * D + e];
+  dst[i] += v;
+}
+void launch_grad_add_rows(float* dst, const float* src, long rows, int D, long src_stride,
+                          int nsrc, hipStream_t s) {
+  const long n = rows * D;
+  if (n > 0)
+    hipLaunchKernelGGL(grad_add_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       dst, src, rows, D, src_stride, nsrc);
+}
+
+// dst[r][e] = src[r * src_stride + e] (bf16 rows of D)
+__global__ __launch_bounds__(256) void grad_copy_rows_kernel(const bf16* src, long src_stride,
+                                                             bf16* dst, long rows, int D) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * D) return;
+  dst[i] = src[(i / D) * src_stride + i % D];
+}
+void launch_grad_copy_rows(const bf16* src, long src_stride, bf16* dst, long rows, int D,
+                           hipStream_t s) {
+  const long n = rows * D;
+  if (n > 0)
+    hipLaunchKernelGGL(grad_copy_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       src, src_stride, dst, rows, D);
+}
+
 // Zeroes the router weight entries (o, m) whose source layer sel[m] lies above channel
 // o / L (the no-feedback ablation's mask): W [kL][Lp D] rows, in place (bf16 or fp32).
 template <typename T>

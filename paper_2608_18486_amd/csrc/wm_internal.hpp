@@ -208,6 +208,14 @@ void launch_grad_mix(const MixGradArgs& a, hipStream_t s);
 template <typename T>
 void launch_grad_mask(T* W, int kL, int L, int Lp, int D, const LayerTable& sel, hipStream_t s);
 
+void launch_grad_fill(float* p, long n, float v, hipStream_t s);
+void launch_grad_cast(const float* src, bf16* dst, long n, hipStream_t s);
+// dst[r][e] += sum over l < nsrc of src[r src_stride + l D + e]
+void launch_grad_add_rows(float* dst, const float* src, long rows, int D, long src_stride,
+                          int nsrc, hipStream_t s);
+void launch_grad_copy_rows(const bf16* src, long src_stride, bf16* dst, long rows, int D,
+                           hipStream_t s);
+
 // Split-S decode for small T_new; partials live in the workspace.
 size_t decode_partials_bytes(const Shape& sh);
 int decode_splits(const Shape& sh);

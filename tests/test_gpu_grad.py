@@ -176,3 +176,77 @@ def test_layer_step_backward(wm, mask_mode, d, Hq, Hkv, T_new, ctx):
             check_close(dVc_h[:, b, :, :c0], ref["dVc_ctx"][:, b, :, :c0], "bf16", "dVc ctx b%d" % b)
         # slots past the call's span are never written
         assert not np.any(dKc_h[:, b, :, c0 + w.T_new:]) and not np.any(dVc_h[:, b, :, c0 + w.T_new:])
+
+
+# ------------------------------------------------ passes with truncated backprop
+
+PASS_CASES = [
+    dict(),
+    dict(mask_mode=1, mix_mode=1),
+    dict(d=96, Hq=6, Hkv=3, p=2, L=5, k=3),
+    dict(router_mode=1),
+]
+
+
+@pytest.mark.parametrize("case", range(len(PASS_CASES)))
+@pytest.mark.parametrize("passes,n_grad", [(2, 2), (3, 1), (3, 2)])
+def test_prefill_passes_backward(wm, case, passes, n_grad):
+    """The passes' forward and the truncated backward against the oracle's autograd of the
+    same passes with the states entering the window detached."""
+    kw = dict(PASS_CASES[case])
+    modes = {m: kw.pop(m) for m in ("mix_mode", "router_mode", "mask_mode") if m in kw}
+    shape = dict(d=64, Hq=4, Hkv=2, L=4, k=2, p=1)
+    shape.update(kw)
+    w = synth.small("pp%d" % case, B=2, T_new=150, D=128, ctx=0, dtype="bf16", **shape)
+    print("passes backward case %d %s passes %d window %d" % (case, modes, passes, n_grad),
+          flush=True)
+    P = synth.make_params(w, _bias(w), gains="random")
+    X = synth.make_embeddings(w)
+    # the block's output projection at std 0.4 (20 times the forward tests' 0.02): at 0.02
+    # the layers' states differ from the embedding by a few percent, every normed state is
+    # then nearly parallel to every mixed channel, and the router's and pre-mix gains'
+    # gradients (dalpha_jl = dh~_j . h^_l with dh~_j orthogonal to h~_j) become small
+    # differences that the states' bf16 rounding swamps
+    W_o = (synth.make_out_proj(w).float() * 20.0).to(torch.bfloat16)
+    dh = synth._normal((w.B, w.T_new, w.D), 1.0, 801, torch.float32)
+    od = _odims(w, S_cap=w.T_new, **modes)
+    ref = ob.passes_grads(od, P, _f64(W_o), _f64(X), w.chan_map, passes, n_grad,
+                          dh.double().numpy())
+    # how far bf16 storage of the states, caches, queries and outputs moves each gradient
+    # (the oracle's own measure of the gradient's sensitivity to that rounding)
+    stored = ob.passes_grads(od, P, _f64(W_o), _f64(X), w.chan_map, passes, n_grad,
+                             dh.double().numpy(), bf16_storage=True)
+    _, top_ref = ob.passes_forward(od, {n: ob._t(P[n]) for n in ob.PARAM_NAMES}, ob._t(W_o),
+                                   ob._t(X), w.chan_map, passes, n_grad)
+    names = [n for n in ob.PARAM_NAMES if not (n == "W_alpha" and modes.get("router_mode") == 1)
+             and not (n in ("Kd", "Vd") and modes.get("mask_mode") == 1)]
+    dims = _gdims(wm, w, S_cap=w.T_new, ctx_max=0, **modes)
+    dX0 = synth._normal(tuple(X.shape), 1.0, 802, torch.float32).cuda()
+    dX = dX0.clone()
+    dW0 = synth._normal(tuple(W_o.shape), 0.5, 803, torch.float32).cuda()
+    dW = dW0.clone()
+    g0 = _grads_like(P, names, 804)
+    g = {n: t.clone() for n, t in g0.items()}
+    top = torch.empty(tuple(X.shape), dtype=torch.bfloat16, device="cuda")
+    wm.prefill_passes_backward(dims, _dev(P), W_o.cuda(), X.cuda(), w.chan_map, passes, n_grad,
+                               dh.cuda(), dX, dW, g, h_top=top)
+    torch.cuda.synchronize()
+    check_close(top.cpu(), top_ref.detach().numpy(), "bf16", "h_top")
+    # Every stage of the gradient chain (a layer's block, attention and query; a pass's
+    # pool) works on bf16 operands and stays within the bf16 bound on its own; down a
+    # chain of S stages the rounding adds up like a random walk. The bound is scaled by
+    # sqrt(S / 4) (four stages: the depth of the single-step tests' chain), with
+    # S = n_grad (3 L + 2) for the deepest path, from h_top back to X. Where the gradient
+    # itself is sensitive to rounding (the linear router's logits when the layers' states
+    # are nearly parallel, e.g. H^(0) = X in every layer), twice the oracle's own
+    # storage-rounding shift is allowed on top.
+    depth = n_grad * (3 * w.L + 2)
+    scale = max(1.0, float(np.sqrt(depth / 4.0)))
+    got = {"dX": (dX - dX0).cpu(), "dW_o": (dW - dW0).cpu()}
+    got.update({"d" + n: (g[n] - g0[n]).cpu() for n in names})
+    for n, v in got.items():
+        r = ref[n]
+        rms = float(np.sqrt(np.mean(np.square(r))))
+        shift = float(np.abs(stored[n] - r).max())
+        check_close(v, r, "bf16", "passes %s" % n,
+                    slack=(scale - 1.0) * TOL_BF16_REL * (np.abs(r) + rms) + 2.0 * shift)

@@ -372,3 +372,27 @@ def test_truncated_pass_gradients_match_finite_differences(kw, passes, n_grad):
         num = _fd(f, x, v, eps=2e-5)
         ana = (g[name] * v).sum()
         assert abs(num - ana) <= 1e-6 * max(1.0, abs(num)), (name, num, ana)
+
+
+def test_bf16_storage_rounds_values_and_passes_gradients():
+    """bf16_store: the value is the bf16 rounding (round to nearest even, checked against
+    the float32 bit pattern rounded to its upper half), the derivative the identity."""
+    import torch
+    x = torch.tensor([1.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -9, -3.14159, 1e-3],
+                     dtype=torch.float64, requires_grad=True)
+    y = ob.bf16_store(x)
+    f = x.detach().numpy().astype(np.float32).view(np.uint32)
+    rnd = ((f + 0x7FFF + ((f >> 16) & 1)) & 0xFFFF0000).view(np.float32).astype(np.float64)
+    assert np.array_equal(y.detach().numpy(), rnd)
+    (g,) = torch.autograd.grad(y.sum(), x)
+    assert np.array_equal(g.numpy(), np.ones(5))
+    # storage rounding moves the passes' gradients by rounding-sized amounts
+    dm = _dims(T_new=5)
+    dm.S_cap = dm.T_new
+    P, W_o, X, dh, _ = _pass_inputs(dm)
+    cmap = [l % dm.k for l in range(dm.L)]
+    a = ob.passes_grads(dm, P, W_o, X, cmap, 2, 2, dh)
+    b = ob.passes_grads(dm, P, W_o, X, cmap, 2, 2, dh, bf16_storage=True)
+    for n in ("dX", "dW_o", "dWq", "dW_alpha"):
+        rel = np.abs(a[n] - b[n]).max() / np.abs(a[n]).max()
+        assert 1e-6 < rel < 0.1, (n, rel)
