@@ -47,7 +47,7 @@ struct Layout {
   // projection and its gradient, the pool side's normed states, mid-normed channels,
   // K/V pre-norm values and gradients, channel gradients, state gradients, logit gradients
   size_t dq = 0, dgp = 0, gkd = 0, x = 0, yq = 0, dyq = 0, dx = 0, hn = 0, u = 0, ydy = 0,
-         dyb = 0, du = 0, dhn = 0, dlog = 0, dlogb = 0;
+         dyb = 0, du = 0, dhn = 0, dlog = 0, dlogb = 0, split = 0;
 };
 
 int group_stride(const wm_dims& d) { return d.groups > 1 ? d.groups : 1; }
@@ -108,6 +108,21 @@ wm::Shape dense_shape(wm::Shape sh) {
 
 // Partial rows per gain or bias gradient: fixed, so every sum has one order on any device.
 constexpr int kGradChunks = 64;
+// fp32 scratch of the split-K weight-gradient GEMMs (K = the call's tokens)
+constexpr size_t kSplitElems = (size_t)8 << 20;
+// Partial rows of a gain gradient with `outer` gain rows: kGradChunks per row, more when
+// that would leave fewer than ~1024 workgroups (one layer at a time).
+int red_chunks(int outer) {
+  return std::max(kGradChunks, std::min(1024, (1024 + outer - 1) / std::max(outer, 1)));
+}
+// Floats of partial rows the gradient ops need at most: outer red_chunks(outer) rows of the
+// gain width for the gains (L or k rows of D, of d), kGradChunks rows of kL for the bias.
+size_t dgp_elems(const wm_dims& d) {
+  size_t m = (size_t)kGradChunks * d.k * d.L;
+  for (int outer : {d.L, d.k})
+    m = std::max(m, (size_t)outer * red_chunks(outer) * std::max(d.D, d.d));
+  return m;
+}
 
 // Workspace of the backward ops. The step's backward recomputes Q into q, takes the
 // attention gradients (dQ into dq), then runs the Q side and the pool side one after the
@@ -132,7 +147,8 @@ Layout grad_layout(const wm_dims& d, int op) {
   }
   Ly.rinv = take(N * L * 4);
   Ly.tab = take(N * d.d * 4);
-  Ly.dgp = take(std::max(std::max(L, k) * kGradChunks * D, kGradChunks * k * L) * 4);
+  Ly.dgp = take(dgp_elems(d) * 4);
+  Ly.split = take(kSplitElems * 4);
   const size_t base = off;
   size_t end = off;
   if (op == WM_OP_Q_BACKWARD || op == WM_OP_STEP_BACKWARD) {
@@ -166,7 +182,7 @@ Layout grad_layout(const wm_dims& d, int op) {
 // Workspace regions for an op (offsets in bytes, each 256-byte aligned).
 struct PassBwdLayout {
   size_t fw = 0, hs = 0, kp = 0, op = 0, gcur = 0, gb = 0, dof = 0, dob = 0, dql = 0, h1 = 0,
-         rows = 0, gkd = 0, dpk = 0, dpv = 0, dhn = 0, sub = 0, total = 0;
+         rows = 0, gkd = 0, dpk = 0, dpv = 0, dhn = 0, split = 0, sub = 0, total = 0;
   size_t state = 0, cache = 0, outs = 0;  // bytes of one state array, cache, output set
 };
 
@@ -644,10 +660,12 @@ wm::GemmOperand opnd(const void* p, long s_row, long s_k, long s_z, bool f32, bo
 }
 
 // C[z] (+)= A[z] B[z]^T over `batches`; see GemmArgs for the k / row limits.
+// part: kSplitElems floats of split-K scratch (or NULL: no split)
 void gemm(const wm::GemmOperand& A, const wm::GemmOperand& B, float* C, long c_row, long c_col,
           long c_z, int M, int N, int K, int batches, bool acc, hipStream_t s, long klo0 = 0,
-          long klo_dz = 0, long mlo0 = 0, long mlo_dz = 0) {
-  wm::GemmArgs g{A, B, C, c_row, c_col, c_z, M, N, K, acc ? 1 : 0, klo0, klo_dz, mlo0, mlo_dz};
+          long klo_dz = 0, long mlo0 = 0, long mlo_dz = 0, float* part = nullptr) {
+  wm::GemmArgs g{A, B, C, c_row, c_col, c_z, M, N, K, acc ? 1 : 0, klo0, klo_dz, mlo0, mlo_dz,
+                 part, part ? (long)kSplitElems : 0, 1, 0};
   wm::launch_grad_gemm(g, batches, s);
 }
 
@@ -655,14 +673,15 @@ void gemm(const wm::GemmOperand& A, const wm::GemmOperand& B, float* C, long c_r
 void rms_backward(const float* dy, long dy_o, long dy_i, const bf16* x, long x_o, long x_i,
                   float* out, long out_o, long out_i, const float* rinv, long r_o, long r_i,
                   const bf16* g, int D, int nouter, int ninner, bool acc, float* dgp,
-                  hipStream_t s) {
+                  hipStream_t s, int* chunks) {
   wm::RmsArgs a;
   a.dy = dy, a.dy_o = dy_o, a.dy_i = dy_i;
   a.x = x, a.x_o = x_o, a.x_i = x_i;
   a.out = out, a.out_o = out_o, a.out_i = out_i;
   a.rinv = rinv, a.r_o = r_o, a.r_i = r_i;
   a.g = g, a.dgp = dgp;
-  a.D = D, a.ninner = ninner, a.chunks = kGradChunks, a.accumulate = acc ? 1 : 0;
+  a.D = D, a.ninner = ninner, a.chunks = red_chunks(nouter), a.accumulate = acc ? 1 : 0;
+  *chunks = a.chunks;
   wm::launch_grad_rms(a, nouter, s);
 }
 
@@ -711,18 +730,19 @@ void run_q_backward(const wm_dims& d, const wm_params& P, const bf16* H, const i
   h.src = dQ, h.sZ = (long)d.B * d.Hq * d.T_new, h.sB = (long)d.Hq * d.T_new, h.sH = d.T_new;
   h.slot_ctx = 0, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
   h.y = yq, h.dy = dyq, h.g = (const bf16*)P.g_qnorm, h.tab = tab, h.dgp = dgp;
-  h.B = d.B, h.H = d.Hq, h.T = d.T_new, h.chunks = kGradChunks, h.eps = d.eps;
+  h.B = d.B, h.H = d.Hq, h.T = d.T_new, h.chunks = red_chunks(L), h.eps = d.eps;
   wm::launch_grad_head(h, L, d.d, s);
-  wm::launch_grad_sum(dgp, L, kGradChunks, d.d, G.g_qnorm, 1.f, 1, s);
+  wm::launch_grad_sum(dgp, L, h.chunks, d.d, G.g_qnorm, 1.f, 1, s);
   // dx_l = dy_l Wq_l [N][D] (into [N][L][D]); dWq_l += dy_l^T x_l [HQ][D]
   gemm(opnd(dyq, HQ, 1, (long)N * HQ, false), opnd(Wq, 1, D, (long)HQ * D, false), dx,
        (long)L * D, 1, D, N, D, HQ, L, false, s);
   gemm(opnd(dyq, 1, HQ, (long)N * HQ, false), opnd(x, 1, (long)L * D, D, false), G.Wq, D, 1,
-       (long)HQ * D, HQ, D, N, L, true, s);
+       (long)HQ * D, HQ, D, N, L, true, s, 0, 0, 0, 0, (float*)at(ws, Ly.split));
   // input norm backward: rows (l, n) at n L + l
+  int nch = 0;
   rms_backward(dx, 1, L, H, 1, L, dH, 1, L, rinv, 1, L, (const bf16*)P.g_in, D, L, N, true, dgp,
-               s);
-  wm::launch_grad_sum(dgp, L, kGradChunks, D, G.g_in, 1.f, 1, s);
+               s, &nch);
+  wm::launch_grad_sum(dgp, L, nch, D, G.g_in, 1.f, 1, s);
 }
 
 // Gradients of the pool (Steps 1-2) for the gradients of the call's new cache slots
@@ -775,9 +795,9 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
       h.src = dKc, h.sZ = (long)d.B * d.Hkv * d.S_cap, h.sB = (long)d.Hkv * d.S_cap;
       h.sH = d.S_cap, h.slot_ctx = 1, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
       h.y = ydy, h.dy = dyb, h.g = (const bf16*)P.g_knorm, h.tab = tab, h.dgp = dgp;
-      h.B = d.B, h.H = d.Hkv, h.T = d.T_new, h.chunks = kGradChunks, h.eps = d.eps;
+      h.B = d.B, h.H = d.Hkv, h.T = d.T_new, h.chunks = red_chunks(k), h.eps = d.eps;
       wm::launch_grad_head(h, k, d.d, s);
-      wm::launch_grad_sum(dgp, k, kGradChunks, d.d, G.g_knorm, 1.f, 1, s);
+      wm::launch_grad_sum(dgp, k, h.chunks, d.d, G.g_knorm, 1.f, 1, s);
     } else {
       wm::launch_grad_gather(dVc, k, d.B, d.Hkv, d.T_new, d.S_cap, d.d, ctx_len, sh.ctx_hi, dyb,
                              s);
@@ -786,10 +806,12 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
     gemm(opnd(dyb, HK, 1, (long)N * HK, false), opnd(W, 1, D, (long)HK * D, false), du, D, 1,
          (long)N * D, N, D, HK, k, false, s);
     gemm(opnd(dyb, 1, HK, (long)N * HK, false), opnd(u, 1, D, (long)N * D, false),
-         br ? G.Wv : G.Wk, D, 1, (long)HK * D, HK, D, N, k, true, s);
+         br ? G.Wv : G.Wk, D, 1, (long)HK * D, HK, D, N, k, true, s, 0, 0, 0, 0,
+         (float*)at(ws, Ly.split));
     // mid norm backward in place: du becomes the mixed channels' gradient
-    rms_backward(du, N, 1, mix_b, N, 1, du, N, 1, rmid, N, 1, gmid, D, k, N, false, dgp, s);
-    wm::launch_grad_sum(dgp, k, kGradChunks, D, G.g_mid + (long)br * k * D, 1.f, 1, s);
+    int nch = 0;
+    rms_backward(du, N, 1, mix_b, N, 1, du, N, 1, rmid, N, 1, gmid, D, k, N, false, dgp, s, &nch);
+    wm::launch_grad_sum(dgp, k, nch, D, G.g_mid + (long)br * k * D, 1.f, 1, s);
     // mix backward: dhn (written) and the logits' gradient
     wm::MixGradArgs m{H, gpre, rinv, du, alpha + (long)br * N * kL, dhn, dlog, dlogb, N, L, k,
                       D, d.mix_mode == WM_MIX_SOFTMAX ? 1 : 0, nofb ? 1 : 0, kLp};
@@ -809,11 +831,11 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
       gemm(opnd(dlogb, 1, kLp, 0, false, true),
            opnd(hn + s0 * D, 1, (long)L * D, (long)d.p * D, false),
            G.W_alpha + (long)br * kL * Lp * D, (long)Lp * D, 1, D, kL, D, N, Lp, true, s, 0, 0,
-           klo0, klo_dz);
+           klo0, klo_dz, (float*)at(ws, Ly.split));
     }
     // pre-mix norm backward into dH: rows (l, n) at n L + l
-    rms_backward(dhn, 1, L, H, 1, L, dH, 1, L, rinv, 1, L, gpre, D, L, N, true, dgp, s);
-    wm::launch_grad_sum(dgp, L, kGradChunks, D, G.g_pre + (long)br * L * D, 1.f, 1, s);
+    rms_backward(dhn, 1, L, H, 1, L, dH, 1, L, rinv, 1, L, gpre, D, L, N, true, dgp, s, &nch);
+    wm::launch_grad_sum(dgp, L, nch, D, G.g_pre + (long)br * L * D, 1.f, 1, s);
   }
 }
 
@@ -859,6 +881,7 @@ PassBwdLayout passes_bwd_layout(const wm_dims& d, int n_grad) {
   Ly.dpk = take(Ly.cache * 2);
   Ly.dpv = take(Ly.cache * 2);
   Ly.dhn = take(N * L * D * 4);
+  Ly.split = take(kSplitElems * 4);
   wm_dims dq = d;
   dq.L = 1;
   Ly.sub = take(std::max(layout(dq, WM_OP_Q_BACKWARD).total, layout(d, WM_OP_POOL_BACKWARD).total));
@@ -959,7 +982,7 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
            N, HQ, D, 1, false, s);
       wm::launch_grad_cast(dof, dob, (long)N * HQ, s);
       gemm(opnd(gb, 1, D, 0, false), opnd(Ol, 1, HQ, 0, false), dW_o + (long)l * D * HQ, HQ, 1, 0,
-           D, HQ, N, 1, true, s);
+           D, HQ, N, 1, true, s, 0, 0, 0, 0, (float*)at(ws, Ly.split));
       // layer l's queries again, then its attention gradients on channel c alone
       bf16* Ql = (bf16*)at(fw, Lf.q);
       float* rinv = (float*)at(fw, Lf.rinv);

@@ -17,6 +17,8 @@
 //   attend_bwd_dummy_*     the dummy's dk, dv: a sum over every row of its readers.
 // Products run on the matrix cores in bf16 (P and dS rounded to bf16 as operands), sums
 // in fp32; gradients leave in fp32.
+#include <algorithm>
+
 #include "wm_device.hpp"
 #include "wm_frag.hpp"
 #include "wm_internal.hpp"
@@ -33,6 +35,7 @@ struct BwdArgs {
   LayerTable chan;
   ChannelGroups grp;
   int accumulate;  // add the slot and dummy gradients into dKc, dVc, dKd, dVd
+  int dchunks;     // partial sums per (channel, KV head) of the dummy's gradients
 };
 
 constexpr int kBwdThreads = 256;
@@ -402,21 +405,27 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) 
 
 // -------------------------------------------------------------------- dummy
 // The dummy's gradients sum over every row that reads its channel and KV head: the rows
-// (consumer, query head, sequence, position) are split into kDummyChunks contiguous
+// (consumer, query head, sequence, position) are split into dummy_chunks(sh) contiguous
 // chunks, one workgroup of 4 DH threads each (thread (rl, e) sums column e over every
 // fourth row of the chunk), and a second kernel adds the chunks in order.
-constexpr int kDummyChunks = 32;
+// chunks per (channel, KV head): at least 32, and enough for ~4096 workgroups in all (a
+// fixed function of the shape, so the sums keep one order on any device)
+static int dummy_chunks(const Shape& sh) {
+  const int pairs = sh.k * sh.Hkv;
+  return std::max(32, std::min(1024, (2048 + pairs - 1) / pairs));
+}
 
 template <int DH>
 __global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_part_kernel(BwdArgs a, float* part) {
   __shared__ float s_v[4 * DH], s_k[4 * DH];
-  const int ck = blockIdx.x / kDummyChunks, chunk = blockIdx.x % kDummyChunks;
+  const int nch = a.dchunks;
+  const int ck = blockIdx.x / nch, chunk = blockIdx.x % nch;
   const int c = ck / a.Hkv, kvh = ck % a.Hkv;
   const int tid = threadIdx.x, e = tid % DH, rl = tid / DH;
   const int G = a.Hq / a.Hkv;
   const long per_b = a.T, per_h = (long)a.B * per_b, per_m = G * per_h;
   const long nrow = (long)(a.grp.offsets[c + 1] - a.grp.offsets[c]) * per_m;
-  const long r0 = nrow * chunk / kDummyChunks, r1 = nrow * (chunk + 1) / kDummyChunks;
+  const long r0 = nrow * chunk / nch, r1 = nrow * (chunk + 1) / nch;
   float av = 0.f, ak = 0.f;
   if (a.mask_paper) {
     for (long rr = r0 + rl; rr < r1; rr += 4) {
@@ -438,23 +447,34 @@ __global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_part_kernel(BwdArgs a
   }
 }
 
+// The chunks' partial sums, added in a fixed order: thread (q, e) of 4 DH sums chunks
+// q, q + 4, ... of column e, then the four in order.
 template <int DH>
-__global__ __launch_bounds__(DH) void attend_bwd_dummy_sum_kernel(BwdArgs a, const float* part) {
-  const int ck = blockIdx.x, e = threadIdx.x;
+__global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_sum_kernel(BwdArgs a,
+                                                                       const float* part) {
+  __shared__ float s_v[4 * DH], s_k[4 * DH];
+  const int ck = blockIdx.x, tid = threadIdx.x, e = tid % DH, q = tid / DH;
   float v = 0.f, k = 0.f;
-  for (int ch = 0; ch < kDummyChunks; ++ch) {
-    const float* p = part + ((long)ck * kDummyChunks + ch) * 2 * DH;
+  for (int ch = q; ch < a.dchunks; ch += 4) {
+    const float* p = part + ((long)ck * a.dchunks + ch) * 2 * DH;
     v += p[e];
     k += p[DH + e];
   }
-  float* pv = a.dVd + (long)ck * DH + e;
-  float* pk = a.dKd + (long)ck * DH + e;
-  *pv = a.accumulate ? *pv + v : v;
-  *pk = a.accumulate ? *pk + k * a.scale : k * a.scale;
+  s_v[tid] = v;
+  s_k[tid] = k;
+  __syncthreads();
+  if (q == 0) {
+    v = (s_v[e] + s_v[DH + e]) + (s_v[2 * DH + e] + s_v[3 * DH + e]);
+    k = (s_k[e] + s_k[DH + e]) + (s_k[2 * DH + e] + s_k[3 * DH + e]);
+    float* pv = a.dVd + (long)ck * DH + e;
+    float* pk = a.dKd + (long)ck * DH + e;
+    *pv = a.accumulate ? *pv + v : v;
+    *pk = a.accumulate ? *pk + k * a.scale : k * a.scale;
+  }
 }
 
 size_t attend_backward_rows_bytes(const Shape& sh) {
-  return (4ul * sh.L * sh.B * sh.Hq * sh.T_new + 2ul * sh.k * sh.Hkv * kDummyChunks * sh.d) *
+  return (4ul * sh.L * sh.B * sh.Hq * sh.T_new + 2ul * sh.k * sh.Hkv * dummy_chunks(sh) * sh.d) *
          sizeof(float);
 }
 
@@ -470,20 +490,23 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
             rows + 2 * nrow, rows + 3 * nrow, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
             sh.mask_paper, sh.ctx_hi, (sh.T_new + 127) / 128,
             (int)(((long)sh.ctx_max + sh.T_new + 127) / 128), kLog2e / sqrtf((float)sh.d),
-            1.0f / sqrtf((float)sh.d), chan_map, groups, accumulate ? 1 : 0};
+            1.0f / sqrtf((float)sh.d), chan_map, groups, accumulate ? 1 : 0,
+            dummy_chunks(sh)};
   const dim3 ga(a.n_qtiles * sh.Hq * sh.B * sh.L), gb(a.n_stiles * sh.Hkv * sh.B * sh.k),
-      gp(sh.k * sh.Hkv * kDummyChunks), gs(sh.k * sh.Hkv);
+      gp(sh.k * sh.Hkv * a.dchunks), gs(sh.k * sh.Hkv);
   float* part = rows + 4 * nrow;
   if (sh.d == 64) {
     hipLaunchKernelGGL(attend_bwd_dq_kernel<64>, ga, dim3(kBwdThreads), 0, s, a);
     hipLaunchKernelGGL(attend_bwd_dkv_kernel<64>, gb, dim3(kBwdThreads), 0, s, a);
     hipLaunchKernelGGL(attend_bwd_dummy_part_kernel<64>, gp, dim3(4 * 64), 0, s, a, part);
-    hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<64>, gs, dim3(64), 0, s, a, (const float*)part);
+    hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<64>, gs, dim3(4 * 64), 0, s, a,
+                       (const float*)part);
   } else {
     hipLaunchKernelGGL(attend_bwd_dq_kernel<96>, ga, dim3(kBwdThreads), 0, s, a);
     hipLaunchKernelGGL(attend_bwd_dkv_kernel<96>, gb, dim3(kBwdThreads), 0, s, a);
     hipLaunchKernelGGL(attend_bwd_dummy_part_kernel<96>, gp, dim3(4 * 96), 0, s, a, part);
-    hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<96>, gs, dim3(96), 0, s, a, (const float*)part);
+    hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<96>, gs, dim3(4 * 96), 0, s, a,
+                       (const float*)part);
   }
 }
 

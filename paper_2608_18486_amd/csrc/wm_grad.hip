@@ -17,6 +17,8 @@
 //                          dh~_j . ĥ_l (fp32), then the softmax (or masking) backward into
 //                          the router logits' gradient.
 //   grad_sum_kernel        deterministic sums of partial rows (gain and bias gradients).
+#include <algorithm>
+
 #include "wm_device.hpp"
 #include "wm_frag.hpp"
 #include "wm_internal.hpp"
@@ -155,8 +157,10 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
   __shared__ __align__(16) char smem[2][C::TA_BYTES + C::TB_BYTES];  // [buffer][A | B]
   const int tm = (a.M + C::BM - 1) / C::BM, tn = (a.N + C::BN - 1) / C::BN;
   const int tile = xcd_tile(blockIdx.x, (int)gridDim.x);
-  const int z = tile / (tm * tn), t = tile % (tm * tn);
+  const int zs = tile / (tm * tn), t = tile % (tm * tn);
+  const int z = zs / a.splits, slice = zs % a.splits;
   const int m0 = (t / tn) * C::BM, n0 = (t % tn) * C::BN;
+  const int kbeg = slice * a.kchunk, kend = min(a.K, kbeg + a.kchunk);
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
   const int w = tid >> 6, wm = w % C::WGM, wn = w / C::WGM;
   const long za = (long)z * a.A.s_z, zb = (long)z * a.B.s_z;
@@ -167,14 +171,14 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < C::WN; ++j) acc[i][j] = zero16();
   bf16x8 va[C::VA], vb[C::VB];
-  const int nk = (a.K + 31) / 32;
+  const int nk = (kend - kbeg + 31) / 32;
   auto load = [&](int k0) {
     if constexpr (TA) gemm_load_t<C::BM, C::NT, C::VA, VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
     else gemm_load_n<C::BM, C::NT, C::VA, VEC>(a.A, za, m0, k0, a.M, a.K, 0, tid, va);
     if constexpr (TB) gemm_load_t<C::BN, C::NT, C::VB, VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
     else gemm_load_n<C::BN, C::NT, C::VB, VEC>(a.B, zb, n0, k0, a.N, a.K, klo, tid, vb);
   };
-  load(0);
+  load(kbeg);
   for (int kt = 0; kt < nk; ++kt) {
     char* sa = smem[kt & 1];
     char* sb = sa + C::TA_BYTES;
@@ -183,7 +187,7 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
     if constexpr (TB) gemm_store_t<C::BN, C::NT, C::VB>(sb, tid, vb);
     else gemm_store_n<C::NT, C::VB>(sb, tid, vb);
     __syncthreads();  // tile kt in LDS; every wave is done with tile kt - 1
-    if (kt + 1 < nk) load(32 * (kt + 1));
+    if (kt + 1 < nk) load(kbeg + 32 * (kt + 1));
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 fa[C::WM], fb[C::WN];
@@ -200,8 +204,12 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
     }
   }
   // lane (h, r): column n0 + 32 (WN wn + j) + r, rows m0 + 32 (WM wm + i) + 8 (q / 4) + 4 h + q % 4
-  float* Cz = a.C + (long)z * a.c_z;
-  const int mlo = (int)(a.m_lo0 + a.m_lo_dz * z);
+  // (split K: the slice's partial tile goes to part[z][slice] as M x N rows, written)
+  const bool split = a.splits > 1;
+  float* Cz = split ? a.part + ((long)z * a.splits + slice) * a.M * a.N : a.C + (long)z * a.c_z;
+  const long crow = split ? a.N : a.c_row, ccol = split ? 1 : a.c_col;
+  const int mlo = split ? 0 : (int)(a.m_lo0 + a.m_lo_dz * z);
+  const int acc_in = split ? 0 : a.accumulate;
 #pragma unroll
   for (int j = 0; j < C::WN; ++j) {
     const int n = n0 + 32 * (C::WN * wn + j) + r;
@@ -212,8 +220,8 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
       for (int q = 0; q < 16; ++q) {
         const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
         if (m < a.M && m >= mlo) {
-          float* p = Cz + (long)m * a.c_row + (long)n * a.c_col;
-          *p = a.accumulate ? *p + acc[i][j][q] : acc[i][j][q];
+          float* p = Cz + (long)m * crow + (long)n * ccol;
+          *p = acc_in ? *p + acc[i][j][q] : acc[i][j][q];
         }
       }
   }
@@ -229,9 +237,26 @@ static bool operand_vec(const GemmOperand& o, int nrows, int K) {
   return o.s_k == 1 && o.s_row % 8 == 0 && (K % 8 == 0 || o.pad8);
 }
 
+// C[z] (+)= sum over slices of part[z][slice], in slice order; rows below the batch's
+// m_lo untouched.
+__global__ __launch_bounds__(256) void grad_split_sum_kernel(GemmArgs a) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long mn = (long)a.M * a.N;
+  const int z = blockIdx.y;
+  if (idx >= mn) return;
+  const int m = (int)(idx / a.N), n = (int)(idx % a.N);
+  if (m < a.m_lo0 + a.m_lo_dz * z) return;
+  const float* p = a.part + (long)z * a.splits * mn + idx;
+  float v = 0.f;
+  for (int sl = 0; sl < a.splits; ++sl) v += p[sl * mn];
+  float* c = a.C + (long)z * a.c_z + (long)m * a.c_row + (long)n * a.c_col;
+  *c = a.accumulate ? *c + v : v;
+}
+
 template <class C, bool TA, bool TB, bool VEC>
 static void launch_gemm_cfg(const GemmArgs& a, int batches, hipStream_t s) {
-  const long tiles = (long)((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN) * batches;
+  const long tiles = (long)((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN) * batches *
+                     a.splits;
   hipLaunchKernelGGL((grad_gemm_kernel<C, TA, TB, VEC>), dim3((unsigned)tiles), dim3(C::NT), 0, s,
                      a);
 }
@@ -249,10 +274,28 @@ void launch_grad_gemm(GemmArgs a, int batches, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || batches <= 0) return;
   const bool vec = operand_vec(a.A, a.M, a.K) && operand_vec(a.B, a.N, a.K);
   const bool ta = operand_t(a.A), tb = operand_t(a.B);
+  // split K when the 128 x 128 tiles number under two per CU and K spans >= 64 K-steps
+  a.splits = 1;
+  a.kchunk = ((a.K + 31) / 32) * 32;
+  const long tiles = (long)((a.M + 127) / 128) * ((a.N + 127) / 128) * batches;
+  const long mnb = (long)a.M * a.N * batches;
+  if (vec && a.part && a.K >= 2048 && tiles < 2L * device_cus()) {
+    long sp = std::min<long>((2L * device_cus() + tiles - 1) / tiles, a.K / 1024);
+    sp = std::min<long>(sp, a.part_elems / std::max(mnb, 1L));
+    if (sp > 1) {
+      a.kchunk = (int)(((a.K + sp - 1) / sp + 31) / 32 * 32);
+      a.splits = (a.K + a.kchunk - 1) / a.kchunk;
+    }
+  }
   if (ta && tb) launch_gemm_t<true, true>(a, batches, vec, s);
   else if (ta) launch_gemm_t<true, false>(a, batches, vec, s);
   else if (tb) launch_gemm_t<false, true>(a, batches, vec, s);
   else launch_gemm_t<false, false>(a, batches, vec, s);
+  if (a.splits > 1) {
+    const long mn = (long)a.M * a.N;
+    hipLaunchKernelGGL(grad_split_sum_kernel, dim3((unsigned)((mn + 255) / 256), batches),
+                       dim3(256), 0, s, a);
+  }
 }
 
 // --------------------------------------------------------------- row kernels
@@ -499,22 +542,47 @@ void launch_grad_rms(const RmsArgs& a, int nouter, hipStream_t s) {
   else hipLaunchKernelGGL(grad_rms_kernel, grid, blk, 0, s, a);
 }
 
-// out[o][e] (+)= scale * sum over c < chunks of part[(o chunks + c) n + e] (fixed order).
-__global__ __launch_bounds__(256) void grad_sum_kernel(const float* part, int chunks, long n,
-                                                       float* out, float scale, int accumulate) {
+// out[o][e] (+)= scale * sum over c < chunks of part[(o chunks + c) n + e], in a fixed
+// order: with many chunks, first groups of kSumGroup chunks (each group's sum written over
+// its first row, read only by the thread that writes it), then the groups' sums in order.
+constexpr int kSumGroup = 32;
+
+__global__ __launch_bounds__(256) void grad_sum_group_kernel(float* part, int chunks, long n) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const int ngr = (chunks + kSumGroup - 1) / kSumGroup;
+  const long o = blockIdx.y / ngr;
+  const int g = blockIdx.y % ngr;
+  if (idx >= n) return;
+  const int c0 = g * kSumGroup, c1 = min(chunks, c0 + kSumGroup);
+  float v = 0.f;
+  for (int c = c0; c < c1; ++c) v += part[(o * chunks + c) * n + idx];
+  part[(o * chunks + c0) * n + idx] = v;
+}
+
+__global__ __launch_bounds__(256) void grad_sum_kernel(const float* part, int chunks, int step,
+                                                       long n, float* out, float scale,
+                                                       int accumulate) {
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   const long o = blockIdx.y;
   if (idx >= n) return;
   float v = 0.f;
-  for (int c = 0; c < chunks; ++c) v += part[(o * chunks + c) * n + idx];
+  for (int c = 0; c < chunks; c += step) v += part[(o * chunks + c) * n + idx];
   out[o * n + idx] = accumulate ? out[o * n + idx] + v * scale : v * scale;
 }
 
-void launch_grad_sum(const float* part, int outer, int chunks, long n, float* out, float scale,
+void launch_grad_sum(float* part, int outer, int chunks, long n, float* out, float scale,
                      int accumulate, hipStream_t s) {
   if (outer <= 0 || n <= 0) return;
-  hipLaunchKernelGGL(grad_sum_kernel, dim3((unsigned)((n + 255) / 256), outer), dim3(256), 0, s,
-                     part, chunks, n, out, scale, accumulate);
+  const unsigned bx = (unsigned)((n + 255) / 256);
+  int step = 1;
+  if (chunks > 2 * kSumGroup) {
+    const int ngr = (chunks + kSumGroup - 1) / kSumGroup;
+    hipLaunchKernelGGL(grad_sum_group_kernel, dim3(bx, outer * ngr), dim3(256), 0, s, part,
+                       chunks, n);
+    step = kSumGroup;
+  }
+  hipLaunchKernelGGL(grad_sum_kernel, dim3(bx, outer), dim3(256), 0, s, (const float*)part,
+                     chunks, step, n, out, scale, accumulate);
 }
 
 // Per token and branch, with hn[l] = g[l] h[l] / rms(h[l]) recomputed in fp32 from the

@@ -146,12 +146,19 @@ struct GemmOperand {
 // C[z][m][n] (+)= sum_k A(m, k) B(n, k) over batches z; C at C + z c_z + m c_row + n c_col.
 // Batch z uses only k >= k_lo0 + k_lo_dz z of B and stores only rows m >= m_lo0 + m_lo_dz z
 // (the no-feedback router's triangular weights); zero both for a plain GEMM.
+// part / part_elems (optional): fp32 scratch for split K. When the tiles would leave CUs
+// idle and K is long, each tile's K range is cut into slices computed by separate
+// workgroups into part, then summed in slice order into C (the same sum on any device).
 struct GemmArgs {
   GemmOperand A, B;
   float* C;
   long c_row, c_col, c_z;
   int M, N, K, accumulate;
   long k_lo0, k_lo_dz, m_lo0, m_lo_dz;
+  float* part;
+  long part_elems;
+  int splits;   // set by launch_grad_gemm
+  int kchunk;   // set by launch_grad_gemm: K per slice, a multiple of 32
 };
 void launch_grad_gemm(GemmArgs a, int batches, hipStream_t s);
 // out[r] = g[(r / gdiv) % gmod] * x[r] * rinv[r] (bf16 rows of D)
@@ -186,8 +193,8 @@ struct RmsArgs {           // rows (o, i); offsets in rows of D
   int D, ninner, chunks, accumulate;
 };
 void launch_grad_rms(const RmsArgs& a, int nouter, hipStream_t s);
-// out[o][e] (+)= scale * sum_c part[(o chunks + c) n + e]
-void launch_grad_sum(const float* part, int outer, int chunks, long n, float* out, float scale,
+// out[o][e] (+)= scale * sum_c part[(o chunks + c) n + e] (part is overwritten)
+void launch_grad_sum(float* part, int outer, int chunks, long n, float* out, float scale,
                      int accumulate, hipStream_t s);
 void launch_grad_colsum(const float* x, long rows, int n, int chunks, float* part, hipStream_t s);
 void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,

@@ -62,6 +62,26 @@ def test_q_project_backward(wm, d, Hq, Hkv, T_new, ctx):
     _check_grads("q", g, g0, ref, ob.QUERY_PARAMS)
 
 
+def test_weight_gradients_split_k(wm):
+    """Many tokens, few weight tiles: the weight gradients' GEMMs cut K (the tokens) into
+    slices summed in order (dWq here, 2 layers of 128 x 128 against 4096 tokens)."""
+    w = synth.small("qb_split", B=2, T_new=2048, L=2, k=1, D=128, Hq=2, Hkv=1, d=64,
+                    ctx=2048, dtype="bf16")
+    print("q backward split K", flush=True)
+    P = synth.make_params(w, _bias(w), gains="random")
+    H = synth.make_states(w)
+    dQ = synth._normal((w.L, w.B, w.Hq, w.T_new, w.d), 1.0, 511, torch.float32)
+    ref = ob.q_project_grads(_odims(w), P, H, dQ.double().numpy())
+    dH = torch.zeros(tuple(H.shape), dtype=torch.float32, device="cuda")
+    g = {n: torch.zeros(tuple(P[n].shape), dtype=torch.float32, device="cuda")
+         for n in ob.QUERY_PARAMS}
+    wm.q_project_backward(_gdims(wm, w, ctx_max=0), _dev(P), H.cuda(), None, dQ.cuda(), dH, g)
+    torch.cuda.synchronize()
+    check_close(dH.cpu(), ref["dH"], "bf16", "dH")
+    for n in ob.QUERY_PARAMS:
+        check_close(g[n].cpu(), ref["d" + n], "bf16", "split d%s" % n)
+
+
 POOL_CASES = [
     dict(),
     dict(mix_mode=1),
