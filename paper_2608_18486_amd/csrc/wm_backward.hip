@@ -38,23 +38,32 @@ struct BwdArgs {
   int dchunks;     // partial sums per (channel, KV head) of the dummy's gradients
 };
 
-constexpr int kBwdThreads = 256;
+// waves per workgroup of the query-major and the slot-major kernel (32 rows each)
+#ifndef WM_BWD_QWAVES
+#define WM_BWD_QWAVES 8
+#endif
+#ifndef WM_BWD_KWAVES
+#define WM_BWD_KWAVES 8
+#endif
+constexpr int kBwdQWaves = WM_BWD_QWAVES, kBwdKWaves = WM_BWD_KWAVES;
 
 __device__ __forceinline__ float bwd_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Copies rows row0 .. row0 + ROWS - 1 (DH bf16 each, row_bytes apart in the view) into the
 // LDS block at lds_base with LDS DMA, in the fragment readers' chunk swizzle: wave w's
 // n-th instruction fills LDS chunks 64 (NI w + n) + lane, and each lane fetches the chunk
-// the swizzle puts there. Rows at or past nvalid arrive as zeros. Every wave issues NI
-// copies; the caller waits for them (vmcnt) before the barrier that publishes the block.
-template <int DH, int ROWS>
+// the swizzle puts there. Rows at or past nvalid arrive as zeros. Every wave of the NW
+// issues up to NI copies (the block's 16-byte chunks in whole 64-lane instructions); the
+// caller waits for them (vmcnt) before the barrier that publishes the block.
+template <int DH, int ROWS, int NW>
 __device__ __forceinline__ void bwd_dma(uint32_t lds_base, __amdgpu_buffer_rsrc_t view,
                                         uint32_t row_bytes, int row0, int nvalid, int w,
                                         int lane) {
-  constexpr int CPR = DH * 2 / 16, NI = ROWS * CPR / 256;
-  static_assert(NI * 256 == ROWS * CPR, "whole instructions per wave");
+  constexpr int CPR = DH * 2 / 16, TOT = ROWS * CPR, NI = (TOT + 64 * NW - 1) / (64 * NW);
+  static_assert(TOT % 64 == 0, "whole 64-lane instructions");
 #pragma unroll
   for (int n = 0; n < NI; ++n) {
+    if ((NI * w + n) * 64 >= TOT) break;  // wave-uniform: the block is complete
     const int pos = (NI * w + n) * 64 + lane, row = pos / CPR, cc = pos - row * CPR;
     const int gr = row0 + row;
     const uint32_t off = gr < nvalid ? (uint32_t)gr * row_bytes + 16u * (uint32_t)(cc ^ pf_swz<DH>(row))
@@ -68,13 +77,13 @@ __device__ __forceinline__ bf16x4 bwd_ld8(__amdgpu_buffer_rsrc_t r, uint32_t off
 }
 
 // --------------------------------------------------------------- dq, LSE, D
-// Tile: 128 query rows of one (consumer, sequence, query head), 32 per wave; S^T = K q^T
+// Tile: 32 NW query rows of one (consumer, sequence, query head), 32 per wave; S^T = K q^T
 // puts one query in a lane (as in the forward), dP^T = V dO^T likewise, and
 // dq^T += K^T dS^T takes dS^T straight from those registers through the transposing
 // read of the K block.
-template <int DH>
-__global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
-  constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, BLK = 64;
+template <int DH, int NW>
+__global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
+  constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, BLK = 64, NH = DH == 64 ? 2 : 1;
   // two buffers, each a K block then a V block (pass 1 uses the K blocks only)
   __shared__ __align__(16) char smem[4 * BLK * ROW];
   const uint32_t lbase = (uint32_t)(uintptr_t)smem;
@@ -89,7 +98,7 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int pos0 = __builtin_amdgcn_readfirstlane(ctx_at(a.ctx_len, b, a.ctx_hi));
   const int incl = a.mask_paper ? 0 : 1;
-  const int q0 = qtile * 128, qw0 = q0 + 32 * w, qi = qw0 + r;
+  const int q0 = qtile * 32 * NW, qw0 = q0 + 32 * w, qi = qw0 + r;
   const bool valid = qi < a.T;
   const float cl2 = a.scale_log2;
 
@@ -131,7 +140,7 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
   const float sd = halves_sum(sdp) * cl2;  // the dummy's score, log2 units
   dpd = halves_sum(dpd);
 
-  const int qlast = min(q0 + 127, a.T - 1);
+  const int qlast = min(q0 + 32 * NW - 1, a.T - 1);
   const int kend = min(pos0 + qlast + incl, a.S_cap);            // slots the tile may see
   const int wq_last = min(qw0 + 31, a.T - 1);
   const int wkend = wq_last >= qw0 ? pos0 + wq_last + incl : 0;  // ... this wave
@@ -147,31 +156,50 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
   float m = a.mask_paper ? sd : kNegBig;
   float sum = a.mask_paper && h == 0 ? 1.f : 0.f;
   // blocks are double-buffered: block j + 1 is copied while block j is multiplied
-  if (nblk > 0) bwd_dma<DH, BLK>(lbase, kv, ROW, 0, kend, w, lane);
+  if (nblk > 0) bwd_dma<DH, BLK, NW>(lbase, kv, ROW, 0, kend, w, lane);
   for (int j = 0; j < nblk; ++j) {
     const uint32_t kb = (uint32_t)(j & 1) * 2 * BLK * ROW;
     wait_vmcnt<0>();
     __syncthreads();  // block j is in LDS; every wave is done with block j - 1
-    if (j + 1 < nblk) bwd_dma<DH, BLK>(lbase + (kb ^ (2 * BLK * ROW)), kv, ROW, (j + 1) * BLK, kend, w, lane);
+    if (j + 1 < nblk)
+      bwd_dma<DH, BLK, NW>(lbase + (kb ^ (2 * BLK * ROW)), kv, ROW, (j + 1) * BLK, kend, w, lane);
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int s0 = j * BLK + 32 * hf;
-      if (s0 < wkend) {
-        f32x16 sc = zero16();
+    for (int hg = 0; hg < 2 / NH; ++hg) {
+      const int sb = j * BLK + 32 * NH * hg;  // the group's first slot
+      if (sb < wkend) {
+        f32x16 sc[NH];
+#pragma unroll
+        for (int x = 0; x < NH; ++x) sc[x] = zero16();
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
-          sc = mma32(sc, pf_ldk<DH>(smem, lo, kb + hf * 32 * ROW, ks), qf[ks]);
-        float mx = kNegBig;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int s = s0 + 8 * (q >> 2) + 4 * h + (q & 3);
-          sc[q] = s < lim ? sc[q] * cl2 : kNegBig;
-          mx = fmaxf(mx, sc[q]);
+          for (int x = 0; x < NH; ++x)
+            sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, kb + (NH * hg + x) * 32 * ROW, ks), qf[ks]);
+        float mx = kNegBig;
+        if (sb + 32 * NH - 1 < pos0 + qw0 + incl) {  // every row of the wave sees the group
+#pragma unroll
+          for (int x = 0; x < NH; ++x)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              sc[x][q] *= cl2;
+              mx = fmaxf(mx, sc[x][q]);
+            }
+        } else {
+          const int thr = lim - sb - 4 * h;  // slot sb + 32 x + 8 (q / 4) + 4 h + q % 4 < lim
+#pragma unroll
+          for (int x = 0; x < NH; ++x)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              sc[x][q] = 32 * x + 8 * (q >> 2) + (q & 3) < thr ? sc[x][q] * cl2 : kNegBig;
+              mx = fmaxf(mx, sc[x][q]);
+            }
         }
         const float mn = fmaxf(m, halves_max(mx));
         float part = 0.f;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) part += bwd_exp2(sc[q] - mn);
+        for (int x = 0; x < NH; ++x)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) part += bwd_exp2(sc[x][q] - mn);
         sum = sum * bwd_exp2(m - mn) + part;
         m = mn;
       }
@@ -185,8 +213,8 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) dq[dt] = zero16();
   if (nblk > 0) {
-    bwd_dma<DH, BLK>(lbase, kv, ROW, 0, kend, w, lane);
-    bwd_dma<DH, BLK>(lbase + BLK * ROW, vv, ROW, 0, kend, w, lane);
+    bwd_dma<DH, BLK, NW>(lbase, kv, ROW, 0, kend, w, lane);
+    bwd_dma<DH, BLK, NW>(lbase + BLK * ROW, vv, ROW, 0, kend, w, lane);
   }
   for (int j = 0; j < nblk; ++j) {
     const uint32_t kb = (uint32_t)(j & 1) * 2 * BLK * ROW;
@@ -194,31 +222,52 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
     __syncthreads();
     if (j + 1 < nblk) {
       const uint32_t nb = lbase + (kb ^ (2 * BLK * ROW));
-      bwd_dma<DH, BLK>(nb, kv, ROW, (j + 1) * BLK, kend, w, lane);
-      bwd_dma<DH, BLK>(nb + BLK * ROW, vv, ROW, (j + 1) * BLK, kend, w, lane);
+      bwd_dma<DH, BLK, NW>(nb, kv, ROW, (j + 1) * BLK, kend, w, lane);
+      bwd_dma<DH, BLK, NW>(nb + BLK * ROW, vv, ROW, (j + 1) * BLK, kend, w, lane);
     }
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int s0 = j * BLK + 32 * hf;
-      if (s0 < wkend) {
-        f32x16 sc = zero16(), dp = zero16();
+    for (int hg = 0; hg < 2 / NH; ++hg) {
+      const int sb = j * BLK + 32 * NH * hg;
+      if (sb < wkend) {
+        f32x16 sc[NH], dp[NH];
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          sc = mma32(sc, pf_ldk<DH>(smem, lo, kb + hf * 32 * ROW, ks), qf[ks]);
-          dp = mma32(dp, pf_ldk<DH>(smem, lo, kb + BLK * ROW + hf * 32 * ROW, ks), df[ks]);
+        for (int x = 0; x < NH; ++x) sc[x] = dp[x] = zero16();
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+          for (int x = 0; x < NH; ++x) {
+            const uint32_t ho = kb + (NH * hg + x) * 32 * ROW;
+            sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, ho, ks), qf[ks]);
+            dp[x] = mma32(dp[x], pf_ldk<DH>(smem, lo, ho + BLK * ROW, ks), df[ks]);
+          }
+        bf16x8 ds[NH][2];
+        if (sb + 32 * NH - 1 < pos0 + qw0 + incl) {  // no mask in this group
+#pragma unroll
+          for (int x = 0; x < NH; ++x)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              const float p = bwd_exp2(sc[x][q] * cl2 - lse);
+              ds[x][q >> 3][q & 7] = (bf16)(p * (dp[x][q] - delta));
+            }
+        } else {
+          const int thr = lim - sb - 4 * h;
+#pragma unroll
+          for (int x = 0; x < NH; ++x)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              const float p = 32 * x + 8 * (q >> 2) + (q & 3) < thr
+                                  ? bwd_exp2(sc[x][q] * cl2 - lse) : 0.f;
+              ds[x][q >> 3][q & 7] = (bf16)(p * (dp[x][q] - delta));
+            }
         }
-        bf16x8 ds[2];
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int s = s0 + 8 * (q >> 2) + 4 * h + (q & 3);
-          const float p = s < lim ? bwd_exp2(sc[q] * cl2 - lse) : 0.f;
-          ds[q >> 3][q & 7] = (bf16)(p * (dp[q] - delta));
-        }
+        for (int x = 0; x < NH; ++x)
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
+          for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-          for (int kh = 0; kh < 2; ++kh)
-            dq[dt] = mma32(dq[dt], pf_ldv<DH>(smem, lo, kb + hf * 32 * ROW, kh, dt), ds[kh]);
+            for (int kh = 0; kh < 2; ++kh)
+              dq[dt] = mma32(dq[dt], pf_ldv<DH>(smem, lo, kb + (NH * hg + x) * 32 * ROW, kh, dt),
+                             ds[x][kh]);
       }
     }
   }
@@ -249,7 +298,7 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
 }
 
 // ------------------------------------------------------------------- dk, dv
-// Tile: 128 slots of one (channel, sequence, KV head), 32 per wave; the wave's K and V
+// Tile: 32 NW slots of one (channel, sequence, KV head), 32 per wave; the wave's K and V
 // rows stay in registers as the column operand. The tile walks every query block of 64
 // rows that may read its slots, for every consumer of the channel and every query head of
 // the KV head, as one flat sequence, so the next block (queries and dO by LDS DMA, the
@@ -257,9 +306,9 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dq_kernel(BwdArgs a) {
 // each 32-row half: S = Q K^T and dP = dO V^T put one slot in a lane, and dv^T += dO^T P
 // and dk^T += Q^T dS take P and dS from those registers through the transposing reads
 // of the dO and Q blocks.
-template <int DH>
-__global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) {
-  constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, QB = 64;
+template <int DH, int NW>
+__global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
+  constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, QB = 64, NH = DH == 64 ? 2 : 1;
   constexpr uint32_t BUF = 2 * QB * ROW;  // one buffer: a Q block, then a dO block
   __shared__ __align__(16) char smem[2 * BUF];
   __shared__ __align__(16) float s_lse[2][QB], s_dlt[2][QB];
@@ -276,7 +325,7 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) 
   const int pos0 = __builtin_amdgcn_readfirstlane(ctx_at(a.ctx_len, b, a.ctx_hi));
   const int incl = a.mask_paper ? 0 : 1;
   const int send = pos0 + a.T;  // slots written: [0, send)
-  const int sbase = stile * 128;
+  const int sbase = stile * 32 * NW;
   if (sbase >= send) return;
   const int ws0 = sbase + 32 * w, slot = ws0 + r;
   const bool slot_ok = slot < send;
@@ -320,8 +369,8 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) 
     const long rowl = ((long)l * a.B + b) * a.T;
     const auto qv = make_view(a.Q + rows0 * DH, (uint32_t)a.T * DH * 2u);
     const auto dov = make_view(a.dO + rowl * a.Hq * DH + (long)hq * DH, (uint32_t)a.T * ostride);
-    bwd_dma<DH, QB>(buf, qv, DH * 2u, qb * QB, a.T, w, lane);
-    bwd_dma<DH, QB>(buf + QB * ROW, dov, ostride, qb * QB, a.T, w, lane);
+    bwd_dma<DH, QB, NW>(buf, qv, DH * 2u, qb * QB, a.T, w, lane);
+    bwd_dma<DH, QB, NW>(buf + QB * ROW, dov, ostride, qb * QB, a.T, w, lane);
     if (tid < QB) {
       const int qr = qb * QB + tid;
       lse_n = qr < a.T ? a.lse[rows0 + qr] : 1.0e30f;  // a row past T weighs 0
@@ -343,40 +392,70 @@ __global__ __launch_bounds__(kBwdThreads) void attend_bwd_dkv_kernel(BwdArgs a) 
     (void)l;
     (void)hq;
     if (it + 1 < nit) fetch(it + 1, lbase + (kb ^ BUF));
+    // the block's 32-row halves NH at a time (NH = 2: their products interleave; NH = 1
+    // where two halves' registers would not fit): S = Q K^T and dP = dO V^T put one slot in a
+    // lane; a group is skipped when its last row cannot see the wave's first slot
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int q0 = qb * QB + 32 * hf;
-      // the half's last row (position pos0 + q0 + 31) sees slots below that + incl: skip
-      // the half when the wave's first slot is not among them, or when it is past T
-      if (q0 < a.T && pos0 + min(q0 + 31, a.T - 1) + incl > ws0) {
-        const uint32_t qo = kb + hf * 32 * ROW, doo = kb + QB * ROW + hf * 32 * ROW;
-        f32x16 sc = zero16(), dp = zero16();
+    for (int hg = 0; hg < 2 / NH; ++hg) {
+      const int qg = qb * QB + 32 * NH * hg;  // the group's first row
+      if (qg < a.T && pos0 + min(qg + 32 * NH - 1, a.T - 1) + incl > ws0) {
+        f32x16 sc[NH], dp[NH];
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          sc = mma32(sc, pf_ldk<DH>(smem, lo, qo, ks), kf[ks]);
-          dp = mma32(dp, pf_ldk<DH>(smem, lo, doo, ks), vf[ks]);
-        }
-        // lane (h, r): slot r of the wave, query rows 8 (i / 4) + 4 h + i % 4 of the half
-        bf16x8 pp[2], pds[2];
+        for (int x = 0; x < NH; ++x) sc[x] = dp[x] = zero16();
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 lz = *(const f32x4*)(&s_lse[u][32 * hf + 8 * g + 4 * h]);
-          const f32x4 dz = *(const f32x4*)(&s_dlt[u][32 * hf + 8 * g + 4 * h]);
+        for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int i = 4 * g + e, qr = q0 + 8 * g + 4 * h + e;
-            const float p = slot < pos0 + qr + incl ? bwd_exp2(sc[i] * cl2 - lz[e]) : 0.f;
-            pp[i >> 3][i & 7] = (bf16)p;
-            pds[i >> 3][i & 7] = (bf16)(p * (dp[i] - dz[e]));
+          for (int x = 0; x < NH; ++x) {
+            const uint32_t ho = kb + (NH * hg + x) * 32 * ROW;
+            sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, ho, ks), kf[ks]);
+            dp[x] = mma32(dp[x], pf_ldk<DH>(smem, lo, ho + QB * ROW, ks), vf[ks]);
           }
+        // lane (h, r): slot r of the wave, rows 32 x + 8 (i / 4) + 4 h + i % 4 of the group
+        bf16x8 pp[NH][2], pds[NH][2];
+        const int hb = 32 * NH * hg;  // the group's rows in the staged block
+        if (ws0 + 31 < pos0 + qg + incl) {  // every row of the group sees every slot
+#pragma unroll
+          for (int x = 0; x < NH; ++x)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const f32x4 lz = *(const f32x4*)(&s_lse[u][hb + 32 * x + 8 * g + 4 * h]);
+              const f32x4 dz = *(const f32x4*)(&s_dlt[u][hb + 32 * x + 8 * g + 4 * h]);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int i = 4 * g + e;
+                const float p = bwd_exp2(sc[x][i] * cl2 - lz[e]);
+                pp[x][i >> 3][i & 7] = (bf16)p;
+                pds[x][i >> 3][i & 7] = (bf16)(p * (dp[x][i] - dz[e]));
+              }
+            }
+        } else {
+          const int thr = slot - pos0 - incl - qg - 4 * h;  // row 32 x + 8 g + e sees it iff > thr
+#pragma unroll
+          for (int x = 0; x < NH; ++x)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const f32x4 lz = *(const f32x4*)(&s_lse[u][hb + 32 * x + 8 * g + 4 * h]);
+              const f32x4 dz = *(const f32x4*)(&s_dlt[u][hb + 32 * x + 8 * g + 4 * h]);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int i = 4 * g + e;
+                const float p = 32 * x + 8 * g + e > thr ? bwd_exp2(sc[x][i] * cl2 - lz[e]) : 0.f;
+                pp[x][i >> 3][i & 7] = (bf16)p;
+                pds[x][i >> 3][i & 7] = (bf16)(p * (dp[x][i] - dz[e]));
+              }
+            }
         }
+        // dv^T += dO^T P and dk^T += Q^T dS, P and dS through the transposing reads
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
+        for (int x = 0; x < NH; ++x)
 #pragma unroll
-          for (int kh = 0; kh < 2; ++kh) {
-            dv[dt] = mma32(dv[dt], pf_ldv<DH>(smem, lo, doo, kh, dt), pp[kh]);
-            dk[dt] = mma32(dk[dt], pf_ldv<DH>(smem, lo, qo, kh, dt), pds[kh]);
-          }
+          for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh) {
+              const uint32_t ho = kb + (NH * hg + x) * 32 * ROW;
+              dv[dt] = mma32(dv[dt], pf_ldv<DH>(smem, lo, ho + QB * ROW, kh, dt), pp[x][kh]);
+              dk[dt] = mma32(dk[dt], pf_ldv<DH>(smem, lo, ho, kh, dt), pds[x][kh]);
+            }
       }
     }
   }
@@ -427,14 +506,27 @@ __global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_part_kernel(BwdArgs a
   const long nrow = (long)(a.grp.offsets[c + 1] - a.grp.offsets[c]) * per_m;
   const long r0 = nrow * chunk / nch, r1 = nrow * (chunk + 1) / nch;
   float av = 0.f, ak = 0.f;
-  if (a.mask_paper) {
-    for (long rr = r0 + rl; rr < r1; rr += 4) {
-      const int mi = (int)(rr / per_m), hg = (int)(rr / per_h % G), b = (int)(rr / per_b % a.B);
-      const int i = (int)(rr % per_b);
+  if (a.mask_paper && r0 + rl < r1) {
+    // row rr = ((mi G + hg) B + b) T + i, stepped by 4 without divisions in the loop
+    long rr = r0 + rl;
+    int mi = (int)(rr / per_m), hg = (int)(rr / per_h % G), b = (int)(rr / per_b % a.B);
+    int i = (int)(rr % per_b);
+    for (; rr < r1; rr += 4) {
       const int l = a.grp.members[a.grp.offsets[c] + mi], hq = kvh * G + hg;
       const long row = (((long)l * a.B + b) * a.Hq + hq) * a.T + i;
       av += a.pd[row] * (float)a.dO[(((long)l * a.B + b) * a.T + i) * a.Hq * DH + (long)hq * DH + e];
       ak += a.dsd[row] * (float)a.Q[row * DH + e];
+      i += 4;
+      while (i >= a.T) {
+        i -= a.T;
+        if (++b == a.B) {
+          b = 0;
+          if (++hg == G) {
+            hg = 0;
+            ++mi;
+          }
+        }
+      }
     }
   }
   s_v[tid] = av;
@@ -488,22 +580,25 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
   const long nrow = (long)sh.L * sh.B * sh.Hq * sh.T_new;
   BwdArgs a{Q, Kc, Vc, Kd, Vd, O, dO, ctx_len, dQ, dKc, dVc, dKd, dVd, rows, rows + nrow,
             rows + 2 * nrow, rows + 3 * nrow, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
-            sh.mask_paper, sh.ctx_hi, (sh.T_new + 127) / 128,
-            (int)(((long)sh.ctx_max + sh.T_new + 127) / 128), kLog2e / sqrtf((float)sh.d),
+            sh.mask_paper, sh.ctx_hi, (sh.T_new + 32 * kBwdQWaves - 1) / (32 * kBwdQWaves),
+            (int)(((long)sh.ctx_max + sh.T_new + 32 * kBwdKWaves - 1) / (32 * kBwdKWaves)),
+            kLog2e / sqrtf((float)sh.d),
             1.0f / sqrtf((float)sh.d), chan_map, groups, accumulate ? 1 : 0,
             dummy_chunks(sh)};
   const dim3 ga(a.n_qtiles * sh.Hq * sh.B * sh.L), gb(a.n_stiles * sh.Hkv * sh.B * sh.k),
       gp(sh.k * sh.Hkv * a.dchunks), gs(sh.k * sh.Hkv);
   float* part = rows + 4 * nrow;
   if (sh.d == 64) {
-    hipLaunchKernelGGL(attend_bwd_dq_kernel<64>, ga, dim3(kBwdThreads), 0, s, a);
-    hipLaunchKernelGGL(attend_bwd_dkv_kernel<64>, gb, dim3(kBwdThreads), 0, s, a);
+    hipLaunchKernelGGL((attend_bwd_dq_kernel<64, kBwdQWaves>), ga, dim3(64 * kBwdQWaves), 0, s, a);
+    hipLaunchKernelGGL((attend_bwd_dkv_kernel<64, kBwdKWaves>), gb, dim3(64 * kBwdKWaves), 0, s,
+                       a);
     hipLaunchKernelGGL(attend_bwd_dummy_part_kernel<64>, gp, dim3(4 * 64), 0, s, a, part);
     hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<64>, gs, dim3(4 * 64), 0, s, a,
                        (const float*)part);
   } else {
-    hipLaunchKernelGGL(attend_bwd_dq_kernel<96>, ga, dim3(kBwdThreads), 0, s, a);
-    hipLaunchKernelGGL(attend_bwd_dkv_kernel<96>, gb, dim3(kBwdThreads), 0, s, a);
+    hipLaunchKernelGGL((attend_bwd_dq_kernel<96, kBwdQWaves>), ga, dim3(64 * kBwdQWaves), 0, s, a);
+    hipLaunchKernelGGL((attend_bwd_dkv_kernel<96, kBwdKWaves>), gb, dim3(64 * kBwdKWaves), 0, s,
+                       a);
     hipLaunchKernelGGL(attend_bwd_dummy_part_kernel<96>, gp, dim3(4 * 96), 0, s, a, part);
     hipLaunchKernelGGL(attend_bwd_dummy_sum_kernel<96>, gs, dim3(4 * 96), 0, s, a,
                        (const float*)part);
