@@ -87,7 +87,9 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
   // two buffers, each a K block then a V block (pass 1 uses the K blocks only)
   __shared__ __align__(16) char smem[4 * BLK * ROW];
   const uint32_t lbase = (uint32_t)(uintptr_t)smem;
-  const int tile = blockIdx.x;
+  // XCD-aware order: each XCD walks a contiguous run of tiles, so the query tiles of one
+  // head (which read the same K/V slice) share its L2
+  const int tile = xcd_tile(blockIdx.x, (int)gridDim.x);
   const int qtile = a.n_qtiles - 1 - tile % a.n_qtiles;
   int y = tile / a.n_qtiles;
   const int hq = y % a.Hq;
@@ -313,7 +315,9 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
   __shared__ __align__(16) char smem[2 * BUF];
   __shared__ __align__(16) float s_lse[2][QB], s_dlt[2][QB];
   const uint32_t lbase = (uint32_t)(uintptr_t)smem;
-  const int tile = blockIdx.x;
+  // XCD-aware order: the slot tiles of one (channel, sequence, KV head), which read the
+  // same queries and output gradients, run on one XCD
+  const int tile = xcd_tile(blockIdx.x, (int)gridDim.x);
   const int stile = tile % a.n_stiles;
   int y = tile / a.n_stiles;
   const int kvh = y % a.Hkv;
