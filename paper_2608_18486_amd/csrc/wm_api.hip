@@ -656,7 +656,7 @@ int static_scratch(void** out) {
 
 // ------------------------------------------------------------------ gradients
 wm::GemmOperand opnd(const void* p, long s_row, long s_k, long s_z, bool f32, bool pad8 = false) {
-  return wm::GemmOperand{p, s_row, s_k, s_z, f32 ? 1 : 0, pad8 ? 1 : 0};
+  return wm::GemmOperand{p, s_row, s_k, s_z, f32 ? 1 : 0, pad8 ? 1 : 0, 0};
 }
 
 // C[z] (+)= A[z] B[z]^T over `batches`; see GemmArgs for the k / row limits.

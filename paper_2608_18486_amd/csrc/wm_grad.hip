@@ -227,6 +227,140 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
   }
 }
 
+// ---- the same product with LDS DMA: every tile goes from memory straight into LDS
+// (buffer_load ... lds, no registers), kGemmStages K-steps in flight. Layouts as above,
+// except that the k-major (T) tile has no padding: k row kk holds its BM rows as 16-byte
+// chunks, chunk c at position c ^ 2 (kk mod 4), so the four k rows one transposing read
+// touches fall in disjoint banks. Each wave issues the same number of copies per stage
+// (BM / 16 per operand over the workgroup), which the vmcnt waits rely on.
+constexpr int kGemmStages = 3;
+
+// this lane's copy n of a tile: LDS chunk q = 64 (NI w + n) + lane; returns the byte offset
+// of the chunk it fetches within the batch's view (kOffOob: zeros)
+template <bool T, int BM>
+__device__ __forceinline__ uint32_t dma_src(const GemmOperand& o, int q, int row0, int k0, int nrows,
+                                            int K, int klo) {
+  if constexpr (T) {
+    const int kk = q / (BM / 8), c = (q % (BM / 8)) ^ (2 * (kk & 3));
+    const int k = k0 + kk, row = row0 + 8 * c;
+    const bool ok = k < K && k >= klo && row < nrows;
+    return ok ? (uint32_t)(((long)k * o.s_k + row) * 2) : kOffOob;
+  } else {
+    const int r = q >> 2, c = (q & 3) ^ grad_swz(r);
+    const int row = row0 + r, k = k0 + 8 * c;
+    const bool ok = row < nrows && k < K;
+    return ok ? (uint32_t)(((long)row * o.s_row + k) * 2) : kOffOob;
+  }
+}
+
+// fragment of rows rb .. rb + 31, k 16 ks + 8 h .. + 7 from a DMA-staged tile
+template <bool T, int BM>
+__device__ __forceinline__ bf16x8 gemm_frag_dma(const char* tile, int rb, int ks, int lane) {
+  if constexpr (T) {
+    const int j = lane & 15, grp = lane >> 4, h = lane >> 5;
+    const int row = rb + 16 * (grp & 1) + 4 * (j & 3), c = row >> 3, within = row & 7;
+    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+    i16x4 v[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int kk = 16 * ks + 8 * h + 4 * s + (j >> 2);
+      const char* p = tile + kk * BM * 2 + 16 * (c ^ (2 * (kk & 3))) + 2 * within;
+      v[s] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+    }
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(v[0], v[1], 0, 1, 2, 3, 4, 5, 6, 7));
+  } else {
+    const int h = lane >> 5, row = rb + (lane & 31);
+    return *(const bf16x8*)(tile + row * 64 + 16 * ((2 * ks + h) ^ grad_swz(row)));
+  }
+}
+
+template <class C, bool TA, bool TB>
+__global__ __launch_bounds__(C::NT) void grad_gemm_dma_kernel(GemmArgs a) {
+  constexpr int S = kGemmStages, AB = C::BM * 64, BB = C::BN * 64;
+  constexpr int NIA = C::BM / 16 / (C::NT / 64), NIB = C::BN / 16 / (C::NT / 64);
+  static_assert(NIA * (C::NT / 64) * 16 == C::BM && NIB * (C::NT / 64) * 16 == C::BN,
+                "whole copies per wave");
+  static_assert((S - 2) * (NIA + NIB) < 16, "vmcnt range");
+  __shared__ __align__(16) char smem[S][AB + BB];
+  const int tm = (a.M + C::BM - 1) / C::BM, tn = (a.N + C::BN - 1) / C::BN;
+  const int tile = xcd_tile(blockIdx.x, (int)gridDim.x);
+  const int zs = tile / (tm * tn), t = tile % (tm * tn);
+  const int z = zs / a.splits, slice = zs % a.splits;
+  const int m0 = (t / tn) * C::BM, n0 = (t % tn) * C::BN;
+  const int kbeg = slice * a.kchunk, kend = min(a.K, kbeg + a.kchunk);
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, r = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), wm = w % C::WGM, wn = w / C::WGM;
+  const int klo = (int)(a.k_lo0 + a.k_lo_dz * z);
+  const auto va = make_view((const bf16*)a.A.p + (long)z * a.A.s_z, (uint32_t)a.A.span);
+  const auto vb = make_view((const bf16*)a.B.p + (long)z * a.B.s_z, (uint32_t)a.B.span);
+  const uint32_t lbase = (uint32_t)(uintptr_t)&smem[0][0];
+  const int nk = (kend - kbeg + 31) / 32;
+  auto issue = [&](int kt) {
+    const int k0 = kbeg + 32 * kt;
+    const uint32_t st = lbase + (uint32_t)(kt % S) * (AB + BB);
+#pragma unroll
+    for (int n = 0; n < NIA; ++n) {
+      const int q = 64 * (NIA * w + n) + lane;
+      lds_dma16(__builtin_amdgcn_readfirstlane(st + 1024u * (NIA * w + n)),
+                dma_src<TA, C::BM>(a.A, q, m0, k0, a.M, a.K, 0), va);
+    }
+#pragma unroll
+    for (int n = 0; n < NIB; ++n) {
+      const int q = 64 * (NIB * w + n) + lane;
+      lds_dma16(__builtin_amdgcn_readfirstlane(st + AB + 1024u * (NIB * w + n)),
+                dma_src<TB, C::BN>(a.B, q, n0, k0, a.N, a.K, klo), vb);
+    }
+  };
+  f32x16 acc[C::WM][C::WN];
+#pragma unroll
+  for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::WN; ++j) acc[i][j] = zero16();
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st)
+    if (st < nk) issue(st);
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + S - 2 < nk) wait_vmcnt<(S - 2) * (NIA + NIB)>();
+    else wait_vmcnt<0>();
+    __syncthreads();  // stage kt in LDS; every wave is done with stage kt - 1
+    if (kt + S - 1 < nk) issue(kt + S - 1);
+    const char* sa = smem[kt % S];
+    const char* sb = sa + AB;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 fa[C::WM], fb[C::WN];
+#pragma unroll
+      for (int i = 0; i < C::WM; ++i) fa[i] = gemm_frag_dma<TA, C::BM>(sa, 32 * (C::WM * wm + i), ks, lane);
+#pragma unroll
+      for (int j = 0; j < C::WN; ++j) fb[j] = gemm_frag_dma<TB, C::BN>(sb, 32 * (C::WN * wn + j), ks, lane);
+#pragma unroll
+      for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::WN; ++j) acc[i][j] = mma32(acc[i][j], fa[i], fb[j]);
+    }
+  }
+  const bool split = a.splits > 1;
+  float* Cz = split ? a.part + ((long)z * a.splits + slice) * a.M * a.N : a.C + (long)z * a.c_z;
+  const long crow = split ? a.N : a.c_row, ccol = split ? 1 : a.c_col;
+  const int mlo = split ? 0 : (int)(a.m_lo0 + a.m_lo_dz * z);
+  const int acc_in = split ? 0 : a.accumulate;
+#pragma unroll
+  for (int j = 0; j < C::WN; ++j) {
+    const int n = n0 + 32 * (C::WN * wn + j) + r;
+    if (n >= a.N) continue;
+#pragma unroll
+    for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
+        if (m < a.M && m >= mlo) {
+          float* p = Cz + (long)m * crow + (long)n * ccol;
+          *p = acc_in ? *p + acc[i][j][q] : acc[i][j][q];
+        }
+      }
+  }
+}
+
 static bool operand_t(const GemmOperand& o) { return o.s_row == 1 && o.s_k != 1; }
 
 // Vector loads need bf16, 16-byte alignment and strides in whole 8-element groups, with
@@ -253,6 +387,20 @@ __global__ __launch_bounds__(256) void grad_split_sum_kernel(GemmArgs a) {
   *c = a.accumulate ? *c + v : v;
 }
 
+// bytes a batch's tile loads may reach (vector rows / k rounded up to 8)
+static long operand_span(const GemmOperand& o, int nrows, int K) {
+  const long r8 = (nrows + 7) / 8 * 8, k8 = ((long)K + 7) / 8 * 8;
+  if (operand_t(o)) return ((long)(K - 1) * o.s_k + r8) * 2;
+  return ((long)(nrows - 1) * o.s_row + k8) * 2;
+}
+
+template <class C, bool TA, bool TB>
+static void launch_gemm_dma(const GemmArgs& a, int batches, hipStream_t s) {
+  const long tiles = (long)((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN) * batches *
+                     a.splits;
+  hipLaunchKernelGGL((grad_gemm_dma_kernel<C, TA, TB>), dim3((unsigned)tiles), dim3(C::NT), 0, s, a);
+}
+
 template <class C, bool TA, bool TB, bool VEC>
 static void launch_gemm_cfg(const GemmArgs& a, int batches, hipStream_t s) {
   const long tiles = (long)((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN) * batches *
@@ -262,10 +410,18 @@ static void launch_gemm_cfg(const GemmArgs& a, int batches, hipStream_t s) {
 }
 
 template <bool TA, bool TB>
-static void launch_gemm_t(const GemmArgs& a, int batches, bool vec, hipStream_t s) {
-  // the large tiles (vector operands only) when they still give every CU at least two
+static void launch_gemm_t(GemmArgs a, int batches, bool vec, hipStream_t s) {
+  // the large tiles (vector operands only) when they still give every CU at least two;
+  // LDS DMA when both operands' batch spans fit a buffer view and no k-contiguous B
+  // operand carries a k limit (its copies are whole 8-element chunks)
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256) * batches;
-  if (vec && big >= 2L * device_cus()) launch_gemm_cfg<GemmBig, TA, TB, true>(a, batches, s);
+  a.A.span = operand_span(a.A, a.M, a.K);
+  a.B.span = operand_span(a.B, a.N, a.K);
+  const bool dma = vec && a.A.span < (1L << 31) && a.B.span < (1L << 31) &&
+                   (TB || (a.k_lo0 == 0 && a.k_lo_dz == 0));
+  if (dma && big >= 2L * device_cus()) launch_gemm_dma<GemmBig, TA, TB>(a, batches, s);
+  else if (dma) launch_gemm_dma<GemmSmall, TA, TB>(a, batches, s);
+  else if (vec && big >= 2L * device_cus()) launch_gemm_cfg<GemmBig, TA, TB, true>(a, batches, s);
   else if (vec) launch_gemm_cfg<GemmSmall, TA, TB, true>(a, batches, s);
   else launch_gemm_cfg<GemmSmall, TA, TB, false>(a, batches, s);
 }

@@ -142,6 +142,7 @@ struct GemmOperand {
   int f32;
   int pad8;  // the operand's memory extends to a whole group of 8 past its last row (rows
              // contiguous) or k (k contiguous), zero-filled: vector loads may read it
+  long span; // set by launch_grad_gemm: bytes one batch's tile loads may reach
 };
 // C[z][m][n] (+)= sum_k A(m, k) B(n, k) over batches z; C at C + z c_z + m c_row + n c_col.
 // Batch z uses only k >= k_lo0 + k_lo_dz z of B and stores only rows m >= m_lo0 + m_lo_dz z
