@@ -281,8 +281,9 @@ int wm_q_project_backward(const wm_dims *dims, const wm_params *params, const vo
  * are recomputed from H with the forward's kernels.
  * bf16, head dims 64 and 96, contiguous tokens, D <= 4608; every router mode and mix mode.
  *   H, ctx_len  as wm_pool
- *   dKc, dVc device float [k][B][Hkv][S_cap][d]: slot ctx_len[b] + i of every (channel,
- *            sequence, KV head) is read (the call's new rows); no other slot is read
+ *   dKc, dVc device float [k][B][Hkv][S_cap][d], 16-byte aligned: slot ctx_len[b] + i of
+ *            every (channel, sequence, KV head) is read (the call's new rows); no other slot
+ *            is read
  *   dH       device float [B][T_new][L][D]: ADDED
  *   grads    g_pre, W_alpha (not with WM_ROUTER_STATIC), b_alpha, g_mid, Wk, Wv, g_knorm:
  *            ADDED. Without feedback the router entries a channel never reads get nothing.

@@ -1465,8 +1465,8 @@ int wm_pool_backward(const wm_dims* dims, const wm_params* params, const void* H
   WM_TRY(check_backward(d));
   WM_TRY(check_pool_grads(d, params, grads));
   WM_TRY(need_ptr(H, "H"));
-  WM_TRY(grad_ptr(dKc, "(dKc)"));
-  WM_TRY(grad_ptr(dVc, "(dVc)"));
+  WM_TRY(need_ptr(dKc, "dKc"));
+  WM_TRY(need_ptr(dVc, "dVc"));
   WM_TRY(grad_ptr(dH, "(dH)"));
   WM_TRY(check_ws(d, WM_OP_POOL_BACKWARD, ws, ws_bytes));
   (void)hipGetLastError();

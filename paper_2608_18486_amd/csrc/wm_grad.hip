@@ -455,15 +455,21 @@ void launch_grad_gemm(GemmArgs a, int batches, hipStream_t s) {
 }
 
 // --------------------------------------------------------------- row kernels
-// out[r][e] = g[(r / gdiv) % gmod][e] * x[r][e] * rinv[r], as bf16; one block per row.
+// out[r][e] = g[(r / gdiv) % gmod][e] * x[r][e] * rinv[r], as bf16; one block per row,
+// eight elements per thread (D is a multiple of 32, rows 16-byte aligned).
 __global__ __launch_bounds__(256) void grad_norm_apply_kernel(const bf16* x, const bf16* g,
                                                               const float* rinv, long gdiv,
                                                               int gmod, int D, bf16* out) {
   const long r = blockIdx.x;
   const bf16* gr = g + ((r / gdiv) % gmod) * (long)D;
   const float ri = rinv[r];
-  for (int e = threadIdx.x; e < D; e += 256)
-    out[r * D + e] = (bf16)((float)gr[e] * (float)x[r * D + e] * ri);
+  for (int e = 8 * threadIdx.x; e < D; e += 2048) {
+    const bf16x8 xv = *(const bf16x8*)(x + r * D + e), gv = *(const bf16x8*)(gr + e);
+    bf16x8 o;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) o[u] = (bf16)((float)gv[u] * (float)xv[u] * ri);
+    *(bf16x8*)(out + r * D + e) = o;
+  }
 }
 
 void launch_grad_norm_apply(const bf16* x, const bf16* g, const float* rinv, long rows, long gdiv,
@@ -490,8 +496,10 @@ __global__ __launch_bounds__(256) void grad_head_kernel(HeadArgs a) {
 #pragma unroll
   for (int q = 0; q < PER; ++q) dg[q] = 0.f;
   const bf16* g = a.g + (long)z * DH;
-  for (long rr = r0 + w; rr < r1; rr += 4) {
-    const int i = (int)(rr % a.T), hh = (int)(rr / a.T % a.H), b = (int)(rr / ((long)a.T * a.H));
+  // row rr = (b H + hh) T + i, stepped by 4 without divisions in the loop
+  long rr = r0 + w;
+  int i = (int)(rr % a.T), hh = (int)(rr / a.T % a.H), b = (int)(rr / ((long)a.T * a.H));
+  for (; rr < r1; rr += 4) {
     const int slot = a.slot_ctx ? ctx_at(a.ctx_len, b, a.ctx_hi) + i : i;
     const float* src = a.src + ((long)z * a.sZ + (long)b * a.sB + (long)hh * a.sH + slot) * DH;
     const long yrow = ((long)z * a.B * a.T + (long)b * a.T + i) * a.H * DH + (long)hh * DH;
@@ -526,6 +534,14 @@ __global__ __launch_bounds__(256) void grad_head_kernel(HeadArgs a) {
       if (e < DH) {
         a.dy[yrow + e] = (bf16)(ri * (gy[q] - yv[q] * c2));
         dg[q] += dr[q] * yv[q] * ri;
+      }
+    }
+    i += 4;
+    while (i >= a.T) {
+      i -= a.T;
+      if (++hh == a.H) {
+        hh = 0;
+        ++b;
       }
     }
   }
@@ -885,22 +901,27 @@ __global__ __launch_bounds__(256) void grad_gather_kernel(const float* src, int 
                                                           int T, int S_cap, int d,
                                                           const int32_t* ctx_len, int ctx_hi,
                                                           bf16* dst) {
-  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  const long n = (long)k * B * T * H * d;
-  if (idx >= n) return;
-  const int e = (int)(idx % d), hh = (int)(idx / d % H);
-  const long t = idx / ((long)d * H);  // (j, b, i)
-  const int i = (int)(t % T), b = (int)(t / T % B), j = (int)(t / ((long)T * B));
-  const int slot = ctx_at(ctx_len, b, ctx_hi) + i;
-  dst[idx] = (bf16)src[((((long)j * B + b) * H + hh) * S_cap + slot) * d + e];
+  // four consecutive elements per thread (d is a multiple of 4); the group count fits 31 bits
+  const unsigned n4 = (unsigned)((long)k * B * T * H * d / 4);
+  const unsigned idx = blockIdx.x * 256u + threadIdx.x;
+  if (idx >= n4) return;
+  const unsigned d4 = (unsigned)d / 4, e = 4 * (idx % d4), hh = idx / d4 % (unsigned)H;
+  const unsigned t = idx / (d4 * (unsigned)H);  // (j, b, i)
+  const unsigned i = t % (unsigned)T, b = t / (unsigned)T % (unsigned)B, j = t / ((unsigned)T * B);
+  const int slot = ctx_at(ctx_len, (int)b, ctx_hi) + (int)i;
+  const f32x4 v = *(const f32x4*)(src + ((((long)j * B + b) * H + hh) * S_cap + slot) * d + e);
+  bf16x4 o;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) o[u] = (bf16)v[u];
+  *(bf16x4*)(dst + (long)idx * 4) = o;
 }
 
 void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,
                         const int32_t* ctx_len, int ctx_hi, bf16* dst, hipStream_t s) {
-  const long n = (long)k * B * T * H * d;
-  if (n <= 0) return;
-  hipLaunchKernelGGL(grad_gather_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,
-                     k, B, H, T, S_cap, d, ctx_len, ctx_hi, dst);
+  const long n4 = (long)k * B * T * H * d / 4;
+  if (n4 <= 0) return;
+  hipLaunchKernelGGL(grad_gather_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s,
+                     src, k, B, H, T, S_cap, d, ctx_len, ctx_hi, dst);
 }
 
 // part[c][o] = sum over rows r in chunk c of x[r][o] (x [rows][n]); chunks = gridDim.y.
