@@ -337,17 +337,6 @@ def jacobi(dims: Dims, params, W_o, chan_map, X, passes: int):
     return H, top, Kc, Vc
 
 
-def jacobi_from(dims: Dims, params, W_o, chan_map, X, H0, passes: int):
-    """Jacobi iteration from given states H0 [B, T, L, D] in place of the embeddings."""
-    P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)
-    H0 = _f64(H0)
-    assert H0.shape == (dims.B, dims.T_new, dims.L, dims.D)
-    H, top, Kc, Vc = _pass_outputs(dims)
-    lib().wmo_jacobi_from(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(m), _ptr(X),
-                          _ptr(H0), ctypes.c_int(passes), _ptr(H), _ptr(top), _ptr(Kc), _ptr(Vc))
-    return H, top, Kc, Vc
-
-
 def gauss_seidel(dims: Dims, params, W_o, chan_map, X, g: int, passes: int):
     """Cyclic Gauss-Seidel iteration over g strided groups (Section 3.3)."""
     P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)
@@ -355,6 +344,19 @@ def gauss_seidel(dims: Dims, params, W_o, chan_map, X, g: int, passes: int):
     lib().wmo_gauss_seidel(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(m), _ptr(X),
                            ctypes.c_int(g), ctypes.c_int(passes), _ptr(H), _ptr(top), _ptr(Kc),
                            _ptr(Vc))
+    return H, top, Kc, Vc
+
+
+def gauss_seidel_from(dims: Dims, params, W_o, chan_map, X, g: int, Kc0, Vc0, passes: int):
+    """Gauss-Seidel passes from a given cache (Kc0, Vc0 [k, B, Hkv, S_cap, d]) in place of
+    Pool(H^(0))."""
+    P, W, m, X = _pass_args(dims, params, W_o, chan_map, X)
+    K0, V0 = np.ascontiguousarray(_f64(Kc0)), np.ascontiguousarray(_f64(Vc0))
+    H, top, Kc, Vc = _pass_outputs(dims)
+    assert K0.shape == Kc.shape and V0.shape == Vc.shape
+    lib().wmo_gauss_seidel_from(ctypes.byref(dims.c()), ctypes.byref(P.c), _ptr(W), _ptr(m),
+                                _ptr(X), ctypes.c_int(g), _ptr(K0), _ptr(V0),
+                                ctypes.c_int(passes), _ptr(H), _ptr(top), _ptr(Kc), _ptr(Vc))
     return H, top, Kc, Vc
 
 

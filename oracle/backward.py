@@ -64,17 +64,25 @@ def _router_layers(L, p):
     return [L - 1 - p * m for m in range(Lp)][::-1]
 
 
-def pool(dims: Dims, P: dict, H, ctx, store=_same):
+def _positions(B, T, ctx, grp):
+    """[B, T] float64 positions ctx[b] + q + g i of the call's tokens (grp = (g, q): the
+    strided token group of Section 3.3; (1, 0): contiguous tokens)."""
+    g, q = grp
+    return ctx.to(F64).reshape(B, 1) + q + g * torch.arange(T, dtype=F64)
+
+
+def pool(dims: Dims, P: dict, H, ctx, store=_same, grp=(1, 0)):
     """Steps 1-2 for every new token: H [B, T, L, D] -> the new cache rows
-    K, V [k, B, Hkv, T, d] (key norm and RoPE applied to K). store: applied to the mixed
-    channels and to the rows (bf16_store: as a path that keeps them in bf16)."""
+    K, V [k, B, Hkv, T, d] (key norm and RoPE applied to K, at the tokens' positions). store:
+    applied to the mixed channels and to the rows (bf16_store: as a path that keeps them in
+    bf16)."""
     B, T, L, k, D = dims.B, dims.T_new, dims.L, dims.k, dims.D
     Hkv, d = dims.Hkv, dims.d
     N = B * T
     h = H.reshape(N, L, D)
     sel = _router_layers(L, dims.p)
     Lp = len(sel)
-    pos = (ctx.to(F64).reshape(B, 1) + torch.arange(T, dtype=F64)).reshape(N)
+    pos = _positions(B, T, ctx, grp).reshape(N)
     out = []
     for br in range(2):
         hn = _rms(h, P["g_pre"][br], dims.eps)                            # [N, L, D]
@@ -110,23 +118,23 @@ def pool(dims: Dims, P: dict, H, ctx, store=_same):
     return out[0], out[1]
 
 
-def queries(dims: Dims, P: dict, H, ctx):
+def queries(dims: Dims, P: dict, H, ctx, grp=(1, 0)):
     """Step 7 for every consumer: Q [L, B, Hq, T, d] (input norm, W^Q, q-norm, RoPE)."""
     B, T, L, D, Hq, d = dims.B, dims.T_new, dims.L, dims.D, dims.Hq, dims.d
     x = _rms(H, P["g_in"], dims.eps)                                       # [B, T, L, D]
     y = torch.einsum("btld,lod->btlo", x, P["Wq"].reshape(L, Hq * d, D))
     y = y.reshape(B, T, L, Hq, d)
     y = _rms(y, P["g_qnorm"].reshape(1, 1, L, 1, d), dims.eps)
-    pos = ctx.to(F64).reshape(B, 1) + torch.arange(T, dtype=F64)           # [B, T]
+    pos = _positions(B, T, ctx, grp)                                      # [B, T]
     y = _rope(y, pos.reshape(B, T, 1, 1).expand(B, T, L, Hq), dims.rope_theta)
     return y.permute(2, 0, 3, 1, 4)
 
 
-def attend(dims: Dims, Kd, Vd, Q, chan_map, ctx, K, V):
+def attend(dims: Dims, Kd, Vd, Q, chan_map, ctx, K, V, grp=(1, 0)):
     """Step 3 (and Section 3.2's dummy): consumer l reads channel chan_map[l]. K, V are
-    the caches [k, B, Hkv, S, d] with token i of sequence b at slot ctx[b] + i; a query
-    at position t sees the dummy and slots < t (paper mask) or slots <= t (inclusive).
-    Returns O [L, B, T, Hq*d]."""
+    the caches [k, B, Hkv, S, d]; query i of sequence b sits at position t = ctx[b] + q +
+    g i (grp = (g, q)) and sees the dummy and slots < t (paper mask) or slots <= t
+    (inclusive). Returns O [L, B, T, Hq*d]."""
     B, T, L, Hq, Hkv, d = dims.B, dims.T_new, dims.L, dims.Hq, dims.Hkv, dims.d
     G = Hq // Hkv
     cm = torch.as_tensor(list(chan_map), dtype=torch.long)
@@ -134,12 +142,12 @@ def attend(dims: Dims, Kd, Vd, Q, chan_map, ctx, K, V):
     outs = []
     for b in range(B):
         c0 = int(ctx[b])
-        S = c0 + T
+        S = c0 + grp[1] + grp[0] * (T - 1) + 1
         Kb = K[cm, b, :, :S, :].repeat_interleave(G, dim=1)                 # [L, Hq, S, d]
         Vb = V[cm, b, :, :S, :].repeat_interleave(G, dim=1)
         q = Q[:, b]                                                        # [L, Hq, T, d]
         s = q @ Kb.transpose(-1, -2) / np.sqrt(d)                          # [L, Hq, T, S]
-        t = torch.arange(T).reshape(T, 1) + c0
+        t = (c0 + grp[1] + grp[0] * torch.arange(T)).reshape(T, 1)
         slot = torch.arange(S).reshape(1, S)
         vis = slot < t if paper else slot <= t
         s = s.masked_fill(~vis, float("-inf"))
@@ -286,13 +294,13 @@ def new_rows(dims: Dims, cache, ctx_len=None):
 
 # ------------------------------------------- Section 3.3: passes, truncated backprop
 
-def _states(dims: Dims, P: dict, W_o, X, chan_map, K, V, store=_same):
-    """States(X; P) with the stand-in block h_{l+1} = h_l + W_o[l] o_l: layer l's query from
-    h_l, its attention over channel chan_map[l] of the caches K, V [k, B, Hkv, T, d] (every
-    position's slot written by the pool). Returns (H [B, T, L, D], h_top [B, T, D]). store:
-    applied to each query, attention output and state."""
+def _states(dims: Dims, P: dict, W_o, X, chan_map, K, V, store=_same, grp=(1, 0)):
+    """States(X; P) with the stand-in block h_{l+1} = h_l + W_o[l] o_l for the call's tokens
+    (X [B, n, D] at positions q + g i, grp = (g, q)): layer l's query from h_l, its attention
+    over channel chan_map[l] of the caches K, V [k, B, Hkv, S, d]. Returns (H [B, n, L, D],
+    h_top [B, n, D]). store: applied to each query, attention output and state."""
     L = dims.L
-    one = dataclasses.replace(dims, L=1)
+    one = dataclasses.replace(dims, L=1, T_new=X.shape[1])
     ctx = torch.zeros(dims.B, dtype=torch.long)
     h = X
     Hs = []
@@ -300,44 +308,53 @@ def _states(dims: Dims, P: dict, W_o, X, chan_map, K, V, store=_same):
         Hs.append(h)
         sub = {**P, "g_in": P["g_in"][l:l + 1], "Wq": P["Wq"][l:l + 1],
                "g_qnorm": P["g_qnorm"][l:l + 1]}
-        q = store(queries(one, sub, h.unsqueeze(2), ctx))                  # [1, B, Hq, T, d]
-        o = store(attend(one, P["Kd"], P["Vd"], q, [chan_map[l]], ctx, K, V)[0])
+        q = store(queries(one, sub, h.unsqueeze(2), ctx, grp))             # [1, B, Hq, n, d]
+        o = store(attend(one, P["Kd"], P["Vd"], q, [chan_map[l]], ctx, K, V, grp)[0])
         h = store(h + o @ W_o[l].T)
     return torch.stack(Hs, dim=2), h
 
 
 def passes_forward(dims: Dims, P: dict, W_o, X, chan_map, passes: int, n_grad: int,
-                   store=_same):
-    """Jacobi passes (Section 3.3) as the C oracle runs them: H^(0) = X in every layer; pass
-    t pools H^(t-1) into the caches and recomputes H^(t) = States(X; caches). The states
-    entering the last n_grad passes are detached (truncated backpropagation): only those
-    passes carry gradients; with n_grad = passes nothing is cut and H^(0) stays a function
-    of X. Returns (H^(passes), h_top^(passes))."""
+                   store=_same, g: int = 1):
+    """The fixed-point passes of Section 3.3 as the C oracle's Gauss-Seidel driver runs them
+    (g = 1: Jacobi iteration): H^(0) = X in every layer and the cache starts as Pool(H^(0));
+    each pass runs the strided groups G_q = {i : i mod g = q} in order, group q recomputing
+    the states of its positions from the cache as it stands, then pooling them into its
+    slots. The cache entering the last n_grad passes is detached (truncated
+    backpropagation: the passes before run without gradient); with n_grad = passes nothing
+    is cut and the initial pool's gradient reaches X. Returns (H, h_top) after the last
+    pass."""
     B, T, L, D = dims.B, dims.T_new, dims.L, dims.D
-    H = X.unsqueeze(2).expand(B, T, L, D)
     ctx = torch.zeros(B, dtype=torch.long)
-    top = None
+    H = X.unsqueeze(2).expand(B, T, L, D)
+    K, V = pool(dims, P, H, ctx, store)
+    top = torch.zeros(B, T, D, dtype=F64)
     for t in range(1, passes + 1):
         if t == passes - n_grad + 1 and n_grad < passes:
-            H = H.detach()
-        K, V = pool(dims, P, H, ctx, store)
-        H, top = _states(dims, P, W_o, X, chan_map, K, V, store)
+            K, V = K.detach(), V.detach()
+        for q in range(g):
+            idx = torch.arange(q, T, g)
+            dq = dataclasses.replace(dims, T_new=len(idx))
+            Hq, tq = _states(dq, P, W_o, X[:, idx], chan_map, K, V, store, (g, q))
+            Kn, Vn = pool(dq, P, Hq, ctx, store, (g, q))
+            K, V = K.index_copy(3, idx, Kn), V.index_copy(3, idx, Vn)
+            H, top = H.index_copy(1, idx, Hq), top.index_copy(1, idx, tq)
     return H, top
 
 
 def passes_grads(dims: Dims, params, W_o, X, chan_map, passes: int, n_grad: int, dh_top,
-                 bf16_storage: bool = False) -> dict:
-    """Gradients of <dh_top, h_top> after `passes` Jacobi passes with backpropagation
-    truncated to the last n_grad (1 <= n_grad <= passes): dX, dW_o and d + name for every
-    parameter. bf16_storage: the forward rounds what a bf16 path stores between its steps
-    (mixed channels, cache rows, queries, attention outputs, states) to bf16, the
-    derivatives passing through the rounding; how far that moves the gradients measures
-    their sensitivity to the storage precision."""
+                 bf16_storage: bool = False, g: int = 1) -> dict:
+    """Gradients of <dh_top, h_top> after `passes` passes over g groups (passes_forward) with
+    backpropagation truncated to the last n_grad (1 <= n_grad <= passes): dX, dW_o and
+    d + name for every parameter. bf16_storage: the forward rounds what a bf16 path stores
+    between its steps (mixed channels, cache rows, queries, attention outputs, states) to
+    bf16, the derivatives passing through the rounding; how far that moves the gradients
+    measures their sensitivity to the storage precision."""
     assert 1 <= n_grad <= passes
     P = _params(params, True)
     Xt, Wt = _t(X, True), _t(W_o, True)
     _, top = passes_forward(dims, P, Wt, Xt, chan_map, passes, n_grad,
-                            bf16_store if bf16_storage else _same)
+                            bf16_store if bf16_storage else _same, g)
     loss = (top * _t(dh_top)).sum()
     leaves = [Xt, Wt] + [P[n] for n in PARAM_NAMES]
     g = torch.autograd.grad(loss, leaves, allow_unused=True)

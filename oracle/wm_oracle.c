@@ -672,26 +672,6 @@ void wmo_jacobi(const wmo_dims *dm, const wmo_params *P, const double *W_o, cons
     }
 }
 
-/* The same iteration from given states H0[B][T][L][D] in place of H^(0): the passes
- * that follow a point where the states are held fixed, as in truncated backpropagation
- * through the last passes (Section 3.3). */
-void wmo_jacobi_from(const wmo_dims *dm, const wmo_params *P, const double *W_o, const int *map,
-                     const double *X, const double *H0, int passes, double *H, double *h_top,
-                     double *Kc, double *Vc)
-{
-    int B = dm->B, T = dm->T_new, L = dm->L, D = dm->D;
-    memcpy(H, H0, sizeof(double) * (size_t)B * T * L * D);
-    for (int t = 1; t <= passes; ++t) {
-#pragma omp parallel for schedule(dynamic)
-        for (int n = 0; n < B * T; ++n)
-            pool_position(dm, P, H + (size_t)n * L * D, n / T, n % T, Kc, Vc);
-#pragma omp parallel for schedule(dynamic)
-        for (int n = 0; n < B * T; ++n)
-            states_position(dm, P, W_o, map, X + (size_t)n * D, n / T, n % T, Kc, Vc,
-                            H + (size_t)n * L * D, h_top + (size_t)n * D);
-    }
-}
-
 /* Cyclic Gauss-Seidel iteration, Section 3.3: the positions split into g
  * strided groups G_q = {i : i mod g = q}. The cache starts as Pool(H^(0)); each
  * pass evaluates G_0 .. G_{g-1} in order, and group q first recomputes the
@@ -712,6 +692,38 @@ void wmo_gauss_seidel(const wmo_dims *dm, const wmo_params *P, const double *W_o
     for (int t = 1; t <= passes; ++t) {
         for (int q = 0; q < g; ++q) {
             int per = (T - q + g - 1) / g; /* positions q, q + g, ... below T */
+#pragma omp parallel for schedule(dynamic)
+            for (int u = 0; u < B * per; ++u) {
+                int b = u / per, i = q + g * (u % per);
+                size_t n = (size_t)b * T + i;
+                states_position(dm, P, W_o, map, X + n * D, b, i, Kc, Vc, H + n * L * D,
+                                h_top + n * D);
+            }
+#pragma omp parallel for schedule(dynamic)
+            for (int u = 0; u < B * per; ++u) {
+                int b = u / per, i = q + g * (u % per);
+                pool_position(dm, P, H + ((size_t)b * T + i) * L * D, b, i, Kc, Vc);
+            }
+        }
+    }
+}
+
+/* The same iteration from a given cache Kc0, Vc0 in place of Pool(H^(0)): the passes that
+ * follow a point where the cache is held fixed, as in truncated backpropagation through
+ * the last passes (Section 3.3). */
+void wmo_gauss_seidel_from(const wmo_dims *dm, const wmo_params *P, const double *W_o,
+                           const int *map, const double *X, int g, const double *Kc0,
+                           const double *Vc0, int passes, double *H, double *h_top,
+                           double *Kc, double *Vc)
+{
+    int B = dm->B, T = dm->T_new, L = dm->L, D = dm->D;
+    size_t cache = (size_t)dm->k * B * dm->Hkv * dm->S_cap * dm->d;
+    memcpy(Kc, Kc0, sizeof(double) * cache);
+    memcpy(Vc, Vc0, sizeof(double) * cache);
+    initial_states(dm, X, H);
+    for (int t = 1; t <= passes; ++t) {
+        for (int q = 0; q < g; ++q) {
+            int per = (T - q + g - 1) / g;
 #pragma omp parallel for schedule(dynamic)
             for (int u = 0; u < B * per; ++u) {
                 int b = u / per, i = q + g * (u % per);

@@ -332,45 +332,47 @@ PASS_CASES = [dict(), dict(mask_mode=oracle.MASK_INCLUSIVE, mix_mode=oracle.MIX_
 
 
 @pytest.mark.parametrize("kw", PASS_CASES)
-def test_passes_forward_matches_c_oracle(kw):
+@pytest.mark.parametrize("g", [1, 2, 3])
+def test_passes_forward_matches_c_oracle(kw, g):
     dm = _dims(T_new=6, **kw)
     dm.S_cap = dm.T_new
     P, W_o, X, _, _ = _pass_inputs(dm)
     cmap = [(l + 1) % dm.k for l in range(dm.L)]
-    H, top, _, _ = oracle.jacobi(dm, P, W_o, cmap, X, 3)
+    H, top, _, _ = oracle.gauss_seidel(dm, P, W_o, cmap, X, g, 3)
     Pt = {n: ob._t(P[n]) for n in oracle.PARAM_NAMES}
-    Ht, topt = ob.passes_forward(dm, Pt, ob._t(W_o), ob._t(X), cmap, 3, 3)
+    Ht, topt = ob.passes_forward(dm, Pt, ob._t(W_o), ob._t(X), cmap, 3, 3, g=g)
     assert np.abs(Ht.detach().numpy() - H).max() < 1e-12
     assert np.abs(topt.detach().numpy() - top).max() < 1e-12
 
 
 @pytest.mark.parametrize("kw", PASS_CASES)
-@pytest.mark.parametrize("passes,n_grad", [(2, 2), (3, 1), (3, 2)])
-def test_truncated_pass_gradients_match_finite_differences(kw, passes, n_grad):
+@pytest.mark.parametrize("passes,n_grad,g", [(2, 2, 1), (3, 1, 1), (3, 2, 1), (2, 2, 2),
+                                             (2, 1, 3)])
+def test_truncated_pass_gradients_match_finite_differences(kw, passes, n_grad, g):
     """Full backpropagation (n_grad = passes) against central differences of the C oracle's
-    Jacobi passes; truncated backpropagation against central differences of the last
-    n_grad passes run from the states entering them, held fixed at their value (the C
-    oracle's passes from given states)."""
-    dm = _dims(T_new=5, **kw)
+    passes; truncated backpropagation against central differences of the last n_grad passes
+    run by the C oracle from the cache entering them, held fixed at its value."""
+    dm = _dims(T_new=6, **kw)
     dm.S_cap = dm.T_new
     P, W_o, X, dh, rng = _pass_inputs(dm)
     cmap = [(2 * l + 1) % dm.k for l in range(dm.L)]
-    g = ob.passes_grads(dm, P, W_o, X, cmap, passes, n_grad, dh)
+    gr = ob.passes_grads(dm, P, W_o, X, cmap, passes, n_grad, dh, g=g)
     if n_grad == passes:
         def top(Px, Wx, Xx):
-            return (oracle.jacobi(dm, Px, Wx, cmap, Xx, passes)[1] * dh).sum()
+            return (oracle.gauss_seidel(dm, Px, Wx, cmap, Xx, g, passes)[1] * dh).sum()
     else:
-        H0 = oracle.jacobi(dm, P, W_o, cmap, X, passes - n_grad)[0]
+        _, _, K0, V0 = oracle.gauss_seidel(dm, P, W_o, cmap, X, g, passes - n_grad)
 
         def top(Px, Wx, Xx):
-            return (oracle.jacobi_from(dm, Px, Wx, cmap, Xx, H0, n_grad)[1] * dh).sum()
+            return (oracle.gauss_seidel_from(dm, Px, Wx, cmap, Xx, g, K0, V0, n_grad)[1]
+                    * dh).sum()
     checks = [("dX", lambda x: top(P, W_o, x), X), ("dW_o", lambda x: top(P, x, X), W_o)]
     for n in oracle.PARAM_NAMES:
         checks.append(("d" + n, lambda x, n=n: top({**P, n: x}, W_o, X), P[n]))
     for name, f, x in checks:
         v = rng.standard_normal(x.shape)
         num = _fd(f, x, v, eps=2e-5)
-        ana = (g[name] * v).sum()
+        ana = (gr[name] * v).sum()
         assert abs(num - ana) <= 1e-6 * max(1.0, abs(num)), (name, num, ana)
 
 
