@@ -238,20 +238,21 @@ int wm_channel_attend_dense(const wm_dims *dims, const wm_params *params, const 
  * dS_j = P_j (dO.v_j - dO.O): dQ = sum_j dS_j k_j / sqrt(d); every slot's dK sums
  * dS_j q / sqrt(d) and its dV sums P_j dO over all rows that read it (every consumer of
  * its channel and every query head of its KV head); the dummy's likewise.
- * bf16 only, head dims 64 and 96, full-sequence calls (T_new > 4) of contiguous tokens
- * (dims.groups <= 1), no document mask.
+ * bf16 only, head dims 64 and 96, full-sequence calls (T_new > 4) of contiguous tokens or
+ * of one strided group (dims.groups, dims.group), no document mask.
  *   Q, chan_map, ctx_len, Kc, Vc  as wm_channel_attend
  *   O        device [L][B][T_new][Hq*d] bf16: that call's output
  *   dO       device [L][B][T_new][Hq*d] bf16: the gradient of the loss in O
  *   dQ       device float [L][B][Hq][T_new][d]
- *   dKc, dVc device float [k][B][Hkv][S_cap][d]: slots below ctx_len[b] + T_new of every
- *            (channel, sequence, KV head) are written (zero where no row reads the slot);
+ *   dKc, dVc device float [k][B][Hkv][S_cap][d]: slots below ctx_len[b] + span of every
+ *            (channel, sequence, KV head) are written (zero where no row reads the slot),
+ *            span = T_new for contiguous tokens, q + g (T_new - 1) + 1 for group q of g;
  *            the others are left as they are
  *   dKd, dVd device float [k][Hkv][d] (written; zero in WM_MASK_INCLUSIVE)
  * Workspace: wm_workspace_size(dims, WM_OP_ATTEND_BACKWARD) bytes (four floats per query
  * row: the row's log-sum-exp, dO.O and the dummy's weight and dS). Errors: WM_ERR_DTYPE for
- * fp32, WM_ERR_SHAPE for other head dims or T_new <= 4, WM_ERR_ARG for groups > 1 or a
- * NULL pointer, otherwise as wm_channel_attend. */
+ * fp32, WM_ERR_SHAPE for other head dims or T_new <= 4, WM_ERR_ARG for a NULL pointer,
+ * otherwise as wm_channel_attend. */
 int wm_channel_attend_backward(const wm_dims *dims, const wm_params *params, const void *Q,
                                const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
                                const void *Vc, const void *O, const void *dO, float *dQ,
@@ -261,7 +262,7 @@ int wm_channel_attend_backward(const wm_dims *dims, const wm_params *params, con
 /* Gradients of the consumer queries (wm_q_project) for a loss gradient dQ in the
  * queries: back through RoPE (the transposed rotation), the q norm, W^Q_l and the input
  * norm, with the forward's intermediate values recomputed from H.
- * bf16, head dims 64 and 96, contiguous tokens (dims.groups <= 1), D <= 4608.
+ * bf16, head dims 64 and 96, contiguous tokens or one strided group, D <= 4608.
  *   H        device [B][T_new][L][D] bf16, ctx_len device int32 [B] or NULL: as the forward
  *   dQ       device float [L][B][Hq][T_new][d]
  *   dH       device float [B][T_new][L][D]: the gradient in H is ADDED
@@ -279,11 +280,12 @@ int wm_q_project_backward(const wm_dims *dims, const wm_params *params, const vo
  * through the softmax over depth, or the no-feedback mask, to the router's logits), the
  * router (W_alpha, b_alpha) and the pre-mix norm. The router, mix and norms of the forward
  * are recomputed from H with the forward's kernels.
- * bf16, head dims 64 and 96, contiguous tokens, D <= 4608; every router mode and mix mode.
+ * bf16, head dims 64 and 96, contiguous tokens or one strided group, D <= 4608; every
+ * router mode and mix mode.
  *   H, ctx_len  as wm_pool
- *   dKc, dVc device float [k][B][Hkv][S_cap][d], 16-byte aligned: slot ctx_len[b] + i of
- *            every (channel, sequence, KV head) is read (the call's new rows); no other slot
- *            is read
+ *   dKc, dVc device float [k][B][Hkv][S_cap][d], 16-byte aligned: the slot of token i,
+ *            ctx_len[b] + i (ctx_len[b] + q + g i in group q of g), of every (channel,
+ *            sequence, KV head) is read (the call's new rows); no other slot is read
  *   dH       device float [B][T_new][L][D]: ADDED
  *   grads    g_pre, W_alpha (not with WM_ROUTER_STATIC), b_alpha, g_mid, Wk, Wv, g_knorm:
  *            ADDED. Without feedback the router entries a channel never reads get nothing.
@@ -304,9 +306,10 @@ int wm_pool_backward(const wm_dims *dims, const wm_params *params, const void *H
  *   dO       device [L][B][T_new][Hq*d] bf16
  *   dKc, dVc device float [k][B][Hkv][S_cap][d], 16-byte aligned, in/out: on entry the
  *            gradient that reaches the caches from elsewhere (zero if none); the attention's
- *            gradient is added to slots below ctx_len[b] + T_new, and the new slots' total
- *            is what the pool's backward receives. On return the context slots (below
- *            ctx_len[b]) hold the gradient for the step that wrote them.
+ *            gradient is added to slots below ctx_len[b] + span (as in
+ *            wm_channel_attend_backward), and the new slots' total is what the pool's
+ *            backward receives. On return the other slots hold the gradient for the steps
+ *            that wrote them.
  *   dH       device float [B][T_new][L][D]: ADDED
  *   grads    every entry (Kd, Vd only with WM_MASK_PAPER; W_alpha not with static
  *            weights): ADDED

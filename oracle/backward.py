@@ -206,35 +206,56 @@ def _splice(dims, ctx, Kc, Vc, Kn, Vn):
     return torch.stack(Kcs, dim=1), torch.stack(Vcs, dim=1)
 
 
-def channel_attend_grads(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, dO) -> dict:
-    """Gradients of <dO, O> for O = channel attention over the given cache: dQ, dKc, dVc
-    (every cache slot; zero where no query reads it) and the dummy's dKd, dVd."""
+def channel_attend_grads(dims: Dims, params, Q, chan_map, ctx_len, Kc, Vc, dO,
+                         grp=(1, 0)) -> dict:
+    """Gradients of <dO, O> for O = channel attention over the given cache (queries at
+    positions ctx[b] + q + g i, grp = (g, q)): dQ, dKc, dVc (every cache slot; zero where no
+    query reads it) and the dummy's dKd, dVd."""
     P = _params(params, False)
     ctx = _ctx(dims, ctx_len)
     Qt, Kt, Vt = _t(Q, True), _t(Kc, True), _t(Vc, True)
     Kd, Vd = P["Kd"].requires_grad_(True), P["Vd"].requires_grad_(True)
-    O = attend(dims, Kd, Vd, Qt, chan_map, ctx, Kt, Vt)
+    O = attend(dims, Kd, Vd, Qt, chan_map, ctx, Kt, Vt, grp)
     g = torch.autograd.grad(O, [Qt, Kt, Vt, Kd, Vd], grad_outputs=_t(dO), allow_unused=True)
     names = ("dQ", "dKc", "dVc", "dKd", "dVd")
     return {n: (x if x is not None else torch.zeros_like(v)).numpy()
             for n, x, v in zip(names, g, [Qt, Kt, Vt, Kd, Vd])}
 
 
+def _splice_group(dims, ctx, Kc, Vc, Kn, Vn, grp):
+    """The given caches (every slot the call's queries may read) with the call's rows
+    written at slots ctx[b] + q + g i."""
+    g, q = grp
+    Ks, Vs = [], []
+    for b in range(dims.B):
+        idx = int(ctx[b]) + q + g * torch.arange(dims.T_new)
+        Ks.append(Kc[:, b].index_copy(2, idx, Kn[:, b]))
+        Vs.append(Vc[:, b].index_copy(2, idx, Vn[:, b]))
+    return torch.stack(Ks, dim=1), torch.stack(Vs, dim=1)
+
+
 def layer_step_grads(dims: Dims, params, H, chan_map, dO, ctx_len=None, Kc=None, Vc=None,
-                     dKc=None, dVc=None) -> dict:
+                     dKc=None, dVc=None, grp=(1, 0)) -> dict:
     """Gradients of <dO, O> (+ <dKc, K> + <dVc, V> over the new cache slots, when given:
     the gradient a later reader of this step's cache sends back) through the whole fused
     step: dH [B, T, L, D], one entry per parameter (d + name), and the gradients of the
-    context cache slots read (dKc_ctx, dVc_ctx, shaped like Kc)."""
+    cache slots read that the step does not write (dKc_ctx, dVc_ctx, shaped like Kc). With
+    a strided token group (grp = (g, q), tokens at ctx[b] + q + g i) Kc, Vc hold every slot
+    the queries may read (the other groups' and the context's)."""
     P = _params(params, True)
     ctx = _ctx(dims, ctx_len)
     Ht = _t(H, True)
-    have_ctx = Kc is not None and int(ctx.max()) > 0
+    strided = tuple(grp) != (1, 0)
+    have_ctx = Kc is not None and (strided or int(ctx.max()) > 0)
     Kci = _t(Kc, True) if have_ctx else None
     Vci = _t(Vc, True) if have_ctx else None
-    Kn, Vn = pool(dims, P, Ht, ctx)
-    Kall, Vall = _splice(dims, ctx, Kci, Vci, Kn, Vn)
-    O = attend(dims, P["Kd"], P["Vd"], queries(dims, P, Ht, ctx), chan_map, ctx, Kall, Vall)
+    Kn, Vn = pool(dims, P, Ht, ctx, grp=grp)
+    if strided:
+        Kall, Vall = _splice_group(dims, ctx, Kci, Vci, Kn, Vn, grp)
+    else:
+        Kall, Vall = _splice(dims, ctx, Kci, Vci, Kn, Vn)
+    O = attend(dims, P["Kd"], P["Vd"], queries(dims, P, Ht, ctx, grp), chan_map, ctx, Kall,
+               Vall, grp)
     loss = (O * _t(dO)).sum()
     if dKc is not None:
         loss = loss + (Kn * _t(dKc)).sum() + (Vn * _t(dVc)).sum()

@@ -691,13 +691,11 @@ int grad_ptr(const float* p, const char* name) {
   return WM_OK;
 }
 
-// What every gradient op supports: bf16, head dims 64 and 96, contiguous tokens, rows of
-// at most 4608 for the norms' backward, and the mix gradient's LDS.
+// What every gradient op supports: bf16, head dims 64 and 96, rows of at most 4608 for the
+// norms' backward, and the mix gradient's LDS.
 int check_backward(const wm_dims& d) {
   if (d.dtype != WM_BF16) return fail(WM_ERR_DTYPE, "the gradients are built for bf16");
   if (d.d != 64 && d.d != 96) return fail(WM_ERR_SHAPE, "the gradients support head dims 64 and 96");
-  if (group_stride(d) > 1)
-    return fail(WM_ERR_ARG, "the gradients need contiguous new tokens (groups <= 1)");
   if (d.D > 4608) return fail(WM_ERR_SHAPE, "the gradients support D <= 4608");
   if (wm::grad_mix_smem(d.L, d.k, d.D) > 65536)
     return fail(WM_ERR_SHAPE, "L and k too large for the mix gradient's LDS");
@@ -728,7 +726,7 @@ void run_q_backward(const wm_dims& d, const wm_params& P, const bf16* H, const i
   // RoPE and q norm backward: y's gradient (bf16)
   wm::HeadArgs h{};
   h.src = dQ, h.sZ = (long)d.B * d.Hq * d.T_new, h.sB = (long)d.Hq * d.T_new, h.sH = d.T_new;
-  h.slot_ctx = 0, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
+  h.slot_ctx = 0, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi, h.gs = 1, h.gq = 0;
   h.y = yq, h.dy = dyq, h.g = (const bf16*)P.g_qnorm, h.tab = tab, h.dgp = dgp;
   h.B = d.B, h.H = d.Hq, h.T = d.T_new, h.chunks = red_chunks(L), h.eps = d.eps;
   wm::launch_grad_head(h, L, d.d, s);
@@ -794,13 +792,14 @@ void run_pool_backward(const wm_dims& d, const wm_params& P, const bf16* H,
       wm::HeadArgs h{};
       h.src = dKc, h.sZ = (long)d.B * d.Hkv * d.S_cap, h.sB = (long)d.Hkv * d.S_cap;
       h.sH = d.S_cap, h.slot_ctx = 1, h.ctx_len = ctx_len, h.ctx_hi = sh.ctx_hi;
+      h.gs = sh.gs, h.gq = sh.gq;
       h.y = ydy, h.dy = dyb, h.g = (const bf16*)P.g_knorm, h.tab = tab, h.dgp = dgp;
       h.B = d.B, h.H = d.Hkv, h.T = d.T_new, h.chunks = red_chunks(k), h.eps = d.eps;
       wm::launch_grad_head(h, k, d.d, s);
       wm::launch_grad_sum(dgp, k, h.chunks, d.d, G.g_knorm, 1.f, 1, s);
     } else {
-      wm::launch_grad_gather(dVc, k, d.B, d.Hkv, d.T_new, d.S_cap, d.d, ctx_len, sh.ctx_hi, dyb,
-                             s);
+      wm::launch_grad_gather(dVc, k, d.B, d.Hkv, d.T_new, d.S_cap, d.d, ctx_len, sh.ctx_hi, sh.gs,
+                             sh.gq, dyb, s);
     }
     // du_j = dy_j W_j [N][D]; dW_j += dy_j^T u_j [HK][D]
     gemm(opnd(dyb, HK, 1, (long)N * HK, false), opnd(W, 1, D, (long)HK * D, false), du, D, 1,
@@ -1308,8 +1307,6 @@ int wm_channel_attend_backward(const wm_dims* dims, const wm_params* params, con
     return fail(WM_ERR_SHAPE, "the attention gradients support head dims 64 and 96");
   if (decode_path(d))
     return fail(WM_ERR_SHAPE, "the attention gradients need a full-sequence call (T_new > 4)");
-  if (group_stride(d) > 1)
-    return fail(WM_ERR_ARG, "the attention gradients need contiguous new tokens (groups <= 1)");
   if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_KD, P_VD}));
   else if (!params) return fail(WM_ERR_ARG, "params is NULL");
   WM_TRY(need_ptr(Q, "Q"));

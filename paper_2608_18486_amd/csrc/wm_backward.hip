@@ -10,7 +10,7 @@
 //   attend_bwd_dq_kernel   query-major, like the forward: LSE (one pass over the slots),
 //                          then dq (a second pass); writes per-row LSE, D and the dummy's
 //                          P and dS.
-//   attend_bwd_dkv_kernel  slot-major: a workgroup owns 128 slots of one channel, sequence
+//   attend_bwd_dkv_kernel  slot-major: a workgroup owns 256 slots of one channel, sequence
 //                          and KV head and walks every query that reads them (all
 //                          consumers of the channel, all grouped query heads), so each
 //                          slot's dk and dv are summed in registers and written once.
@@ -36,6 +36,7 @@ struct BwdArgs {
   ChannelGroups grp;
   int accumulate;  // add the slot and dummy gradients into dKc, dVc, dKd, dVd
   int dchunks;     // partial sums per (channel, KV head) of the dummy's gradients
+  int gs, gq;      // query i of sequence b sits at position ctx_len[b] + gq + gs i
 };
 
 // waves per workgroup of the query-major and the slot-major kernel (32 rows each)
@@ -142,11 +143,13 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
   const float sd = halves_sum(sdp) * cl2;  // the dummy's score, log2 units
   dpd = halves_sum(dpd);
 
+  const int pq = pos0 + a.gq + incl;  // position (+ incl) of query 0; query i adds gs i
   const int qlast = min(q0 + 32 * NW - 1, a.T - 1);
-  const int kend = min(pos0 + qlast + incl, a.S_cap);            // slots the tile may see
+  const int kend = min(pq + a.gs * qlast, a.S_cap);              // slots the tile may see
   const int wq_last = min(qw0 + 31, a.T - 1);
-  const int wkend = wq_last >= qw0 ? pos0 + wq_last + incl : 0;  // ... this wave
-  const int lim = pos0 + qi + incl;                              // ... this lane's row
+  const int wkend = wq_last >= qw0 ? pq + a.gs * wq_last : 0;    // ... this wave
+  const int lim = pq + a.gs * qi;                                // ... this lane's row
+  const int wlim0 = pq + a.gs * qw0;                             // ... the wave's first row
   const int nblk = (kend + BLK - 1) / BLK;
   const long cbase = (((long)c * a.B + b) * a.Hkv + kvh) * (long)a.S_cap * DH;
   const auto kv = make_view(a.Kc + cbase, (uint32_t)max(kend, 0) * ROW);
@@ -178,7 +181,7 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
           for (int x = 0; x < NH; ++x)
             sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, kb + (NH * hg + x) * 32 * ROW, ks), qf[ks]);
         float mx = kNegBig;
-        if (sb + 32 * NH - 1 < pos0 + qw0 + incl) {  // every row of the wave sees the group
+        if (sb + 32 * NH - 1 < wlim0) {  // every row of the wave sees the group
 #pragma unroll
           for (int x = 0; x < NH; ++x)
 #pragma unroll
@@ -243,7 +246,7 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
             dp[x] = mma32(dp[x], pf_ldk<DH>(smem, lo, ho + BLK * ROW, ks), df[ks]);
           }
         bf16x8 ds[NH][2];
-        if (sb + 32 * NH - 1 < pos0 + qw0 + incl) {  // no mask in this group
+        if (sb + 32 * NH - 1 < wlim0) {  // no mask in this group
 #pragma unroll
           for (int x = 0; x < NH; ++x)
 #pragma unroll
@@ -328,7 +331,8 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int pos0 = __builtin_amdgcn_readfirstlane(ctx_at(a.ctx_len, b, a.ctx_hi));
   const int incl = a.mask_paper ? 0 : 1;
-  const int send = pos0 + a.T;  // slots written: [0, send)
+  const int pq = pos0 + a.gq + incl;  // query qr sees slots below pq + gs qr
+  const int send = pos0 + a.gq + a.gs * (a.T - 1) + 1;  // slots written: [0, send)
   const int sbase = stile * 32 * NW;
   if (sbase >= send) return;
   const int ws0 = sbase + 32 * w, slot = ws0 + r;
@@ -351,8 +355,9 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) dk[dt] = dv[dt] = zero16();
   const PfLane<DH> lo = pf_lane<DH>(lane);
-  // the first query that sees slot sbase sits at position sbase + 1 - incl
-  const int i_first = max(0, sbase + 1 - incl - pos0);
+  // the first query that sees slot sbase: the least qr with pq + gs qr > sbase
+  const int i_num = sbase - pq;
+  const int i_first = i_num < 0 ? 0 : i_num / a.gs + 1;
   const int qb0 = i_first / QB, nqb = (a.T + QB - 1) / QB - qb0;
   const int nmem = a.grp.offsets[c + 1] - a.grp.offsets[c];
   const int nit = nqb > 0 ? nmem * G * nqb : 0;
@@ -402,7 +407,7 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
 #pragma unroll
     for (int hg = 0; hg < 2 / NH; ++hg) {
       const int qg = qb * QB + 32 * NH * hg;  // the group's first row
-      if (qg < a.T && pos0 + min(qg + 32 * NH - 1, a.T - 1) + incl > ws0) {
+      if (qg < a.T && pq + a.gs * min(qg + 32 * NH - 1, a.T - 1) > ws0) {
         f32x16 sc[NH], dp[NH];
 #pragma unroll
         for (int x = 0; x < NH; ++x) sc[x] = dp[x] = zero16();
@@ -417,7 +422,7 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
         // lane (h, r): slot r of the wave, rows 32 x + 8 (i / 4) + 4 h + i % 4 of the group
         bf16x8 pp[NH][2], pds[NH][2];
         const int hb = 32 * NH * hg;  // the group's rows in the staged block
-        if (ws0 + 31 < pos0 + qg + incl) {  // every row of the group sees every slot
+        if (ws0 + 31 < pq + a.gs * qg) {  // every row of the group sees every slot
 #pragma unroll
           for (int x = 0; x < NH; ++x)
 #pragma unroll
@@ -433,7 +438,8 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
               }
             }
         } else {
-          const int thr = slot - pos0 - incl - qg - 4 * h;  // row 32 x + 8 g + e sees it iff > thr
+          // row qg + 32 x + 8 g + 4 h + e sees the slot iff thr + gs (32 x + 8 g + e) > 0
+          const int thr = pq + a.gs * (qg + 4 * h) - slot;
 #pragma unroll
           for (int x = 0; x < NH; ++x)
 #pragma unroll
@@ -443,7 +449,8 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 const int i = 4 * g + e;
-                const float p = 32 * x + 8 * g + e > thr ? bwd_exp2(sc[x][i] * cl2 - lz[e]) : 0.f;
+                const float p = thr + a.gs * (32 * x + 8 * g + e) > 0
+                                    ? bwd_exp2(sc[x][i] * cl2 - lz[e]) : 0.f;
                 pp[x][i >> 3][i & 7] = (bf16)p;
                 pds[x][i >> 3][i & 7] = (bf16)(p * (dp[x][i] - dz[e]));
               }
@@ -585,10 +592,10 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
   BwdArgs a{Q, Kc, Vc, Kd, Vd, O, dO, ctx_len, dQ, dKc, dVc, dKd, dVd, rows, rows + nrow,
             rows + 2 * nrow, rows + 3 * nrow, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
             sh.mask_paper, sh.ctx_hi, (sh.T_new + 32 * kBwdQWaves - 1) / (32 * kBwdQWaves),
-            (int)(((long)sh.ctx_max + sh.T_new + 32 * kBwdKWaves - 1) / (32 * kBwdKWaves)),
+            (int)(((long)sh.ctx_max + sh.span() + 32 * kBwdKWaves - 1) / (32 * kBwdKWaves)),
             kLog2e / sqrtf((float)sh.d),
             1.0f / sqrtf((float)sh.d), chan_map, groups, accumulate ? 1 : 0,
-            dummy_chunks(sh)};
+            dummy_chunks(sh), sh.gs, sh.gq};
   const dim3 ga(a.n_qtiles * sh.Hq * sh.B * sh.L), gb(a.n_stiles * sh.Hkv * sh.B * sh.k),
       gp(sh.k * sh.Hkv * a.dchunks), gs(sh.k * sh.Hkv);
   float* part = rows + 4 * nrow;

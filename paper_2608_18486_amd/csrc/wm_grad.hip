@@ -500,7 +500,7 @@ __global__ __launch_bounds__(256) void grad_head_kernel(HeadArgs a) {
   long rr = r0 + w;
   int i = (int)(rr % a.T), hh = (int)(rr / a.T % a.H), b = (int)(rr / ((long)a.T * a.H));
   for (; rr < r1; rr += 4) {
-    const int slot = a.slot_ctx ? ctx_at(a.ctx_len, b, a.ctx_hi) + i : i;
+    const int slot = a.slot_ctx ? ctx_at(a.ctx_len, b, a.ctx_hi) + a.gq + a.gs * i : i;
     const float* src = a.src + ((long)z * a.sZ + (long)b * a.sB + (long)hh * a.sH + slot) * DH;
     const long yrow = ((long)z * a.B * a.T + (long)b * a.T + i) * a.H * DH + (long)hh * DH;
     const float* tab = a.tab + ((long)b * a.T + i) * DH;  // DH / 2 (cos, sin) pairs
@@ -895,12 +895,12 @@ void launch_grad_mix(const MixGradArgs& a, hipStream_t s) {
   else hipLaunchKernelGGL(grad_mix_kernel<64>, grid, blk, sm, s, a);
 }
 
-// dst[j][b T + i][h d + e] = src[j][b][h][ctx_len[b] + i][e]: the new slots' rows of a
-// cache-layout gradient, token-major for the projection GEMMs.
+// dst[j][b T + i][h d + e] = src[j][b][h][ctx_len[b] + gq + gs i][e]: the call's slots' rows
+// of a cache-layout gradient, token-major for the projection GEMMs.
 __global__ __launch_bounds__(256) void grad_gather_kernel(const float* src, int k, int B, int H,
                                                           int T, int S_cap, int d,
                                                           const int32_t* ctx_len, int ctx_hi,
-                                                          bf16* dst) {
+                                                          int gs, int gq, bf16* dst) {
   // four consecutive elements per thread (d is a multiple of 4); the group count fits 31 bits
   const unsigned n4 = (unsigned)((long)k * B * T * H * d / 4);
   const unsigned idx = blockIdx.x * 256u + threadIdx.x;
@@ -908,7 +908,7 @@ __global__ __launch_bounds__(256) void grad_gather_kernel(const float* src, int 
   const unsigned d4 = (unsigned)d / 4, e = 4 * (idx % d4), hh = idx / d4 % (unsigned)H;
   const unsigned t = idx / (d4 * (unsigned)H);  // (j, b, i)
   const unsigned i = t % (unsigned)T, b = t / (unsigned)T % (unsigned)B, j = t / ((unsigned)T * B);
-  const int slot = ctx_at(ctx_len, (int)b, ctx_hi) + (int)i;
+  const int slot = ctx_at(ctx_len, (int)b, ctx_hi) + gq + gs * (int)i;
   const f32x4 v = *(const f32x4*)(src + ((((long)j * B + b) * H + hh) * S_cap + slot) * d + e);
   bf16x4 o;
 #pragma unroll
@@ -917,11 +917,12 @@ __global__ __launch_bounds__(256) void grad_gather_kernel(const float* src, int 
 }
 
 void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,
-                        const int32_t* ctx_len, int ctx_hi, bf16* dst, hipStream_t s) {
+                        const int32_t* ctx_len, int ctx_hi, int gs, int gq, bf16* dst,
+                        hipStream_t s) {
   const long n4 = (long)k * B * T * H * d / 4;
   if (n4 <= 0) return;
   hipLaunchKernelGGL(grad_gather_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s,
-                     src, k, B, H, T, S_cap, d, ctx_len, ctx_hi, dst);
+                     src, k, B, H, T, S_cap, d, ctx_len, ctx_hi, gs, gq, dst);
 }
 
 // part[c][o] = sum over rows r in chunk c of x[r][o] (x [rows][n]); chunks = gridDim.y.

@@ -168,7 +168,8 @@ void launch_grad_norm_apply(const bf16* x, const bf16* g, const float* rinv, lon
 struct HeadArgs {
   const float* src;       // rotated output's gradient, rows of d at (z sZ + b sB + h sH + slot)
   long sZ, sB, sH;
-  int slot_ctx;           // slot = ctx_len[b] + i (cache layout) or i
+  int slot_ctx;           // slot = ctx_len[b] + gq + gs i (cache layout) or i
+  int gs, gq;
   const int32_t* ctx_len;
   int ctx_hi;
   const float* y;         // pre-norm values [Z][B T][H d]
@@ -199,7 +200,8 @@ void launch_grad_sum(float* part, int outer, int chunks, long n, float* out, flo
                      int accumulate, hipStream_t s);
 void launch_grad_colsum(const float* x, long rows, int n, int chunks, float* part, hipStream_t s);
 void launch_grad_gather(const float* src, int k, int B, int H, int T, int S_cap, int d,
-                        const int32_t* ctx_len, int ctx_hi, bf16* dst, hipStream_t s);
+                        const int32_t* ctx_len, int ctx_hi, int gs, int gq, bf16* dst,
+                        hipStream_t s);
 struct MixGradArgs {
   const bf16* H;           // [N][L][D] states
   const bf16* g;           // [L][D] the branch's pre-mix gains

@@ -265,8 +265,9 @@ def test_new_entry_points_reject_bad_arguments_before_launch(wm):
 
 
 def test_attention_backward_rejects_unsupported_calls_before_launch(wm):
-    """The attention gradients cover bf16 full-sequence calls at head dims 64 and 96 with
-    contiguous tokens; everything else is refused on the host with its own code."""
+    """The attention gradients cover bf16 full-sequence calls at head dims 64 and 96, over
+    contiguous tokens or one strided group; everything else is refused on the host with its
+    own code."""
     cmap = [0, 1, 0, 1]
     args = (None, None, cmap, None, None, None, None, None, None, None, None, None, None)
 
@@ -278,7 +279,7 @@ def test_attention_backward_rejects_unsupported_calls_before_launch(wm):
     assert call(d=64, dtype=wm.F32) == wm.ERR_DTYPE
     assert call(d=32) == wm.ERR_SHAPE
     assert call(d=64, T_new=4) == wm.ERR_SHAPE
-    assert call(d=64, groups=2) == wm.ERR_ARG
+    assert call(d=64, groups=2, group=2) == wm.ERR_ARG  # group outside [0, g)
     assert call(d=64) == wm.ERR_ARG            # params NULL
     # four floats per query row of workspace
     d = _dims(wm, d=64)
@@ -287,7 +288,7 @@ def test_attention_backward_rejects_unsupported_calls_before_launch(wm):
 
 def test_step_gradients_reject_unsupported_calls_before_launch(wm):
     """The queries', pool's and step's gradients: bf16, head dims 64 and 96, contiguous
-    tokens, D <= 4608, the step's only with T_new > 4; NULL parameters or gradient pointers
+    tokens or one strided group, D <= 4608, the step's only with T_new > 4; NULL parameters or gradient pointers
     are refused on the host."""
     def code(fn, *args, **kw):
         with pytest.raises(wm.WMError) as e:
@@ -301,7 +302,7 @@ def test_step_gradients_reject_unsupported_calls_before_launch(wm):
                      (wm.layer_step_backward, s)):
         assert code(fn, *args, d=64, dtype=wm.F32) == wm.ERR_DTYPE
         assert code(fn, *args, d=32) == wm.ERR_SHAPE
-        assert code(fn, *args, d=64, groups=2) == wm.ERR_ARG
+        assert code(fn, *args, d=64, groups=2, group=2) == wm.ERR_ARG
         assert code(fn, *args, d=64) == wm.ERR_ARG  # params NULL
     assert code(wm.layer_step_backward, *s, d=64, T_new=4) == wm.ERR_SHAPE
     # the workspace grows with the tokens and holds at least the recomputed queries

@@ -158,3 +158,45 @@ def test_channel_attend_backward_at_full_size(wm, name):
         vd += g["dVd"][0, 0]
     check_close(dKd[1, 0], kd, "bf16", "%s dKd" % name)
     check_close(dVd[1, 0], vd, "bf16", "%s dVd" % name)
+
+
+@pytest.mark.parametrize("mask_mode", [0, 1])
+@pytest.mark.parametrize("d,Hq,Hkv", [(64, 4, 2), (96, 6, 3)])
+def test_channel_attend_backward_strided_group(wm, mask_mode, d, Hq, Hkv):
+    """Queries of the strided token group q = 2 of g = 3 (positions ctx + 2 + 3 i, Section
+    3.3) over a cache whose every slot is given."""
+    g, q, T_new, ctx = 3, 2, 90, 40
+    w = synth.small("bwd_grp_d%d" % d, B=2, T_new=T_new, L=5, k=3, D=64, Hq=Hq, Hkv=Hkv, d=d,
+                    ctx=ctx + q + g * (T_new - 1) + 1, dtype="bf16", chan_map=[2, 0, 2, 1, 0])
+    print("attention backward strided group d%d mask%d" % (d, mask_mode), flush=True)
+    P = synth.make_params(w, _bias(w))
+    Q = synth.make_queries(w)
+    Kc, Vc = synth.make_cache_cpu(w)  # every slot below the span holds values
+    ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+    od = _odims(w, mask_mode=mask_mode)
+    O = ob.attend(od, ob._t(P["Kd"]), ob._t(P["Vd"]), ob._t(Q), w.chan_map,
+                  torch.as_tensor(ctx_len.numpy(), dtype=torch.long), ob._t(Kc), ob._t(Vc),
+                  (g, q)).detach().numpy()
+    dO = synth._normal(O.shape, 1.0, 4343, torch.bfloat16)
+    ref = ob.channel_attend_grads(od, P, Q, w.chan_map, ctx_len.numpy(), _f64(Kc), _f64(Vc),
+                                  _f64(dO), grp=(g, q))
+    dev = "cuda"
+    f32 = dict(dtype=torch.float32, device=dev)
+    dQ = torch.empty(tuple(Q.shape), **f32)
+    dKc = torch.full(tuple(Kc.shape), float("nan"), **f32)
+    dVc = torch.full(tuple(Kc.shape), float("nan"), **f32)
+    dKd, dVd = torch.empty(tuple(P["Kd"].shape), **f32), torch.empty(tuple(P["Kd"].shape), **f32)
+    dims = _gdims(wm, w, mask_mode=mask_mode, ctx_max=ctx, groups=g, group=q)
+    wm.channel_attend_backward(dims, _dev(P), Q.cuda(), w.chan_map, ctx_len.cuda(), Kc.cuda(),
+                               Vc.cuda(), torch.from_numpy(O).to(torch.bfloat16).cuda(),
+                               dO.cuda(), dQ, dKc, dVc, dKd, dVd)
+    torch.cuda.synchronize()
+    check_close(dQ, ref["dQ"], "bf16", "dQ")
+    check_close(dKd, ref["dKd"], "bf16", "dKd")
+    check_close(dVd, ref["dVd"], "bf16", "dVd")
+    dKc_h, dVc_h = dKc.cpu().numpy(), dVc.cpu().numpy()
+    for b, c0 in enumerate(ctx_len.tolist()):
+        hi = c0 + q + g * (T_new - 1) + 1
+        check_close(dKc_h[:, b, :, :hi], ref["dKc"][:, b, :, :hi], "bf16", "dKc b%d" % b)
+        check_close(dVc_h[:, b, :, :hi], ref["dVc"][:, b, :, :hi], "bf16", "dVc b%d" % b)
+        assert np.isnan(dKc_h[:, b, :, hi:]).all() and np.isnan(dVc_h[:, b, :, hi:]).all()

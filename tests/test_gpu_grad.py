@@ -198,6 +198,52 @@ def test_layer_step_backward(wm, mask_mode, d, Hq, Hkv, T_new, ctx):
         assert not np.any(dKc_h[:, b, :, c0 + w.T_new:]) and not np.any(dVc_h[:, b, :, c0 + w.T_new:])
 
 
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_layer_step_backward_strided_group(wm, mask_mode):
+    """The step over the strided token group q = 1 of g = 4 (Section 3.3): pool, queries and
+    attention at positions ctx + 1 + 4 i, the other slots given."""
+    g, q, T_new, ctx = 4, 1, 60, 30
+    span = q + g * (T_new - 1) + 1
+    w = synth.small("sbg", B=2, T_new=T_new, L=5, k=3, D=128, Hq=4, Hkv=2, d=64,
+                    ctx=ctx + span, dtype="bf16", chan_map=[2, 0, 2, 1, 0])
+    print("step backward strided group mask%d" % mask_mode, flush=True)
+    P = synth.make_params(w, _bias(w), gains="random")
+    H = synth.make_states(w)
+    ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+    Kc, Vc = synth.make_cache_cpu(w)
+    dO = synth._normal((w.L, w.B, w.T_new, w.Hq * w.d), 1.0, 711, torch.bfloat16)
+    od = _odims(w, mask_mode=mask_mode)
+    ref = ob.layer_step_grads(od, P, H, w.chan_map, _f64(dO), ctx_len.numpy(), _f64(Kc),
+                              _f64(Vc), grp=(g, q))
+    dims = _gdims(wm, w, ctx_max=ctx, mask_mode=mask_mode, groups=g, group=q)
+    Pd, Hd, cl = _dev(P), H.cuda(), ctx_len.cuda()
+    Kd_, Vd_ = Kc.cuda(), Vc.cuda()
+    O = torch.empty((w.L, w.B, w.T_new, w.Hq * w.d), dtype=torch.bfloat16, device="cuda")
+    wm.layer_step(dims, Pd, Hd, w.chan_map, cl, Kd_, Vd_, O)
+    dKc = torch.zeros(tuple(Kc.shape), **F32)
+    dVc = torch.zeros(tuple(Kc.shape), **F32)
+    names = list(ob.POOL_PARAMS) + list(ob.QUERY_PARAMS) + (["Kd", "Vd"] if mask_mode == 0
+                                                            else [])
+    dH = torch.zeros(tuple(H.shape), **F32)
+    gz = {n: torch.zeros(tuple(P[n].shape), **F32) for n in names}
+    wm.layer_step_backward(dims, Pd, Hd, w.chan_map, cl, Kd_, Vd_, O, dO.cuda(), dKc, dVc, dH, gz)
+    torch.cuda.synchronize()
+    check_close(dH.cpu(), ref["dH"], "bf16", "dH", slack=_chain_slack(ref["dH"]))
+    for n in names:
+        check_close(gz[n].cpu(), ref["d" + n], "bf16", "strided d%s" % n,
+                    slack=_chain_slack(ref["d" + n]))
+    # the slots the step reads but does not write carry the attention's gradient
+    dKc_h = dKc.cpu().numpy()
+    mine = np.zeros(w.S_cap, dtype=bool)
+    for b, c0 in enumerate(ctx_len.tolist()):
+        mine[:] = False
+        mine[c0 + q + g * np.arange(T_new)] = True
+        other = ~mine
+        other[c0 + span:] = False
+        check_close(dKc_h[:, b][:, :, other], ref["dKc_ctx"][:, b][:, :, other], "bf16",
+                    "dKc others b%d" % b)
+
+
 # ------------------------------------------------ passes with truncated backprop
 
 PASS_CASES = [

@@ -398,3 +398,52 @@ def test_bf16_storage_rounds_values_and_passes_gradients():
     for n in ("dX", "dW_o", "dWq", "dW_alpha"):
         rel = np.abs(a[n] - b[n]).max() / np.abs(a[n]).max()
         assert 1e-6 < rel < 0.1, (n, rel)
+
+
+@pytest.mark.parametrize("mask_mode", [0, 1])
+def test_strided_group_step_gradients_match_finite_differences(mask_mode):
+    """A step over the strided token group q = 1 of g = 3 (positions 1, 4, 7, ...) with every
+    other slot given: every gradient against central differences of the C oracle's pool and
+    channel attention at those positions (the C oracle's pool with a token list, its
+    attention over the spliced cache)."""
+    dm = _dims(T_new=4, mask_mode=mask_mode, L=3, k=2)
+    g, q = 3, 1
+    dm.S_cap = q + g * (dm.T_new - 1) + 1
+    P = _params(dm, seed=31)
+    rng = np.random.default_rng(32)
+    H = rng.standard_normal((dm.B, dm.T_new, dm.L, dm.D))
+    cmap = [1, 0, 1]
+    Kc = rng.standard_normal((dm.k, dm.B, dm.Hkv, dm.S_cap, dm.d))
+    Vc = rng.standard_normal((dm.k, dm.B, dm.Hkv, dm.S_cap, dm.d))
+    dO = rng.standard_normal((dm.L, dm.B, dm.T_new, dm.Hq * dm.d))
+    gr = ob.layer_step_grads(dm, P, H, cmap, dO, None, Kc, Vc, grp=(g, q))
+    # the C oracle at the group's positions: a full-length problem whose other tokens' H
+    # are ignored (their rows come from Kc, Vc)
+    full = _dims(T_new=dm.S_cap, mask_mode=mask_mode, L=3, k=2)
+    full.S_cap = dm.S_cap
+    pos = [q + g * i for i in range(dm.T_new)]
+
+    def loss(Hx, Px, Kx=Kc, Vx=Vc):
+        Hf = np.zeros((dm.B, full.T_new, dm.L, dm.D))
+        Hf[:, pos] = Hx
+        K, V = Kx.copy(), Vx.copy()
+        oracle.pool(full, Px, Hf, None, K, V, toks=[b * full.T_new + p for b in range(dm.B)
+                                                    for p in pos])
+        Qf = oracle.q_project(full, Px, Hf)
+        O = oracle.channel_attend(full, Px, Qf, cmap, None, K, V)
+        return (O[:, :, pos] * dO).sum()
+
+    gslots = np.zeros(dm.S_cap, dtype=bool)
+    gslots[pos] = True
+    checks = [("dH", lambda x: loss(x, P), H)]
+    for n in oracle.PARAM_NAMES:
+        checks.append(("d" + n, lambda x, n=n: loss(H, {**P, n: x}), P[n]))
+    checks.append(("dKc_ctx", lambda x: loss(H, P, x, Vc), Kc))
+    checks.append(("dVc_ctx", lambda x: loss(H, P, Kc, x), Vc))
+    for name, f, x in checks:
+        v = rng.standard_normal(x.shape)
+        if name in ("dKc_ctx", "dVc_ctx"):
+            v[..., gslots, :] = 0.0  # the group's own slots are overwritten by the step
+        num = _fd(f, x, v)
+        ana = (gr[name] * v).sum()
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(num)), (name, num, ana)
