@@ -575,8 +575,9 @@ def passes_bench(wm, torch, np, synth, hip, dev, stream, log, groups=("8", "16",
     D512, 6 query / 3 KV heads of 96, p = 2, bf16) with the stand-in decoder block:
     cyclic Gauss-Seidel with the paper's g = 8 groups and with g = 16, Jacobi (g = 1), 3
     passes each, and one pass of g = T (exact left-to-right evaluation), event-timed; then
-    (train) a training step's passes: 3 Jacobi passes with gradients through the last 1 or
-    2 (wm_prefill_passes_backward)."""
+    (train) a training step's passes (wm_prefill_passes_backward): the paper's 3 passes of
+    g = 8 with gradients through the last 2 or 1, and 3 Jacobi passes with gradients
+    through the last 2."""
     w0 = synth.WORKLOADS["paper_T2048_L16_k8"]
     w = synth.Workload("paper_passes", w0.B, w0.T_new, w0.L, w0.k, w0.D, w0.Hq, w0.Hkv, w0.d, 0,
                        w0.dtype, list(w0.chan_map), w0.p, w0.seed)
@@ -615,17 +616,17 @@ def passes_bench(wm, torch, np, synth, hip, dev, stream, log, groups=("8", "16",
         log("bench: passes g=%d x %d: %.3f ms (%.3f ms per pass, %.0f tokens/s)"
             % (g, passes, ms, ms / passes, w.B * w.T_new / (ms * 1e-3)))
         del ws
-    # a training step's passes: 3 Jacobi passes, then backpropagation truncated to the last
-    # n_g of them (wm_prefill_passes_backward: the forward and the backward in one call)
+    # a training step's passes: 3 passes, then backpropagation truncated to the last n_g
+    # of them (wm_prefill_passes_backward: the forward and the backward in one call)
     if train:
-        dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p, S_cap=w.T_new,
-                            ctx_max=0, dtype=wm.BF16)
         f32 = dict(dtype=torch.float32, device=dev)
         dh = synth._normal((w.B, w.T_new, w.D), 1.0, 9301, torch.float32).to(dev)
         dX = torch.zeros((w.B, w.T_new, w.D), **f32)
         dW = torch.zeros(tuple(W_o.shape), **f32)
         grads = {n: torch.zeros(tuple(P.tensors[n].shape), **f32) for n in wm.PARAM_NAMES}
-        for n_grad in (1, 2):
+        for g, n_grad in ((8, 2), (8, 1), (1, 2)):
+            dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p,
+                                S_cap=w.T_new, ctx_max=0, dtype=wm.BF16, groups=g)
             ws = torch.empty(wm.passes_backward_workspace(dims, n_grad), dtype=torch.uint8,
                              device=dev)
             run = lambda: wm.prefill_passes_backward(  # noqa: E731
@@ -643,12 +644,12 @@ def passes_bench(wm, torch, np, synth, hip, dev, stream, log, groups=("8", "16",
             ms = float(np.median([hip.elapsed_ms(ev[r], ev[r + 1]) for r in range(reps)]))
             for e in ev:
                 hip.destroy(e)
-            out["train_g1_x3_ng%d" % n_grad] = {
-                "passes": 3, "n_grad": n_grad, "ms": round(ms, 3),
+            out["train_g%d_x3_ng%d" % (g, n_grad)] = {
+                "passes": 3, "groups": g, "n_grad": n_grad, "ms": round(ms, 3),
                 "workspace_gb": round(ws.numel() / 1e9, 2),
                 "tokens_per_s": round(w.B * w.T_new / (ms * 1e-3), 1)}
-            log("bench: training passes (3 Jacobi, gradients through the last %d): %.3f ms"
-                % (n_grad, ms))
+            log("bench: training passes (3 of g=%d, gradients through the last %d): %.3f ms"
+                % (g, n_grad, ms))
             del ws
             torch.cuda.empty_cache()
     return out

@@ -408,19 +408,22 @@ int wm_prefill_passes(const wm_dims *dims, const wm_params *params, const void *
                       void *Vc, void *H, void *h_top, void *ws, size_t ws_bytes,
                       wm_stream_t stream);
 
-/* A training step's passes with truncated backpropagation (Section 3.3): the Jacobi
- * passes of wm_prefill_passes (dims->groups <= 1), then the gradients of the loss through
- * the last n_grad of them only. Pass t pools H^(t-1) into the caches and recomputes
- * H^(t) = States(X; caches) with the stand-in block h_{l+1} = h_l + W_o[l] o_l; the
- * states entering pass passes - n_grad + 1 are held fixed (no gradient flows into them or
- * the passes before), except with n_grad = passes, where they are H^(0) = X in every layer
- * and their gradient goes to X. Each window pass is differentiated whole: its pool (the
- * router, mix, projections and norms that wrote the caches), then every layer from the
- * top down (the block's W_o, the consumer's attention over its channel with the dummy,
- * its query), the residual stream carrying the gradient down to X. The window's states,
- * caches and per-layer attention outputs are kept in the workspace; the queries are
- * recomputed.
- * bf16, head dims 64 and 96, T_new = T > 4, D <= 4608, every mask, mix and router mode.
+/* A training step's passes with truncated backpropagation (Section 3.3): the passes of
+ * wm_prefill_passes over g = dims->groups strided groups (g = 1: Jacobi iteration), then
+ * the gradients of the loss through the last n_grad of them only. The cache starts as
+ * Pool(H^(0)) with H^(0) = X in every layer; in each pass group q recomputes the states of
+ * its positions from X and the cache as it stands (the stand-in block
+ * h_{l+1} = h_l + W_o[l] o_l), then pools them into its slots. The cache entering pass
+ * passes - n_grad + 1 is held fixed (no gradient flows into it or the passes before),
+ * except with n_grad = passes, where the initial pool's gradient goes to X. Each window
+ * step (one group of one pass) is differentiated whole: its pool (the router, mix,
+ * projections and norms that wrote its slots), then every layer from the top down (the
+ * block's W_o, the consumer's attention over its channel with the dummy, its query), the
+ * residual stream carrying the gradient down to X. The window's group states, per-layer
+ * attention outputs and the cache slots each step overwrote are kept in the workspace; the
+ * queries are recomputed.
+ * bf16, head dims 64 and 96, T_new = T with T / g > 4, D <= 4608, every mask, mix and
+ * router mode.
  *   dims, params, W_o, X, chan_map, passes  as wm_prefill_passes
  *   n_grad   1 <= n_grad <= passes: the passes that carry gradients
  *   dh_top   device float [B][T][D]: the loss gradient in the state leaving the top layer
@@ -431,8 +434,9 @@ int wm_prefill_passes(const wm_dims *dims, const wm_params *params, const void *
  *   grads    every entry (Kd, Vd only with WM_MASK_PAPER; W_alpha not with static
  *            weights): ADDED
  * Workspace: wm_passes_backward_workspace(dims, n_grad) bytes, 256-byte aligned (it grows
- * with n_grad: three state-sized arrays per window pass). Errors as wm_prefill_passes and
- * wm_layer_step_backward; WM_ERR_ARG for n_grad outside [1, passes] or groups > 1. */
+ * with n_grad: per window pass the states, the attention outputs and two caches' worth of
+ * the T written slots). Errors as wm_prefill_passes and wm_layer_step_backward;
+ * WM_ERR_SHAPE for T / g <= 4, WM_ERR_ARG for n_grad outside [1, passes]. */
 int wm_prefill_passes_backward(const wm_dims *dims, const wm_params *params, const void *W_o,
                                const void *X, const int32_t *chan_map, int32_t passes,
                                int32_t n_grad, const float *dh_top, void *h_top, float *dX,

@@ -344,7 +344,8 @@ def passes_backward_workspace(dims: Dims, n_grad: int) -> int:
 
 def prefill_passes_backward(dims: Dims, params, W_o, X, chan_map, passes: int, n_grad: int,
                             dh_top, dX, dW_o, grads, h_top=None, ws=None, stream=None):
-    """Jacobi passes, then the gradients of <dh_top, h_top> through the last n_grad passes:
+    """The passes over dims.groups strided groups (1: Jacobi), then the gradients of
+    <dh_top, h_top> through the last n_grad passes:
     added into dX, dW_o and grads (float32 tensors); h_top (bf16, optional) receives the
     forward's top state."""
     if ws is None and getattr(X, "device", None) is not None:

@@ -181,9 +181,11 @@ Layout grad_layout(const wm_dims& d, int op) {
 
 // Workspace regions for an op (offsets in bytes, each 256-byte aligned).
 struct PassBwdLayout {
-  size_t fw = 0, hs = 0, kp = 0, op = 0, gcur = 0, gb = 0, dof = 0, dob = 0, dql = 0, h1 = 0,
-         rows = 0, gkd = 0, dpk = 0, dpv = 0, dhn = 0, split = 0, sub = 0, total = 0;
-  size_t state = 0, cache = 0, outs = 0;  // bytes of one state array, cache, output set
+  size_t fw = 0, kv = 0, hs = 0, undo = 0, op = 0, gcur = 0, gb = 0, dof = 0, dob = 0, dql = 0,
+         h1 = 0, rows = 0, gkd = 0, dpk = 0, dpv = 0, dhn = 0, split = 0, sub = 0, total = 0;
+  // bytes of one cache, and per window step: one group's states, its slots of one cache,
+  // its layers' attention outputs
+  size_t cache = 0, state = 0, slots = 0, outs = 0;
 };
 
 PassBwdLayout passes_bwd_layout(const wm_dims& d, int n_grad);
@@ -320,8 +322,6 @@ int validate_dims(const wm_dims* dp, int op, const int32_t* chan_map) {
     for (double v : views)
       if (v >= lim) return fail(WM_ERR_SHAPE, "an operand spans more than 2 GiB (%.0f B)", v);
   }
-  if (op == WM_OP_PASSES_BACKWARD && group_stride(d) > 1)
-    return fail(WM_ERR_ARG, "the pass gradients run Jacobi passes: groups must be <= 1");
   if (pass_op) {
     if (d.group != 0) return fail(WM_ERR_ARG, "the pass driver runs every group: group must be 0");
     if (d.T_new % group_stride(d) != 0)
@@ -855,10 +855,13 @@ wm_dims one_consumer(const wm_dims& d) {
 
 PassBwdLayout passes_bwd_layout(const wm_dims& d, int n_grad) {
   PassBwdLayout Ly;
-  const size_t N = (size_t)d.B * d.T_new, L = d.L, D = d.D, HQ = (size_t)d.Hq * d.d;
-  Ly.state = N * L * D * 2;
+  const int g = group_stride(d);
+  const size_t Ng = (size_t)d.B * (d.T_new / g), L = d.L, D = d.D, HQ = (size_t)d.Hq * d.d;
+  const size_t steps = (size_t)n_grad * g;
   Ly.cache = (size_t)d.k * d.B * d.Hkv * d.S_cap * d.d * 2;
-  Ly.outs = L * N * HQ * 2;
+  Ly.state = al256(Ng * L * D * 2);
+  Ly.slots = al256((size_t)d.k * d.B * d.Hkv * (d.T_new / g) * d.d * 2);
+  Ly.outs = al256(L * Ng * HQ * 2);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t at = off;
@@ -866,37 +869,44 @@ PassBwdLayout passes_bwd_layout(const wm_dims& d, int n_grad) {
     return at;
   };
   Ly.fw = take(layout(d, WM_OP_PASSES).total);
-  Ly.hs = take(al256(Ly.state) * (n_grad + 1));
-  Ly.kp = take(al256(Ly.cache) * 2 * n_grad);
-  Ly.op = take(al256(Ly.outs) * n_grad);
-  Ly.gcur = take(N * D * 4);
-  Ly.gb = take(N * D * 2);
-  Ly.dof = take(N * HQ * 4);
-  Ly.dob = take(N * HQ * 2);
-  Ly.dql = take(N * HQ * 4);
-  Ly.h1 = take(N * D * 2);
-  Ly.rows = take(wm::attend_backward_rows_bytes(make_shape(one_consumer(d))));
+  Ly.kv = take(al256(Ly.cache) * 2);
+  Ly.hs = take(Ly.state * steps);
+  Ly.undo = take(Ly.slots * 2 * steps);
+  Ly.op = take(Ly.outs * steps);
+  Ly.gcur = take(Ng * D * 4);
+  Ly.gb = take(Ng * D * 2);
+  Ly.dof = take(Ng * HQ * 4);
+  Ly.dob = take(Ng * HQ * 2);
+  Ly.dql = take(Ng * HQ * 4);
+  Ly.h1 = take(Ng * D * 2);
+  Ly.rows = take(wm::attend_backward_rows_bytes(make_shape(one_consumer(group_dims(d, 0)))));
   Ly.gkd = take(2 * (size_t)d.Hkv * d.d * 4);
   Ly.dpk = take(Ly.cache * 2);
   Ly.dpv = take(Ly.cache * 2);
-  Ly.dhn = take(N * L * D * 4);
+  Ly.dhn = take(Ng * L * D * 4);
   Ly.split = take(kSplitElems * 4);
-  wm_dims dq = d;
+  wm_dims dq = group_dims(d, 0);
   dq.L = 1;
-  Ly.sub = take(std::max(layout(dq, WM_OP_Q_BACKWARD).total, layout(d, WM_OP_POOL_BACKWARD).total));
-  Ly.total = N == 0 ? 0 : off;
+  Ly.sub = take(std::max(layout(dq, WM_OP_Q_BACKWARD).total,
+                         layout(group_dims(d, 0), WM_OP_POOL_BACKWARD).total));
+  Ly.total = Ng == 0 ? 0 : off;
   return Ly;
 }
 
-// Jacobi passes (groups <= 1) as the fixed point's iteration: H^(0) = X in every layer; pass
-// t pools H^(t-1) into the caches, then recomputes H^(t) = States(X; caches) layer by
-// layer. The passes before the gradient window run in scratch; the window's passes keep
-// their input states, caches and per-layer outputs. Then the backward, pass by pass from
-// the last: the stand-in blocks and the consumers' attention and queries layer by layer
-// from the top (the residual stream's gradient in gcur), then the pool of the pass's
-// caches into the gradient of the states it read, which the pass before receives; the
-// states entering the window are held fixed (their gradient is dropped) unless the window
-// starts at H^(0), whose gradient goes to X.
+// The passes of Section 3.3 over g strided groups (g = 1: Jacobi iteration), as
+// wm_prefill_passes runs them: the cache starts as Pool(H^(0) = X in every layer); each
+// pass runs the groups in order, group q recomputing the states of its positions layer by
+// layer from the cache as it stands, then pooling them into its slots. The passes before
+// the gradient window run in scratch; each window step (pass t, group q) keeps its group's
+// states, its layers' attention outputs and the slots its pool overwrote.
+// The backward walks the window's steps from the last. It holds the loss gradient in the
+// whole cache (dK, dV) as the forward left it at that point: the step's pool sends the
+// gradient at its slots to its states, and those slots are then given back the values the
+// step read (their gradient cleared); its layers from the top down (the stand-in blocks,
+// the consumers' attention over the restored cache, whose gradient joins dK, dV, and
+// their queries) carry the residual stream's gradient down to X. The cache entering the
+// window is held fixed unless the window starts at the initial pool, whose gradient goes
+// to X through every layer.
 void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, const bf16* X,
                          const int32_t* chan_map, int passes, int n_grad, const float* dh_top,
                          bf16* h_top, float* dX, float* dW_o, const wm_grads& G, void* ws,
@@ -904,39 +914,63 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
   const PassBwdLayout Ly = passes_bwd_layout(d, n_grad);
   const Layout Lf = layout(d, WM_OP_PASSES);
   void* fw = at(ws, Ly.fw);
-  const wm::Shape sh = make_shape(d);
-  const int L = d.L, D = d.D, HQ = d.Hq * d.d, N = sh.N();
+  const int g = group_stride(d), Tg = d.T_new / g, L = d.L, D = d.D, HQ = d.Hq * d.d;
+  const int Ng = d.B * Tg;
+  const long gsz = (long)Ng * L * D;                        // one group's states
   const long cslice = (long)d.B * d.Hkv * d.S_cap * d.d;  // one channel of a cache
-  auto Hs = [&](int i) { return (bf16*)at(ws, Ly.hs + al256(Ly.state) * i); };
-  auto Kp = [&](int i) { return (bf16*)at(ws, Ly.kp + al256(Ly.cache) * (2 * (i - 1))); };
-  auto Vp = [&](int i) { return (bf16*)at(ws, Ly.kp + al256(Ly.cache) * (2 * (i - 1) + 1)); };
-  auto Os = [&](int i) { return (bf16*)at(ws, Ly.op + al256(Ly.outs) * (i - 1)); };
-  bf16* top = h_top ? h_top : (bf16*)at(fw, Lf.topg);
-  wm::launch_router_fold<bf16>(sh, router_layers(d), (const bf16*)P.g_pre, (const bf16*)P.W_alpha,
-                               (bf16*)at(fw, Lf.wa), s);
-  wm::launch_kv_fold<bf16>(sh, (const bf16*)P.g_mid, (const bf16*)P.Wk, (const bf16*)P.Wv,
+  const long cache_elems = (long)d.k * cslice;
+  const long crows = (long)d.k * d.B * d.Hkv;              // cache rows of S_cap slots
+  const int first = passes - n_grad;                       // passes before the window
+  bf16* K = (bf16*)at(ws, Ly.kv);
+  bf16* V = (bf16*)at(ws, Ly.kv + al256(Ly.cache));
+  bf16* Hg = (bf16*)at(fw, Lf.hg);
+  bf16* topg = (bf16*)at(fw, Lf.topg);
+  float* tab = (float*)at(fw, Lf.tab);
+  // window step j = (t - first - 1) g + q
+  auto Hs = [&](int j) { return (bf16*)at(ws, Ly.hs + Ly.state * j); };
+  auto Uk = [&](int j) { return (bf16*)at(ws, Ly.undo + Ly.slots * (2 * j)); };
+  auto Uv = [&](int j) { return (bf16*)at(ws, Ly.undo + Ly.slots * (2 * j + 1)); };
+  auto Os = [&](int j) { return (bf16*)at(ws, Ly.op + Ly.outs * j); };
+  const wm::Shape sh0 = make_shape(group_dims(d, 0));
+  wm::launch_router_fold<bf16>(sh0, router_layers(d), (const bf16*)P.g_pre,
+                               (const bf16*)P.W_alpha, (bf16*)at(fw, Lf.wa), s);
+  wm::launch_kv_fold<bf16>(sh0, (const bf16*)P.g_mid, (const bf16*)P.Wk, (const bf16*)P.Wv,
                            (bf16*)at(fw, Lf.wkv), s);
-  wm::launch_q_fold<bf16>(sh, (const bf16*)P.g_in, (const bf16*)P.Wq, (bf16*)at(fw, Lf.wq), 0, L,
-                          s);
-  wm::launch_rope_table(sh, nullptr, (float*)at(fw, Lf.tab), s);
-  // one pass: pool H_in into (K, V), then the states into H_out (layer 0 = X) and top,
-  // the layers' attention outputs into O (layer l at l N HQ) or scratch
-  auto pass = [&](const bf16* H_in, bf16* K, bf16* V, bf16* H_out, bf16* O) {
-    run_pool<bf16>(d, P, H_in, nullptr, K, V, Lf, fw, s, false, true, true);
-    if (H_out != H_in) wm::launch_group_gather<bf16>(X, H_out, d.B, d.T_new, 1, L, D, s);
+  wm::launch_q_fold<bf16>(sh0, (const bf16*)P.g_in, (const bf16*)P.Wq, (bf16*)at(fw, Lf.wq), 0,
+                          L, s);
+  // H^(0) = X in every layer, group by group; the initial pool
+  wm::launch_group_gather<bf16>(X, Hg, d.B, d.T_new, g, L, D, s);
+  for (int q = 0; q < g; ++q)
+    run_pool<bf16>(group_dims(d, q), P, Hg + q * gsz, nullptr, K, V, Lf, fw, s, false, false,
+                   true);
+  // one step: group q's states in Hq (layer 0 holds X) from the cache, its layers' outputs
+  // into O (layer l at l Ng HQ) or scratch, the slots it overwrites into (uk, uv) if given,
+  // then its pool
+  auto step = [&](int q, bf16* Hq, bf16* O, bf16* uk, bf16* uv) {
+    const wm_dims dq = group_dims(d, q);
+    wm::launch_rope_table(make_shape(dq), nullptr, tab, s);
     for (int l = 0; l < L; ++l) {
-      bf16* Ol = O ? O + (long)l * N * HQ : (bf16*)at(fw, Lf.ol);
-      run_layer_attend<bf16>(d, P, l, H_out, chan_map, nullptr, K, V, Ol, Lf, fw, s, true, true);
+      bf16* Ol = O ? O + (long)l * Ng * HQ : (bf16*)at(fw, Lf.ol);
+      run_layer_attend<bf16>(dq, P, l, Hq, chan_map, nullptr, K, V, Ol, Lf, fw, s, true, true);
       const bool last = l + 1 == L;
-      wm::launch_block_residual<bf16>(N, D, HQ, Ol, W_o + (long)l * D * HQ, H_out + (long)l * D,
-                                      (long)L * D, last ? top : H_out + (long)(l + 1) * D,
+      wm::launch_block_residual<bf16>(Ng, D, HQ, Ol, W_o + (long)l * D * HQ, Hq + (long)l * D,
+                                      (long)L * D,
+                                      last ? topg + (long)q * Ng * D : Hq + (long)(l + 1) * D,
                                       last ? D : (long)L * D, s);
     }
+    if (uk) wm::launch_grad_slots(K, V, uk, uv, nullptr, nullptr, crows, Tg, g, q, d.S_cap, d.d,
+                                  false, s);
+    run_pool<bf16>(dq, P, Hq, nullptr, K, V, Lf, fw, s, true, true, true);
   };
-  // H^(0), then the passes before the window (in place in Hs(0), caches in slot 1)
-  wm::launch_group_gather<bf16>(X, Hs(0), d.B, d.T_new, 1, L, D, s);
-  for (int t = 1; t <= passes - n_grad; ++t) pass(Hs(0), Kp(1), Vp(1), Hs(0), nullptr);
-  for (int i = 1; i <= n_grad; ++i) pass(Hs(i - 1), Kp(i), Vp(i), Hs(i), Os(i));
+  for (int t = 1; t <= first; ++t)
+    for (int q = 0; q < g; ++q) step(q, Hg + q * gsz, nullptr, nullptr, nullptr);
+  for (int j = 0; j < n_grad * g; ++j) {
+    const int q = j % g;
+    (void)hipMemcpyAsync(Hs(j), Hg + q * gsz, (size_t)gsz * sizeof(bf16), hipMemcpyDeviceToDevice,
+                         s);
+    step(q, Hs(j), Os(j), Uk(j), Uv(j));
+  }
+  if (h_top) wm::launch_group_scatter<bf16>(topg, h_top, d.B, d.T_new, g, D, s);
 
   // backward
   float* gcur = (float*)at(ws, Ly.gcur);
@@ -950,53 +984,58 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
   float* dhn = (float*)at(ws, Ly.dhn);
   float* gkd = (float*)at(ws, Ly.gkd);
   void* sub = at(ws, Ly.sub);
-  const wm_dims d1 = one_consumer(d);
-  const wm::Shape sh1 = make_shape(d1);
   wm::LayerTable m0{};
   wm::ChannelGroups cg0{};
   cg0.offsets[1] = 1;
-  wm_dims dq = d;
-  dq.L = 1;
-  const Layout Lq = layout(dq, WM_OP_Q_BACKWARD), Lp = layout(d, WM_OP_POOL_BACKWARD);
+  const Layout Lp = layout(group_dims(d, 0), WM_OP_POOL_BACKWARD);
+  wm_dims dq1 = group_dims(d, 0);
+  dq1.L = 1;
+  const Layout Lq = layout(dq1, WM_OP_Q_BACKWARD);
   const bool paper = d.mask_mode == WM_MASK_PAPER;
-  const long cache_elems = (long)d.k * cslice;
-  bool have_dhn = false;
-  for (int i = n_grad; i >= 1; --i) {
-    const bf16* H = Hs(i);
-    const bf16* O = Os(i);
-    if (i == n_grad) {
-      wm::launch_grad_fill(gcur, (long)N * D, 0.f, s);
-      wm::launch_grad_add_rows(gcur, dh_top, N, D, D, 1, s);
-    } else {
-      wm::launch_grad_fill(gcur, (long)N * D, 0.f, s);
-    }
-    wm::launch_grad_fill(dpk, cache_elems, 0.f, s);
-    wm::launch_grad_fill(dpv, cache_elems, 0.f, s);
+  bf16* Ql = (bf16*)at(fw, Lf.q);
+  float* rinv = (float*)at(fw, Lf.rinv);
+  wm::launch_grad_fill(dpk, cache_elems, 0.f, s);
+  wm::launch_grad_fill(dpv, cache_elems, 0.f, s);
+  for (int j = n_grad * g - 1; j >= 0; --j) {
+    const int q = j % g;
+    const bool last_pass = j >= (n_grad - 1) * g;
+    const wm_dims dq = group_dims(d, q);
+    const wm::Shape shq = make_shape(dq), sh1 = make_shape(one_consumer(dq));
+    const bf16* H = Hs(j);
+    const bf16* O = Os(j);
+    // the step's pool: the gradient at its slots goes to its states (dhn); the slots then
+    // hold what the step read, their gradient cleared
+    wm::launch_grad_fill(dhn, gsz, 0.f, s);
+    run_pool_backward(dq, P, H, nullptr, dpk, dpv, dhn, G, Lp, sub, s);
+    wm::launch_grad_slots(K, V, Uk(j), Uv(j), dpk, dpv, crows, Tg, g, q, d.S_cap, d.d, true, s);
+    // gcur: the gradient in h_{l+1}, from the loss at the top of the last pass
+    wm::launch_grad_fill(gcur, (long)Ng * D, 0.f, s);
+    if (last_pass) wm::launch_grad_add_rows(gcur, D, dh_top + (long)q * D, Ng, D, (long)g * D, 1, s);
+    wm::launch_rope_table(shq, nullptr, tab, s);
     for (int l = L - 1; l >= 0; --l) {
       const int c = chan_map[l];
-      const bf16* Ol = O + (long)l * N * HQ;
-      // gcur: the gradient in h_{l+1}. do_l = W_o[l]^T gcur, dW_o[l] += gcur^T o_l
-      wm::launch_grad_cast(gcur, gb, (long)N * D, s);
+      const bf16* Ol = O + (long)l * Ng * HQ;
+      // do_l = W_o[l]^T gcur, dW_o[l] += gcur^T o_l
+      wm::launch_grad_cast(gcur, gb, (long)Ng * D, s);
       gemm(opnd(gb, D, 1, 0, false), opnd(W_o + (long)l * D * HQ, 1, HQ, 0, false), dof, HQ, 1, 0,
-           N, HQ, D, 1, false, s);
-      wm::launch_grad_cast(dof, dob, (long)N * HQ, s);
+           Ng, HQ, D, 1, false, s);
+      wm::launch_grad_cast(dof, dob, (long)Ng * HQ, s);
       gemm(opnd(gb, 1, D, 0, false), opnd(Ol, 1, HQ, 0, false), dW_o + (long)l * D * HQ, HQ, 1, 0,
-           D, HQ, N, 1, true, s, 0, 0, 0, 0, (float*)at(ws, Ly.split));
+           D, HQ, Ng, 1, true, s, 0, 0, 0, 0, (float*)at(ws, Ly.split));
       // layer l's queries again, then its attention gradients on channel c alone
-      bf16* Ql = (bf16*)at(fw, Lf.q);
-      float* rinv = (float*)at(fw, Lf.rinv);
-      wm::launch_row_rms_strided<bf16>(H + (long)l * D, N, D, (long)L * D, L, sh.eps, rinv + l, s);
-      wm::launch_q_layers<bf16>(sh, H, rinv, (const bf16*)P.g_qnorm, (const float*)at(fw, Lf.tab),
-                                Ql, (const bf16*)at(fw, Lf.wq), l, 1, s);
+      wm::launch_row_rms_strided<bf16>(H + (long)l * D, Ng, D, (long)L * D, L, d.eps, rinv + l,
+                                       s);
+      wm::launch_q_layers<bf16>(shq, H, rinv, (const bf16*)P.g_qnorm, tab, Ql,
+                                (const bf16*)at(fw, Lf.wq), l, 1, s);
       const long dofs = ((long)c * d.Hkv) * d.d;
-      wm::launch_attend_backward(sh1, m0, cg0, Ql, Kp(i) + c * cslice, Vp(i) + c * cslice,
+      wm::launch_attend_backward(sh1, m0, cg0, Ql, K + c * cslice, V + c * cslice,
                                  (const bf16*)P.Kd + dofs, (const bf16*)P.Vd + dofs, Ol, dob,
                                  nullptr, dql, dpk + c * cslice, dpv + c * cslice,
                                  paper ? G.Kd + dofs : gkd,
                                  paper ? G.Vd + dofs : gkd + (long)d.Hkv * d.d,
                                  (float*)at(ws, Ly.rows), s, true);
-      // the queries' backward of layer l adds its h_l gradient into gcur
-      wm::launch_grad_copy_rows(H + (long)l * D, (long)L * D, h1, N, D, s);
+      // the queries' backward adds its h_l gradient into gcur, then the pool's
+      wm::launch_grad_copy_rows(H + (long)l * D, (long)L * D, h1, Ng, D, s);
       wm_params P1 = P;
       P1.g_in = (const bf16*)P.g_in + (long)l * D;
       P1.Wq = (const bf16*)P.Wq + (long)l * HQ * D;
@@ -1005,17 +1044,20 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
       G1.g_in = G.g_in + (long)l * D;
       G1.Wq = G.Wq + (long)l * HQ * D;
       G1.g_qnorm = G.g_qnorm + (long)l * d.d;
-      run_q_backward(dq, P1, h1, nullptr, dql, gcur, G1, Lq, sub, s);
-      // and the gradient the next pass's pool sent to h_l
-      if (have_dhn) wm::launch_grad_add_rows(gcur, dhn + (long)l * D, N, D, (long)L * D, 1, s);
+      wm_dims dl = dq;
+      dl.L = 1;
+      run_q_backward(dl, P1, h1, nullptr, dql, gcur, G1, Lq, sub, s);
+      wm::launch_grad_add_rows(gcur, D, dhn + (long)l * D, Ng, D, (long)L * D, 1, s);
     }
-    wm::launch_grad_add_rows(dX, gcur, N, D, D, 1, s);  // h_0 = X
-    // the pool that made this pass's caches from the states of the pass before
-    wm::launch_grad_fill(dhn, (long)N * L * D, 0.f, s);
-    run_pool_backward(d, P, Hs(i - 1), nullptr, dpk, dpv, dhn, G, Lp, sub, s);
-    have_dhn = i > 1;
-    if (i == 1 && n_grad == passes)  // H^(0) = X in every layer
-      wm::launch_grad_add_rows(dX, dhn, N, D, (long)L * D, L, s);
+    wm::launch_grad_add_rows(dX + (long)q * D, (long)g * D, gcur, Ng, D, D, 1, s);  // h_0 = X
+  }
+  if (n_grad == passes) {  // the initial pool read X in every layer
+    wm::launch_group_gather<bf16>(X, Hg, d.B, d.T_new, g, L, D, s);
+    for (int q = 0; q < g; ++q) {
+      wm::launch_grad_fill(dhn, gsz, 0.f, s);
+      run_pool_backward(group_dims(d, q), P, Hg + q * gsz, nullptr, dpk, dpv, dhn, G, Lp, sub, s);
+      wm::launch_grad_add_rows(dX + (long)q * D, (long)g * D, dhn, Ng, D, (long)L * D, L, s);
+    }
   }
 }
 
@@ -1548,7 +1590,8 @@ int wm_prefill_passes_backward(const wm_dims* dims, const wm_params* params, con
   if (n_grad < 1 || n_grad > passes) return fail(WM_ERR_ARG, "n_grad must be in [1, passes]");
   if ((size_t)d.B * d.T_new == 0) return WM_OK;
   WM_TRY(check_backward(d));
-  if (decode_path(d)) return fail(WM_ERR_SHAPE, "the pass gradients need T_new > 4");
+  if (decode_path(group_dims(d, 0)))
+    return fail(WM_ERR_SHAPE, "the pass gradients need T_new / groups > 4");
   WM_TRY(check_pool_grads(d, params, grads));
   WM_TRY(check_params(params, {P_GIN, P_WQ, P_GQN}));
   if (d.mask_mode == WM_MASK_PAPER) WM_TRY(check_params(params, {P_KD, P_VD}));

@@ -963,24 +963,61 @@ void launch_grad_cast(const float* src, bf16* dst, long n, hipStream_t s) {
                        dst, n);
 }
 
-// dst[r][e] += sum over l < nsrc of src[r * src_stride + l * D + e] (rows of D)
-__global__ __launch_bounds__(256) void grad_add_rows_kernel(float* dst, const float* src,
-                                                            long rows, int D, long src_stride,
-                                                            int nsrc) {
+// dst[r * dst_stride + e] += sum over l < nsrc of src[r * src_stride + l * D + e] (rows of D)
+__global__ __launch_bounds__(256) void grad_add_rows_kernel(float* dst, long dst_stride,
+                                                            const float* src, long rows, int D,
+                                                            long src_stride, int nsrc) {
   const long i = (long)blockIdx.x * 256 + threadIdx.x;
   if (i >= rows * D) return;
   const long r = i / D;
   const int e = (int)(i % D);
   float v = 0.f;
   for (int l = 0; l < nsrc; ++l) v += src[r * src_stride + (long)l * D + e];
-  dst[i] += v;
+  dst[r * dst_stride + e] += v;
 }
-void launch_grad_add_rows(float* dst, const float* src, long rows, int D, long src_stride,
-                          int nsrc, hipStream_t s) {
+void launch_grad_add_rows(float* dst, long dst_stride, const float* src, long rows, int D,
+                          long src_stride, int nsrc, hipStream_t s) {
   const long n = rows * D;
   if (n > 0)
     hipLaunchKernelGGL(grad_add_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       dst, src, rows, D, src_stride, nsrc);
+                       dst, dst_stride, src, rows, D, src_stride, nsrc);
+}
+
+// The slots q + g i (i < Tg) of every row of S_cap slots of the caches K and V, copied to
+// (restore = 0) or back from (restore = 1) compact [rows][Tg][d] arrays, 8 elements a
+// thread; on the way back the slots' fp32 gradients dK, dV are cleared when given.
+__global__ __launch_bounds__(256) void grad_slots_kernel(bf16* K, bf16* V, bf16* Kg, bf16* Vg,
+                                                         float* dK, float* dV, long rows, int Tg,
+                                                         int g, int q, int S_cap, int d,
+                                                         int restore) {
+  const int dv = d / 8;
+  const long n = (long)blockIdx.x * 256 + threadIdx.x;
+  if (n >= rows * Tg * dv) return;
+  const long ri = n / dv;  // r Tg + i
+  const int v = (int)(n - ri * dv), i = (int)(ri % Tg);
+  const long r = ri / Tg;
+  const long full = (r * S_cap + q + (long)g * i) * d + 8 * v, comp = ri * d + 8 * v;
+  if (!restore) {
+    *(uint4*)(Kg + comp) = *(const uint4*)(K + full);
+    *(uint4*)(Vg + comp) = *(const uint4*)(V + full);
+    return;
+  }
+  *(uint4*)(K + full) = *(const uint4*)(Kg + comp);
+  *(uint4*)(V + full) = *(const uint4*)(Vg + comp);
+  if (dK) {
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    *(float4*)(dK + full) = z;
+    *(float4*)(dK + full + 4) = z;
+    *(float4*)(dV + full) = z;
+    *(float4*)(dV + full + 4) = z;
+  }
+}
+void launch_grad_slots(bf16* K, bf16* V, bf16* Kg, bf16* Vg, float* dK, float* dV, long rows,
+                       int Tg, int g, int q, int S_cap, int d, bool restore, hipStream_t s) {
+  const long n = rows * Tg * (d / 8);
+  if (n > 0)
+    hipLaunchKernelGGL(grad_slots_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, K,
+                       V, Kg, Vg, dK, dV, rows, Tg, g, q, S_cap, d, restore ? 1 : 0);
 }
 
 // dst[r][e] = src[r * src_stride + e] (bf16 rows of D)

@@ -220,9 +220,13 @@ void launch_grad_mask(T* W, int kL, int L, int Lp, int D, const LayerTable& sel,
 
 void launch_grad_fill(float* p, long n, float v, hipStream_t s);
 void launch_grad_cast(const float* src, bf16* dst, long n, hipStream_t s);
-// dst[r][e] += sum over l < nsrc of src[r src_stride + l D + e]
-void launch_grad_add_rows(float* dst, const float* src, long rows, int D, long src_stride,
-                          int nsrc, hipStream_t s);
+// dst[r dst_stride + e] += sum over l < nsrc of src[r src_stride + l D + e]
+void launch_grad_add_rows(float* dst, long dst_stride, const float* src, long rows, int D,
+                          long src_stride, int nsrc, hipStream_t s);
+// slots q + g i (i < Tg) of the [rows][S_cap][d] caches to (restore false) or back from
+// (restore true) compact [rows][Tg][d] copies; restoring clears dK, dV there when given
+void launch_grad_slots(bf16* K, bf16* V, bf16* Kg, bf16* Vg, float* dK, float* dV, long rows,
+                       int Tg, int g, int q, int S_cap, int d, bool restore, hipStream_t s);
 void launch_grad_copy_rows(const bf16* src, long src_stride, bf16* dst, long rows, int D,
                            hipStream_t s);
 

@@ -255,17 +255,19 @@ PASS_CASES = [
 
 
 @pytest.mark.parametrize("case", range(len(PASS_CASES)))
-@pytest.mark.parametrize("passes,n_grad", [(2, 2), (3, 1), (3, 2)])
-def test_prefill_passes_backward(wm, case, passes, n_grad):
-    """The passes' forward and the truncated backward against the oracle's autograd of the
-    same passes with the states entering the window detached."""
+@pytest.mark.parametrize("passes,n_grad,g", [(2, 2, 1), (3, 1, 1), (3, 2, 1), (2, 2, 2),
+                                             (3, 2, 3)])
+def test_prefill_passes_backward(wm, case, passes, n_grad, g):
+    """The passes' forward and the truncated backward, over g strided groups (g = 1:
+    Jacobi), against the oracle's autograd of the same passes with the cache entering the
+    window detached."""
     kw = dict(PASS_CASES[case])
     modes = {m: kw.pop(m) for m in ("mix_mode", "router_mode", "mask_mode") if m in kw}
     shape = dict(d=64, Hq=4, Hkv=2, L=4, k=2, p=1)
     shape.update(kw)
     w = synth.small("pp%d" % case, B=2, T_new=150, D=128, ctx=0, dtype="bf16", **shape)
-    print("passes backward case %d %s passes %d window %d" % (case, modes, passes, n_grad),
-          flush=True)
+    print("passes backward case %d %s passes %d window %d groups %d"
+          % (case, modes, passes, n_grad, g), flush=True)
     P = synth.make_params(w, _bias(w), gains="random")
     X = synth.make_embeddings(w)
     # the block's output projection at std 0.4 (20 times the forward tests' 0.02): at 0.02
@@ -277,16 +279,16 @@ def test_prefill_passes_backward(wm, case, passes, n_grad):
     dh = synth._normal((w.B, w.T_new, w.D), 1.0, 801, torch.float32)
     od = _odims(w, S_cap=w.T_new, **modes)
     ref = ob.passes_grads(od, P, _f64(W_o), _f64(X), w.chan_map, passes, n_grad,
-                          dh.double().numpy())
+                          dh.double().numpy(), g=g)
     # how far bf16 storage of the states, caches, queries and outputs moves each gradient
     # (the oracle's own measure of the gradient's sensitivity to that rounding)
     stored = ob.passes_grads(od, P, _f64(W_o), _f64(X), w.chan_map, passes, n_grad,
-                             dh.double().numpy(), bf16_storage=True)
+                             dh.double().numpy(), bf16_storage=True, g=g)
     _, top_ref = ob.passes_forward(od, {n: ob._t(P[n]) for n in ob.PARAM_NAMES}, ob._t(W_o),
-                                   ob._t(X), w.chan_map, passes, n_grad)
+                                   ob._t(X), w.chan_map, passes, n_grad, g=g)
     names = [n for n in ob.PARAM_NAMES if not (n == "W_alpha" and modes.get("router_mode") == 1)
              and not (n in ("Kd", "Vd") and modes.get("mask_mode") == 1)]
-    dims = _gdims(wm, w, S_cap=w.T_new, ctx_max=0, **modes)
+    dims = _gdims(wm, w, S_cap=w.T_new, ctx_max=0, groups=g, **modes)
     dX0 = synth._normal(tuple(X.shape), 1.0, 802, torch.float32).cuda()
     dX = dX0.clone()
     dW0 = synth._normal(tuple(W_o.shape), 0.5, 803, torch.float32).cuda()
