@@ -898,7 +898,8 @@ PassBwdLayout passes_bwd_layout(const wm_dims& d, int n_grad) {
 // pass runs the groups in order, group q recomputing the states of its positions layer by
 // layer from the cache as it stands, then pooling them into its slots. The passes before
 // the gradient window run in scratch; each window step (pass t, group q) keeps its group's
-// states, its layers' attention outputs and the slots its pool overwrote.
+// states, its layers' attention outputs and the slots its pool overwrote. The last step's
+// pool is left out: nothing reads the slots it would write.
 // The backward walks the window's steps from the last. It holds the loss gradient in the
 // whole cache (dK, dV) as the forward left it at that point: the step's pool sends the
 // gradient at its slots to its states, and those slots are then given back the values the
@@ -945,8 +946,8 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
                    true);
   // one step: group q's states in Hq (layer 0 holds X) from the cache, its layers' outputs
   // into O (layer l at l Ng HQ) or scratch, the slots it overwrites into (uk, uv) if given,
-  // then its pool
-  auto step = [&](int q, bf16* Hq, bf16* O, bf16* uk, bf16* uv) {
+  // then its pool unless it is the last step (whose pool nothing reads)
+  auto step = [&](int q, bf16* Hq, bf16* O, bf16* uk, bf16* uv, bool pool) {
     const wm_dims dq = group_dims(d, q);
     wm::launch_rope_table(make_shape(dq), nullptr, tab, s);
     for (int l = 0; l < L; ++l) {
@@ -958,17 +959,19 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
                                       last ? topg + (long)q * Ng * D : Hq + (long)(l + 1) * D,
                                       last ? D : (long)L * D, s);
     }
+    if (!pool) return;
     if (uk) wm::launch_grad_slots(K, V, uk, uv, nullptr, nullptr, crows, Tg, g, q, d.S_cap, d.d,
                                   false, s);
     run_pool<bf16>(dq, P, Hq, nullptr, K, V, Lf, fw, s, true, true, true);
   };
+  const int nsteps = n_grad * g;
   for (int t = 1; t <= first; ++t)
-    for (int q = 0; q < g; ++q) step(q, Hg + q * gsz, nullptr, nullptr, nullptr);
-  for (int j = 0; j < n_grad * g; ++j) {
+    for (int q = 0; q < g; ++q) step(q, Hg + q * gsz, nullptr, nullptr, nullptr, true);
+  for (int j = 0; j < nsteps; ++j) {
     const int q = j % g;
     (void)hipMemcpyAsync(Hs(j), Hg + q * gsz, (size_t)gsz * sizeof(bf16), hipMemcpyDeviceToDevice,
                          s);
-    step(q, Hs(j), Os(j), Uk(j), Uv(j));
+    step(q, Hs(j), Os(j), Uk(j), Uv(j), j + 1 < nsteps);
   }
   if (h_top) wm::launch_group_scatter<bf16>(topg, h_top, d.B, d.T_new, g, D, s);
 
@@ -996,18 +999,20 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
   float* rinv = (float*)at(fw, Lf.rinv);
   wm::launch_grad_fill(dpk, cache_elems, 0.f, s);
   wm::launch_grad_fill(dpv, cache_elems, 0.f, s);
-  for (int j = n_grad * g - 1; j >= 0; --j) {
+  for (int j = nsteps - 1; j >= 0; --j) {
     const int q = j % g;
-    const bool last_pass = j >= (n_grad - 1) * g;
+    const bool last_pass = j >= (n_grad - 1) * g, pooled = j + 1 < nsteps;
     const wm_dims dq = group_dims(d, q);
     const wm::Shape shq = make_shape(dq), sh1 = make_shape(one_consumer(dq));
     const bf16* H = Hs(j);
     const bf16* O = Os(j);
     // the step's pool: the gradient at its slots goes to its states (dhn); the slots then
     // hold what the step read, their gradient cleared
-    wm::launch_grad_fill(dhn, gsz, 0.f, s);
-    run_pool_backward(dq, P, H, nullptr, dpk, dpv, dhn, G, Lp, sub, s);
-    wm::launch_grad_slots(K, V, Uk(j), Uv(j), dpk, dpv, crows, Tg, g, q, d.S_cap, d.d, true, s);
+    if (pooled) {
+      wm::launch_grad_fill(dhn, gsz, 0.f, s);
+      run_pool_backward(dq, P, H, nullptr, dpk, dpv, dhn, G, Lp, sub, s);
+      wm::launch_grad_slots(K, V, Uk(j), Uv(j), dpk, dpv, crows, Tg, g, q, d.S_cap, d.d, true, s);
+    }
     // gcur: the gradient in h_{l+1}, from the loss at the top of the last pass
     wm::launch_grad_fill(gcur, (long)Ng * D, 0.f, s);
     if (last_pass) wm::launch_grad_add_rows(gcur, D, dh_top + (long)q * D, Ng, D, (long)g * D, 1, s);
@@ -1047,7 +1052,7 @@ void run_passes_backward(const wm_dims& d, const wm_params& P, const bf16* W_o, 
       wm_dims dl = dq;
       dl.L = 1;
       run_q_backward(dl, P1, h1, nullptr, dql, gcur, G1, Lq, sub, s);
-      wm::launch_grad_add_rows(gcur, D, dhn + (long)l * D, Ng, D, (long)L * D, 1, s);
+      if (pooled) wm::launch_grad_add_rows(gcur, D, dhn + (long)l * D, Ng, D, (long)L * D, 1, s);
     }
     wm::launch_grad_add_rows(dX + (long)q * D, (long)g * D, gcur, Ng, D, D, 1, s);  // h_0 = X
   }

@@ -498,11 +498,14 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
 // (consumer, query head, sequence, position) are split into dummy_chunks(sh) contiguous
 // chunks, one workgroup of 4 DH threads each (thread (rl, e) sums column e over every
 // fourth row of the chunk), and a second kernel adds the chunks in order.
-// chunks per (channel, KV head): at least 32, and enough for ~4096 workgroups in all (a
+// chunks per (channel, KV head): at least 32, and enough for ~4096 workgroups in all, but
+// no more than one per 128 rows of an even spread of the consumers over the channels (a
 // fixed function of the shape, so the sums keep one order on any device)
 static int dummy_chunks(const Shape& sh) {
   const int pairs = sh.k * sh.Hkv;
-  return std::max(32, std::min(1024, (2048 + pairs - 1) / pairs));
+  const long rows = (long)((sh.L + sh.k - 1) / sh.k) * (sh.Hq / sh.Hkv) * sh.B * sh.T_new;
+  const int by_rows = (int)std::min(1024L, std::max(1L, (rows + 127) / 128));
+  return std::min(by_rows, std::max(32, std::min(1024, (2048 + pairs - 1) / pairs)));
 }
 
 template <int DH>

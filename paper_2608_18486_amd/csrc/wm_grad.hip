@@ -51,6 +51,7 @@ template <int WGM_, int WGN_, int WM_, int WN_> struct GemmCfg {
 };
 typedef GemmCfg<2, 4, 4, 2> GemmBig;    // 256 x 256, 8 waves
 typedef GemmCfg<2, 2, 2, 2> GemmSmall;  // 128 x 128, 4 waves
+typedef GemmCfg<2, 2, 1, 1> GemmTiny;   // 64 x 64, 4 waves
 
 __device__ __forceinline__ int grad_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
 
@@ -411,15 +412,18 @@ static void launch_gemm_cfg(const GemmArgs& a, int batches, hipStream_t s) {
 
 template <bool TA, bool TB>
 static void launch_gemm_t(GemmArgs a, int batches, bool vec, hipStream_t s) {
-  // the large tiles (vector operands only) when they still give every CU at least two;
-  // LDS DMA when both operands' batch spans fit a buffer view and no k-contiguous B
-  // operand carries a k limit (its copies are whole 8-element chunks)
+  // the large tiles (vector operands only) when they still give every CU at least two, the
+  // 64 x 64 ones when the 128 x 128 ones would leave CUs idle; LDS DMA when both operands'
+  // batch spans fit a buffer view and no k-contiguous B operand carries a k limit (its
+  // copies are whole 8-element chunks)
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256) * batches;
   a.A.span = operand_span(a.A, a.M, a.K);
   a.B.span = operand_span(a.B, a.N, a.K);
   const bool dma = vec && a.A.span < (1L << 31) && a.B.span < (1L << 31) &&
                    (TB || (a.k_lo0 == 0 && a.k_lo_dz == 0));
+  const long small = (long)((a.M + 127) / 128) * ((a.N + 127) / 128) * batches * a.splits;
   if (dma && big >= 2L * device_cus()) launch_gemm_dma<GemmBig, TA, TB>(a, batches, s);
+  else if (dma && small < device_cus()) launch_gemm_dma<GemmTiny, TA, TB>(a, batches, s);
   else if (dma) launch_gemm_dma<GemmSmall, TA, TB>(a, batches, s);
   else if (vec && big >= 2L * device_cus()) launch_gemm_cfg<GemmBig, TA, TB, true>(a, batches, s);
   else if (vec) launch_gemm_cfg<GemmSmall, TA, TB, true>(a, batches, s);
