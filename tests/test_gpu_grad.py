@@ -82,6 +82,55 @@ def test_weight_gradients_split_k(wm):
         check_close(g[n].cpu(), ref["d" + n], "bf16", "split d%s" % n)
 
 
+def test_query_and_pool_gradients_at_full_size(wm):
+    """The queries' and the pool's gradients of the 4096-token, 24-layer pass in the launch
+    configuration a training step uses (256 x 256 and 128 x 128 GEMM tiles): dH of sampled
+    token runs, whose rows depend only on their own states and incoming gradients, and the
+    query weights' and gains' gradients of the first and the last layer, each of which
+    depends only on its own layer, against the oracle on those sub-problems. (The pool's
+    weight gradients mix every layer of every token; they are checked on the small shapes.)"""
+    import dataclasses
+    w = synth.WORKLOADS["c4_T4096_L24_k12"]
+    print("query and pool gradients full size", flush=True)
+    P = synth.make_params(w, _bias(w), gains="random")
+    H = synth.make_states(w)
+    dQ = synth._normal((w.L, w.B, w.Hq, w.T_new, w.d), 1.0, 521, torch.float32)
+    rows = (w.k, w.B, w.Hkv, w.T_new, w.d)
+    dK = synth._normal(rows, 1.0, 522, torch.float32)
+    dV = synth._normal(rows, 1.0, 523, torch.float32)
+    dims = _gdims(wm, w, S_cap=w.T_new, ctx_max=0)
+    Pd, Hd = _dev(P), H.cuda()
+    dHq = torch.zeros(tuple(H.shape), **F32)
+    gq = {n: torch.zeros(tuple(P[n].shape), **F32) for n in ob.QUERY_PARAMS}
+    wm.q_project_backward(dims, Pd, Hd, None, dQ.cuda(), dHq, gq)
+    dHp = torch.zeros(tuple(H.shape), **F32)
+    gp = {n: torch.zeros(tuple(P[n].shape), **F32) for n in ob.POOL_PARAMS}
+    wm.pool_backward(dims, Pd, Hd, None, dK.cuda(), dV.cuda(), dHp, gp)
+    torch.cuda.synchronize()
+    dHq, dHp = dHq.cpu().numpy(), dHp.cpu().numpy()
+    gq = {n: t.cpu() for n, t in gq.items()}
+    del Pd, Hd, gp
+    base = _odims(w, S_cap=w.T_new)
+    for b, s0, n in ((0, 0, 24), (w.B - 1, w.T_new - 24, 24), (1, 1500, 16)):
+        sub = dataclasses.replace(base, B=1, T_new=n)
+        ctx = np.array([s0])
+        rq = ob.q_project_grads(sub, P, H[b:b + 1, s0:s0 + n],
+                                dQ[:, b:b + 1, :, s0:s0 + n].double().numpy(), ctx)
+        check_close(dHq[b, s0:s0 + n], rq["dH"][0], "bf16", "queries dH b%d %d+%d" % (b, s0, n))
+        rp = ob.pool_grads(sub, P, H[b:b + 1, s0:s0 + n],
+                           dK[:, b:b + 1, :, s0:s0 + n].double().numpy(),
+                           dV[:, b:b + 1, :, s0:s0 + n].double().numpy(), ctx)
+        check_close(dHp[b, s0:s0 + n], rp["dH"][0], "bf16", "pool dH b%d %d+%d" % (b, s0, n))
+    for l in (0, w.L - 1):
+        sub = dataclasses.replace(base, L=1)
+        Pl = dict(P)
+        for n in ob.QUERY_PARAMS:
+            Pl[n] = P[n][l:l + 1]
+        r = ob.q_project_grads(sub, Pl, H[:, :, l:l + 1], dQ[l:l + 1].double().numpy())
+        for n in ob.QUERY_PARAMS:
+            check_close(gq[n][l], r["d" + n][0], "bf16", "layer %d d%s" % (l, n))
+
+
 POOL_CASES = [
     dict(),
     dict(mix_mode=1),
