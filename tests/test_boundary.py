@@ -310,3 +310,31 @@ def test_step_gradients_reject_unsupported_calls_before_launch(wm):
     for op in (wm.OP_Q_BACKWARD, wm.OP_POOL_BACKWARD, wm.OP_STEP_BACKWARD):
         assert wm.workspace_size(d, op) > 0
     assert wm.workspace_size(d, wm.OP_STEP_BACKWARD) >= 6 * d.L * d.B * d.Hq * d.T_new * d.d
+
+
+def test_passes_backward_rejects_unsupported_calls_before_launch(wm):
+    """The training passes: passes >= 1, 1 <= n_grad <= passes, bf16, T a multiple of the
+    groups with more than 4 tokens per group (the gradients' full-sequence kernels); each is
+    refused on the host with its own code, before any pointer is needed."""
+    cmap = [0, 1, 0, 1]
+
+    def code(passes, n_grad, **kw):
+        kw = dict(dict(d=64, T_new=48, S_cap=48, ctx_max=0), **kw)
+        with pytest.raises(wm.WMError) as e:
+            wm.prefill_passes_backward(_dims(wm, **kw), None, None, None, cmap, passes, n_grad,
+                                       None, None, None, None)
+        return e.value.code
+
+    assert code(0, 1) == wm.ERR_ARG
+    assert code(3, 0) == wm.ERR_ARG
+    assert code(3, 4) == wm.ERR_ARG
+    assert code(3, 2, dtype=wm.F32) == wm.ERR_DTYPE
+    assert code(3, 2, groups=5) == wm.ERR_SHAPE    # 48 tokens are not 5 groups
+    assert code(3, 2, groups=12) == wm.ERR_SHAPE   # 4 tokens per group
+    assert code(3, 2, groups=8) == wm.ERR_ARG      # 6 per group: params NULL comes next
+    assert code(3, 2, groups=8, group=1) == wm.ERR_ARG  # the driver runs every group
+    # the workspace holds each window step's states, outputs and overwritten slots
+    d = _dims(wm, d=64, T_new=48, S_cap=48, ctx_max=0, groups=8)
+    w1, w2 = wm.passes_backward_workspace(d, 1), wm.passes_backward_workspace(d, 2)
+    assert 0 < w1 < w2
+    assert wm.passes_backward_workspace(d, 0) == 0
