@@ -192,7 +192,10 @@ int wm_q_project(const wm_dims *dims, const wm_params *params, const void *H,
  *            included in WM_MASK_PAPER)
  * Uses Kd, Vd. T_new <= 4 takes the split-S decode kernels (their partial sums go to the
  * workspace); longer calls take the full-sequence kernels, whose workgroups take query tiles
- * from a 512-byte work queue in the workspace, reset on `stream` before each launch. */
+ * from a 512-byte work queue in the workspace, reset on `stream` before each launch, or,
+ * when the query tiles are few against long slot ranges (bf16, no document mask), walk
+ * split ranges of each tile's slots whose partial softmax states go to the workspace and are
+ * merged in a fixed order. */
 int wm_channel_attend(const wm_dims *dims, const wm_params *params, const void *Q,
                       const int32_t *chan_map, const int32_t *ctx_len, const void *Kc,
                       const void *Vc, void *O, void *ws, size_t ws_bytes,
@@ -323,9 +326,10 @@ int wm_layer_step_backward(const wm_dims *dims, const wm_params *params, const v
 
 /* wm_channel_attend for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument. Its only
- * scratch, the split-S decode partials (T_new <= 4) or the full-sequence kernels' 512-byte
- * work queue, lives in a fixed array of 64 MiB of device memory inside the library; each device holds
- * its own copy until the process ends. The call itself allocates nothing. Calls on one
+ * scratch, the split-S decode partials (T_new <= 4), the full-sequence kernels' 512-byte
+ * work queue or, on grids of few query tiles, the partial states of their split slot
+ * ranges, lives in a fixed array of 64 MiB of device memory inside the library; each
+ * device holds its own copy until the process ends. The call itself allocates nothing. Calls on one
  * device share that array, so calls that overlap on one device race; serialise them (one
  * stream, or events). A call needing more scratch than the array holds (its
  * wm_workspace_size(dims, WM_OP_CHANNEL_ATTEND)) fails with WM_ERR_WORKSPACE before any

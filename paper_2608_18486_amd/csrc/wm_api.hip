@@ -240,9 +240,13 @@ Layout layout(const wm_dims& dd, int op) {
   }
   if (layer && decode_path(d)) Ly.part = take(wm::decode_partials_bytes(one_layer(make_shape(d))));
   if (op == WM_OP_ATTEND_BACKWARD) Ly.part = take(wm::attend_backward_rows_bytes(make_shape(d)));
-  // the full-sequence attention's work queue takes the decode partials' place
-  if (!decode_path(d) && (op == WM_OP_CHANNEL_ATTEND || all || layer || op == WM_OP_DENSE_ATTEND))
-    Ly.part = take(wm::kPrefillQueueBytes);
+  // the full-sequence attention's work queue (or its split ranges' partial states) takes
+  // the decode partials' place
+  if (!decode_path(d) && (op == WM_OP_CHANNEL_ATTEND || all || layer || op == WM_OP_DENSE_ATTEND)) {
+    const wm::Shape sp = layer ? one_layer(make_shape(d))
+                               : op == WM_OP_DENSE_ATTEND ? dense_shape(make_shape(d)) : make_shape(d);
+    Ly.part = take(wm::prefill_scratch_bytes(sp));
+  }
   if (op == WM_OP_KV_PROJECT || all || pool) Ly.wkv = take(wm::kv_fold_elems(make_shape(d)) * es);
   if (op == WM_OP_Q_PROJECT || all || layer) Ly.wq = take(wm::q_fold_elems(make_shape(d)) * es);
   if (op == WM_OP_ROUTER_MIX || all || pool) {

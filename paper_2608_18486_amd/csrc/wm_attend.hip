@@ -94,6 +94,12 @@ template <typename T> struct AttnArgs {
   float scale_log2;  // log2(e) / sqrt(d)
   LayerTable chan;
   LayerTable lord;  // the consumers in channel order (the bf16 kernels' tile order)
+  // split slot ranges (bf16 full-sequence kernel, small grids): each query tile's walk is
+  // cut into nsplit ranges of split_blk 64-slot blocks, one workgroup each, whose partial
+  // softmax states go to part and are merged by attend_split_combine_kernel (nsplit = 1:
+  // one workgroup walks the whole range and writes O)
+  int nsplit, split_blk;
+  float* part;
 };
 
 #ifndef WM_PREFILL_WAVES
@@ -683,9 +689,9 @@ __device__ __forceinline__ void pf_step(const char* sm, const PfLane<DH>& lo, ui
 // One query tile of the persistent kernel below: 32 QT rows per wave of one (consumer,
 // sequence, head). On entry every wave is past the previous tile (its copies have
 // landed and its ring reads are done) and the rings hold finite values.
-template <int QT, int DH, bool DOC>
-__device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile, char* smem,
-                                        int* s_lo) {
+template <int QT, int DH, bool DOC, bool SPLIT>
+__device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile, const int split,
+                                        char* smem, int* s_lo) {
   using P = PfDma<QT, DH>;
   constexpr int NKS = P::NKS, NDT = P::NDT;
   // Tile order: sequence, KV head, consumer (in channel order), query head of the KV
@@ -771,6 +777,7 @@ __device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile,
   } else {
 #pragma unroll
     for (int t = 0; t < QT; ++t) dlo[t] = 0;
+    if constexpr (SPLIT) base0 = split * a.split_blk * P::BKV;  // a split walks from its first block
   }
   const int ctxr = pos0 - base0;  // the first new token's position relative to base0
 
@@ -778,15 +785,40 @@ __device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile,
                      (long)base0 * DH;
   const int qlast = min(q0 + P::BQ, a.T_new) - 1;
   const int scap = a.S_cap - base0;
-  const int kend = min(ctxr + gs * qlast + incl, scap);   // slots the workgroup may see
+  int kend = min(ctxr + gs * qlast + incl, scap);   // slots the workgroup may see
+  if constexpr (SPLIT) {
+    if (kend <= 0) {  // the tile's walk ends before this split: an empty partial state
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const int qi = qw0 + 32 * t + r;
+        if (qi < a.T_new && h == 0) {
+          const long rows = (long)a.L * a.B * a.Hq * a.T_new;
+          const long row = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + qi;
+          float* ml = a.part + rows * a.nsplit * DH + 2 * ((long)split * rows + row);
+          ml[0] = kNoRef;
+          ml[1] = 0.f;
+        }
+      }
+      return;
+    }
+    kend = min(kend, a.split_blk * P::BKV);
+  }
   const int nblk = (kend + P::BKV - 1) / P::BKV;
   const int wq_last = min(qw0 + 32 * QT - 1, a.T_new - 1);
   const int wkend = wq_last >= qw0 ? ctxr + gs * wq_last + incl : 0;  // slots this wave may see
   const int wfree = ctxr + gs * qw0 + incl;  // slots < wfree are visible to all its rows ...
   // ... and at or past wlo_max (the document starts); a step is masked unless both hold
   auto masked = [&](int i) { return 32 * i + 32 > wfree || (DOC && 32 * i < wlo_max); };
-  const int ilast = (wkend + 31) / 32 - 1;  // the wave's last 32-slot step (-1: none)
-  const int lim0 = ctxr + gs * (qw0 + r) + incl, tstride = 32 * gs;
+  int ilast = (wkend + 31) / 32 - 1;  // the wave's last 32-slot step (-1: none)
+  int lim0 = ctxr + gs * (qw0 + r) + incl;
+  const int tstride = 32 * gs;
+  if constexpr (SPLIT) {
+    // a split stops at its last block (the step after it only adds that block's PV, its
+    // own slots hidden by the limit) and a wave that sees nothing in it takes no step
+    ilast = ilast < 0 ? -2 : min(ilast, 2 * nblk - 1);
+    lim0 = min(lim0, kend);
+    static_assert(QT == 1, "one query tile per wave: lim0 is the row's only limit");
+  }
 
   // copies: wave w moves slot rows RPW w .. RPW w + RPW-1 of each K and V block, 1 KB
   // (64 chunks of 16 B) per instruction; lane x of instruction n fills LDS chunk
@@ -839,7 +871,7 @@ __device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile,
   for (int t = 0; t < QT; ++t) {
     st.pf[0][t] = zero_frag<bf16>();
     st.pf[1][t] = zero_frag<bf16>();
-    if (a.mask_paper) {
+    if (a.mask_paper && split == 0) {  // the dummy starts the first split's state
       float part = 0.f;
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks)
@@ -914,6 +946,33 @@ __device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile,
   }
   wait_vmcnt<0>();  // no copy may land after the workgroup ends
 
+  if constexpr (SPLIT) {  // the partial state: O unnormalised, the reference and the weights' sum
+    const long rows = (long)a.L * a.B * a.Hq * a.T_new;
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      const int qi = qw0 + 32 * t + r;
+      const float lt = halves_sum(st.lsum[t]);
+      if (qi < a.T_new) {
+        const long row = (((long)l * a.B + b) * a.Hq + hq) * a.T_new + qi;
+        float* po = a.part + ((long)split * rows + row) * DH;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            f32x4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = st.o[dt][t][4 * g + i];
+            *(f32x4*)(po + 32 * dt + 8 * g + 4 * h) = v;
+          }
+        if (h == 0) {
+          float* ml = a.part + rows * a.nsplit * DH + 2 * ((long)split * rows + row);
+          ml[0] = st.m[t];
+          ml[1] = lt;
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     const int qi = qw0 + 32 * t + r;
@@ -947,7 +1006,7 @@ __device__ __forceinline__ void pf_tile(const AttnArgs<bf16>& a, const int tile,
 // queue null the grid has one workgroup per tile (tile order as above, XCD-aware).
 // DOC: the document mask is on (a.doc is not null); the kernel without it keeps the
 // step loop free of the document bookkeeping.
-template <int QT, int DH, bool DOC>
+template <int QT, int DH, bool DOC, bool SPLIT = false>
 __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(DH == 64 ? 3 : 2)))
 void attend_prefill_dma_kernel(AttnArgs<bf16> a, uint32_t* queue) {
   using P = PfDma<QT, DH>;
@@ -966,9 +1025,15 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a, uint32_t* queue) {
       *(i32x4*)(smem + 16 * (tid + P::NT * k)) = z;
   }
   const int total = a.n_qtiles * a.Hq * a.B * a.L;
+  if constexpr (SPLIT) {  // a workgroup per tile and split range (consecutive: one tile)
+    __syncthreads();  // the zeroed rings are in place before any copy lands
+    const int idx = xcd_tile(blockIdx.x, total * a.nsplit);
+    pf_tile<QT, DH, DOC, true>(a, idx / a.nsplit, idx % a.nsplit, smem, s_lo);
+    return;
+  }
   if (!queue) {  // a grid of one workgroup per tile (grids the CUs hold at once)
     __syncthreads();  // the zeroed rings are in place before any copy lands
-    pf_tile<QT, DH, DOC>(a, xcd_tile(blockIdx.x, total), smem, s_lo);
+    pf_tile<QT, DH, DOC, false>(a, xcd_tile(blockIdx.x, total), 0, smem, s_lo);
     return;
   }
   const int nq = min((int)gridDim.x, kNumXcd), x = blockIdx.x % nq;
@@ -979,7 +1044,7 @@ void attend_prefill_dma_kernel(AttnArgs<bf16> a, uint32_t* queue) {
   __syncthreads();  // also: the zeroed rings are in place before any copy lands
   int t = __builtin_amdgcn_readfirstlane(s_tile);
   while (t < count) {
-    pf_tile<QT, DH, DOC>(a, first + t, smem, s_lo);
+    pf_tile<QT, DH, DOC, false>(a, first + t, 0, smem, s_lo);
     // every wave reads s_tile after this barrier and before the next tile's first one,
     // so thread 0 rewrites it only once all have read it
     if (tid == 0) s_tile = (int)atomicAdd(ctr, 1u);
@@ -1004,10 +1069,89 @@ int device_cus() {
   return n;
 }
 
+// Split slot ranges for small grids (bf16 kernel, no documents): when the query tiles
+// fill at most a quarter of the workgroup slots the CUs hold at once, each tile's walk is
+// cut into ranges of split_blk 64-slot blocks (at least 16) so that about one resident
+// round of workgroups runs. Measured on the pass driver's group calls at the paper's
+// shape: 2 ranges at 96 tiles, 11% faster; at 192 tiles any split was slower (the
+// partial states' write and merge, 28 MB a call, cost more than the shorter walks save),
+// as were ranges of 4-11 blocks.
+// Returns the splits aimed at (an upper bound on *nsplit that grows with the slot range,
+// which sizes the partial states).
+static long prefill_split(const Shape& sh, long tiles, int* nsplit, int* split_blk) {
+  const long resident = (long)device_cus() * (sh.d == 64 ? PfDma<kPfQt, 64>::WPE
+                                                         : PfDma<kPfQt, 96>::WPE);
+  const long kmax = (long)sh.ctx_max + sh.span();  // bound on any tile's visible slots
+  const int max_blk = (int)std::max(1L, (kmax + 63) / 64);
+  long n = 1;
+  if (4 * tiles <= resident) n = std::min<long>((resident + tiles - 1) / tiles, max_blk / 16);
+  if (n < 2) {
+    *nsplit = 1;
+    *split_blk = max_blk;
+    return 1;
+  }
+  const int blk = (int)((max_blk + n - 1) / n);
+  *nsplit = (max_blk + blk - 1) / blk;
+  *split_blk = blk;
+  return n;
+}
+
+static long prefill_tiles(const Shape& sh) {
+  return (long)((sh.T_new + PfDma<kPfQt, 64>::BQ - 1) / PfDma<kPfQt, 64>::BQ) * sh.Hq * sh.B *
+         sh.L;
+}
+
+size_t prefill_scratch_bytes(const Shape& sh) {
+  if (sh.d != 64 && sh.d != 96) return kPrefillQueueBytes;
+  int nsplit, blk;
+  const long n = prefill_split(sh, prefill_tiles(sh), &nsplit, &blk);
+  const size_t rows = (size_t)sh.L * sh.B * sh.Hq * sh.T_new;
+  return n > 1 ? std::max(kPrefillQueueBytes, rows * n * (sh.d + 2) * sizeof(float))
+               : kPrefillQueueBytes;
+}
+
+// The split ranges' partial states merged per row in split order: with M the largest
+// reference among the ranges that saw a slot, O = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s
+// (part: o [nsplit][rows][DH] unnormalised, then (m, l) [nsplit][rows][2]). A thread takes
+// four columns of one row.
+template <int DH>
+__global__ __launch_bounds__(256) void attend_split_combine_kernel(const float* part, int nsplit,
+                                                                   int T, int Hq, long rows,
+                                                                   bf16* O) {
+  constexpr int C4 = DH / 4;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= rows * C4) return;
+  const long row = idx / C4;
+  const int c = (int)(idx - row * C4);
+  const float* ml = part + rows * nsplit * DH;
+  float M = -3.0e38f;
+  for (int s = 0; s < nsplit; ++s)
+    if (ml[2 * (s * rows + row) + 1] > 0.f) M = fmaxf(M, ml[2 * (s * rows + row)]);
+  float lsum = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < nsplit; ++s) {
+    const float ls = ml[2 * (s * rows + row) + 1];
+    if (ls > 0.f) {
+      const float wgt = fast_exp2(ml[2 * (s * rows + row)] - M);
+      const f32x4 o = *(const f32x4*)(part + (s * rows + row) * DH + 4 * c);
+      lsum += ls * wgt;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] += o[i] * wgt;
+    }
+  }
+  const float inv = 1.0f / lsum;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] *= inv;
+  // row = ((l B + b) Hq + hq) T + i  ->  O[(l B + b) T + i][hq DH + 4 c]
+  const long i = row % T, lbh = row / T;
+  const int hq = (int)(lbh % Hq);
+  const long lb = lbh / Hq;
+  store4(O + ((lb * T + i) * Hq + hq) * DH + 4 * c, acc);
+}
+
 template <typename T>
 void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q, const T* Kc,
                            const T* Vc, const T* Kd, const T* Vd, const int32_t* ctx_len,
-                           const int32_t* doc, T* O, uint32_t* queue, hipStream_t s) {
+                           const int32_t* doc, T* O, void* scratch, hipStream_t s) {
   if (sh.N() <= 0) return;
   constexpr int BQ = PrefillCfg<T, 64>::BQ, NT = PrefillCfg<T, 64>::NT;
   static_assert(BQ == PrefillCfg<T, 32>::BQ && NT == PrefillCfg<T, 32>::NT, "tile shapes");
@@ -1017,7 +1161,7 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
       if (chan_map.v[l] == c) lord.v[n++] = l;
   AttnArgs<T> a{Q, Kc, Vc, Kd, Vd, ctx_len, doc, O, sh.B, sh.T_new, sh.L, sh.Hq, sh.Hkv, sh.S_cap,
                 sh.mask_paper, (sh.T_new + BQ - 1) / BQ, sh.gs, sh.gq, sh.ctx_hi,
-                kLog2e / sqrtf((float)sh.d), chan_map, lord};
+                kLog2e / sqrtf((float)sh.d), chan_map, lord, 1, 0, nullptr};
   dim3 grid(a.n_qtiles * sh.Hq * sh.B * sh.L);
   if (sizeof(T) == 2 && (sh.d == 64 || sh.d == 96)) {  // fp32 at d = 96 fails validation
     constexpr int BQD = PfDma<kPfQt, 64>::BQ;
@@ -1025,22 +1169,42 @@ void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T*
                   "tile shapes");
     AttnArgs<T> ad = a;
     ad.n_qtiles = (sh.T_new + BQD - 1) / BQD;
-    const AttnArgs<bf16>& ab = *reinterpret_cast<const AttnArgs<bf16>*>(&ad);
-    const long tiles = (long)ad.n_qtiles * sh.Hq * sh.B * sh.L;
+    const long tiles = prefill_tiles(sh);
     const long resident = (long)device_cus() * (sh.d == 64 ? PfDma<kPfQt, 64>::WPE
                                                            : PfDma<kPfQt, 96>::WPE);
     // persistent only when the tiles outnumber what the CUs hold at once; smaller grids
-    // start every tile at once and skip the queue (its reset launch and atomics)
+    // start every tile at once and skip the queue (its reset launch and atomics), and the
+    // smallest split their tiles' slot ranges
     const bool persistent = tiles > resident;
-    const dim3 gd((unsigned)(persistent ? resident : tiles)), bd(PfDma<kPfQt, 64>::NT);
+    if (!persistent && !doc) {
+      prefill_split(sh, tiles, &ad.nsplit, &ad.split_blk);
+      if (ad.nsplit > 1) ad.part = (float*)scratch;
+    }
+    uint32_t* queue = persistent ? (uint32_t*)scratch : nullptr;
+    const AttnArgs<bf16>& ab = *reinterpret_cast<const AttnArgs<bf16>*>(&ad);
+    const dim3 gd((unsigned)(persistent ? resident : tiles * ad.nsplit)),
+        bd(PfDma<kPfQt, 64>::NT);
     if (persistent) hipLaunchKernelGGL(queue_reset_kernel, dim3(1), dim3(kQueueWords), 0, s, queue);
-    else queue = nullptr;
     if (sh.d == 64) {
       if (doc) hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 64, true>), gd, bd, 0, s, ab, queue);
+      else if (ad.nsplit > 1)
+        hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 64, false, true>), gd, bd, 0, s, ab, queue);
       else hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 64, false>), gd, bd, 0, s, ab, queue);
     } else {
       if (doc) hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 96, true>), gd, bd, 0, s, ab, queue);
+      else if (ad.nsplit > 1)
+        hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 96, false, true>), gd, bd, 0, s, ab, queue);
       else hipLaunchKernelGGL((attend_prefill_dma_kernel<kPfQt, 96, false>), gd, bd, 0, s, ab, queue);
+    }
+    if (ad.nsplit > 1) {
+      const long rows = (long)sh.L * sh.B * sh.Hq * sh.T_new;
+      const unsigned nb = (unsigned)((rows * (sh.d / 4) + 255) / 256);
+      if (sh.d == 64)
+        hipLaunchKernelGGL(attend_split_combine_kernel<64>, dim3(nb), dim3(256), 0, s,
+                           (const float*)ad.part, ad.nsplit, sh.T_new, sh.Hq, rows, (bf16*)O);
+      else
+        hipLaunchKernelGGL(attend_split_combine_kernel<96>, dim3(nb), dim3(256), 0, s,
+                           (const float*)ad.part, ad.nsplit, sh.T_new, sh.Hq, rows, (bf16*)O);
     }
   } else if (sh.d == 64)
     hipLaunchKernelGGL((attend_prefill_kernel<T, 64>), grid, dim3(NT), 0, s, a);
@@ -1437,7 +1601,7 @@ void launch_soft_read(const Shape& sh, const float* w, const T* Kc, const T* Vc,
 #define WM_INST(T)                                                                              \
   template void launch_attend_prefill<T>(const Shape&, const LayerTable&, const T*, const T*,   \
                                          const T*, const T*, const T*, const int32_t*,          \
-                                         const int32_t*, T*, uint32_t*, hipStream_t);           \
+                                         const int32_t*, T*, void*, hipStream_t);               \
   template void launch_attend_decode<T>(const Shape&, const LayerTable&, const ChannelGroups&,  \
                                         const T*, const T*, const T*, const T*, const T*,       \
                                         const int32_t*, const int32_t*, float*, T*, hipStream_t); \

@@ -111,13 +111,16 @@ struct ChannelGroups {       // CSR inverse of the consumer -> channel map
   int members[kMaxLayers];
 };
 
-// queue: kPrefillQueueBytes of device memory the bf16 kernels take their tiles from
-// (reset on the stream before each launch); other paths ignore it.
+// scratch: prefill_scratch_bytes(sh) of device memory (at least kPrefillQueueBytes): the
+// work queue the bf16 kernel's persistent grid takes its tiles from (reset on the stream
+// before each launch), or the partial states of its split slot ranges on small grids;
+// other paths ignore it.
 constexpr size_t kPrefillQueueBytes = 512;
+size_t prefill_scratch_bytes(const Shape& sh);
 template <typename T>
 void launch_attend_prefill(const Shape& sh, const LayerTable& chan_map, const T* Q,
                            const T* Kc, const T* Vc, const T* Kd, const T* Vd,
-                           const int32_t* ctx_len, const int32_t* doc, T* O, uint32_t* queue,
+                           const int32_t* ctx_len, const int32_t* doc, T* O, void* scratch,
                            hipStream_t s);
 
 // Gradients of the full-sequence channel attention (bf16, head dims 64 and 96): dQ

@@ -1,5 +1,6 @@
 """The entry point that allocates nothing (wm_channel_attend_static): its decode partials
-live in the library's fixed device array instead of a caller workspace. Checked through
+(and the split ranges' partial states of a full-sequence call on a small grid) live in the
+library's fixed device array instead of a caller workspace. Checked through
 the C ABI against wm_channel_attend (same kernels: bit for bit) and against the oracle
 (the parity bar), on two calls in a row, the second smaller; a call that needs more than
 the array holds is rejected before any launch."""
@@ -40,6 +41,9 @@ def test_static_scratch_matches_workspace_entry_point(wm, dtype, d):
                      dtype=dtype), 3000),
         (synth.small("static_prefill", B=2, T_new=40, L=3, k=2, D=64, Hq=2, Hkv=1, d=d, ctx=140,
                      dtype=dtype), 100),
+        # few query tiles over a 2000-slot context: the bf16 kernel splits the slot ranges
+        (synth.small("static_split", B=2, T_new=40, L=3, k=2, D=64, Hq=2, Hkv=1, d=d, ctx=2240,
+                     dtype=dtype), 2200),
     ]
     for w, ctx in cases:
         print("static scratch", w.name, dtype, d, flush=True)
