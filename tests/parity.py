@@ -108,7 +108,7 @@ def _written_mask(w, ctx):
     return m
 
 
-def _check_cache(Kg, Ko, Kin, w, ctx, dtype, name):
+def _check_cache(Kg, Ko, Kin, w, ctx, dtype, name, f32_scale=1.0):
     """Written slots within tolerance, every other slot bit-identical to the input, and
     the NaN-sentinel write set equal to the oracle's."""
     kg = _f64(Kg)
@@ -116,7 +116,7 @@ def _check_cache(Kg, Ko, Kin, w, ctx, dtype, name):
     assert (nan_g == nan_o).all(), "%s: written slot set differs from the oracle's" % name
     mask = _written_mask(w, ctx)[None, :, None, :, None]
     mask = np.broadcast_to(mask, kg.shape)
-    check_close(kg[mask], Ko[mask], dtype, name + " (written slots)")
+    check_close(kg[mask], Ko[mask], dtype, name + " (written slots)", f32_scale=f32_scale)
     kin = _f64(Kin)
     same = ~mask & ~np.isnan(kin)
     assert (kg[same] == kin[same]).all(), "%s: a slot outside the write set changed" % name
