@@ -306,7 +306,8 @@ def test_channel_attend_work_queue(wm, d, L, Hq, Hkv, mask_mode, docs):
 # ------------------------------------------------------------ full workloads
 
 FULL = ["c2_T2048_L12_k12", "c3_T2048_L12_k6", "c4_T4096_L24_k12", "paper_T2048_L16_k8",
-        "paper_T2048_L16_k16"]
+        "paper_T2048_L16_k16", "paper_T2048_L16_k1", "paper_T2048_L16_k2", "paper_T2048_L16_k4",
+        "paper_T2048_L16_k12"]
 
 
 def _sample_rows(w, b):
