@@ -652,6 +652,52 @@ def passes_bench(wm, torch, np, synth, hip, dev, stream, log, groups=("8", "16",
                 % (g, n_grad, ms))
             del ws
             torch.cuda.empty_cache()
+    out["schedule_s44"] = schedule_bench(wm, torch, np, synth, hip, dev, stream, log)
+    return out
+
+
+def schedule_bench(wm, torch, np, synth, hip, dev, stream, log):
+    """The schedules of the paper's prefill timing (Section 4.4: a 4-layer model, D = 512,
+    k = 4, 2048-token sequences in batches of 64, time per sequence = batch time / 64) run
+    by the pass driver with the stand-in block in place of the decoder layer (heads 6 / 3
+    of 96 as the paper's model family; p = 1): cyclic g = 16 with the 4 passes the paper
+    needs and Jacobi with its 75. Context for the paper's figures (0.01245 and 0.1393 s per
+    sequence on an RTX A6000 with full decoder layers), not the same computation."""
+    w = synth.Workload("paper_s44", 64, 2048, 4, 4, 512, 6, 3, 96, 0, "bf16",
+                       [l % 4 for l in range(4)], 1, 1404)
+    P = wm.ParamSet({k: v.to(dev) for k, v in
+                     synth.make_params(w, np.asarray(wm.init_bias(w.L, w.k)) + 0.2).items()})
+    X = synth.make_embeddings(w).to(dev)
+    W_o = synth.make_out_proj(w).to(dev)
+    Kc = torch.zeros((w.k, w.B, w.Hkv, w.T_new, w.d), dtype=torch.bfloat16, device=dev)
+    Vc = torch.zeros_like(Kc)
+    H = torch.empty((w.B, w.T_new, w.L, w.D), dtype=torch.bfloat16, device=dev)
+    top = torch.empty((w.B, w.T_new, w.D), dtype=torch.bfloat16, device=dev)
+    out = {"workload": "Section 4.4 schedules: B64 T2048 L4 k4 D512 6q/3kv x96, p1, bf16, "
+                       "stand-in block h + W_o o (the paper times full decoder layers)"}
+    for g, passes, reps in ((16, 4, 5), (1, 75, 2)):
+        dims = wm.make_dims(w.B, w.T_new, w.L, w.k, w.D, w.Hq, w.Hkv, w.d, p=w.p,
+                            S_cap=w.T_new, ctx_max=0, dtype=wm.BF16, groups=g)
+        ws = wm.workspace(dims, wm.OP_PASSES, dev)
+        run = lambda: wm.prefill_passes(dims, P, W_o, X, w.chan_map, passes, Kc, Vc, H, top,  # noqa: E731
+                                        ws=ws, stream=stream)
+        run()
+        torch.cuda.synchronize()
+        ev = [hip.create() for _ in range(reps + 1)]
+        hip.record(ev[0], stream.cuda_stream)
+        for r in range(reps):
+            run()
+            hip.record(ev[r + 1], stream.cuda_stream)
+        torch.cuda.synchronize()
+        ms = float(np.median([hip.elapsed_ms(ev[r], ev[r + 1]) for r in range(reps)]))
+        for e in ev:
+            hip.destroy(e)
+        out["g%d_x%d" % (g, passes)] = {"passes": passes, "ms": round(ms, 3),
+                                        "s_per_sequence": round(ms * 1e-3 / w.B, 6),
+                                        "tokens_per_s": round(w.B * w.T_new / (ms * 1e-3), 1)}
+        log("bench: Section 4.4 schedule g=%d x %d: %.3f ms per batch of 64 (%.5f s per sequence)"
+            % (g, passes, ms, ms * 1e-3 / w.B))
+        del ws
     return out
 
 
