@@ -723,6 +723,21 @@ void launch_grad_rms(const RmsArgs& a, int nouter, hipStream_t s) {
 // its first row, read only by the thread that writes it), then the groups' sums in order.
 constexpr int kSumGroup = 32;
 
+// v + p[0] + p[stride] + ... over cnt rows, added in row order; the loads are issued eight
+// at a time before their adds, so a thread waits for memory once per eight rows
+__device__ __forceinline__ float sum_rows(float v, const float* p, long stride, int cnt) {
+  int c = 0;
+  for (; c + 8 <= cnt; c += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = p[(c + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += t[u];
+  }
+  for (; c < cnt; ++c) v += p[c * stride];
+  return v;
+}
+
 __global__ __launch_bounds__(256) void grad_sum_group_kernel(float* part, int chunks, long n) {
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   const int ngr = (chunks + kSumGroup - 1) / kSumGroup;
@@ -730,9 +745,9 @@ __global__ __launch_bounds__(256) void grad_sum_group_kernel(float* part, int ch
   const int g = blockIdx.y % ngr;
   if (idx >= n) return;
   const int c0 = g * kSumGroup, c1 = min(chunks, c0 + kSumGroup);
-  float v = 0.f;
-  for (int c = c0; c < c1; ++c) v += part[(o * chunks + c) * n + idx];
-  part[(o * chunks + c0) * n + idx] = v;
+  float* p = part + (o * chunks + c0) * n + idx;
+  const float v = sum_rows(0.f, p, n, c1 - c0);
+  *p = v;
 }
 
 __global__ __launch_bounds__(256) void grad_sum_kernel(const float* part, int chunks, int step,
@@ -741,8 +756,8 @@ __global__ __launch_bounds__(256) void grad_sum_kernel(const float* part, int ch
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   const long o = blockIdx.y;
   if (idx >= n) return;
-  float v = 0.f;
-  for (int c = 0; c < chunks; c += step) v += part[(o * chunks + c) * n + idx];
+  const float v = sum_rows(0.f, part + o * chunks * n + idx, (long)step * n,
+                           (chunks + step - 1) / step);
   out[o * n + idx] = accumulate ? out[o * n + idx] + v * scale : v * scale;
 }
 
