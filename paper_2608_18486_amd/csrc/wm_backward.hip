@@ -496,8 +496,10 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
 // -------------------------------------------------------------------- dummy
 // The dummy's gradients sum over every row that reads its channel and KV head: the rows
 // (consumer, query head, sequence, position) are split into dummy_chunks(sh) contiguous
-// chunks, one workgroup of 4 DH threads each (thread (rl, e) sums column e over every
-// fourth row of the chunk), and a second kernel adds the chunks in order.
+// chunks, one workgroup of 4 DH threads each, and a second kernel adds the chunks in order.
+// In a chunk, thread (rl, cg) of 32 x DH / 8 sums columns 8 cg .. 8 cg + 7 over every 32nd
+// row from rl (16-byte loads of the row's output gradient and query), and the 32 partial
+// rows are added in order.
 // chunks per (channel, KV head): at least 32, and enough for ~4096 workgroups in all, but
 // no more than one per 128 rows of an even spread of the consumers over the channels (a
 // fixed function of the shape, so the sums keep one order on any device)
@@ -510,27 +512,37 @@ static int dummy_chunks(const Shape& sh) {
 
 template <int DH>
 __global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_part_kernel(BwdArgs a, float* part) {
-  __shared__ float s_v[4 * DH], s_k[4 * DH];
+  constexpr int CG = DH / 8, R = 4 * DH / CG;  // column groups, rows per pass (32)
+  __shared__ float s_v[R][DH], s_k[R][DH];
   const int nch = a.dchunks;
   const int ck = blockIdx.x / nch, chunk = blockIdx.x % nch;
   const int c = ck / a.Hkv, kvh = ck % a.Hkv;
-  const int tid = threadIdx.x, e = tid % DH, rl = tid / DH;
+  const int tid = threadIdx.x, cg = tid % CG, rl = tid / CG;
   const int G = a.Hq / a.Hkv;
   const long per_b = a.T, per_h = (long)a.B * per_b, per_m = G * per_h;
   const long nrow = (long)(a.grp.offsets[c + 1] - a.grp.offsets[c]) * per_m;
   const long r0 = nrow * chunk / nch, r1 = nrow * (chunk + 1) / nch;
-  float av = 0.f, ak = 0.f;
+  float av[8], ak[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) av[u] = ak[u] = 0.f;
   if (a.mask_paper && r0 + rl < r1) {
-    // row rr = ((mi G + hg) B + b) T + i, stepped by 4 without divisions in the loop
+    // row rr = ((mi G + hg) B + b) T + i, stepped by R without divisions in the loop
     long rr = r0 + rl;
     int mi = (int)(rr / per_m), hg = (int)(rr / per_h % G), b = (int)(rr / per_b % a.B);
     int i = (int)(rr % per_b);
-    for (; rr < r1; rr += 4) {
+    for (; rr < r1; rr += R) {
       const int l = a.grp.members[a.grp.offsets[c] + mi], hq = kvh * G + hg;
       const long row = (((long)l * a.B + b) * a.Hq + hq) * a.T + i;
-      av += a.pd[row] * (float)a.dO[(((long)l * a.B + b) * a.T + i) * a.Hq * DH + (long)hq * DH + e];
-      ak += a.dsd[row] * (float)a.Q[row * DH + e];
-      i += 4;
+      const float pd = a.pd[row], ds = a.dsd[row];
+      const bf16x8 dov = *(const bf16x8*)(a.dO + (((long)l * a.B + b) * a.T + i) * a.Hq * DH +
+                                          (long)hq * DH + 8 * cg);
+      const bf16x8 qv = *(const bf16x8*)(a.Q + row * DH + 8 * cg);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        av[u] += pd * (float)dov[u];
+        ak[u] += ds * (float)qv[u];
+      }
+      i += R;
       while (i >= a.T) {
         i -= a.T;
         if (++b == a.B) {
@@ -543,13 +555,18 @@ __global__ __launch_bounds__(4 * DH) void attend_bwd_dummy_part_kernel(BwdArgs a
       }
     }
   }
-  s_v[tid] = av;
-  s_k[tid] = ak;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    s_v[rl][8 * cg + u] = av[u];
+    s_k[rl][8 * cg + u] = ak[u];
+  }
   __syncthreads();
-  if (rl == 0) {
-    float* o = part + (long)blockIdx.x * 2 * DH;
-    o[e] = (s_v[e] + s_v[DH + e]) + (s_v[2 * DH + e] + s_v[3 * DH + e]);
-    o[DH + e] = (s_k[e] + s_k[DH + e]) + (s_k[2 * DH + e] + s_k[3 * DH + e]);
+  if (tid < 2 * DH) {
+    const int e = tid % DH;
+    const float(*src)[DH] = tid < DH ? s_v : s_k;
+    float v = 0.f;
+    for (int q = 0; q < R; ++q) v += src[q][e];
+    part[(long)blockIdx.x * 2 * DH + tid] = v;  // V's sums, then K's
   }
 }
 
