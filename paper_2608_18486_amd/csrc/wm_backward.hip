@@ -85,7 +85,7 @@ __device__ __forceinline__ bf16x4 bwd_ld8(__amdgpu_buffer_rsrc_t r, uint32_t off
 template <int DH, int NW>
 __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
   constexpr int NKS = DH / 16, NDT = DH / 32, ROW = 2 * DH, BLK = 64, NH = DH == 64 ? 2 : 1;
-  // two buffers, each a K block then a V block (pass 1 uses the K blocks only)
+  // two buffers, each a K block then a V block
   __shared__ __align__(16) char smem[4 * BLK * ROW];
   const uint32_t lbase = (uint32_t)(uintptr_t)smem;
   // XCD-aware order: each XCD walks a contiguous run of tiles, so the query tiles of one
@@ -156,30 +156,45 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
   const auto vv = make_view(a.Vc + cbase, (uint32_t)max(kend, 0) * ROW);
   const PfLane<DH> lo = pf_lane<DH>(lane);
 
-  // pass 1: the row's log-sum-exp (log2 units) over the dummy and the visible slots; the
-  // two lanes of a row share the running maximum and keep partial sums
+  // One walk over the blocks with an online normaliser: the row keeps a running maximum m
+  // (log2 units, shared by the two lanes of the row) and sums l = sum 2^(s - m) and
+  // dq~ = sum 2^(s - m) (dP - D) k, both rescaled when m grows; at the end
+  // lse = m + log2 l and dq = dq~ / l, since dS = P (dP - D) with P = 2^(s - lse).
   float m = a.mask_paper ? sd : kNegBig;
   float sum = a.mask_paper && h == 0 ? 1.f : 0.f;
+  f32x16 dq[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) dq[dt] = zero16();
   // blocks are double-buffered: block j + 1 is copied while block j is multiplied
-  if (nblk > 0) bwd_dma<DH, BLK, NW>(lbase, kv, ROW, 0, kend, w, lane);
+  if (nblk > 0) {
+    bwd_dma<DH, BLK, NW>(lbase, kv, ROW, 0, kend, w, lane);
+    bwd_dma<DH, BLK, NW>(lbase + BLK * ROW, vv, ROW, 0, kend, w, lane);
+  }
   for (int j = 0; j < nblk; ++j) {
     const uint32_t kb = (uint32_t)(j & 1) * 2 * BLK * ROW;
     wait_vmcnt<0>();
     __syncthreads();  // block j is in LDS; every wave is done with block j - 1
-    if (j + 1 < nblk)
-      bwd_dma<DH, BLK, NW>(lbase + (kb ^ (2 * BLK * ROW)), kv, ROW, (j + 1) * BLK, kend, w, lane);
+    if (j + 1 < nblk) {
+      const uint32_t nb = lbase + (kb ^ (2 * BLK * ROW));
+      bwd_dma<DH, BLK, NW>(nb, kv, ROW, (j + 1) * BLK, kend, w, lane);
+      bwd_dma<DH, BLK, NW>(nb + BLK * ROW, vv, ROW, (j + 1) * BLK, kend, w, lane);
+    }
 #pragma unroll
     for (int hg = 0; hg < 2 / NH; ++hg) {
       const int sb = j * BLK + 32 * NH * hg;  // the group's first slot
       if (sb < wkend) {
-        f32x16 sc[NH];
+        f32x16 sc[NH], dp[NH];
 #pragma unroll
-        for (int x = 0; x < NH; ++x) sc[x] = zero16();
+        for (int x = 0; x < NH; ++x) sc[x] = dp[x] = zero16();
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-          for (int x = 0; x < NH; ++x)
-            sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, kb + (NH * hg + x) * 32 * ROW, ks), qf[ks]);
+          for (int x = 0; x < NH; ++x) {
+            const uint32_t ho = kb + (NH * hg + x) * 32 * ROW;
+            sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, ho, ks), qf[ks]);
+            dp[x] = mma32(dp[x], pf_ldk<DH>(smem, lo, ho + BLK * ROW, ks), df[ks]);
+          }
+        // scores in log2 units, hidden slots at kNegBig
         float mx = kNegBig;
         if (sb + 32 * NH - 1 < wlim0) {  // every row of the wave sees the group
 #pragma unroll
@@ -200,71 +215,24 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
             }
         }
         const float mn = fmaxf(m, halves_max(mx));
+        if (__builtin_expect(__any(mn > m), 0)) {  // the maximum grew: rescale the sums
+          const float f = bwd_exp2(m - mn);
+          sum *= f;
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt) dq[dt] *= f;
+          m = mn;
+        }
+        bf16x8 ds[NH][2];
         float part = 0.f;
 #pragma unroll
         for (int x = 0; x < NH; ++x)
 #pragma unroll
-          for (int q = 0; q < 16; ++q) part += bwd_exp2(sc[x][q] - mn);
-        sum = sum * bwd_exp2(m - mn) + part;
-        m = mn;
-      }
-    }
-  }
-  __syncthreads();  // pass 2 reuses the buffers
-  const float lse = m + __log2f(halves_sum(sum));
-
-  // pass 2: dS and dq^T += K^T dS^T
-  f32x16 dq[NDT];
-#pragma unroll
-  for (int dt = 0; dt < NDT; ++dt) dq[dt] = zero16();
-  if (nblk > 0) {
-    bwd_dma<DH, BLK, NW>(lbase, kv, ROW, 0, kend, w, lane);
-    bwd_dma<DH, BLK, NW>(lbase + BLK * ROW, vv, ROW, 0, kend, w, lane);
-  }
-  for (int j = 0; j < nblk; ++j) {
-    const uint32_t kb = (uint32_t)(j & 1) * 2 * BLK * ROW;
-    wait_vmcnt<0>();
-    __syncthreads();
-    if (j + 1 < nblk) {
-      const uint32_t nb = lbase + (kb ^ (2 * BLK * ROW));
-      bwd_dma<DH, BLK, NW>(nb, kv, ROW, (j + 1) * BLK, kend, w, lane);
-      bwd_dma<DH, BLK, NW>(nb + BLK * ROW, vv, ROW, (j + 1) * BLK, kend, w, lane);
-    }
-#pragma unroll
-    for (int hg = 0; hg < 2 / NH; ++hg) {
-      const int sb = j * BLK + 32 * NH * hg;
-      if (sb < wkend) {
-        f32x16 sc[NH], dp[NH];
-#pragma unroll
-        for (int x = 0; x < NH; ++x) sc[x] = dp[x] = zero16();
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-          for (int x = 0; x < NH; ++x) {
-            const uint32_t ho = kb + (NH * hg + x) * 32 * ROW;
-            sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, ho, ks), qf[ks]);
-            dp[x] = mma32(dp[x], pf_ldk<DH>(smem, lo, ho + BLK * ROW, ks), df[ks]);
+          for (int q = 0; q < 16; ++q) {
+            const float p = bwd_exp2(sc[x][q] - m);  // 0 at kNegBig
+            part += p;
+            ds[x][q >> 3][q & 7] = (bf16)(p * (dp[x][q] - delta));
           }
-        bf16x8 ds[NH][2];
-        if (sb + 32 * NH - 1 < wlim0) {  // no mask in this group
-#pragma unroll
-          for (int x = 0; x < NH; ++x)
-#pragma unroll
-            for (int q = 0; q < 16; ++q) {
-              const float p = bwd_exp2(sc[x][q] * cl2 - lse);
-              ds[x][q >> 3][q & 7] = (bf16)(p * (dp[x][q] - delta));
-            }
-        } else {
-          const int thr = lim - sb - 4 * h;
-#pragma unroll
-          for (int x = 0; x < NH; ++x)
-#pragma unroll
-            for (int q = 0; q < 16; ++q) {
-              const float p = 32 * x + 8 * (q >> 2) + (q & 3) < thr
-                                  ? bwd_exp2(sc[x][q] * cl2 - lse) : 0.f;
-              ds[x][q >> 3][q & 7] = (bf16)(p * (dp[x][q] - delta));
-            }
-        }
+        sum += part;
 #pragma unroll
         for (int x = 0; x < NH; ++x)
 #pragma unroll
@@ -276,6 +244,10 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
       }
     }
   }
+  const float ltot = halves_sum(sum);
+  const float lse = m + __log2f(ltot), inv = 1.0f / ltot;
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) dq[dt] *= inv;
 
   // the dummy's term, then dq / sqrt(d) out
   const float p_d = a.mask_paper ? bwd_exp2(sd - lse) : 0.f;
