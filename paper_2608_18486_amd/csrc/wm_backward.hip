@@ -37,6 +37,8 @@ struct BwdArgs {
   int accumulate;  // add the slot and dummy gradients into dKc, dVc, dKd, dVd
   int dchunks;     // partial sums per (channel, KV head) of the dummy's gradients
   int gs, gq;      // query i of sequence b sits at position ctx_len[b] + gq + gs i
+  int kv_heavy_first;  // slot-major grid: each XCD takes its (channel, sequence, KV head)
+                       // slices' slot tiles lowest slots (most readers) first
 };
 
 // waves per workgroup of the query-major and the slot-major kernel (32 rows each)
@@ -292,9 +294,18 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dkv_kernel(BwdArgs a) {
   const uint32_t lbase = (uint32_t)(uintptr_t)smem;
   // XCD-aware order: the slot tiles of one (channel, sequence, KV head), which read the
   // same queries and output gradients, run on one XCD
-  const int tile = xcd_tile(blockIdx.x, (int)gridDim.x);
-  const int stile = tile % a.n_stiles;
-  int y = tile / a.n_stiles;
+  int stile, y;
+  if (a.kv_heavy_first) {
+    // a grid of at most two rounds: XCD x owns a contiguous band of the slices and starts
+    // every slice's first slot tile, then every second, ..., so the long tiles start first
+    const int px = (int)gridDim.x / (a.n_stiles * kNumXcd), sidx = blockIdx.x / kNumXcd;
+    stile = sidx / px;
+    y = (blockIdx.x % kNumXcd) * px + sidx % px;
+  } else {
+    const int tile = xcd_tile(blockIdx.x, (int)gridDim.x);
+    stile = tile % a.n_stiles;
+    y = tile / a.n_stiles;
+  }
   const int kvh = y % a.Hkv;
   y /= a.Hkv;
   const int b = y % a.B, c = y / a.B;
@@ -587,7 +598,13 @@ void launch_attend_backward(const Shape& sh, const LayerTable& chan_map,
             (int)(((long)sh.ctx_max + sh.span() + 32 * kBwdKWaves - 1) / (32 * kBwdKWaves)),
             kLog2e / sqrtf((float)sh.d),
             1.0f / sqrtf((float)sh.d), chan_map, groups, accumulate ? 1 : 0,
-            dummy_chunks(sh), sh.gs, sh.gq};
+            dummy_chunks(sh), sh.gs, sh.gq, 0};
+  {
+    // small slot-major grids (two rounds at most) take their heavy tiles first; larger ones
+    // keep each slice's tiles together, so they share its queries in one L2
+    const long slices = (long)sh.Hkv * sh.B * sh.k;
+    a.kv_heavy_first = slices % kNumXcd == 0 && (long)a.n_stiles * slices <= 2L * device_cus();
+  }
   const dim3 ga(a.n_qtiles * sh.Hq * sh.B * sh.L), gb(a.n_stiles * sh.Hkv * sh.B * sh.k),
       gp(sh.k * sh.Hkv * a.dchunks), gs(sh.k * sh.Hkv);
   float* part = rows + 4 * nrow;

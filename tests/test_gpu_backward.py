@@ -15,16 +15,20 @@ pytestmark = pytest.mark.gpu
 
 @pytest.mark.parametrize("T_new,ctx", [(40, 0), (300, 0), (70, 130)])
 @pytest.mark.parametrize("mask_mode", [0, 1])
-@pytest.mark.parametrize("d,Hq,Hkv", [(64, 4, 2), (96, 6, 3), (64, 2, 2)])
-def test_channel_attend_backward(wm, T_new, ctx, mask_mode, d, Hq, Hkv):
-    w = synth.small("bwd_d%d" % d, B=2, T_new=T_new, L=5, k=3, D=64, Hq=Hq, Hkv=Hkv, d=d,
+@pytest.mark.parametrize("d,Hq,Hkv,B", [(64, 4, 2, 2), (96, 6, 3, 2), (64, 2, 2, 2),
+                                        (64, 4, 2, 4), (96, 6, 3, 4)])
+def test_channel_attend_backward(wm, T_new, ctx, mask_mode, d, Hq, Hkv, B):
+    """B = 4 with Hkv = 2 gives 24 slices (channel, sequence, KV head): with their few slot
+    tiles, the slot-major grid takes each XCD's heavy tiles first (slices a multiple of 8);
+    Hkv = 3 at B = 4 does not divide and keeps the slice-major order."""
+    w = synth.small("bwd_d%d" % d, B=B, T_new=T_new, L=5, k=3, D=64, Hq=Hq, Hkv=Hkv, d=d,
                     ctx=ctx + T_new, dtype="bf16", chan_map=[2, 0, 2, 2, 0])
     print("attention backward d%d %d/%d T%d ctx%d mask%d" % (d, Hq, Hkv, T_new, ctx, mask_mode),
           flush=True)
     P = synth.make_params(w, _bias(w))
     Q = synth.make_queries(w)
     Kc, Vc = synth.make_cache_cpu(w)
-    ctx_len = torch.tensor([ctx, ctx // 2], dtype=torch.int32)
+    ctx_len = torch.tensor([ctx, ctx // 2, ctx // 3, ctx][:B], dtype=torch.int32)
     od = _odims(w, mask_mode=mask_mode)
     O = oracle.channel_attend(od, P, Q, w.chan_map, ctx_len.numpy(), _f64(Kc), _f64(Vc))
     O_bf = torch.from_numpy(O).to(torch.bfloat16)
