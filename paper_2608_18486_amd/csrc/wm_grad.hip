@@ -153,6 +153,47 @@ __device__ __forceinline__ bf16x8 gemm_frag(const char* tile, int rb, int ks, in
   }
 }
 
+// The tile's results into C (or a split's partial rows): lane (h, r) holds column
+// n0 + 32 (WN wn + j) + r, rows m0 + 32 (WM wm + i) + 8 (q / 4) + 4 h + q % 4. When adding
+// into C, the 16 old values of a 32 x 32 block are all loaded before any is stored, so
+// those loads wait on memory together rather than one round trip per element.
+template <class C>
+__device__ __forceinline__ void gemm_store(const f32x16 (&acc)[C::WM][C::WN], float* Cz,
+                                           long crow, long ccol, int M, int N, int mlo,
+                                           int acc_in, int m0, int n0, int wm, int wn, int h,
+                                           int r) {
+#pragma unroll
+  for (int j = 0; j < C::WN; ++j) {
+    const int n = n0 + 32 * (C::WN * wn + j) + r;
+    if (n >= N) continue;
+    float* col = Cz + (long)n * ccol;
+    if (acc_in) {
+#pragma unroll
+      for (int i = 0; i < C::WM; ++i) {
+        float old[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
+          old[q] = m < M && m >= mlo ? col[(long)m * crow] : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
+          if (m < M && m >= mlo) col[(long)m * crow] = old[q] + acc[i][j][q];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
+          if (m < M && m >= mlo) col[(long)m * crow] = acc[i][j][q];
+        }
+    }
+  }
+}
+
 template <class C, bool TA, bool TB, bool VEC>
 __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
   __shared__ __align__(16) char smem[2][C::TA_BYTES + C::TB_BYTES];  // [buffer][A | B]
@@ -211,21 +252,7 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_kernel(GemmArgs a) {
   const long crow = split ? a.N : a.c_row, ccol = split ? 1 : a.c_col;
   const int mlo = split ? 0 : (int)(a.m_lo0 + a.m_lo_dz * z);
   const int acc_in = split ? 0 : a.accumulate;
-#pragma unroll
-  for (int j = 0; j < C::WN; ++j) {
-    const int n = n0 + 32 * (C::WN * wn + j) + r;
-    if (n >= a.N) continue;
-#pragma unroll
-    for (int i = 0; i < C::WM; ++i)
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
-        if (m < a.M && m >= mlo) {
-          float* p = Cz + (long)m * crow + (long)n * ccol;
-          *p = acc_in ? *p + acc[i][j][q] : acc[i][j][q];
-        }
-      }
-  }
+  gemm_store<C>(acc, Cz, crow, ccol, a.M, a.N, mlo, acc_in, m0, n0, wm, wn, h, r);
 }
 
 // ---- the same product with LDS DMA: every tile goes from memory straight into LDS
@@ -345,21 +372,7 @@ __global__ __launch_bounds__(C::NT) void grad_gemm_dma_kernel(GemmArgs a) {
   const long crow = split ? a.N : a.c_row, ccol = split ? 1 : a.c_col;
   const int mlo = split ? 0 : (int)(a.m_lo0 + a.m_lo_dz * z);
   const int acc_in = split ? 0 : a.accumulate;
-#pragma unroll
-  for (int j = 0; j < C::WN; ++j) {
-    const int n = n0 + 32 * (C::WN * wn + j) + r;
-    if (n >= a.N) continue;
-#pragma unroll
-    for (int i = 0; i < C::WM; ++i)
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int m = m0 + 32 * (C::WM * wm + i) + 8 * (q >> 2) + 4 * h + (q & 3);
-        if (m < a.M && m >= mlo) {
-          float* p = Cz + (long)m * crow + (long)n * ccol;
-          *p = acc_in ? *p + acc[i][j][q] : acc[i][j][q];
-        }
-      }
-  }
+  gemm_store<C>(acc, Cz, crow, ccol, a.M, a.N, mlo, acc_in, m0, n0, wm, wn, h, r);
 }
 
 static bool operand_t(const GemmOperand& o) { return o.s_row == 1 && o.s_k != 1; }
