@@ -196,27 +196,25 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
             sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, ho, ks), qf[ks]);
             dp[x] = mma32(dp[x], pf_ldk<DH>(smem, lo, ho + BLK * ROW, ks), df[ks]);
           }
-        // scores in log2 units, hidden slots at kNegBig
+        // the group's largest raw score (hidden slots at kNegBig); cl2 > 0 scales it to
+        // log2 units, and each weight is 2^(s cl2 - m) from one fma
         float mx = kNegBig;
         if (sb + 32 * NH - 1 < wlim0) {  // every row of the wave sees the group
 #pragma unroll
           for (int x = 0; x < NH; ++x)
 #pragma unroll
-            for (int q = 0; q < 16; ++q) {
-              sc[x][q] *= cl2;
-              mx = fmaxf(mx, sc[x][q]);
-            }
+            for (int q = 0; q < 16; ++q) mx = fmaxf(mx, sc[x][q]);
         } else {
           const int thr = lim - sb - 4 * h;  // slot sb + 32 x + 8 (q / 4) + 4 h + q % 4 < lim
 #pragma unroll
           for (int x = 0; x < NH; ++x)
 #pragma unroll
             for (int q = 0; q < 16; ++q) {
-              sc[x][q] = 32 * x + 8 * (q >> 2) + (q & 3) < thr ? sc[x][q] * cl2 : kNegBig;
+              sc[x][q] = 32 * x + 8 * (q >> 2) + (q & 3) < thr ? sc[x][q] : kNegBig;
               mx = fmaxf(mx, sc[x][q]);
             }
         }
-        const float mn = fmaxf(m, halves_max(mx));
+        const float mn = fmaxf(m, halves_max(mx) * cl2);
         if (__builtin_expect(__any(mn > m), 0)) {  // the maximum grew: rescale the sums
           const float f = bwd_exp2(m - mn);
           sum *= f;
@@ -230,7 +228,7 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
         for (int x = 0; x < NH; ++x)
 #pragma unroll
           for (int q = 0; q < 16; ++q) {
-            const float p = bwd_exp2(sc[x][q] - m);  // 0 at kNegBig
+            const float p = bwd_exp2(__builtin_fmaf(sc[x][q], cl2, -m));  // 0 at kNegBig
             part += p;
             ds[x][q >> 3][q & 7] = (bf16)(p * (dp[x][q] - delta));
           }
