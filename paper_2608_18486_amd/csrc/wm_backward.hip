@@ -196,9 +196,11 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
             sc[x] = mma32(sc[x], pf_ldk<DH>(smem, lo, ho, ks), qf[ks]);
             dp[x] = mma32(dp[x], pf_ldk<DH>(smem, lo, ho + BLK * ROW, ks), df[ks]);
           }
-        // the group's largest raw score (hidden slots at kNegBig); cl2 > 0 scales it to
-        // log2 units, and each weight is 2^(s cl2 - m) from one fma
-        float mx = kNegBig;
+        // the group's largest raw score (hidden slots at -inf, whose weight is 0 against any
+        // reference, and which leave the maximum alone); cl2 > 0 scales it to log2 units,
+        // and each weight is 2^(s cl2 - m) from one fma
+        constexpr float kHidden = -__builtin_inff();
+        float mx = kHidden;
         if (sb + 32 * NH - 1 < wlim0) {  // every row of the wave sees the group
 #pragma unroll
           for (int x = 0; x < NH; ++x)
@@ -210,7 +212,7 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
           for (int x = 0; x < NH; ++x)
 #pragma unroll
             for (int q = 0; q < 16; ++q) {
-              sc[x][q] = 32 * x + 8 * (q >> 2) + (q & 3) < thr ? sc[x][q] : kNegBig;
+              sc[x][q] = 32 * x + 8 * (q >> 2) + (q & 3) < thr ? sc[x][q] : kHidden;
               mx = fmaxf(mx, sc[x][q]);
             }
         }
@@ -228,7 +230,7 @@ __global__ __launch_bounds__(64 * NW) void attend_bwd_dq_kernel(BwdArgs a) {
         for (int x = 0; x < NH; ++x)
 #pragma unroll
           for (int q = 0; q < 16; ++q) {
-            const float p = bwd_exp2(__builtin_fmaf(sc[x][q], cl2, -m));  // 0 at kNegBig
+            const float p = bwd_exp2(__builtin_fmaf(sc[x][q], cl2, -m));  // 0 when hidden
             part += p;
             ds[x][q >> 3][q & 7] = (bf16)(p * (dp[x][q] - delta));
           }

@@ -204,3 +204,4 @@ def test_channel_attend_backward_strided_group(wm, mask_mode, d, Hq, Hkv):
         check_close(dKc_h[:, b, :, :hi], ref["dKc"][:, b, :, :hi], "bf16", "dKc b%d" % b)
         check_close(dVc_h[:, b, :, :hi], ref["dVc"][:, b, :, :hi], "bf16", "dVc b%d" % b)
         assert np.isnan(dKc_h[:, b, :, hi:]).all() and np.isnan(dVc_h[:, b, :, hi:]).all()
+
