@@ -303,6 +303,36 @@ def test_channel_attend_work_queue(wm, d, L, Hq, Hkv, mask_mode, docs):
     check_close(O, Oo, "bf16", "queue d%d mask%d docs%d" % (d, mask_mode, docs))
 
 
+def test_channel_attend_work_queue_short_walks(wm):
+    """Persistent workgroups over one-token tiles whose walks are empty (no cached slot: the
+    row reads only the dummy) or one block long, interleaved, so a workgroup's next tile
+    finds its queries copied ahead by the previous walk or, after an empty walk, copies them
+    itself; every output element against the oracle."""
+    T_new, ctx = 1, 9
+    # 4096 tiles: an XCD's share of the tile order (sequence-major) spans two sequences,
+    # one with an empty walk and one with a one-block walk, about 5 tiles a workgroup
+    w = synth.small("queue_short", B=16, T_new=T_new, L=16, k=4, D=64, Hq=16, Hkv=4, d=64,
+                    ctx=ctx + T_new, dtype="bf16", chan_map=[l % 4 for l in range(16)])
+    tiles = w.Hq * w.B * w.L
+    resident = torch.cuda.get_device_properties(0).multi_processor_count * 3
+    assert tiles > resident, (tiles, resident)
+    print("short-walk queue case tiles %d resident %d" % (tiles, resident), flush=True)
+    P = synth.make_params(w, _bias(w))
+    Q = synth.make_queries(w)
+    Kc, Vc = synth.make_cache_cpu(w)
+    ctx_len = torch.tensor([0, 5, 0, 9] * 4, dtype=torch.int32)
+    Oo = oracle.channel_attend(_odims(w, mask_mode=0), P, Q, w.chan_map, ctx_len.numpy(),
+                               _f64(Kc), _f64(Vc))
+    O = torch.full((w.L, w.B, w.T_new, w.Hq * w.d), float("nan"), dtype=w.torch_dtype,
+                   device="cuda")
+    dims = _gdims(wm, w, mask_mode=0, ctx_max=ctx)
+    wm.channel_attend(dims, _dev(P), Q.cuda(), w.chan_map, ctx_len.cuda(), Kc.cuda(), Vc.cuda(),
+                      O)
+    torch.cuda.synchronize()
+    assert not torch.isnan(O.float()).any(), "a query tile was never computed"
+    check_close(O, Oo, "bf16", "short-walk queue")
+
+
 # ------------------------------------------------------------ full workloads
 
 FULL = ["c2_T2048_L12_k12", "c3_T2048_L12_k6", "c4_T4096_L24_k12", "paper_T2048_L16_k8",
