@@ -303,20 +303,21 @@ def test_channel_attend_work_queue(wm, d, L, Hq, Hkv, mask_mode, docs):
     check_close(O, Oo, "bf16", "queue d%d mask%d docs%d" % (d, mask_mode, docs))
 
 
-def test_channel_attend_work_queue_short_walks(wm):
+@pytest.mark.parametrize("d,Hq,Hkv", [(64, 16, 4), (96, 6, 3)])
+def test_channel_attend_work_queue_short_walks(wm, d, Hq, Hkv):
     """Persistent workgroups over one-token tiles whose walks are empty (no cached slot: the
-    row reads only the dummy) or one block long, interleaved, so a workgroup's next tile
-    finds its queries copied ahead by the previous walk or, after an empty walk, copies them
-    itself; every output element against the oracle."""
+    row reads only the dummy) or one block long, interleaved within each workgroup's run of
+    tiles; every output element against the oracle."""
     T_new, ctx = 1, 9
-    # 4096 tiles: an XCD's share of the tile order (sequence-major) spans two sequences,
-    # one with an empty walk and one with a one-block walk, about 5 tiles a workgroup
-    w = synth.small("queue_short", B=16, T_new=T_new, L=16, k=4, D=64, Hq=16, Hkv=4, d=64,
-                    ctx=ctx + T_new, dtype="bf16", chan_map=[l % 4 for l in range(16)])
+    # 4096 (d = 64) or 1536 (d = 96) tiles: an XCD's share of the tile order
+    # (sequence-major) spans two sequences, one with an empty walk and one with a one-block
+    # walk, several tiles a workgroup
+    w = synth.small("queue_short_d%d" % d, B=16, T_new=T_new, L=16, k=4, D=64, Hq=Hq, Hkv=Hkv,
+                    d=d, ctx=ctx + T_new, dtype="bf16", chan_map=[l % 4 for l in range(16)])
     tiles = w.Hq * w.B * w.L
-    resident = torch.cuda.get_device_properties(0).multi_processor_count * 3
+    resident = torch.cuda.get_device_properties(0).multi_processor_count * (3 if d == 64 else 2)
     assert tiles > resident, (tiles, resident)
-    print("short-walk queue case tiles %d resident %d" % (tiles, resident), flush=True)
+    print("short-walk queue case d%d tiles %d resident %d" % (d, tiles, resident), flush=True)
     P = synth.make_params(w, _bias(w))
     Q = synth.make_queries(w)
     Kc, Vc = synth.make_cache_cpu(w)
@@ -330,7 +331,7 @@ def test_channel_attend_work_queue_short_walks(wm):
                       O)
     torch.cuda.synchronize()
     assert not torch.isnan(O.float()).any(), "a query tile was never computed"
-    check_close(O, Oo, "bf16", "short-walk queue")
+    check_close(O, Oo, "bf16", "short-walk queue d%d" % d)
 
 
 # ------------------------------------------------------------ full workloads
